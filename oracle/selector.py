@@ -1,0 +1,151 @@
+"""Speculative-length selection (oracle).  Test infrastructure only.
+
+Paper: LibraSpec, Sec. 3.2-3.4, Appendix A.
+All arithmetic is IEEE binary64 with one rounding per operation, in the order
+written (Python floats never fuse a multiply into an add), so the GPU selector --
+compiled with FMA contraction disabled -- must agree bit for bit.
+
+Notation (paper): q_k drafter confidence of draft k (k = 1..G), standing in for
+the target acceptance probability p_k (Assumption 3.7); d = speculative length;
+T(d) = verification cost of length d (``cost[d]``, cost[0] unused).
+
+* P_j = prod_{k<=j} q_k is the probability that drafts 1..j are all accepted
+  (prefix acceptance, proof of Thm. 3.3 with i = 1);
+* N(d) = E[tau_d] = sum_{j<=d} P_j (linearity of expectation, same proof);
+* f(d) = N(d) / T(d) is the simplified speedup objective of Eq. 2 up to the
+  constant per-token target latency.
+
+Readings where the paper is silent (each listed in the design notes):
+* the bonus token is excluded from E[tau_d] as in the paper's formula; flag
+  ``BONUS`` adds the +1 of the always-emitted correction/bonus token;
+* EXHAUSTIVE returns the smallest maximiser of f over 1..d_max;
+* MARGINAL moves one position at a time: extend while f(d+1) > f(d) strictly
+  (Def. 3.1 requires a strict gain), else contract while f(d-1) >= f(d);
+* ALG1 follows Algorithm 1: eps_i = floor(alpha * S_i + i) with S_i summed up to
+  the *current* d, eps* = min_i eps_i; stop with d = eps* at the first eps* <= d
+  (the single rollback); otherwise eps* is clamped to d_max, the budget B pays for
+  the extension and ceil(-B/n) new blocks are requested when B < 0.
+"""
+import math
+
+SEL_MARGINAL, SEL_EXHAUSTIVE, SEL_ALG1 = 0, 1, 2
+FLAG_BONUS = 1
+
+
+def prefix_products(q):
+    """[P_1, ..., P_G] with P_j = P_{j-1} * q_j, P_0 = 1 (left-to-right products)."""
+    out, p = [], 1.0
+    for x in q:
+        p = p * float(x)
+        out.append(p)
+    return out
+
+
+def expected_accepted(q, bonus=False):
+    """[N(1), ..., N(G)], N(d) = [bonus] + sum_{j<=d} P_j, accumulated left to right."""
+    out, n = [], (1.0 if bonus else 0.0)
+    for pj in prefix_products(q):
+        n = n + pj
+        out.append(n)
+    return out
+
+
+def objective(q, cost, bonus=False):
+    """[f(1), ..., f(G)], f(d) = N(d) / cost[d]."""
+    N = expected_accepted(q, bonus)
+    return [N[d - 1] / float(cost[d]) for d in range(1, len(q) + 1)]
+
+
+def select_exhaustive(q, cost, d_max, bonus=False):
+    """Smallest d in [1, d_max] maximising f(d) (the exhaustive-search optimum)."""
+    f = objective(q, cost, bonus)
+    best = 1
+    for d in range(2, d_max + 1):
+        if f[d - 1] > f[best - 1]:
+            best = d
+    return best
+
+
+def select_marginal(q, cost, d_init, d_max, bonus=False):
+    """Iterated single beneficial adjustments of size one (Def. 3.1, Thm. 3.5/3.6).
+
+    Returns (d, steps)."""
+    f = objective(q, cost, bonus)
+    d = min(max(d_init, 1), d_max)
+    steps = 0
+    while True:
+        if d < d_max and f[d] > f[d - 1]:        # f(d+1) > f(d): extension is beneficial
+            d += 1
+        elif d > 1 and f[d - 2] >= f[d - 1]:     # f(d-1) >= f(d): truncation does not lose
+            d -= 1
+        else:
+            break
+        steps += 1
+    return d, steps
+
+
+def suffix_gain(q, i, d):
+    """S_i = sum_{j=i}^{d} prod_{k=i}^{j} q_k (expected extra accepted drafts from
+    position i on, given drafts before i were accepted; proof of Thm. 3.3)."""
+    s, p = 0.0, 1.0
+    for j in range(i, d + 1):
+        p = p * float(q[j - 1])
+        s = s + p
+    return s
+
+
+def eps_star(q, d, alpha):
+    """min_{i=1..d} floor(alpha * S_i + i)  (Algorithm 1, position-wise bounds)."""
+    best = None
+    for i in range(1, d + 1):
+        e = math.floor(alpha * suffix_gain(q, i, d) + i)
+        best = e if best is None or e < best else best
+    return best
+
+
+def select_alg1(q, d_max, alpha, n, trace=None):
+    """Algorithm 1 (LibraSpec).  q holds the confidences of all G drafted tokens;
+    d_max <= G.  Returns (d, blocks) where blocks counts drafter blocks of size n
+    (the initial one included).  ``trace`` (a list) receives (d, eps*, B) per
+    iteration."""
+    d = min(n, d_max)
+    B = 0
+    blocks = 1
+    while d < d_max:
+        e = eps_star(q, d, alpha)
+        if trace is not None:
+            trace.append((d, e, B))
+        if e <= d:
+            d = e
+            break
+        e = min(e, d_max)
+        B = B - (e - d)
+        d = e
+        if B < 0:
+            k = -(B // n)          # ceil(-B / n) for B < 0
+            blocks += k
+            B = B + k * n
+    return d, blocks
+
+
+def select(mode, q, cost, d_init, d_max, alpha, n, flags=0):
+    """Dispatch one sequence; returns (gamma, aux) with aux = steps (MARGINAL),
+    0 (EXHAUSTIVE) or blocks (ALG1)."""
+    bonus = bool(flags & FLAG_BONUS)
+    if mode == SEL_MARGINAL:
+        return select_marginal(q, cost, d_init, d_max, bonus)
+    if mode == SEL_EXHAUSTIVE:
+        return select_exhaustive(q, cost, d_max, bonus), 0
+    if mode == SEL_ALG1:
+        return select_alg1(q, d_max, alpha, n)
+    raise ValueError(mode)
+
+
+def select_batch(mode, conf, cost, d_init, d_max, alpha, n, flags=0):
+    """conf: [B][G] float32 confidences; returns (gamma[B], aux[B])."""
+    g, a = [], []
+    for row in conf:
+        x, y = select(mode, [float(v) for v in row], cost, d_init, d_max, alpha, n, flags)
+        g.append(x)
+        a.append(y)
+    return g, a
