@@ -1,0 +1,233 @@
+/*
+ * lsv.h -- C-ABI of the LibraSpec verification hot path on AMD MI355X (gfx950).
+ *
+ * LibraSpec (arXiv 2608.08721) decodes with a diffusion drafter and a target
+ * model.  Each round (Sec. 3.1, Algorithm 1):
+ *   1. lsv_select_length  -- choose how many drafted tokens to verify from the
+ *      drafter's confidences (Sec. 3.2-3.4);
+ *   2. lsv_verify_block   -- one target forward pass over the drafted block,
+ *      giving the target distribution at every drafted position (Sec. 3.1);
+ *   3. lsv_accept         -- compare draft and target, keep the accepted prefix
+ *      and emit one corrected or bonus token (Sec. 3.1).
+ *
+ * Conventions for every entry point
+ *   - All buffers are caller-owned.  "d_" arguments are device pointers, all
+ *     other pointers are host pointers.  The library never allocates device
+ *     memory; scratch space comes from a caller-provided workspace.
+ *   - Calls are asynchronous on `stream` (a hipStream_t; NULL = default stream),
+ *     perform no host<->device copies and no synchronisation, and may be
+ *     captured in a HIP graph.  Per-round shapes live in device arrays
+ *     (row offsets, cached lengths); host integers are upper bounds.
+ *   - Host-side argument checks run before any HIP call; a failed check returns
+ *     LSV_ERR_INVALID_ARG (or LSV_ERR_UNSUPPORTED) and launches nothing.
+ *     lsv_last_error() then describes the failure (thread-local).
+ *   - Problems only the device can see (a token id out of range, a cache slab
+ *     overflow, non-finite logits or confidences) are reported per sequence in
+ *     a d_status array; that sequence's outputs are then unspecified but no
+ *     memory outside the documented buffers is touched.
+ *   - A workspace must not be shared by calls that may run concurrently.
+ */
+#ifndef LSV_H
+#define LSV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ------------------------------------------------------------------ status */
+enum {
+  LSV_OK = 0,
+  LSV_ERR_INVALID_ARG = -1,
+  LSV_ERR_UNSUPPORTED = -2,
+  LSV_ERR_HIP = -3,
+  LSV_ERR_CAPACITY = -4,
+  LSV_ERR_NONFINITE = -5
+};
+
+/* Static description of a status code. */
+const char* lsv_status_string(int status);
+/* Detail of the last failing call on this host thread ("" if none). */
+const char* lsv_last_error(void);
+/* ABI version: bumped whenever a signature or a documented layout changes. */
+int lsv_abi_version(void);
+
+/* ------------------------------------------------------------------ model */
+enum { LSV_DTYPE_F32 = 0, LSV_DTYPE_BF16 = 1 };
+
+/* Pre-norm decoder of the Llama family: RMSNorm, rotary position embedding
+ * (rotate-half pairs (i, i + head_dim/2), angle = pos * rope_base^(-2i/head_dim)),
+ * SwiGLU feed-forward, grouped-query attention where query head h reads kv head
+ * h / (n_q_heads / n_kv_heads).  No biases; untied LM head.
+ * dtype is the storage and matrix-operand type of weights, KV cache and
+ * activations between kernels; residual stream, softmax and logits are fp32.
+ * Supported: head_dim in {64, 128}; n_q_heads % n_kv_heads == 0;
+ * d_model % 64 == 0; rope applies to q and k. */
+typedef struct lsv_model_config {
+  int32_t n_layers;
+  int32_t d_model;
+  int32_t n_q_heads;
+  int32_t n_kv_heads;
+  int32_t head_dim;
+  int32_t d_ff;
+  int32_t vocab;
+  int32_t dtype;     /* LSV_DTYPE_F32 | LSV_DTYPE_BF16 */
+  float rms_eps;     /* RMSNorm epsilon, e.g. 1e-5 */
+  float reserved0;   /* must be 0 */
+  double rope_base;  /* e.g. 10000.0 */
+} lsv_model_config;
+
+/* --------------------------------------------------------- packed weights */
+/* The forward pass reads weights from one device buffer in a library-defined
+ * layout ("packed"): each projection is cut into 16-row x (32 bf16 | 16 fp32)
+ * fragments stored contiguously in the order the matrix cores consume them,
+ * zero-padded to whole fragments.  Packing is a one-time re-layout (not part of
+ * a verify step) from the usual row-major [out_features, in_features] matrices
+ * (torch.nn.Linear.weight layout) in the model dtype.
+ *
+ * lsv_packed_model_bytes: size of the packed buffer for `cfg` (0 if cfg is
+ * invalid).  lsv_pack_globals / lsv_pack_layer: write the embedding table
+ * [vocab, d_model], the final norm gain [d_model] and the LM head
+ * [vocab, d_model], respectively one layer's projections and norm gains, into
+ * d_packed.  Source pointers are device pointers in the model dtype; they may be
+ * freed once the stream has passed the call.  Layers may be packed in any order. */
+size_t lsv_packed_model_bytes(const lsv_model_config* cfg);
+int lsv_pack_globals(const lsv_model_config* cfg, const void* d_embed, const void* d_final_norm,
+                     const void* d_lm_head, void* d_packed, void* stream);
+int lsv_pack_layer(const lsv_model_config* cfg, int32_t layer,
+                   const void* d_wq,   /* [n_q_heads*head_dim, d_model]  */
+                   const void* d_wk,   /* [n_kv_heads*head_dim, d_model] */
+                   const void* d_wv,   /* [n_kv_heads*head_dim, d_model] */
+                   const void* d_wo,   /* [d_model, n_q_heads*head_dim]  */
+                   const void* d_wg,   /* [d_ff, d_model] */
+                   const void* d_wu,   /* [d_ff, d_model] */
+                   const void* d_wd,   /* [d_model, d_ff] */
+                   const void* d_attn_norm, const void* d_ffn_norm, /* [d_model] */
+                   void* d_packed, void* stream);
+
+/* ---------------------------------------------------------------- KV cache */
+/* One device buffer.  For layer l the K block precedes the V block; each is
+ * [batch][n_kv_heads][capacity][head_dim] in the model dtype, i.e. element
+ * (l, kv, b, h, pos, i) is at index
+ *   ((((l * 2 + kv) * batch + b) * n_kv_heads + h) * capacity + pos) * head_dim + i
+ * with kv = 0 for K and 1 for V.  K is stored after the rotary embedding.
+ * Sequence b owns a slab of `capacity` positions; d_seq_len[b] of them are valid. */
+size_t lsv_kv_cache_bytes(const lsv_model_config* cfg, int32_t batch, int32_t capacity);
+
+/* ------------------------------------------------------------ verify step */
+/* Workspace for lsv_verify_block with the given bounds.  The workspace must be
+ * zero-filled once after allocation (e.g. with lsv_workspace_clear); every call
+ * leaves its internal counters at zero again. */
+size_t lsv_verify_workspace_bytes(const lsv_model_config* cfg, int32_t batch, int32_t max_rows,
+                                  int32_t max_ctx);
+int lsv_workspace_clear(void* d_workspace, size_t workspace_bytes, void* stream);
+
+/* One forward pass of the target over a block of rows per sequence
+ * (Sec. 3.1: all drafted positions are scored in parallel in one pass).
+ *
+ * Rows: sequence b owns rows d_row_offsets[b] .. d_row_offsets[b+1]-1 of
+ * d_tokens; in a verify step they are [root, x_1, ..., x_g] where root is the
+ * pending token emitted by the previous round and x_v are drafts.  Row r of
+ * sequence b sits at position d_seq_len[b] + (r - d_row_offsets[b]); its K/V
+ * are written to those cache positions, and it attends to cache positions
+ * 0 .. its own position (causal).  d_seq_len is NOT modified (lsv_accept
+ * commits).  The same call with d_seq_len[b] = 0 and the prompt as the block
+ * is a prefill; long prompts may be fed in chunks.
+ *
+ *   cfg, d_packed      model and its packed weights
+ *   d_kv, capacity     KV cache (layout above) with `capacity` positions per slab
+ *   batch              number of sequences (1..LSV_MAX_BATCH)
+ *   d_seq_len          [batch] int32, cached positions before this block
+ *   d_tokens           [rows] int32 token ids
+ *   d_row_offsets      [batch+1] int32, non-decreasing, d_row_offsets[0] = 0; a sequence
+ *                      may have no rows (it is left untouched; status LSV_OK)
+ *   max_rows           host bound: d_row_offsets[batch] <= max_rows <= LSV_MAX_ROWS
+ *   max_ctx            host bound: d_seq_len[b] + rows_b <= max_ctx <= capacity
+ *   d_logits           [max_rows, vocab] fp32 out; rows >= d_row_offsets[batch] untouched
+ *   d_status           [batch] int32 out (nullable): LSV_OK, LSV_ERR_INVALID_ARG (token id
+ *                      out of range), LSV_ERR_CAPACITY (block exceeds max_ctx)
+ *   d_workspace        lsv_verify_workspace_bytes(cfg, batch, max_rows, max_ctx) bytes */
+enum { LSV_MAX_BATCH = 64, LSV_MAX_ROWS = 64 };
+int lsv_verify_block(const lsv_model_config* cfg, const void* d_packed, void* d_kv, int32_t capacity,
+                     int32_t batch, const int32_t* d_seq_len, const int32_t* d_tokens,
+                     const int32_t* d_row_offsets, int32_t max_rows, int32_t max_ctx, float* d_logits,
+                     int32_t* d_status, void* d_workspace, size_t workspace_bytes, void* stream);
+
+/* -------------------------------------------------------------- acceptance */
+/* Compare drafts with the target's scores (Sec. 3.1).  Per sequence b with
+ * g_b = rows_b - 1 drafts, row v of the block scores draft x_{v+1}.
+ *
+ * LSV_ACC_GREEDY (temperature 0): argmax = smallest index of the row maximum;
+ *   a_b = longest prefix with argmax(row v-1) == x_v; emitted tokens are
+ *   x_1..x_{a_b} followed by argmax(row a_b).
+ * LSV_ACC_SAMPLE (temperature T > 0), speculative rejection sampling:
+ *   p_v = softmax(logits_v / T); draft v is accepted iff u_v * q_v(x_v) < p_{v-1}(x_v);
+ *   at the first rejection the emitted token is drawn from max(0, p_a - q_{a+1})
+ *   renormalised (from p_a if that is identically zero); if every draft passes
+ *   the bonus token is drawn from p_g.  Draws use the exponential race
+ *   argmin_x (-ln U_x) / w_x.  Uniforms come from Philox4x64-10 (Salmon et al.,
+ *   SC'11) with U = ((w >> 12) + 0.5) * 2^-52 and
+ *     ratio test of draft v:  key (seed, 1), counter (0, v | b << 32, round, 0), word 0
+ *     draw from row r:        key (seed, 2), counter (x >> 2, r | b << 32, round, 0), word x & 3.
+ *   Draft distributions: d_draft_probs row (d_row_offsets[b] - b + v - 1) is q_v of
+ *   sequence b, [*, vocab] fp32.
+ *
+ *   d_logits           [rows, vocab] fp32 (as written by lsv_verify_block)
+ *   max_rows           host bound on d_row_offsets[batch]
+ *   max_rows_per_seq   host bound on rows_b; width of d_out_tokens
+ *   d_accept_len       [batch] out: a_b
+ *   d_out_tokens       [batch, max_rows_per_seq] out: emitted tokens, then -1
+ *   d_seq_len          [batch] in/out, nullable: if given, d_seq_len[b] += a_b + 1
+ *                      (root and accepted drafts stay cached) for sequences with status OK
+ *   d_status           [batch] out (nullable): LSV_OK; LSV_ERR_NONFINITE (a non-finite
+ *                      logit in the sequence's rows, or a non-finite draft probability read);
+ *                      LSV_ERR_INVALID_ARG if the sequence has no rows or more than
+ *                      max_rows_per_seq (sampling: then every sequence of the batch), or
+ *                      the rows run past max_rows
+ *   d_workspace        lsv_accept_workspace_bytes(batch, max_rows, vocab) bytes */
+enum { LSV_ACC_GREEDY = 0, LSV_ACC_SAMPLE = 1 };
+size_t lsv_accept_workspace_bytes(int32_t batch, int32_t max_rows, int32_t vocab);
+int lsv_accept(int32_t mode, int32_t batch, int32_t vocab, const float* d_logits,
+               const int32_t* d_row_offsets, int32_t max_rows, int32_t max_rows_per_seq,
+               const int32_t* d_tokens, const float* d_draft_probs, float temperature, uint64_t seed,
+               uint64_t round, int32_t* d_accept_len, int32_t* d_out_tokens, int32_t* d_seq_len,
+               int32_t* d_status, void* d_workspace, size_t workspace_bytes, void* stream);
+
+/* -------------------------------------------------------- length selection */
+/* Choose the speculative length gamma_b per sequence from drafter confidences
+ * q_1..q_G (Assumption 3.7 uses them in place of the target's acceptance
+ * probabilities).  All arithmetic is binary64, one rounding per operation, in
+ * the order below (no fused multiply-add):
+ *   P_j = P_{j-1} * q_j (P_0 = 1);  N(d) = [BONUS] + sum_{j<=d} P_j;  f(d) = N(d) / cost[d]
+ *   (Eq. 2, the simplified speedup objective, up to a constant).
+ * LSV_SEL_EXHAUSTIVE: smallest d in [1, d_max] maximising f.
+ * LSV_SEL_MARGINAL:   from d = clamp(d_init, 1, d_max), repeat single beneficial
+ *   adjustments (Def. 3.1): d += 1 while f(d+1) > f(d), else d -= 1 while
+ *   f(d-1) >= f(d).  By Thm. 3.5/3.6 this reaches the EXHAUSTIVE answer when the
+ *   cost table is convex.  aux = number of steps.
+ * LSV_SEL_ALG1: Algorithm 1 with block size n = block_n and trade-off alpha:
+ *   d = min(n, d_max), B = 0; while d < d_max: eps* = min_{i<=d} floor(alpha * S_i + i),
+ *   S_i = sum_{j=i}^{d} prod_{k=i}^{j} q_k; if eps* <= d { d = eps*; stop }
+ *   eps* = min(eps*, d_max); B -= eps* - d; d = eps*; if B < 0 request
+ *   ceil(-B/n) more blocks and add them to B.  cost is not read.  aux = blocks used.
+ *
+ *   d_conf   [batch, G] fp32 confidences in [0, 1]
+ *   d_cost   [G+1] fp64 verification cost of each length, cost[0] unused; cost[d] > 0
+ *            for d <= d_max (MARGINAL / EXHAUSTIVE; may be NULL for ALG1)
+ *   flags    LSV_SEL_BONUS: count the always-emitted token in N(d)
+ *   d_gamma  [batch] out; d_aux [batch] out (nullable)
+ *   d_status [batch] out (nullable): LSV_OK, or LSV_ERR_INVALID_ARG when a confidence is
+ *            outside [0, 1] or a needed cost is not finite and positive (then gamma = 0). */
+enum { LSV_SEL_MARGINAL = 0, LSV_SEL_EXHAUSTIVE = 1, LSV_SEL_ALG1 = 2 };
+enum { LSV_SEL_BONUS = 1 };
+enum { LSV_MAX_G = 64 };
+int lsv_select_length(int32_t mode, int32_t batch, int32_t G, const float* d_conf, const double* d_cost,
+                      int32_t d_init, int32_t d_max, double alpha, int32_t block_n, uint32_t flags,
+                      int32_t* d_gamma, int32_t* d_aux, int32_t* d_status, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* LSV_H */

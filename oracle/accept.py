@@ -25,13 +25,15 @@ Sampling (temperature T > 0):
   Categorical draws use the exponential race: y = argmin_x E_x / w_x over w_x > 0,
   E_x = -ln U_x, ties to the smallest x; P(y = x) = w_x / sum(w).
 Status: a sequence whose logits rows (or the draft probabilities that the rule reads)
-hold a non-finite value gets LSV_ERR_NONFINITE, a_b = 0, no emitted token, no commit.
+hold a non-finite value gets LSV_ERR_NONFINITE, a_b = 0, no emitted token, no commit;
+a sequence with no rows gets LSV_ERR_INVALID_ARG (in sampling mode every sequence of the
+batch does, since the draft-row indexing needs every sequence to own a row).
 """
 import numpy as np
 
 from . import philox
 
-LSV_OK, LSV_ERR_NONFINITE = 0, -5
+LSV_OK, LSV_ERR_INVALID_ARG, LSV_ERR_NONFINITE = 0, -1, -5
 
 
 def argmax_first(row):
@@ -53,6 +55,9 @@ def accept_greedy(logits, row_offsets, tokens, out_width=None):
         r0, r1 = off[b], off[b + 1]
         g = r1 - r0 - 1
         rows = logits[r0:r1]
+        if g < 0:
+            status[b] = LSV_ERR_INVALID_ARG
+            continue
         if not np.all(np.isfinite(rows)):
             status[b] = LSV_ERR_NONFINITE
             continue
@@ -91,6 +96,10 @@ def accept_sample(logits, row_offsets, tokens, draft_probs, temperature, seed, r
     width = out_width or max(off[b + 1] - off[b] for b in range(B))
     acc, out, status = _empty(B, width)
     diag = []
+    if any(off[b + 1] - off[b] < 1 for b in range(B)):
+        # draft rows are indexed row_offsets[b] - b + v - 1: undefined unless every sequence has a row
+        status[:] = LSV_ERR_INVALID_ARG
+        return {"accept_len": acc, "out_tokens": out, "status": status, "diag": [{} for _ in range(B)]}
     for b in range(B):
         r0, r1 = off[b], off[b + 1]
         g = r1 - r0 - 1
@@ -98,6 +107,9 @@ def accept_sample(logits, row_offsets, tokens, draft_probs, temperature, seed, r
         rows = logits[r0:r1]
         d = {"tests": [], "row": None, "residual": None, "keys": None, "weights": None}
         diag.append(d)
+        if g < 0:
+            status[b] = LSV_ERR_INVALID_ARG
+            continue
         if not np.all(np.isfinite(rows)):
             status[b] = LSV_ERR_NONFINITE
             continue

@@ -1,0 +1,291 @@
+// Verify forward pass: packed-model layout, workspace layout, embedding kernel
+// and the per-layer launch sequence (LibraSpec Sec. 3.1: one target pass over all
+// drafted positions).
+//
+// Per layer, five launches (+1 attention merge for bf16):
+//   QKV GEMM   : RMSNorm prologue, RoPE + K/V cache append epilogue
+//   attention  : split-context chunks (+ merge)
+//   O GEMM     : residual add + per-row sum-of-squares partials for the next norm
+//   gate/up    : RMSNorm prologue, SwiGLU epilogue
+//   down GEMM  : residual add + sum-of-squares partials
+// then the LM head (final RMSNorm prologue) writes fp32 logits.
+#include "lsv_attn.h"
+#include "lsv_device.h"
+#include "lsv_gemm.h"
+
+namespace lsv {
+
+static size_t al256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+Shape shape_of(const lsv_model_config* c) {
+  Shape s;
+  s.L = c->n_layers;
+  s.d = c->d_model;
+  s.nq = c->n_q_heads;
+  s.nkv = c->n_kv_heads;
+  s.hd = c->head_dim;
+  s.F = c->d_ff;
+  s.V = c->vocab;
+  s.dtype = c->dtype;
+  s.es = c->dtype == LSV_DTYPE_BF16 ? 2 : 4;
+  s.eps = c->rms_eps;
+  s.rope_base = c->rope_base;
+  return s;
+}
+
+static PackedMat packed(size_t& off, int N, int K, int KT, int Nt_override = -1) {
+  PackedMat p;
+  p.offset = off;
+  p.N = N;
+  p.K = K;
+  p.Nt = Nt_override >= 0 ? Nt_override : (N + 15) / 16;
+  p.Kt = (K + KT - 1) / KT;
+  off = al256(off + (size_t)p.Nt * p.Kt * 1024);
+  return p;
+}
+
+ModelLayout model_layout(const Shape& s) {
+  const int KT = s.dtype == LSV_DTYPE_BF16 ? 32 : 16;
+  ModelLayout m;
+  size_t off = 0;
+  m.embed = off;
+  off = al256(off + (size_t)s.V * s.d * s.es);
+  m.final_norm = off;
+  off = al256(off + (size_t)s.d * s.es);
+  m.lm_head = packed(off, s.V, s.d, KT);
+  m.layer_base = off;
+  size_t lo = 0;
+  m.attn_norm = lo;
+  lo = al256(lo + (size_t)s.d * s.es);
+  m.ffn_norm = lo;
+  lo = al256(lo + (size_t)s.d * s.es);
+  m.qkv = packed(lo, (s.nq + 2 * s.nkv) * s.hd, s.d, KT);
+  m.o = packed(lo, s.d, s.nq * s.hd, KT);
+  m.gateup = packed(lo, 2 * s.F, s.d, KT, 2 * ((s.F + 15) / 16));
+  m.down = packed(lo, s.d, s.F, KT);
+  m.layer_stride = lo;
+  m.total = m.layer_base + (size_t)s.L * lo;
+  return m;
+}
+
+// ------------------------------------------------------------------ workspace
+struct VerifyWs {
+  float* h;        // [M_max][d]
+  float* stats;    // [d/64][M_max]
+  void* q;         // [M_max][nq][hd]
+  void* attn;      // [M_max][nq][hd]
+  void* u;         // [M_max][F]
+  float* part;     // split-K partials
+  float* o_part;   // attention chunk partials
+  float* ml_part;
+  int* counters;
+  size_t total;
+};
+
+static constexpr int kWantWgs = 512, kMaxSplits = 32;
+
+struct VerifyPlan {
+  int MT, n_chunks;
+  GemmPlan g[5];
+  size_t part_floats;
+  int max_groups;
+};
+
+static VerifyPlan plan_verify(const Shape& s, const ModelLayout& ml, int max_rows, int max_ctx) {
+  VerifyPlan v;
+  v.MT = (max_rows + 15) / 16;
+  v.n_chunks = (max_ctx + kAttnChunk - 1) / kAttnChunk;
+  const int KT = s.dtype == LSV_DTYPE_BF16 ? 32 : 16;
+  const PackedMat* mats[5] = {&ml.qkv, &ml.o, &ml.gateup, &ml.down, &ml.lm_head};
+  v.part_floats = 0;
+  v.max_groups = 1;
+  for (int k = 0; k < 5; ++k) {
+    const GemmKind kind = (GemmKind)k;
+    v.g[k] = plan_gemm(mats[k]->Nt, mats[k]->Kt, KT, s.es, v.MT, gemm_tpw(kind), kWantWgs, kMaxSplits);
+    if (v.g[k].S > 1) {
+      size_t pf = (size_t)v.g[k].S * max_rows * mats[k]->Nt * 16;
+      v.part_floats = pf > v.part_floats ? pf : v.part_floats;
+    }
+    v.max_groups = v.g[k].groups > v.max_groups ? v.g[k].groups : v.max_groups;
+  }
+  return v;
+}
+
+static VerifyWs carve_verify(const Shape& s, const VerifyPlan& v, int max_rows, void* base) {
+  VerifyWs w;
+  char* p = (char*)base;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    char* r = p ? p + off : nullptr;
+    off = al256(off + bytes);
+    return (void*)r;
+  };
+  w.h = (float*)take(sizeof(float) * (size_t)max_rows * s.d);
+  w.stats = (float*)take(sizeof(float) * (size_t)(s.d / 64) * max_rows);
+  w.q = take((size_t)s.es * max_rows * s.nq * s.hd);
+  w.attn = take((size_t)s.es * max_rows * s.nq * s.hd);
+  w.u = take((size_t)s.es * max_rows * s.F);
+  w.part = (float*)take(sizeof(float) * v.part_floats);
+  if (s.dtype == LSV_DTYPE_BF16) {
+    w.o_part = (float*)take(sizeof(float) * (size_t)v.n_chunks * max_rows * s.nq * s.hd);
+    w.ml_part = (float*)take(sizeof(float) * (size_t)v.n_chunks * max_rows * s.nq * 2);
+  } else {
+    w.o_part = w.ml_part = nullptr;
+  }
+  w.counters = (int*)take(sizeof(int) * (size_t)v.max_groups);
+  w.total = off;
+  return w;
+}
+
+size_t verify_workspace_bytes(const Shape& s, int batch, int max_rows, int max_ctx) {
+  (void)batch;
+  ModelLayout ml = model_layout(s);
+  VerifyPlan v = plan_verify(s, ml, max_rows, max_ctx);
+  return carve_verify(s, v, max_rows, nullptr).total;
+}
+
+// ------------------------------------------------------------------ embedding
+// h[m] = E[token_m] (fp32) and per-64-column sums of squares for the first RMSNorm.
+// Workgroup 0 also validates every sequence: token ids in range and the block
+// within max_ctx.  Invalid tokens embed as zeros.
+template <typename T>
+__global__ void __launch_bounds__(256) embed_kernel(const T* __restrict__ E, int V, int d, const int32_t* tokens,
+                                                    const int32_t* row_offsets, const int32_t* seq_len, int batch,
+                                                    int ctx_limit, int M_max, float* h, float* stats,
+                                                    int32_t* status) {
+  const int m = blockIdx.x;
+  if (m == 0 && status) {
+    for (int b = threadIdx.x; b < batch; b += blockDim.x) {
+      const int r0 = row_offsets[b], r1 = row_offsets[b + 1];
+      int st = LSV_OK;
+      if (r1 < r0 || seq_len[b] < 0 || seq_len[b] + (r1 - r0) > ctx_limit) st = LSV_ERR_CAPACITY;
+      if (r0 < 0 || r1 > M_max) {
+        status[b] = LSV_ERR_INVALID_ARG;
+        continue;
+      }
+      for (int r = r0; r < r1; ++r)
+        if (tokens[r] < 0 || tokens[r] >= V) st = LSV_ERR_INVALID_ARG;
+      status[b] = st;
+    }
+  }
+  if (m >= row_offsets[batch] || m >= M_max) return;
+  const int tok = tokens[m];
+  const bool ok = tok >= 0 && tok < V;
+  for (int p = threadIdx.x; p < d / 64; p += blockDim.x) {
+    float ss = 0.f;
+    for (int j = 0; j < 64; ++j) {
+      const int k = 64 * p + j;
+      const float x = ok ? to_f32<T>(E[(size_t)tok * d + k]) : 0.f;
+      h[(size_t)m * d + k] = x;
+      ss += x * x;
+    }
+    stats[(size_t)p * M_max + m] = ss;
+  }
+}
+
+int launch_verify(const Shape& s, const ModelLayout& ml, const void* packed, void* kv, int capacity, int batch,
+                  const int32_t* seq_len, const int32_t* tokens, const int32_t* row_offsets, int max_rows,
+                  int max_ctx, float* logits, int32_t* status, void* ws, size_t ws_bytes, hipStream_t st) {
+  const VerifyPlan v = plan_verify(s, ml, max_rows, max_ctx);
+  const VerifyWs w = carve_verify(s, v, max_rows, ws);
+  if (w.total > ws_bytes) return LSV_ERR_INVALID_ARG;
+  const char* P = (const char*)packed;
+  const int P64 = s.d / 64;
+
+  if (s.dtype == LSV_DTYPE_BF16)
+    hipLaunchKernelGGL(embed_kernel<bf16_t>, dim3(max_rows), dim3(256), 0, st, (const bf16_t*)(P + ml.embed), s.V,
+                       s.d, tokens, row_offsets, seq_len, batch, max_ctx, max_rows, w.h, w.stats, status);
+  else
+    hipLaunchKernelGGL(embed_kernel<float>, dim3(max_rows), dim3(256), 0, st, (const float*)(P + ml.embed), s.V, s.d,
+                       tokens, row_offsets, seq_len, batch, max_ctx, max_rows, w.h, w.stats, status);
+  if (hipGetLastError() != hipSuccess) return LSV_ERR_HIP;
+
+  GemmArgs base = {};
+  base.M_max = max_rows;
+  base.batch = batch;
+  base.row_offsets = row_offsets;
+  base.stats = w.stats;
+  base.P = P64;
+  base.eps = s.eps;
+  base.part = w.part;
+  base.counters = w.counters;
+  base.seq_len = seq_len;
+  base.kv = kv;
+  base.capacity = capacity;
+  base.nq = s.nq;
+  base.nkv = s.nkv;
+  base.hd = s.hd;
+  base.rope_base = s.rope_base;
+  base.F = s.F;
+
+  auto gemm = [&](GemmKind kind, const PackedMat& pm, const char* layer_base, GemmArgs a) {
+    const GemmPlan& p = v.g[kind];
+    a.W = (const uint4*)(layer_base + pm.offset);
+    a.N = pm.N;
+    a.K = pm.K;
+    a.Nt = pm.Nt;
+    a.Kt = pm.Kt;
+    a.S = p.S;
+    a.kf_max = p.kf_max;
+    return launch_gemm(s.dtype, kind, v.MT, a, p, st);
+  };
+
+  const size_t kv_layer_elems = (size_t)2 * batch * s.nkv * (size_t)capacity * s.hd;
+  int rc;
+  for (int l = 0; l < s.L; ++l) {
+    const char* LB = P + ml.layer_base + (size_t)l * ml.layer_stride;
+    // QKV + RoPE + cache append
+    GemmArgs a = base;
+    a.h = w.h;
+    a.gain = LB + ml.attn_norm;
+    a.q_out = w.q;
+    a.layer = l;
+    if ((rc = gemm(GEMM_QKV, ml.qkv, LB, a)) != LSV_OK) return rc;
+    // attention
+    AttnArgs at;
+    at.q = w.q;
+    at.k = (const char*)kv + (size_t)l * kv_layer_elems * s.es;
+    at.v = (const char*)at.k + kv_layer_elems / 2 * s.es;
+    at.capacity = capacity;
+    at.ctx_limit = max_ctx;
+    at.batch = batch;
+    at.nq = s.nq;
+    at.nkv = s.nkv;
+    at.M_max = max_rows;
+    at.row_offsets = row_offsets;
+    at.seq_len = seq_len;
+    at.o_part = w.o_part;
+    at.ml_part = w.ml_part;
+    at.out = w.attn;
+    at.scale_log2 = (float)(1.4426950408889634 / sqrt((double)s.hd));
+    if ((rc = launch_attention(s.dtype, s.hd, at, max_rows, v.n_chunks, st)) != LSV_OK) return rc;
+    // O projection + residual
+    a = base;
+    a.x = w.attn;
+    a.ldx = s.nq * s.hd;
+    a.h_out = w.h;
+    a.stats_out = w.stats;
+    if ((rc = gemm(GEMM_O, ml.o, LB, a)) != LSV_OK) return rc;
+    // gate/up + SwiGLU
+    a = base;
+    a.h = w.h;
+    a.gain = LB + ml.ffn_norm;
+    a.u_out = w.u;
+    if ((rc = gemm(GEMM_GATEUP, ml.gateup, LB, a)) != LSV_OK) return rc;
+    // down + residual
+    a = base;
+    a.x = w.u;
+    a.ldx = s.F;
+    a.h_out = w.h;
+    a.stats_out = w.stats;
+    if ((rc = gemm(GEMM_DOWN, ml.down, LB, a)) != LSV_OK) return rc;
+  }
+  GemmArgs a = base;
+  a.h = w.h;
+  a.gain = P + ml.final_norm;
+  a.out_f32 = logits;
+  a.ldo = s.V;
+  return gemm(GEMM_LMHEAD, ml.lm_head, P, a);
+}
+
+}  // namespace lsv

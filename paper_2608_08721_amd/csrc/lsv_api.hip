@@ -1,0 +1,204 @@
+// C-ABI of liblsv (declared in include/lsv.h): host-side validation, then launches.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include "lsv_device.h"
+#include "lsv_gemm.h"
+#include "lsv_internal.h"
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+int fail(int code, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof g_err, fmt, ap);
+  va_end(ap);
+  return code;
+}
+int ok() {
+  g_err[0] = 0;
+  return LSV_OK;
+}
+int hip_rc(int rc, const char* what) {
+  if (rc == LSV_ERR_HIP) return fail(LSV_ERR_HIP, "%s: %s", what, hipGetErrorString(hipGetLastError()));
+  if (rc == LSV_ERR_UNSUPPORTED) return fail(rc, "%s: unsupported shape", what);
+  if (rc != LSV_OK) return fail(rc, "%s failed", what);
+  return ok();
+}
+
+int check_config(const lsv_model_config* c) {
+  if (!c) return fail(LSV_ERR_INVALID_ARG, "cfg is NULL");
+  if (c->n_layers < 1 || c->d_model < 64 || c->d_model % 64 || c->n_q_heads < 1 || c->n_kv_heads < 1 ||
+      c->n_q_heads % c->n_kv_heads || c->d_ff < 4 || c->d_ff % 4 || c->vocab < 1)
+    return fail(LSV_ERR_INVALID_ARG, "bad model dimensions (d_model %% 64, n_q %% n_kv, d_ff %% 4 required)");
+  if (c->head_dim != 64 && c->head_dim != 128) return fail(LSV_ERR_UNSUPPORTED, "head_dim must be 64 or 128");
+  if (c->dtype != LSV_DTYPE_F32 && c->dtype != LSV_DTYPE_BF16) return fail(LSV_ERR_INVALID_ARG, "bad dtype");
+  if (!(c->rms_eps > 0.f) || !(c->rope_base > 0.0) || !isfinite(c->rope_base) || c->reserved0 != 0.f)
+    return fail(LSV_ERR_INVALID_ARG, "bad rms_eps / rope_base / reserved0");
+  return LSV_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* lsv_status_string(int s) {
+  switch (s) {
+    case LSV_OK: return "ok";
+    case LSV_ERR_INVALID_ARG: return "invalid argument";
+    case LSV_ERR_UNSUPPORTED: return "unsupported configuration";
+    case LSV_ERR_HIP: return "HIP runtime error";
+    case LSV_ERR_CAPACITY: return "KV-cache capacity exceeded";
+    case LSV_ERR_NONFINITE: return "non-finite value";
+  }
+  return "unknown status";
+}
+
+const char* lsv_last_error(void) { return g_err; }
+int lsv_abi_version(void) { return 1; }
+
+size_t lsv_packed_model_bytes(const lsv_model_config* cfg) {
+  if (check_config(cfg) != LSV_OK) return 0;
+  return lsv::model_layout(lsv::shape_of(cfg)).total;
+}
+
+int lsv_pack_globals(const lsv_model_config* cfg, const void* d_embed, const void* d_final_norm, const void* d_lm_head,
+                     void* d_packed, void* stream) {
+  int rc = check_config(cfg);
+  if (rc) return rc;
+  if (!d_embed || !d_final_norm || !d_lm_head || !d_packed) return fail(LSV_ERR_INVALID_ARG, "NULL pointer");
+  const lsv::Shape s = lsv::shape_of(cfg);
+  const lsv::ModelLayout ml = lsv::model_layout(s);
+  hipStream_t st = (hipStream_t)stream;
+  char* P = (char*)d_packed;
+  if (hipMemcpyAsync(P + ml.embed, d_embed, (size_t)s.V * s.d * s.es, hipMemcpyDeviceToDevice, st) != hipSuccess ||
+      hipMemcpyAsync(P + ml.final_norm, d_final_norm, (size_t)s.d * s.es, hipMemcpyDeviceToDevice, st) != hipSuccess)
+    return fail(LSV_ERR_HIP, "copy: %s", hipGetErrorString(hipGetLastError()));
+  return hip_rc(lsv::launch_pack(s, lsv::PACK_PLAIN, ml.lm_head, d_lm_head, nullptr, nullptr, P, st), "pack lm_head");
+}
+
+int lsv_pack_layer(const lsv_model_config* cfg, int32_t layer, const void* d_wq, const void* d_wk, const void* d_wv,
+                   const void* d_wo, const void* d_wg, const void* d_wu, const void* d_wd, const void* d_attn_norm,
+                   const void* d_ffn_norm, void* d_packed, void* stream) {
+  int rc = check_config(cfg);
+  if (rc) return rc;
+  if (layer < 0 || layer >= cfg->n_layers) return fail(LSV_ERR_INVALID_ARG, "layer %d out of range", layer);
+  if (!d_wq || !d_wk || !d_wv || !d_wo || !d_wg || !d_wu || !d_wd || !d_attn_norm || !d_ffn_norm || !d_packed)
+    return fail(LSV_ERR_INVALID_ARG, "NULL pointer");
+  const lsv::Shape s = lsv::shape_of(cfg);
+  const lsv::ModelLayout ml = lsv::model_layout(s);
+  hipStream_t st = (hipStream_t)stream;
+  char* LB = (char*)d_packed + ml.layer_base + (size_t)layer * ml.layer_stride;
+  if (hipMemcpyAsync(LB + ml.attn_norm, d_attn_norm, (size_t)s.d * s.es, hipMemcpyDeviceToDevice, st) != hipSuccess ||
+      hipMemcpyAsync(LB + ml.ffn_norm, d_ffn_norm, (size_t)s.d * s.es, hipMemcpyDeviceToDevice, st) != hipSuccess)
+    return fail(LSV_ERR_HIP, "copy: %s", hipGetErrorString(hipGetLastError()));
+  if ((rc = lsv::launch_pack(s, lsv::PACK_QKV, ml.qkv, d_wq, d_wk, d_wv, LB, st)) ||
+      (rc = lsv::launch_pack(s, lsv::PACK_PLAIN, ml.o, d_wo, nullptr, nullptr, LB, st)) ||
+      (rc = lsv::launch_pack(s, lsv::PACK_GATEUP, ml.gateup, d_wg, d_wu, nullptr, LB, st)) ||
+      (rc = lsv::launch_pack(s, lsv::PACK_PLAIN, ml.down, d_wd, nullptr, nullptr, LB, st)))
+    return hip_rc(rc, "pack layer");
+  return ok();
+}
+
+size_t lsv_kv_cache_bytes(const lsv_model_config* cfg, int32_t batch, int32_t capacity) {
+  if (check_config(cfg) != LSV_OK || batch < 1 || capacity < 1) return 0;
+  const lsv::Shape s = lsv::shape_of(cfg);
+  return (size_t)s.L * 2 * batch * s.nkv * (size_t)capacity * s.hd * s.es;
+}
+
+size_t lsv_verify_workspace_bytes(const lsv_model_config* cfg, int32_t batch, int32_t max_rows, int32_t max_ctx) {
+  if (check_config(cfg) != LSV_OK || batch < 1 || max_rows < 1 || max_rows > LSV_MAX_ROWS || max_ctx < 1) return 0;
+  return lsv::verify_workspace_bytes(lsv::shape_of(cfg), batch, max_rows, max_ctx);
+}
+
+__global__ void lsv_clear_kernel(uint4* p, size_t n16) {
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n16; i += (size_t)gridDim.x * blockDim.x)
+    p[i] = make_uint4(0, 0, 0, 0);
+}
+
+int lsv_workspace_clear(void* d_workspace, size_t bytes, void* stream) {
+  if (!d_workspace || bytes % 16 || ((uintptr_t)d_workspace & 15))
+    return fail(LSV_ERR_INVALID_ARG, "workspace must be non-NULL, 16-byte aligned and a multiple of 16 bytes");
+  const size_t n16 = bytes / 16;
+  unsigned blocks = (unsigned)((n16 + 255) / 256);
+  blocks = blocks > 4096 ? 4096 : (blocks == 0 ? 1 : blocks);
+  hipLaunchKernelGGL(lsv_clear_kernel, dim3(blocks), dim3(256), 0, (hipStream_t)stream, (uint4*)d_workspace, n16);
+  return hip_rc(hipGetLastError() == hipSuccess ? LSV_OK : LSV_ERR_HIP, "workspace clear");
+}
+
+int lsv_verify_block(const lsv_model_config* cfg, const void* d_packed, void* d_kv, int32_t capacity, int32_t batch,
+                     const int32_t* d_seq_len, const int32_t* d_tokens, const int32_t* d_row_offsets, int32_t max_rows,
+                     int32_t max_ctx, float* d_logits, int32_t* d_status, void* d_workspace, size_t workspace_bytes,
+                     void* stream) {
+  int rc = check_config(cfg);
+  if (rc) return rc;
+  if (!d_packed || !d_kv || !d_seq_len || !d_tokens || !d_row_offsets || !d_logits || !d_workspace)
+    return fail(LSV_ERR_INVALID_ARG, "NULL pointer");
+  if (batch < 1 || batch > LSV_MAX_BATCH) return fail(LSV_ERR_INVALID_ARG, "batch %d not in [1, %d]", batch, LSV_MAX_BATCH);
+  if (max_rows < 1 || max_rows > LSV_MAX_ROWS)
+    return fail(LSV_ERR_INVALID_ARG, "max_rows %d not in [1, %d]", max_rows, LSV_MAX_ROWS);
+  if (capacity < 1 || max_ctx < 1 || max_ctx > capacity)
+    return fail(LSV_ERR_INVALID_ARG, "need 1 <= max_ctx (%d) <= capacity (%d)", max_ctx, capacity);
+  const lsv::Shape s = lsv::shape_of(cfg);
+  if (s.dtype == LSV_DTYPE_F32 && max_ctx > 16384)
+    return fail(LSV_ERR_UNSUPPORTED, "fp32 models support max_ctx <= 16384");
+  const size_t need = lsv::verify_workspace_bytes(s, batch, max_rows, max_ctx);
+  if (workspace_bytes < need)
+    return fail(LSV_ERR_INVALID_ARG, "workspace %zu bytes < %zu required", workspace_bytes, need);
+  const lsv::ModelLayout ml = lsv::model_layout(s);
+  rc = lsv::launch_verify(s, ml, d_packed, d_kv, capacity, batch, d_seq_len, d_tokens, d_row_offsets, max_rows, max_ctx,
+                          d_logits, d_status, d_workspace, workspace_bytes, (hipStream_t)stream);
+  return hip_rc(rc, "verify");
+}
+
+size_t lsv_accept_workspace_bytes(int32_t batch, int32_t max_rows, int32_t vocab) {
+  if (batch < 1 || max_rows < 1 || vocab < 1) return 0;
+  return lsv::accept_workspace_bytes(batch, max_rows, vocab);
+}
+
+int lsv_accept(int32_t mode, int32_t batch, int32_t vocab, const float* d_logits, const int32_t* d_row_offsets,
+               int32_t max_rows, int32_t max_rows_per_seq, const int32_t* d_tokens, const float* d_draft_probs,
+               float temperature, uint64_t seed, uint64_t round, int32_t* d_accept_len, int32_t* d_out_tokens,
+               int32_t* d_seq_len, int32_t* d_status, void* d_workspace, size_t workspace_bytes, void* stream) {
+  if (mode != LSV_ACC_GREEDY && mode != LSV_ACC_SAMPLE) return fail(LSV_ERR_INVALID_ARG, "bad accept mode %d", mode);
+  if (batch < 1 || batch > LSV_MAX_BATCH || vocab < 1) return fail(LSV_ERR_INVALID_ARG, "bad batch or vocab");
+  if (max_rows < 1 || max_rows_per_seq < 1 || max_rows_per_seq > LSV_MAX_ROWS)
+    return fail(LSV_ERR_INVALID_ARG, "bad max_rows / max_rows_per_seq");
+  if (!d_logits || !d_row_offsets || !d_tokens || !d_accept_len || !d_out_tokens || !d_workspace)
+    return fail(LSV_ERR_INVALID_ARG, "NULL pointer");
+  if (mode == LSV_ACC_SAMPLE && (!d_draft_probs || !(temperature > 0.f) || !isfinite(temperature)))
+    return fail(LSV_ERR_INVALID_ARG, "sampling needs draft probabilities and a finite temperature > 0");
+  if (workspace_bytes < lsv::accept_workspace_bytes(batch, max_rows, vocab))
+    return fail(LSV_ERR_INVALID_ARG, "accept workspace too small");
+  int rc = lsv::launch_accept(mode, batch, vocab, d_logits, d_row_offsets, max_rows, max_rows_per_seq, d_tokens,
+                              d_draft_probs, temperature, seed, round, d_accept_len, d_out_tokens, d_seq_len, d_status,
+                              d_workspace, (hipStream_t)stream);
+  return hip_rc(rc, "accept");
+}
+
+int lsv_select_length(int32_t mode, int32_t batch, int32_t G, const float* d_conf, const double* d_cost, int32_t d_init,
+                      int32_t d_max, double alpha, int32_t block_n, uint32_t flags, int32_t* d_gamma, int32_t* d_aux,
+                      int32_t* d_status, void* stream) {
+  if (mode != LSV_SEL_MARGINAL && mode != LSV_SEL_EXHAUSTIVE && mode != LSV_SEL_ALG1)
+    return fail(LSV_ERR_INVALID_ARG, "bad selector mode %d", mode);
+  if (batch < 1 || G < 1 || G > LSV_MAX_G) return fail(LSV_ERR_INVALID_ARG, "need batch >= 1 and 1 <= G <= %d", LSV_MAX_G);
+  if (d_max < 1 || d_max > G) return fail(LSV_ERR_INVALID_ARG, "need 1 <= d_max (%d) <= G (%d)", d_max, G);
+  if (!d_conf || !d_gamma) return fail(LSV_ERR_INVALID_ARG, "NULL pointer");
+  if (flags & ~(uint32_t)LSV_SEL_BONUS) return fail(LSV_ERR_INVALID_ARG, "unknown flags");
+  if (mode == LSV_SEL_ALG1) {
+    if (block_n < 1) return fail(LSV_ERR_INVALID_ARG, "block_n must be >= 1");
+    if (!(alpha > 0.0) || !(alpha <= 1.0e6)) return fail(LSV_ERR_INVALID_ARG, "alpha must be in (0, 1e6]");
+  } else {
+    if (!d_cost) return fail(LSV_ERR_INVALID_ARG, "cost table required");
+    if (mode == LSV_SEL_MARGINAL && d_init < 1) return fail(LSV_ERR_INVALID_ARG, "d_init must be >= 1");
+  }
+  int rc = lsv::launch_select(mode, batch, G, d_conf, d_cost, d_init, d_max, alpha, block_n, flags, d_gamma, d_aux,
+                              d_status, (hipStream_t)stream);
+  return hip_rc(rc, "select");
+}
+
+}  // extern "C"

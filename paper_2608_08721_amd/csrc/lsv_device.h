@@ -1,0 +1,69 @@
+// Internal device helpers shared by the gfx950 kernels of liblsv.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#define LSV_DEV __device__ __forceinline__
+
+typedef uint16_t bf16_t;  // storage type: IEEE bfloat16 bit pattern
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+namespace lsv {
+
+constexpr int kWave = 64;
+
+LSV_DEV float bf2f(bf16_t b) { return __uint_as_float(((uint32_t)b) << 16); }
+
+// fp32 -> bf16, round to nearest even; NaN stays a quiet NaN.
+LSV_DEV bf16_t f2bf(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7f800000u) == 0x7f800000u && (u & 0x007fffffu)) return (bf16_t)((u >> 16) | 0x40u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (bf16_t)(u >> 16);
+}
+
+// Element conversions for the two storage types.
+template <typename T> LSV_DEV float to_f32(T x);
+template <> LSV_DEV float to_f32<float>(float x) { return x; }
+template <> LSV_DEV float to_f32<bf16_t>(bf16_t x) { return bf2f(x); }
+template <typename T> LSV_DEV T from_f32(float x);
+template <> LSV_DEV float from_f32<float>(float x) { return x; }
+template <> LSV_DEV bf16_t from_f32<bf16_t>(float x) { return f2bf(x); }
+
+// Sequence that owns block row m (linear scan: batches are small).
+LSV_DEV int seq_of_row(const int32_t* row_offsets, int batch, int m) {
+  int b = 0;
+  while (b + 1 < batch && row_offsets[b + 1] <= m) ++b;
+  return b;
+}
+
+// Device-scope release/acquire around a "last workgroup finishes" counter.
+// Returns true in every thread of the workgroup that arrived last.
+LSV_DEV bool arrive_last(int* counter, int expected, int* lds_flag) {
+  __threadfence();
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int old = __hip_atomic_fetch_add(counter, 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+    *lds_flag = (old == expected - 1);
+  }
+  __syncthreads();
+  bool last = *lds_flag != 0;
+  if (last) __threadfence();
+  return last;
+}
+
+LSV_DEV void reset_counter(int* counter) {
+  if (threadIdx.x == 0) __hip_atomic_store(counter, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+LSV_DEV float wave_max(float v) {
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, kWave));
+  return v;
+}
+LSV_DEV float wave_sum(float v) {
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
+  return v;
+}
+
+}  // namespace lsv

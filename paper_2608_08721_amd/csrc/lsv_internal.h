@@ -1,0 +1,58 @@
+// Internal host/device declarations of liblsv (not part of the public ABI).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "lsv.h"
+
+namespace lsv {
+
+// ---------------------------------------------------------------- selector
+int launch_select(int mode, int batch, int G, const float* conf, const double* cost, int d_init, int d_max,
+                  double alpha, int block_n, unsigned flags, int32_t* gamma, int32_t* aux, int32_t* status,
+                  hipStream_t stream);
+
+// ---------------------------------------------------------------- accept
+constexpr int kAcceptChunk = 4096;  // vocabulary entries per workgroup in the row scans
+inline int accept_chunks(int vocab) { return (vocab + kAcceptChunk - 1) / kAcceptChunk; }
+size_t accept_workspace_bytes(int batch, int max_rows, int vocab);
+int launch_accept(int mode, int batch, int vocab, const float* logits, const int32_t* row_offsets, int max_rows,
+                  int max_rows_per_seq, const int32_t* tokens, const float* draft_probs, float temperature,
+                  uint64_t seed, uint64_t round, int32_t* accept_len, int32_t* out_tokens, int32_t* seq_len,
+                  int32_t* status, void* ws, hipStream_t stream);
+
+// ---------------------------------------------------------------- forward
+struct Shape {
+  int L, d, nq, nkv, hd, F, V, dtype, es;  // es = element size of the storage type
+  float eps;
+  double rope_base;
+};
+Shape shape_of(const lsv_model_config* c);
+
+// Packed matrix = fragments of 16 rows x KT columns (KT = 32 bf16 / 16 fp32), 1 KiB each.
+struct PackedMat {
+  size_t offset;  // byte offset in the packed model buffer
+  int N, K;       // logical rows (out features) and columns (in features)
+  int Nt, Kt;     // fragment counts (zero-padded)
+};
+struct ModelLayout {
+  size_t embed, final_norm;  // raw row-major embedding [V, d], gain [d]
+  PackedMat lm_head;
+  size_t layer_base, layer_stride;  // per-layer block
+  size_t attn_norm, ffn_norm;       // offsets inside a layer block
+  PackedMat qkv, o, gateup, down;   // offsets inside a layer block
+  size_t total;
+};
+ModelLayout model_layout(const Shape& s);
+
+enum PackKind { PACK_PLAIN = 0, PACK_QKV = 1, PACK_GATEUP = 2 };
+int launch_pack(const Shape& s, PackKind kind, const PackedMat& pm, const void* src0, const void* src1,
+                const void* src2, void* dst, hipStream_t stream);
+
+size_t verify_workspace_bytes(const Shape& s, int batch, int max_rows, int max_ctx);
+int launch_verify(const Shape& s, const ModelLayout& ml, const void* packed, void* kv, int capacity, int batch,
+                  const int32_t* seq_len, const int32_t* tokens, const int32_t* row_offsets, int max_rows,
+                  int max_ctx, float* logits, int32_t* status, void* ws, size_t ws_bytes, hipStream_t stream);
+
+}  // namespace lsv

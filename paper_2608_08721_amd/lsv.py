@@ -1,0 +1,161 @@
+"""ctypes binding of liblsv (include/lsv.h): argument marshalling only.
+
+Every function has the C name and argument order.  Device buffers may be given as
+torch tensors (their data_ptr() is passed) or as raw integer addresses; ``stream``
+defaults to torch's current stream.  A non-zero status raises LsvError carrying
+the code and lsv_last_error().  Nothing here computes: each call enqueues HIP work.
+"""
+import ctypes
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "liblsv.so")
+
+LSV_OK, LSV_ERR_INVALID_ARG, LSV_ERR_UNSUPPORTED, LSV_ERR_HIP, LSV_ERR_CAPACITY, LSV_ERR_NONFINITE = 0, -1, -2, -3, -4, -5
+LSV_DTYPE_F32, LSV_DTYPE_BF16 = 0, 1
+LSV_MAX_BATCH, LSV_MAX_ROWS, LSV_MAX_G = 64, 64, 64
+LSV_ACC_GREEDY, LSV_ACC_SAMPLE = 0, 1
+LSV_SEL_MARGINAL, LSV_SEL_EXHAUSTIVE, LSV_SEL_ALG1 = 0, 1, 2
+LSV_SEL_BONUS = 1
+
+EXPORTED = (
+    "lsv_status_string", "lsv_last_error", "lsv_abi_version", "lsv_packed_model_bytes", "lsv_pack_globals",
+    "lsv_pack_layer", "lsv_kv_cache_bytes", "lsv_verify_workspace_bytes", "lsv_workspace_clear",
+    "lsv_verify_block", "lsv_accept_workspace_bytes", "lsv_accept", "lsv_select_length",
+)
+
+
+class LsvError(RuntimeError):
+    def __init__(self, code, msg):
+        super().__init__(f"lsv status {code}: {msg}")
+        self.code = code
+
+
+class ModelConfig(ctypes.Structure):
+    _fields_ = [
+        ("n_layers", ctypes.c_int32), ("d_model", ctypes.c_int32), ("n_q_heads", ctypes.c_int32),
+        ("n_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32), ("d_ff", ctypes.c_int32),
+        ("vocab", ctypes.c_int32), ("dtype", ctypes.c_int32), ("rms_eps", ctypes.c_float),
+        ("reserved0", ctypes.c_float), ("rope_base", ctypes.c_double),
+    ]
+
+
+_lib = None
+
+
+def load(path=LIB_PATH):
+    """Load liblsv.so; raises (never falls back) when the HIP library is missing."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise ImportError(f"{path} is not built: run __graft_entry__.build() (hipcc, gfx950)")
+    lib = ctypes.CDLL(path)
+    P, I32, U32, U64, SZ, F32, F64 = (ctypes.c_void_p, ctypes.c_int32, ctypes.c_uint32, ctypes.c_uint64,
+                                      ctypes.c_size_t, ctypes.c_float, ctypes.c_double)
+    CP = ctypes.POINTER(ModelConfig)
+    sig = {
+        "lsv_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+        "lsv_last_error": (ctypes.c_char_p, []),
+        "lsv_abi_version": (ctypes.c_int, []),
+        "lsv_packed_model_bytes": (SZ, [CP]),
+        "lsv_pack_globals": (ctypes.c_int, [CP, P, P, P, P, P]),
+        "lsv_pack_layer": (ctypes.c_int, [CP, I32, P, P, P, P, P, P, P, P, P, P, P]),
+        "lsv_kv_cache_bytes": (SZ, [CP, I32, I32]),
+        "lsv_verify_workspace_bytes": (SZ, [CP, I32, I32, I32]),
+        "lsv_workspace_clear": (ctypes.c_int, [P, SZ, P]),
+        "lsv_verify_block": (ctypes.c_int, [CP, P, P, I32, I32, P, P, P, I32, I32, P, P, P, SZ, P]),
+        "lsv_accept_workspace_bytes": (SZ, [I32, I32, I32]),
+        "lsv_accept": (ctypes.c_int, [I32, I32, I32, P, P, I32, I32, P, P, F32, U64, U64, P, P, P, P, P, SZ, P]),
+        "lsv_select_length": (ctypes.c_int, [I32, I32, I32, P, P, I32, I32, F64, I32, U32, P, P, P, P]),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = lib
+    return lib
+
+
+def _ptr(x):
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    return x.data_ptr()
+
+
+def _stream(s):
+    if s is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(s, int):
+        return s
+    return s.cuda_stream
+
+
+def _check(rc):
+    if rc != LSV_OK:
+        raise LsvError(rc, load().lsv_last_error().decode())
+
+
+def lsv_status_string(code):
+    return load().lsv_status_string(code).decode()
+
+
+def lsv_last_error():
+    return load().lsv_last_error().decode()
+
+
+def lsv_abi_version():
+    return load().lsv_abi_version()
+
+
+def lsv_packed_model_bytes(cfg):
+    return load().lsv_packed_model_bytes(ctypes.byref(cfg))
+
+
+def lsv_pack_globals(cfg, embed, final_norm, lm_head, packed, stream=None):
+    _check(load().lsv_pack_globals(ctypes.byref(cfg), _ptr(embed), _ptr(final_norm), _ptr(lm_head), _ptr(packed),
+                                   _stream(stream)))
+
+
+def lsv_pack_layer(cfg, layer, wq, wk, wv, wo, wg, wu, wd, attn_norm, ffn_norm, packed, stream=None):
+    _check(load().lsv_pack_layer(ctypes.byref(cfg), layer, *(_ptr(t) for t in (wq, wk, wv, wo, wg, wu, wd, attn_norm,
+                                                                                  ffn_norm, packed)), _stream(stream)))
+
+
+def lsv_kv_cache_bytes(cfg, batch, capacity):
+    return load().lsv_kv_cache_bytes(ctypes.byref(cfg), batch, capacity)
+
+
+def lsv_verify_workspace_bytes(cfg, batch, max_rows, max_ctx):
+    return load().lsv_verify_workspace_bytes(ctypes.byref(cfg), batch, max_rows, max_ctx)
+
+
+def lsv_workspace_clear(ws, nbytes, stream=None):
+    _check(load().lsv_workspace_clear(_ptr(ws), nbytes, _stream(stream)))
+
+
+def lsv_verify_block(cfg, packed, kv, capacity, batch, seq_len, tokens, row_offsets, max_rows, max_ctx, logits,
+                     status, ws, ws_bytes, stream=None):
+    _check(load().lsv_verify_block(ctypes.byref(cfg), _ptr(packed), _ptr(kv), capacity, batch, _ptr(seq_len),
+                                   _ptr(tokens), _ptr(row_offsets), max_rows, max_ctx, _ptr(logits), _ptr(status),
+                                   _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def lsv_accept_workspace_bytes(batch, max_rows, vocab):
+    return load().lsv_accept_workspace_bytes(batch, max_rows, vocab)
+
+
+def lsv_accept(mode, batch, vocab, logits, row_offsets, max_rows, max_rows_per_seq, tokens, draft_probs, temperature,
+               seed, round, accept_len, out_tokens, seq_len, status, ws, ws_bytes, stream=None):
+    _check(load().lsv_accept(mode, batch, vocab, _ptr(logits), _ptr(row_offsets), max_rows, max_rows_per_seq,
+                             _ptr(tokens), _ptr(draft_probs), temperature, seed, round, _ptr(accept_len),
+                             _ptr(out_tokens), _ptr(seq_len), _ptr(status), _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def lsv_select_length(mode, batch, G, conf, cost, d_init, d_max, alpha, block_n, flags, gamma, aux, status,
+                      stream=None):
+    _check(load().lsv_select_length(mode, batch, G, _ptr(conf), _ptr(cost), d_init, d_max, alpha, block_n, flags,
+                                    _ptr(gamma), _ptr(aux), _ptr(status), _stream(stream)))

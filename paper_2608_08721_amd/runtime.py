@@ -1,0 +1,85 @@
+"""Device buffers for the verify path: packed model, KV cache, workspaces.
+
+torch provides device memory and streams; all compute is in liblsv.so."""
+import numpy as np
+import torch
+
+from . import lsv
+
+
+def model_config(shape):
+    """lsv.ModelConfig from any object with the usual fields (n_layers, d_model, ...)."""
+    return lsv.ModelConfig(
+        n_layers=shape.n_layers, d_model=shape.d_model, n_q_heads=shape.n_q_heads, n_kv_heads=shape.n_kv_heads,
+        head_dim=shape.head_dim, d_ff=shape.d_ff, vocab=shape.vocab,
+        dtype=lsv.LSV_DTYPE_BF16 if shape.dtype == "bf16" else lsv.LSV_DTYPE_F32,
+        rms_eps=shape.rms_eps, reserved0=0.0, rope_base=shape.rope_base)
+
+
+def storage_dtype(cfg):
+    return torch.bfloat16 if cfg.dtype == lsv.LSV_DTYPE_BF16 else torch.float32
+
+
+def to_device(arr, device="cuda"):
+    """numpy array in storage form (float32, or uint16 bf16 bit patterns) -> device tensor."""
+    a = np.ascontiguousarray(arr)
+    if a.dtype == np.uint16:
+        return torch.from_numpy(a.view(np.int16)).to(device).view(torch.bfloat16)
+    return torch.from_numpy(a).to(device)
+
+
+class DeviceModel:
+    """Packed weights of one model in a single device buffer."""
+
+    def __init__(self, cfg, device="cuda"):
+        self.cfg = cfg
+        self.device = device
+        self.nbytes = lsv.lsv_packed_model_bytes(cfg)
+        if self.nbytes == 0:
+            raise lsv.LsvError(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_last_error())
+        self.buf = torch.empty(self.nbytes, dtype=torch.uint8, device=device)
+
+    def pack_globals(self, embed, final_norm, lm_head):
+        t = [to_device(x, self.device) for x in (embed, final_norm, lm_head)]
+        lsv.lsv_pack_globals(self.cfg, *t, self.buf)
+        torch.cuda.current_stream().synchronize()
+
+    def pack_layer(self, layer, w):
+        keys = ("wq", "wk", "wv", "wo", "wg", "wu", "wd", "attn_norm", "ffn_norm")
+        t = [to_device(w[k], self.device) for k in keys]
+        lsv.lsv_pack_layer(self.cfg, layer, *t, self.buf)
+        torch.cuda.current_stream().synchronize()
+
+    @classmethod
+    def from_weights(cls, cfg, weights, device="cuda"):
+        """weights: {"embed", "final_norm", "lm_head", "layers": [dict per layer]} in storage form."""
+        dm = cls(cfg, device)
+        dm.pack_globals(weights["embed"], weights["final_norm"], weights["lm_head"])
+        for l, w in enumerate(weights["layers"]):
+            dm.pack_layer(l, w)
+        return dm
+
+
+class KVCache:
+    def __init__(self, cfg, batch, capacity, device="cuda"):
+        self.cfg, self.batch, self.capacity = cfg, batch, capacity
+        nbytes = lsv.lsv_kv_cache_bytes(cfg, batch, capacity)
+        self.buf = torch.zeros(nbytes, dtype=torch.uint8, device=device)
+
+    def view(self):
+        """[layer][K/V][batch][kv_head][pos][head_dim] typed view of the buffer."""
+        c = self.cfg
+        return self.buf.view(storage_dtype(c)).view(c.n_layers, 2, self.batch, c.n_kv_heads, self.capacity,
+                                                    c.head_dim)
+
+
+class Workspace:
+    """Zero-initialised device scratch (the library keeps its counters at zero)."""
+
+    def __init__(self, nbytes, device="cuda"):
+        self.nbytes = max(256, (int(nbytes) + 255) // 256 * 256)
+        self.buf = torch.zeros(self.nbytes, dtype=torch.uint8, device=device)
+
+
+def row_offsets_of(rows_per_seq):
+    return np.concatenate([[0], np.cumsum(rows_per_seq)]).astype(np.int32)

@@ -1,0 +1,69 @@
+"""Helpers shared by the GPU tests: device set-up and oracle comparisons."""
+import numpy as np
+import torch
+
+from oracle import forward as OF
+from paper_2608_08721_amd import lsv, runtime
+
+DEV = "cuda"
+
+
+def i32(x):
+    return torch.tensor(np.asarray(x, dtype=np.int32), device=DEV)
+
+
+def note(msg):
+    print(msg, flush=True)
+
+
+class GpuModel:
+    """Packed model + KV cache + verify workspace on the GPU, driven through the C-ABI."""
+
+    def __init__(self, shape, weights, batch, capacity, max_rows=64):
+        self.shape = shape
+        self.cfg = runtime.model_config(shape)
+        self.dm = runtime.DeviceModel.from_weights(self.cfg, weights)
+        self.batch, self.capacity, self.max_rows = batch, capacity, max_rows
+        self.kv = runtime.KVCache(self.cfg, batch, capacity)
+        self.ws = runtime.Workspace(lsv.lsv_verify_workspace_bytes(self.cfg, batch, max_rows, capacity))
+        self.logits = torch.full((max_rows, shape.vocab), float("nan"), dtype=torch.float32, device=DEV)
+        self.status = torch.full((batch,), 99, dtype=torch.int32, device=DEV)
+
+    def verify(self, seq_len, tokens, row_offsets, max_ctx=None):
+        M = int(row_offsets[-1])
+        lsv.lsv_verify_block(self.cfg, self.dm.buf, self.kv.buf, self.capacity, self.batch, i32(seq_len),
+                             i32(tokens), i32(row_offsets), self.max_rows, max_ctx or self.capacity, self.logits,
+                             self.status, self.ws.buf, self.ws.nbytes)
+        torch.cuda.synchronize()
+        return self.logits[:M].double().cpu().numpy(), self.status.cpu().numpy()
+
+    def prefill(self, prompts):
+        """Chunked prefill of every sequence through lsv_verify_block; returns last-row logits."""
+        B = len(prompts)
+        filled = [0] * B
+        last = [None] * B
+        per = max(1, self.max_rows // B)
+        while any(filled[b] < len(prompts[b]) for b in range(B)):
+            take = [min(per, len(prompts[b]) - filled[b]) for b in range(B)]
+            toks = [prompts[b][filled[b]:filled[b] + take[b]] for b in range(B)]
+            off = runtime.row_offsets_of(take)
+            seq = list(filled)
+            lg, st = self.verify(seq, np.concatenate(toks), off)
+            for b in range(B):
+                if take[b]:
+                    assert st[b] == 0, st
+                    filled[b] += take[b]
+                    if filled[b] == len(prompts[b]):
+                        last[b] = lg[off[b + 1] - 1]
+        return np.stack(last), np.array(filled, dtype=np.int32)
+
+
+def row_rel_err(got, want):
+    """Per row: max |got - want| / max |want|."""
+    den = np.maximum(np.abs(want).max(axis=1), 1e-30)
+    return (np.abs(got - want).max(axis=1) / den)
+
+
+def top2_margin(row):
+    s = np.sort(row)
+    return s[-1] - s[-2]

@@ -1,0 +1,101 @@
+"""CPU-only checks of the C-ABI: the library loads, exports every function that
+include/lsv.h declares, and rejects bad arguments on the host before any HIP call."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2608_08721_amd import lsv
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared():
+    src = open(os.path.join(ROOT, "include", "lsv.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(lsv_[a-z_0-9]+)\s*\(", src)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(lsv.LIB_PATH):
+        from paper_2608_08721_amd import build
+        build.build()
+    return lsv.load()
+
+
+def test_exports_every_declared_symbol(lib):
+    names = declared()
+    assert len(names) >= 13
+    for n in names:
+        assert hasattr(lib, n), n
+    assert sorted(lsv.EXPORTED) == names
+
+
+def test_status_strings(lib):
+    assert lsv.lsv_status_string(0) == "ok"
+    assert "capacity" in lsv.lsv_status_string(lsv.LSV_ERR_CAPACITY)
+    assert lsv.lsv_abi_version() == 1
+
+
+def tiny_cfg(**kw):
+    c = dict(n_layers=2, d_model=256, n_q_heads=4, n_kv_heads=4, head_dim=64, d_ff=688, vocab=1024,
+             dtype=lsv.LSV_DTYPE_F32, rms_eps=1e-5, reserved0=0.0, rope_base=10000.0)
+    c.update(kw)
+    return lsv.ModelConfig(**c)
+
+
+def test_size_queries_are_host_only(lib):
+    cfg = tiny_cfg()
+    assert lsv.lsv_packed_model_bytes(cfg) > 0
+    assert lsv.lsv_kv_cache_bytes(cfg, 2, 100) == 2 * 2 * 2 * 4 * 100 * 64 * 4
+    assert lsv.lsv_verify_workspace_bytes(cfg, 1, 17, 145) > 0
+    assert lsv.lsv_verify_workspace_bytes(cfg, 1, 65, 145) == 0
+    assert lsv.lsv_packed_model_bytes(tiny_cfg(head_dim=96)) == 0
+    assert lsv.lsv_packed_model_bytes(tiny_cfg(n_kv_heads=3)) == 0
+    assert lsv.lsv_accept_workspace_bytes(1, 17, 128256) > 0
+
+
+def expect(code, fn, *args):
+    with pytest.raises(lsv.LsvError) as e:
+        fn(*args)
+    assert e.value.code == code, str(e.value)
+    return str(e.value)
+
+
+def test_host_validation(lib):
+    cfg = tiny_cfg()
+    S = 0  # stream handle; never reached
+    # selector
+    expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_select_length, 7, 1, 4, 1, 1, 1, 4, 2.0, 2, 0, 1, None, None, S)
+    expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_select_length, 0, 1, 65, 1, 1, 1, 4, 2.0, 2, 0, 1, None, None, S)
+    expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_select_length, 0, 1, 4, 1, 1, 1, 5, 2.0, 2, 0, 1, None, None, S)
+    expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_select_length, 0, 1, 4, 1, None, 1, 4, 2.0, 2, 0, 1, None, None, S)
+    expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_select_length, 2, 1, 4, 1, None, 1, 4, 0.0, 2, 0, 1, None, None, S)
+    expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_select_length, 2, 1, 4, 1, None, 1, 4, 2.0, 0, 0, 1, None, None, S)
+    expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_select_length, 1, 1, 4, 1, 1, 1, 4, 2.0, 2, 4, 1, None, None, S)
+    # accept
+    expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_accept, 3, 1, 10, 1, 1, 2, 2, 1, None, 0.0, 0, 0, 1, 1, None, None, 1,
+           1 << 20, S)
+    expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_accept, 1, 1, 10, 1, 1, 2, 2, 1, 1, 0.0, 0, 0, 1, 1, None, None, 1,
+           1 << 20, S)
+    expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_accept, 1, 1, 10, 1, 1, 2, 2, 1, None, 1.0, 0, 0, 1, 1, None, None, 1,
+           1 << 20, S)
+    expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_accept, 0, 1, 10, 1, 1, 2, 65, 1, None, 0.0, 0, 0, 1, 1, None, None, 1,
+           1 << 20, S)
+    expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_accept, 0, 1, 10, 1, 1, 2, 2, 1, None, 0.0, 0, 0, 1, 1, None, None, 1,
+           16, S)
+    # verify
+    args = [cfg, 1, 1, 100, 1, 1, 1, 1, 17, 100, 1, None, 1, 1 << 30, S]
+    msg = expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_verify_block, *(args[:9] + [101] + args[10:]))
+    assert "max_ctx" in msg
+    expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_verify_block, *(args[:8] + [65] + args[9:]))
+    expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_verify_block, *(args[:4] + [0] + args[5:]))
+    expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_verify_block, *(args[:13] + [16] + args[14:]))
+    expect(lsv.LSV_ERR_UNSUPPORTED, lsv.lsv_verify_block, *([tiny_cfg(head_dim=96)] + args[1:]))
+    expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_verify_block, *([tiny_cfg(reserved0=1.0)] + args[1:]))
+    expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_verify_block, *(args[:1] + [None] + args[2:]))
+    # pack
+    expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_pack_layer, cfg, 2, *([1] * 10), S)
+    expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_workspace_clear, 1, 17, S)

@@ -1,0 +1,133 @@
+"""GPU verify forward pass (lsv_verify_block) and the whole step vs the oracle.
+
+* tiny fp32 decoder (2 layers, d 256, 4 x 64 heads, F 688, V 1024, context 128):
+  prefill and verify logits within 1e-5 of the largest logit of each row, and the
+  greedy accept results bit-exact (argmax margins dwarf that error);
+* bf16 decoders (grouped-query attention, head_dim 64 and 128, ragged contexts over
+  several 64-key chunks): logits within 2e-2; greedy decisions equal wherever the
+  oracle's top-2 margin exceeds twice the measured logit error;
+* Llama-3-8B width (d 4096, 32/8 x 128 heads, F 14336, V 128256) with 2 of its 32
+  layers, context 2048 from the seeded KV generator, 17 rows: the same bf16 bar."""
+import copy
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import accept as OA
+from oracle import forward as OF
+from paper_2608_08721_amd import lsv, runtime
+from synth import configs, gen
+from tests.lsv_testing import GpuModel, i32, note, row_rel_err, top2_margin
+
+pytestmark = pytest.mark.gpu
+
+
+def greedy_gpu(logits_t, off, tokens, width):
+    B = len(off) - 1
+    M, V = logits_t.shape
+    ws = runtime.Workspace(lsv.lsv_accept_workspace_bytes(B, M, V))
+    acc = torch.zeros(B, dtype=torch.int32, device="cuda")
+    out = torch.zeros((B, width), dtype=torch.int32, device="cuda")
+    st = torch.zeros(B, dtype=torch.int32, device="cuda")
+    lsv.lsv_accept(lsv.LSV_ACC_GREEDY, B, V, logits_t, i32(off), M, width, i32(tokens), None, 0.0, 0, 0, acc, out,
+                   None, st, ws.buf, ws.nbytes)
+    torch.cuda.synchronize()
+    return acc.cpu().numpy(), out.cpu().numpy(), st.cpu().numpy()
+
+
+def test_tiny_f32_end_to_end():
+    wl = configs.WORKLOADS["tiny-f32-b1-c128"]
+    m = wl.model
+    w = gen.model_weights(m, wl.seed)
+    C = int(gen.contexts(wl)[0])
+    prompt = gen.prefix_ids(wl.seed, 1, [C], m.vocab)[0]
+    note(f"tiny f32: prefill {C} tokens")
+    om = OF.Model(m, w)
+    ocache = OF.KVCache(m, 1, 256)
+    o_last, o_len = OF.prefill(om, ocache, [prompt])
+    gm = GpuModel(m, w, 1, 256)
+    g_last, g_len = gm.prefill([prompt])
+    assert row_rel_err(g_last, o_last).max() <= 1e-5
+    root = int(np.argmax(o_last[0]))
+    assert root == int(np.argmax(g_last[0]))
+    # plant: first k drafts are the target's greedy continuation, the rest random ids
+    for k in (0, 5, 16):
+        cont = OF.greedy_continuation(om, copy.deepcopy(ocache), C, root, k) if k else []
+        rand = list(gen.randint(wl.seed, 500 + k, wl.G - k, m.vocab))
+        drafts = cont + rand
+        toks = np.array([root] + drafts, np.int32)
+        off = [0, wl.G + 1]
+        oc = copy.deepcopy(ocache)
+        o_logits, _ = OF.verify_block(om, oc, [C], toks, off)
+        g_logits, st = gm.verify([C], toks, off)
+        assert st[0] == 0
+        err = row_rel_err(g_logits, o_logits)
+        note(f"  k={k}: max row rel err {err.max():.2e}")
+        assert err.max() <= 1e-5
+        want = OA.accept_greedy(o_logits, off, toks)
+        margins = [top2_margin(r) / np.abs(r).max() for r in o_logits]
+        assert min(margins) > 1e-4   # every decision is far outside the error bound
+        acc, out, st = greedy_gpu(gm.logits[:wl.G + 1], off, toks, wl.G + 1)
+        assert acc[0] == want["accept_len"][0] and np.array_equal(out[0], want["out_tokens"][0])
+        if k == 16:
+            assert acc[0] == 16
+
+
+def _bf16_case(shape, seed, contexts, rows, tol=2e-2):
+    B = len(contexts)
+    w = gen.model_weights(shape, seed)
+    cap = max(contexts) + max(rows) + 8
+    gm = GpuModel(shape, w, B, cap)
+    om = OF.Model(shape, w)
+    oc = OF.KVCache(shape, B, cap)
+    kvv = gm.kv.view()
+    for l in range(shape.n_layers):
+        for b in range(B):
+            k, v = gen.synthetic_kv(shape, seed + 31 * b, l, 1, contexts[b])
+            kvv[l, 0, b, :, :contexts[b]] = runtime.to_device(k[0])
+            kvv[l, 1, b, :, :contexts[b]] = runtime.to_device(v[0])
+            oc.k[l][b, :, :contexts[b]] = OF.stored_to_f64(k[0], "bf16")
+            oc.v[l][b, :, :contexts[b]] = OF.stored_to_f64(v[0], "bf16")
+    off = runtime.row_offsets_of(rows)
+    toks = gen.randint(seed, 900, int(off[-1]), shape.vocab)
+    g_logits, st = gm.verify(contexts, toks, off)
+    assert np.all(st == 0)
+    o_logits, _ = OF.verify_block(om, oc, contexts, toks, off)
+    err = row_rel_err(g_logits, o_logits)
+    note(f"  {shape.name}: contexts {list(contexts)} rows {list(rows)}: max row rel err {err.max():.2e}")
+    assert err.max() <= tol
+    # the K/V the GPU appended match the oracle's block entries
+    kvv_np = kvv.float().cpu().numpy()
+    for b in range(B):
+        if rows[b] == 0:
+            continue
+        for l in range(shape.n_layers):
+            gk = kvv_np[l, 0, b, :, contexts[b]:contexts[b] + rows[b]]
+            ok = oc.k[l][b, :, contexts[b]:contexts[b] + rows[b]]
+            assert np.abs(gk - ok).max() <= tol * max(np.abs(ok).max(), 1e-6) * 4
+    # greedy decisions agree wherever the oracle's margin clears the error
+    abs_err = np.abs(g_logits - o_logits).max()
+    am_g, am_o = g_logits.argmax(axis=1), o_logits.argmax(axis=1)
+    decided = [r for r in range(len(o_logits)) if top2_margin(o_logits[r]) > 2 * abs_err]
+    assert all(am_g[r] == am_o[r] for r in decided)
+    note(f"    argmax equal on {len(decided)}/{len(o_logits)} decided rows")
+    return gm, g_logits, o_logits
+
+
+def test_bf16_gqa_hd64_ragged():
+    _bf16_case(configs.TINY_BF16, 11, [200, 77, 1, 130], [17, 5, 1, 33])
+
+
+def test_bf16_hd128_ragged():
+    _bf16_case(configs.SMALL_BF16, 12, [129, 300], [17, 9])
+
+
+def test_bf16_single_row_and_empty_sequence():
+    _bf16_case(configs.TINY_BF16, 13, [64, 63], [1, 0])
+
+
+def test_llama8b_width_two_layers():
+    shape = configs.LLAMA3_8B.with_layers(2)
+    note("llama3-8b width, 2 layers: generating weights")
+    _bf16_case(shape, 2, [2048], [17])

@@ -1,0 +1,103 @@
+"""GPU length selector vs the oracle, bit for bit (binary64, no fused multiply-add)."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import selector as S
+from paper_2608_08721_amd import lsv
+from tests.lsv_testing import note
+
+pytestmark = pytest.mark.gpu
+
+
+def gpu_select(mode, conf, cost, d_init, d_max, alpha, n, flags):
+    B, G = conf.shape
+    c = torch.tensor(conf, dtype=torch.float32, device="cuda")
+    co = torch.tensor(cost, dtype=torch.float64, device="cuda") if cost is not None else None
+    g = torch.full((B,), -7, dtype=torch.int32, device="cuda")
+    aux = torch.full((B,), -7, dtype=torch.int32, device="cuda")
+    st = torch.full((B,), 99, dtype=torch.int32, device="cuda")
+    lsv.lsv_select_length(mode, B, G, c, co, d_init, d_max, alpha, n, flags, g, aux, st)
+    torch.cuda.synchronize()
+    return g.cpu().numpy(), aux.cpu().numpy(), st.cpu().numpy()
+
+
+def random_conf(rng, B, G):
+    kind = rng.integers(5)
+    if kind == 0:
+        x = rng.random((B, G))
+    elif kind == 1:
+        x = rng.beta(8, 2, (B, G)) * 0.92 ** np.arange(1, G + 1)
+    elif kind == 2:
+        x = np.round(rng.random((B, G)), 1)          # exact ties
+    elif kind == 3:
+        x = rng.choice([0.0, 1.0, 0.5, 0.9], size=(B, G))
+    else:
+        x = 1.0 - rng.random((B, G)) ** 6
+    return x.astype(np.float32)
+
+
+def random_cost(rng, G):
+    kind = rng.integers(4)
+    d = np.arange(G + 1, dtype=np.float64)
+    if kind == 0:
+        c = rng.random() * 2 + 0.01 + (rng.random() * 0.2) * d
+    elif kind == 1:
+        c = np.concatenate([[0.0], np.cumsum(np.sort(rng.random(G)) + 1e-3)]) + rng.random()
+    elif kind == 2:   # tile-step table
+        c = 1.0 + 0.02 * d + 0.5 * (d > rng.integers(1, G + 1))
+    else:
+        c = rng.random(G + 1) + 0.05
+    c[0] = 0.0
+    return c
+
+
+def test_selector_parity_random():
+    rng = np.random.default_rng(123)
+    n_cases = 0
+    for trial in range(90):
+        G = int(rng.choice([1, 2, 3, 7, 16, 32, 64]))
+        B = 64
+        conf = random_conf(rng, B, G)
+        cost = random_cost(rng, G)
+        for mode in (S.SEL_MARGINAL, S.SEL_EXHAUSTIVE, S.SEL_ALG1):
+            flags = int(rng.integers(2)) if mode != S.SEL_ALG1 else 0
+            d_max = int(rng.integers(1, G + 1))
+            d_init = int(rng.integers(1, G + 1))
+            alpha = float(rng.choice([1.8, 2.0, 2.2, 0.5, 3.7]))
+            n = int(rng.integers(1, G + 1))
+            g, aux, st = gpu_select(mode, conf, cost if mode != S.SEL_ALG1 else None, d_init, d_max, alpha, n, flags)
+            want_g, want_a = S.select_batch(mode, conf, list(cost), d_init, d_max, alpha, n, flags)
+            assert np.all(st == 0)
+            assert list(g) == want_g, (trial, mode)
+            assert list(aux) == want_a, (trial, mode)
+            n_cases += B
+    note(f"selector parity: {n_cases} sequences bit-exact")
+
+
+def test_selector_rejects_bad_confidence_and_cost():
+    conf = np.full((3, 8), 0.5, np.float32)
+    conf[1, 3] = np.nan
+    conf[2, 0] = 1.5
+    cost = np.linspace(0, 1.4, 9)
+    g, aux, st = gpu_select(S.SEL_EXHAUSTIVE, conf, cost, 1, 8, 2.0, 4, 0)
+    assert list(st) == [0, lsv.LSV_ERR_INVALID_ARG, lsv.LSV_ERR_INVALID_ARG]
+    assert g[1] == 0 and g[2] == 0 and g[0] == S.select_exhaustive([0.5] * 8, list(cost), 8)
+    bad = cost.copy()
+    bad[5] = -1.0
+    g, aux, st = gpu_select(S.SEL_MARGINAL, conf[:1], bad, 1, 8, 2.0, 4, 0)
+    assert st[0] == lsv.LSV_ERR_INVALID_ARG
+    g, aux, st = gpu_select(S.SEL_MARGINAL, conf[:1], bad, 1, 4, 2.0, 4, 0)  # cost[5] beyond d_max: unused
+    assert st[0] == 0
+
+
+def test_selector_paper_hyperparameters():
+    """The paper's settings: alpha 2.0 with d_max 60 and initial length 10, alpha 2.2 with d_max 24 and block 16
+    (Sec. 4, implementation details)."""
+    rng = np.random.default_rng(7)
+    for alpha, d_max, n in ((2.0, 60, 10), (2.2, 24, 16)):
+        G = 64 if d_max > 32 else 32
+        conf = (rng.beta(8, 2, (64, G)) * 0.97 ** np.arange(1, G + 1)).astype(np.float32)
+        g, aux, st = gpu_select(S.SEL_ALG1, conf, None, 1, d_max, alpha, n, 0)
+        want = S.select_batch(S.SEL_ALG1, conf, None, 1, d_max, alpha, n)
+        assert list(g) == want[0] and list(aux) == want[1]
