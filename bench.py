@@ -1,0 +1,322 @@
+#!/usr/bin/env python3
+"""Benchmark of the LibraSpec verification step on one MI355X.
+
+One step = the whole hot path on one batch:
+  lsv_select_length (MARGINAL rule on the measured per-gamma cost table)
+  -> lsv_verify_block (target forward over [root, x_1..x_gamma] against the KV cache)
+  -> lsv_accept (greedy; commits the cached length),
+captured once as a HIP graph and replayed.  Inputs are resident in HBM before the
+timed region.  Default workload: Llama-3-8B-shaped random-init bf16 decoder (32
+layers, d 4096, 32/8 x 128 heads, SwiGLU 14336, vocab 128256), batch 1, context
+2048 prefilled from seeded random prompt ids, 16 drafted ids with confidences
+Beta(8, 2) * 0.92^i.
+
+Prints one JSON line (rank 0).  `value` = verified tokens per second
+(batch * (gamma + 1) / step time); the per-gamma latency sweep is in `sweep`.
+"""
+import argparse
+import ctypes
+import json
+import os
+import statistics
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "verify-step latency (us) & tokens/s vs gamma; % of HBM BW / MFMA bf16 peak"
+HBM_PEAK_GBPS = 8000.0
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=100)
+    p.add_argument("--warmup", type=int, default=10)
+    p.add_argument("--workload", default="llama3-8b-b1-c2048")
+    p.add_argument("--sweep-reps", type=int, default=20)
+    p.add_argument("--roofline-steps", type=int, default=5)
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--calib-copy", action="store_true",
+                   help="also run one plain 256 MiB copy kernel (counter calibration for --pmc runs)")
+    return p.parse_args()
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+class HipEvents:
+    """Raw hipEvent_t handles from the process's HIP runtime (for the timing hook)."""
+
+    def __init__(self, n):
+        from paper_2608_08721_amd import lsv
+        self.hip = lsv.hip_runtime()
+        self.ev = []
+        for _ in range(n):
+            e = ctypes.c_void_p()
+            assert self.hip.hipEventCreate(ctypes.byref(e)) == 0
+            self.ev.append(e.value)
+
+    def elapsed_ms(self, a, b):
+        ms = ctypes.c_float()
+        rc = self.hip.hipEventElapsedTime(ctypes.byref(ms), ctypes.c_void_p(self.ev[a]), ctypes.c_void_p(self.ev[b]))
+        assert rc == 0, rc
+        return ms.value
+
+
+def gateup_bytes(m, rows):
+    """Algorithmic HBM bytes of one gate/up launch: the packed gate and up weights once, the
+    storage-type activation rows and their norm statistics in, the SwiGLU output out."""
+    es = 2 if m.dtype == "bf16" else 4
+    return 2 * m.d_ff * m.d_model * es + rows * m.d_model * es + rows * (m.d_model // 64) * 4 + rows * m.d_ff * es
+
+
+def step_bytes(m, contexts, rows):
+    es = 2 if m.dtype == "bf16" else 4
+    kv_row = 2 * m.n_kv_heads * m.head_dim * es
+    return m.matmul_params() * es + m.n_layers * (sum(contexts) + rows) * kv_row
+
+
+def step_flops(m, contexts, rows_per_seq):
+    M = sum(rows_per_seq)
+    att = 0
+    for C, r in zip(contexts, rows_per_seq):
+        att += sum(4 * m.n_q_heads * m.head_dim * (C + v + 1) for v in range(r))
+    return 2 * M * m.matmul_params() + m.n_layers * att
+
+
+def cpu_baseline(m, seed, C, rows, tokens, gamma):
+    """The oracle (fp64 numpy) on a bounded sample of the same workload: one verify of the
+    block at full width with 1 and then 2 layers (+ embedding and LM head), context from the
+    seeded KV generator; the per-layer time is extrapolated to all layers."""
+    from threadpoolctl import threadpool_info
+
+    from oracle import forward as OF
+    from synth import gen
+    ws = {"embed": gen.embed_weights(m, seed), "final_norm": gen.final_norm_weights(m),
+          "lm_head": gen.lm_head_weights(m, seed), "layers": [gen.layer_weights(m, seed, l) for l in range(2)]}
+    times = []
+    for L in (1, 2):
+        shape = m.with_layers(L)
+        cache = OF.KVCache(shape, 1, C + rows)
+        for l in range(L):
+            k, v = gen.synthetic_kv(shape, seed, l, 1, C)
+            cache.k[l][0, :, :C] = OF.stored_to_f64(k[0], m.dtype)
+            cache.v[l][0, :, :C] = OF.stored_to_f64(v[0], m.dtype)
+        model = OF.Model(shape, {**ws, "layers": ws["layers"][:L]})
+        t0 = time.perf_counter()
+        OF.verify_block(model, cache, [C], tokens[:rows], [0, rows])
+        times.append(time.perf_counter() - t0)
+    per_layer = max(times[1] - times[0], 1e-9)
+    fixed = max(times[0] - per_layer, 0.0)
+    t_step = fixed + m.n_layers * per_layer
+    threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    return {"value": rows / t_step, "unit": "verified tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"fp64 numpy oracle, one verify of {rows} rows (gamma {gamma}) at {m.name} width with 1 and 2 "
+                      f"of {m.n_layers} layers + embedding + LM head, context {C} (seeded KV); "
+                      f"{times[0]:.1f} s + {times[1]:.1f} s measured, per-layer time extrapolated to "
+                      f"{m.n_layers} layers; host cpu_count {os.cpu_count()}",
+            "seconds_per_step": t_step}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only: this build has no multi-GPU path (asked for --gpus {args.gpus}).",
+              file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    from paper_2608_08721_amd import lsv, runtime
+    from synth import configs, gen
+
+    wl = configs.WORKLOADS[args.workload]
+    m = wl.model
+    if wl.batch != 1 or wl.accept != "greedy":
+        raise SystemExit("bench.py times the batch-1 greedy workloads")
+    torch.cuda.set_device(0)
+    dev = "cuda"
+    i32 = lambda x: torch.tensor(np.asarray(x, dtype=np.int32), device=dev)
+    seed, B, G = wl.seed, wl.batch, wl.G
+    C = int(gen.contexts(wl)[0])
+    rows_max = G + 1
+    cap = C + rows_max
+    cfg = runtime.model_config(m)
+
+    # ---- model: seeded weights, generated and packed one layer at a time (untimed)
+    t0 = time.time()
+    dm = runtime.DeviceModel(cfg, dev)
+    dm.pack_globals(gen.embed_weights(m, seed), gen.final_norm_weights(m), gen.lm_head_weights(m, seed))
+    for l in range(m.n_layers):
+        dm.pack_layer(l, gen.layer_weights(m, seed, l))
+        if l % 8 == 7:
+            log(f"packed layer {l + 1}/{m.n_layers} ({time.time() - t0:.1f} s)")
+    kv = runtime.KVCache(cfg, B, cap, dev)
+    ws = runtime.Workspace(lsv.lsv_verify_workspace_bytes(cfg, B, 64, cap), dev)
+    aws = runtime.Workspace(lsv.lsv_accept_workspace_bytes(B, 64, m.vocab), dev)
+    logits = torch.zeros((64, m.vocab), dtype=torch.float32, device=dev)
+    status = torch.zeros(B, dtype=torch.int32, device=dev)
+
+    # ---- prefill the context from seeded prompt ids (chunks of 64 rows, untimed)
+    prompt = gen.prefix_ids(seed, B, [C], m.vocab)[0]
+    for s in range(0, C, 64):
+        chunk = prompt[s:s + 64]
+        lsv.lsv_verify_block(cfg, dm.buf, kv.buf, cap, B, i32([s]), i32(chunk), i32([0, len(chunk)]), 64, cap,
+                             logits, status, ws.buf, ws.nbytes)
+    last = len(prompt) - 64 * ((len(prompt) - 1) // 64) - 1
+    acc = torch.zeros(B, dtype=torch.int32, device=dev)
+    out = torch.zeros((B, rows_max), dtype=torch.int32, device=dev)
+    # root = greedy token after the prompt, chosen by the library's own acceptance on one row
+    lsv.lsv_accept(lsv.LSV_ACC_GREEDY, 1, m.vocab, logits[last:last + 1], i32([0, 1]), 1, rows_max,
+                   i32([prompt[-1]]), None, 0.0, 0, 0, acc, out, None, status, aws.buf, aws.nbytes)
+    torch.cuda.synchronize()
+    assert int(status.item()) == 0
+    root = int(out[0, 0].item())
+    log(f"model + prefill of {C} tokens ready ({time.time() - t0:.1f} s); root token {root}")
+
+    drafts = gen.draft_ids(seed, B, G, m.vocab)[0]
+    tokens = i32([root] + list(drafts))
+    conf_np = gen.confidences(wl)
+    conf = torch.tensor(conf_np, device=dev)
+    seq_base = i32([C])
+    seq_work = i32([C])
+    stream = torch.cuda.current_stream()
+
+    # ---- per-gamma latency sweep (graph of verify + accept per gamma): the measured cost table
+    sweep = {}
+    for g in range(1, G + 1):
+        ro = i32([0, g + 1])
+
+        def body():
+            seq_work.copy_(seq_base)
+            lsv.lsv_verify_block(cfg, dm.buf, kv.buf, cap, B, seq_base, tokens, ro, rows_max, cap, logits, status,
+                                 ws.buf, ws.nbytes)
+            lsv.lsv_accept(lsv.LSV_ACC_GREEDY, B, m.vocab, logits, ro, rows_max, rows_max, tokens, None, 0.0, 0, 0,
+                           acc, out, seq_work, status, aws.buf, aws.nbytes)
+        body()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            body()
+        for _ in range(3):
+            graph.replay()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.sweep_reps + 1)]
+        ev[0].record()
+        for r in range(args.sweep_reps):
+            graph.replay()
+            ev[r + 1].record()
+        torch.cuda.synchronize()
+        lat = [ev[r].elapsed_time(ev[r + 1]) for r in range(args.sweep_reps)]
+        sweep[g] = statistics.median(lat)
+        del graph
+    cost = np.array([0.0] + [sweep[g] for g in range(1, G + 1)], dtype=np.float64)
+    log("sweep (us): " + " ".join(f"{g}:{sweep[g] * 1e3:.0f}" for g in range(1, G + 1)))
+
+    # ---- LibraSpec selection on the measured table (reported for all three rules)
+    cost_t = torch.tensor(cost, device=dev)
+    gamma = torch.zeros(B, dtype=torch.int32, device=dev)
+    aux = torch.zeros(B, dtype=torch.int32, device=dev)
+    row_off = torch.zeros(B + 1, dtype=torch.int32, device=dev)
+    chosen = {}
+    for name, mode in (("exhaustive", lsv.LSV_SEL_EXHAUSTIVE), ("alg1", lsv.LSV_SEL_ALG1),
+                       ("marginal", lsv.LSV_SEL_MARGINAL)):
+        lsv.lsv_select_length(mode, B, G, conf, cost_t, 1, G, 2.2, 8, 0, gamma, aux, row_off, status)
+        torch.cuda.synchronize()
+        chosen[name] = int(gamma[0].item())
+    g_star = chosen["marginal"]
+    log(f"chosen gamma: {chosen}")
+
+    # ---- the timed step: select -> verify -> accept, one graph, dominant kernel bracketed by events
+    n_slots = m.n_layers
+    hev = HipEvents(2 * n_slots)
+
+    def step():
+        seq_work.copy_(seq_base)
+        lsv.lsv_select_length(lsv.LSV_SEL_MARGINAL, B, G, conf, cost_t, 1, G, 2.2, 8, 0, gamma, aux, row_off, status)
+        lsv.lsv_verify_block(cfg, dm.buf, kv.buf, cap, B, seq_base, tokens, row_off, rows_max, cap, logits, status,
+                             ws.buf, ws.nbytes)
+        lsv.lsv_accept(lsv.LSV_ACC_GREEDY, B, m.vocab, logits, row_off, rows_max, rows_max, tokens, None, 0.0, 0, 0,
+                       acc, out, seq_work, status, aws.buf, aws.nbytes)
+    step()
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        step()
+    for _ in range(args.warmup):
+        graph.replay()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t_wall = time.perf_counter()
+    e0.record()
+    for _ in range(args.steps):
+        graph.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter() - t_wall
+    ms_step = e0.elapsed_time(e1) / args.steps
+    # dominant kernel: the same steps launched eagerly with HIP events recorded around every
+    # gate/up launch on the step's stream (32 launches per step, several steps)
+    lsv.lsv_set_timing_events(lsv.LSV_KERNEL_GATEUP, hev.ev, n_slots, 0)
+    gateup_ms = []
+    for _ in range(args.roofline_steps):
+        step()
+        torch.cuda.synchronize()
+        gateup_ms += [hev.elapsed_ms(2 * i, 2 * i + 1) for i in range(n_slots)]
+    lsv.lsv_set_timing_events(lsv.LSV_KERNEL_GATEUP, [], 0, 0)
+    assert int(status.item()) == 0 and int(gamma.item()) == g_star
+    a_len = int(acc.item())
+    rows = g_star + 1
+
+    avg_gu = statistics.mean(gateup_ms)
+    gu_bytes = gateup_bytes(m, rows)
+    achieved = gu_bytes / (avg_gu * 1e-3) / 1e9
+    sb = step_bytes(m, [C], rows)
+    sf = step_flops(m, [C], [rows])
+    if args.calib_copy:
+        x = torch.empty(256 << 20, dtype=torch.uint8, device=dev)
+        y = torch.empty_like(x)
+        y.copy_(x)
+        torch.cuda.synchronize()
+
+    # expected emitted tokens per step under the drafter-confidence model (Assumption 3.7)
+    P = np.cumprod(conf_np[0].astype(np.float64))
+    exp_tokens = B * (1.0 + P[:g_star].sum())
+    result = {
+        "metric": METRIC,
+        "value": B * rows / (ms_step * 1e-3),
+        "unit": "verified tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if m.dtype == "bf16" else "f32",
+        "data": "synthetic (seeded random-init weights, random prompt and draft ids)",
+        "config": {"workload": wl.name, "model_shape": m.name, "batch": B, "context": C, "drafted": G,
+                   "gamma": g_star, "selector": "marginal on measured cost", "accept": "greedy"},
+        "roofline": {"bound": "hbm", "kernel": "gemm gate/up + SwiGLU (one launch per layer)",
+                     "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBPS,
+                     "traffic": None, "bytes_per_launch": gu_bytes, "avg_launch_us": avg_gu * 1e3,
+                     "launches_timed": len(gateup_ms),
+                     "how": "HIP events around each gate/up launch in eagerly launched steps"},
+        "step": {"latency_us": ms_step * 1e3, "wall_ms_per_step": t_wall / args.steps * 1e3,
+                 "algorithmic_bytes": sb, "hbm_frac": sb / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBPS,
+                 "flops": sf, "mfma_frac": sf / (ms_step * 1e-3) / 2.5e15,
+                 "expected_tokens_per_s": exp_tokens / (ms_step * 1e-3),
+                 "realized_tokens_per_s": B * (a_len + 1) / (ms_step * 1e-3)},
+        "selection": chosen,
+        "sweep": {str(g): round(sweep[g] * 1e3, 2) for g in range(1, G + 1)},
+    }
+    if not args.no_cpu_baseline:
+        log("cpu baseline: timing the oracle on a bounded sample")
+        result["cpu_baseline"] = cpu_baseline(m, seed, C, rows, [root] + list(drafts), g_star)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

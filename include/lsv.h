@@ -218,6 +218,10 @@ int lsv_accept(int32_t mode, int32_t batch, int32_t vocab, const float* d_logits
  *            for d <= d_max (MARGINAL / EXHAUSTIVE; may be NULL for ALG1)
  *   flags    LSV_SEL_BONUS: count the always-emitted token in N(d)
  *   d_gamma  [batch] out; d_aux [batch] out (nullable)
+ *   d_row_offsets [batch+1] out (nullable; needs batch <= LSV_MAX_BATCH): the row layout of
+ *            the verify block that follows, row_offsets[0] = 0 and
+ *            row_offsets[b+1] = row_offsets[b] + gamma_b + 1 (root plus gamma_b drafts), so
+ *            select -> verify -> accept can run without a host round trip
  *   d_status [batch] out (nullable): LSV_OK, or LSV_ERR_INVALID_ARG when a confidence is
  *            outside [0, 1] or a needed cost is not finite and positive (then gamma = 0). */
 enum { LSV_SEL_MARGINAL = 0, LSV_SEL_EXHAUSTIVE = 1, LSV_SEL_ALG1 = 2 };
@@ -225,7 +229,29 @@ enum { LSV_SEL_BONUS = 1 };
 enum { LSV_MAX_G = 64 };
 int lsv_select_length(int32_t mode, int32_t batch, int32_t G, const float* d_conf, const double* d_cost,
                       int32_t d_init, int32_t d_max, double alpha, int32_t block_n, uint32_t flags,
-                      int32_t* d_gamma, int32_t* d_aux, int32_t* d_status, void* stream);
+                      int32_t* d_gamma, int32_t* d_aux, int32_t* d_row_offsets, int32_t* d_status,
+                      void* stream);
+
+/* ------------------------------------------------------------- measurement */
+/* Kernel classes of lsv_verify_block, one launch per layer each (LM head once). */
+enum {
+  LSV_KERNEL_QKV = 0,
+  LSV_KERNEL_O = 1,
+  LSV_KERNEL_GATEUP = 2,
+  LSV_KERNEL_DOWN = 3,
+  LSV_KERNEL_LMHEAD = 4,
+  LSV_KERNEL_ATTENTION = 5
+};
+/* While set (n_slots > 0), every lsv_verify_block records events[2i] just before
+ * and events[2i+1] just after the i-th launch of kernel class `kernel` in that call
+ * (i < n_slots), on the call's stream, with hipEventRecordWithFlags(record_flags):
+ * pass hipEventRecordExternal (1) while capturing a graph so the records become
+ * graph nodes, 0 otherwise.  `events` is a host array of 2 * n_slots hipEvent_t
+ * created by the caller with timing enabled; the array is copied.  n_slots = 0
+ * clears the hook.  Process-wide setting; set it while no other thread calls the
+ * library. */
+enum { LSV_MAX_TIMING_SLOTS = 256 };
+int lsv_set_timing_events(int32_t kernel, void* const* events, int32_t n_slots, uint32_t record_flags);
 
 #ifdef __cplusplus
 }

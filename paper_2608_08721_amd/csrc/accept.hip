@@ -94,7 +94,7 @@ __global__ void __launch_bounds__(256) row_scan_kernel(const float* __restrict__
                                                        int batch, int vocab, float temperature, RowPartial* out) {
   const int r = blockIdx.y, c = blockIdx.x, nc = gridDim.x;
   if (r >= row_offsets[batch]) return;
-  const float* row = logits + (size_t)r * vocab;
+  const auto* row = GL(logits) + (size_t)r * vocab;
   const int x0 = c * kAcceptChunk, x1 = min(vocab, x0 + kAcceptChunk);
   float best = -INFINITY;
   int bidx = 0x7fffffff, bad = 0;
@@ -275,8 +275,8 @@ __global__ void __launch_bounds__(256) accept_sample_race_kernel(
   double kr = INFINITY, kp = INFINITY;
   int ir = 0x7fffffff, ip = 0x7fffffff, bad = 0;
   if (d.status == LSV_OK) {
-    const float* row = logits + (size_t)d.row * vocab;
-    const float* qrow = d.residual ? q + (size_t)d.draft_row * vocab : nullptr;
+    const auto* row = GL(logits) + (size_t)d.row * vocab;
+    const auto* qrow = d.residual ? GL(q) + (size_t)d.draft_row * vocab : nullptr;
     const uint64_t c1 = (uint64_t)(uint32_t)(d.a) | ((uint64_t)b << 32);
     // each thread owns groups of 4 consecutive tokens (one Philox call each)
     for (int x4 = (x0 >> 2) + threadIdx.x; x4 < ((x1 + 3) >> 2); x4 += blockDim.x) {

@@ -22,7 +22,7 @@ template <int HD>
 __global__ void __launch_bounds__(256) attn_chunk_bf16_kernel(AttnArgs a) {
   const int c = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, g4 = lane >> 4, l16 = lane & 15;
-  const int r0 = a.row_offsets[b], rows = a.row_offsets[b + 1] - r0, C = a.seq_len[b];
+  const int r0 = GL(a.row_offsets)[b], rows = GL(a.row_offsets)[b + 1] - r0, C = GL(a.seq_len)[b];
   if (r0 < 0 || r0 + rows > a.M_max) return;  // rows beyond the host bound are never read
   const int group = a.nq / a.nkv;
   const int L = min(C + rows, a.ctx_limit);  // cached + block keys that exist
@@ -32,19 +32,19 @@ __global__ void __launch_bounds__(256) attn_chunk_bf16_kernel(AttnArgs a) {
   __shared__ __align__(16) bf16_t Ks[kCh][HD + 8];
   __shared__ __align__(16) bf16_t Vt[HD][kCh + 8];
   const size_t slab = ((size_t)b * a.nkv + kvh) * (size_t)a.capacity * HD;
-  const bf16_t* kbase = (const bf16_t*)a.k + slab;
-  const bf16_t* vbase = (const bf16_t*)a.v + slab;
+  const auto* kbase = GL((const bf16_t*)a.k) + slab;
+  const auto* vbase = GL((const bf16_t*)a.v) + slab;
   constexpr int C8 = HD / 8;  // 16-byte chunks per row
   for (int i = threadIdx.x; i < kCh * C8; i += blockDim.x) {
     const int key = i / C8, d8 = i % C8;
-    uint4 x = make_uint4(0, 0, 0, 0);
-    if (k0 + key < L) x = *(const uint4*)(kbase + (size_t)(k0 + key) * HD + d8 * 8);
-    *(uint4*)&Ks[key][d8 * 8] = x;
+    u32x4_t x = {0u, 0u, 0u, 0u};
+    if (k0 + key < L) x = *(const GLOBAL u32x4_t*)(kbase + (size_t)(k0 + key) * HD + d8 * 8);
+    *(u32x4_t*)&Ks[key][d8 * 8] = x;
   }
   for (int i = threadIdx.x; i < kCh * C8; i += blockDim.x) {
     const int key = i % kCh, d8 = i / kCh;
-    uint4 x = make_uint4(0, 0, 0, 0);
-    if (k0 + key < L) x = *(const uint4*)(vbase + (size_t)(k0 + key) * HD + d8 * 8);
+    u32x4_t x = {0u, 0u, 0u, 0u};
+    if (k0 + key < L) x = *(const GLOBAL u32x4_t*)(vbase + (size_t)(k0 + key) * HD + d8 * 8);
     const bf16_t* e = (const bf16_t*)&x;
 #pragma unroll
     for (int j = 0; j < 8; ++j) Vt[d8 * 8 + j][key] = e[j];
@@ -56,10 +56,13 @@ __global__ void __launch_bounds__(256) attn_chunk_bf16_kernel(AttnArgs a) {
     const int qv = qt * 16 + l16;
     const bool qvalid = qv < nqv;
     const int rr = qvalid ? qv / group : 0, head = kvh * group + (qvalid ? qv % group : 0);
-    const bf16_t* qp = (const bf16_t*)a.q + ((size_t)(r0 + rr) * a.nq + head) * HD + 8 * g4;
-    uint4 qf[HD / 32];
+    const auto* qp = GL((const bf16_t*)a.q) + ((size_t)(r0 + rr) * a.nq + head) * HD + 8 * g4;
+    u32x4_t qf[HD / 32];
 #pragma unroll
-    for (int ds = 0; ds < HD / 32; ++ds) qf[ds] = qvalid ? *(const uint4*)(qp + 32 * ds) : make_uint4(0, 0, 0, 0);
+    for (int ds = 0; ds < HD / 32; ++ds) {  // rr = 0 for invalid columns: the load stays in bounds
+      const u32x4_t t = *(const GLOBAL u32x4_t*)(qp + 32 * ds);
+      qf[ds] = qvalid ? t : u32x4_t{0u, 0u, 0u, 0u};
+    }
 
     f32x4_t s[4];
 #pragma unroll
@@ -67,7 +70,7 @@ __global__ void __launch_bounds__(256) attn_chunk_bf16_kernel(AttnArgs a) {
       s[kt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int ds = 0; ds < HD / 32; ++ds) {
-        const uint4 kf = *(const uint4*)&Ks[16 * kt + l16][32 * ds + 8 * g4];
+        const u32x4_t kf = *(const u32x4_t*)&Ks[16 * kt + l16][32 * ds + 8 * g4];
         s[kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, kf),
                                                         __builtin_bit_cast(bf16x8_t, qf[ds]), s[kt], 0, 0, 0);
       }
@@ -112,18 +115,18 @@ __global__ void __launch_bounds__(256) attn_chunk_bf16_kernel(AttnArgs a) {
       }
 #pragma unroll
       for (int dt = 0; dt < HD / 16; ++dt) {
-        const uint2 lo = *(const uint2*)&Vt[16 * dt + l16][32 * ks + 4 * g4];
-        const uint2 hi = *(const uint2*)&Vt[16 * dt + l16][32 * ks + 16 + 4 * g4];
-        const uint4 vf = make_uint4(lo.x, lo.y, hi.x, hi.y);
+        const u32x2_t lo = *(const u32x2_t*)&Vt[16 * dt + l16][32 * ks + 4 * g4];
+        const u32x2_t hi = *(const u32x2_t*)&Vt[16 * dt + l16][32 * ks + 16 + 4 * g4];
+        const u32x4_t vf = {lo[0], lo[1], hi[0], hi[1]};
         o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, vf), pb, o[dt], 0, 0, 0);
       }
     }
     if (qvalid) {
       const size_t base = ((size_t)c * a.M_max + (r0 + rr)) * a.nq + head;
-      float* op = a.o_part + base * HD;
+      auto* op = GL(a.o_part) + base * HD;
 #pragma unroll
-      for (int dt = 0; dt < HD / 16; ++dt) *(f32x4_t*)(op + 16 * dt + 4 * g4) = o[dt];
-      if (g4 == 0) *(float2*)(a.ml_part + base * 2) = make_float2(mx, sum);
+      for (int dt = 0; dt < HD / 16; ++dt) *(GLOBAL f32x4_t*)(op + 16 * dt + 4 * g4) = o[dt];
+      if (g4 == 0) *(GLOBAL f32x2_t*)(a.ml_part + base * 2) = f32x2_t{mx, sum};
     }
   }
 }
@@ -133,22 +136,27 @@ __global__ void __launch_bounds__(256) attn_chunk_bf16_kernel(AttnArgs a) {
 template <typename T>
 __global__ void attn_merge_kernel(AttnArgs a, int hd) {
   const int m = blockIdx.x, head = blockIdx.y, d = threadIdx.x;
-  if (m >= a.row_offsets[a.batch] || m >= a.M_max) return;
+  if (m >= GL(a.row_offsets)[a.batch] || m >= a.M_max) return;
   const int b = seq_of_row(a.row_offsets, a.batch, m);
-  const int rows = a.row_offsets[b + 1] - a.row_offsets[b];
-  const int L = min(a.seq_len[b] + rows, a.ctx_limit);
+  const int rows = GL(a.row_offsets)[b + 1] - GL(a.row_offsets)[b];
+  const int L = min(GL(a.seq_len)[b] + rows, a.ctx_limit);
   const int n_used = (L + kCh - 1) / kCh;
+  const auto* ml = (const GLOBAL f32x2_t*)a.ml_part;
+  const auto* op = GL(a.o_part);
+  const size_t stride = (size_t)a.M_max * a.nq;  // between chunks, in (row, head) units
+  const size_t rh = (size_t)m * a.nq + head;
   float M = -INFINITY;
-  for (int c = 0; c < n_used; ++c) M = fmaxf(M, a.ml_part[(((size_t)c * a.M_max + m) * a.nq + head) * 2]);
+#pragma unroll 8
+  for (int c = 0; c < n_used; ++c) M = fmaxf(M, ml[c * stride + rh][0]);
   float num = 0.f, den = 0.f;
+#pragma unroll 8
   for (int c = 0; c < n_used; ++c) {
-    const size_t base = ((size_t)c * a.M_max + m) * a.nq + head;
-    const float2 ml = *(const float2*)(a.ml_part + base * 2);
-    const float w = ml.x == -INFINITY ? 0.f : exp2f(ml.x - M);
-    den += w * ml.y;
-    num += w * a.o_part[base * hd + d];
+    const f32x2_t v = ml[c * stride + rh];
+    const float w = v[0] == -INFINITY ? 0.f : exp2f(v[0] - M);
+    den += w * v[1];
+    num += w * op[(c * stride + rh) * hd + d];
   }
-  ((T*)a.out)[((size_t)m * a.nq + head) * hd + d] = from_f32<T>(num / den);
+  GL((T*)a.out)[rh * hd + d] = from_f32<T>(num / den);
 }
 
 // fp32 path: one wave per (row, query head); scores in LDS.

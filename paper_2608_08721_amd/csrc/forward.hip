@@ -3,12 +3,12 @@
 // drafted positions).
 //
 // Per layer, five launches (+1 attention merge for bf16):
-//   QKV GEMM   : RMSNorm prologue, RoPE + K/V cache append epilogue
+//   QKV GEMM   : 1/rms row scaling, RoPE, K/V cache append
 //   attention  : split-context chunks (+ merge)
-//   O GEMM     : residual add + per-row sum-of-squares partials for the next norm
-//   gate/up    : RMSNorm prologue, SwiGLU epilogue
-//   down GEMM  : residual add + sum-of-squares partials
-// then the LM head (final RMSNorm prologue) writes fp32 logits.
+//   O GEMM     : residual add, storage-type copy of h, row sum-of-squares partials
+//   gate/up    : 1/rms row scaling, SwiGLU
+//   down GEMM  : residual add, storage-type copy of h, sum-of-squares partials
+// then the LM head (1/rms row scaling) writes fp32 logits.
 #include "lsv_attn.h"
 #include "lsv_device.h"
 #include "lsv_gemm.h"
@@ -50,15 +50,9 @@ ModelLayout model_layout(const Shape& s) {
   size_t off = 0;
   m.embed = off;
   off = al256(off + (size_t)s.V * s.d * s.es);
-  m.final_norm = off;
-  off = al256(off + (size_t)s.d * s.es);
   m.lm_head = packed(off, s.V, s.d, KT);
   m.layer_base = off;
   size_t lo = 0;
-  m.attn_norm = lo;
-  lo = al256(lo + (size_t)s.d * s.es);
-  m.ffn_norm = lo;
-  lo = al256(lo + (size_t)s.d * s.es);
   m.qkv = packed(lo, (s.nq + 2 * s.nkv) * s.hd, s.d, KT);
   m.o = packed(lo, s.d, s.nq * s.hd, KT);
   m.gateup = packed(lo, 2 * s.F, s.d, KT, 2 * ((s.F + 15) / 16));
@@ -70,19 +64,23 @@ ModelLayout model_layout(const Shape& s) {
 
 // ------------------------------------------------------------------ workspace
 struct VerifyWs {
-  float* h;        // [M_max][d]
-  float* stats;    // [d/64][M_max]
+  float* h;        // [M_max][d] fp32 residual stream
+  void* hx;        // [M_max][d] storage-type copy of h (bf16 models; fp32 models read h)
+  float* stats;    // [d/64][M_max] per-64-column sums of squares of h
   void* q;         // [M_max][nq][hd]
   void* attn;      // [M_max][nq][hd]
-  void* u;         // [M_max][F]
+  void* u;         // [M_max][ldu], columns >= d_ff stay zero
   float* part;     // split-K partials
   float* o_part;   // attention chunk partials
   float* ml_part;
   int* counters;
+  int ldu;
   size_t total;
 };
 
-static constexpr int kWantWgs = 512, kMaxSplits = 32;
+// Target about two workgroups of four waves per compute unit per launch, and at least
+// 16 fragments (16 KiB of weights) per wave so the per-wave pipeline amortises.
+static constexpr int kWantWgs = 640, kMinFragsPerWave = 16;
 
 struct VerifyPlan {
   int MT, n_chunks;
@@ -95,13 +93,12 @@ static VerifyPlan plan_verify(const Shape& s, const ModelLayout& ml, int max_row
   VerifyPlan v;
   v.MT = (max_rows + 15) / 16;
   v.n_chunks = (max_ctx + kAttnChunk - 1) / kAttnChunk;
-  const int KT = s.dtype == LSV_DTYPE_BF16 ? 32 : 16;
   const PackedMat* mats[5] = {&ml.qkv, &ml.o, &ml.gateup, &ml.down, &ml.lm_head};
   v.part_floats = 0;
   v.max_groups = 1;
   for (int k = 0; k < 5; ++k) {
     const GemmKind kind = (GemmKind)k;
-    v.g[k] = plan_gemm(mats[k]->Nt, mats[k]->Kt, KT, s.es, v.MT, gemm_tpw(kind), kWantWgs, kMaxSplits);
+    v.g[k] = plan_gemm(mats[k]->Nt, mats[k]->Kt, gemm_tpw(kind), kWantWgs, kMinFragsPerWave);
     if (v.g[k].S > 1) {
       size_t pf = (size_t)v.g[k].S * max_rows * mats[k]->Nt * 16;
       v.part_floats = pf > v.part_floats ? pf : v.part_floats;
@@ -111,7 +108,7 @@ static VerifyPlan plan_verify(const Shape& s, const ModelLayout& ml, int max_row
   return v;
 }
 
-static VerifyWs carve_verify(const Shape& s, const VerifyPlan& v, int max_rows, void* base) {
+static VerifyWs carve_verify(const Shape& s, const ModelLayout& ml, const VerifyPlan& v, int max_rows, void* base) {
   VerifyWs w;
   char* p = (char*)base;
   size_t off = 0;
@@ -120,11 +117,14 @@ static VerifyWs carve_verify(const Shape& s, const VerifyPlan& v, int max_rows, 
     off = al256(off + bytes);
     return (void*)r;
   };
+  const int KT = s.dtype == LSV_DTYPE_BF16 ? 32 : 16;
+  w.ldu = ml.down.Kt * KT;  // the down projection reads whole fragments of u
   w.h = (float*)take(sizeof(float) * (size_t)max_rows * s.d);
+  w.hx = s.dtype == LSV_DTYPE_BF16 ? take((size_t)s.es * max_rows * s.d) : (void*)w.h;
   w.stats = (float*)take(sizeof(float) * (size_t)(s.d / 64) * max_rows);
   w.q = take((size_t)s.es * max_rows * s.nq * s.hd);
   w.attn = take((size_t)s.es * max_rows * s.nq * s.hd);
-  w.u = take((size_t)s.es * max_rows * s.F);
+  w.u = take((size_t)s.es * max_rows * w.ldu);
   w.part = (float*)take(sizeof(float) * v.part_floats);
   if (s.dtype == LSV_DTYPE_BF16) {
     w.o_part = (float*)take(sizeof(float) * (size_t)v.n_chunks * max_rows * s.nq * s.hd);
@@ -141,7 +141,7 @@ size_t verify_workspace_bytes(const Shape& s, int batch, int max_rows, int max_c
   (void)batch;
   ModelLayout ml = model_layout(s);
   VerifyPlan v = plan_verify(s, ml, max_rows, max_ctx);
-  return carve_verify(s, v, max_rows, nullptr).total;
+  return carve_verify(s, ml, v, max_rows, nullptr).total;
 }
 
 // ------------------------------------------------------------------ embedding
@@ -151,7 +151,7 @@ size_t verify_workspace_bytes(const Shape& s, int batch, int max_rows, int max_c
 template <typename T>
 __global__ void __launch_bounds__(256) embed_kernel(const T* __restrict__ E, int V, int d, const int32_t* tokens,
                                                     const int32_t* row_offsets, const int32_t* seq_len, int batch,
-                                                    int ctx_limit, int M_max, float* h, float* stats,
+                                                    int ctx_limit, int M_max, float* h, T* hx, float* stats,
                                                     int32_t* status) {
   const int m = blockIdx.x;
   if (m == 0 && status) {
@@ -168,18 +168,23 @@ __global__ void __launch_bounds__(256) embed_kernel(const T* __restrict__ E, int
       status[b] = st;
     }
   }
-  if (m >= row_offsets[batch] || m >= M_max) return;
-  const int tok = tokens[m];
-  const bool ok = tok >= 0 && tok < V;
+  if (m >= GL(row_offsets)[batch] || m >= M_max) return;
+  const int tok_in = GL(tokens)[m];
+  const bool ok = tok_in >= 0 && tok_in < V;
+  const int tok = ok ? tok_in : 0;  // invalid ids read row 0 and are zeroed below
   for (int p = threadIdx.x; p < d / 64; p += blockDim.x) {
     float ss = 0.f;
+#pragma unroll 8
     for (int j = 0; j < 64; ++j) {
       const int k = 64 * p + j;
-      const float x = ok ? to_f32<T>(E[(size_t)tok * d + k]) : 0.f;
-      h[(size_t)m * d + k] = x;
+      const T ld = GL(E)[(size_t)tok * d + k];
+      const T e = ok ? ld : from_f32<T>(0.f);
+      const float x = to_f32<T>(e);
+      GL(h)[(size_t)m * d + k] = x;
+      if (hx) GL(hx)[(size_t)m * d + k] = e;
       ss += x * x;
     }
-    stats[(size_t)p * M_max + m] = ss;
+    GL(stats)[(size_t)p * M_max + m] = ss;
   }
 }
 
@@ -187,17 +192,18 @@ int launch_verify(const Shape& s, const ModelLayout& ml, const void* packed, voi
                   const int32_t* seq_len, const int32_t* tokens, const int32_t* row_offsets, int max_rows,
                   int max_ctx, float* logits, int32_t* status, void* ws, size_t ws_bytes, hipStream_t st) {
   const VerifyPlan v = plan_verify(s, ml, max_rows, max_ctx);
-  const VerifyWs w = carve_verify(s, v, max_rows, ws);
+  const VerifyWs w = carve_verify(s, ml, v, max_rows, ws);
   if (w.total > ws_bytes) return LSV_ERR_INVALID_ARG;
   const char* P = (const char*)packed;
-  const int P64 = s.d / 64;
+  const bool bf16 = s.dtype == LSV_DTYPE_BF16;
 
-  if (s.dtype == LSV_DTYPE_BF16)
+  if (bf16)
     hipLaunchKernelGGL(embed_kernel<bf16_t>, dim3(max_rows), dim3(256), 0, st, (const bf16_t*)(P + ml.embed), s.V,
-                       s.d, tokens, row_offsets, seq_len, batch, max_ctx, max_rows, w.h, w.stats, status);
+                       s.d, tokens, row_offsets, seq_len, batch, max_ctx, max_rows, w.h, (bf16_t*)w.hx, w.stats,
+                       status);
   else
     hipLaunchKernelGGL(embed_kernel<float>, dim3(max_rows), dim3(256), 0, st, (const float*)(P + ml.embed), s.V, s.d,
-                       tokens, row_offsets, seq_len, batch, max_ctx, max_rows, w.h, w.stats, status);
+                       tokens, row_offsets, seq_len, batch, max_ctx, max_rows, w.h, (float*)nullptr, w.stats, status);
   if (hipGetLastError() != hipSuccess) return LSV_ERR_HIP;
 
   GemmArgs base = {};
@@ -205,7 +211,7 @@ int launch_verify(const Shape& s, const ModelLayout& ml, const void* packed, voi
   base.batch = batch;
   base.row_offsets = row_offsets;
   base.stats = w.stats;
-  base.P = P64;
+  base.P = s.d / 64;
   base.eps = s.eps;
   base.part = w.part;
   base.counters = w.counters;
@@ -215,8 +221,9 @@ int launch_verify(const Shape& s, const ModelLayout& ml, const void* packed, voi
   base.nq = s.nq;
   base.nkv = s.nkv;
   base.hd = s.hd;
-  base.rope_base = s.rope_base;
+  base.log2_rope_base = log2(s.rope_base);
   base.F = s.F;
+  base.ldu = w.ldu;
 
   auto gemm = [&](GemmKind kind, const PackedMat& pm, const char* layer_base, GemmArgs a) {
     const GemmPlan& p = v.g[kind];
@@ -226,20 +233,24 @@ int launch_verify(const Shape& s, const ModelLayout& ml, const void* packed, voi
     a.Nt = pm.Nt;
     a.Kt = pm.Kt;
     a.S = p.S;
-    a.kf_max = p.kf_max;
-    return launch_gemm(s.dtype, kind, v.MT, a, p, st);
+    const int idx = kind == GEMM_LMHEAD ? 0 : a.layer_index;
+    timing_before((int)kind, idx, st);
+    const int rc = launch_gemm(s.dtype, kind, v.MT, a, p, st);
+    timing_after((int)kind, idx, st);
+    return rc;
   };
 
   const size_t kv_layer_elems = (size_t)2 * batch * s.nkv * (size_t)capacity * s.hd;
   int rc;
   for (int l = 0; l < s.L; ++l) {
     const char* LB = P + ml.layer_base + (size_t)l * ml.layer_stride;
-    // QKV + RoPE + cache append
+    // QKV (normalised input) + RoPE + cache append
     GemmArgs a = base;
-    a.h = w.h;
-    a.gain = LB + ml.attn_norm;
-    a.q_out = w.q;
+    a.layer_index = l;
     a.layer = l;
+    a.x = w.hx;
+    a.ldx = s.d;
+    a.q_out = w.q;
     if ((rc = gemm(GEMM_QKV, ml.qkv, LB, a)) != LSV_OK) return rc;
     // attention
     AttnArgs at;
@@ -258,31 +269,38 @@ int launch_verify(const Shape& s, const ModelLayout& ml, const void* packed, voi
     at.ml_part = w.ml_part;
     at.out = w.attn;
     at.scale_log2 = (float)(1.4426950408889634 / sqrt((double)s.hd));
+    timing_before(LSV_KERNEL_ATTENTION, l, st);
     if ((rc = launch_attention(s.dtype, s.hd, at, max_rows, v.n_chunks, st)) != LSV_OK) return rc;
+    timing_after(LSV_KERNEL_ATTENTION, l, st);
     // O projection + residual
     a = base;
+    a.layer_index = l;
     a.x = w.attn;
     a.ldx = s.nq * s.hd;
     a.h_out = w.h;
+    a.hx_out = bf16 ? w.hx : nullptr;
     a.stats_out = w.stats;
     if ((rc = gemm(GEMM_O, ml.o, LB, a)) != LSV_OK) return rc;
-    // gate/up + SwiGLU
+    // gate/up (normalised input) + SwiGLU
     a = base;
-    a.h = w.h;
-    a.gain = LB + ml.ffn_norm;
+    a.layer_index = l;
+    a.x = w.hx;
+    a.ldx = s.d;
     a.u_out = w.u;
     if ((rc = gemm(GEMM_GATEUP, ml.gateup, LB, a)) != LSV_OK) return rc;
     // down + residual
     a = base;
+    a.layer_index = l;
     a.x = w.u;
-    a.ldx = s.F;
+    a.ldx = w.ldu;
     a.h_out = w.h;
+    a.hx_out = bf16 ? w.hx : nullptr;
     a.stats_out = w.stats;
     if ((rc = gemm(GEMM_DOWN, ml.down, LB, a)) != LSV_OK) return rc;
   }
   GemmArgs a = base;
-  a.h = w.h;
-  a.gain = P + ml.final_norm;
+  a.x = w.hx;
+  a.ldx = s.d;
   a.out_f32 = logits;
   a.ldo = s.V;
   return gemm(GEMM_LMHEAD, ml.lm_head, P, a);

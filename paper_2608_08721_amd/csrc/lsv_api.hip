@@ -12,6 +12,12 @@ namespace {
 
 thread_local char g_err[512] = "";
 
+struct TimingHook {
+  int kernel = 0, n = 0;
+  unsigned flags = 0;
+  hipEvent_t ev[2 * LSV_MAX_TIMING_SLOTS];
+} g_timing;
+
 int fail(int code, const char* fmt, ...) {
   va_list ap;
   va_start(ap, fmt);
@@ -24,6 +30,7 @@ int ok() {
   return LSV_OK;
 }
 int hip_rc(int rc, const char* what) {
+  if (rc == LSV_ERR_HIP && strncmp(g_err, "timing event", 12) == 0) return rc;
   if (rc == LSV_ERR_HIP) return fail(LSV_ERR_HIP, "%s: %s", what, hipGetErrorString(hipGetLastError()));
   if (rc == LSV_ERR_UNSUPPORTED) return fail(rc, "%s: unsupported shape", what);
   if (rc != LSV_OK) return fail(rc, "%s failed", what);
@@ -75,10 +82,10 @@ int lsv_pack_globals(const lsv_model_config* cfg, const void* d_embed, const voi
   const lsv::ModelLayout ml = lsv::model_layout(s);
   hipStream_t st = (hipStream_t)stream;
   char* P = (char*)d_packed;
-  if (hipMemcpyAsync(P + ml.embed, d_embed, (size_t)s.V * s.d * s.es, hipMemcpyDeviceToDevice, st) != hipSuccess ||
-      hipMemcpyAsync(P + ml.final_norm, d_final_norm, (size_t)s.d * s.es, hipMemcpyDeviceToDevice, st) != hipSuccess)
+  if (hipMemcpyAsync(P + ml.embed, d_embed, (size_t)s.V * s.d * s.es, hipMemcpyDeviceToDevice, st) != hipSuccess)
     return fail(LSV_ERR_HIP, "copy: %s", hipGetErrorString(hipGetLastError()));
-  return hip_rc(lsv::launch_pack(s, lsv::PACK_PLAIN, ml.lm_head, d_lm_head, nullptr, nullptr, P, st), "pack lm_head");
+  return hip_rc(lsv::launch_pack(s, lsv::PACK_PLAIN, ml.lm_head, d_lm_head, nullptr, nullptr, d_final_norm, P, st),
+                "pack lm_head");
 }
 
 int lsv_pack_layer(const lsv_model_config* cfg, int32_t layer, const void* d_wq, const void* d_wk, const void* d_wv,
@@ -93,13 +100,10 @@ int lsv_pack_layer(const lsv_model_config* cfg, int32_t layer, const void* d_wq,
   const lsv::ModelLayout ml = lsv::model_layout(s);
   hipStream_t st = (hipStream_t)stream;
   char* LB = (char*)d_packed + ml.layer_base + (size_t)layer * ml.layer_stride;
-  if (hipMemcpyAsync(LB + ml.attn_norm, d_attn_norm, (size_t)s.d * s.es, hipMemcpyDeviceToDevice, st) != hipSuccess ||
-      hipMemcpyAsync(LB + ml.ffn_norm, d_ffn_norm, (size_t)s.d * s.es, hipMemcpyDeviceToDevice, st) != hipSuccess)
-    return fail(LSV_ERR_HIP, "copy: %s", hipGetErrorString(hipGetLastError()));
-  if ((rc = lsv::launch_pack(s, lsv::PACK_QKV, ml.qkv, d_wq, d_wk, d_wv, LB, st)) ||
-      (rc = lsv::launch_pack(s, lsv::PACK_PLAIN, ml.o, d_wo, nullptr, nullptr, LB, st)) ||
-      (rc = lsv::launch_pack(s, lsv::PACK_GATEUP, ml.gateup, d_wg, d_wu, nullptr, LB, st)) ||
-      (rc = lsv::launch_pack(s, lsv::PACK_PLAIN, ml.down, d_wd, nullptr, nullptr, LB, st)))
+  if ((rc = lsv::launch_pack(s, lsv::PACK_QKV, ml.qkv, d_wq, d_wk, d_wv, d_attn_norm, LB, st)) ||
+      (rc = lsv::launch_pack(s, lsv::PACK_PLAIN, ml.o, d_wo, nullptr, nullptr, nullptr, LB, st)) ||
+      (rc = lsv::launch_pack(s, lsv::PACK_GATEUP, ml.gateup, d_wg, d_wu, nullptr, d_ffn_norm, LB, st)) ||
+      (rc = lsv::launch_pack(s, lsv::PACK_PLAIN, ml.down, d_wd, nullptr, nullptr, nullptr, LB, st)))
     return hip_rc(rc, "pack layer");
   return ok();
 }
@@ -182,13 +186,15 @@ int lsv_accept(int32_t mode, int32_t batch, int32_t vocab, const float* d_logits
 
 int lsv_select_length(int32_t mode, int32_t batch, int32_t G, const float* d_conf, const double* d_cost, int32_t d_init,
                       int32_t d_max, double alpha, int32_t block_n, uint32_t flags, int32_t* d_gamma, int32_t* d_aux,
-                      int32_t* d_status, void* stream) {
+                      int32_t* d_row_offsets, int32_t* d_status, void* stream) {
   if (mode != LSV_SEL_MARGINAL && mode != LSV_SEL_EXHAUSTIVE && mode != LSV_SEL_ALG1)
     return fail(LSV_ERR_INVALID_ARG, "bad selector mode %d", mode);
   if (batch < 1 || G < 1 || G > LSV_MAX_G) return fail(LSV_ERR_INVALID_ARG, "need batch >= 1 and 1 <= G <= %d", LSV_MAX_G);
   if (d_max < 1 || d_max > G) return fail(LSV_ERR_INVALID_ARG, "need 1 <= d_max (%d) <= G (%d)", d_max, G);
   if (!d_conf || !d_gamma) return fail(LSV_ERR_INVALID_ARG, "NULL pointer");
   if (flags & ~(uint32_t)LSV_SEL_BONUS) return fail(LSV_ERR_INVALID_ARG, "unknown flags");
+  if (d_row_offsets && batch > LSV_MAX_BATCH)
+    return fail(LSV_ERR_INVALID_ARG, "row offsets need batch <= %d", LSV_MAX_BATCH);
   if (mode == LSV_SEL_ALG1) {
     if (block_n < 1) return fail(LSV_ERR_INVALID_ARG, "block_n must be >= 1");
     if (!(alpha > 0.0) || !(alpha <= 1.0e6)) return fail(LSV_ERR_INVALID_ARG, "alpha must be in (0, 1e6]");
@@ -197,8 +203,35 @@ int lsv_select_length(int32_t mode, int32_t batch, int32_t G, const float* d_con
     if (mode == LSV_SEL_MARGINAL && d_init < 1) return fail(LSV_ERR_INVALID_ARG, "d_init must be >= 1");
   }
   int rc = lsv::launch_select(mode, batch, G, d_conf, d_cost, d_init, d_max, alpha, block_n, flags, d_gamma, d_aux,
-                              d_status, (hipStream_t)stream);
+                              d_row_offsets, d_status, (hipStream_t)stream);
   return hip_rc(rc, "select");
 }
 
+int lsv_set_timing_events(int32_t kernel, void* const* events, int32_t n_slots, uint32_t record_flags) {
+  if (kernel < LSV_KERNEL_QKV || kernel > LSV_KERNEL_ATTENTION) return fail(LSV_ERR_INVALID_ARG, "bad kernel class");
+  if (n_slots < 0 || n_slots > LSV_MAX_TIMING_SLOTS || (n_slots > 0 && !events))
+    return fail(LSV_ERR_INVALID_ARG, "n_slots must be in [0, %d] with a non-NULL event array", LSV_MAX_TIMING_SLOTS);
+  g_timing.kernel = kernel;
+  g_timing.n = n_slots;
+  g_timing.flags = record_flags;
+  for (int i = 0; i < 2 * n_slots; ++i) g_timing.ev[i] = (hipEvent_t)events[i];
+  return ok();
+}
+
 }  // extern "C"
+
+namespace lsv {
+// Events are recorded with the caller's flags (hipEventRecordExternal while capturing
+// a graph).  Failures are reported through the sticky error that the surrounding
+// launch checks.
+static void timing_record(hipEvent_t ev, hipStream_t st) {
+  const hipError_t e = hipEventRecordWithFlags(ev, st, g_timing.flags);
+  if (e != hipSuccess) fail(LSV_ERR_HIP, "timing event record (flags %u): %s", g_timing.flags, hipGetErrorString(e));
+}
+void timing_before(int kernel, int index, hipStream_t st) {
+  if (g_timing.n > 0 && kernel == g_timing.kernel && index < g_timing.n) timing_record(g_timing.ev[2 * index], st);
+}
+void timing_after(int kernel, int index, hipStream_t st) {
+  if (g_timing.n > 0 && kernel == g_timing.kernel && index < g_timing.n) timing_record(g_timing.ev[2 * index + 1], st);
+}
+}  // namespace lsv

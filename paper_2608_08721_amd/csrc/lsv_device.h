@@ -3,11 +3,23 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
+// Global-memory view of a pointer.  Pointers reaching a kernel inside a struct are
+// generic; generic (flat) accesses also count against the LDS wait counter, which
+// forces full waits between the weight stream and LDS reads.  GL() makes every
+// global access a global_load / global_store.
+#define GL(p) ((__attribute__((address_space(1))) std::remove_reference_t<decltype(*(p))>*)(p))
+
 #define LSV_DEV __device__ __forceinline__
 
 typedef uint16_t bf16_t;  // storage type: IEEE bfloat16 bit pattern
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));  // 16-byte global / LDS accesses
+typedef unsigned int u32x2_t __attribute__((ext_vector_type(2)));
+#define GLOBAL __attribute__((address_space(1)))
 
 namespace lsv {
 
@@ -34,7 +46,7 @@ template <> LSV_DEV bf16_t from_f32<bf16_t>(float x) { return f2bf(x); }
 // Sequence that owns block row m (linear scan: batches are small).
 LSV_DEV int seq_of_row(const int32_t* row_offsets, int batch, int m) {
   int b = 0;
-  while (b + 1 < batch && row_offsets[b + 1] <= m) ++b;
+  while (b + 1 < batch && GL(row_offsets)[b + 1] <= m) ++b;
   return b;
 }
 

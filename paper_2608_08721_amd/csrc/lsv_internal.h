@@ -10,8 +10,12 @@ namespace lsv {
 
 // ---------------------------------------------------------------- selector
 int launch_select(int mode, int batch, int G, const float* conf, const double* cost, int d_init, int d_max,
-                  double alpha, int block_n, unsigned flags, int32_t* gamma, int32_t* aux, int32_t* status,
-                  hipStream_t stream);
+                  double alpha, int block_n, unsigned flags, int32_t* gamma, int32_t* aux, int32_t* row_offsets,
+                  int32_t* status, hipStream_t stream);
+
+// measurement hook (lsv_set_timing_events): called around each launch of a kernel class
+void timing_before(int kernel, int index, hipStream_t st);
+void timing_after(int kernel, int index, hipStream_t st);
 
 // ---------------------------------------------------------------- accept
 constexpr int kAcceptChunk = 4096;  // vocabulary entries per workgroup in the row scans
@@ -36,11 +40,12 @@ struct PackedMat {
   int N, K;       // logical rows (out features) and columns (in features)
   int Nt, Kt;     // fragment counts (zero-padded)
 };
+// RMSNorm gains are folded into the projection that follows them (QKV, gate/up,
+// LM head), so the packed model stores no separate gains.
 struct ModelLayout {
-  size_t embed, final_norm;  // raw row-major embedding [V, d], gain [d]
+  size_t embed;                     // raw row-major embedding [V, d]
   PackedMat lm_head;
   size_t layer_base, layer_stride;  // per-layer block
-  size_t attn_norm, ffn_norm;       // offsets inside a layer block
   PackedMat qkv, o, gateup, down;   // offsets inside a layer block
   size_t total;
 };
@@ -48,7 +53,7 @@ ModelLayout model_layout(const Shape& s);
 
 enum PackKind { PACK_PLAIN = 0, PACK_QKV = 1, PACK_GATEUP = 2 };
 int launch_pack(const Shape& s, PackKind kind, const PackedMat& pm, const void* src0, const void* src1,
-                const void* src2, void* dst, hipStream_t stream);
+                const void* src2, const void* gain, void* dst, hipStream_t stream);
 
 size_t verify_workspace_bytes(const Shape& s, int batch, int max_rows, int max_ctx);
 int launch_verify(const Shape& s, const ModelLayout& ml, const void* packed, void* kv, int capacity, int batch,

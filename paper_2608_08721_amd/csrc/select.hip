@@ -36,13 +36,9 @@ __device__ static int eps_star(const float* q, int d, double alpha) {
   return best;
 }
 
-__global__ void __launch_bounds__(64) select_length_kernel(int mode, int batch, int G, const float* __restrict__ conf,
-                                                           const double* __restrict__ cost, int d_init, int d_max,
-                                                           double alpha, int block_n, unsigned flags,
-                                                           int32_t* __restrict__ gamma, int32_t* __restrict__ aux,
-                                                           int32_t* __restrict__ status) {
-  int b = blockIdx.x * blockDim.x + threadIdx.x;
-  if (b >= batch) return;
+__device__ static int select_one(int mode, int G, const float* __restrict__ conf, const double* __restrict__ cost,
+                                 int d_init, int d_max, double alpha, int block_n, unsigned flags, int b,
+                                 int32_t* __restrict__ aux, int32_t* __restrict__ status) {
   float q[LSV_MAX_G];
   bool ok = true;
   for (int j = 0; j < G; ++j) {
@@ -95,17 +91,38 @@ __global__ void __launch_bounds__(64) select_length_kernel(int mode, int batch, 
       }
     }
   }
-  gamma[b] = d;
   if (aux) aux[b] = a;
   if (status) status[b] = ok ? LSV_OK : LSV_ERR_INVALID_ARG;
+  return d;
+}
+
+__global__ void __launch_bounds__(64) select_length_kernel(int mode, int batch, int G, const float* __restrict__ conf,
+                                                           const double* __restrict__ cost, int d_init, int d_max,
+                                                           double alpha, int block_n, unsigned flags,
+                                                           int32_t* __restrict__ gamma, int32_t* __restrict__ aux,
+                                                           int32_t* __restrict__ row_offsets,
+                                                           int32_t* __restrict__ status) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  int d = 0;
+  if (b < batch) d = select_one(mode, G, conf, cost, d_init, d_max, alpha, block_n, flags, b, aux, status);
+  if (b < batch) gamma[b] = d;
+  if (row_offsets) {  // single wave (batch <= 64): inclusive scan of gamma + 1
+    int v = b < batch ? d + 1 : 0;
+    for (int o = 1; o < 64; o <<= 1) {
+      const int t = __shfl_up(v, o, 64);
+      if ((threadIdx.x & 63) >= o) v += t;
+    }
+    if (b < batch) row_offsets[b + 1] = v;
+    if (b == 0) row_offsets[0] = 0;
+  }
 }
 
 int launch_select(int mode, int batch, int G, const float* conf, const double* cost, int d_init, int d_max,
-                  double alpha, int block_n, unsigned flags, int32_t* gamma, int32_t* aux, int32_t* status,
-                  hipStream_t stream) {
+                  double alpha, int block_n, unsigned flags, int32_t* gamma, int32_t* aux, int32_t* row_offsets,
+                  int32_t* status, hipStream_t stream) {
   dim3 grid((batch + 63) / 64);
   hipLaunchKernelGGL(select_length_kernel, grid, dim3(64), 0, stream, mode, batch, G, conf, cost, d_init, d_max,
-                     alpha, block_n, flags, gamma, aux, status);
+                     alpha, block_n, flags, gamma, aux, row_offsets, status);
   return hipGetLastError() == hipSuccess ? LSV_OK : LSV_ERR_HIP;
 }
 

@@ -21,8 +21,10 @@ LSV_SEL_BONUS = 1
 EXPORTED = (
     "lsv_status_string", "lsv_last_error", "lsv_abi_version", "lsv_packed_model_bytes", "lsv_pack_globals",
     "lsv_pack_layer", "lsv_kv_cache_bytes", "lsv_verify_workspace_bytes", "lsv_workspace_clear",
-    "lsv_verify_block", "lsv_accept_workspace_bytes", "lsv_accept", "lsv_select_length",
+    "lsv_verify_block", "lsv_accept_workspace_bytes", "lsv_accept", "lsv_select_length", "lsv_set_timing_events",
 )
+LSV_KERNEL_QKV, LSV_KERNEL_O, LSV_KERNEL_GATEUP, LSV_KERNEL_DOWN, LSV_KERNEL_LMHEAD, LSV_KERNEL_ATTENTION = range(6)
+LSV_MAX_TIMING_SLOTS = 256
 
 
 class LsvError(RuntimeError):
@@ -50,6 +52,10 @@ def load(path=LIB_PATH):
         return _lib
     if not os.path.exists(path):
         raise ImportError(f"{path} is not built: run __graft_entry__.build() (hipcc, gfx950)")
+    try:  # torch first, so the process holds exactly one HIP runtime (torch's), matched by soname
+        import torch  # noqa: F401
+    except ImportError:
+        pass
     lib = ctypes.CDLL(path)
     P, I32, U32, U64, SZ, F32, F64 = (ctypes.c_void_p, ctypes.c_int32, ctypes.c_uint32, ctypes.c_uint64,
                                       ctypes.c_size_t, ctypes.c_float, ctypes.c_double)
@@ -67,7 +73,8 @@ def load(path=LIB_PATH):
         "lsv_verify_block": (ctypes.c_int, [CP, P, P, I32, I32, P, P, P, I32, I32, P, P, P, SZ, P]),
         "lsv_accept_workspace_bytes": (SZ, [I32, I32, I32]),
         "lsv_accept": (ctypes.c_int, [I32, I32, I32, P, P, I32, I32, P, P, F32, U64, U64, P, P, P, P, P, SZ, P]),
-        "lsv_select_length": (ctypes.c_int, [I32, I32, I32, P, P, I32, I32, F64, I32, U32, P, P, P, P]),
+        "lsv_select_length": (ctypes.c_int, [I32, I32, I32, P, P, I32, I32, F64, I32, U32, P, P, P, P, P]),
+        "lsv_set_timing_events": (ctypes.c_int, [I32, ctypes.POINTER(ctypes.c_void_p), I32, U32]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -155,7 +162,24 @@ def lsv_accept(mode, batch, vocab, logits, row_offsets, max_rows, max_rows_per_s
                              _ptr(out_tokens), _ptr(seq_len), _ptr(status), _ptr(ws), ws_bytes, _stream(stream)))
 
 
-def lsv_select_length(mode, batch, G, conf, cost, d_init, d_max, alpha, block_n, flags, gamma, aux, status,
-                      stream=None):
+def lsv_select_length(mode, batch, G, conf, cost, d_init, d_max, alpha, block_n, flags, gamma, aux, row_offsets,
+                      status, stream=None):
     _check(load().lsv_select_length(mode, batch, G, _ptr(conf), _ptr(cost), d_init, d_max, alpha, block_n, flags,
-                                    _ptr(gamma), _ptr(aux), _ptr(status), _stream(stream)))
+                                    _ptr(gamma), _ptr(aux), _ptr(row_offsets), _ptr(status), _stream(stream)))
+
+
+def lsv_set_timing_events(kernel, events, n_slots, record_flags=0):
+    """events: sequence of 2 * n_slots hipEvent_t handles (ints); record_flags 1 = external
+    (use while capturing a graph)."""
+    arr = (ctypes.c_void_p * max(1, 2 * n_slots))(*[int(e) for e in events][:2 * n_slots])
+    _check(load().lsv_set_timing_events(kernel, arr, n_slots, record_flags))
+
+
+def hip_runtime():
+    """ctypes handle of the HIP runtime already loaded in this process (for events)."""
+    load()
+    for line in open("/proc/self/maps"):
+        parts = line.split()
+        if parts and "libamdhip64" in parts[-1]:
+            return ctypes.CDLL(parts[-1])
+    raise RuntimeError("HIP runtime not loaded")

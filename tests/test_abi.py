@@ -39,6 +39,12 @@ def test_status_strings(lib):
     assert lsv.lsv_abi_version() == 1
 
 
+def test_timing_hook_validation(lib):
+    expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_set_timing_events, 9, [], 0, 0)
+    expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_set_timing_events, 2, [0] * 2, 257, 0)
+    lsv.lsv_set_timing_events(2, [], 0)
+
+
 def tiny_cfg(**kw):
     c = dict(n_layers=2, d_model=256, n_q_heads=4, n_kv_heads=4, head_dim=64, d_ff=688, vocab=1024,
              dtype=lsv.LSV_DTYPE_F32, rms_eps=1e-5, reserved0=0.0, rope_base=10000.0)
@@ -68,13 +74,14 @@ def test_host_validation(lib):
     cfg = tiny_cfg()
     S = 0  # stream handle; never reached
     # selector
-    expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_select_length, 7, 1, 4, 1, 1, 1, 4, 2.0, 2, 0, 1, None, None, S)
-    expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_select_length, 0, 1, 65, 1, 1, 1, 4, 2.0, 2, 0, 1, None, None, S)
-    expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_select_length, 0, 1, 4, 1, 1, 1, 5, 2.0, 2, 0, 1, None, None, S)
-    expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_select_length, 0, 1, 4, 1, None, 1, 4, 2.0, 2, 0, 1, None, None, S)
-    expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_select_length, 2, 1, 4, 1, None, 1, 4, 0.0, 2, 0, 1, None, None, S)
-    expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_select_length, 2, 1, 4, 1, None, 1, 4, 2.0, 0, 0, 1, None, None, S)
-    expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_select_length, 1, 1, 4, 1, 1, 1, 4, 2.0, 2, 4, 1, None, None, S)
+    expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_select_length, 7, 1, 4, 1, 1, 1, 4, 2.0, 2, 0, 1, None, None, None, S)
+    expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_select_length, 0, 1, 65, 1, 1, 1, 4, 2.0, 2, 0, 1, None, None, None, S)
+    expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_select_length, 0, 1, 4, 1, 1, 1, 5, 2.0, 2, 0, 1, None, None, None, S)
+    expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_select_length, 0, 1, 4, 1, None, 1, 4, 2.0, 2, 0, 1, None, None, None, S)
+    expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_select_length, 2, 1, 4, 1, None, 1, 4, 0.0, 2, 0, 1, None, None, None, S)
+    expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_select_length, 2, 1, 4, 1, None, 1, 4, 2.0, 0, 0, 1, None, None, None, S)
+    expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_select_length, 1, 1, 4, 1, 1, 1, 4, 2.0, 2, 4, 1, None, None, None, S)
+    expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_select_length, 1, 65, 4, 1, 1, 1, 4, 2.0, 2, 0, 1, None, 1, None, S)
     # accept
     expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_accept, 3, 1, 10, 1, 1, 2, 2, 1, None, 0.0, 0, 0, 1, 1, None, None, 1,
            1 << 20, S)

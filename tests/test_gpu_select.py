@@ -17,9 +17,13 @@ def gpu_select(mode, conf, cost, d_init, d_max, alpha, n, flags):
     g = torch.full((B,), -7, dtype=torch.int32, device="cuda")
     aux = torch.full((B,), -7, dtype=torch.int32, device="cuda")
     st = torch.full((B,), 99, dtype=torch.int32, device="cuda")
-    lsv.lsv_select_length(mode, B, G, c, co, d_init, d_max, alpha, n, flags, g, aux, st)
+    ro = torch.full((B + 1,), -7, dtype=torch.int32, device="cuda") if B <= 64 else None
+    lsv.lsv_select_length(mode, B, G, c, co, d_init, d_max, alpha, n, flags, g, aux, ro, st)
     torch.cuda.synchronize()
-    return g.cpu().numpy(), aux.cpu().numpy(), st.cpu().numpy()
+    g_np = g.cpu().numpy()
+    if ro is not None:  # the verify row layout: root plus gamma drafts per sequence
+        assert ro.cpu().numpy().tolist() == [0] + list(np.cumsum(g_np + 1))
+    return g_np, aux.cpu().numpy(), st.cpu().numpy()
 
 
 def random_conf(rng, B, G):
@@ -57,7 +61,7 @@ def test_selector_parity_random():
     n_cases = 0
     for trial in range(90):
         G = int(rng.choice([1, 2, 3, 7, 16, 32, 64]))
-        B = 64
+        B = 64 if trial % 4 else 97   # beyond one wave: no row offsets
         conf = random_conf(rng, B, G)
         cost = random_cost(rng, G)
         for mode in (S.SEL_MARGINAL, S.SEL_EXHAUSTIVE, S.SEL_ALG1):
