@@ -42,6 +42,12 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--calib-copy", action="store_true",
                    help="also run one plain 256 MiB copy kernel (counter calibration for --pmc runs)")
+    p.add_argument("--summarize", nargs=3, metavar=("TRACE_DIR", "FETCH_DIR", "WRITE_DIR"),
+                   help="no GPU work: turn the csv output of three rocprofv3 runs of this script (kernel trace, "
+                        "--pmc FETCH_SIZE, --pmc WRITE_SIZE; each dir also holds that run's bench.json) into the "
+                        "gate/up profile summary")
+    p.add_argument("--sweep-reps-counters", type=int, default=1,
+                   help="--sweep-reps of the two counter runs (with --summarize)")
     return p.parse_args()
 
 
@@ -73,6 +79,157 @@ def gateup_bytes(m, rows):
     storage-type activation rows and their norm statistics in, the SwiGLU output out."""
     es = 2 if m.dtype == "bf16" else 4
     return 2 * m.d_ff * m.d_model * es + rows * m.d_model * es + rows * (m.d_model // 64) * 4 + rows * m.d_ff * es
+
+
+GATEUP_PROFILE = os.path.join(ROOT, "profiles", "gemm_gateup_llama3-8b-b1-c2048.md")
+KERNEL_SOURCES = ("gemm.hip", "lsv_gemm.h", "lsv_device.h", "forward.hip")
+
+
+def kernel_source_hash():
+    import hashlib
+    h = hashlib.sha256()
+    for name in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, "paper_2608_08721_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(rows):
+    """HBM bytes (read + written) per gate/up launch at `rows` block rows, from the committed
+    counter profile; None when the kernel sources changed since the counters were taken."""
+    try:
+        lines = open(GATEUP_PROFILE).read().splitlines()
+    except OSError:
+        return None
+    vals = dict(l.split(":", 1) for l in lines if l.startswith(("source_hash:", "traffic_rows_")))
+    if vals.get("source_hash", "").strip() != kernel_source_hash():
+        return None
+    v = vals.get(f"traffic_rows_{rows}")
+    return None if v is None else float(v)
+
+
+GATEUP_KERNEL = "gemm_kernel<unsigned short, 2, 2, 3>"  # bf16, up to 32 rows, 2 tiles per wave, SwiGLU
+SELECT_KERNEL = "select_length_kernel"
+CALIB_BYTES = 256 << 20
+
+
+def _short(name):
+    name = name.replace("void lsv::", "").replace("lsv::", "")
+    return name.split("(")[0] if not name.startswith("__") else name
+
+
+def summarize(trace_dir, fetch_dir, write_dir, reps_c):
+    """Profile summary (markdown) of the default workload from three rocprofv3 runs of this
+    script.  Dispatches are attributed by their order, which the script fixes: for each
+    gamma = 1..G the sweep runs its graph body 1 + 3 + reps times; then one eager step,
+    `warmup` + `steps` replays of the step graph and the eager roofline steps."""
+    import csv
+    import glob
+    from synth import configs
+
+    def one(d, pat):
+        f = glob.glob(os.path.join(d, pat))
+        assert len(f) == 1, (d, pat, f)
+        return f[0]
+
+    def bench_json(d):
+        return json.loads(open(os.path.join(d, "bench.json")).read().strip().splitlines()[-1])
+
+    bt = bench_json(trace_dir)
+    wl = configs.WORKLOADS[bt["config"]["workload"]]
+    m, G, L = wl.model, wl.G, wl.model.n_layers
+    trace = sorted(csv.DictReader(open(one(trace_dir, "*kernel_trace.csv"))), key=lambda r: int(r["Dispatch_Id"]))
+    dur = lambda r: (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+    gu = [r for r in trace if GATEUP_KERNEL in r["Kernel_Name"]]
+    n_roof = bt["roofline"]["launches_timed"]
+    roof = [dur(r) for r in gu[-n_roof:]]
+    # timed region: from the first timed replay's selector launch to the first roofline step's
+    sel = [r for r in trace if SELECT_KERNEL in r["Kernel_Name"]]
+    i0 = 3 + 1 + bt["warmup"]
+    t_lo, t_hi = int(sel[i0]["Start_Timestamp"]), int(sel[i0 + bt["steps"]]["Start_Timestamp"])
+    per = {}
+    for r in trace:
+        if t_lo <= int(r["Start_Timestamp"]) < t_hi:
+            per.setdefault(_short(r["Kernel_Name"]), []).append(dur(r))
+    steps = bt["steps"]
+    busy = sum(sum(v) for v in per.values()) / steps
+
+    out = []
+    w = out.append
+    cmd_t = ("rocprofv3 --kernel-trace --stats --output-format csv -d gpurun_out/pf/trace -o t -- "
+             f"python3 bench.py --steps {bt['steps']} --warmup {bt['warmup']} --no-cpu-baseline")
+    cmd_c = ("rocprofv3 --pmc {c} --output-format csv -d gpurun_out/pf/{d} -o {o} -- python3 bench.py --steps 2 "
+             f"--warmup 1 --sweep-reps {reps_c} --roofline-steps 1 --no-cpu-baseline --calib-copy")
+    w(f"# gate/up GEMM + SwiGLU: {wl.name} ({m.name} shape, batch {wl.batch}, context {bt['config']['context']})")
+    w("")
+    w("Commands (repository root, after `cd /tmp && export TMPDIR=/tmp` for the profiler's own files; each")
+    w("run's stdout saved as bench.json in its output directory):")
+    w("")
+    w("```")
+    w(cmd_t)
+    w(cmd_c.format(c="FETCH_SIZE", d="fetch", o="f"))
+    w(cmd_c.format(c="WRITE_SIZE", d="write", o="w"))
+    w("python3 bench.py --summarize gpurun_out/pf/trace gpurun_out/pf/fetch gpurun_out/pf/write")
+    w("```")
+    w("")
+    w(f"source_hash: {kernel_source_hash()}")
+    w("")
+    w("## Timing run")
+    w("")
+    w(f"- bench line: {bt['ms_per_step'] * 1e3:.1f} us per step at gamma {bt['config']['gamma']} "
+      f"({bt['value']:.0f} verified tokens/s), step HBM fraction {bt['step']['hbm_frac']:.3f}")
+    w(f"- gate/up launches of the eager roofline steps: {len(roof)}, average {statistics.mean(roof):.2f} us in the "
+      f"kernel trace vs {bt['roofline']['avg_launch_us']:.2f} us from the script's HIP events "
+      f"(frac {bt['roofline']['frac']:.3f} of 8 TB/s)")
+    w(f"- timed graph replays: kernels busy {busy:.1f} us of {bt['ms_per_step'] * 1e3:.1f} us per step")
+    w("")
+    w("| kernel (timed replays) | launches/step | avg us | us/step | share |")
+    w("|---|---:|---:|---:|---:|")
+    for k, v in sorted(per.items(), key=lambda kv: -sum(kv[1])):
+        w(f"| `{k}` | {len(v) / steps:g} | {statistics.mean(v):.2f} | {sum(v) / steps:.1f} | "
+          f"{sum(v) / steps / busy * 100:.1f}% |")
+    w("")
+
+    # counters
+    def counters(d, pat, name):
+        rows = sorted(csv.DictReader(open(one(d, pat))), key=lambda r: int(r["Dispatch_Id"]))
+        rows = [r for r in rows if r["Counter_Name"] == name]
+        copy = [float(r["Counter_Value"]) for r in rows if "copyBuffer" in r["Kernel_Name"]
+                and int(r["Grid_Size"]) >= 131072]
+        kib = copy[-1]
+        g = [float(r["Counter_Value"]) for r in rows if GATEUP_KERNEL in r["Kernel_Name"]]
+        return kib, g
+    f_copy, f_gu = counters(fetch_dir, "*counter_collection.csv", "FETCH_SIZE")
+    w_copy, w_gu = counters(write_dir, "*counter_collection.csv", "WRITE_SIZE")
+    f_scale = (CALIB_BYTES / 1024) / f_copy
+    w_scale = (CALIB_BYTES / 1024) / w_copy
+    per_g = (1 + 3 + reps_c) * L
+    assert len(f_gu) == len(w_gu) and len(f_gu) >= G * per_g, (len(f_gu), len(w_gu), G * per_g)
+    w("## HBM traffic (two counter runs)")
+    w("")
+    w(f"Calibration: a plain {CALIB_BYTES >> 20} MiB device copy reads FETCH_SIZE {f_copy:.0f} KiB and "
+      f"WRITE_SIZE {w_copy:.0f} KiB, so FETCH_SIZE is scaled by {f_scale:.3f} and WRITE_SIZE by {w_scale:.3f}.")
+    w("Per-launch traffic of the gate/up kernel in the sweep graph of each gamma (rows = gamma + 1; "
+      f"{per_g} launches each), against the algorithmic bytes:")
+    w("")
+    w("| rows | read MB | written MB | traffic MB | algorithmic MB | ratio |")
+    w("|---:|---:|---:|---:|---:|---:|")
+    keys = []
+    for g in range(1, G + 1):
+        sl = slice((g - 1) * per_g, g * per_g)
+        rd = statistics.mean(f_gu[sl]) * 1024 * f_scale
+        wr = statistics.mean(w_gu[sl]) * 1024 * w_scale
+        alg = gateup_bytes(m, g + 1)
+        w(f"| {g + 1} | {rd / 1e6:.2f} | {wr / 1e6:.2f} | {(rd + wr) / 1e6:.2f} | {alg / 1e6:.2f} | "
+          f"{(rd + wr) / alg:.3f} |")
+        keys.append(f"traffic_rows_{g + 1}: {rd + wr:.0f}")
+    w("")
+    w("Bytes per launch (read + written) by block rows, read by bench.py while source_hash matches:")
+    w("")
+    w("```")
+    out += keys
+    w("```")
+    return "\n".join(out) + "\n"
 
 
 def step_bytes(m, contexts, rows):
@@ -125,6 +282,9 @@ def cpu_baseline(m, seed, C, rows, tokens, gamma):
 
 def main():
     args = parse()
+    if args.summarize:
+        sys.stdout.write(summarize(*args.summarize, args.sweep_reps_counters))
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only: this build has no multi-GPU path (asked for --gpus {args.gpus}).",
               file=sys.stderr)
@@ -262,6 +422,9 @@ def main():
     lsv.lsv_set_timing_events(lsv.LSV_KERNEL_GATEUP, hev.ev, n_slots, 0)
     gateup_ms = []
     for _ in range(args.roofline_steps):
+        # a bounded spin kernel first, so that the host has queued the whole step before the GPU
+        # reaches it and each event pair brackets back-to-back execution, not launch latency
+        torch.cuda._sleep(20_000_000)
         step()
         torch.cuda.synchronize()
         gateup_ms += [hev.elapsed_ms(2 * i, 2 * i + 1) for i in range(n_slots)]
@@ -301,7 +464,7 @@ def main():
                    "gamma": g_star, "selector": "marginal on measured cost", "accept": "greedy"},
         "roofline": {"bound": "hbm", "kernel": "gemm gate/up + SwiGLU (one launch per layer)",
                      "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBPS,
-                     "traffic": None, "bytes_per_launch": gu_bytes, "avg_launch_us": avg_gu * 1e3,
+                     "traffic": measured_traffic(rows), "bytes_per_launch": gu_bytes, "avg_launch_us": avg_gu * 1e3,
                      "launches_timed": len(gateup_ms),
                      "how": "HIP events around each gate/up launch in eagerly launched steps"},
         "step": {"latency_us": ms_step * 1e3, "wall_ms_per_step": t_wall / args.steps * 1e3,

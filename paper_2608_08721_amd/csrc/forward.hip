@@ -78,9 +78,9 @@ struct VerifyWs {
   size_t total;
 };
 
-// Target about two workgroups of four waves per compute unit per launch, and at least
-// 16 fragments (16 KiB of weights) per wave so the per-wave pipeline amortises.
-static constexpr int kWantWgs = 640, kMinFragsPerWave = 16;
+// Two resident workgroups of four waves per compute unit, each streaming at least 16
+// steps (16 KiB of weights per wave) so the per-wave pipeline amortises.
+static constexpr int kWantWgs = 512, kMinStepsPerWg = 16;
 
 struct VerifyPlan {
   int MT, n_chunks;
@@ -98,9 +98,9 @@ static VerifyPlan plan_verify(const Shape& s, const ModelLayout& ml, int max_row
   v.max_groups = 1;
   for (int k = 0; k < 5; ++k) {
     const GemmKind kind = (GemmKind)k;
-    v.g[k] = plan_gemm(mats[k]->Nt, mats[k]->Kt, gemm_tpw(kind), kWantWgs, kMinFragsPerWave);
-    if (v.g[k].S > 1) {
-      size_t pf = (size_t)v.g[k].S * max_rows * mats[k]->Nt * 16;
+    v.g[k] = plan_gemm(mats[k]->Nt, mats[k]->Kt, gemm_tpw(kind), kWantWgs, kMinStepsPerWg);
+    if (v.g[k].cmax > 1) {
+      size_t pf = (size_t)v.g[k].groups * v.g[k].cmax * max_rows * 64 * gemm_tpw(kind);
       v.part_floats = pf > v.part_floats ? pf : v.part_floats;
     }
     v.max_groups = v.g[k].groups > v.max_groups ? v.g[k].groups : v.max_groups;
@@ -194,6 +194,7 @@ int launch_verify(const Shape& s, const ModelLayout& ml, const void* packed, voi
   const VerifyPlan v = plan_verify(s, ml, max_rows, max_ctx);
   const VerifyWs w = carve_verify(s, ml, v, max_rows, ws);
   if (w.total > ws_bytes) return LSV_ERR_INVALID_ARG;
+  if (v.part_floats * sizeof(float) >= ((size_t)1 << 31)) return LSV_ERR_UNSUPPORTED;  // 32-bit buffer offsets
   const char* P = (const char*)packed;
   const bool bf16 = s.dtype == LSV_DTYPE_BF16;
 
@@ -232,7 +233,9 @@ int launch_verify(const Shape& s, const ModelLayout& ml, const void* packed, voi
     a.K = pm.K;
     a.Nt = pm.Nt;
     a.Kt = pm.Kt;
-    a.S = p.S;
+    a.groups = p.groups;
+    a.cmax = p.cmax;
+    a.part_bytes = sizeof(float) * v.part_floats;
     const int idx = kind == GEMM_LMHEAD ? 0 : a.layer_index;
     timing_before((int)kind, idx, st);
     const int rc = launch_gemm(s.dtype, kind, v.MT, a, p, st);

@@ -17,12 +17,16 @@
 // column sums of squares, and the consumer scales row m by inv_rms[m] in its
 // epilogue.
 //
-// Work split: blockIdx.x = 4 waves x TPW fragment rows (64*TPW output columns),
-// blockIdx.y = a split of K.  With several splits every workgroup publishes fp32
-// partials with device-scope stores and bumps a device-scope counter; the last
-// one to arrive reads them back (device scope) in split order -- deterministic
-// -- and runs the epilogue.  Device-scope accesses go through the coherent path,
-// so no cache write-back is needed between the producer and the reducer.
+// Work split (stream-K): a workgroup of 4 waves processes "steps" = one k-fragment
+// of a tile group (4 waves x TPW fragment rows = 64*TPW output columns).  The
+// groups x Kt steps are cut into gridDim.x equal contiguous ranges, so every
+// workgroup streams the same number of bytes and the launch has no tail round.
+// A group covered by one workgroup runs its epilogue directly; otherwise each
+// contributor publishes an fp32 partial with 16-byte device-scope stores and bumps
+// a device-scope counter, and the last to arrive reads the partials back (device
+// scope) in k order -- deterministic -- and runs the epilogue.  Device-scope
+// accesses go through the coherent path, so no cache write-back is needed between
+// a contributor and the reducer.
 #include <math.h>
 
 #include "lsv_device.h"
@@ -128,265 +132,333 @@ LSV_DEV void store4(bf16_t* p, const f32x4_t v) { *(GLOBAL u32x2_t*)p = pack_bf1
 // 1 / rms of activation row m from the producer's per-64-column sums of squares.
 // The four lanes sharing (lane & 15) split the partials (p = g, g+4, ...) and
 // combine them with a fixed shuffle tree: deterministic and the same in every lane.
+// All loads are issued before the first use (P <= kMaxStatParts), then summed in order.
+constexpr int kMaxStatParts = 128;  // d_model <= 8192
 LSV_DEV float inv_rms_of_row(const GemmArgs& a, int m, int g4) {
-  float ss = 0.f;
   const GLOBAL float* st = GL(a.stats) + (m < a.M_max ? m : 0);
-#pragma unroll 4
-  for (int p = g4; p < a.P; p += 4) ss += st[(size_t)p * a.M_max];
+  float v[kMaxStatParts / 4];
+#pragma unroll
+  for (int j = 0; j < kMaxStatParts / 4; ++j) {
+    const int p = g4 + 4 * j;
+    v[j] = p < a.P ? st[(size_t)min(p, a.P - 1) * a.M_max] : 0.f;
+  }
+  float ss = 0.f;
+#pragma unroll
+  for (int j = 0; j < kMaxStatParts / 4; ++j) ss += v[j];
   ss += __shfl_xor(ss, 16, kWave);
   ss += __shfl_xor(ss, 32, kWave);
   return 1.0f / sqrtf(ss / (float)a.K + a.eps);
 }
 
 // ------------------------------------------------------------------ the GEMM
-template <typename T, int MT, int TPW, int EPI>
-__global__ void __launch_bounds__(256) gemm_kernel(GemmArgs a) {
+// Raw buffer resource over the partials (word 3 = the gfx9-family raw-buffer format).
+LSV_DEV __amdgpu_buffer_rsrc_t part_rsrc(float* base, size_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(base, 0, (int)(bytes > 0x7fffffffu ? 0x7fffffffu : bytes), 0x00020000);
+}
+constexpr int kDeviceScope = 16;  // buffer cache policy: sc1 (coherent at device scope)
+
+// Which workgroup's step range contains step i (ranges start at floor(w T / W)).
+LSV_DEV int owner_of(long long i, long long T, int W) { return (int)(((i + 1) * W - 1) / T); }
+
+template <typename T, int MT, int TPW, int EPI, int ROWS_SH>
+LSV_DEV void gemm_body(const GemmArgs& a, const int M, float (*red)[ROWS_SH], int& flag) {
   constexpr int KT = FragTraits<T>::KT, EPL = FragTraits<T>::EPL;
   constexpr int WAVES = 4, U = 4;  // U k-steps per pipeline stage
   constexpr bool RMS = EPI != EPI_RESID;  // consumer of a normalised activation
-  constexpr int ROWS = MT * 16;
+  constexpr int ROWS = MT * 16, GCOLS = 64 * TPW;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, l16 = lane & 15, g4 = lane >> 4;
-  const int group = blockIdx.x, split = blockIdx.y;
-  const int M = min(GL(a.row_offsets)[a.batch], a.M_max);  // never trust device rows beyond the host bound
-  const int kf0 = (int)((long long)split * a.Kt / a.S), kf1 = (int)((long long)(split + 1) * a.Kt / a.S);
-  const int nkf = kf1 - kf0;
+  const int W = gridDim.x, w = blockIdx.x;
+  const long long Tsteps = (long long)a.groups * a.Kt;
+  const long long s_begin = (long long)w * Tsteps / W, s_end = (long long)(w + 1) * Tsteps / W;
 
-  __shared__ float red[WAVES * TPW][ROWS];  // residual epilogue: per-16-column sums of squares
-  __shared__ int flag;
 
-  // ---- operand streams: A = packed weights, B = activation rows (clamped into the buffer;
-  // columns of rows >= M are never stored, so their contents do not matter)
-  const int tn0 = (group * WAVES + wave) * TPW;
-  bool tvalid[TPW];
-  const GLOBAL u32x4_t* wp[TPW];
-#pragma unroll
-  for (int t = 0; t < TPW; ++t) {
-    tvalid[t] = tn0 + t < a.Nt;
-    wp[t] = (const GLOBAL u32x4_t*)a.W + ((size_t)(tvalid[t] ? tn0 + t : 0) * a.Kt + kf0) * 64 + lane;
-  }
+  // B operand: activation rows (clamped into the buffer; columns of rows >= M are never
+  // stored, so their contents do not matter)
   const GLOBAL T* xp[MT];
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt) {
     const int m = min(mt * 16 + l16, a.M_max - 1);
-    xp[mt] = (const GLOBAL T*)a.x + (size_t)m * a.ldx + (size_t)kf0 * KT + g4 * EPL;
+    xp[mt] = (const GLOBAL T*)a.x + (size_t)m * a.ldx + g4 * EPL;
   }
-  // Every load hits an in-bounds fragment (index clamped): a conditional load would become
-  // a select between addresses and a generic access.  Steps past the range are never used.
-  u32x4_t wa[2][U][TPW], xb[2][U][MT];
-  auto load_stage = [&](int s, int kb) {
+  float inv[MT];  // computed at the first epilogue, off the weight stream's critical path
+  bool inv_ready = false;
+  const __amdgpu_buffer_rsrc_t prs = part_rsrc(a.part, a.part_bytes);
+
+  for (long long g = s_begin / a.Kt; g * a.Kt < s_end; ++g) {
+    const int k0 = (int)(max(s_begin, g * a.Kt) - g * a.Kt), k1 = (int)(min(s_end, (g + 1) * a.Kt) - g * a.Kt);
+    const int nk = k1 - k0;
+    const int tn0 = ((int)g * WAVES + wave) * TPW;
+    bool tvalid[TPW];
+    const GLOBAL u32x4_t* wp[TPW];
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int kf = min(kb + u, nkf - 1);
-#pragma unroll
-      for (int t = 0; t < TPW; ++t) wa[s][u][t] = wp[t][(size_t)kf * 64];
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt) xb[s][u][mt] = *(const GLOBAL u32x4_t*)(xp[mt] + (size_t)kf * KT);
+    for (int t = 0; t < TPW; ++t) {
+      tvalid[t] = tn0 + t < a.Nt;
+      wp[t] = (const GLOBAL u32x4_t*)a.W + ((size_t)(tvalid[t] ? tn0 + t : 0) * a.Kt + k0) * 64 + lane;
     }
-  };
-  f32x4_t acc[TPW][MT];
+    // Every load hits an in-bounds fragment (index clamped): a conditional load would become
+    // a select between addresses and a generic access.  Steps past the range are never used.
+    u32x4_t wa[2][U][TPW], xb[2][U][MT];
+    auto load_stage = [&](int st, int kb) {
 #pragma unroll
-  for (int t = 0; t < TPW; ++t)
+      for (int u = 0; u < U; ++u) {
+        const int kf = min(kb + u, nk - 1);
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt) acc[t][mt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  auto compute_stage = [&](int s, int kb) {
+        for (int t = 0; t < TPW; ++t) wa[st][u][t] = wp[t][(size_t)kf * 64];
 #pragma unroll
-    for (int u = 0; u < U; ++u)
-      if (kb + u < nkf)
+        for (int mt = 0; mt < MT; ++mt) xb[st][u][mt] = *(const GLOBAL u32x4_t*)(xp[mt] + (size_t)(k0 + kf) * KT);
+      }
+    };
+    f32x4_t acc[TPW][MT];
+#pragma unroll
+    for (int t = 0; t < TPW; ++t)
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) acc[t][mt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    auto compute_stage = [&](int st) {  // all U steps, no per-step conditions
+#pragma unroll
+      for (int u = 0; u < U; ++u)
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-          for (int t = 0; t < TPW; ++t) mfma_frag(wa[s][u][t], xb[s][u][mt], acc[t][mt], T{});
-  };
-  load_stage(0, 0);
-  load_stage(1, U);
-  for (int kb = 0; kb < nkf; kb += 2 * U) {
-    compute_stage(0, kb);
-    if (kb + 2 * U < nkf) load_stage(0, kb + 2 * U);
-    compute_stage(1, kb + U);
-    if (kb + 3 * U < nkf) load_stage(1, kb + 3 * U);
-  }
+          for (int t = 0; t < TPW; ++t) mfma_frag(wa[st][u][t], xb[st][u][mt], acc[t][mt], T{});
+    };
+    auto compute_tail = [&](int st, int kb) {  // the last (< 2U) steps
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+        if (kb + u < nk)
+#pragma unroll
+          for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int t = 0; t < TPW; ++t) mfma_frag(wa[st][u][t], xb[st][u][mt], acc[t][mt], T{});
+    };
+    // Scheduling barriers keep the loads issued -- and so retired, vmcnt counting in
+    // order -- stage by stage, and the loop body has no branches: while one stage is
+    // multiplied the other is in flight.  Loads past the range re-read the last step.
+    const int nfull = nk - nk % (2 * U);
+    load_stage(0, 0);
+    __builtin_amdgcn_sched_barrier(0);
+    load_stage(1, U);
+    __builtin_amdgcn_sched_barrier(0);
+    for (int kb = 0; kb < nfull; kb += 2 * U) {
+      compute_stage(0);
+      __builtin_amdgcn_sched_barrier(0);
+      load_stage(0, kb + 2 * U);
+      __builtin_amdgcn_sched_barrier(0);
+      compute_stage(1);
+      __builtin_amdgcn_sched_barrier(0);
+      load_stage(1, kb + 3 * U);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    compute_tail(0, nfull);
+    compute_tail(1, nfull + U);
 
-  // ---- split-K: device-scope partials, the last workgroup reduces in split order
-  const int Np = a.Nt * 16;
-  if (a.S > 1) {
+    // ---- groups shared with other workgroups: device-scope partials, last arrival reduces
+    const int first = owner_of(g * a.Kt, Tsteps, W), last = owner_of(g * a.Kt + a.Kt - 1, Tsteps, W);
+    const int contributors = last - first + 1;
+    if (contributors > 1) {
+      const size_t slot = (size_t)g * a.cmax + (w - first);
 #pragma unroll
-    for (int t = 0; t < TPW; ++t)
+      for (int t = 0; t < TPW; ++t)
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt) {
-        const int m = mt * 16 + l16, n = (tn0 + t) * 16 + 4 * g4;
-        if (m < M && tvalid[t]) {
-          float* p = a.part + ((size_t)split * a.M_max + m) * Np + n;
-#pragma unroll
-          for (int r = 0; r < 4; ++r) __hip_atomic_store(p + r, acc[t][mt][r], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        }
-      }
-    __builtin_amdgcn_s_waitcnt(0);  // this thread's partials have reached the coherent level
-    __syncthreads();
-    if (threadIdx.x == 0)
-      flag = __hip_atomic_fetch_add(&a.counters[group], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == a.S - 1;
-    __syncthreads();
-    if (!flag) return;
-#pragma unroll
-    for (int t = 0; t < TPW; ++t)
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt) {
-        const int m = mt * 16 + l16, n = (tn0 + t) * 16 + 4 * g4;
-        f32x4_t s = f32x4_t{0.f, 0.f, 0.f, 0.f};
-        if (m < M && tvalid[t]) {
-          for (int sp = 0; sp < a.S; ++sp) {
-            float* p = a.part + ((size_t)sp * a.M_max + m) * Np + n;
-#pragma unroll
-            for (int r = 0; r < 4; ++r) s[r] += __hip_atomic_load(p + r, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        for (int mt = 0; mt < MT; ++mt) {
+          const int m = mt * 16 + l16, col = (wave * TPW + t) * 16 + 4 * g4;
+          if (m < M) {
+            const int off = (int)(((slot * a.M_max + m) * GCOLS + col) * sizeof(float));
+            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4_t, acc[t][mt]), prs, off, 0, kDeviceScope);
           }
         }
-        acc[t][mt] = s;
-      }
-    if (threadIdx.x == 0) __hip_atomic_store(&a.counters[group], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  }
-
-  // ---- epilogues; lane holds output columns n0..n0+3 (weight rows) of activation row m
-  float inv[MT];
-  if (RMS) {
+      __builtin_amdgcn_s_waitcnt(0);  // this thread's partials have reached the coherent level
+      __syncthreads();
+      if (threadIdx.x == 0)
+        flag = __hip_atomic_fetch_add(&a.counters[g], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == contributors - 1;
+      __syncthreads();
+      const bool is_last = flag != 0;
+      __syncthreads();  // flag is rewritten by the next group
+      if (!is_last) continue;
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt) inv[mt] = inv_rms_of_row(a, mt * 16 + l16, g4);
-  }
-  if (EPI == EPI_LOGITS) {
+      for (int t = 0; t < TPW; ++t)
 #pragma unroll
-    for (int t = 0; t < TPW; ++t)
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt) {
-        const int m = mt * 16 + l16, n0 = (tn0 + t) * 16 + 4 * g4;
-        if (m >= M || !tvalid[t]) continue;
-        const f32x4_t v = acc[t][mt] * inv[mt];
-        GLOBAL float* o = GL(a.out_f32) + (size_t)m * a.ldo;
-        if (n0 + 3 < a.N && (a.ldo & 3) == 0) {
-          *(GLOBAL f32x4_t*)(o + n0) = v;
-        } else {
-#pragma unroll
-          for (int r = 0; r < 4; ++r)
-            if (n0 + r < a.N) o[n0 + r] = v[r];
-        }
-      }
-  } else if (EPI == EPI_QKV) {
-    const int qrows = a.nq * a.hd, krows = a.nkv * a.hd;
-#pragma unroll
-    for (int t = 0; t < TPW; ++t)
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt) {
-        const int m = mt * 16 + l16, n0 = (tn0 + t) * 16 + 4 * g4;
-        if (m >= M || !tvalid[t] || n0 >= qrows + 2 * krows) continue;
-        const int b = seq_of_row(a.row_offsets, a.batch, m);
-        const int pos = GL(a.seq_len)[b] + (m - GL(a.row_offsets)[b]);
-        const f32x4_t v = acc[t][mt] * inv[mt];
-        if (n0 < qrows + krows) {
-          const bool isq = n0 < qrows;
-          const int local = isq ? n0 : n0 - qrows;
-          const int head = local / a.hd, i0 = (local % a.hd) >> 1;  // pairs (i0, i0+hd/2), (i0+1, i0+1+hd/2)
-          float out[4];
-#pragma unroll
-          for (int pr = 0; pr < 2; ++pr) {
-            // angle = pos * base^(-2i/hd) in fp64, reduced to [-pi, pi] in fp64, then fp32 sin/cos
-            const int i = i0 + pr;
-            const double inv_freq = exp2(-(double)(2 * i) / (double)a.hd * a.log2_rope_base);
-            const double ang = (double)pos * inv_freq;
-            const double red2pi = ang - 6.283185307179586 * rint(ang * 0.15915494309189535);
-            float s, c;
-            sincosf((float)red2pi, &s, &c);
-            const float x1 = v[2 * pr], x2 = v[2 * pr + 1];
-            out[2 * pr] = x1 * c - x2 * s;
-            out[2 * pr + 1] = x2 * c + x1 * s;
+        for (int mt = 0; mt < MT; ++mt) {
+          const int m = mt * 16 + l16, col = (wave * TPW + t) * 16 + 4 * g4;
+          f32x4_t sum = f32x4_t{0.f, 0.f, 0.f, 0.f};
+          if (m < M) {
+            for (int j = 0; j < contributors; ++j) {
+              const size_t sl = (size_t)g * a.cmax + j;
+              const int off = (int)(((sl * a.M_max + m) * GCOLS + col) * sizeof(float));
+              sum += __builtin_bit_cast(f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(prs, off, 0, kDeviceScope));
+            }
           }
-          T* dst;
-          if (isq) {
-            dst = (T*)a.q_out + ((size_t)m * a.nq + head) * a.hd;
+          acc[t][mt] = sum;
+        }
+      if (threadIdx.x == 0) __hip_atomic_store(&a.counters[g], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+
+    // ---- epilogues; lane holds output columns n0..n0+3 (weight rows) of activation row m
+    if (RMS && !inv_ready) {
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) inv[mt] = inv_rms_of_row(a, mt * 16 + l16, g4);
+      inv_ready = true;
+    }
+    if (EPI == EPI_LOGITS) {
+#pragma unroll
+      for (int t = 0; t < TPW; ++t)
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+          const int m = mt * 16 + l16, n0 = (tn0 + t) * 16 + 4 * g4;
+          if (m >= M || !tvalid[t]) continue;
+          const f32x4_t v = acc[t][mt] * inv[mt];
+          GLOBAL float* o = GL(a.out_f32) + (size_t)m * a.ldo;
+          if (n0 + 3 < a.N && (a.ldo & 3) == 0) {
+            *(GLOBAL f32x4_t*)(o + n0) = v;
+          } else {
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+              if (n0 + r < a.N) o[n0 + r] = v[r];
+          }
+        }
+    } else if (EPI == EPI_QKV) {
+      const int qrows = a.nq * a.hd, krows = a.nkv * a.hd;
+#pragma unroll
+      for (int t = 0; t < TPW; ++t)
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+          const int m = mt * 16 + l16, n0 = (tn0 + t) * 16 + 4 * g4;
+          if (m >= M || !tvalid[t] || n0 >= qrows + 2 * krows) continue;
+          const int b = seq_of_row(a.row_offsets, a.batch, m);
+          const int pos = GL(a.seq_len)[b] + (m - GL(a.row_offsets)[b]);
+          const f32x4_t v = acc[t][mt] * inv[mt];
+          if (n0 < qrows + krows) {
+            const bool isq = n0 < qrows;
+            const int local = isq ? n0 : n0 - qrows;
+            const int head = local / a.hd, i0 = (local % a.hd) >> 1;  // pairs (i0, i0+hd/2), (i0+1, i0+1+hd/2)
+            float out[4];
+#pragma unroll
+            for (int pr = 0; pr < 2; ++pr) {
+              // angle = pos * base^(-2i/hd) in fp64, reduced to [-pi, pi] in fp64, then fp32 sin/cos
+              const int i = i0 + pr;
+              const double inv_freq = exp2(-(double)(2 * i) / (double)a.hd * a.log2_rope_base);
+              const double ang = (double)pos * inv_freq;
+              const double red2pi = ang - 6.283185307179586 * rint(ang * 0.15915494309189535);
+              float sn, cs;
+              sincosf((float)red2pi, &sn, &cs);
+              const float x1 = v[2 * pr], x2 = v[2 * pr + 1];
+              out[2 * pr] = x1 * cs - x2 * sn;
+              out[2 * pr + 1] = x2 * cs + x1 * sn;
+            }
+            T* dst;
+            if (isq) {
+              dst = (T*)a.q_out + ((size_t)m * a.nq + head) * a.hd;
+            } else {
+              if (pos < 0 || pos >= a.capacity) continue;
+              dst = (T*)a.kv + ((((size_t)a.layer * 2 + 0) * a.batch + b) * a.nkv + head) * (size_t)a.capacity * a.hd +
+                    (size_t)pos * a.hd;
+            }
+            GLOBAL T* gd = GL(dst);
+            gd[i0] = from_f32<T>(out[0]);
+            gd[i0 + a.hd / 2] = from_f32<T>(out[1]);
+            gd[i0 + 1] = from_f32<T>(out[2]);
+            gd[i0 + 1 + a.hd / 2] = from_f32<T>(out[3]);
           } else {
             if (pos < 0 || pos >= a.capacity) continue;
-            dst = (T*)a.kv + ((((size_t)a.layer * 2 + 0) * a.batch + b) * a.nkv + head) * (size_t)a.capacity * a.hd +
-                  (size_t)pos * a.hd;
+            const int local = n0 - qrows - krows;
+            const int head = local / a.hd, d0 = local % a.hd;
+            T* dst = (T*)a.kv + ((((size_t)a.layer * 2 + 1) * a.batch + b) * a.nkv + head) * (size_t)a.capacity * a.hd +
+                     (size_t)pos * a.hd + d0;
+            store4(dst, v);
           }
-          GLOBAL T* gd = GL(dst);
-          gd[i0] = from_f32<T>(out[0]);
-          gd[i0 + a.hd / 2] = from_f32<T>(out[1]);
-          gd[i0 + 1] = from_f32<T>(out[2]);
-          gd[i0 + 1 + a.hd / 2] = from_f32<T>(out[3]);
-        } else {
-          if (pos < 0 || pos >= a.capacity) continue;
-          const int local = n0 - qrows - krows;
-          const int head = local / a.hd, d0 = local % a.hd;
-          T* dst = (T*)a.kv + ((((size_t)a.layer * 2 + 1) * a.batch + b) * a.nkv + head) * (size_t)a.capacity * a.hd +
-                   (size_t)pos * a.hd + d0;
-          store4(dst, v);
         }
-      }
-  } else if (EPI == EPI_RESID) {
-    // h += y; the storage-type copy of h for the next consumer; per-row sums of squares of
-    // the new h over each 64-column group
+    } else if (EPI == EPI_RESID) {
+      // h += y; the storage-type copy of h for the next consumer; per-row sums of squares of
+      // the new h over each 64-column group
 #pragma unroll
-    for (int t = 0; t < TPW; ++t)
+      for (int t = 0; t < TPW; ++t)
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+          const int m = mt * 16 + l16, n0 = (tn0 + t) * 16 + 4 * g4;
+          float ss = 0.f;
+          if (m < M && tvalid[t]) {
+            GLOBAL f32x4_t* hp = (GLOBAL f32x4_t*)(a.h_out + (size_t)m * a.N + n0);
+            const f32x4_t h4 = *hp + acc[t][mt];
+            *hp = h4;
+            if (a.hx_out) store4((T*)a.hx_out + (size_t)m * a.N + n0, h4);
+            ss = ((h4[0] * h4[0] + h4[1] * h4[1]) + h4[2] * h4[2]) + h4[3] * h4[3];
+          }
+          ss += __shfl_xor(ss, 16, kWave);
+          ss += __shfl_xor(ss, 32, kWave);
+          if (lane < 16) red[wave * TPW + t][mt * 16 + lane] = ss;
+        }
+      __syncthreads();
+      // 64-column groups: tiles 4p..4p+3 of this tile group, summed in order
+      constexpr int PARTS = WAVES * TPW / 4;
+      for (int i = threadIdx.x; i < PARTS * ROWS; i += blockDim.x) {
+        const int p = i / ROWS, m = i % ROWS;
+        if (m >= M) continue;
+        const int gp = (int)g * PARTS + p;
+        if (gp * 64 >= a.N) continue;
+        const float sm = ((red[4 * p + 0][m] + red[4 * p + 1][m]) + red[4 * p + 2][m]) + red[4 * p + 3][m];
+        GL(a.stats_out)[(size_t)gp * a.M_max + m] = sm;
+      }
+      __syncthreads();  // red is rewritten by the next group
+    } else if (EPI == EPI_SWIGLU) {
+      static_assert(EPI != EPI_SWIGLU || TPW == 2, "SwiGLU pairs a gate and an up fragment row");
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) {
-        const int m = mt * 16 + l16, n0 = (tn0 + t) * 16 + 4 * g4;
-        float ss = 0.f;
-        if (m < M && tvalid[t]) {
-          GLOBAL f32x4_t* hp = (GLOBAL f32x4_t*)(a.h_out + (size_t)m * a.N + n0);
-          const f32x4_t h4 = *hp + acc[t][mt];
-          *hp = h4;
-          if (a.hx_out) store4((T*)a.hx_out + (size_t)m * a.N + n0, h4);
-          ss = ((h4[0] * h4[0] + h4[1] * h4[1]) + h4[2] * h4[2]) + h4[3] * h4[3];
+        const int m = mt * 16 + l16, f0 = (tn0 >> 1) * 16 + 4 * g4;
+        if (m >= M || !tvalid[0]) continue;
+        f32x4_t out;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float gt = acc[0][mt][r] * inv[mt], up = acc[TPW - 1][mt][r] * inv[mt];
+          out[r] = gt / (1.0f + expf(-gt)) * up;
         }
-        ss += __shfl_xor(ss, 16, kWave);
-        ss += __shfl_xor(ss, 32, kWave);
-        if (lane < 16) red[wave * TPW + t][mt * 16 + lane] = ss;
-      }
-    __syncthreads();
-    // 64-column groups: tiles 4p..4p+3 of this workgroup, summed in order
-    constexpr int PARTS = WAVES * TPW / 4;
-    for (int i = threadIdx.x; i < PARTS * ROWS; i += blockDim.x) {
-      const int p = i / ROWS, m = i % ROWS;
-      if (m >= M) continue;
-      const int gp = group * PARTS + p;
-      if (gp * 64 >= a.N) continue;
-      const float s = ((red[4 * p + 0][m] + red[4 * p + 1][m]) + red[4 * p + 2][m]) + red[4 * p + 3][m];
-      GL(a.stats_out)[(size_t)gp * a.M_max + m] = s;
-    }
-  } else if (EPI == EPI_SWIGLU) {
-    static_assert(EPI != EPI_SWIGLU || TPW == 2, "SwiGLU pairs a gate and an up fragment row");
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-      const int m = mt * 16 + l16, f0 = (tn0 >> 1) * 16 + 4 * g4;
-      if (m >= M || !tvalid[0]) continue;
-      f32x4_t out;
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const float g = acc[0][mt][r] * inv[mt], u = acc[TPW - 1][mt][r] * inv[mt];
-        out[r] = g / (1.0f + expf(-g)) * u;
-      }
-      T* dst = (T*)a.u_out + (size_t)m * a.ldu + f0;
-      if (f0 + 3 < a.F) {
-        store4(dst, out);
-      } else {
-        for (int r = 0; r < 4; ++r)
-          if (f0 + r < a.F) GL(dst)[r] = from_f32<T>(out[r]);
+        T* dst = (T*)a.u_out + (size_t)m * a.ldu + f0;
+        if (f0 + 3 < a.F) {
+          store4(dst, out);
+        } else {
+          for (int r = 0; r < 4; ++r)
+            if (f0 + r < a.F) GL(dst)[r] = from_f32<T>(out[r]);
+        }
       }
     }
   }
 }
 
+
+// The host bound on rows fixes MT_MAX; the kernel runs the body for the activation
+// tiles that the device row count actually needs, so a generous bound costs nothing.
+template <typename T, int MT_MAX, int TPW, int EPI>
+__global__ void __launch_bounds__(256) gemm_kernel(GemmArgs a) {
+  __shared__ float red[4 * TPW][MT_MAX * 16];  // residual epilogue: per-16-column sums of squares
+  __shared__ int flag;
+  const int M = min(GL(a.row_offsets)[a.batch], a.M_max);  // never trust device rows beyond the host bound
+  const int mt = M <= 16 ? 1 : (M <= 32 ? 2 : (M <= 48 ? 3 : 4));
+  if (mt <= 1 || MT_MAX == 1) gemm_body<T, 1, TPW, EPI, MT_MAX * 16>(a, M, red, flag);
+  else if (mt == 2 || MT_MAX == 2) gemm_body<T, (MT_MAX >= 2 ? 2 : 1), TPW, EPI, MT_MAX * 16>(a, M, red, flag);
+  else if (mt == 3 || MT_MAX == 3) gemm_body<T, (MT_MAX >= 3 ? 3 : 1), TPW, EPI, MT_MAX * 16>(a, M, red, flag);
+  else gemm_body<T, MT_MAX, TPW, EPI, MT_MAX * 16>(a, M, red, flag);
+}
+
 // ------------------------------------------------------------------ planning and launch
-GemmPlan plan_gemm(int Nt, int Kt, int TPW, int want_wgs, int min_frags_per_wave) {
+GemmPlan plan_gemm(int Nt, int Kt, int TPW, int want_wgs, int min_steps_per_wg) {
   GemmPlan p;
   p.groups = (Nt + 4 * TPW - 1) / (4 * TPW);
-  int S = (want_wgs + p.groups / 2) / p.groups;
-  const int s_cap = Kt / min_frags_per_wave;
-  S = S > s_cap ? s_cap : S;
-  S = S < 1 ? 1 : S;
-  p.S = S;
+  const long long T = (long long)p.groups * Kt;
+  long long W = want_wgs;
+  if (W > T / min_steps_per_wg) W = T / min_steps_per_wg;
+  if (W < 1) W = 1;
+  p.wgs = (int)W;
+  // largest number of workgroups sharing one tile group
+  p.cmax = 1;
+  for (int g = 0; g < p.groups; ++g) {
+    const long long i0 = (long long)g * Kt, i1 = i0 + Kt - 1;
+    const int c = (int)(((i1 + 1) * W - 1) / T - ((i0 + 1) * W - 1) / T) + 1;
+    p.cmax = c > p.cmax ? c : p.cmax;
+  }
   return p;
 }
 
 template <typename T, int MT, int TPW, int EPI>
 static void launch_one(const GemmArgs& a, const GemmPlan& p, hipStream_t st) {
-  hipLaunchKernelGGL((gemm_kernel<T, MT, TPW, EPI>), dim3(p.groups, p.S), dim3(256), 0, st, a);
+  hipLaunchKernelGGL((gemm_kernel<T, MT, TPW, EPI>), dim3(p.wgs), dim3(256), 0, st, a);
 }
 
 template <typename T, int TPW, int EPI>

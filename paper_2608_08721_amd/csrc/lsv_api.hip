@@ -43,6 +43,7 @@ int check_config(const lsv_model_config* c) {
       c->n_q_heads % c->n_kv_heads || c->d_ff < 4 || c->d_ff % 4 || c->vocab < 1)
     return fail(LSV_ERR_INVALID_ARG, "bad model dimensions (d_model %% 64, n_q %% n_kv, d_ff %% 4 required)");
   if (c->head_dim != 64 && c->head_dim != 128) return fail(LSV_ERR_UNSUPPORTED, "head_dim must be 64 or 128");
+  if (c->d_model > 8192) return fail(LSV_ERR_UNSUPPORTED, "d_model must be <= 8192");
   if (c->dtype != LSV_DTYPE_F32 && c->dtype != LSV_DTYPE_BF16) return fail(LSV_ERR_INVALID_ARG, "bad dtype");
   if (!(c->rms_eps > 0.f) || !(c->rope_base > 0.0) || !isfinite(c->rope_base) || c->reserved0 != 0.f)
     return fail(LSV_ERR_INVALID_ARG, "bad rms_eps / rope_base / reserved0");

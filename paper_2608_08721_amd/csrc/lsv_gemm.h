@@ -19,7 +19,7 @@ enum GemmKind { GEMM_QKV = 0, GEMM_O = 1, GEMM_GATEUP = 2, GEMM_DOWN = 3, GEMM_L
 struct GemmArgs {
   const uint4* W;  // packed fragments
   int N, K, Nt, Kt;
-  int S;
+  int groups;  // tile groups of 4 waves x TPW fragment rows
   int M_max, batch;
   const int32_t* row_offsets;  // [batch+1]; rows = row_offsets[batch]
   // B operand: activation rows [M_max][ldx] in the storage type, columns >= K zero up to Kt*KT
@@ -29,8 +29,10 @@ struct GemmArgs {
   const float* stats;
   int P;
   float eps;
-  // split-K
-  float* part;    // [S][M_max][Nt*16]
+  // stream-K partials of tile groups shared by several workgroups
+  float* part;    // [groups][cmax][M_max][64*TPW]
+  size_t part_bytes;
+  int cmax;
   int* counters;  // [groups], zero on entry and on exit
   // EPI_LOGITS
   float* out_f32;
@@ -52,10 +54,10 @@ struct GemmArgs {
 };
 
 struct GemmPlan {
-  int groups, S;
+  int groups, wgs, cmax;
 };
 
-GemmPlan plan_gemm(int Nt, int Kt, int TPW, int want_wgs, int min_frags_per_wave);
+GemmPlan plan_gemm(int Nt, int Kt, int TPW, int want_wgs, int min_steps_per_wg);
 int gemm_tpw(GemmKind kind);
 int launch_gemm(int dtype, GemmKind kind, int MT, const GemmArgs& a, const GemmPlan& p, hipStream_t st);
 
