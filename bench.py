@@ -29,6 +29,7 @@ sys.path.insert(0, ROOT)
 
 METRIC = "verify-step latency (us) & tokens/s vs gamma; % of HBM BW / MFMA bf16 peak"
 HBM_PEAK_GBPS = 8000.0
+HIP_EVENT_DISABLE_SYSTEM_FENCE = 0x20000000
 
 
 def parse():
@@ -64,7 +65,8 @@ class HipEvents:
         self.ev = []
         for _ in range(n):
             e = ctypes.c_void_p()
-            assert self.hip.hipEventCreate(ctypes.byref(e)) == 0
+            # timing-only events: no system-scope fence (cache write-back) when they are recorded
+            assert self.hip.hipEventCreateWithFlags(ctypes.byref(e), ctypes.c_uint(HIP_EVENT_DISABLE_SYSTEM_FENCE)) == 0
             self.ev.append(e.value)
 
     def elapsed_ms(self, a, b):
@@ -149,7 +151,7 @@ def summarize(trace_dir, fetch_dir, write_dir, reps_c):
     t_lo, t_hi = int(sel[i0]["Start_Timestamp"]), int(sel[i0 + bt["steps"]]["Start_Timestamp"])
     per = {}
     for r in trace:
-        if t_lo <= int(r["Start_Timestamp"]) < t_hi:
+        if t_lo <= int(r["Start_Timestamp"]) < t_hi and "spin_kernel" not in r["Kernel_Name"]:
             per.setdefault(_short(r["Kernel_Name"]), []).append(dur(r))
     steps = bt["steps"]
     busy = sum(sum(v) for v in per.values()) / steps
@@ -304,7 +306,7 @@ def main():
     seed, B, G = wl.seed, wl.batch, wl.G
     C = int(gen.contexts(wl)[0])
     rows_max = G + 1
-    cap = C + rows_max
+    cap = runtime.kv_capacity(C + rows_max)
     cfg = runtime.model_config(m)
 
     # ---- model: seeded weights, generated and packed one layer at a time (untimed)

@@ -91,8 +91,13 @@ typedef struct lsv_model_config {
  * invalid).  lsv_pack_globals / lsv_pack_layer: write the embedding table
  * [vocab, d_model], the final norm gain [d_model] and the LM head
  * [vocab, d_model], respectively one layer's projections and norm gains, into
- * d_packed.  Source pointers are device pointers in the model dtype; they may be
- * freed once the stream has passed the call.  Layers may be packed in any order. */
+ * d_packed.  Each RMSNorm gain is folded into the projection that consumes the
+ * normalised activations (attention norm into Q/K/V, FFN norm into gate/up,
+ * final norm into the LM head): packed column j holds W[:, j] * g[j], rounded to
+ * the model dtype, and the kernels scale each output row by 1/rms(h) (the norm
+ * commutes with the product because it is a per-row scalar).  Source pointers
+ * are device pointers in the model dtype; they may be freed once the stream has
+ * passed the call.  Layers may be packed in any order. */
 size_t lsv_packed_model_bytes(const lsv_model_config* cfg);
 int lsv_pack_globals(const lsv_model_config* cfg, const void* d_embed, const void* d_final_norm,
                      const void* d_lm_head, void* d_packed, void* stream);
@@ -108,12 +113,20 @@ int lsv_pack_layer(const lsv_model_config* cfg, int32_t layer,
                    void* d_packed, void* stream);
 
 /* ---------------------------------------------------------------- KV cache */
-/* One device buffer.  For layer l the K block precedes the V block; each is
- * [batch][n_kv_heads][capacity][head_dim] in the model dtype, i.e. element
- * (l, kv, b, h, pos, i) is at index
- *   ((((l * 2 + kv) * batch + b) * n_kv_heads + h) * capacity + pos) * head_dim + i
- * with kv = 0 for K and 1 for V.  K is stored after the rotary embedding.
- * Sequence b owns a slab of `capacity` positions; d_seq_len[b] of them are valid. */
+/* One device buffer in the model dtype.  For layer l the K block precedes the V
+ * block; each holds batch x n_kv_heads slabs of capacity x head_dim elements:
+ *   slab(l, kv, b, h) = (((l * 2 + kv) * batch + b) * n_kv_heads + h) * capacity * head_dim
+ * with kv = 0 for K and 1 for V.
+ *   K (after the rotary embedding) is row-major [capacity][head_dim]:
+ *     K(l, b, h, pos, i) at slab(l, 0, b, h) + pos * head_dim + i
+ *   V is transposed, [head_dim][capacity], with positions permuted inside each
+ *   aligned block of 32 so that the keys one matrix-core lane consumes are adjacent:
+ *     V(l, b, h, pos, i) at slab(l, 1, b, h) + i * capacity + LSV_V_COLUMN(pos)
+ * Sequence b owns `capacity` positions per slab; d_seq_len[b] of them are valid.
+ * capacity must be a positive multiple of LSV_KV_ALIGN (lsv_kv_cache_bytes returns 0
+ * and lsv_verify_block LSV_ERR_INVALID_ARG otherwise). */
+enum { LSV_KV_ALIGN = 64 };
+#define LSV_V_COLUMN(pos) (((pos) & ~31) | (((pos) & 12) << 1) | (((pos) & 16) >> 2) | ((pos) & 3))
 size_t lsv_kv_cache_bytes(const lsv_model_config* cfg, int32_t batch, int32_t capacity);
 
 /* ------------------------------------------------------------ verify step */
@@ -137,7 +150,8 @@ int lsv_workspace_clear(void* d_workspace, size_t workspace_bytes, void* stream)
  * is a prefill; long prompts may be fed in chunks.
  *
  *   cfg, d_packed      model and its packed weights
- *   d_kv, capacity     KV cache (layout above) with `capacity` positions per slab
+ *   d_kv, capacity     KV cache (layout above) with `capacity` positions per slab,
+ *                      capacity % LSV_KV_ALIGN == 0
  *   batch              number of sequences (1..LSV_MAX_BATCH)
  *   d_seq_len          [batch] int32, cached positions before this block
  *   d_tokens           [rows] int32 token ids

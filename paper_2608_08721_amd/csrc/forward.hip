@@ -4,7 +4,7 @@
 //
 // Per layer, five launches (+1 attention merge for bf16):
 //   QKV GEMM   : 1/rms row scaling, RoPE, K/V cache append
-//   attention  : split-context chunks (+ merge)
+//   attention  : split-context running softmax (+ merge)
 //   O GEMM     : residual add, storage-type copy of h, row sum-of-squares partials
 //   gate/up    : 1/rms row scaling, SwiGLU
 //   down GEMM  : residual add, storage-type copy of h, sum-of-squares partials
@@ -66,45 +66,25 @@ ModelLayout model_layout(const Shape& s) {
 struct VerifyWs {
   float* h;        // [M_max][d] fp32 residual stream
   void* hx;        // [M_max][d] storage-type copy of h (bf16 models; fp32 models read h)
-  float* stats;    // [d/64][M_max] per-64-column sums of squares of h
+  float* stats;    // [M_max][d/16] per-16-column sums of squares of h
   void* q;         // [M_max][nq][hd]
   void* attn;      // [M_max][nq][hd]
   void* u;         // [M_max][ldu], columns >= d_ff stay zero
-  float* part;     // split-K partials
-  float* o_part;   // attention chunk partials
+  float* o_part;   // attention split partials
   float* ml_part;
-  int* counters;
   int ldu;
   size_t total;
 };
 
-// Two resident workgroups of four waves per compute unit, each streaming at least 16
-// steps (16 KiB of weights per wave) so the per-wave pipeline amortises.
-static constexpr int kWantWgs = 512, kMinStepsPerWg = 16;
-
 struct VerifyPlan {
-  int MT, n_chunks;
-  GemmPlan g[5];
-  size_t part_floats;
-  int max_groups;
+  int MT;
+  AttnPlan attn;
 };
 
-static VerifyPlan plan_verify(const Shape& s, const ModelLayout& ml, int max_rows, int max_ctx) {
+static VerifyPlan plan_verify(const Shape& s, int batch, int max_rows, int max_ctx) {
   VerifyPlan v;
   v.MT = (max_rows + 15) / 16;
-  v.n_chunks = (max_ctx + kAttnChunk - 1) / kAttnChunk;
-  const PackedMat* mats[5] = {&ml.qkv, &ml.o, &ml.gateup, &ml.down, &ml.lm_head};
-  v.part_floats = 0;
-  v.max_groups = 1;
-  for (int k = 0; k < 5; ++k) {
-    const GemmKind kind = (GemmKind)k;
-    v.g[k] = plan_gemm(mats[k]->Nt, mats[k]->Kt, gemm_tpw(kind), kWantWgs, kMinStepsPerWg);
-    if (v.g[k].cmax > 1) {
-      size_t pf = (size_t)v.g[k].groups * v.g[k].cmax * max_rows * 64 * gemm_tpw(kind);
-      v.part_floats = pf > v.part_floats ? pf : v.part_floats;
-    }
-    v.max_groups = v.g[k].groups > v.max_groups ? v.g[k].groups : v.max_groups;
-  }
+  v.attn = plan_attention(batch, s.nkv, max_ctx);
   return v;
 }
 
@@ -121,18 +101,16 @@ static VerifyWs carve_verify(const Shape& s, const ModelLayout& ml, const Verify
   w.ldu = ml.down.Kt * KT;  // the down projection reads whole fragments of u
   w.h = (float*)take(sizeof(float) * (size_t)max_rows * s.d);
   w.hx = s.dtype == LSV_DTYPE_BF16 ? take((size_t)s.es * max_rows * s.d) : (void*)w.h;
-  w.stats = (float*)take(sizeof(float) * (size_t)(s.d / 64) * max_rows);
+  w.stats = (float*)take(sizeof(float) * (size_t)(s.d / 16) * max_rows);
   w.q = take((size_t)s.es * max_rows * s.nq * s.hd);
   w.attn = take((size_t)s.es * max_rows * s.nq * s.hd);
   w.u = take((size_t)s.es * max_rows * w.ldu);
-  w.part = (float*)take(sizeof(float) * v.part_floats);
   if (s.dtype == LSV_DTYPE_BF16) {
-    w.o_part = (float*)take(sizeof(float) * (size_t)v.n_chunks * max_rows * s.nq * s.hd);
-    w.ml_part = (float*)take(sizeof(float) * (size_t)v.n_chunks * max_rows * s.nq * 2);
+    w.o_part = (float*)take(sizeof(float) * (size_t)v.attn.n_splits * max_rows * s.nq * s.hd);
+    w.ml_part = (float*)take(sizeof(float) * (size_t)v.attn.n_splits * max_rows * s.nq * 2);
   } else {
     w.o_part = w.ml_part = nullptr;
   }
-  w.counters = (int*)take(sizeof(int) * (size_t)v.max_groups);
   w.total = off;
   return w;
 }
@@ -140,12 +118,12 @@ static VerifyWs carve_verify(const Shape& s, const ModelLayout& ml, const Verify
 size_t verify_workspace_bytes(const Shape& s, int batch, int max_rows, int max_ctx) {
   (void)batch;
   ModelLayout ml = model_layout(s);
-  VerifyPlan v = plan_verify(s, ml, max_rows, max_ctx);
+  VerifyPlan v = plan_verify(s, batch, max_rows, max_ctx);
   return carve_verify(s, ml, v, max_rows, nullptr).total;
 }
 
 // ------------------------------------------------------------------ embedding
-// h[m] = E[token_m] (fp32) and per-64-column sums of squares for the first RMSNorm.
+// h[m] = E[token_m] (fp32) and per-16-column sums of squares for the first RMSNorm.
 // Workgroup 0 also validates every sequence: token ids in range and the block
 // within max_ctx.  Invalid tokens embed as zeros.
 template <typename T>
@@ -172,29 +150,49 @@ __global__ void __launch_bounds__(256) embed_kernel(const T* __restrict__ E, int
   const int tok_in = GL(tokens)[m];
   const bool ok = tok_in >= 0 && tok_in < V;
   const int tok = ok ? tok_in : 0;  // invalid ids read row 0 and are zeroed below
-  for (int p = threadIdx.x; p < d / 64; p += blockDim.x) {
-    float ss = 0.f;
-#pragma unroll 8
-    for (int j = 0; j < 64; ++j) {
-      const int k = 64 * p + j;
-      const T ld = GL(E)[(size_t)tok * d + k];
-      const T e = ok ? ld : from_f32<T>(0.f);
-      const float x = to_f32<T>(e);
-      GL(h)[(size_t)m * d + k] = x;
-      if (hx) GL(hx)[(size_t)m * d + k] = e;
-      ss += x * x;
+  // one 16-column group per thread: 16-byte loads and stores, the group's sum of squares
+  constexpr int PER16 = 16 * sizeof(T) / 16;  // 16-byte pieces per 16 elements
+  const GLOBAL u32x4_t* src = (const GLOBAL u32x4_t*)(GL(E) + (size_t)tok * d);
+  for (int p = threadIdx.x; p < d / 16; p += blockDim.x) {
+    u32x4_t raw[PER16];
+#pragma unroll
+    for (int i = 0; i < PER16; ++i) {
+      const u32x4_t v = src[p * PER16 + i];
+      raw[i] = ok ? v : u32x4_t{0u, 0u, 0u, 0u};
     }
-    GL(stats)[(size_t)p * M_max + m] = ss;
+    float x[16];
+#pragma unroll
+    for (int i = 0; i < PER16; ++i)
+#pragma unroll
+      for (int e = 0; e < 16 / PER16; ++e) {
+        if (sizeof(T) == 2) {
+          const uint32_t w = raw[i][e >> 1];
+          x[i * 8 + e] = __uint_as_float((e & 1) ? (w & 0xffff0000u) : (w << 16));
+        } else {
+          x[i * 4 + e] = __uint_as_float(raw[i][e]);
+        }
+      }
+    float ss = 0.f;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) ss += x[e] * x[e];
+    GLOBAL f32x4_t* hp = (GLOBAL f32x4_t*)(GL(h) + (size_t)m * d + 16 * p);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) hp[i] = f32x4_t{x[4 * i], x[4 * i + 1], x[4 * i + 2], x[4 * i + 3]};
+    if (hx) {
+      GLOBAL u32x4_t* xp = (GLOBAL u32x4_t*)(GL(hx) + (size_t)m * d + 16 * p);
+#pragma unroll
+      for (int i = 0; i < PER16; ++i) xp[i] = raw[i];
+    }
+    GL(stats)[(size_t)m * (d / 16) + p] = ss;
   }
 }
 
 int launch_verify(const Shape& s, const ModelLayout& ml, const void* packed, void* kv, int capacity, int batch,
                   const int32_t* seq_len, const int32_t* tokens, const int32_t* row_offsets, int max_rows,
                   int max_ctx, float* logits, int32_t* status, void* ws, size_t ws_bytes, hipStream_t st) {
-  const VerifyPlan v = plan_verify(s, ml, max_rows, max_ctx);
+  const VerifyPlan v = plan_verify(s, batch, max_rows, max_ctx);
   const VerifyWs w = carve_verify(s, ml, v, max_rows, ws);
   if (w.total > ws_bytes) return LSV_ERR_INVALID_ARG;
-  if (v.part_floats * sizeof(float) >= ((size_t)1 << 31)) return LSV_ERR_UNSUPPORTED;  // 32-bit buffer offsets
   const char* P = (const char*)packed;
   const bool bf16 = s.dtype == LSV_DTYPE_BF16;
 
@@ -212,10 +210,8 @@ int launch_verify(const Shape& s, const ModelLayout& ml, const void* packed, voi
   base.batch = batch;
   base.row_offsets = row_offsets;
   base.stats = w.stats;
-  base.P = s.d / 64;
+  base.P = s.d / 16;
   base.eps = s.eps;
-  base.part = w.part;
-  base.counters = w.counters;
   base.seq_len = seq_len;
   base.kv = kv;
   base.capacity = capacity;
@@ -227,18 +223,14 @@ int launch_verify(const Shape& s, const ModelLayout& ml, const void* packed, voi
   base.ldu = w.ldu;
 
   auto gemm = [&](GemmKind kind, const PackedMat& pm, const char* layer_base, GemmArgs a) {
-    const GemmPlan& p = v.g[kind];
     a.W = (const uint4*)(layer_base + pm.offset);
     a.N = pm.N;
     a.K = pm.K;
     a.Nt = pm.Nt;
     a.Kt = pm.Kt;
-    a.groups = p.groups;
-    a.cmax = p.cmax;
-    a.part_bytes = sizeof(float) * v.part_floats;
     const int idx = kind == GEMM_LMHEAD ? 0 : a.layer_index;
     timing_before((int)kind, idx, st);
-    const int rc = launch_gemm(s.dtype, kind, v.MT, a, p, st);
+    const int rc = launch_gemm(s.dtype, kind, v.MT, a, st);
     timing_after((int)kind, idx, st);
     return rc;
   };
@@ -272,8 +264,10 @@ int launch_verify(const Shape& s, const ModelLayout& ml, const void* packed, voi
     at.ml_part = w.ml_part;
     at.out = w.attn;
     at.scale_log2 = (float)(1.4426950408889634 / sqrt((double)s.hd));
+    at.n_splits = v.attn.n_splits;
+    at.chunks_per_split = v.attn.chunks_per_split;
     timing_before(LSV_KERNEL_ATTENTION, l, st);
-    if ((rc = launch_attention(s.dtype, s.hd, at, max_rows, v.n_chunks, st)) != LSV_OK) return rc;
+    if ((rc = launch_attention(s.dtype, s.hd, at, max_rows, st)) != LSV_OK) return rc;
     timing_after(LSV_KERNEL_ATTENTION, l, st);
     // O projection + residual
     a = base;

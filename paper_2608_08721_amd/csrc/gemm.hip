@@ -8,28 +8,25 @@
 // fragment is the A operand of v_mfma_f32_16x16x32_bf16 (fp32: four
 // v_mfma_f32_16x16x4_f32), weight rows being the MFMA rows.  The B operand --
 // activation rows as MFMA columns -- is read the same way straight from the
-// (L2-resident) activation buffer: no LDS staging, no barrier in front of the
-// stream, every wave runs its own two-stage software pipeline.  The k order
-// inside a fragment is any permutation shared by A and B.
+// (L2-resident) activation buffer.  The k order inside a fragment is any
+// permutation shared by A and B.
 //
 // RMSNorm: rmsnorm(h) g W^T = inv_rms[m] * (h (W o g)^T).  The gain g is folded
-// into W when packing, the producer of h writes a bf16 copy of h and per-64-
-// column sums of squares, and the consumer scales row m by inv_rms[m] in its
-// epilogue.
+// into W when packing, the producer of h writes a storage-type copy of h and
+// per-16-column sums of squares, and the consumer scales row m by inv_rms[m] in
+// its epilogue.
 //
-// Work split (stream-K): a workgroup of 4 waves processes "steps" = one k-fragment
-// of a tile group (4 waves x TPW fragment rows = 64*TPW output columns).  The
-// groups x Kt steps are cut into gridDim.x equal contiguous ranges, so every
-// workgroup streams the same number of bytes and the launch has no tail round.
-// A group covered by one workgroup runs its epilogue directly; otherwise each
-// contributor publishes an fp32 partial with 16-byte device-scope stores and bumps
-// a device-scope counter, and the last to arrive reads the partials back (device
-// scope) in k order -- deterministic -- and runs the epilogue.  Device-scope
-// accesses go through the coherent path, so no cache write-back is needed between
-// a contributor and the reducer.
+// Work split: a workgroup owns one tile of TPW fragment rows (16*TPW output columns)
+// over the whole K.  Its KS waves take balanced contiguous k-slices, each running its
+// own software pipeline of NS stages x U k-steps; the slices meet in LDS and wave 0
+// adds them in slice order (deterministic) and runs the epilogue.  No data crosses
+// workgroups, so there are no partial buffers, counters or fences.  The residual a
+// tile adds to is loaded ahead of the weight stream; inputs that need dependent loads
+// (1/rms, cache positions) are read in the epilogue.
 #include <math.h>
 
 #include "lsv_device.h"
+#include "lsv_attn.h"
 #include "lsv_gemm.h"
 
 namespace lsv {
@@ -129,48 +126,61 @@ LSV_DEV u32x2_t pack_bf16x4(const f32x4_t v) {
 LSV_DEV void store4(float* p, const f32x4_t v) { *(GLOBAL f32x4_t*)p = v; }
 LSV_DEV void store4(bf16_t* p, const f32x4_t v) { *(GLOBAL u32x2_t*)p = pack_bf16x4(v); }
 
-// 1 / rms of activation row m from the producer's per-64-column sums of squares.
-// The four lanes sharing (lane & 15) split the partials (p = g, g+4, ...) and
-// combine them with a fixed shuffle tree: deterministic and the same in every lane.
-// All loads are issued before the first use (P <= kMaxStatParts), then summed in order.
-constexpr int kMaxStatParts = 128;  // d_model <= 8192
+constexpr int kMaxStatParts = 512;  // d_model / 16 for d_model <= 8192
+
+// 1 / rms of activation row m from the producer's per-16-column sums of squares
+// (stats[m][0..P)).  The four lanes sharing (lane & 15) take every fourth float4 of
+// the row and combine their sums with a fixed shuffle tree: deterministic and the
+// same in every lane.
 LSV_DEV float inv_rms_of_row(const GemmArgs& a, int m, int g4) {
-  const GLOBAL float* st = GL(a.stats) + (m < a.M_max ? m : 0);
-  float v[kMaxStatParts / 4];
+  const GLOBAL f32x4_t* st = (const GLOBAL f32x4_t*)(a.stats + (size_t)min(m, a.M_max - 1) * a.P);
+  const int P4 = a.P >> 2;  // float4s per row (P is a multiple of 4)
+  f32x4_t v[kMaxStatParts / 16];
 #pragma unroll
-  for (int j = 0; j < kMaxStatParts / 4; ++j) {
-    const int p = g4 + 4 * j;
-    v[j] = p < a.P ? st[(size_t)min(p, a.P - 1) * a.M_max] : 0.f;
+  for (int j = 0; j < kMaxStatParts / 16; ++j) {
+    const int i = g4 + 4 * j;
+    v[j] = i < P4 ? st[i] : f32x4_t{0.f, 0.f, 0.f, 0.f};
   }
   float ss = 0.f;
 #pragma unroll
-  for (int j = 0; j < kMaxStatParts / 4; ++j) ss += v[j];
+  for (int j = 0; j < kMaxStatParts / 16; ++j) ss += ((v[j][0] + v[j][1]) + v[j][2]) + v[j][3];
   ss += __shfl_xor(ss, 16, kWave);
   ss += __shfl_xor(ss, 32, kWave);
   return 1.0f / sqrtf(ss / (float)a.K + a.eps);
 }
 
 // ------------------------------------------------------------------ the GEMM
-// Raw buffer resource over the partials (word 3 = the gfx9-family raw-buffer format).
-LSV_DEV __amdgpu_buffer_rsrc_t part_rsrc(float* base, size_t bytes) {
-  return __builtin_amdgcn_make_buffer_rsrc(base, 0, (int)(bytes > 0x7fffffffu ? 0x7fffffffu : bytes), 0x00020000);
-}
-constexpr int kDeviceScope = 16;  // buffer cache policy: sc1 (coherent at device scope)
-
-// Which workgroup's step range contains step i (ranges start at floor(w T / W)).
-LSV_DEV int owner_of(long long i, long long T, int W) { return (int)(((i + 1) * W - 1) / T); }
-
-template <typename T, int MT, int TPW, int EPI, int ROWS_SH>
-LSV_DEV void gemm_body(const GemmArgs& a, const int M, float (*red)[ROWS_SH], int& flag) {
+template <typename T, int MT, int TPW, int KS, int U, int NS, int EPI, int MT_MAX>
+LSV_DEV void gemm_body(const GemmArgs& a, const int M, f32x4_t (*red)[TPW][MT_MAX][kWave]) {
   constexpr int KT = FragTraits<T>::KT, EPL = FragTraits<T>::EPL;
-  constexpr int WAVES = 4, U = 4;  // U k-steps per pipeline stage
   constexpr bool RMS = EPI != EPI_RESID;  // consumer of a normalised activation
-  constexpr int ROWS = MT * 16, GCOLS = 64 * TPW;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, l16 = lane & 15, g4 = lane >> 4;
-  const int W = gridDim.x, w = blockIdx.x;
-  const long long Tsteps = (long long)a.groups * a.Kt;
-  const long long s_begin = (long long)w * Tsteps / W, s_end = (long long)(w + 1) * Tsteps / W;
+  // this workgroup: fragment rows tn0 .. tn0+TPW-1 over the whole K; wave = k-slice
+  const int tn0 = blockIdx.x * TPW;
+  const int k0 = (int)((long long)wave * a.Kt / KS), k1 = (int)((long long)(wave + 1) * a.Kt / KS);
+  const int nk = k1 - k0;  // >= 0, and k0 < Kt for every wave
+  bool tvalid[TPW];
+  const GLOBAL u32x4_t* wp[TPW];
+#pragma unroll
+  for (int t = 0; t < TPW; ++t) {
+    tvalid[t] = tn0 + t < a.Nt;
+    wp[t] = (const GLOBAL u32x4_t*)a.W + ((size_t)(tvalid[t] ? tn0 + t : 0) * a.Kt + k0) * 64 + lane;
+  }
 
+  // ---- the residual this tile adds to (EPI_RESID, wave 0 runs the epilogue): its loads are
+  // issued ahead of the weight stream and retire with it
+  f32x4_t hpre[TPW][MT];
+  if (EPI == EPI_RESID && wave == 0) {
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+      const int m = min(mt * 16 + l16, a.M_max - 1);
+#pragma unroll
+      for (int t = 0; t < TPW; ++t) {
+        const int n0 = (tvalid[t] ? tn0 + t : 0) * 16 + 4 * g4;
+        hpre[t][mt] = *(const GLOBAL f32x4_t*)(a.h_out + (size_t)m * a.N + n0);
+      }
+    }
+  }
 
   // B operand: activation rows (clamped into the buffer; columns of rows >= M are never
   // stored, so their contents do not matter)
@@ -178,53 +188,33 @@ LSV_DEV void gemm_body(const GemmArgs& a, const int M, float (*red)[ROWS_SH], in
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt) {
     const int m = min(mt * 16 + l16, a.M_max - 1);
-    xp[mt] = (const GLOBAL T*)a.x + (size_t)m * a.ldx + g4 * EPL;
+    xp[mt] = (const GLOBAL T*)a.x + (size_t)m * a.ldx + (size_t)k0 * KT + g4 * EPL;
   }
-  float inv[MT];  // computed at the first epilogue, off the weight stream's critical path
-  bool inv_ready = false;
-  const __amdgpu_buffer_rsrc_t prs = part_rsrc(a.part, a.part_bytes);
 
-  for (long long g = s_begin / a.Kt; g * a.Kt < s_end; ++g) {
-    const int k0 = (int)(max(s_begin, g * a.Kt) - g * a.Kt), k1 = (int)(min(s_end, (g + 1) * a.Kt) - g * a.Kt);
-    const int nk = k1 - k0;
-    const int tn0 = ((int)g * WAVES + wave) * TPW;
-    bool tvalid[TPW];
-    const GLOBAL u32x4_t* wp[TPW];
+  f32x4_t acc[TPW][MT];
 #pragma unroll
-    for (int t = 0; t < TPW; ++t) {
-      tvalid[t] = tn0 + t < a.Nt;
-      wp[t] = (const GLOBAL u32x4_t*)a.W + ((size_t)(tvalid[t] ? tn0 + t : 0) * a.Kt + k0) * 64 + lane;
-    }
-    // Every load hits an in-bounds fragment (index clamped): a conditional load would become
-    // a select between addresses and a generic access.  Steps past the range are never used.
-    u32x4_t wa[2][U][TPW], xb[2][U][MT];
+  for (int t = 0; t < TPW; ++t)
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) acc[t][mt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  {
+    // NS pipeline stages of U k-steps.  Every load hits an in-bounds fragment (index
+    // clamped): a conditional load would become a select between addresses and a generic
+    // access.  Steps past the range re-read the last one and are never used.
+    u32x4_t wa[NS][U][TPW], xb[NS][U][MT];
     auto load_stage = [&](int st, int kb) {
 #pragma unroll
       for (int u = 0; u < U; ++u) {
-        const int kf = min(kb + u, nk - 1);
+        const int kf = max(min(kb + u, nk - 1), 0);  // a slice may be empty when Kt < KS
 #pragma unroll
         for (int t = 0; t < TPW; ++t) wa[st][u][t] = wp[t][(size_t)kf * 64];
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt) xb[st][u][mt] = *(const GLOBAL u32x4_t*)(xp[mt] + (size_t)(k0 + kf) * KT);
+        for (int mt = 0; mt < MT; ++mt) xb[st][u][mt] = *(const GLOBAL u32x4_t*)(xp[mt] + (size_t)kf * KT);
       }
     };
-    f32x4_t acc[TPW][MT];
-#pragma unroll
-    for (int t = 0; t < TPW; ++t)
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt) acc[t][mt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-    auto compute_stage = [&](int st) {  // all U steps, no per-step conditions
+    auto compute_stage = [&](int st, int kb, bool tail) {
 #pragma unroll
       for (int u = 0; u < U; ++u)
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-          for (int t = 0; t < TPW; ++t) mfma_frag(wa[st][u][t], xb[st][u][mt], acc[t][mt], T{});
-    };
-    auto compute_tail = [&](int st, int kb) {  // the last (< 2U) steps
-#pragma unroll
-      for (int u = 0; u < U; ++u)
-        if (kb + u < nk)
+        if (!tail || kb + u < nk)
 #pragma unroll
           for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
@@ -232,90 +222,80 @@ LSV_DEV void gemm_body(const GemmArgs& a, const int M, float (*red)[ROWS_SH], in
     };
     // Scheduling barriers keep the loads issued -- and so retired, vmcnt counting in
     // order -- stage by stage, and the loop body has no branches: while one stage is
-    // multiplied the other is in flight.  Loads past the range re-read the last step.
-    const int nfull = nk - nk % (2 * U);
-    load_stage(0, 0);
-    __builtin_amdgcn_sched_barrier(0);
-    load_stage(1, U);
-    __builtin_amdgcn_sched_barrier(0);
-    for (int kb = 0; kb < nfull; kb += 2 * U) {
-      compute_stage(0);
-      __builtin_amdgcn_sched_barrier(0);
-      load_stage(0, kb + 2 * U);
-      __builtin_amdgcn_sched_barrier(0);
-      compute_stage(1);
-      __builtin_amdgcn_sched_barrier(0);
-      load_stage(1, kb + 3 * U);
+    // multiplied the later ones are in flight.
+    const int nfull = nk - nk % (NS * U);
+#pragma unroll
+    for (int st = 0; st < NS; ++st) {
+      load_stage(st, st * U);
       __builtin_amdgcn_sched_barrier(0);
     }
-    compute_tail(0, nfull);
-    compute_tail(1, nfull + U);
+    for (int kb = 0; kb < nfull; kb += NS * U) {
+#pragma unroll
+      for (int st = 0; st < NS; ++st) {
+        compute_stage(st, kb + st * U, false);
+        __builtin_amdgcn_sched_barrier(0);
+        load_stage(st, kb + (NS + st) * U);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+#pragma unroll
+    for (int st = 0; st < NS; ++st) compute_stage(st, nfull + st * U, true);
+  }
 
-    // ---- groups shared with other workgroups: device-scope partials, last arrival reduces
-    const int first = owner_of(g * a.Kt, Tsteps, W), last = owner_of(g * a.Kt + a.Kt - 1, Tsteps, W);
-    const int contributors = last - first + 1;
-    if (contributors > 1) {
-      const size_t slot = (size_t)g * a.cmax + (w - first);
+  // ---- k-slices: waves 1.. hand their sums to wave 0 through LDS; summed in slice order
+  if (KS > 1) {
+    if (wave > 0) {
 #pragma unroll
       for (int t = 0; t < TPW; ++t)
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt) {
-          const int m = mt * 16 + l16, col = (wave * TPW + t) * 16 + 4 * g4;
-          if (m < M) {
-            const int off = (int)(((slot * a.M_max + m) * GCOLS + col) * sizeof(float));
-            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4_t, acc[t][mt]), prs, off, 0, kDeviceScope);
-          }
-        }
-      __builtin_amdgcn_s_waitcnt(0);  // this thread's partials have reached the coherent level
-      __syncthreads();
-      if (threadIdx.x == 0)
-        flag = __hip_atomic_fetch_add(&a.counters[g], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == contributors - 1;
-      __syncthreads();
-      const bool is_last = flag != 0;
-      __syncthreads();  // flag is rewritten by the next group
-      if (!is_last) continue;
-#pragma unroll
-      for (int t = 0; t < TPW; ++t)
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt) {
-          const int m = mt * 16 + l16, col = (wave * TPW + t) * 16 + 4 * g4;
-          f32x4_t sum = f32x4_t{0.f, 0.f, 0.f, 0.f};
-          if (m < M) {
-            for (int j = 0; j < contributors; ++j) {
-              const size_t sl = (size_t)g * a.cmax + j;
-              const int off = (int)(((sl * a.M_max + m) * GCOLS + col) * sizeof(float));
-              sum += __builtin_bit_cast(f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(prs, off, 0, kDeviceScope));
-            }
-          }
-          acc[t][mt] = sum;
-        }
-      if (threadIdx.x == 0) __hip_atomic_store(&a.counters[g], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        for (int mt = 0; mt < MT; ++mt) red[wave - 1][t][mt][lane] = acc[t][mt];
     }
+    __syncthreads();
+    if (wave > 0) return;
+#pragma unroll
+    for (int w = 1; w < KS; ++w)
+#pragma unroll
+      for (int t = 0; t < TPW; ++t)
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) acc[t][mt] += red[w - 1][t][mt][lane];
+  }
 
-    // ---- epilogues; lane holds output columns n0..n0+3 (weight rows) of activation row m
-    if (RMS && !inv_ready) {
+  // ---- epilogues (wave 0); lane holds output columns n0..n0+3 (weight rows) of activation row m.
+  // Row inputs that need dependent loads (1/rms, cache positions) are read here, off the
+  // weight stream's critical path.
+  float inv[MT];
+  if (RMS) {
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt) inv[mt] = inv_rms_of_row(a, mt * 16 + l16, g4);
-      inv_ready = true;
+    for (int mt = 0; mt < MT; ++mt) inv[mt] = inv_rms_of_row(a, mt * 16 + l16, g4);
+  }
+  int qkv_b[MT], qkv_pos[MT];
+  if (EPI == EPI_QKV) {
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+      const int m = min(mt * 16 + l16, a.M_max - 1);
+      const int b = seq_of_row(a.row_offsets, a.batch, m);
+      qkv_b[mt] = b;
+      qkv_pos[mt] = GL(a.seq_len)[b] + (m - GL(a.row_offsets)[b]);
     }
-    if (EPI == EPI_LOGITS) {
+  }
+  if (EPI == EPI_LOGITS) {
 #pragma unroll
-      for (int t = 0; t < TPW; ++t)
+    for (int t = 0; t < TPW; ++t)
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt) {
-          const int m = mt * 16 + l16, n0 = (tn0 + t) * 16 + 4 * g4;
-          if (m >= M || !tvalid[t]) continue;
-          const f32x4_t v = acc[t][mt] * inv[mt];
-          GLOBAL float* o = GL(a.out_f32) + (size_t)m * a.ldo;
-          if (n0 + 3 < a.N && (a.ldo & 3) == 0) {
-            *(GLOBAL f32x4_t*)(o + n0) = v;
-          } else {
+      for (int mt = 0; mt < MT; ++mt) {
+        const int m = mt * 16 + l16, n0 = (tn0 + t) * 16 + 4 * g4;
+        if (m >= M || !tvalid[t]) continue;
+        const f32x4_t v = acc[t][mt] * inv[mt];
+        GLOBAL float* o = GL(a.out_f32) + (size_t)m * a.ldo;
+        if (n0 + 3 < a.N && (a.ldo & 3) == 0) {
+          *(GLOBAL f32x4_t*)(o + n0) = v;
+        } else {
 #pragma unroll
-            for (int r = 0; r < 4; ++r)
-              if (n0 + r < a.N) o[n0 + r] = v[r];
-          }
+          for (int r = 0; r < 4; ++r)
+            if (n0 + r < a.N) o[n0 + r] = v[r];
         }
-    } else if (EPI == EPI_QKV) {
+      }
+  } else if (EPI == EPI_QKV) {
       const int qrows = a.nq * a.hd, krows = a.nkv * a.hd;
 #pragma unroll
       for (int t = 0; t < TPW; ++t)
@@ -323,8 +303,7 @@ LSV_DEV void gemm_body(const GemmArgs& a, const int M, float (*red)[ROWS_SH], in
         for (int mt = 0; mt < MT; ++mt) {
           const int m = mt * 16 + l16, n0 = (tn0 + t) * 16 + 4 * g4;
           if (m >= M || !tvalid[t] || n0 >= qrows + 2 * krows) continue;
-          const int b = seq_of_row(a.row_offsets, a.batch, m);
-          const int pos = GL(a.seq_len)[b] + (m - GL(a.row_offsets)[b]);
+          const int b = qkv_b[mt], pos = qkv_pos[mt];
           const f32x4_t v = acc[t][mt] * inv[mt];
           if (n0 < qrows + krows) {
             const bool isq = n0 < qrows;
@@ -359,16 +338,19 @@ LSV_DEV void gemm_body(const GemmArgs& a, const int M, float (*red)[ROWS_SH], in
             gd[i0 + 1 + a.hd / 2] = from_f32<T>(out[3]);
           } else {
             if (pos < 0 || pos >= a.capacity) continue;
+            // V rows are stored transposed: [head_dim][capacity], column v_column(pos)
             const int local = n0 - qrows - krows;
             const int head = local / a.hd, d0 = local % a.hd;
-            T* dst = (T*)a.kv + ((((size_t)a.layer * 2 + 1) * a.batch + b) * a.nkv + head) * (size_t)a.capacity * a.hd +
-                     (size_t)pos * a.hd + d0;
-            store4(dst, v);
+            GLOBAL T* dst = GL((T*)a.kv) +
+                            ((((size_t)a.layer * 2 + 1) * a.batch + b) * a.nkv + head) * (size_t)a.capacity * a.hd +
+                            (size_t)d0 * a.capacity + v_column(pos);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) dst[(size_t)r * a.capacity] = from_f32<T>(v[r]);
           }
         }
     } else if (EPI == EPI_RESID) {
-      // h += y; the storage-type copy of h for the next consumer; per-row sums of squares of
-      // the new h over each 64-column group
+      // h += y; the storage-type copy of h for the next consumer; per-row sum of squares of
+      // the new h over this fragment row's 16 columns (stats[m][n / 16])
 #pragma unroll
       for (int t = 0; t < TPW; ++t)
 #pragma unroll
@@ -376,28 +358,15 @@ LSV_DEV void gemm_body(const GemmArgs& a, const int M, float (*red)[ROWS_SH], in
           const int m = mt * 16 + l16, n0 = (tn0 + t) * 16 + 4 * g4;
           float ss = 0.f;
           if (m < M && tvalid[t]) {
-            GLOBAL f32x4_t* hp = (GLOBAL f32x4_t*)(a.h_out + (size_t)m * a.N + n0);
-            const f32x4_t h4 = *hp + acc[t][mt];
-            *hp = h4;
+            const f32x4_t h4 = hpre[t][mt] + acc[t][mt];
+            *(GLOBAL f32x4_t*)(a.h_out + (size_t)m * a.N + n0) = h4;
             if (a.hx_out) store4((T*)a.hx_out + (size_t)m * a.N + n0, h4);
             ss = ((h4[0] * h4[0] + h4[1] * h4[1]) + h4[2] * h4[2]) + h4[3] * h4[3];
           }
           ss += __shfl_xor(ss, 16, kWave);
           ss += __shfl_xor(ss, 32, kWave);
-          if (lane < 16) red[wave * TPW + t][mt * 16 + lane] = ss;
+          if (g4 == 0 && m < M && tvalid[t]) GL(a.stats_out)[(size_t)m * (a.N / 16) + tn0 + t] = ss;
         }
-      __syncthreads();
-      // 64-column groups: tiles 4p..4p+3 of this tile group, summed in order
-      constexpr int PARTS = WAVES * TPW / 4;
-      for (int i = threadIdx.x; i < PARTS * ROWS; i += blockDim.x) {
-        const int p = i / ROWS, m = i % ROWS;
-        if (m >= M) continue;
-        const int gp = (int)g * PARTS + p;
-        if (gp * 64 >= a.N) continue;
-        const float sm = ((red[4 * p + 0][m] + red[4 * p + 1][m]) + red[4 * p + 2][m]) + red[4 * p + 3][m];
-        GL(a.stats_out)[(size_t)gp * a.M_max + m] = sm;
-      }
-      __syncthreads();  // red is rewritten by the next group
     } else if (EPI == EPI_SWIGLU) {
       static_assert(EPI != EPI_SWIGLU || TPW == 2, "SwiGLU pairs a gate and an up fragment row");
 #pragma unroll
@@ -419,78 +388,81 @@ LSV_DEV void gemm_body(const GemmArgs& a, const int M, float (*red)[ROWS_SH], in
         }
       }
     }
-  }
 }
 
+// Launch configuration of each product: fragment rows per wave (TPW), k-slices = waves
+// per workgroup (KS), k-steps per pipeline stage (U) and stages in flight (NS).  Chosen by
+// measurement on the Llama-3-8B shapes: enough bytes in flight per compute unit, a wave
+// count that spreads evenly over the 256 compute units, and few waves per tile for the
+// long products.
+template <int KIND> struct GemmCfg;
+template <> struct GemmCfg<GEMM_QKV> { static constexpr int TPW = 1, KS = 2, U = 8, NS = 2, EPI = EPI_QKV; };
+template <> struct GemmCfg<GEMM_O> { static constexpr int TPW = 1, KS = 4, U = 8, NS = 2, EPI = EPI_RESID; };
+template <> struct GemmCfg<GEMM_GATEUP> { static constexpr int TPW = 2, KS = 1, U = 4, NS = 3, EPI = EPI_SWIGLU; };
+template <> struct GemmCfg<GEMM_DOWN> { static constexpr int TPW = 1, KS = 4, U = 8, NS = 2, EPI = EPI_RESID; };
+template <> struct GemmCfg<GEMM_LMHEAD> { static constexpr int TPW = 2, KS = 1, U = 4, NS = 3, EPI = EPI_LOGITS; };
+
+// Wide activation tiles (prefill bounds) use a shallower pipeline to stay in registers.
+template <int KIND, int MT_MAX> struct GemmShape {
+  using C = GemmCfg<KIND>;
+  static constexpr int TPW = C::TPW, KS = C::KS, EPI = C::EPI;
+  static constexpr int U = MT_MAX <= 2 ? C::U : 4, NS = MT_MAX <= 2 ? C::NS : 2;
+};
 
 // The host bound on rows fixes MT_MAX; the kernel runs the body for the activation
 // tiles that the device row count actually needs, so a generous bound costs nothing.
-template <typename T, int MT_MAX, int TPW, int EPI>
-__global__ void __launch_bounds__(256) gemm_kernel(GemmArgs a) {
-  __shared__ float red[4 * TPW][MT_MAX * 16];  // residual epilogue: per-16-column sums of squares
-  __shared__ int flag;
+template <typename T, int KIND, int MT_MAX>
+__global__ void __launch_bounds__(64 * GemmCfg<KIND>::KS) gemm_kernel(GemmArgs a) {
+  using S = GemmShape<KIND, MT_MAX>;
+  __shared__ f32x4_t red[S::KS > 1 ? S::KS - 1 : 1][S::TPW][MT_MAX][kWave];  // k-slice sums
   const int M = min(GL(a.row_offsets)[a.batch], a.M_max);  // never trust device rows beyond the host bound
   const int mt = M <= 16 ? 1 : (M <= 32 ? 2 : (M <= 48 ? 3 : 4));
-  if (mt <= 1 || MT_MAX == 1) gemm_body<T, 1, TPW, EPI, MT_MAX * 16>(a, M, red, flag);
-  else if (mt == 2 || MT_MAX == 2) gemm_body<T, (MT_MAX >= 2 ? 2 : 1), TPW, EPI, MT_MAX * 16>(a, M, red, flag);
-  else if (mt == 3 || MT_MAX == 3) gemm_body<T, (MT_MAX >= 3 ? 3 : 1), TPW, EPI, MT_MAX * 16>(a, M, red, flag);
-  else gemm_body<T, MT_MAX, TPW, EPI, MT_MAX * 16>(a, M, red, flag);
+  if (mt <= 1 || MT_MAX == 1)
+    gemm_body<T, 1, S::TPW, S::KS, S::U, S::NS, S::EPI, MT_MAX>(a, M, red);
+  else if (mt == 2 || MT_MAX == 2)
+    gemm_body<T, (MT_MAX >= 2 ? 2 : 1), S::TPW, S::KS, S::U, S::NS, S::EPI, MT_MAX>(a, M, red);
+  else if (mt == 3 || MT_MAX == 3)
+    gemm_body<T, (MT_MAX >= 3 ? 3 : 1), S::TPW, S::KS, S::U, S::NS, S::EPI, MT_MAX>(a, M, red);
+  else
+    gemm_body<T, MT_MAX, S::TPW, S::KS, S::U, S::NS, S::EPI, MT_MAX>(a, M, red);
 }
 
 // ------------------------------------------------------------------ planning and launch
-GemmPlan plan_gemm(int Nt, int Kt, int TPW, int want_wgs, int min_steps_per_wg) {
-  GemmPlan p;
-  p.groups = (Nt + 4 * TPW - 1) / (4 * TPW);
-  const long long T = (long long)p.groups * Kt;
-  long long W = want_wgs;
-  if (W > T / min_steps_per_wg) W = T / min_steps_per_wg;
-  if (W < 1) W = 1;
-  p.wgs = (int)W;
-  // largest number of workgroups sharing one tile group
-  p.cmax = 1;
-  for (int g = 0; g < p.groups; ++g) {
-    const long long i0 = (long long)g * Kt, i1 = i0 + Kt - 1;
-    const int c = (int)(((i1 + 1) * W - 1) / T - ((i0 + 1) * W - 1) / T) + 1;
-    p.cmax = c > p.cmax ? c : p.cmax;
-  }
-  return p;
+template <typename T, int KIND, int MT_MAX>
+static void launch_one(const GemmArgs& a, hipStream_t st) {
+  constexpr int TPW = GemmCfg<KIND>::TPW, KS = GemmCfg<KIND>::KS;
+  const int tiles = (a.Nt + TPW - 1) / TPW;
+  hipLaunchKernelGGL((gemm_kernel<T, KIND, MT_MAX>), dim3(tiles), dim3(64 * KS), 0, st, a);
 }
 
-template <typename T, int MT, int TPW, int EPI>
-static void launch_one(const GemmArgs& a, const GemmPlan& p, hipStream_t st) {
-  hipLaunchKernelGGL((gemm_kernel<T, MT, TPW, EPI>), dim3(p.wgs), dim3(256), 0, st, a);
-}
-
-template <typename T, int TPW, int EPI>
-static int launch_mt(int MT, const GemmArgs& a, const GemmPlan& p, hipStream_t st) {
+template <typename T, int KIND>
+static int launch_mt(int MT, const GemmArgs& a, hipStream_t st) {
   switch (MT) {
-    case 1: launch_one<T, 1, TPW, EPI>(a, p, st); break;
-    case 2: launch_one<T, 2, TPW, EPI>(a, p, st); break;
-    case 3: launch_one<T, 3, TPW, EPI>(a, p, st); break;
-    case 4: launch_one<T, 4, TPW, EPI>(a, p, st); break;
+    case 1: launch_one<T, KIND, 1>(a, st); break;
+    case 2: launch_one<T, KIND, 2>(a, st); break;
+    case 3: launch_one<T, KIND, 3>(a, st); break;
+    case 4: launch_one<T, KIND, 4>(a, st); break;
     default: return LSV_ERR_UNSUPPORTED;
   }
   return LSV_OK;
 }
 
 template <typename T>
-static int launch_typed(GemmKind kind, int MT, const GemmArgs& a, const GemmPlan& p, hipStream_t st) {
+static int launch_typed(GemmKind kind, int MT, const GemmArgs& a, hipStream_t st) {
   switch (kind) {
-    case GEMM_QKV: return launch_mt<T, 1, EPI_QKV>(MT, a, p, st);
-    case GEMM_O: return launch_mt<T, 1, EPI_RESID>(MT, a, p, st);
-    case GEMM_GATEUP: return launch_mt<T, 2, EPI_SWIGLU>(MT, a, p, st);
-    case GEMM_DOWN: return launch_mt<T, 1, EPI_RESID>(MT, a, p, st);
-    case GEMM_LMHEAD: return launch_mt<T, 1, EPI_LOGITS>(MT, a, p, st);
+    case GEMM_QKV: return launch_mt<T, GEMM_QKV>(MT, a, st);
+    case GEMM_O: return launch_mt<T, GEMM_O>(MT, a, st);
+    case GEMM_GATEUP: return launch_mt<T, GEMM_GATEUP>(MT, a, st);
+    case GEMM_DOWN: return launch_mt<T, GEMM_DOWN>(MT, a, st);
+    case GEMM_LMHEAD: return launch_mt<T, GEMM_LMHEAD>(MT, a, st);
   }
   return LSV_ERR_UNSUPPORTED;
 }
 
-int launch_gemm(int dtype, GemmKind kind, int MT, const GemmArgs& a, const GemmPlan& p, hipStream_t st) {
-  int rc = dtype == LSV_DTYPE_BF16 ? launch_typed<bf16_t>(kind, MT, a, p, st) : launch_typed<float>(kind, MT, a, p, st);
+int launch_gemm(int dtype, GemmKind kind, int MT, const GemmArgs& a, hipStream_t st) {
+  int rc = dtype == LSV_DTYPE_BF16 ? launch_typed<bf16_t>(kind, MT, a, st) : launch_typed<float>(kind, MT, a, st);
   if (rc != LSV_OK) return rc;
   return hipGetLastError() == hipSuccess ? LSV_OK : LSV_ERR_HIP;
 }
-
-int gemm_tpw(GemmKind kind) { return kind == GEMM_GATEUP ? 2 : 1; }
 
 }  // namespace lsv

@@ -110,7 +110,7 @@ int lsv_pack_layer(const lsv_model_config* cfg, int32_t layer, const void* d_wq,
 }
 
 size_t lsv_kv_cache_bytes(const lsv_model_config* cfg, int32_t batch, int32_t capacity) {
-  if (check_config(cfg) != LSV_OK || batch < 1 || capacity < 1) return 0;
+  if (check_config(cfg) != LSV_OK || batch < 1 || capacity < 1 || capacity % LSV_KV_ALIGN) return 0;
   const lsv::Shape s = lsv::shape_of(cfg);
   return (size_t)s.L * 2 * batch * s.nkv * (size_t)capacity * s.hd * s.es;
 }
@@ -148,6 +148,8 @@ int lsv_verify_block(const lsv_model_config* cfg, const void* d_packed, void* d_
     return fail(LSV_ERR_INVALID_ARG, "max_rows %d not in [1, %d]", max_rows, LSV_MAX_ROWS);
   if (capacity < 1 || max_ctx < 1 || max_ctx > capacity)
     return fail(LSV_ERR_INVALID_ARG, "need 1 <= max_ctx (%d) <= capacity (%d)", max_ctx, capacity);
+  if (capacity % LSV_KV_ALIGN)
+    return fail(LSV_ERR_INVALID_ARG, "capacity %d is not a multiple of %d", capacity, (int)LSV_KV_ALIGN);
   const lsv::Shape s = lsv::shape_of(cfg);
   if (s.dtype == LSV_DTYPE_F32 && max_ctx > 16384)
     return fail(LSV_ERR_UNSUPPORTED, "fp32 models support max_ctx <= 16384");

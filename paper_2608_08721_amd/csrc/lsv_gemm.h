@@ -19,21 +19,16 @@ enum GemmKind { GEMM_QKV = 0, GEMM_O = 1, GEMM_GATEUP = 2, GEMM_DOWN = 3, GEMM_L
 struct GemmArgs {
   const uint4* W;  // packed fragments
   int N, K, Nt, Kt;
-  int groups;  // tile groups of 4 waves x TPW fragment rows
   int M_max, batch;
   const int32_t* row_offsets;  // [batch+1]; rows = row_offsets[batch]
   // B operand: activation rows [M_max][ldx] in the storage type, columns >= K zero up to Kt*KT
   const void* x;
   int ldx;
-  // row scaling of normalised-activation consumers: 1/rms from [P][M_max] sums of squares
+  // row scaling of normalised-activation consumers: 1/rms from [M_max][P] sums of squares
+  // over 16-column groups (P = K / 16)
   const float* stats;
   int P;
   float eps;
-  // stream-K partials of tile groups shared by several workgroups
-  float* part;    // [groups][cmax][M_max][64*TPW]
-  size_t part_bytes;
-  int cmax;
-  int* counters;  // [groups], zero on entry and on exit
   // EPI_LOGITS
   float* out_f32;
   int ldo;
@@ -46,19 +41,14 @@ struct GemmArgs {
   // EPI_RESID
   float* h_out;      // [M][N] fp32 residual, updated in place
   void* hx_out;      // [M][N] storage-type copy for the next consumer (NULL for fp32 models)
-  float* stats_out;  // [N/64][M_max]
+  float* stats_out;  // [M_max][N/16]
   // EPI_SWIGLU
   void* u_out;  // [M][ldu]
   int F, ldu;
   int layer_index;  // host-side only: which layer a launch belongs to (measurement hook)
 };
 
-struct GemmPlan {
-  int groups, wgs, cmax;
-};
-
-GemmPlan plan_gemm(int Nt, int Kt, int TPW, int want_wgs, int min_steps_per_wg);
-int gemm_tpw(GemmKind kind);
-int launch_gemm(int dtype, GemmKind kind, int MT, const GemmArgs& a, const GemmPlan& p, hipStream_t st);
+// One launch: a workgroup per tile of output columns, the whole K per workgroup.
+int launch_gemm(int dtype, GemmKind kind, int MT, const GemmArgs& a, hipStream_t st);
 
 }  // namespace lsv

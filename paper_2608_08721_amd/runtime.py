@@ -60,17 +60,56 @@ class DeviceModel:
         return dm
 
 
+def kv_capacity(positions):
+    """Smallest valid cache capacity (a multiple of LSV_KV_ALIGN) holding `positions`."""
+    a = lsv.LSV_KV_ALIGN
+    return max(a, (int(positions) + a - 1) // a * a)
+
+
+def v_column(pos):
+    """Column of cache position `pos` in a transposed V row (lsv.h, LSV_V_COLUMN)."""
+    return (pos & ~31) | ((pos & 12) << 1) | ((pos & 16) >> 2) | (pos & 3)
+
+
 class KVCache:
+    """The library's KV cache: K row-major per slab, V transposed with permuted columns."""
+
     def __init__(self, cfg, batch, capacity, device="cuda"):
         self.cfg, self.batch, self.capacity = cfg, batch, capacity
         nbytes = lsv.lsv_kv_cache_bytes(cfg, batch, capacity)
+        if nbytes == 0:
+            raise lsv.LsvError(lsv.LSV_ERR_INVALID_ARG, f"invalid KV cache shape (capacity {capacity} must be a "
+                                                        f"positive multiple of {lsv.LSV_KV_ALIGN})")
         self.buf = torch.zeros(nbytes, dtype=torch.uint8, device=device)
 
-    def view(self):
-        """[layer][K/V][batch][kv_head][pos][head_dim] typed view of the buffer."""
+    def _blocks(self):
         c = self.cfg
-        return self.buf.view(storage_dtype(c)).view(c.n_layers, 2, self.batch, c.n_kv_heads, self.capacity,
-                                                    c.head_dim)
+        return self.buf.view(storage_dtype(c)).view(c.n_layers, 2, self.batch, c.n_kv_heads,
+                                                    self.capacity * c.head_dim)
+
+    def k_view(self):
+        """[layer][batch][kv_head][pos][head_dim] view of the K blocks."""
+        c = self.cfg
+        return self._blocks()[:, 0].view(c.n_layers, self.batch, c.n_kv_heads, self.capacity, c.head_dim)
+
+    def vt_view(self):
+        """[layer][batch][kv_head][head_dim][column] view of the transposed V blocks."""
+        c = self.cfg
+        return self._blocks()[:, 1].view(c.n_layers, self.batch, c.n_kv_heads, c.head_dim, self.capacity)
+
+    def write(self, layer, b, start, k, v):
+        """Store K and V of positions start.. (device tensors [kv_head][n][head_dim])."""
+        n = k.shape[1]
+        self.k_view()[layer, b, :, start:start + n] = k
+        cols = v_column(torch.arange(start, start + n, device=self.buf.device))
+        self.vt_view()[layer, b][:, :, cols] = v.transpose(1, 2)
+
+    def read(self, layer, b, start, n):
+        """(K, V) of positions start..start+n-1 as [kv_head][n][head_dim] tensors."""
+        k = self.k_view()[layer, b, :, start:start + n]
+        cols = v_column(torch.arange(start, start + n, device=self.buf.device))
+        v = self.vt_view()[layer, b][:, :, cols].transpose(1, 2)
+        return k, v
 
 
 class Workspace:

@@ -55,7 +55,8 @@ def tiny_cfg(**kw):
 def test_size_queries_are_host_only(lib):
     cfg = tiny_cfg()
     assert lsv.lsv_packed_model_bytes(cfg) > 0
-    assert lsv.lsv_kv_cache_bytes(cfg, 2, 100) == 2 * 2 * 2 * 4 * 100 * 64 * 4
+    assert lsv.lsv_kv_cache_bytes(cfg, 2, 128) == 2 * 2 * 2 * 4 * 128 * 64 * 4
+    assert lsv.lsv_kv_cache_bytes(cfg, 2, 100) == 0  # capacity must be a multiple of LSV_KV_ALIGN
     assert lsv.lsv_verify_workspace_bytes(cfg, 1, 17, 145) > 0
     assert lsv.lsv_verify_workspace_bytes(cfg, 1, 65, 145) == 0
     assert lsv.lsv_packed_model_bytes(tiny_cfg(head_dim=96)) == 0
@@ -94,9 +95,11 @@ def test_host_validation(lib):
     expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_accept, 0, 1, 10, 1, 1, 2, 2, 1, None, 0.0, 0, 0, 1, 1, None, None, 1,
            16, S)
     # verify
-    args = [cfg, 1, 1, 100, 1, 1, 1, 1, 17, 100, 1, None, 1, 1 << 30, S]
-    msg = expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_verify_block, *(args[:9] + [101] + args[10:]))
+    args = [cfg, 1, 1, 128, 1, 1, 1, 1, 17, 128, 1, None, 1, 1 << 30, S]
+    msg = expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_verify_block, *(args[:9] + [129] + args[10:]))
     assert "max_ctx" in msg
+    msg = expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_verify_block, *(args[:3] + [100] + args[4:9] + [100] + args[10:]))
+    assert "multiple" in msg
     expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_verify_block, *(args[:8] + [65] + args[9:]))
     expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_verify_block, *(args[:4] + [0] + args[5:]))
     expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_verify_block, *(args[:13] + [16] + args[14:]))

@@ -77,16 +77,14 @@ def test_tiny_f32_end_to_end():
 def _bf16_case(shape, seed, contexts, rows, tol=2e-2):
     B = len(contexts)
     w = gen.model_weights(shape, seed)
-    cap = max(contexts) + max(rows) + 8
+    cap = runtime.kv_capacity(max(contexts) + max(rows) + 8)
     gm = GpuModel(shape, w, B, cap)
     om = OF.Model(shape, w)
     oc = OF.KVCache(shape, B, cap)
-    kvv = gm.kv.view()
     for l in range(shape.n_layers):
         for b in range(B):
             k, v = gen.synthetic_kv(shape, seed + 31 * b, l, 1, contexts[b])
-            kvv[l, 0, b, :, :contexts[b]] = runtime.to_device(k[0])
-            kvv[l, 1, b, :, :contexts[b]] = runtime.to_device(v[0])
+            gm.kv.write(l, b, 0, runtime.to_device(k[0]), runtime.to_device(v[0]))
             oc.k[l][b, :, :contexts[b]] = OF.stored_to_f64(k[0], "bf16")
             oc.v[l][b, :, :contexts[b]] = OF.stored_to_f64(v[0], "bf16")
     off = runtime.row_offsets_of(rows)
@@ -97,15 +95,19 @@ def _bf16_case(shape, seed, contexts, rows, tol=2e-2):
     err = row_rel_err(g_logits, o_logits)
     note(f"  {shape.name}: contexts {list(contexts)} rows {list(rows)}: max row rel err {err.max():.2e}")
     assert err.max() <= tol
-    # the K/V the GPU appended match the oracle's block entries
-    kvv_np = kvv.float().cpu().numpy()
+    # the K/V the GPU appended match the oracle's block entries, and the cached context is untouched
     for b in range(B):
-        if rows[b] == 0:
-            continue
         for l in range(shape.n_layers):
-            gk = kvv_np[l, 0, b, :, contexts[b]:contexts[b] + rows[b]]
-            ok = oc.k[l][b, :, contexts[b]:contexts[b] + rows[b]]
-            assert np.abs(gk - ok).max() <= tol * max(np.abs(ok).max(), 1e-6) * 4
+            gk, gv = (t.float().cpu().numpy() for t in gm.kv.read(l, b, 0, contexts[b] + rows[b]))
+            k0, v0 = gen.synthetic_kv(shape, seed + 31 * b, l, 1, contexts[b])
+            assert np.array_equal(gk[:, :contexts[b]], OF.stored_to_f64(k0[0], "bf16"))
+            assert np.array_equal(gv[:, :contexts[b]], OF.stored_to_f64(v0[0], "bf16"))
+            if rows[b] == 0:
+                continue
+            for got, want in ((gk, oc.k[l]), (gv, oc.v[l])):
+                new_g = got[:, contexts[b]:]
+                new_o = want[b, :, contexts[b]:contexts[b] + rows[b]]
+                assert np.abs(new_g - new_o).max() <= tol * max(np.abs(new_o).max(), 1e-6) * 4
     # greedy decisions agree wherever the oracle's margin clears the error
     abs_err = np.abs(g_logits - o_logits).max()
     am_g, am_o = g_logits.argmax(axis=1), o_logits.argmax(axis=1)
