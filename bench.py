@@ -110,7 +110,7 @@ def measured_traffic(rows):
     return None if v is None else float(v)
 
 
-GATEUP_KERNEL = "gemm_kernel<unsigned short, 2, 2, 3>"  # bf16, up to 32 rows, 2 tiles per wave, SwiGLU
+GATEUP_KERNEL = "gemm_kernel<unsigned short, 2, 2>"  # bf16 gate/up + SwiGLU, up to 32 rows
 SELECT_KERNEL = "select_length_kernel"
 CALIB_BYTES = 256 << 20
 
