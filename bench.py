@@ -78,9 +78,10 @@ class HipEvents:
 
 def gateup_bytes(m, rows):
     """Algorithmic HBM bytes of one gate/up launch: the packed gate and up weights once, the
-    storage-type activation rows and their norm statistics in, the SwiGLU output out."""
+    storage-type activation rows and their per-16-column norm statistics in, the SwiGLU
+    output out."""
     es = 2 if m.dtype == "bf16" else 4
-    return 2 * m.d_ff * m.d_model * es + rows * m.d_model * es + rows * (m.d_model // 64) * 4 + rows * m.d_ff * es
+    return 2 * m.d_ff * m.d_model * es + rows * m.d_model * es + rows * (m.d_model // 16) * 4 + rows * m.d_ff * es
 
 
 GATEUP_PROFILE = os.path.join(ROOT, "profiles", "gemm_gateup_llama3-8b-b1-c2048.md")
