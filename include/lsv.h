@@ -163,7 +163,7 @@ int lsv_workspace_clear(void* d_workspace, size_t workspace_bytes, void* stream)
  *   d_status           [batch] int32 out (nullable): LSV_OK, LSV_ERR_INVALID_ARG (token id
  *                      out of range), LSV_ERR_CAPACITY (block exceeds max_ctx)
  *   d_workspace        lsv_verify_workspace_bytes(cfg, batch, max_rows, max_ctx) bytes */
-enum { LSV_MAX_BATCH = 64, LSV_MAX_ROWS = 64 };
+enum { LSV_MAX_BATCH = 64, LSV_MAX_ROWS = 512 };
 int lsv_verify_block(const lsv_model_config* cfg, const void* d_packed, void* d_kv, int32_t capacity,
                      int32_t batch, const int32_t* d_seq_len, const int32_t* d_tokens,
                      const int32_t* d_row_offsets, int32_t max_rows, int32_t max_ctx, float* d_logits,
@@ -189,8 +189,9 @@ int lsv_verify_block(const lsv_model_config* cfg, const void* d_packed, void* d_
  *   sequence b, [*, vocab] fp32.
  *
  *   d_logits           [rows, vocab] fp32 (as written by lsv_verify_block)
- *   max_rows           host bound on d_row_offsets[batch]
- *   max_rows_per_seq   host bound on rows_b; width of d_out_tokens
+ *   max_rows           host bound on d_row_offsets[batch] (<= LSV_MAX_ROWS)
+ *   max_rows_per_seq   host bound on rows_b (<= LSV_MAX_SEQ_ROWS: one wave decides a
+ *                      sequence); width of d_out_tokens
  *   d_accept_len       [batch] out: a_b
  *   d_out_tokens       [batch, max_rows_per_seq] out: emitted tokens, then -1
  *   d_seq_len          [batch] in/out, nullable: if given, d_seq_len[b] += a_b + 1
@@ -202,6 +203,7 @@ int lsv_verify_block(const lsv_model_config* cfg, const void* d_packed, void* d_
  *                      the rows run past max_rows
  *   d_workspace        lsv_accept_workspace_bytes(batch, max_rows, vocab) bytes */
 enum { LSV_ACC_GREEDY = 0, LSV_ACC_SAMPLE = 1 };
+enum { LSV_MAX_SEQ_ROWS = 64 };
 size_t lsv_accept_workspace_bytes(int32_t batch, int32_t max_rows, int32_t vocab);
 int lsv_accept(int32_t mode, int32_t batch, int32_t vocab, const float* d_logits,
                const int32_t* d_row_offsets, int32_t max_rows, int32_t max_rows_per_seq,

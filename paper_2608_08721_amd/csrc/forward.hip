@@ -83,7 +83,7 @@ struct VerifyPlan {
 
 static VerifyPlan plan_verify(const Shape& s, int batch, int max_rows, int max_ctx) {
   VerifyPlan v;
-  v.MT = (max_rows + 15) / 16;
+  v.MT = max_rows > 64 ? 4 : (max_rows + 15) / 16;  // activation tiles per 64-row chunk
   v.attn = plan_attention(batch, s.nkv, max_ctx);
   return v;
 }

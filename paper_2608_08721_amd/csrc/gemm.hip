@@ -151,12 +151,14 @@ LSV_DEV float inv_rms_of_row(const GemmArgs& a, int m, int g4) {
 
 // ------------------------------------------------------------------ the GEMM
 template <typename T, int MT, int TPW, int KS, int U, int NS, int EPI, int MT_MAX>
-LSV_DEV void gemm_body(const GemmArgs& a, const int M, f32x4_t (*red)[TPW][MT_MAX][kWave]) {
+LSV_DEV void gemm_body(const GemmArgs& a, const int M, const int tile, const int m0,
+                       f32x4_t (*red)[TPW][MT_MAX][kWave]) {
   constexpr int KT = FragTraits<T>::KT, EPL = FragTraits<T>::EPL;
   constexpr bool RMS = EPI != EPI_RESID;  // consumer of a normalised activation
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, l16 = lane & 15, g4 = lane >> 4;
-  // this workgroup: fragment rows tn0 .. tn0+TPW-1 over the whole K; wave = k-slice
-  const int tn0 = blockIdx.x * TPW;
+  // this workgroup: fragment rows tn0 .. tn0+TPW-1 over the whole K, activation rows
+  // m0 .. min(M, m0 + 16 MT) - 1; wave = k-slice
+  const int tn0 = tile * TPW;
   const int k0 = (int)((long long)wave * a.Kt / KS), k1 = (int)((long long)(wave + 1) * a.Kt / KS);
   const int nk = k1 - k0;  // >= 0, and k0 < Kt for every wave
   bool tvalid[TPW];
@@ -173,7 +175,7 @@ LSV_DEV void gemm_body(const GemmArgs& a, const int M, f32x4_t (*red)[TPW][MT_MA
   if (EPI == EPI_RESID && wave == 0) {
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
-      const int m = min(mt * 16 + l16, a.M_max - 1);
+      const int m = min(m0 + mt * 16 + l16, a.M_max - 1);
 #pragma unroll
       for (int t = 0; t < TPW; ++t) {
         const int n0 = (tvalid[t] ? tn0 + t : 0) * 16 + 4 * g4;
@@ -187,7 +189,7 @@ LSV_DEV void gemm_body(const GemmArgs& a, const int M, f32x4_t (*red)[TPW][MT_MA
   const GLOBAL T* xp[MT];
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt) {
-    const int m = min(mt * 16 + l16, a.M_max - 1);
+    const int m = min(m0 + mt * 16 + l16, a.M_max - 1);
     xp[mt] = (const GLOBAL T*)a.x + (size_t)m * a.ldx + (size_t)k0 * KT + g4 * EPL;
   }
 
@@ -266,13 +268,13 @@ LSV_DEV void gemm_body(const GemmArgs& a, const int M, f32x4_t (*red)[TPW][MT_MA
   float inv[MT];
   if (RMS) {
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt) inv[mt] = inv_rms_of_row(a, mt * 16 + l16, g4);
+    for (int mt = 0; mt < MT; ++mt) inv[mt] = inv_rms_of_row(a, m0 + mt * 16 + l16, g4);
   }
   int qkv_b[MT], qkv_pos[MT];
   if (EPI == EPI_QKV) {
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
-      const int m = min(mt * 16 + l16, a.M_max - 1);
+      const int m = min(m0 + mt * 16 + l16, a.M_max - 1);
       const int b = seq_of_row(a.row_offsets, a.batch, m);
       qkv_b[mt] = b;
       qkv_pos[mt] = GL(a.seq_len)[b] + (m - GL(a.row_offsets)[b]);
@@ -283,7 +285,7 @@ LSV_DEV void gemm_body(const GemmArgs& a, const int M, f32x4_t (*red)[TPW][MT_MA
     for (int t = 0; t < TPW; ++t)
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) {
-        const int m = mt * 16 + l16, n0 = (tn0 + t) * 16 + 4 * g4;
+        const int m = m0 + mt * 16 + l16, n0 = (tn0 + t) * 16 + 4 * g4;
         if (m >= M || !tvalid[t]) continue;
         const f32x4_t v = acc[t][mt] * inv[mt];
         GLOBAL float* o = GL(a.out_f32) + (size_t)m * a.ldo;
@@ -301,7 +303,7 @@ LSV_DEV void gemm_body(const GemmArgs& a, const int M, f32x4_t (*red)[TPW][MT_MA
       for (int t = 0; t < TPW; ++t)
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) {
-          const int m = mt * 16 + l16, n0 = (tn0 + t) * 16 + 4 * g4;
+          const int m = m0 + mt * 16 + l16, n0 = (tn0 + t) * 16 + 4 * g4;
           if (m >= M || !tvalid[t] || n0 >= qrows + 2 * krows) continue;
           const int b = qkv_b[mt], pos = qkv_pos[mt];
           const f32x4_t v = acc[t][mt] * inv[mt];
@@ -355,7 +357,7 @@ LSV_DEV void gemm_body(const GemmArgs& a, const int M, f32x4_t (*red)[TPW][MT_MA
       for (int t = 0; t < TPW; ++t)
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) {
-          const int m = mt * 16 + l16, n0 = (tn0 + t) * 16 + 4 * g4;
+          const int m = m0 + mt * 16 + l16, n0 = (tn0 + t) * 16 + 4 * g4;
           float ss = 0.f;
           if (m < M && tvalid[t]) {
             const f32x4_t h4 = hpre[t][mt] + acc[t][mt];
@@ -371,7 +373,7 @@ LSV_DEV void gemm_body(const GemmArgs& a, const int M, f32x4_t (*red)[TPW][MT_MA
       static_assert(EPI != EPI_SWIGLU || TPW == 2, "SwiGLU pairs a gate and an up fragment row");
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) {
-        const int m = mt * 16 + l16, f0 = (tn0 >> 1) * 16 + 4 * g4;
+        const int m = m0 + mt * 16 + l16, f0 = (tn0 >> 1) * 16 + 4 * g4;
         if (m >= M || !tvalid[0]) continue;
         f32x4_t out;
 #pragma unroll
@@ -409,30 +411,41 @@ template <int KIND, int MT_MAX> struct GemmShape {
   static constexpr int U = MT_MAX <= 2 ? C::U : 4, NS = MT_MAX <= 2 ? C::NS : 2;
 };
 
-// The host bound on rows fixes MT_MAX; the kernel runs the body for the activation
-// tiles that the device row count actually needs, so a generous bound costs nothing.
+// Rows come in chunks of 64 (4 activation tiles); a chunk's workgroups read the same
+// weights, so the grid puts the chunks of one column tile on the same XCD (workgroup
+// ids congruent mod 8 share one) where the repeated reads hit its L2.  The host bound
+// on rows fixes MT_MAX; the kernel runs the body for the activation tiles that the
+// device row count of its chunk actually needs, so a generous bound costs nothing.
 template <typename T, int KIND, int MT_MAX>
 __global__ void __launch_bounds__(64 * GemmCfg<KIND>::KS) gemm_kernel(GemmArgs a) {
   using S = GemmShape<KIND, MT_MAX>;
   __shared__ f32x4_t red[S::KS > 1 ? S::KS - 1 : 1][S::TPW][MT_MAX][kWave];  // k-slice sums
+  const int tiles = (a.Nt + S::TPW - 1) / S::TPW, nch = (a.M_max + 63) / 64;
+  const int round = blockIdx.x >> 3, chunk = round % nch, tile = (round / nch) * 8 + (blockIdx.x & 7);
+  if (tile >= tiles) return;
   const int M = min(GL(a.row_offsets)[a.batch], a.M_max);  // never trust device rows beyond the host bound
-  const int mt = M <= 16 ? 1 : (M <= 32 ? 2 : (M <= 48 ? 3 : 4));
+  const int m0 = chunk * 64;
+  if (m0 >= M) return;
+  const int Mc = min(M - m0, 64);
+  const int M_end = m0 + Mc;
+  const int mt = Mc <= 16 ? 1 : (Mc <= 32 ? 2 : (Mc <= 48 ? 3 : 4));
   if (mt <= 1 || MT_MAX == 1)
-    gemm_body<T, 1, S::TPW, S::KS, S::U, S::NS, S::EPI, MT_MAX>(a, M, red);
+    gemm_body<T, 1, S::TPW, S::KS, S::U, S::NS, S::EPI, MT_MAX>(a, M_end, tile, m0, red);
   else if (mt == 2 || MT_MAX == 2)
-    gemm_body<T, (MT_MAX >= 2 ? 2 : 1), S::TPW, S::KS, S::U, S::NS, S::EPI, MT_MAX>(a, M, red);
+    gemm_body<T, (MT_MAX >= 2 ? 2 : 1), S::TPW, S::KS, S::U, S::NS, S::EPI, MT_MAX>(a, M_end, tile, m0, red);
   else if (mt == 3 || MT_MAX == 3)
-    gemm_body<T, (MT_MAX >= 3 ? 3 : 1), S::TPW, S::KS, S::U, S::NS, S::EPI, MT_MAX>(a, M, red);
+    gemm_body<T, (MT_MAX >= 3 ? 3 : 1), S::TPW, S::KS, S::U, S::NS, S::EPI, MT_MAX>(a, M_end, tile, m0, red);
   else
-    gemm_body<T, MT_MAX, S::TPW, S::KS, S::U, S::NS, S::EPI, MT_MAX>(a, M, red);
+    gemm_body<T, MT_MAX, S::TPW, S::KS, S::U, S::NS, S::EPI, MT_MAX>(a, M_end, tile, m0, red);
 }
 
 // ------------------------------------------------------------------ planning and launch
 template <typename T, int KIND, int MT_MAX>
 static void launch_one(const GemmArgs& a, hipStream_t st) {
   constexpr int TPW = GemmCfg<KIND>::TPW, KS = GemmCfg<KIND>::KS;
-  const int tiles = (a.Nt + TPW - 1) / TPW;
-  hipLaunchKernelGGL((gemm_kernel<T, KIND, MT_MAX>), dim3(tiles), dim3(64 * KS), 0, st, a);
+  const int tiles = (a.Nt + TPW - 1) / TPW, nch = (a.M_max + 63) / 64;
+  const unsigned grid = (unsigned)((tiles + 7) / 8 * 8 * nch);
+  hipLaunchKernelGGL((gemm_kernel<T, KIND, MT_MAX>), dim3(grid), dim3(64 * KS), 0, st, a);
 }
 
 template <typename T, int KIND>

@@ -173,8 +173,9 @@ int lsv_accept(int32_t mode, int32_t batch, int32_t vocab, const float* d_logits
                int32_t* d_seq_len, int32_t* d_status, void* d_workspace, size_t workspace_bytes, void* stream) {
   if (mode != LSV_ACC_GREEDY && mode != LSV_ACC_SAMPLE) return fail(LSV_ERR_INVALID_ARG, "bad accept mode %d", mode);
   if (batch < 1 || batch > LSV_MAX_BATCH || vocab < 1) return fail(LSV_ERR_INVALID_ARG, "bad batch or vocab");
-  if (max_rows < 1 || max_rows_per_seq < 1 || max_rows_per_seq > LSV_MAX_ROWS)
-    return fail(LSV_ERR_INVALID_ARG, "bad max_rows / max_rows_per_seq");
+  if (max_rows < 1 || max_rows > LSV_MAX_ROWS || max_rows_per_seq < 1 || max_rows_per_seq > LSV_MAX_SEQ_ROWS)
+    return fail(LSV_ERR_INVALID_ARG, "bad max_rows %d (<= %d) / max_rows_per_seq %d (<= %d)", max_rows,
+                (int)LSV_MAX_ROWS, max_rows_per_seq, (int)LSV_MAX_SEQ_ROWS);
   if (!d_logits || !d_row_offsets || !d_tokens || !d_accept_len || !d_out_tokens || !d_workspace)
     return fail(LSV_ERR_INVALID_ARG, "NULL pointer");
   if (mode == LSV_ACC_SAMPLE && (!d_draft_probs || !(temperature > 0.f) || !isfinite(temperature)))

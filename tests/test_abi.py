@@ -58,7 +58,8 @@ def test_size_queries_are_host_only(lib):
     assert lsv.lsv_kv_cache_bytes(cfg, 2, 128) == 2 * 2 * 2 * 4 * 128 * 64 * 4
     assert lsv.lsv_kv_cache_bytes(cfg, 2, 100) == 0  # capacity must be a multiple of LSV_KV_ALIGN
     assert lsv.lsv_verify_workspace_bytes(cfg, 1, 17, 145) > 0
-    assert lsv.lsv_verify_workspace_bytes(cfg, 1, 65, 145) == 0
+    assert lsv.lsv_verify_workspace_bytes(cfg, 1, 264, 145) > 0
+    assert lsv.lsv_verify_workspace_bytes(cfg, 1, lsv.LSV_MAX_ROWS + 1, 145) == 0
     assert lsv.lsv_packed_model_bytes(tiny_cfg(head_dim=96)) == 0
     assert lsv.lsv_packed_model_bytes(tiny_cfg(n_kv_heads=3)) == 0
     assert lsv.lsv_accept_workspace_bytes(1, 17, 128256) > 0
@@ -100,7 +101,7 @@ def test_host_validation(lib):
     assert "max_ctx" in msg
     msg = expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_verify_block, *(args[:3] + [100] + args[4:9] + [100] + args[10:]))
     assert "multiple" in msg
-    expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_verify_block, *(args[:8] + [65] + args[9:]))
+    expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_verify_block, *(args[:8] + [lsv.LSV_MAX_ROWS + 1] + args[9:]))
     expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_verify_block, *(args[:4] + [0] + args[5:]))
     expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_verify_block, *(args[:13] + [16] + args[14:]))
     expect(lsv.LSV_ERR_UNSUPPORTED, lsv.lsv_verify_block, *([tiny_cfg(head_dim=96)] + args[1:]))

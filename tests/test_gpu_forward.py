@@ -78,7 +78,7 @@ def _bf16_case(shape, seed, contexts, rows, tol=2e-2):
     B = len(contexts)
     w = gen.model_weights(shape, seed)
     cap = runtime.kv_capacity(max(contexts) + max(rows) + 8)
-    gm = GpuModel(shape, w, B, cap)
+    gm = GpuModel(shape, w, B, cap, max_rows=max(64, int(sum(rows))))
     om = OF.Model(shape, w)
     oc = OF.KVCache(shape, B, cap)
     for l in range(shape.n_layers):
@@ -114,7 +114,7 @@ def _bf16_case(shape, seed, contexts, rows, tol=2e-2):
     decided = [r for r in range(len(o_logits)) if top2_margin(o_logits[r]) > 2 * abs_err]
     assert all(am_g[r] == am_o[r] for r in decided)
     note(f"    argmax equal on {len(decided)}/{len(o_logits)} decided rows")
-    return gm, g_logits, o_logits
+    return gm, g_logits, o_logits, toks, off
 
 
 def test_bf16_gqa_hd64_ragged():
