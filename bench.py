@@ -30,6 +30,7 @@ sys.path.insert(0, ROOT)
 METRIC = "verify-step latency (us) & tokens/s vs gamma; % of HBM BW / MFMA bf16 peak"
 HBM_PEAK_GBPS = 8000.0
 HIP_EVENT_DISABLE_SYSTEM_FENCE = 0x20000000
+MFMA_PEAK_FLOPS = 2.5e15  # dense bf16
 
 
 def parse():
@@ -299,15 +300,19 @@ def main():
 
     wl = configs.WORKLOADS[args.workload]
     m = wl.model
-    if wl.batch != 1 or wl.accept != "greedy":
-        raise SystemExit("bench.py times the batch-1 greedy workloads")
+    if "greedy" not in wl.accept:
+        raise SystemExit("bench.py times the greedy-acceptance workloads")
     torch.cuda.set_device(0)
     dev = "cuda"
     i32 = lambda x: torch.tensor(np.asarray(x, dtype=np.int32), device=dev)
     seed, B, G = wl.seed, wl.batch, wl.G
-    C = int(gen.contexts(wl)[0])
-    rows_max = G + 1
-    cap = runtime.kv_capacity(C + rows_max)
+    ctx = [int(c) for c in gen.contexts(wl)]
+    rows_seq = G + 1                     # root + drafts per sequence
+    # prefill rows per sequence and call: for batches, keep the whole block within the
+    # batched GEMM path's row bound
+    pre = 64 if B == 1 else max(1, min(64, lsv.LSV_WIDE_ROWS // B))
+    rows_buf = max(B * rows_seq, B * pre)
+    cap = runtime.kv_capacity(max(ctx) + rows_seq)
     cfg = runtime.model_config(m)
 
     # ---- model: seeded weights, generated and packed one layer at a time (untimed)
@@ -319,46 +324,62 @@ def main():
         if l % 8 == 7:
             log(f"packed layer {l + 1}/{m.n_layers} ({time.time() - t0:.1f} s)")
     kv = runtime.KVCache(cfg, B, cap, dev)
-    ws = runtime.Workspace(lsv.lsv_verify_workspace_bytes(cfg, B, 64, cap), dev)
-    aws = runtime.Workspace(lsv.lsv_accept_workspace_bytes(B, 64, m.vocab), dev)
-    logits = torch.zeros((64, m.vocab), dtype=torch.float32, device=dev)
+    ws = runtime.Workspace(lsv.lsv_verify_workspace_bytes(cfg, B, rows_buf, cap), dev)
+    aws = runtime.Workspace(lsv.lsv_accept_workspace_bytes(B, rows_buf, m.vocab), dev)
+    logits = torch.zeros((rows_buf, m.vocab), dtype=torch.float32, device=dev)
     status = torch.zeros(B, dtype=torch.int32, device=dev)
 
-    # ---- prefill the context from seeded prompt ids (chunks of 64 rows, untimed)
-    prompt = gen.prefix_ids(seed, B, [C], m.vocab)[0]
-    for s in range(0, C, 64):
-        chunk = prompt[s:s + 64]
-        lsv.lsv_verify_block(cfg, dm.buf, kv.buf, cap, B, i32([s]), i32(chunk), i32([0, len(chunk)]), 64, cap,
-                             logits, status, ws.buf, ws.nbytes)
-    last = len(prompt) - 64 * ((len(prompt) - 1) // 64) - 1
+    # ---- prefill every context from seeded prompt ids (untimed), in chunks of `pre` rows per
+    # sequence; a sequence starts late enough that all of them end in the last call
+    prompts = gen.prefix_ids(seed, B, ctx, m.vocab)
+    chunks = [(c + pre - 1) // pre for c in ctx]
+    n_calls = max(chunks)
+    filled = [0] * B
+    for i in range(n_calls):
+        take = []
+        for b in range(B):
+            first = n_calls - chunks[b]
+            take.append(0 if i < first else (ctx[b] - (chunks[b] - 1) * pre if i == first else pre))
+        off = runtime.row_offsets_of(take)
+        toks = np.concatenate([prompts[b][filled[b]:filled[b] + take[b]] for b in range(B)])
+        lsv.lsv_verify_block(cfg, dm.buf, kv.buf, cap, B, i32(filled), i32(toks), i32(off), rows_buf, cap, logits,
+                             status, ws.buf, ws.nbytes)
+        filled = [filled[b] + take[b] for b in range(B)]
+    assert filled == ctx
+    last_rows = torch.tensor(off[1:] - 1, dtype=torch.long, device=dev)
     acc = torch.zeros(B, dtype=torch.int32, device=dev)
-    out = torch.zeros((B, rows_max), dtype=torch.int32, device=dev)
-    # root = greedy token after the prompt, chosen by the library's own acceptance on one row
-    lsv.lsv_accept(lsv.LSV_ACC_GREEDY, 1, m.vocab, logits[last:last + 1], i32([0, 1]), 1, rows_max,
-                   i32([prompt[-1]]), None, 0.0, 0, 0, acc, out, None, status, aws.buf, aws.nbytes)
+    out = torch.zeros((B, rows_seq), dtype=torch.int32, device=dev)
+    # roots = greedy tokens after each prompt, chosen by the library's own acceptance on one row each
+    lsv.lsv_accept(lsv.LSV_ACC_GREEDY, B, m.vocab, logits[last_rows].contiguous(), i32(np.arange(B + 1)), B,
+                   rows_seq, i32([p[-1] for p in prompts]), None, 0.0, 0, 0, acc, out, None, status, aws.buf,
+                   aws.nbytes)
     torch.cuda.synchronize()
-    assert int(status.item()) == 0
-    root = int(out[0, 0].item())
-    log(f"model + prefill of {C} tokens ready ({time.time() - t0:.1f} s); root token {root}")
+    assert bool((status == 0).all())
+    roots = [int(x) for x in out[:, 0].cpu()]
+    log(f"model + prefill of {ctx} tokens ready ({time.time() - t0:.1f} s); roots {roots}")
 
-    drafts = gen.draft_ids(seed, B, G, m.vocab)[0]
-    tokens = i32([root] + list(drafts))
+    drafts = gen.draft_ids(seed, B, G, m.vocab)
+
+    def layout(gammas):
+        """Verify rows [root_b, x_1..x_gamma_b] per sequence, concatenated."""
+        return i32(np.concatenate([[roots[b]] + list(drafts[b][:gammas[b]]) for b in range(B)]))
+
     conf_np = gen.confidences(wl)
     conf = torch.tensor(conf_np, device=dev)
-    seq_base = i32([C])
-    seq_work = i32([C])
-    stream = torch.cuda.current_stream()
+    seq_base = i32(ctx)
+    seq_work = i32(ctx)
 
-    # ---- per-gamma latency sweep (graph of verify + accept per gamma): the measured cost table
+    # ---- per-gamma latency sweep (graph of verify + accept per uniform gamma): the measured cost table
     sweep = {}
     for g in range(1, G + 1):
-        ro = i32([0, g + 1])
+        ro = i32(runtime.row_offsets_of([g + 1] * B))
+        tok_g = layout([g] * B)
 
         def body():
             seq_work.copy_(seq_base)
-            lsv.lsv_verify_block(cfg, dm.buf, kv.buf, cap, B, seq_base, tokens, ro, rows_max, cap, logits, status,
+            lsv.lsv_verify_block(cfg, dm.buf, kv.buf, cap, B, seq_base, tok_g, ro, rows_buf, cap, logits, status,
                                  ws.buf, ws.nbytes)
-            lsv.lsv_accept(lsv.LSV_ACC_GREEDY, B, m.vocab, logits, ro, rows_max, rows_max, tokens, None, 0.0, 0, 0,
+            lsv.lsv_accept(lsv.LSV_ACC_GREEDY, B, m.vocab, logits, ro, rows_buf, rows_seq, tok_g, None, 0.0, 0, 0,
                            acc, out, seq_work, status, aws.buf, aws.nbytes)
         body()
         graph = torch.cuda.CUDAGraph()
@@ -378,18 +399,21 @@ def main():
     cost = np.array([0.0] + [sweep[g] for g in range(1, G + 1)], dtype=np.float64)
     log("sweep (us): " + " ".join(f"{g}:{sweep[g] * 1e3:.0f}" for g in range(1, G + 1)))
 
-    # ---- LibraSpec selection on the measured table (reported for all three rules)
+    # ---- LibraSpec selection on the measured table (reported for all three rules); each
+    # sequence selects on the uniform-gamma table of the batch
     cost_t = torch.tensor(cost, device=dev)
     gamma = torch.zeros(B, dtype=torch.int32, device=dev)
     aux = torch.zeros(B, dtype=torch.int32, device=dev)
     row_off = torch.zeros(B + 1, dtype=torch.int32, device=dev)
+    n_alg1 = 8 if G <= 16 else 16
     chosen = {}
     for name, mode in (("exhaustive", lsv.LSV_SEL_EXHAUSTIVE), ("alg1", lsv.LSV_SEL_ALG1),
                        ("marginal", lsv.LSV_SEL_MARGINAL)):
-        lsv.lsv_select_length(mode, B, G, conf, cost_t, 1, G, 2.2, 8, 0, gamma, aux, row_off, status)
+        lsv.lsv_select_length(mode, B, G, conf, cost_t, 1, G, 2.2, n_alg1, 0, gamma, aux, row_off, status)
         torch.cuda.synchronize()
-        chosen[name] = int(gamma[0].item())
+        chosen[name] = [int(x) for x in gamma.cpu()]
     g_star = chosen["marginal"]
+    tokens = layout(g_star)
     log(f"chosen gamma: {chosen}")
 
     # ---- the timed step: select -> verify -> accept, one graph, dominant kernel bracketed by events
@@ -398,10 +422,11 @@ def main():
 
     def step():
         seq_work.copy_(seq_base)
-        lsv.lsv_select_length(lsv.LSV_SEL_MARGINAL, B, G, conf, cost_t, 1, G, 2.2, 8, 0, gamma, aux, row_off, status)
-        lsv.lsv_verify_block(cfg, dm.buf, kv.buf, cap, B, seq_base, tokens, row_off, rows_max, cap, logits, status,
+        lsv.lsv_select_length(lsv.LSV_SEL_MARGINAL, B, G, conf, cost_t, 1, G, 2.2, n_alg1, 0, gamma, aux, row_off,
+                              status)
+        lsv.lsv_verify_block(cfg, dm.buf, kv.buf, cap, B, seq_base, tokens, row_off, rows_buf, cap, logits, status,
                              ws.buf, ws.nbytes)
-        lsv.lsv_accept(lsv.LSV_ACC_GREEDY, B, m.vocab, logits, row_off, rows_max, rows_max, tokens, None, 0.0, 0, 0,
+        lsv.lsv_accept(lsv.LSV_ACC_GREEDY, B, m.vocab, logits, row_off, rows_buf, rows_seq, tokens, None, 0.0, 0, 0,
                        acc, out, seq_work, status, aws.buf, aws.nbytes)
     step()
     torch.cuda.synchronize()
@@ -432,15 +457,30 @@ def main():
         torch.cuda.synchronize()
         gateup_ms += [hev.elapsed_ms(2 * i, 2 * i + 1) for i in range(n_slots)]
     lsv.lsv_set_timing_events(lsv.LSV_KERNEL_GATEUP, [], 0, 0)
-    assert int(status.item()) == 0 and int(gamma.item()) == g_star
-    a_len = int(acc.item())
-    rows = g_star + 1
+    assert bool((status == 0).all()) and [int(x) for x in gamma.cpu()] == g_star
+    a_len = [int(x) for x in acc.cpu()]
+    rows = sum(g + 1 for g in g_star)
 
+    # dominant kernel: bytes and flops of one gate/up launch at this step's rows
     avg_gu = statistics.mean(gateup_ms)
     gu_bytes = gateup_bytes(m, rows)
-    achieved = gu_bytes / (avg_gu * 1e-3) / 1e9
-    sb = step_bytes(m, [C], rows)
-    sf = step_flops(m, [C], [rows])
+    gu_flops = 2.0 * rows * 2 * m.d_ff * m.d_model
+    t_gu = avg_gu * 1e-3
+    hbm_gu, mfma_gu = gu_bytes / t_gu / 1e9 / HBM_PEAK_GBPS, gu_flops / t_gu / MFMA_PEAK_FLOPS
+    bound = "mfma" if gu_flops / MFMA_PEAK_FLOPS > gu_bytes / (HBM_PEAK_GBPS * 1e9) else "hbm"
+    if bound == "hbm":
+        roof = {"bound": "hbm", "achieved": gu_bytes / t_gu / 1e9, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                "frac": hbm_gu, "traffic": measured_traffic(rows) if B == 1 else None}
+    else:
+        roof = {"bound": "mfma", "achieved": gu_flops / t_gu / 1e12, "peak": MFMA_PEAK_FLOPS / 1e12, "unit": "TFLOP/s",
+                "frac": mfma_gu, "traffic": None}
+    roof.update({"kernel": "gemm gate/up + SwiGLU (one launch per layer)", "bytes_per_launch": gu_bytes,
+                 "flops_per_launch": gu_flops, "hbm_frac": hbm_gu, "mfma_frac": mfma_gu,
+                 "avg_launch_us": avg_gu * 1e3, "launches_timed": len(gateup_ms),
+                 "how": "HIP events around each gate/up launch in eagerly launched steps"})
+    rows_per_seq = [g + 1 for g in g_star]
+    sb = step_bytes(m, ctx, rows)
+    sf = step_flops(m, ctx, rows_per_seq)
     if args.calib_copy:
         x = torch.empty(256 << 20, dtype=torch.uint8, device=dev)
         y = torch.empty_like(x)
@@ -448,11 +488,14 @@ def main():
         torch.cuda.synchronize()
 
     # expected emitted tokens per step under the drafter-confidence model (Assumption 3.7)
-    P = np.cumprod(conf_np[0].astype(np.float64))
-    exp_tokens = B * (1.0 + P[:g_star].sum())
+    exp_tokens = 0.0
+    for b in range(B):
+        P = np.cumprod(conf_np[b].astype(np.float64))
+        exp_tokens += 1.0 + P[:g_star[b]].sum()
+    one = (lambda v: v[0]) if B == 1 else (lambda v: v)
     result = {
         "metric": METRIC,
-        "value": B * rows / (ms_step * 1e-3),
+        "value": rows / (ms_step * 1e-3),
         "unit": "verified tokens/s",
         "n_gpus": 1,
         "steps": args.steps,
@@ -463,24 +506,29 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16" if m.dtype == "bf16" else "f32",
         "data": "synthetic (seeded random-init weights, random prompt and draft ids)",
-        "config": {"workload": wl.name, "model_shape": m.name, "batch": B, "context": C, "drafted": G,
-                   "gamma": g_star, "selector": "marginal on measured cost", "accept": "greedy"},
-        "roofline": {"bound": "hbm", "kernel": "gemm gate/up + SwiGLU (one launch per layer)",
-                     "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBPS,
-                     "traffic": measured_traffic(rows), "bytes_per_launch": gu_bytes, "avg_launch_us": avg_gu * 1e3,
-                     "launches_timed": len(gateup_ms),
-                     "how": "HIP events around each gate/up launch in eagerly launched steps"},
+        "config": {"workload": wl.name, "model_shape": m.name, "batch": B, "context": one(ctx), "drafted": G,
+                   "gamma": one(g_star), "rows": rows, "selector": "marginal on measured cost", "accept": "greedy"},
+        "roofline": roof,
         "step": {"latency_us": ms_step * 1e3, "wall_ms_per_step": t_wall / args.steps * 1e3,
                  "algorithmic_bytes": sb, "hbm_frac": sb / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBPS,
-                 "flops": sf, "mfma_frac": sf / (ms_step * 1e-3) / 2.5e15,
+                 "flops": sf, "mfma_frac": sf / (ms_step * 1e-3) / MFMA_PEAK_FLOPS,
                  "expected_tokens_per_s": exp_tokens / (ms_step * 1e-3),
-                 "realized_tokens_per_s": B * (a_len + 1) / (ms_step * 1e-3)},
-        "selection": chosen,
+                 "realized_tokens_per_s": sum(a + 1 for a in a_len) / (ms_step * 1e-3)},
+        "selection": {k: one(v) for k, v in chosen.items()},
         "sweep": {str(g): round(sweep[g] * 1e3, 2) for g in range(1, G + 1)},
     }
-    if not args.no_cpu_baseline:
+    if B > 1:
+        # every sequence at the largest gamma: the batched regime the matrix cores serve
+        rows_g = B * (G + 1)
+        t_g = sweep[G] * 1e-3
+        sf_g = step_flops(m, ctx, [G + 1] * B)
+        sb_g = step_bytes(m, ctx, rows_g)
+        result["uniform_gamma_max"] = {"gamma": G, "rows": rows_g, "latency_us": sweep[G] * 1e3,
+                                       "mfma_frac": sf_g / t_g / MFMA_PEAK_FLOPS,
+                                       "hbm_frac": sb_g / t_g / 1e9 / HBM_PEAK_GBPS}
+    if not args.no_cpu_baseline and B == 1:
         log("cpu baseline: timing the oracle on a bounded sample")
-        result["cpu_baseline"] = cpu_baseline(m, seed, C, rows, [root] + list(drafts), g_star)
+        result["cpu_baseline"] = cpu_baseline(m, seed, ctx[0], rows, [roots[0]] + list(drafts[0]), g_star[0])
     print(json.dumps(result), flush=True)
 
 

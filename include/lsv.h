@@ -164,6 +164,10 @@ int lsv_workspace_clear(void* d_workspace, size_t workspace_bytes, void* stream)
  *                      out of range), LSV_ERR_CAPACITY (block exceeds max_ctx)
  *   d_workspace        lsv_verify_workspace_bytes(cfg, batch, max_rows, max_ctx) bytes */
 enum { LSV_MAX_BATCH = 64, LSV_MAX_ROWS = 512 };
+/* Performance note: bf16 blocks whose host bound max_rows lies in (64, LSV_WIDE_ROWS]
+ * run the batched GEMM path (every row in one workgroup, activations shared through
+ * LDS, matrix-core bound); other bounds process rows in chunks of 64. */
+enum { LSV_WIDE_ROWS = 272 };
 int lsv_verify_block(const lsv_model_config* cfg, const void* d_packed, void* d_kv, int32_t capacity,
                      int32_t batch, const int32_t* d_seq_len, const int32_t* d_tokens,
                      const int32_t* d_row_offsets, int32_t max_rows, int32_t max_ctx, float* d_logits,

@@ -72,18 +72,36 @@ struct VerifyWs {
   void* u;         // [M_max][ldu], columns >= d_ff stay zero
   float* o_part;   // attention split partials
   float* ml_part;
+  float* part;     // wide blocks: k-split partials
+  int* counters;   // wide blocks: per-tile arrivals, zero between calls
   int ldu;
   size_t total;
 };
 
 struct VerifyPlan {
   int MT;
+  bool wide;  // bf16 blocks of 64 < rows <= kWideRows: all rows per workgroup, activations via LDS
+  WidePlan w[5];
+  size_t part_floats;
+  int max_tiles;
   AttnPlan attn;
 };
 
-static VerifyPlan plan_verify(const Shape& s, int batch, int max_rows, int max_ctx) {
+static VerifyPlan plan_verify(const Shape& s, const ModelLayout& ml, int batch, int max_rows, int max_ctx) {
   VerifyPlan v;
   v.MT = max_rows > 64 ? 4 : (max_rows + 15) / 16;  // activation tiles per 64-row chunk
+  v.wide = s.dtype == LSV_DTYPE_BF16 && max_rows > 64 && max_rows <= kWideRows;
+  v.part_floats = 0;
+  v.max_tiles = 1;
+  if (v.wide) {
+    const PackedMat* mats[5] = {&ml.qkv, &ml.o, &ml.gateup, &ml.down, &ml.lm_head};
+    for (int k = 0; k < 5; ++k) {
+      v.w[k] = plan_wide(mats[k]->Nt, mats[k]->Kt);
+      const size_t pf = wide_part_floats(v.w[k], max_rows);
+      v.part_floats = pf > v.part_floats ? pf : v.part_floats;
+      v.max_tiles = v.w[k].tiles > v.max_tiles ? v.w[k].tiles : v.max_tiles;
+    }
+  }
   v.attn = plan_attention(batch, s.nkv, max_ctx);
   return v;
 }
@@ -111,6 +129,8 @@ static VerifyWs carve_verify(const Shape& s, const ModelLayout& ml, const Verify
   } else {
     w.o_part = w.ml_part = nullptr;
   }
+  w.part = (float*)take(sizeof(float) * v.part_floats);
+  w.counters = (int*)take(sizeof(int) * (size_t)v.max_tiles);
   w.total = off;
   return w;
 }
@@ -118,7 +138,7 @@ static VerifyWs carve_verify(const Shape& s, const ModelLayout& ml, const Verify
 size_t verify_workspace_bytes(const Shape& s, int batch, int max_rows, int max_ctx) {
   (void)batch;
   ModelLayout ml = model_layout(s);
-  VerifyPlan v = plan_verify(s, batch, max_rows, max_ctx);
+  VerifyPlan v = plan_verify(s, ml, batch, max_rows, max_ctx);
   return carve_verify(s, ml, v, max_rows, nullptr).total;
 }
 
@@ -190,9 +210,10 @@ __global__ void __launch_bounds__(256) embed_kernel(const T* __restrict__ E, int
 int launch_verify(const Shape& s, const ModelLayout& ml, const void* packed, void* kv, int capacity, int batch,
                   const int32_t* seq_len, const int32_t* tokens, const int32_t* row_offsets, int max_rows,
                   int max_ctx, float* logits, int32_t* status, void* ws, size_t ws_bytes, hipStream_t st) {
-  const VerifyPlan v = plan_verify(s, batch, max_rows, max_ctx);
+  const VerifyPlan v = plan_verify(s, ml, batch, max_rows, max_ctx);
   const VerifyWs w = carve_verify(s, ml, v, max_rows, ws);
   if (w.total > ws_bytes) return LSV_ERR_INVALID_ARG;
+  if (v.part_floats * sizeof(float) >= ((size_t)1 << 31)) return LSV_ERR_UNSUPPORTED;  // 32-bit buffer offsets
   const char* P = (const char*)packed;
   const bool bf16 = s.dtype == LSV_DTYPE_BF16;
 
@@ -230,7 +251,16 @@ int launch_verify(const Shape& s, const ModelLayout& ml, const void* packed, voi
     a.Kt = pm.Kt;
     const int idx = kind == GEMM_LMHEAD ? 0 : a.layer_index;
     timing_before((int)kind, idx, st);
-    const int rc = launch_gemm(s.dtype, kind, v.MT, a, st);
+    int rc;
+    if (v.wide) {
+      a.part = w.part;
+      a.part_bytes = sizeof(float) * v.part_floats;
+      a.splits = v.w[kind].splits;
+      a.counters = w.counters;
+      rc = launch_gemm_wide(kind, a, v.w[kind], st);
+    } else {
+      rc = launch_gemm(s.dtype, kind, v.MT, a, st);
+    }
     timing_after((int)kind, idx, st);
     return rc;
   };

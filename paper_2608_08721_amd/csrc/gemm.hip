@@ -149,7 +149,183 @@ LSV_DEV float inv_rms_of_row(const GemmArgs& a, int m, int g4) {
   return 1.0f / sqrtf(ss / (float)a.K + a.eps);
 }
 
+// The same value as inv_rms_of_row, summed by one thread in the same order: lane group
+// g (of 4) adds float4s g, g+4, ... each as ((x+y)+z)+w, and the groups combine as
+// (g0+g1)+(g2+g3).
+LSV_DEV float inv_rms_serial(const GemmArgs& a, int m) {
+  const GLOBAL f32x4_t* st = (const GLOBAL f32x4_t*)(a.stats + (size_t)min(m, a.M_max - 1) * a.P);
+  const int P4 = a.P >> 2;
+  float part[4];
+#pragma unroll
+  for (int g = 0; g < 4; ++g) {
+    float ss = 0.f;
+    for (int i = g; i < P4; i += 16) {
+      f32x4_t v[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) v[u] = i + 4 * u < P4 ? st[i + 4 * u] : f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int u = 0; u < 4; ++u) ss += ((v[u][0] + v[u][1]) + v[u][2]) + v[u][3];
+    }
+    part[g] = ss;
+  }
+  const float ss = (part[0] + part[1]) + (part[2] + part[3]);
+  return 1.0f / sqrtf(ss / (float)a.K + a.eps);
+}
+
 // ------------------------------------------------------------------ the GEMM
+// Epilogue of one wave: lane holds output columns n0..n0+3 (weight rows) of activation
+// row m for each of its TPW fragment rows and MT activation tiles.  Row inputs that need
+// dependent loads (1/rms, cache positions) are read here, off the weight stream's
+// critical path.  HPRE: the residual was loaded ahead into hpre (else it is read here).
+// Per-row inputs of the epilogue gathered once per workgroup (wide blocks): 1/rms and the
+// sequence / cache position of every row, in LDS.
+struct RowInputs {
+  const float* inv;  // [rows]
+  const int* seq;    // [rows]
+  const int* pos;    // [rows]
+};
+
+template <typename T, int MT, int TPW, int EPI, bool HPRE>
+LSV_DEV void gemm_epilogue(const GemmArgs& a, const int M, const int m0, const int tn0, const bool (&tvalid)[TPW],
+                           f32x4_t (&acc)[TPW][MT], const f32x4_t (&hpre)[TPW][MT], const RowInputs* rin = nullptr) {
+  constexpr bool RMS = EPI != EPI_RESID;
+  const int lane = threadIdx.x & 63, l16 = lane & 15, g4 = lane >> 4;
+  float inv[MT];
+  if (RMS) {
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+      const int m = m0 + mt * 16 + l16;
+      inv[mt] = rin ? rin->inv[min(m, a.M_max - 1)] : inv_rms_of_row(a, m, g4);
+    }
+  }
+  int qkv_b[MT], qkv_pos[MT];
+  if (EPI == EPI_QKV) {
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+      const int m = min(m0 + mt * 16 + l16, a.M_max - 1);
+      if (rin) {
+        qkv_b[mt] = rin->seq[m];
+        qkv_pos[mt] = rin->pos[m];
+      } else {
+        const int b = seq_of_row(a.row_offsets, a.batch, m);
+        qkv_b[mt] = b;
+        qkv_pos[mt] = GL(a.seq_len)[b] + (m - GL(a.row_offsets)[b]);
+      }
+    }
+  }
+  if (EPI == EPI_LOGITS) {
+#pragma unroll
+    for (int t = 0; t < TPW; ++t)
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) {
+        const int m = m0 + mt * 16 + l16, n0 = (tn0 + t) * 16 + 4 * g4;
+        if (m >= M || !tvalid[t]) continue;
+        const f32x4_t v = acc[t][mt] * inv[mt];
+        GLOBAL float* o = GL(a.out_f32) + (size_t)m * a.ldo;
+        if (n0 + 3 < a.N && (a.ldo & 3) == 0) {
+          *(GLOBAL f32x4_t*)(o + n0) = v;
+        } else {
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            if (n0 + r < a.N) o[n0 + r] = v[r];
+        }
+      }
+  } else if (EPI == EPI_QKV) {
+      const int qrows = a.nq * a.hd, krows = a.nkv * a.hd;
+#pragma unroll
+      for (int t = 0; t < TPW; ++t)
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+          const int m = m0 + mt * 16 + l16, n0 = (tn0 + t) * 16 + 4 * g4;
+          if (m >= M || !tvalid[t] || n0 >= qrows + 2 * krows) continue;
+          const int b = qkv_b[mt], pos = qkv_pos[mt];
+          const f32x4_t v = acc[t][mt] * inv[mt];
+          if (n0 < qrows + krows) {
+            const bool isq = n0 < qrows;
+            const int local = isq ? n0 : n0 - qrows;
+            const int head = local / a.hd, i0 = (local % a.hd) >> 1;  // pairs (i0, i0+hd/2), (i0+1, i0+1+hd/2)
+            float out[4];
+#pragma unroll
+            for (int pr = 0; pr < 2; ++pr) {
+              // angle = pos * base^(-2i/hd) in fp64, reduced to [-pi, pi] in fp64, then fp32 sin/cos
+              const int i = i0 + pr;
+              const double inv_freq = exp2(-(double)(2 * i) / (double)a.hd * a.log2_rope_base);
+              const double ang = (double)pos * inv_freq;
+              const double red2pi = ang - 6.283185307179586 * rint(ang * 0.15915494309189535);
+              float sn, cs;
+              sincosf((float)red2pi, &sn, &cs);
+              const float x1 = v[2 * pr], x2 = v[2 * pr + 1];
+              out[2 * pr] = x1 * cs - x2 * sn;
+              out[2 * pr + 1] = x2 * cs + x1 * sn;
+            }
+            T* dst;
+            if (isq) {
+              dst = (T*)a.q_out + ((size_t)m * a.nq + head) * a.hd;
+            } else {
+              if (pos < 0 || pos >= a.capacity) continue;
+              dst = (T*)a.kv + ((((size_t)a.layer * 2 + 0) * a.batch + b) * a.nkv + head) * (size_t)a.capacity * a.hd +
+                    (size_t)pos * a.hd;
+            }
+            GLOBAL T* gd = GL(dst);
+            gd[i0] = from_f32<T>(out[0]);
+            gd[i0 + a.hd / 2] = from_f32<T>(out[1]);
+            gd[i0 + 1] = from_f32<T>(out[2]);
+            gd[i0 + 1 + a.hd / 2] = from_f32<T>(out[3]);
+          } else {
+            if (pos < 0 || pos >= a.capacity) continue;
+            // V rows are stored transposed: [head_dim][capacity], column v_column(pos)
+            const int local = n0 - qrows - krows;
+            const int head = local / a.hd, d0 = local % a.hd;
+            GLOBAL T* dst = GL((T*)a.kv) +
+                            ((((size_t)a.layer * 2 + 1) * a.batch + b) * a.nkv + head) * (size_t)a.capacity * a.hd +
+                            (size_t)d0 * a.capacity + v_column(pos);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) dst[(size_t)r * a.capacity] = from_f32<T>(v[r]);
+          }
+        }
+    } else if (EPI == EPI_RESID) {
+      // h += y; the storage-type copy of h for the next consumer; per-row sum of squares of
+      // the new h over this fragment row's 16 columns (stats[m][n / 16])
+#pragma unroll
+      for (int t = 0; t < TPW; ++t)
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+          const int m = m0 + mt * 16 + l16, n0 = (tn0 + t) * 16 + 4 * g4;
+          float ss = 0.f;
+          if (m < M && tvalid[t]) {
+            const f32x4_t hv = HPRE ? hpre[t][mt] : *(const GLOBAL f32x4_t*)(a.h_out + (size_t)m * a.N + n0);
+            const f32x4_t h4 = hv + acc[t][mt];
+            *(GLOBAL f32x4_t*)(a.h_out + (size_t)m * a.N + n0) = h4;
+            if (a.hx_out) store4((T*)a.hx_out + (size_t)m * a.N + n0, h4);
+            ss = ((h4[0] * h4[0] + h4[1] * h4[1]) + h4[2] * h4[2]) + h4[3] * h4[3];
+          }
+          ss += __shfl_xor(ss, 16, kWave);
+          ss += __shfl_xor(ss, 32, kWave);
+          if (g4 == 0 && m < M && tvalid[t]) GL(a.stats_out)[(size_t)m * (a.N / 16) + tn0 + t] = ss;
+        }
+    } else if (EPI == EPI_SWIGLU) {
+      static_assert(EPI != EPI_SWIGLU || TPW == 2, "SwiGLU pairs a gate and an up fragment row");
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) {
+        const int m = m0 + mt * 16 + l16, f0 = (tn0 >> 1) * 16 + 4 * g4;
+        if (m >= M || !tvalid[0]) continue;
+        f32x4_t out;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float gt = acc[0][mt][r] * inv[mt], up = acc[TPW - 1][mt][r] * inv[mt];
+          out[r] = gt / (1.0f + expf(-gt)) * up;
+        }
+        T* dst = (T*)a.u_out + (size_t)m * a.ldu + f0;
+        if (f0 + 3 < a.F) {
+          store4(dst, out);
+        } else {
+          for (int r = 0; r < 4; ++r)
+            if (f0 + r < a.F) GL(dst)[r] = from_f32<T>(out[r]);
+        }
+      }
+    }
+}
+
 template <typename T, int MT, int TPW, int KS, int U, int NS, int EPI, int MT_MAX>
 LSV_DEV void gemm_body(const GemmArgs& a, const int M, const int tile, const int m0,
                        f32x4_t (*red)[TPW][MT_MAX][kWave]) {
@@ -262,134 +438,7 @@ LSV_DEV void gemm_body(const GemmArgs& a, const int M, const int tile, const int
         for (int mt = 0; mt < MT; ++mt) acc[t][mt] += red[w - 1][t][mt][lane];
   }
 
-  // ---- epilogues (wave 0); lane holds output columns n0..n0+3 (weight rows) of activation row m.
-  // Row inputs that need dependent loads (1/rms, cache positions) are read here, off the
-  // weight stream's critical path.
-  float inv[MT];
-  if (RMS) {
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) inv[mt] = inv_rms_of_row(a, m0 + mt * 16 + l16, g4);
-  }
-  int qkv_b[MT], qkv_pos[MT];
-  if (EPI == EPI_QKV) {
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-      const int m = min(m0 + mt * 16 + l16, a.M_max - 1);
-      const int b = seq_of_row(a.row_offsets, a.batch, m);
-      qkv_b[mt] = b;
-      qkv_pos[mt] = GL(a.seq_len)[b] + (m - GL(a.row_offsets)[b]);
-    }
-  }
-  if (EPI == EPI_LOGITS) {
-#pragma unroll
-    for (int t = 0; t < TPW; ++t)
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt) {
-        const int m = m0 + mt * 16 + l16, n0 = (tn0 + t) * 16 + 4 * g4;
-        if (m >= M || !tvalid[t]) continue;
-        const f32x4_t v = acc[t][mt] * inv[mt];
-        GLOBAL float* o = GL(a.out_f32) + (size_t)m * a.ldo;
-        if (n0 + 3 < a.N && (a.ldo & 3) == 0) {
-          *(GLOBAL f32x4_t*)(o + n0) = v;
-        } else {
-#pragma unroll
-          for (int r = 0; r < 4; ++r)
-            if (n0 + r < a.N) o[n0 + r] = v[r];
-        }
-      }
-  } else if (EPI == EPI_QKV) {
-      const int qrows = a.nq * a.hd, krows = a.nkv * a.hd;
-#pragma unroll
-      for (int t = 0; t < TPW; ++t)
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt) {
-          const int m = m0 + mt * 16 + l16, n0 = (tn0 + t) * 16 + 4 * g4;
-          if (m >= M || !tvalid[t] || n0 >= qrows + 2 * krows) continue;
-          const int b = qkv_b[mt], pos = qkv_pos[mt];
-          const f32x4_t v = acc[t][mt] * inv[mt];
-          if (n0 < qrows + krows) {
-            const bool isq = n0 < qrows;
-            const int local = isq ? n0 : n0 - qrows;
-            const int head = local / a.hd, i0 = (local % a.hd) >> 1;  // pairs (i0, i0+hd/2), (i0+1, i0+1+hd/2)
-            float out[4];
-#pragma unroll
-            for (int pr = 0; pr < 2; ++pr) {
-              // angle = pos * base^(-2i/hd) in fp64, reduced to [-pi, pi] in fp64, then fp32 sin/cos
-              const int i = i0 + pr;
-              const double inv_freq = exp2(-(double)(2 * i) / (double)a.hd * a.log2_rope_base);
-              const double ang = (double)pos * inv_freq;
-              const double red2pi = ang - 6.283185307179586 * rint(ang * 0.15915494309189535);
-              float sn, cs;
-              sincosf((float)red2pi, &sn, &cs);
-              const float x1 = v[2 * pr], x2 = v[2 * pr + 1];
-              out[2 * pr] = x1 * cs - x2 * sn;
-              out[2 * pr + 1] = x2 * cs + x1 * sn;
-            }
-            T* dst;
-            if (isq) {
-              dst = (T*)a.q_out + ((size_t)m * a.nq + head) * a.hd;
-            } else {
-              if (pos < 0 || pos >= a.capacity) continue;
-              dst = (T*)a.kv + ((((size_t)a.layer * 2 + 0) * a.batch + b) * a.nkv + head) * (size_t)a.capacity * a.hd +
-                    (size_t)pos * a.hd;
-            }
-            GLOBAL T* gd = GL(dst);
-            gd[i0] = from_f32<T>(out[0]);
-            gd[i0 + a.hd / 2] = from_f32<T>(out[1]);
-            gd[i0 + 1] = from_f32<T>(out[2]);
-            gd[i0 + 1 + a.hd / 2] = from_f32<T>(out[3]);
-          } else {
-            if (pos < 0 || pos >= a.capacity) continue;
-            // V rows are stored transposed: [head_dim][capacity], column v_column(pos)
-            const int local = n0 - qrows - krows;
-            const int head = local / a.hd, d0 = local % a.hd;
-            GLOBAL T* dst = GL((T*)a.kv) +
-                            ((((size_t)a.layer * 2 + 1) * a.batch + b) * a.nkv + head) * (size_t)a.capacity * a.hd +
-                            (size_t)d0 * a.capacity + v_column(pos);
-#pragma unroll
-            for (int r = 0; r < 4; ++r) dst[(size_t)r * a.capacity] = from_f32<T>(v[r]);
-          }
-        }
-    } else if (EPI == EPI_RESID) {
-      // h += y; the storage-type copy of h for the next consumer; per-row sum of squares of
-      // the new h over this fragment row's 16 columns (stats[m][n / 16])
-#pragma unroll
-      for (int t = 0; t < TPW; ++t)
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt) {
-          const int m = m0 + mt * 16 + l16, n0 = (tn0 + t) * 16 + 4 * g4;
-          float ss = 0.f;
-          if (m < M && tvalid[t]) {
-            const f32x4_t h4 = hpre[t][mt] + acc[t][mt];
-            *(GLOBAL f32x4_t*)(a.h_out + (size_t)m * a.N + n0) = h4;
-            if (a.hx_out) store4((T*)a.hx_out + (size_t)m * a.N + n0, h4);
-            ss = ((h4[0] * h4[0] + h4[1] * h4[1]) + h4[2] * h4[2]) + h4[3] * h4[3];
-          }
-          ss += __shfl_xor(ss, 16, kWave);
-          ss += __shfl_xor(ss, 32, kWave);
-          if (g4 == 0 && m < M && tvalid[t]) GL(a.stats_out)[(size_t)m * (a.N / 16) + tn0 + t] = ss;
-        }
-    } else if (EPI == EPI_SWIGLU) {
-      static_assert(EPI != EPI_SWIGLU || TPW == 2, "SwiGLU pairs a gate and an up fragment row");
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt) {
-        const int m = m0 + mt * 16 + l16, f0 = (tn0 >> 1) * 16 + 4 * g4;
-        if (m >= M || !tvalid[0]) continue;
-        f32x4_t out;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const float gt = acc[0][mt][r] * inv[mt], up = acc[TPW - 1][mt][r] * inv[mt];
-          out[r] = gt / (1.0f + expf(-gt)) * up;
-        }
-        T* dst = (T*)a.u_out + (size_t)m * a.ldu + f0;
-        if (f0 + 3 < a.F) {
-          store4(dst, out);
-        } else {
-          for (int r = 0; r < 4; ++r)
-            if (f0 + r < a.F) GL(dst)[r] = from_f32<T>(out[r]);
-        }
-      }
-    }
+  gemm_epilogue<T, MT, TPW, EPI, true>(a, M, m0, tn0, tvalid, acc, hpre);
 }
 
 // Launch configuration of each product: fragment rows per wave (TPW), k-slices = waves
@@ -470,6 +519,192 @@ static int launch_typed(GemmKind kind, int MT, const GemmArgs& a, hipStream_t st
     case GEMM_LMHEAD: return launch_mt<T, GEMM_LMHEAD>(MT, a, st);
   }
   return LSV_ERR_UNSUPPORTED;
+}
+
+// ------------------------------------------------------------------ wide blocks
+// Batched verification (64 < rows <= kWideRows): the matrix cores become the bound, so a
+// workgroup keeps every activation row and shares the activation operand through LDS.
+// Workgroup = 4 waves x 2 fragment rows (128 output columns) x one of `splits` k ranges.
+// Each k-step's activation slab (rows x 32 columns, one fragment per 16 rows) is staged in
+// LDS (double buffered) by the whole workgroup and multiplied by every wave with its own
+// weight fragments: 2 x 17 MFMAs per k-step and wave.  Slab pieces and weight fragments of
+// the next kWideRing k-steps are in flight in a register ring.  A split
+// group hands fp32 partials over with 16-byte device-scope stores and a device-scope
+// counter; the last arrival reads them back in split order (deterministic) and runs the
+// epilogue.
+constexpr int kWideMT = kWideRows / 16;  // activation tiles
+constexpr int kWideRing = 3;            // k-steps of loads in flight (register ring)
+constexpr int kWideTPW = 2;             // fragment rows per wave
+
+LSV_DEV __amdgpu_buffer_rsrc_t part_rsrc(float* base, size_t bytes) {
+  // raw buffer over the partials (word 3 = the gfx9-family raw-buffer format)
+  return __builtin_amdgcn_make_buffer_rsrc(base, 0, (int)(bytes > 0x7fffffffu ? 0x7fffffffu : bytes), 0x00020000);
+}
+constexpr int kDeviceScope = 16;  // buffer cache policy: sc1 (coherent at device scope)
+
+template <int EPI>
+__global__ void __launch_bounds__(256) gemm_wide_kernel(GemmArgs a) {
+  using T = bf16_t;
+  constexpr int TPW = kWideTPW, MT = kWideMT, KT = 32, EPL = 8, R = kWideRing;
+  constexpr int PIECES = MT * kWave, PPT = (PIECES + 255) / 256;  // 16-byte pieces of one k-step's slab
+  __shared__ u32x4_t Bs[2][MT][kWave];
+  __shared__ int flag;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, l16 = lane & 15, g4 = lane >> 4;
+  const int S = a.splits, tile = blockIdx.x / S, j = blockIdx.x % S;
+  const int k0 = (int)((long long)j * a.Kt / S), k1 = (int)((long long)(j + 1) * a.Kt / S), nk = k1 - k0;
+  const int M = min(GL(a.row_offsets)[a.batch], a.M_max);  // never trust device rows beyond the host bound
+  const int mt_n = (M + 15) / 16;                           // <= MT: the host bound is <= kWideRows
+  const int tn0 = (tile * 4 + wave) * TPW;
+  bool tvalid[TPW];
+  const GLOBAL u32x4_t* wp[TPW];
+#pragma unroll
+  for (int t = 0; t < TPW; ++t) {
+    tvalid[t] = tn0 + t < a.Nt;
+    wp[t] = (const GLOBAL u32x4_t*)a.W + ((size_t)(tvalid[t] ? tn0 + t : 0) * a.Kt + k0) * 64 + lane;
+  }
+  const GLOBAL T* xg = (const GLOBAL T*)a.x;
+
+  // Register ring of R k-steps: activation slab pieces and the wave's weight fragments.
+  // Slab piece p = (mt, ln): activation tile mt, lane ln of its fragment.
+  u32x4_t bst[R][PPT], wa[R][TPW];
+  auto issue = [&](int st, int k) {
+    const int kk = max(min(k, nk - 1), 0);
+#pragma unroll
+    for (int i = 0; i < PPT; ++i) {
+      const int p = tid + 256 * i, mt = p / kWave, ln = p % kWave;
+      if (p < PIECES && mt < mt_n) {
+        const int row = min(mt * 16 + (ln & 15), a.M_max - 1);
+        bst[st][i] = *(const GLOBAL u32x4_t*)(xg + (size_t)row * a.ldx + (size_t)(k0 + kk) * KT + (ln >> 4) * EPL);
+      }
+    }
+#pragma unroll
+    for (int t = 0; t < TPW; ++t) wa[st][t] = wp[t][(size_t)kk * 64];
+  };
+  auto store = [&](int st, int buf) {
+#pragma unroll
+    for (int i = 0; i < PPT; ++i) {
+      const int p = tid + 256 * i;
+      if (p < PIECES && p / kWave < mt_n) (&Bs[buf][0][0])[p] = bst[st][i];
+    }
+  };
+  f32x4_t acc[TPW][MT];
+#pragma unroll
+  for (int t = 0; t < TPW; ++t)
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) acc[t][mt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  u32x4_t wcur[TPW];
+  auto compute = [&](int buf) {
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+      if (mt >= mt_n) break;
+      const u32x4_t b = Bs[buf][mt][lane];
+#pragma unroll
+      for (int t = 0; t < TPW; ++t) mfma_frag(wcur[t], b, acc[t][mt], T{});
+    }
+  };
+  // k-step c: its slab sits in LDS buffer c & 1 (stored during step c - 1); the slab of
+  // step c + 1 moves from registers to the other buffer; step c + R is issued into the
+  // register stage that step c freed.  One barrier per step.
+  auto step = [&](int st, int c) {
+    // st = c % R: stage of step c (already consumed into LDS); stage of c + 1 is (st + 1) % R
+#pragma unroll
+    for (int t = 0; t < TPW; ++t) wcur[t] = wa[st][t];
+    if (c + 1 < nk) store((st + 1) % R, (c + 1) & 1);
+    issue(st, c + R);
+    compute(c & 1);
+    __syncthreads();
+  };
+#pragma unroll
+  for (int st = 0; st < R; ++st) issue(st, st);
+  store(0, 0);
+  __syncthreads();
+  int c = 0;
+  for (; c + R <= nk; c += R) {
+#pragma unroll
+    for (int st = 0; st < R; ++st) step(st, c + st);
+  }
+#pragma unroll
+  for (int st = 0; st < R; ++st)
+    if (c + st < nk) step(st, c + st);
+
+  if (S > 1) {
+    const __amdgpu_buffer_rsrc_t prs = part_rsrc(a.part, a.part_bytes);
+    constexpr int COLS = 4 * TPW * 16;  // output columns of the workgroup
+    const size_t slot = (size_t)tile * S + j;
+#pragma unroll
+    for (int t = 0; t < TPW; ++t)
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) {
+        const int m = mt * 16 + l16, col = (wave * TPW + t) * 16 + 4 * g4;
+        if (mt < mt_n && m < M) {
+          const int off = (int)(((slot * a.M_max + m) * COLS + col) * sizeof(float));
+          __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4_t, acc[t][mt]), prs, off, 0, kDeviceScope);
+        }
+      }
+    __builtin_amdgcn_s_waitcnt(0);  // this thread's partials have reached the coherent level
+    __syncthreads();
+    if (tid == 0)
+      flag = __hip_atomic_fetch_add(&a.counters[tile], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == S - 1;
+    __syncthreads();
+    if (flag == 0) return;
+#pragma unroll
+    for (int t = 0; t < TPW; ++t)
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) {
+        const int m = mt * 16 + l16, col = (wave * TPW + t) * 16 + 4 * g4;
+        f32x4_t sum = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        if (mt < mt_n && m < M) {
+          for (int jj = 0; jj < S; ++jj) {
+            const int off = (int)(((((size_t)tile * S + jj) * a.M_max + m) * COLS + col) * sizeof(float));
+            sum += __builtin_bit_cast(f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(prs, off, 0, kDeviceScope));
+          }
+        }
+        acc[t][mt] = sum;
+      }
+    if (tid == 0) __hip_atomic_store(&a.counters[tile], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  __shared__ float s_inv[kWideRows];
+  __shared__ int s_seq[kWideRows], s_pos[kWideRows];
+  for (int r = tid; r < a.M_max; r += 256) {
+    if (EPI != EPI_RESID) s_inv[r] = inv_rms_serial(a, r);
+    if (EPI == EPI_QKV) {
+      const int b = seq_of_row(a.row_offsets, a.batch, r);
+      s_seq[r] = b;
+      s_pos[r] = GL(a.seq_len)[b] + (r - GL(a.row_offsets)[b]);
+    }
+  }
+  __syncthreads();
+  const RowInputs rin{s_inv, s_seq, s_pos};
+  const f32x4_t none[TPW][MT] = {};
+  gemm_epilogue<T, MT, TPW, EPI, false>(a, M, 0, tn0, tvalid, acc, none, &rin);
+}
+
+WidePlan plan_wide(int Nt, int Kt) {
+  WidePlan p;
+  p.tiles = (Nt + 4 * kWideTPW - 1) / (4 * kWideTPW);
+  // one resident workgroup per compute unit (the accumulators fill the AGPRs); at least
+  // eight k-steps per workgroup
+  p.splits = 256 / p.tiles;
+  const int most = Kt / 8;
+  if (p.splits > most) p.splits = most;
+  if (p.splits < 1) p.splits = 1;
+  return p;
+}
+
+size_t wide_part_floats(const WidePlan& p, int M_max) {
+  return p.splits > 1 ? (size_t)p.tiles * p.splits * M_max * (4 * kWideTPW * 16) : 0;
+}
+
+int launch_gemm_wide(GemmKind kind, const GemmArgs& a, const WidePlan& p, hipStream_t st) {
+  const dim3 grid((unsigned)(p.tiles * p.splits)), block(256);
+  switch (kind) {
+    case GEMM_QKV: hipLaunchKernelGGL(gemm_wide_kernel<EPI_QKV>, grid, block, 0, st, a); break;
+    case GEMM_O: hipLaunchKernelGGL(gemm_wide_kernel<EPI_RESID>, grid, block, 0, st, a); break;
+    case GEMM_GATEUP: hipLaunchKernelGGL(gemm_wide_kernel<EPI_SWIGLU>, grid, block, 0, st, a); break;
+    case GEMM_DOWN: hipLaunchKernelGGL(gemm_wide_kernel<EPI_RESID>, grid, block, 0, st, a); break;
+    case GEMM_LMHEAD: hipLaunchKernelGGL(gemm_wide_kernel<EPI_LOGITS>, grid, block, 0, st, a); break;
+  }
+  return hipGetLastError() == hipSuccess ? LSV_OK : LSV_ERR_HIP;
 }
 
 int launch_gemm(int dtype, GemmKind kind, int MT, const GemmArgs& a, hipStream_t st) {

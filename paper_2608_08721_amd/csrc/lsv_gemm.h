@@ -29,6 +29,11 @@ struct GemmArgs {
   const float* stats;
   int P;
   float eps;
+  // wide blocks: k-split partials [tiles][splits][M_max][128] and per-tile arrival counters
+  float* part;
+  size_t part_bytes;
+  int splits;
+  int* counters;  // zero on entry and on exit
   // EPI_LOGITS
   float* out_f32;
   int ldo;
@@ -50,5 +55,14 @@ struct GemmArgs {
 
 // One launch: a workgroup per tile of output columns, the whole K per workgroup.
 int launch_gemm(int dtype, GemmKind kind, int MT, const GemmArgs& a, hipStream_t st);
+
+// Batched blocks (bf16, 64 < rows <= kWideRows): every row in one workgroup, activations via LDS.
+constexpr int kWideRows = LSV_WIDE_ROWS;
+struct WidePlan {
+  int tiles, splits;
+};
+WidePlan plan_wide(int Nt, int Kt);
+size_t wide_part_floats(const WidePlan& p, int M_max);
+int launch_gemm_wide(GemmKind kind, const GemmArgs& a, const WidePlan& p, hipStream_t st);
 
 }  // namespace lsv

@@ -13,7 +13,7 @@ LIB_PATH = os.path.join(_HERE, "liblsv.so")
 
 LSV_OK, LSV_ERR_INVALID_ARG, LSV_ERR_UNSUPPORTED, LSV_ERR_HIP, LSV_ERR_CAPACITY, LSV_ERR_NONFINITE = 0, -1, -2, -3, -4, -5
 LSV_DTYPE_F32, LSV_DTYPE_BF16 = 0, 1
-LSV_MAX_BATCH, LSV_MAX_ROWS, LSV_MAX_G, LSV_MAX_SEQ_ROWS = 64, 512, 64, 64
+LSV_MAX_BATCH, LSV_MAX_ROWS, LSV_MAX_G, LSV_MAX_SEQ_ROWS, LSV_WIDE_ROWS = 64, 512, 64, 64, 272
 LSV_KV_ALIGN = 64
 LSV_ACC_GREEDY, LSV_ACC_SAMPLE = 0, 1
 LSV_SEL_MARGINAL, LSV_SEL_EXHAUSTIVE, LSV_SEL_ALG1 = 0, 1, 2
