@@ -311,7 +311,8 @@ def main():
     # prefill rows per sequence and call: for batches, keep the whole block within the
     # batched GEMM path's row bound
     pre = 64 if B == 1 else max(1, min(64, lsv.LSV_WIDE_ROWS // B))
-    rows_buf = max(B * rows_seq, B * pre)
+    rows_step = B * rows_seq            # host row bound of the verify steps
+    rows_buf = max(rows_step, B * pre)  # buffers also hold a prefill chunk
     cap = runtime.kv_capacity(max(ctx) + rows_seq)
     cfg = runtime.model_config(m)
 
@@ -377,9 +378,9 @@ def main():
 
         def body():
             seq_work.copy_(seq_base)
-            lsv.lsv_verify_block(cfg, dm.buf, kv.buf, cap, B, seq_base, tok_g, ro, rows_buf, cap, logits, status,
+            lsv.lsv_verify_block(cfg, dm.buf, kv.buf, cap, B, seq_base, tok_g, ro, rows_step, cap, logits, status,
                                  ws.buf, ws.nbytes)
-            lsv.lsv_accept(lsv.LSV_ACC_GREEDY, B, m.vocab, logits, ro, rows_buf, rows_seq, tok_g, None, 0.0, 0, 0,
+            lsv.lsv_accept(lsv.LSV_ACC_GREEDY, B, m.vocab, logits, ro, rows_step, rows_seq, tok_g, None, 0.0, 0, 0,
                            acc, out, seq_work, status, aws.buf, aws.nbytes)
         body()
         graph = torch.cuda.CUDAGraph()
@@ -424,9 +425,9 @@ def main():
         seq_work.copy_(seq_base)
         lsv.lsv_select_length(lsv.LSV_SEL_MARGINAL, B, G, conf, cost_t, 1, G, 2.2, n_alg1, 0, gamma, aux, row_off,
                               status)
-        lsv.lsv_verify_block(cfg, dm.buf, kv.buf, cap, B, seq_base, tokens, row_off, rows_buf, cap, logits, status,
+        lsv.lsv_verify_block(cfg, dm.buf, kv.buf, cap, B, seq_base, tokens, row_off, rows_step, cap, logits, status,
                              ws.buf, ws.nbytes)
-        lsv.lsv_accept(lsv.LSV_ACC_GREEDY, B, m.vocab, logits, row_off, rows_buf, rows_seq, tokens, None, 0.0, 0, 0,
+        lsv.lsv_accept(lsv.LSV_ACC_GREEDY, B, m.vocab, logits, row_off, rows_step, rows_seq, tokens, None, 0.0, 0, 0,
                        acc, out, seq_work, status, aws.buf, aws.nbytes)
     step()
     torch.cuda.synchronize()

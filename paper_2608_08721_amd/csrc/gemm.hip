@@ -3,8 +3,9 @@
 // Y[M, N] = X[M, K] * W[N, K]^T with M = the block's rows (a few to 64) and N, K
 // in the thousands: the product streams W from HBM once, so the kernel is built
 // around that stream.  W is pre-packed into 1 KiB fragments (16 rows x 32 bf16,
-// or 16 rows x 16 fp32) laid out in the order a wave consumes them; each lane
-// loads 16 contiguous bytes, so one wave-wide load is one contiguous KiB.  The
+// or 16 rows x 16 fp32); each lane loads 16 contiguous bytes, so one wave-wide load
+// is one contiguous KiB.  Fragments are ordered in k blocks (frag_index): runs of 8
+// fragments of one row, all rows of a block before the next block.  The
 // fragment is the A operand of v_mfma_f32_16x16x32_bf16 (fp32: four
 // v_mfma_f32_16x16x4_f32), weight rows being the MFMA rows.  The B operand --
 // activation rows as MFMA columns -- is read the same way straight from the
@@ -43,7 +44,11 @@ __global__ void __launch_bounds__(256) pack_kernel(int kind, int N, int K, int N
   const size_t frag = gid >> 6;
   const int lane = (int)(gid & 63);
   if (frag >= (size_t)Nt * Kt) return;
-  const int tn = (int)(frag / Kt), tk = (int)(frag % Kt);
+  // inverse of frag_index: block of the k range, then row, then k inside the block
+  const int b = (int)(frag / ((size_t)Nt * kFragBlock));
+  const int k0 = b * kFragBlock, bs = Kt - k0 < kFragBlock ? Kt - k0 : kFragBlock;
+  const size_t rem = frag - (size_t)k0 * Nt;
+  const int tn = (int)(rem / bs), tk = k0 + (int)(rem % bs);
   const int pr = 16 * tn + (lane & 15);
   const int col0 = tk * KT + (lane >> 4) * EPL;
   const T* src = nullptr;
@@ -338,12 +343,13 @@ LSV_DEV void gemm_body(const GemmArgs& a, const int M, const int tile, const int
   const int k0 = (int)((long long)wave * a.Kt / KS), k1 = (int)((long long)(wave + 1) * a.Kt / KS);
   const int nk = k1 - k0;  // >= 0, and k0 < Kt for every wave
   bool tvalid[TPW];
-  const GLOBAL u32x4_t* wp[TPW];
+  int tr[TPW];  // fragment row of each of the wave's tiles (row 0 stands in past the end)
 #pragma unroll
   for (int t = 0; t < TPW; ++t) {
     tvalid[t] = tn0 + t < a.Nt;
-    wp[t] = (const GLOBAL u32x4_t*)a.W + ((size_t)(tvalid[t] ? tn0 + t : 0) * a.Kt + k0) * 64 + lane;
+    tr[t] = tvalid[t] ? tn0 + t : 0;
   }
+  const GLOBAL u32x4_t* wbase = (const GLOBAL u32x4_t*)a.W + lane;
 
   // ---- the residual this tile adds to (EPI_RESID, wave 0 runs the epilogue): its loads are
   // issued ahead of the weight stream and retire with it
@@ -384,7 +390,7 @@ LSV_DEV void gemm_body(const GemmArgs& a, const int M, const int tile, const int
       for (int u = 0; u < U; ++u) {
         const int kf = max(min(kb + u, nk - 1), 0);  // a slice may be empty when Kt < KS
 #pragma unroll
-        for (int t = 0; t < TPW; ++t) wa[st][u][t] = wp[t][(size_t)kf * 64];
+        for (int t = 0; t < TPW; ++t) wa[st][u][t] = wbase[frag_index(tr[t], k0 + kf, a.Nt, a.Kt) * 64];
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) xb[st][u][mt] = *(const GLOBAL u32x4_t*)(xp[mt] + (size_t)kf * KT);
       }
@@ -447,10 +453,10 @@ LSV_DEV void gemm_body(const GemmArgs& a, const int M, const int tile, const int
 // count that spreads evenly over the 256 compute units, and few waves per tile for the
 // long products.
 template <int KIND> struct GemmCfg;
-template <> struct GemmCfg<GEMM_QKV> { static constexpr int TPW = 1, KS = 2, U = 8, NS = 2, EPI = EPI_QKV; };
-template <> struct GemmCfg<GEMM_O> { static constexpr int TPW = 1, KS = 4, U = 8, NS = 2, EPI = EPI_RESID; };
+template <> struct GemmCfg<GEMM_QKV> { static constexpr int TPW = 1, KS = 2, U = 4, NS = 2, EPI = EPI_QKV; };
+template <> struct GemmCfg<GEMM_O> { static constexpr int TPW = 1, KS = 4, U = 4, NS = 2, EPI = EPI_RESID; };
 template <> struct GemmCfg<GEMM_GATEUP> { static constexpr int TPW = 2, KS = 1, U = 4, NS = 3, EPI = EPI_SWIGLU; };
-template <> struct GemmCfg<GEMM_DOWN> { static constexpr int TPW = 1, KS = 4, U = 8, NS = 2, EPI = EPI_RESID; };
+template <> struct GemmCfg<GEMM_DOWN> { static constexpr int TPW = 1, KS = 4, U = 4, NS = 2, EPI = EPI_RESID; };
 template <> struct GemmCfg<GEMM_LMHEAD> { static constexpr int TPW = 2, KS = 1, U = 4, NS = 3, EPI = EPI_LOGITS; };
 
 // Wide activation tiles (prefill bounds) use a shallower pipeline to stay in registers.
@@ -556,12 +562,13 @@ __global__ void __launch_bounds__(256) gemm_wide_kernel(GemmArgs a) {
   const int mt_n = (M + 15) / 16;                           // <= MT: the host bound is <= kWideRows
   const int tn0 = (tile * 4 + wave) * TPW;
   bool tvalid[TPW];
-  const GLOBAL u32x4_t* wp[TPW];
+  int tr[TPW];
 #pragma unroll
   for (int t = 0; t < TPW; ++t) {
     tvalid[t] = tn0 + t < a.Nt;
-    wp[t] = (const GLOBAL u32x4_t*)a.W + ((size_t)(tvalid[t] ? tn0 + t : 0) * a.Kt + k0) * 64 + lane;
+    tr[t] = tvalid[t] ? tn0 + t : 0;
   }
+  const GLOBAL u32x4_t* wbase = (const GLOBAL u32x4_t*)a.W + lane;
   const GLOBAL T* xg = (const GLOBAL T*)a.x;
 
   // Register ring of R k-steps: activation slab pieces and the wave's weight fragments.
@@ -578,7 +585,7 @@ __global__ void __launch_bounds__(256) gemm_wide_kernel(GemmArgs a) {
       }
     }
 #pragma unroll
-    for (int t = 0; t < TPW; ++t) wa[st][t] = wp[t][(size_t)kk * 64];
+    for (int t = 0; t < TPW; ++t) wa[st][t] = wbase[frag_index(tr[t], k0 + kk, a.Nt, a.Kt) * 64];
   };
   auto store = [&](int st, int buf) {
 #pragma unroll

@@ -40,6 +40,19 @@ struct PackedMat {
   int N, K;       // logical rows (out features) and columns (in features)
   int Nt, Kt;     // fragment counts (zero-padded)
 };
+
+// Fragment order of a packed matrix: the k range is cut into blocks of kFragBlock
+// fragments; block b holds, for every fragment row in turn, that row's fragments of the
+// block (the last block may be shorter).  A wave still streams contiguous KiB runs
+// (kFragBlock fragments of one row), while the waves of a launch, which advance through
+// k at the same pace, keep their concurrent reads within one block: a narrow window of
+// DRAM pages instead of one page per fragment row.
+constexpr int kFragBlock = 8;
+__host__ __device__ inline size_t frag_index(int tn, int k, int Nt, int Kt) {
+  const int b = k / kFragBlock, k0 = b * kFragBlock;
+  const int bs = Kt - k0 < kFragBlock ? Kt - k0 : kFragBlock;  // size of block b
+  return (size_t)k0 * Nt + (size_t)tn * bs + (k - k0);
+}
 // RMSNorm gains are folded into the projection that follows them (QKV, gate/up,
 // LM head), so the packed model stores no separate gains.
 struct ModelLayout {
