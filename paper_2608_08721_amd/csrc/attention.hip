@@ -22,12 +22,16 @@ namespace lsv {
 
 constexpr int kCh = kAttnChunk;  // keys per chunk
 constexpr int kQpw = 1;          // query tiles per wave and pass
-constexpr int kAttnWgs = 512;    // split-kernel workgroups aimed for
+constexpr int kAttnWgs = 256;     // split-kernel workgroups aimed for
+constexpr int kMaxChunksPerSplit = 16;  // a split walks its chunks in sequence
 
 AttnPlan plan_attention(int batch, int nkv, int max_ctx) {
   const int n_chunks = (max_ctx + kCh - 1) / kCh;
   const int units = batch * nkv;
+  // about one workgroup per compute unit, but no split longer than kMaxChunksPerSplit chunks
   int want = (kAttnWgs + units - 1) / units;
+  const int by_length = (n_chunks + kMaxChunksPerSplit - 1) / kMaxChunksPerSplit;
+  if (want < by_length) want = by_length;
   if (want > n_chunks) want = n_chunks;
   if (want < 1) want = 1;
   AttnPlan p;
