@@ -79,31 +79,40 @@ struct VerifyWs {
 };
 
 struct VerifyPlan {
-  int MT;
+  int MT, batch;
   bool wide;  // bf16 blocks of 64 < rows <= kWideRows: all rows per workgroup, activations via LDS
   WidePlan w[5];
   size_t part_floats;
-  int max_tiles;
   AttnPlan attn;
 };
 
 static VerifyPlan plan_verify(const Shape& s, const ModelLayout& ml, int batch, int max_rows, int max_ctx) {
   VerifyPlan v;
+  v.batch = batch;
   v.MT = max_rows > 64 ? 4 : (max_rows + 15) / 16;  // activation tiles per 64-row chunk
   v.wide = s.dtype == LSV_DTYPE_BF16 && max_rows > 64 && max_rows <= kWideRows;
   v.part_floats = 0;
-  v.max_tiles = 1;
   if (v.wide) {
     const PackedMat* mats[5] = {&ml.qkv, &ml.o, &ml.gateup, &ml.down, &ml.lm_head};
     for (int k = 0; k < 5; ++k) {
       v.w[k] = plan_wide(mats[k]->Nt, mats[k]->Kt);
       const size_t pf = wide_part_floats(v.w[k], max_rows);
       v.part_floats = pf > v.part_floats ? pf : v.part_floats;
-      v.max_tiles = v.w[k].tiles > v.max_tiles ? v.w[k].tiles : v.max_tiles;
     }
   }
   v.attn = plan_attention(batch, s.nkv, max_ctx);
   return v;
+}
+
+// Most tiles any batched GEMM of this model can have (sizes the arrival counters).
+static int max_wide_tiles(const ModelLayout& ml) {
+  const PackedMat* mats[5] = {&ml.qkv, &ml.o, &ml.gateup, &ml.down, &ml.lm_head};
+  int t = 1;
+  for (int k = 0; k < 5; ++k) {
+    const int tiles = plan_wide(mats[k]->Nt, mats[k]->Kt).tiles;
+    t = tiles > t ? tiles : t;
+  }
+  return t;
 }
 
 static VerifyWs carve_verify(const Shape& s, const ModelLayout& ml, const VerifyPlan& v, int max_rows, void* base) {
@@ -115,6 +124,10 @@ static VerifyWs carve_verify(const Shape& s, const ModelLayout& ml, const Verify
     off = al256(off + bytes);
     return (void*)r;
   };
+  // Arrival counters first, sized by the model alone: they stay at zero between calls and
+  // keep their place whatever the batch, row and context bounds of a call, so one zeroed
+  // workspace serves calls with different bounds.
+  w.counters = (int*)take(sizeof(int) * (size_t)max_wide_tiles(ml));
   const int KT = s.dtype == LSV_DTYPE_BF16 ? 32 : 16;
   w.ldu = ml.down.Kt * KT;  // the down projection reads whole fragments of u
   w.h = (float*)take(sizeof(float) * (size_t)max_rows * s.d);
@@ -130,7 +143,6 @@ static VerifyWs carve_verify(const Shape& s, const ModelLayout& ml, const Verify
     w.o_part = w.ml_part = nullptr;
   }
   w.part = (float*)take(sizeof(float) * v.part_floats);
-  w.counters = (int*)take(sizeof(int) * (size_t)v.max_tiles);
   w.total = off;
   return w;
 }

@@ -29,11 +29,13 @@ class GpuModel:
         self.logits = torch.full((max_rows, shape.vocab), float("nan"), dtype=torch.float32, device=DEV)
         self.status = torch.full((batch,), 99, dtype=torch.int32, device=DEV)
 
-    def verify(self, seq_len, tokens, row_offsets, max_ctx=None):
+    def verify(self, seq_len, tokens, row_offsets, max_ctx=None, max_rows=None):
+        """One lsv_verify_block call; max_rows / max_ctx default to the buffers' bounds (a
+        smaller bound reuses the same workspace)."""
         M = int(row_offsets[-1])
         lsv.lsv_verify_block(self.cfg, self.dm.buf, self.kv.buf, self.capacity, self.batch, i32(seq_len),
-                             i32(tokens), i32(row_offsets), self.max_rows, max_ctx or self.capacity, self.logits,
-                             self.status, self.ws.buf, self.ws.nbytes)
+                             i32(tokens), i32(row_offsets), max_rows or self.max_rows, max_ctx or self.capacity,
+                             self.logits, self.status, self.ws.buf, self.ws.nbytes)
         torch.cuda.synchronize()
         return self.logits[:M].double().cpu().numpy(), self.status.cpu().numpy()
 

@@ -133,3 +133,28 @@ def test_llama8b_width_two_layers():
     shape = configs.LLAMA3_8B.with_layers(2)
     note("llama3-8b width, 2 layers: generating weights")
     _bf16_case(shape, 2, [2048], [17])
+
+
+def test_workspace_reused_across_bounds():
+    """One zeroed workspace serves calls with different row and context bounds (the arrival
+    counters keep their place): prefill with the 64-row bound, then verify blocks with the
+    17-, 64- and 5-row bounds and a smaller max_ctx, each against the oracle."""
+    shape = configs.TINY_BF16
+    w = gen.model_weights(shape, 14)
+    cap = 256
+    gm = GpuModel(shape, w, 1, cap)
+    om = OF.Model(shape, w)
+    oc = OF.KVCache(shape, 1, cap)
+    prompt = gen.prefix_ids(14, 1, [150], shape.vocab)[0]
+    g_last, _ = gm.prefill([prompt])
+    o_last, _ = OF.prefill(om, oc, [prompt])
+    assert row_rel_err(g_last, o_last).max() <= 2e-2
+    for rows, bound, ctx in ((17, 17, None), (9, 64, None), (5, 5, 192)):
+        toks = gen.randint(14, 700 + rows, rows, shape.vocab)
+        off = [0, rows]
+        g, st = gm.verify([150], toks, off, max_ctx=ctx, max_rows=bound)
+        o, _ = OF.verify_block(om, copy.deepcopy(oc), [150], toks, off)
+        assert st[0] == 0
+        err = row_rel_err(g, o).max()
+        note(f"  rows {rows} bound {bound} max_ctx {ctx or cap}: max row rel err {err:.2e}")
+        assert err <= 2e-2
