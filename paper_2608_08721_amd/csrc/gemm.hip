@@ -449,14 +449,14 @@ LSV_DEV void gemm_body(const GemmArgs& a, const int M, const int tile, const int
 
 // Launch configuration of each product: fragment rows per wave (TPW), k-slices = waves
 // per workgroup (KS), k-steps per pipeline stage (U) and stages in flight (NS).  Chosen by
-// measurement on the Llama-3-8B shapes: enough bytes in flight per compute unit, a wave
-// count that spreads evenly over the 256 compute units, and few waves per tile for the
-// long products.
+// measurement on the Llama-3-8B shapes: few long weight streams, each with many bytes in
+// flight, beat many short ones (more concurrent streams read more scattered DRAM rows), so
+// every product runs one wave per workgroup over the whole K.
 template <int KIND> struct GemmCfg;
-template <> struct GemmCfg<GEMM_QKV> { static constexpr int TPW = 1, KS = 2, U = 4, NS = 2, EPI = EPI_QKV; };
-template <> struct GemmCfg<GEMM_O> { static constexpr int TPW = 1, KS = 4, U = 4, NS = 2, EPI = EPI_RESID; };
+template <> struct GemmCfg<GEMM_QKV> { static constexpr int TPW = 2, KS = 1, U = 4, NS = 3, EPI = EPI_QKV; };
+template <> struct GemmCfg<GEMM_O> { static constexpr int TPW = 1, KS = 1, U = 8, NS = 3, EPI = EPI_RESID; };
 template <> struct GemmCfg<GEMM_GATEUP> { static constexpr int TPW = 2, KS = 1, U = 4, NS = 3, EPI = EPI_SWIGLU; };
-template <> struct GemmCfg<GEMM_DOWN> { static constexpr int TPW = 1, KS = 4, U = 4, NS = 2, EPI = EPI_RESID; };
+template <> struct GemmCfg<GEMM_DOWN> { static constexpr int TPW = 1, KS = 1, U = 8, NS = 3, EPI = EPI_RESID; };
 template <> struct GemmCfg<GEMM_LMHEAD> { static constexpr int TPW = 2, KS = 1, U = 4, NS = 3, EPI = EPI_LOGITS; };
 
 // Wide activation tiles (prefill bounds) use a shallower pipeline to stay in registers.
