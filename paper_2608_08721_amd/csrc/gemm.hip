@@ -309,15 +309,18 @@ LSV_DEV void gemm_epilogue(const GemmArgs& a, const int M, const int m0, const i
           if (g4 == 0 && m < M && tvalid[t]) GL(a.stats_out)[(size_t)m * (a.N / 16) + tn0 + t] = ss;
         }
     } else if (EPI == EPI_SWIGLU) {
-      static_assert(EPI != EPI_SWIGLU || TPW == 2, "SwiGLU pairs a gate and an up fragment row");
+      // fragment rows come in (gate, up) pairs: even rows gate, odd rows up
+      static_assert(EPI != EPI_SWIGLU || TPW % 2 == 0, "SwiGLU pairs a gate and an up fragment row");
+#pragma unroll
+      for (int t = 0; t < TPW; t += 2)
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) {
-        const int m = m0 + mt * 16 + l16, f0 = (tn0 >> 1) * 16 + 4 * g4;
-        if (m >= M || !tvalid[0]) continue;
+        const int m = m0 + mt * 16 + l16, f0 = ((tn0 + t) >> 1) * 16 + 4 * g4;
+        if (m >= M || !tvalid[t]) continue;
         f32x4_t out;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const float gt = acc[0][mt][r] * inv[mt], up = acc[TPW - 1][mt][r] * inv[mt];
+          const float gt = acc[t][mt][r] * inv[mt], up = acc[t + 1][mt][r] * inv[mt];
           out[r] = gt / (1.0f + expf(-gt)) * up;
         }
         T* dst = (T*)a.u_out + (size_t)m * a.ldu + f0;
@@ -455,9 +458,9 @@ LSV_DEV void gemm_body(const GemmArgs& a, const int M, const int tile, const int
 template <int KIND> struct GemmCfg;
 template <> struct GemmCfg<GEMM_QKV> { static constexpr int TPW = 2, KS = 1, U = 4, NS = 3, EPI = EPI_QKV; };
 template <> struct GemmCfg<GEMM_O> { static constexpr int TPW = 1, KS = 1, U = 8, NS = 3, EPI = EPI_RESID; };
-template <> struct GemmCfg<GEMM_GATEUP> { static constexpr int TPW = 2, KS = 1, U = 4, NS = 3, EPI = EPI_SWIGLU; };
+template <> struct GemmCfg<GEMM_GATEUP> { static constexpr int TPW = 4, KS = 1, U = 4, NS = 3, EPI = EPI_SWIGLU; };
 template <> struct GemmCfg<GEMM_DOWN> { static constexpr int TPW = 1, KS = 1, U = 8, NS = 3, EPI = EPI_RESID; };
-template <> struct GemmCfg<GEMM_LMHEAD> { static constexpr int TPW = 2, KS = 1, U = 4, NS = 3, EPI = EPI_LOGITS; };
+template <> struct GemmCfg<GEMM_LMHEAD> { static constexpr int TPW = 4, KS = 1, U = 4, NS = 3, EPI = EPI_LOGITS; };
 
 // Wide activation tiles (prefill bounds) use a shallower pipeline to stay in registers.
 template <int KIND, int MT_MAX> struct GemmShape {
