@@ -1,12 +1,13 @@
 // Causal grouped-query attention of the block rows over the KV cache.
 //
 // bf16 path (matrix cores), two kernels:
-//  * split kernel: one workgroup of four waves per (context split, kv head, sequence).  A
-//    split is a run of 64-key chunks.  Each chunk's K rows and transposed V rows go HBM ->
-//    registers -> LDS with 16-byte accesses; the first chunk's loads are issued before any
-//    device metadata is read, and each next chunk's loads are in flight while the current
-//    one is consumed.  A wave owns up to kQpw tiles of 16 query vectors (block rows x query
-//    heads of this kv head) and keeps a running softmax over the split:
+//  * split kernel: one workgroup of four or eight waves per (context split, kv head,
+//    sequence).  A split is a run of 64-key chunks.  Each chunk's K rows and transposed V
+//    rows go HBM -> registers -> LDS with 16-byte accesses; the first chunk's loads are
+//    issued before any device metadata is read, and each next chunk's loads are in flight
+//    while the current one is consumed.  A wave owns one tile of 16 query vectors (block
+//    rows x query heads of this kv head) per pass over the split -- eight waves cover up to
+//    32 rows of a 4-query-head group in one pass -- and keeps a running softmax:
 //    S^T = K Q^T and O^T = V^T P^T on v_mfma_f32_16x16x32_bf16.  The probabilities stay in
 //    registers: the D layout of S^T is the B operand layout of P^T, and the V rows are
 //    stored with their keys permuted (v_column) so that one 16-byte read is a fragment.
@@ -21,7 +22,6 @@
 namespace lsv {
 
 constexpr int kCh = kAttnChunk;  // keys per chunk
-constexpr int kQpw = 1;          // query tiles per wave and pass
 constexpr int kAttnWgs = 256;     // split-kernel workgroups aimed for
 constexpr int kMaxChunksPerSplit = 16;  // a split walks its chunks in sequence
 
@@ -40,29 +40,34 @@ AttnPlan plan_attention(int batch, int nkv, int max_ctx) {
   return p;
 }
 
-template <int HD>
-__global__ void __launch_bounds__(256) attn_split_bf16_kernel(AttnArgs a) {
-  constexpr int P8 = HD / 8;             // 16-byte pieces per K row
-  constexpr int NP = kCh * HD / 8 / 256;  // pieces of K (and of V^T) per thread and chunk
+template <int HD, int NW>
+__global__ void __launch_bounds__(64 * NW) attn_split_bf16_kernel(AttnArgs a) {
+  constexpr int NG = NW / 4;               // wave groups: each loads one chunk per step
+  constexpr int P8 = HD / 8;               // 16-byte pieces per K row
+  constexpr int NP = kCh * HD / 8 / 256;   // pieces of K (and of V^T) per thread of a group and chunk
   constexpr int KPITCH = HD + 8, VPITCH = kCh + 8;  // padded LDS rows: conflict-free fragment reads
-  __shared__ __align__(16) bf16_t Ks[kCh * KPITCH];
-  __shared__ __align__(16) bf16_t Vt[HD * VPITCH];
+  static_assert(NG >= 1 && NG * 4 == NW && NP >= 1 && NP * 256 * 8 == kCh * HD, "four-wave groups");
+  __shared__ __align__(16) bf16_t Ks[NG][kCh * KPITCH];  // one chunk buffer per group
+  __shared__ __align__(16) bf16_t Vt[NG][HD * VPITCH];
 
   const int s = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, g4 = lane >> 4, l16 = lane & 15;
+  const int grp = wave >> 2, gtid = tid & 255;
   const size_t slab = ((size_t)b * a.nkv + kvh) * (size_t)a.capacity * HD;
   const GLOBAL bf16_t* kb = GL((const bf16_t*)a.k) + slab;
   const GLOBAL bf16_t* vb = GL((const bf16_t*)a.v) + slab;
   // The grid covers the chunks of ctx_limit <= capacity and capacity is a multiple of the
-  // chunk, so every chunk a workgroup may load lies inside its slab.
-  const int c0 = s * a.chunks_per_split;
+  // chunk, so every chunk below capacity / kCh lies inside the slab.
+  const int c0 = s * a.chunks_per_split, cap_chunks = a.capacity / kCh;
 
+  // a step covers chunks c .. c+NG-1, group g loading chunk c+g into buffer g; the next
+  // step's chunks are in flight in registers while the current ones are used
   u32x4_t kr[NP], vr[NP];
   auto load_chunk = [&](int c) {
     const int k0 = c * kCh;
 #pragma unroll
     for (int j = 0; j < NP; ++j) {
-      const int i = tid + 256 * j;
+      const int i = gtid + 256 * j;
       kr[j] = *(const GLOBAL u32x4_t*)(kb + (size_t)(k0 + i / P8) * HD + (i % P8) * 8);
       vr[j] = *(const GLOBAL u32x4_t*)(vb + (size_t)(i >> 3) * a.capacity + k0 + (i & 7) * 8);
     }
@@ -70,12 +75,12 @@ __global__ void __launch_bounds__(256) attn_split_bf16_kernel(AttnArgs a) {
   auto store_chunk = [&]() {
 #pragma unroll
     for (int j = 0; j < NP; ++j) {
-      const int i = tid + 256 * j;
-      *(u32x4_t*)&Ks[(i / P8) * KPITCH + (i % P8) * 8] = kr[j];
-      *(u32x4_t*)&Vt[(i >> 3) * VPITCH + (i & 7) * 8] = vr[j];
+      const int i = gtid + 256 * j;
+      *(u32x4_t*)&Ks[grp][(i / P8) * KPITCH + (i % P8) * 8] = kr[j];
+      *(u32x4_t*)&Vt[grp][(i >> 3) * VPITCH + (i & 7) * 8] = vr[j];
     }
   };
-  load_chunk(c0);
+  if (grp < a.chunks_per_split && c0 + grp < cap_chunks) load_chunk(c0 + grp);
 
   const int r0 = GL(a.row_offsets)[b], rows = GL(a.row_offsets)[b + 1] - r0, C = GL(a.seq_len)[b];
   if (r0 < 0 || rows <= 0 || r0 + rows > a.M_max) return;  // rows beyond the host bound are never touched
@@ -85,115 +90,155 @@ __global__ void __launch_bounds__(256) attn_split_bf16_kernel(AttnArgs a) {
   const int c1 = min(c0 + a.chunks_per_split, nch);
   const size_t prow = (size_t)s * a.M_max + r0;  // this split's partial row of the sequence's first row
   if (c0 >= c1) {  // no key of this split exists for the sequence: mark its query vectors empty
-    for (int i = tid; i < nqv; i += 256) {
+    for (int i = tid; i < nqv; i += 64 * NW) {
       const size_t base = (prow + i / group) * a.nq + kvh * group + i % group;
       *(GLOBAL f32x2_t*)(a.ml_part + base * 2) = f32x2_t{-INFINITY, 0.f};
     }
     return;
   }
+  // With two groups and at most four query tiles, group g runs the tiles over chunks
+  // c0+g, c0+g+2, ... and the two running softmax states are combined at the end;
+  // otherwise every wave runs its own tile over all chunks in order.
+  const bool halves = NG == 2 && n_qt <= 4;
+  const int tiles_per_pass = halves ? 4 : NW;
 
-  for (int qbase = 0; qbase < n_qt; qbase += 4 * kQpw) {
-    u32x4_t qf[kQpw][HD / 32];
-    f32x4_t o[kQpw][HD / 16];
-    float mrun[kQpw], lrun[kQpw];
-    int qpos[kQpw];
-    bool qval[kQpw];
-#pragma unroll
-    for (int j = 0; j < kQpw; ++j) {
-      const int qv = (qbase + wave + 4 * j) * 16 + l16;
-      qval[j] = qv < nqv;
-      const int rr = qval[j] ? qv / group : 0, head = kvh * group + (qval[j] ? qv % group : 0);
+  for (int qbase = 0; qbase < n_qt; qbase += tiles_per_pass) {
+    const int qt = qbase + (halves ? (wave & 3) : wave);
+    const bool active = qt < n_qt;  // wave-uniform
+    u32x4_t qf[HD / 32];
+    f32x4_t o[HD / 16];
+    float mrun = -INFINITY, lrun = 0.f;
+    const int qv = qt * 16 + l16;
+    const bool qval = active && qv < nqv;
+    const int rr = qval ? qv / group : 0;
+    const int qpos = C + rr;
+    {
+      const int head = kvh * group + (qval ? qv % group : 0);
       const GLOBAL bf16_t* qp = GL((const bf16_t*)a.q) + ((size_t)(r0 + rr) * a.nq + head) * HD + 8 * g4;
 #pragma unroll
       for (int ds = 0; ds < HD / 32; ++ds) {  // rr = 0 for invalid columns: the load stays in bounds
         const u32x4_t t = *(const GLOBAL u32x4_t*)(qp + 32 * ds);
-        qf[j][ds] = qval[j] ? t : u32x4_t{0u, 0u, 0u, 0u};
+        qf[ds] = qval ? t : u32x4_t{0u, 0u, 0u, 0u};
       }
-      qpos[j] = C + rr;
-      mrun[j] = -INFINITY;
-      lrun[j] = 0.f;
 #pragma unroll
-      for (int dt = 0; dt < HD / 16; ++dt) o[j][dt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+      for (int dt = 0; dt < HD / 16; ++dt) o[dt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
     }
-    if (qbase > 0) load_chunk(c0);  // a later pass over the same split
+    if (qbase > 0 && c0 + grp < c1) load_chunk(c0 + grp);  // a later pass over the same split
 
-    for (int c = c0; c < c1; ++c) {
-      __syncthreads();  // the previous chunk's LDS reads are done
-      store_chunk();
-      __syncthreads();
-      if (c + 1 < c1) load_chunk(c + 1);
+    // scores and running-softmax update of this wave's tile for the chunk in buffer g
+    auto consume = [&](int g, int c) {
       const int k0 = c * kCh;
+      f32x4_t sc[4];
 #pragma unroll
-      for (int j = 0; j < kQpw; ++j) {
-        if (qbase + wave + 4 * j >= n_qt) continue;  // wave-uniform
-        f32x4_t sc[4];
+      for (int kt = 0; kt < 4; ++kt) {
+        sc[kt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int kt = 0; kt < 4; ++kt) {
-          sc[kt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-          for (int ds = 0; ds < HD / 32; ++ds) {
-            const u32x4_t kf = *(const u32x4_t*)&Ks[(16 * kt + l16) * KPITCH + 32 * ds + 8 * g4];
-            sc[kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, kf),
-                                                             __builtin_bit_cast(bf16x8_t, qf[j][ds]), sc[kt], 0, 0, 0);
-          }
-        }
-        // scale (log2 units), causal mask, running max over the split
-        float mx = -INFINITY;
-#pragma unroll
-        for (int kt = 0; kt < 4; ++kt)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const int kp = k0 + 16 * kt + 4 * g4 + r;
-            const bool ok = qval[j] && kp < L && kp <= qpos[j];
-            const float v = ok ? sc[kt][r] * a.scale_log2 : -INFINITY;
-            sc[kt][r] = v;
-            mx = fmaxf(mx, v);
-          }
-        mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
-        mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
-        const float mnew = fmaxf(mrun[j], mx);
-        const float alpha = mrun[j] == -INFINITY ? 0.f : exp2f(mrun[j] - mnew);
-        float sum = 0.f;
-#pragma unroll
-        for (int kt = 0; kt < 4; ++kt)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const float p = mnew == -INFINITY ? 0.f : exp2f(sc[kt][r] - mnew);
-            sc[kt][r] = p;
-            sum += p;
-          }
-        sum += __shfl_xor(sum, 16, kWave);
-        sum += __shfl_xor(sum, 32, kWave);
-        mrun[j] = mnew;
-        lrun[j] = lrun[j] * alpha + sum;
-#pragma unroll
-        for (int dt = 0; dt < HD / 16; ++dt) o[j][dt] *= alpha;
-#pragma unroll
-        for (int ks = 0; ks < 2; ++ks) {
-          bf16x8_t pb;
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            pb[r] = (__bf16)sc[2 * ks][r];
-            pb[4 + r] = (__bf16)sc[2 * ks + 1][r];
-          }
-#pragma unroll
-          for (int dt = 0; dt < HD / 16; ++dt) {
-            const u32x4_t vf = *(const u32x4_t*)&Vt[(16 * dt + l16) * VPITCH + 32 * ks + 8 * g4];
-            o[j][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, vf), pb, o[j][dt], 0, 0, 0);
-          }
+        for (int ds = 0; ds < HD / 32; ++ds) {
+          const u32x4_t kf = *(const u32x4_t*)&Ks[g][(16 * kt + l16) * KPITCH + 32 * ds + 8 * g4];
+          sc[kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, kf),
+                                                           __builtin_bit_cast(bf16x8_t, qf[ds]), sc[kt], 0, 0, 0);
         }
       }
-    }
+      // scale (log2 units), causal mask, running max over the split
+      float mx = -INFINITY;
 #pragma unroll
-    for (int j = 0; j < kQpw; ++j) {
-      if (!qval[j]) continue;
-      const int qv = (qbase + wave + 4 * j) * 16 + l16;
+      for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int kp = k0 + 16 * kt + 4 * g4 + r;
+          const bool ok = qval && kp < L && kp <= qpos;
+          const float v = ok ? sc[kt][r] * a.scale_log2 : -INFINITY;
+          sc[kt][r] = v;
+          mx = fmaxf(mx, v);
+        }
+      mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
+      mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
+      const float mnew = fmaxf(mrun, mx);
+      const float alpha = mrun == -INFINITY ? 0.f : exp2f(mrun - mnew);
+      float sum = 0.f;
+#pragma unroll
+      for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float p = mnew == -INFINITY ? 0.f : exp2f(sc[kt][r] - mnew);
+          sc[kt][r] = p;
+          sum += p;
+        }
+      sum += __shfl_xor(sum, 16, kWave);
+      sum += __shfl_xor(sum, 32, kWave);
+      mrun = mnew;
+      lrun = lrun * alpha + sum;
+#pragma unroll
+      for (int dt = 0; dt < HD / 16; ++dt) o[dt] *= alpha;
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks) {
+        bf16x8_t pb;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          pb[r] = (__bf16)sc[2 * ks][r];
+          pb[4 + r] = (__bf16)sc[2 * ks + 1][r];
+        }
+#pragma unroll
+        for (int dt = 0; dt < HD / 16; ++dt) {
+          const u32x4_t vf = *(const u32x4_t*)&Vt[g][(16 * dt + l16) * VPITCH + 32 * ks + 8 * g4];
+          o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, vf), pb, o[dt], 0, 0, 0);
+        }
+      }
+    };
+
+    for (int c = c0; c < c1; c += NG) {
+      __syncthreads();  // the previous step's LDS reads are done
+      if (c + grp < c1) store_chunk();
+      __syncthreads();
+      if (c + NG + grp < c1) load_chunk(c + NG + grp);
+      if (!active) continue;  // wave-uniform: a wave without a query tile in this pass
+      if (halves) {
+        if (c + grp < c1) consume(grp, c + grp);
+      } else {
+#pragma unroll
+        for (int g = 0; g < NG; ++g)
+          if (c + g < c1) consume(g, c + g);
+      }
+    }
+
+    if (halves) {
+      // group 1 hands its state to group 0 through the (now free) chunk buffers; group 0
+      // combines them: its own chunks first, in a fixed order
+      constexpr int OW = HD / 16 * 4 + 2;  // floats per lane: o, then m and l
+      float* xch = reinterpret_cast<float*>(&Ks[0][0]);
+      static_assert(NG == 1 || 4 * 64 * OW * sizeof(float) <= sizeof(Ks), "the exchange fits the K buffers");
+      __syncthreads();
+      float* mine = xch + ((size_t)(wave & 3) * 64 + lane) * OW;
+      if (grp == 1 && active) {
+#pragma unroll
+        for (int dt = 0; dt < HD / 16; ++dt)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) mine[dt * 4 + r] = o[dt][r];
+        mine[OW - 2] = mrun;
+        mine[OW - 1] = lrun;
+      }
+      __syncthreads();
+      if (grp == 0 && active) {
+        const float m1 = mine[OW - 2], l1 = mine[OW - 1];
+        const float mnew = fmaxf(mrun, m1);
+        const float a0 = mrun == -INFINITY ? 0.f : exp2f(mrun - mnew);
+        const float a1 = m1 == -INFINITY ? 0.f : exp2f(m1 - mnew);
+        lrun = lrun * a0 + l1 * a1;
+#pragma unroll
+        for (int dt = 0; dt < HD / 16; ++dt)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) o[dt][r] = o[dt][r] * a0 + mine[dt * 4 + r] * a1;
+        mrun = mnew;
+      }
+    }
+    if (active && qval && (!halves || grp == 0)) {
       const size_t base = (prow + qv / group) * a.nq + kvh * group + qv % group;
       GLOBAL float* op = GL(a.o_part) + base * HD;
 #pragma unroll
-      for (int dt = 0; dt < HD / 16; ++dt) *(GLOBAL f32x4_t*)(op + 16 * dt + 4 * g4) = o[j][dt];
-      if (g4 == 0) *(GLOBAL f32x2_t*)(a.ml_part + base * 2) = f32x2_t{mrun[j], lrun[j]};
+      for (int dt = 0; dt < HD / 16; ++dt) *(GLOBAL f32x4_t*)(op + 16 * dt + 4 * g4) = o[dt];
+      if (g4 == 0) *(GLOBAL f32x2_t*)(a.ml_part + base * 2) = f32x2_t{mrun, lrun};
     }
+    __syncthreads();  // the next pass refills the chunk buffers
   }
 }
 
@@ -290,11 +335,21 @@ int launch_attention(int dtype, int hd, const AttnArgs& a, int max_rows, hipStre
     const dim3 grid(a.n_splits, a.nkv, a.batch);
     const int hpw = 256 / hd;
     const dim3 mgrid(max_rows, (a.nq + hpw - 1) / hpw);
+    // query tiles per sequence (rows of a single sequence, else the mean over the batch): up
+    // to four take four waves, more take eight so that one pass covers them
+    const int rows_seq = (max_rows + a.batch - 1) / a.batch;
+    const bool wide = (size_t)rows_seq * (a.nq / a.nkv) > 64;
     if (hd == 128) {
-      hipLaunchKernelGGL(attn_split_bf16_kernel<128>, grid, dim3(256), 0, st, a);
+      if (wide)
+        hipLaunchKernelGGL((attn_split_bf16_kernel<128, 8>), grid, dim3(512), 0, st, a);
+      else
+        hipLaunchKernelGGL((attn_split_bf16_kernel<128, 4>), grid, dim3(256), 0, st, a);
       hipLaunchKernelGGL(attn_merge_bf16_kernel<128>, mgrid, dim3(64), 0, st, a);
     } else if (hd == 64) {
-      hipLaunchKernelGGL(attn_split_bf16_kernel<64>, grid, dim3(256), 0, st, a);
+      if (wide)
+        hipLaunchKernelGGL((attn_split_bf16_kernel<64, 8>), grid, dim3(512), 0, st, a);
+      else
+        hipLaunchKernelGGL((attn_split_bf16_kernel<64, 4>), grid, dim3(256), 0, st, a);
       hipLaunchKernelGGL(attn_merge_bf16_kernel<64>, mgrid, dim3(64), 0, st, a);
     } else {
       return LSV_ERR_UNSUPPORTED;
