@@ -287,7 +287,8 @@ __global__ void __launch_bounds__(64) attn_merge_bf16_kernel(AttnArgs a) {
   const f32x4_t r = num / den;
   const u32x2_t packed = {(uint32_t)f2bf(r[0]) | ((uint32_t)f2bf(r[1]) << 16),
                           (uint32_t)f2bf(r[2]) | ((uint32_t)f2bf(r[3]) << 16)};
-  *(GLOBAL u32x2_t*)(GL((bf16_t*)a.out) + rh * HD + d) = packed;
+  // the O projection's activation operand: column head * HD + d of row m (d .. d+3 adjacent)
+  *(GLOBAL u32x2_t*)(GL((bf16_t*)a.out) + act_index<32>(m, head * HD + d, a.nq * HD / 32)) = packed;
 }
 
 // fp32 path: one wave per (row, query head); scores in LDS.
@@ -326,7 +327,7 @@ __global__ void __launch_bounds__(64) attn_f32_kernel(AttnArgs a, int hd) {
     const float* vrow = Vt + (size_t)i * a.capacity;
     float o = 0.f;
     for (int j = 0; j < L; ++j) o += sc[j] * vrow[v_column(j)];
-    ((float*)a.out)[((size_t)m * a.nq + head) * hd + i] = o / sum;
+    ((float*)a.out)[act_index<16>(m, head * hd + i, a.nq * hd / 16)] = o / sum;
   }
 }
 

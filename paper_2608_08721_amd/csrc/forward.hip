@@ -64,17 +64,16 @@ ModelLayout model_layout(const Shape& s) {
 
 // ------------------------------------------------------------------ workspace
 struct VerifyWs {
-  float* h;        // [M_max][d] fp32 residual stream
-  void* hx;        // [M_max][d] storage-type copy of h (bf16 models; fp32 models read h)
+  float* h;        // [M_max][d] fp32 residual stream (row-major)
+  void* hx;        // storage-type copy of h, d columns (activation layout, act_index)
   float* stats;    // [M_max][d/16] per-16-column sums of squares of h
   void* q;         // [M_max][nq][hd]
-  void* attn;      // [M_max][nq][hd]
-  void* u;         // [M_max][ldu], columns >= d_ff stay zero
+  void* attn;      // attention output, nq*hd columns (activation layout)
+  void* u;         // SwiGLU output, d_ff columns (activation layout; padding columns stay zero)
   float* o_part;   // attention split partials
   float* ml_part;
   float* part;     // wide blocks: k-split partials
   int* counters;   // wide blocks: per-tile arrivals, zero between calls
-  int ldu;
   size_t total;
 };
 
@@ -128,14 +127,16 @@ static VerifyWs carve_verify(const Shape& s, const ModelLayout& ml, const Verify
   // keep their place whatever the batch, row and context bounds of a call, so one zeroed
   // workspace serves calls with different bounds.
   w.counters = (int*)take(sizeof(int) * (size_t)max_wide_tiles(ml));
-  const int KT = s.dtype == LSV_DTYPE_BF16 ? 32 : 16;
-  w.ldu = ml.down.Kt * KT;  // the down projection reads whole fragments of u
+  // activation buffers hold whole 16-row tiles and whole k-steps
+  auto act_bytes = [&](int K) {
+    return (size_t)s.es * (s.dtype == LSV_DTYPE_BF16 ? act_elems<32>(max_rows, K) : act_elems<16>(max_rows, K));
+  };
   w.h = (float*)take(sizeof(float) * (size_t)max_rows * s.d);
-  w.hx = s.dtype == LSV_DTYPE_BF16 ? take((size_t)s.es * max_rows * s.d) : (void*)w.h;
+  w.hx = take(act_bytes(s.d));
   w.stats = (float*)take(sizeof(float) * (size_t)(s.d / 16) * max_rows);
   w.q = take((size_t)s.es * max_rows * s.nq * s.hd);
-  w.attn = take((size_t)s.es * max_rows * s.nq * s.hd);
-  w.u = take((size_t)s.es * max_rows * w.ldu);
+  w.attn = take(act_bytes(s.nq * s.hd));
+  w.u = take(act_bytes(s.F));
   if (s.dtype == LSV_DTYPE_BF16) {
     w.o_part = (float*)take(sizeof(float) * (size_t)v.attn.n_splits * max_rows * s.nq * s.hd);
     w.ml_part = (float*)take(sizeof(float) * (size_t)v.attn.n_splits * max_rows * s.nq * 2);
@@ -155,9 +156,9 @@ size_t verify_workspace_bytes(const Shape& s, int batch, int max_rows, int max_c
 }
 
 // ------------------------------------------------------------------ embedding
-// h[m] = E[token_m] (fp32) and per-16-column sums of squares for the first RMSNorm.
-// Workgroup 0 also validates every sequence: token ids in range and the block
-// within max_ctx.  Invalid tokens embed as zeros.
+// h[m] = E[token_m] (fp32), its storage-type copy in the activation layout and
+// per-16-column sums of squares for the first RMSNorm.  Workgroup 0 also validates every
+// sequence: token ids in range and the block within max_ctx.  Invalid tokens embed as zeros.
 template <typename T>
 __global__ void __launch_bounds__(256) embed_kernel(const T* __restrict__ E, int V, int d, const int32_t* tokens,
                                                     const int32_t* row_offsets, const int32_t* seq_len, int batch,
@@ -210,11 +211,11 @@ __global__ void __launch_bounds__(256) embed_kernel(const T* __restrict__ E, int
     GLOBAL f32x4_t* hp = (GLOBAL f32x4_t*)(GL(h) + (size_t)m * d + 16 * p);
 #pragma unroll
     for (int i = 0; i < 4; ++i) hp[i] = f32x4_t{x[4 * i], x[4 * i + 1], x[4 * i + 2], x[4 * i + 3]};
-    if (hx) {
-      GLOBAL u32x4_t* xp = (GLOBAL u32x4_t*)(GL(hx) + (size_t)m * d + 16 * p);
+    // a 16-byte piece is one lane's run of a fragment (EPL = 16 / sizeof(T) columns)
+    constexpr int KT = 64 / sizeof(T), EPL = KT / 4;
+    const int Kt = (d + KT - 1) / KT;
 #pragma unroll
-      for (int i = 0; i < PER16; ++i) xp[i] = raw[i];
-    }
+    for (int i = 0; i < PER16; ++i) *(GLOBAL u32x4_t*)(GL(hx) + act_index<KT>(m, 16 * p + i * EPL, Kt)) = raw[i];
     GL(stats)[(size_t)m * (d / 16) + p] = ss;
   }
 }
@@ -235,7 +236,7 @@ int launch_verify(const Shape& s, const ModelLayout& ml, const void* packed, voi
                        status);
   else
     hipLaunchKernelGGL(embed_kernel<float>, dim3(max_rows), dim3(256), 0, st, (const float*)(P + ml.embed), s.V, s.d,
-                       tokens, row_offsets, seq_len, batch, max_ctx, max_rows, w.h, (float*)nullptr, w.stats, status);
+                       tokens, row_offsets, seq_len, batch, max_ctx, max_rows, w.h, (float*)w.hx, w.stats, status);
   if (hipGetLastError() != hipSuccess) return LSV_ERR_HIP;
 
   GemmArgs base = {};
@@ -253,7 +254,6 @@ int launch_verify(const Shape& s, const ModelLayout& ml, const void* packed, voi
   base.hd = s.hd;
   base.log2_rope_base = log2(s.rope_base);
   base.F = s.F;
-  base.ldu = w.ldu;
 
   auto gemm = [&](GemmKind kind, const PackedMat& pm, const char* layer_base, GemmArgs a) {
     a.W = (const uint4*)(layer_base + pm.offset);
@@ -286,7 +286,6 @@ int launch_verify(const Shape& s, const ModelLayout& ml, const void* packed, voi
     a.layer_index = l;
     a.layer = l;
     a.x = w.hx;
-    a.ldx = s.d;
     a.q_out = w.q;
     if ((rc = gemm(GEMM_QKV, ml.qkv, LB, a)) != LSV_OK) return rc;
     // attention
@@ -315,31 +314,27 @@ int launch_verify(const Shape& s, const ModelLayout& ml, const void* packed, voi
     a = base;
     a.layer_index = l;
     a.x = w.attn;
-    a.ldx = s.nq * s.hd;
     a.h_out = w.h;
-    a.hx_out = bf16 ? w.hx : nullptr;
+    a.hx_out = w.hx;
     a.stats_out = w.stats;
     if ((rc = gemm(GEMM_O, ml.o, LB, a)) != LSV_OK) return rc;
     // gate/up (normalised input) + SwiGLU
     a = base;
     a.layer_index = l;
     a.x = w.hx;
-    a.ldx = s.d;
     a.u_out = w.u;
     if ((rc = gemm(GEMM_GATEUP, ml.gateup, LB, a)) != LSV_OK) return rc;
     // down + residual
     a = base;
     a.layer_index = l;
     a.x = w.u;
-    a.ldx = w.ldu;
     a.h_out = w.h;
-    a.hx_out = bf16 ? w.hx : nullptr;
+    a.hx_out = w.hx;
     a.stats_out = w.stats;
     if ((rc = gemm(GEMM_DOWN, ml.down, LB, a)) != LSV_OK) return rc;
   }
   GemmArgs a = base;
   a.x = w.hx;
-  a.ldx = s.d;
   a.out_f32 = logits;
   a.ldo = s.V;
   return gemm(GEMM_LMHEAD, ml.lm_head, P, a);

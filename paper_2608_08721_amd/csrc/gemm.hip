@@ -194,6 +194,7 @@ template <typename T, int MT, int TPW, int EPI, bool HPRE>
 LSV_DEV void gemm_epilogue(const GemmArgs& a, const int M, const int m0, const int tn0, const bool (&tvalid)[TPW],
                            f32x4_t (&acc)[TPW][MT], const f32x4_t (&hpre)[TPW][MT], const RowInputs* rin = nullptr) {
   constexpr bool RMS = EPI != EPI_RESID;
+  constexpr int KT = FragTraits<T>::KT;
   const int lane = threadIdx.x & 63, l16 = lane & 15, g4 = lane >> 4;
   float inv[MT];
   if (RMS) {
@@ -301,7 +302,7 @@ LSV_DEV void gemm_epilogue(const GemmArgs& a, const int M, const int m0, const i
             const f32x4_t hv = HPRE ? hpre[t][mt] : *(const GLOBAL f32x4_t*)(a.h_out + (size_t)m * a.N + n0);
             const f32x4_t h4 = hv + acc[t][mt];
             *(GLOBAL f32x4_t*)(a.h_out + (size_t)m * a.N + n0) = h4;
-            if (a.hx_out) store4((T*)a.hx_out + (size_t)m * a.N + n0, h4);
+            if (a.hx_out) store4((T*)a.hx_out + act_index<KT>(m, n0, (a.N + KT - 1) / KT), h4);
             ss = ((h4[0] * h4[0] + h4[1] * h4[1]) + h4[2] * h4[2]) + h4[3] * h4[3];
           }
           ss += __shfl_xor(ss, 16, kWave);
@@ -323,7 +324,7 @@ LSV_DEV void gemm_epilogue(const GemmArgs& a, const int M, const int m0, const i
           const float gt = acc[t][mt][r] * inv[mt], up = acc[t + 1][mt][r] * inv[mt];
           out[r] = gt / (1.0f + expf(-gt)) * up;
         }
-        T* dst = (T*)a.u_out + (size_t)m * a.ldu + f0;
+        T* dst = (T*)a.u_out + act_index<KT>(m, f0, (a.F + KT - 1) / KT);  // f0 .. f0+3 are adjacent
         if (f0 + 3 < a.F) {
           store4(dst, out);
         } else {
@@ -369,14 +370,12 @@ LSV_DEV void gemm_body(const GemmArgs& a, const int M, const int tile, const int
     }
   }
 
-  // B operand: activation rows (clamped into the buffer; columns of rows >= M are never
-  // stored, so their contents do not matter)
+  // B operand: this lane's piece of each activation tile's fragments (rows >= M hold stale
+  // but finite values; their output columns are never stored)
   const GLOBAL T* xp[MT];
 #pragma unroll
-  for (int mt = 0; mt < MT; ++mt) {
-    const int m = min(m0 + mt * 16 + l16, a.M_max - 1);
-    xp[mt] = (const GLOBAL T*)a.x + (size_t)m * a.ldx + (size_t)k0 * KT + g4 * EPL;
-  }
+  for (int mt = 0; mt < MT; ++mt)
+    xp[mt] = (const GLOBAL T*)a.x + (((size_t)((m0 >> 4) + mt) * a.Kt + k0) * kWave + lane) * EPL;
 
   f32x4_t acc[TPW][MT];
 #pragma unroll
@@ -395,7 +394,7 @@ LSV_DEV void gemm_body(const GemmArgs& a, const int M, const int tile, const int
 #pragma unroll
         for (int t = 0; t < TPW; ++t) wa[st][u][t] = wbase[frag_index(tr[t], k0 + kf, a.Nt, a.Kt) * 64];
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt) xb[st][u][mt] = *(const GLOBAL u32x4_t*)(xp[mt] + (size_t)kf * KT);
+        for (int mt = 0; mt < MT; ++mt) xb[st][u][mt] = *(const GLOBAL u32x4_t*)(xp[mt] + (size_t)kf * kWave * EPL);
       }
     };
     auto compute_stage = [&](int st, int kb, bool tail) {
@@ -582,10 +581,8 @@ __global__ void __launch_bounds__(256) gemm_wide_kernel(GemmArgs a) {
 #pragma unroll
     for (int i = 0; i < PPT; ++i) {
       const int p = tid + 256 * i, mt = p / kWave, ln = p % kWave;
-      if (p < PIECES && mt < mt_n) {
-        const int row = min(mt * 16 + (ln & 15), a.M_max - 1);
-        bst[st][i] = *(const GLOBAL u32x4_t*)(xg + (size_t)row * a.ldx + (size_t)(k0 + kk) * KT + (ln >> 4) * EPL);
-      }
+      if (p < PIECES && mt < mt_n)
+        bst[st][i] = *(const GLOBAL u32x4_t*)(xg + (((size_t)mt * a.Kt + k0 + kk) * kWave + ln) * EPL);
     }
 #pragma unroll
     for (int t = 0; t < TPW; ++t) wa[st][t] = wbase[frag_index(tr[t], k0 + kk, a.Nt, a.Kt) * 64];

@@ -20,7 +20,7 @@ struct AttnArgs {
   const int32_t* seq_len;
   float* o_part;   // [n_splits][M_max][nq][hd]  (bf16 path)
   float* ml_part;  // [n_splits][M_max][nq][2]: running max (log2 units), sum of exponentials
-  void* out;       // [M][nq][hd] storage type
+  void* out;       // nq*hd columns per row in the activation layout (act_index), storage type
   float scale_log2;
   int n_splits, chunks_per_split;
 };

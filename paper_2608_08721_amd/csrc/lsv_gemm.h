@@ -21,9 +21,8 @@ struct GemmArgs {
   int N, K, Nt, Kt;
   int M_max, batch;
   const int32_t* row_offsets;  // [batch+1]; rows = row_offsets[batch]
-  // B operand: activation rows [M_max][ldx] in the storage type, columns >= K zero up to Kt*KT
+  // B operand: activation rows in the storage type, fragment-major (act_index with Kt)
   const void* x;
-  int ldx;
   // row scaling of normalised-activation consumers: 1/rms from [M_max][P] sums of squares
   // over 16-column groups (P = K / 16)
   const float* stats;
@@ -44,12 +43,12 @@ struct GemmArgs {
   const int32_t* seq_len;
   double log2_rope_base;
   // EPI_RESID
-  float* h_out;      // [M][N] fp32 residual, updated in place
-  void* hx_out;      // [M][N] storage-type copy for the next consumer (NULL for fp32 models)
+  float* h_out;      // [M][N] fp32 residual (row-major), updated in place
+  void* hx_out;      // storage-type copy of the new residual for the next consumer (act_index)
   float* stats_out;  // [M_max][N/16]
   // EPI_SWIGLU
-  void* u_out;  // [M][ldu]
-  int F, ldu;
+  void* u_out;  // SwiGLU output, F columns (act_index)
+  int F;
   int layer_index;  // host-side only: which layer a launch belongs to (measurement hook)
 };
 

@@ -53,6 +53,23 @@ __host__ __device__ inline size_t frag_index(int tn, int k, int Nt, int Kt) {
   const int bs = Kt - k0 < kFragBlock ? Kt - k0 : kFragBlock;  // size of block b
   return (size_t)k0 * Nt + (size_t)tn * bs + (k - k0);
 }
+// Activation operand layout (the B side of every projection): rows in tiles of 16, columns
+// in k-steps of KT (32 bf16 or 16 fp32 columns, EPL = KT / 4 per lane).  The 16 x KT block
+// of one (row tile, k-step) is one contiguous KiB in the lane order of the MFMA B operand:
+// lane g * 16 + r holds row r, columns g * EPL .. g * EPL + EPL - 1.  A buffer of K columns
+// has Kt = ceil(K / KT) k-steps per row tile (columns past K stay zero); a wave's activation
+// load is then one contiguous KiB, as its weight loads are.
+template <int KT>
+__host__ __device__ inline size_t act_index(int m, int c, int Kt) {
+  constexpr int EPL = KT / 4;
+  return ((((size_t)(m >> 4) * Kt + c / KT) * 4 + (c % KT) / EPL) * 16 + (m & 15)) * EPL + c % EPL;
+}
+// Elements of an activation buffer of `rows` rows and K columns.
+template <int KT>
+__host__ __device__ inline size_t act_elems(int rows, int K) {
+  return (size_t)((rows + 15) / 16) * 16 * (size_t)((K + KT - 1) / KT) * KT;
+}
+
 // RMSNorm gains are folded into the projection that follows them (QKV, gate/up,
 // LM head), so the packed model stores no separate gains.
 struct ModelLayout {
