@@ -131,10 +131,10 @@ size_t lsv_kv_cache_bytes(const lsv_model_config* cfg, int32_t batch, int32_t ca
 
 /* ------------------------------------------------------------ verify step */
 /* Workspace for lsv_verify_block with the given bounds.  The workspace must be
- * zero-filled once after allocation (e.g. with lsv_workspace_clear); every call
- * leaves its internal counters at zero again.  The counters sit at the start of the
- * workspace and depend on the model configuration only, so a workspace sized for the
- * largest bounds serves calls with any smaller batch, max_rows or max_ctx. */
+ * zero-filled once after allocation (e.g. with lsv_workspace_clear): the padding
+ * columns of its activation buffers are never written and must read as zero.  It
+ * carries no state from one call to the next, and a workspace sized for the largest
+ * bounds serves calls with any smaller batch, max_rows or max_ctx. */
 size_t lsv_verify_workspace_bytes(const lsv_model_config* cfg, int32_t batch, int32_t max_rows,
                                   int32_t max_ctx);
 int lsv_workspace_clear(void* d_workspace, size_t workspace_bytes, void* stream);

@@ -73,7 +73,7 @@ struct VerifyWs {
   float* o_part;   // attention split partials
   float* ml_part;
   float* part;     // wide blocks: k-split partials
-  int* counters;   // wide blocks: per-tile arrivals, zero between calls
+  float* qkv_y;    // wide blocks: [M_max][N_qkv] normalised QKV projection before RoPE
   size_t total;
 };
 
@@ -103,17 +103,6 @@ static VerifyPlan plan_verify(const Shape& s, const ModelLayout& ml, int batch, 
   return v;
 }
 
-// Most tiles any batched GEMM of this model can have (sizes the arrival counters).
-static int max_wide_tiles(const ModelLayout& ml) {
-  const PackedMat* mats[5] = {&ml.qkv, &ml.o, &ml.gateup, &ml.down, &ml.lm_head};
-  int t = 1;
-  for (int k = 0; k < 5; ++k) {
-    const int tiles = plan_wide(mats[k]->Nt, mats[k]->Kt).tiles;
-    t = tiles > t ? tiles : t;
-  }
-  return t;
-}
-
 static VerifyWs carve_verify(const Shape& s, const ModelLayout& ml, const VerifyPlan& v, int max_rows, void* base) {
   VerifyWs w;
   char* p = (char*)base;
@@ -123,10 +112,6 @@ static VerifyWs carve_verify(const Shape& s, const ModelLayout& ml, const Verify
     off = al256(off + bytes);
     return (void*)r;
   };
-  // Arrival counters first, sized by the model alone: they stay at zero between calls and
-  // keep their place whatever the batch, row and context bounds of a call, so one zeroed
-  // workspace serves calls with different bounds.
-  w.counters = (int*)take(sizeof(int) * (size_t)max_wide_tiles(ml));
   // activation buffers hold whole 16-row tiles and whole k-steps
   auto act_bytes = [&](int K) {
     return (size_t)s.es * (s.dtype == LSV_DTYPE_BF16 ? act_elems<32>(max_rows, K) : act_elems<16>(max_rows, K));
@@ -144,6 +129,7 @@ static VerifyWs carve_verify(const Shape& s, const ModelLayout& ml, const Verify
     w.o_part = w.ml_part = nullptr;
   }
   w.part = (float*)take(sizeof(float) * v.part_floats);
+  w.qkv_y = v.wide ? (float*)take(sizeof(float) * (size_t)max_rows * ml.qkv.N) : nullptr;
   w.total = off;
   return w;
 }
@@ -267,8 +253,7 @@ int launch_verify(const Shape& s, const ModelLayout& ml, const void* packed, voi
     if (v.wide) {
       a.part = w.part;
       a.part_bytes = sizeof(float) * v.part_floats;
-      a.splits = v.w[kind].splits;
-      a.counters = w.counters;
+      if (kind == GEMM_QKV) a.out_f32 = w.qkv_y;
       rc = launch_gemm_wide(kind, a, v.w[kind], st);
     } else {
       rc = launch_gemm(s.dtype, kind, v.MT, a, st);

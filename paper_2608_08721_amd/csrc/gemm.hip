@@ -177,6 +177,65 @@ LSV_DEV float inv_rms_serial(const GemmArgs& a, int m) {
   return 1.0f / sqrtf(ss / (float)a.K + a.eps);
 }
 
+// ------------------------------------------------------------------ QKV epilogue
+// base^(-2i/hd) of the two rotary pairs held by output columns n0 .. n0+3 (packed rows
+// (2i, 2i+1) of a q or k head are dims (i, i + hd/2)); they depend on the column only.
+LSV_DEV void qkv_inv_freq(const GemmArgs& a, int n0, double (&f)[2]) {
+  const int qrows = a.nq * a.hd;
+  const int local = n0 < qrows ? n0 : n0 - qrows;
+  const int i0 = (local % a.hd) >> 1;
+#pragma unroll
+  for (int pr = 0; pr < 2; ++pr) f[pr] = exp2(-(double)(2 * (i0 + pr)) / (double)a.hd * a.log2_rope_base);
+}
+
+// Output columns n0 .. n0+3 of row m of the normalised QKV projection (v), for a row of
+// sequence b at cache position pos: rotary embedding of q and k, then the Q store or the
+// cache append (V transposed).
+template <typename T>
+LSV_DEV void qkv_store4(const GemmArgs& a, int m, int n0, const f32x4_t v, int b, int pos, const double (&inv_freq)[2]) {
+  const int qrows = a.nq * a.hd, krows = a.nkv * a.hd;
+  if (n0 >= qrows + 2 * krows) return;
+  if (n0 < qrows + krows) {
+    const bool isq = n0 < qrows;
+    const int local = isq ? n0 : n0 - qrows;
+    const int head = local / a.hd, i0 = (local % a.hd) >> 1;  // pairs (i0, i0+hd/2), (i0+1, i0+1+hd/2)
+    float out[4];
+#pragma unroll
+    for (int pr = 0; pr < 2; ++pr) {
+      // angle = pos * base^(-2i/hd) in fp64, reduced to [-pi, pi] in fp64, then fp32 sin/cos
+      const double ang = (double)pos * inv_freq[pr];
+      const double red2pi = ang - 6.283185307179586 * rint(ang * 0.15915494309189535);
+      float sn, cs;
+      sincosf((float)red2pi, &sn, &cs);
+      const float x1 = v[2 * pr], x2 = v[2 * pr + 1];
+      out[2 * pr] = x1 * cs - x2 * sn;
+      out[2 * pr + 1] = x2 * cs + x1 * sn;
+    }
+    T* dst;
+    if (isq) {
+      dst = (T*)a.q_out + ((size_t)m * a.nq + head) * a.hd;
+    } else {
+      if (pos < 0 || pos >= a.capacity) return;
+      dst = (T*)a.kv + ((((size_t)a.layer * 2 + 0) * a.batch + b) * a.nkv + head) * (size_t)a.capacity * a.hd +
+            (size_t)pos * a.hd;
+    }
+    GLOBAL T* gd = GL(dst);
+    gd[i0] = from_f32<T>(out[0]);
+    gd[i0 + a.hd / 2] = from_f32<T>(out[1]);
+    gd[i0 + 1] = from_f32<T>(out[2]);
+    gd[i0 + 1 + a.hd / 2] = from_f32<T>(out[3]);
+  } else {
+    if (pos < 0 || pos >= a.capacity) return;
+    // V rows are stored transposed: [head_dim][capacity], column v_column(pos)
+    const int local = n0 - qrows - krows;
+    const int head = local / a.hd, d0 = local % a.hd;
+    GLOBAL T* dst = GL((T*)a.kv) + ((((size_t)a.layer * 2 + 1) * a.batch + b) * a.nkv + head) * (size_t)a.capacity * a.hd +
+                    (size_t)d0 * a.capacity + v_column(pos);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) dst[(size_t)r * a.capacity] = from_f32<T>(v[r]);
+  }
+}
+
 // ------------------------------------------------------------------ the GEMM
 // Epilogue of one wave: lane holds output columns n0..n0+3 (weight rows) of activation
 // row m for each of its TPW fragment rows and MT activation tiles.  Row inputs that need
@@ -237,57 +296,16 @@ LSV_DEV void gemm_epilogue(const GemmArgs& a, const int M, const int m0, const i
         }
       }
   } else if (EPI == EPI_QKV) {
-      const int qrows = a.nq * a.hd, krows = a.nkv * a.hd;
+      double inv_freq[TPW][2];
+#pragma unroll
+      for (int t = 0; t < TPW; ++t) qkv_inv_freq(a, (tn0 + t) * 16 + 4 * g4, inv_freq[t]);
 #pragma unroll
       for (int t = 0; t < TPW; ++t)
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) {
           const int m = m0 + mt * 16 + l16, n0 = (tn0 + t) * 16 + 4 * g4;
-          if (m >= M || !tvalid[t] || n0 >= qrows + 2 * krows) continue;
-          const int b = qkv_b[mt], pos = qkv_pos[mt];
-          const f32x4_t v = acc[t][mt] * inv[mt];
-          if (n0 < qrows + krows) {
-            const bool isq = n0 < qrows;
-            const int local = isq ? n0 : n0 - qrows;
-            const int head = local / a.hd, i0 = (local % a.hd) >> 1;  // pairs (i0, i0+hd/2), (i0+1, i0+1+hd/2)
-            float out[4];
-#pragma unroll
-            for (int pr = 0; pr < 2; ++pr) {
-              // angle = pos * base^(-2i/hd) in fp64, reduced to [-pi, pi] in fp64, then fp32 sin/cos
-              const int i = i0 + pr;
-              const double inv_freq = exp2(-(double)(2 * i) / (double)a.hd * a.log2_rope_base);
-              const double ang = (double)pos * inv_freq;
-              const double red2pi = ang - 6.283185307179586 * rint(ang * 0.15915494309189535);
-              float sn, cs;
-              sincosf((float)red2pi, &sn, &cs);
-              const float x1 = v[2 * pr], x2 = v[2 * pr + 1];
-              out[2 * pr] = x1 * cs - x2 * sn;
-              out[2 * pr + 1] = x2 * cs + x1 * sn;
-            }
-            T* dst;
-            if (isq) {
-              dst = (T*)a.q_out + ((size_t)m * a.nq + head) * a.hd;
-            } else {
-              if (pos < 0 || pos >= a.capacity) continue;
-              dst = (T*)a.kv + ((((size_t)a.layer * 2 + 0) * a.batch + b) * a.nkv + head) * (size_t)a.capacity * a.hd +
-                    (size_t)pos * a.hd;
-            }
-            GLOBAL T* gd = GL(dst);
-            gd[i0] = from_f32<T>(out[0]);
-            gd[i0 + a.hd / 2] = from_f32<T>(out[1]);
-            gd[i0 + 1] = from_f32<T>(out[2]);
-            gd[i0 + 1 + a.hd / 2] = from_f32<T>(out[3]);
-          } else {
-            if (pos < 0 || pos >= a.capacity) continue;
-            // V rows are stored transposed: [head_dim][capacity], column v_column(pos)
-            const int local = n0 - qrows - krows;
-            const int head = local / a.hd, d0 = local % a.hd;
-            GLOBAL T* dst = GL((T*)a.kv) +
-                            ((((size_t)a.layer * 2 + 1) * a.batch + b) * a.nkv + head) * (size_t)a.capacity * a.hd +
-                            (size_t)d0 * a.capacity + v_column(pos);
-#pragma unroll
-            for (int r = 0; r < 4; ++r) dst[(size_t)r * a.capacity] = from_f32<T>(v[r]);
-          }
+          if (m >= M || !tvalid[t]) continue;
+          qkv_store4<T>(a, m, n0, acc[t][mt] * inv[mt], qkv_b[mt], qkv_pos[mt], inv_freq[t]);
         }
     } else if (EPI == EPI_RESID) {
       // h += y; the storage-type copy of h for the next consumer; per-row sum of squares of
@@ -536,19 +554,16 @@ static int launch_typed(GemmKind kind, int MT, const GemmArgs& a, hipStream_t st
 // Each k-step's activation slab (rows x 32 columns, one fragment per 16 rows) is staged in
 // LDS (double buffered) by the whole workgroup and multiplied by every wave with its own
 // weight fragments: 2 x 17 MFMAs per k-step and wave.  Slab pieces and weight fragments of
-// the next kWideRing k-steps are in flight in a register ring.  A split
-// group hands fp32 partials over with 16-byte device-scope stores and a device-scope
-// counter; the last arrival reads them back in split order (deterministic) and runs the
-// epilogue.
+// the next kWideRing k-steps are in flight in a register ring.  With more than one k range
+// per tile, each workgroup writes fp32 partials and gemm_wide_reduce_kernel adds them in
+// split order (deterministic) and runs the epilogue, one workgroup per (tile, 16 rows).
+// The QKV projection runs the plain scaled epilogue into an fp32 buffer, and
+// qkv_rope_kernel applies the rotary embedding and the Q store / cache append.
 constexpr int kWideMT = kWideRows / 16;  // activation tiles
 constexpr int kWideRing = 3;            // k-steps of loads in flight (register ring)
 constexpr int kWideTPW = 2;             // fragment rows per wave
 
-LSV_DEV __amdgpu_buffer_rsrc_t part_rsrc(float* base, size_t bytes) {
-  // raw buffer over the partials (word 3 = the gfx9-family raw-buffer format)
-  return __builtin_amdgcn_make_buffer_rsrc(base, 0, (int)(bytes > 0x7fffffffu ? 0x7fffffffu : bytes), 0x00020000);
-}
-constexpr int kDeviceScope = 16;  // buffer cache policy: sc1 (coherent at device scope)
+constexpr int kWideCols = 4 * kWideTPW * 16;  // output columns of a workgroup
 
 template <int EPI>
 __global__ void __launch_bounds__(256) gemm_wide_kernel(GemmArgs a) {
@@ -556,7 +571,6 @@ __global__ void __launch_bounds__(256) gemm_wide_kernel(GemmArgs a) {
   constexpr int TPW = kWideTPW, MT = kWideMT, KT = 32, EPL = 8, R = kWideRing;
   constexpr int PIECES = MT * kWave, PPT = (PIECES + 255) / 256;  // 16-byte pieces of one k-step's slab
   __shared__ u32x4_t Bs[2][MT][kWave];
-  __shared__ int flag;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, l16 = lane & 15, g4 = lane >> 4;
   const int S = a.splits, tile = blockIdx.x / S, j = blockIdx.x % S;
   const int k0 = (int)((long long)j * a.Kt / S), k1 = (int)((long long)(j + 1) * a.Kt / S), nk = k1 - k0;
@@ -634,41 +648,16 @@ __global__ void __launch_bounds__(256) gemm_wide_kernel(GemmArgs a) {
   for (int st = 0; st < R; ++st)
     if (c + st < nk) step(st, c + st);
 
-  if (S > 1) {
-    const __amdgpu_buffer_rsrc_t prs = part_rsrc(a.part, a.part_bytes);
-    constexpr int COLS = 4 * TPW * 16;  // output columns of the workgroup
-    const size_t slot = (size_t)tile * S + j;
+  if (S > 1) {  // partial sums of this k range: [tile][split][M_max][kWideCols]
 #pragma unroll
     for (int t = 0; t < TPW; ++t)
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) {
         const int m = mt * 16 + l16, col = (wave * TPW + t) * 16 + 4 * g4;
-        if (mt < mt_n && m < M) {
-          const int off = (int)(((slot * a.M_max + m) * COLS + col) * sizeof(float));
-          __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4_t, acc[t][mt]), prs, off, 0, kDeviceScope);
-        }
+        if (mt < mt_n && m < M)
+          *(GLOBAL f32x4_t*)(a.part + (((size_t)tile * S + j) * a.M_max + m) * kWideCols + col) = acc[t][mt];
       }
-    __builtin_amdgcn_s_waitcnt(0);  // this thread's partials have reached the coherent level
-    __syncthreads();
-    if (tid == 0)
-      flag = __hip_atomic_fetch_add(&a.counters[tile], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == S - 1;
-    __syncthreads();
-    if (flag == 0) return;
-#pragma unroll
-    for (int t = 0; t < TPW; ++t)
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt) {
-        const int m = mt * 16 + l16, col = (wave * TPW + t) * 16 + 4 * g4;
-        f32x4_t sum = f32x4_t{0.f, 0.f, 0.f, 0.f};
-        if (mt < mt_n && m < M) {
-          for (int jj = 0; jj < S; ++jj) {
-            const int off = (int)(((((size_t)tile * S + jj) * a.M_max + m) * COLS + col) * sizeof(float));
-            sum += __builtin_bit_cast(f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(prs, off, 0, kDeviceScope));
-          }
-        }
-        acc[t][mt] = sum;
-      }
-    if (tid == 0) __hip_atomic_store(&a.counters[tile], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    return;
   }
   __shared__ float s_inv[kWideRows];
   __shared__ int s_seq[kWideRows], s_pos[kWideRows];
@@ -686,6 +675,49 @@ __global__ void __launch_bounds__(256) gemm_wide_kernel(GemmArgs a) {
   gemm_epilogue<T, MT, TPW, EPI, false>(a, M, 0, tn0, tvalid, acc, none, &rin);
 }
 
+// Split-K sums of the batched GEMM: one workgroup per (tile, 16 rows) adds the k ranges in
+// split order and runs the product's epilogue (wave w: fragment rows of the tile's wave w).
+template <int EPI>
+__global__ void __launch_bounds__(256) gemm_wide_reduce_kernel(GemmArgs a) {
+  constexpr int TPW = kWideTPW;
+  const int tile = blockIdx.x, m0 = blockIdx.y * 16, S = a.splits;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, l16 = lane & 15, g4 = lane >> 4;
+  const int M = min(GL(a.row_offsets)[a.batch], a.M_max);
+  if (m0 >= M) return;
+  const int tn0 = (tile * 4 + wave) * TPW, m = m0 + l16;
+  bool tvalid[TPW];
+  f32x4_t acc[TPW][1];
+  const f32x4_t none[TPW][1] = {};
+#pragma unroll
+  for (int t = 0; t < TPW; ++t) {
+    tvalid[t] = tn0 + t < a.Nt;
+    const int col = (wave * TPW + t) * 16 + 4 * g4;
+    f32x4_t sum = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    if (m < M)
+      for (int j = 0; j < S; ++j)
+        sum += *(const GLOBAL f32x4_t*)(a.part + (((size_t)tile * S + j) * a.M_max + m) * kWideCols + col);
+    acc[t][0] = sum;
+  }
+  gemm_epilogue<bf16_t, 1, TPW, EPI, false>(a, M, m0, tn0, tvalid, acc, none);
+}
+
+// Rotary embedding and Q store / cache append of a normalised QKV projection y [M][N] (fp32),
+// four columns per thread.
+__global__ void __launch_bounds__(256) qkv_rope_kernel(GemmArgs a, const float* y) {
+  const int M = min(GL(a.row_offsets)[a.batch], a.M_max);
+  const int groups = a.N / 4;
+  const size_t n = (size_t)M * groups;
+  for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (size_t)gridDim.x * 256) {
+    const int m = (int)(i / groups), n0 = (int)(i % groups) * 4;
+    const f32x4_t v = *(const GLOBAL f32x4_t*)(y + (size_t)m * a.N + n0);
+    const int b = seq_of_row(a.row_offsets, a.batch, m);
+    const int pos = GL(a.seq_len)[b] + (m - GL(a.row_offsets)[b]);
+    double f[2];
+    qkv_inv_freq(a, n0, f);
+    qkv_store4<bf16_t>(a, m, n0, v, b, pos, f);
+  }
+}
+
 WidePlan plan_wide(int Nt, int Kt) {
   WidePlan p;
   p.tiles = (Nt + 4 * kWideTPW - 1) / (4 * kWideTPW);
@@ -699,17 +731,34 @@ WidePlan plan_wide(int Nt, int Kt) {
 }
 
 size_t wide_part_floats(const WidePlan& p, int M_max) {
-  return p.splits > 1 ? (size_t)p.tiles * p.splits * M_max * (4 * kWideTPW * 16) : 0;
+  return p.splits > 1 ? (size_t)p.tiles * p.splits * M_max * kWideCols : 0;
 }
 
-int launch_gemm_wide(GemmKind kind, const GemmArgs& a, const WidePlan& p, hipStream_t st) {
-  const dim3 grid((unsigned)(p.tiles * p.splits)), block(256);
+template <int EPI>
+static void launch_wide_epi(const GemmArgs& a, const WidePlan& p, int max_rows, hipStream_t st) {
+  hipLaunchKernelGGL(gemm_wide_kernel<EPI>, dim3((unsigned)(p.tiles * p.splits)), dim3(256), 0, st, a);
+  if (p.splits > 1)
+    hipLaunchKernelGGL(gemm_wide_reduce_kernel<EPI>, dim3((unsigned)p.tiles, (unsigned)((max_rows + 15) / 16)), dim3(256),
+                       0, st, a);
+}
+
+int launch_gemm_wide(GemmKind kind, const GemmArgs& a0, const WidePlan& p, hipStream_t st) {
+  GemmArgs a = a0;
+  a.splits = p.splits;
   switch (kind) {
-    case GEMM_QKV: hipLaunchKernelGGL(gemm_wide_kernel<EPI_QKV>, grid, block, 0, st, a); break;
-    case GEMM_O: hipLaunchKernelGGL(gemm_wide_kernel<EPI_RESID>, grid, block, 0, st, a); break;
-    case GEMM_GATEUP: hipLaunchKernelGGL(gemm_wide_kernel<EPI_SWIGLU>, grid, block, 0, st, a); break;
-    case GEMM_DOWN: hipLaunchKernelGGL(gemm_wide_kernel<EPI_RESID>, grid, block, 0, st, a); break;
-    case GEMM_LMHEAD: hipLaunchKernelGGL(gemm_wide_kernel<EPI_LOGITS>, grid, block, 0, st, a); break;
+    case GEMM_QKV: {
+      // scaled projection into the caller's fp32 buffer (out_f32, N columns), then RoPE
+      if (!a.out_f32) return LSV_ERR_INVALID_ARG;
+      a.ldo = a.N;
+      launch_wide_epi<EPI_LOGITS>(a, p, a.M_max, st);
+      const size_t n = (size_t)a.M_max * (a.N / 4);
+      hipLaunchKernelGGL(qkv_rope_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, a, a.out_f32);
+      break;
+    }
+    case GEMM_O: launch_wide_epi<EPI_RESID>(a, p, a.M_max, st); break;
+    case GEMM_GATEUP: launch_wide_epi<EPI_SWIGLU>(a, p, a.M_max, st); break;
+    case GEMM_DOWN: launch_wide_epi<EPI_RESID>(a, p, a.M_max, st); break;
+    case GEMM_LMHEAD: launch_wide_epi<EPI_LOGITS>(a, p, a.M_max, st); break;
   }
   return hipGetLastError() == hipSuccess ? LSV_OK : LSV_ERR_HIP;
 }

@@ -28,12 +28,11 @@ struct GemmArgs {
   const float* stats;
   int P;
   float eps;
-  // wide blocks: k-split partials [tiles][splits][M_max][128] and per-tile arrival counters
+  // wide blocks: k-split partials [tiles][splits][M_max][128]
   float* part;
   size_t part_bytes;
   int splits;
-  int* counters;  // zero on entry and on exit
-  // EPI_LOGITS
+  // EPI_LOGITS (and, for wide blocks, the normalised QKV projection before RoPE)
   float* out_f32;
   int ldo;
   // EPI_QKV
