@@ -560,22 +560,27 @@ static int launch_typed(GemmKind kind, int MT, const GemmArgs& a, hipStream_t st
 // The QKV projection runs the plain scaled epilogue into an fp32 buffer, and
 // qkv_rope_kernel applies the rotary embedding and the Q store / cache append.
 constexpr int kWideMT = kWideRows / 16;  // activation tiles
-constexpr int kWideRing = 3;            // k-steps of loads in flight (register ring)
+constexpr int kWideRingW = 8;           // k-steps of weight fragments in flight (register ring)
+constexpr int kWideRingB = 2;           // k-steps of activation slab in flight (it comes from L2)
 constexpr int kWideTPW = 2;             // fragment rows per wave
 
 constexpr int kWideCols = 4 * kWideTPW * 16;  // output columns of a workgroup
 
-template <int EPI>
+// MT activation tiles (from the host row bound, <= kWideMT): every k-step multiplies all of
+// them, with no per-tile branch between the slab reads and the MFMAs; tiles past the device
+// row count hold stale values and give output columns that are never stored.
+template <int EPI, int MT>
 __global__ void __launch_bounds__(256) gemm_wide_kernel(GemmArgs a) {
   using T = bf16_t;
-  constexpr int TPW = kWideTPW, MT = kWideMT, KT = 32, EPL = 8, R = kWideRing;
+  constexpr int TPW = kWideTPW, KT = 32, EPL = 8, RW = kWideRingW, RB = kWideRingB;
+  static_assert(MT <= kWideMT, "activation tiles");
   constexpr int PIECES = MT * kWave, PPT = (PIECES + 255) / 256;  // 16-byte pieces of one k-step's slab
   __shared__ u32x4_t Bs[2][MT][kWave];
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, l16 = lane & 15, g4 = lane >> 4;
   const int S = a.splits, tile = blockIdx.x / S, j = blockIdx.x % S;
   const int k0 = (int)((long long)j * a.Kt / S), k1 = (int)((long long)(j + 1) * a.Kt / S), nk = k1 - k0;
   const int M = min(GL(a.row_offsets)[a.batch], a.M_max);  // never trust device rows beyond the host bound
-  const int mt_n = (M + 15) / 16;                           // <= MT: the host bound is <= kWideRows
+  const int mt_n = min((M + 15) / 16, MT);                  // tiles holding device rows
   const int tn0 = (tile * 4 + wave) * TPW;
   bool tvalid[TPW];
   int tr[TPW];
@@ -587,25 +592,28 @@ __global__ void __launch_bounds__(256) gemm_wide_kernel(GemmArgs a) {
   const GLOBAL u32x4_t* wbase = (const GLOBAL u32x4_t*)a.W + lane;
   const GLOBAL T* xg = (const GLOBAL T*)a.x;
 
-  // Register ring of R k-steps: activation slab pieces and the wave's weight fragments.
-  // Slab piece p = (mt, ln): activation tile mt, lane ln of its fragment.
-  u32x4_t bst[R][PPT], wa[R][TPW];
-  auto issue = [&](int st, int k) {
+  // Register rings: the wave's weight fragments of the next RW k-steps, and the slab pieces
+  // (piece p = (mt, ln): activation tile mt, lane ln of its fragment) of the next RB.
+  u32x4_t bst[RB][PPT], wa[RW][TPW];
+  auto issue_w = [&](int sw, int k) {
+    const int kk = max(min(k, nk - 1), 0);
+#pragma unroll
+    for (int t = 0; t < TPW; ++t) wa[sw][t] = wbase[frag_index(tr[t], k0 + kk, a.Nt, a.Kt) * 64];
+  };
+  auto issue_b = [&](int sb, int k) {
     const int kk = max(min(k, nk - 1), 0);
 #pragma unroll
     for (int i = 0; i < PPT; ++i) {
       const int p = tid + 256 * i, mt = p / kWave, ln = p % kWave;
       if (p < PIECES && mt < mt_n)
-        bst[st][i] = *(const GLOBAL u32x4_t*)(xg + (((size_t)mt * a.Kt + k0 + kk) * kWave + ln) * EPL);
+        bst[sb][i] = *(const GLOBAL u32x4_t*)(xg + (((size_t)mt * a.Kt + k0 + kk) * kWave + ln) * EPL);
     }
-#pragma unroll
-    for (int t = 0; t < TPW; ++t) wa[st][t] = wbase[frag_index(tr[t], k0 + kk, a.Nt, a.Kt) * 64];
   };
-  auto store = [&](int st, int buf) {
+  auto store = [&](int sb, int buf) {
 #pragma unroll
     for (int i = 0; i < PPT; ++i) {
       const int p = tid + 256 * i;
-      if (p < PIECES && p / kWave < mt_n) (&Bs[buf][0][0])[p] = bst[st][i];
+      if (p < PIECES && p / kWave < mt_n) (&Bs[buf][0][0])[p] = bst[sb][i];
     }
   };
   f32x4_t acc[TPW][MT];
@@ -617,36 +625,42 @@ __global__ void __launch_bounds__(256) gemm_wide_kernel(GemmArgs a) {
   auto compute = [&](int buf) {
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
-      if (mt >= mt_n) break;
       const u32x4_t b = Bs[buf][mt][lane];
 #pragma unroll
       for (int t = 0; t < TPW; ++t) mfma_frag(wcur[t], b, acc[t][mt], T{});
     }
   };
   // k-step c: its slab sits in LDS buffer c & 1 (stored during step c - 1); the slab of
-  // step c + 1 moves from registers to the other buffer; step c + R is issued into the
-  // register stage that step c freed.  One barrier per step.
-  auto step = [&](int st, int c) {
-    // st = c % R: stage of step c (already consumed into LDS); stage of c + 1 is (st + 1) % R
+  // step c + 1 moves from its register stage to the other buffer and that stage takes the
+  // slab of step c + 1 + RB; the weight stage of step c takes step c + RW.  One barrier
+  // per step.
+  // u = c mod UNR (a compile-time constant where step is called), so ring stages are static
+  constexpr int UNR = RW % RB == 0 ? RW : RW * RB;  // a multiple of both ring lengths
+  auto step = [&](int c, int u) {
+    const int sw = u % RW, sb = (u + 1) % RB;
 #pragma unroll
-    for (int t = 0; t < TPW; ++t) wcur[t] = wa[st][t];
-    if (c + 1 < nk) store((st + 1) % R, (c + 1) & 1);
-    issue(st, c + R);
+    for (int t = 0; t < TPW; ++t) wcur[t] = wa[sw][t];
+    if (c + 1 < nk) store(sb, (c + 1) & 1);
+    issue_b(sb, c + 1 + RB);
+    issue_w(sw, c + RW);
     compute(c & 1);
     __syncthreads();
   };
 #pragma unroll
-  for (int st = 0; st < R; ++st) issue(st, st);
+  for (int sw = 0; sw < RW; ++sw) issue_w(sw, sw);
+#pragma unroll
+  for (int sb = 0; sb < RB; ++sb) issue_b(sb, sb);
   store(0, 0);
+  issue_b(0, RB);
   __syncthreads();
   int c = 0;
-  for (; c + R <= nk; c += R) {
+  for (; c + UNR <= nk; c += UNR) {
 #pragma unroll
-    for (int st = 0; st < R; ++st) step(st, c + st);
+    for (int u = 0; u < UNR; ++u) step(c + u, u);
   }
 #pragma unroll
-  for (int st = 0; st < R; ++st)
-    if (c + st < nk) step(st, c + st);
+  for (int u = 0; u < UNR; ++u)
+    if (c + u < nk) step(c + u, u);
 
   if (S > 1) {  // partial sums of this k range: [tile][split][M_max][kWideCols]
 #pragma unroll
@@ -736,7 +750,14 @@ size_t wide_part_floats(const WidePlan& p, int M_max) {
 
 template <int EPI>
 static void launch_wide_epi(const GemmArgs& a, const WidePlan& p, int max_rows, hipStream_t st) {
-  hipLaunchKernelGGL(gemm_wide_kernel<EPI>, dim3((unsigned)(p.tiles * p.splits)), dim3(256), 0, st, a);
+  const dim3 grid((unsigned)(p.tiles * p.splits)), block(256);
+  const int tiles = (max_rows + 15) / 16;
+  if (tiles <= 9)
+    hipLaunchKernelGGL((gemm_wide_kernel<EPI, 9>), grid, block, 0, st, a);
+  else if (tiles <= 13)
+    hipLaunchKernelGGL((gemm_wide_kernel<EPI, 13>), grid, block, 0, st, a);
+  else
+    hipLaunchKernelGGL((gemm_wide_kernel<EPI, kWideMT>), grid, block, 0, st, a);
   if (p.splits > 1)
     hipLaunchKernelGGL(gemm_wide_reduce_kernel<EPI>, dim3((unsigned)p.tiles, (unsigned)((max_rows + 15) / 16)), dim3(256),
                        0, st, a);
