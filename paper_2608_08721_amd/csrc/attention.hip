@@ -16,6 +16,8 @@
 // fp32 path: a plain kernel, one wave per (row, query head).
 #include <math.h>
 
+#include <type_traits>
+
 #include "lsv_attn.h"
 #include "lsv_device.h"
 
@@ -125,8 +127,12 @@ __global__ void __launch_bounds__(64 * NW) attn_split_bf16_kernel(AttnArgs a) {
     }
     if (qbase > 0 && c0 + grp < c1) load_chunk(c0 + grp);  // a later pass over the same split
 
-    // scores and running-softmax update of this wave's tile for the chunk in buffer g
-    auto consume = [&](int g, int c) {
+    // scores and running-softmax update of this wave's tile for the chunk in buffer g.
+    // A chunk below the cached length C is visible to every row of the block: no mask,
+    // and its scores are finite (the hardware exp2 then needs no guard); only chunks that
+    // reach the block's own keys apply the causal and length mask.
+    auto consume = [&](int g, int c, auto masked) {
+      constexpr bool MASK = decltype(masked)::value;
       const int k0 = c * kCh;
       f32x4_t sc[4];
 #pragma unroll
@@ -145,25 +151,39 @@ __global__ void __launch_bounds__(64 * NW) attn_split_bf16_kernel(AttnArgs a) {
       for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const int kp = k0 + 16 * kt + 4 * g4 + r;
-          const bool ok = qval && kp < L && kp <= qpos;
-          const float v = ok ? sc[kt][r] * a.scale_log2 : -INFINITY;
+          float v = sc[kt][r] * a.scale_log2;
+          if (MASK) {
+            const int kp = k0 + 16 * kt + 4 * g4 + r;
+            v = qval && kp < L && kp <= qpos ? v : -INFINITY;
+          }
           sc[kt][r] = v;
           mx = fmaxf(mx, v);
         }
       mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
       mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
       const float mnew = fmaxf(mrun, mx);
-      const float alpha = mrun == -INFINITY ? 0.f : exp2f(mrun - mnew);
-      float sum = 0.f;
+      float alpha, sum = 0.f;
+      if (MASK) {
+        alpha = mrun == -INFINITY ? 0.f : exp2f(mrun - mnew);
 #pragma unroll
-      for (int kt = 0; kt < 4; ++kt)
+        for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const float p = mnew == -INFINITY ? 0.f : exp2f(sc[kt][r] - mnew);
-          sc[kt][r] = p;
-          sum += p;
-        }
+          for (int r = 0; r < 4; ++r) {
+            const float p = mnew == -INFINITY ? 0.f : exp2f(sc[kt][r] - mnew);
+            sc[kt][r] = p;
+            sum += p;
+          }
+      } else {  // mnew is finite; exp2(-inf) = 0 covers a first chunk (mrun = -inf)
+        alpha = __builtin_amdgcn_exp2f(mrun - mnew);
+#pragma unroll
+        for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const float p = __builtin_amdgcn_exp2f(sc[kt][r] - mnew);
+            sc[kt][r] = p;
+            sum += p;
+          }
+      }
       sum += __shfl_xor(sum, 16, kWave);
       sum += __shfl_xor(sum, 32, kWave);
       mrun = mnew;
@@ -192,12 +212,21 @@ __global__ void __launch_bounds__(64 * NW) attn_split_bf16_kernel(AttnArgs a) {
       __syncthreads();
       if (c + NG + grp < c1) load_chunk(c + NG + grp);
       if (!active) continue;  // wave-uniform: a wave without a query tile in this pass
+      using Masked = std::true_type;
+      using Full = std::false_type;
       if (halves) {
-        if (c + grp < c1) consume(grp, c + grp);
+        const int cc = c + grp;
+        if (cc < c1) {
+          if ((cc + 1) * kCh <= C) consume(grp, cc, Full{});
+          else consume(grp, cc, Masked{});
+        }
       } else {
 #pragma unroll
         for (int g = 0; g < NG; ++g)
-          if (c + g < c1) consume(g, c + g);
+          if (c + g < c1) {
+            if ((c + g + 1) * kCh <= C) consume(g, c + g, Full{});
+            else consume(g, c + g, Masked{});
+          }
       }
     }
 

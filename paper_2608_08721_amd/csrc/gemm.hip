@@ -566,20 +566,19 @@ constexpr int kWideTPW = 2;             // fragment rows per wave
 
 constexpr int kWideCols = 4 * kWideTPW * 16;  // output columns of a workgroup
 
-// MT activation tiles (from the host row bound, <= kWideMT): every k-step multiplies all of
-// them, with no per-tile branch between the slab reads and the MFMAs; tiles past the device
-// row count hold stale values and give output columns that are never stored.
+// The body for MT activation tiles: every k-step multiplies all MT of them, with no per-tile
+// branch between the slab reads and the MFMAs; tiles past the device row count hold stale
+// values and give output columns that are never stored.  Bs: two slab buffers of kWideMT
+// tiles; s_inv / s_seq / s_pos: per-row epilogue inputs (LDS of the calling kernel).
 template <int EPI, int MT>
-__global__ void __launch_bounds__(256) gemm_wide_kernel(GemmArgs a) {
+LSV_DEV void gemm_wide_body(const GemmArgs& a, const int M, u32x4_t* Bs, float* s_inv, int* s_seq, int* s_pos) {
   using T = bf16_t;
   constexpr int TPW = kWideTPW, KT = 32, EPL = 8, RW = kWideRingW, RB = kWideRingB;
   static_assert(MT <= kWideMT, "activation tiles");
   constexpr int PIECES = MT * kWave, PPT = (PIECES + 255) / 256;  // 16-byte pieces of one k-step's slab
-  __shared__ u32x4_t Bs[2][MT][kWave];
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, l16 = lane & 15, g4 = lane >> 4;
   const int S = a.splits, tile = blockIdx.x / S, j = blockIdx.x % S;
   const int k0 = (int)((long long)j * a.Kt / S), k1 = (int)((long long)(j + 1) * a.Kt / S), nk = k1 - k0;
-  const int M = min(GL(a.row_offsets)[a.batch], a.M_max);  // never trust device rows beyond the host bound
   const int mt_n = min((M + 15) / 16, MT);                  // tiles holding device rows
   const int tn0 = (tile * 4 + wave) * TPW;
   bool tvalid[TPW];
@@ -613,7 +612,7 @@ __global__ void __launch_bounds__(256) gemm_wide_kernel(GemmArgs a) {
 #pragma unroll
     for (int i = 0; i < PPT; ++i) {
       const int p = tid + 256 * i;
-      if (p < PIECES && p / kWave < mt_n) (&Bs[buf][0][0])[p] = bst[sb][i];
+      if (p < PIECES && p / kWave < mt_n) Bs[buf * kWideMT * kWave + p] = bst[sb][i];
     }
   };
   f32x4_t acc[TPW][MT];
@@ -625,7 +624,7 @@ __global__ void __launch_bounds__(256) gemm_wide_kernel(GemmArgs a) {
   auto compute = [&](int buf) {
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
-      const u32x4_t b = Bs[buf][mt][lane];
+      const u32x4_t b = Bs[(buf * kWideMT + mt) * kWave + lane];
 #pragma unroll
       for (int t = 0; t < TPW; ++t) mfma_frag(wcur[t], b, acc[t][mt], T{});
     }
@@ -673,8 +672,6 @@ __global__ void __launch_bounds__(256) gemm_wide_kernel(GemmArgs a) {
       }
     return;
   }
-  __shared__ float s_inv[kWideRows];
-  __shared__ int s_seq[kWideRows], s_pos[kWideRows];
   for (int r = tid; r < a.M_max; r += 256) {
     if (EPI != EPI_RESID) s_inv[r] = inv_rms_serial(a, r);
     if (EPI == EPI_QKV) {
@@ -687,6 +684,25 @@ __global__ void __launch_bounds__(256) gemm_wide_kernel(GemmArgs a) {
   const RowInputs rin{s_inv, s_seq, s_pos};
   const f32x4_t none[TPW][MT] = {};
   gemm_epilogue<T, MT, TPW, EPI, false>(a, M, 0, tn0, tvalid, acc, none, &rin);
+}
+
+// One launch for any row count up to kWideRows: the body is chosen once per workgroup from
+// the device row count (5, 9, 13 or 17 activation tiles).
+template <int EPI>
+__global__ void __launch_bounds__(256) gemm_wide_kernel(GemmArgs a) {
+  __shared__ u32x4_t Bs[2 * kWideMT * kWave];
+  __shared__ float s_inv[kWideRows];
+  __shared__ int s_seq[kWideRows], s_pos[kWideRows];
+  const int M = min(GL(a.row_offsets)[a.batch], a.M_max);  // never trust device rows beyond the host bound
+  const int mt_n = (M + 15) / 16;
+  if (mt_n <= 5)
+    gemm_wide_body<EPI, 5>(a, M, Bs, s_inv, s_seq, s_pos);
+  else if (mt_n <= 9)
+    gemm_wide_body<EPI, 9>(a, M, Bs, s_inv, s_seq, s_pos);
+  else if (mt_n <= 13)
+    gemm_wide_body<EPI, 13>(a, M, Bs, s_inv, s_seq, s_pos);
+  else
+    gemm_wide_body<EPI, kWideMT>(a, M, Bs, s_inv, s_seq, s_pos);
 }
 
 // Split-K sums of the batched GEMM: one workgroup per (tile, 16 rows) adds the k ranges in
@@ -750,14 +766,7 @@ size_t wide_part_floats(const WidePlan& p, int M_max) {
 
 template <int EPI>
 static void launch_wide_epi(const GemmArgs& a, const WidePlan& p, int max_rows, hipStream_t st) {
-  const dim3 grid((unsigned)(p.tiles * p.splits)), block(256);
-  const int tiles = (max_rows + 15) / 16;
-  if (tiles <= 9)
-    hipLaunchKernelGGL((gemm_wide_kernel<EPI, 9>), grid, block, 0, st, a);
-  else if (tiles <= 13)
-    hipLaunchKernelGGL((gemm_wide_kernel<EPI, 13>), grid, block, 0, st, a);
-  else
-    hipLaunchKernelGGL((gemm_wide_kernel<EPI, kWideMT>), grid, block, 0, st, a);
+  hipLaunchKernelGGL(gemm_wide_kernel<EPI>, dim3((unsigned)(p.tiles * p.splits)), dim3(256), 0, st, a);
   if (p.splits > 1)
     hipLaunchKernelGGL(gemm_wide_reduce_kernel<EPI>, dim3((unsigned)p.tiles, (unsigned)((max_rows + 15) / 16)), dim3(256),
                        0, st, a);
