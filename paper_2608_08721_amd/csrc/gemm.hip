@@ -548,109 +548,104 @@ static int launch_typed(GemmKind kind, int MT, const GemmArgs& a, hipStream_t st
 }
 
 // ------------------------------------------------------------------ wide blocks
-// Batched verification (64 < rows <= kWideRows): the matrix cores become the bound, so a
-// workgroup keeps every activation row and shares the activation operand through LDS.
-// Workgroup = 4 waves x 2 fragment rows (128 output columns) x one of `splits` k ranges.
-// Each k-step's activation slab (rows x 32 columns, one fragment per 16 rows) is staged in
-// LDS (double buffered) by the whole workgroup and multiplied by every wave with its own
-// weight fragments: 2 x 17 MFMAs per k-step and wave.  Slab pieces and weight fragments of
-// the next kWideRing k-steps are in flight in a register ring.  With more than one k range
-// per tile, each workgroup writes fp32 partials and gemm_wide_reduce_kernel adds them in
-// split order (deterministic) and runs the epilogue, one workgroup per (tile, 16 rows).
-// The QKV projection runs the plain scaled epilogue into an fp32 buffer, and
-// qkv_rope_kernel applies the rotary embedding and the Q store / cache append.
-constexpr int kWideMT = kWideRows / 16;  // activation tiles
-constexpr int kWideRingW = 8;           // k-steps of weight fragments in flight (register ring)
-constexpr int kWideRingB = 2;           // k-steps of activation slab in flight (it comes from L2)
-constexpr int kWideTPW = 2;             // fragment rows per wave
+// Batched verification (64 < rows <= kWideRows): the matrix cores become the bound.
+// Workgroup = 4 waves x 8 fragment rows (128 output columns) x one of `splits` k ranges;
+// the waves share the 8 weight fragments of each k-step through LDS and split the rows:
+// wave w keeps activation tiles w*MTW .. w*MTW+MTW-1 (MTW <= 5) in registers.  With more
+// than one k range per tile, each workgroup writes fp32 partials and
+// gemm_wide_reduce_kernel adds them in split order (deterministic) and runs the epilogue,
+// one workgroup per (tile, 16 rows).  The QKV projection runs the plain scaled epilogue
+// into an fp32 buffer, and qkv_rope_kernel applies the rotary embedding and the Q store /
+// cache append.
+constexpr int kWideFR = 8;     // fragment rows of a workgroup
+constexpr int kWideRingW = 10;  // k-steps of weight pieces in flight (register ring)
+constexpr int kWideRingX = 2;   // k-steps of activation fragments in flight (from L2)
 
-constexpr int kWideCols = 4 * kWideTPW * 16;  // output columns of a workgroup
+constexpr int kWideCols = kWideFR * 16;  // output columns of a workgroup
 
-// The body for MT activation tiles: every k-step multiplies all MT of them, with no per-tile
-// branch between the slab reads and the MFMAs; tiles past the device row count hold stale
-// values and give output columns that are never stored.  Bs: two slab buffers of kWideMT
-// tiles; s_inv / s_seq / s_pos: per-row epilogue inputs (LDS of the calling kernel).
-template <int EPI, int MT>
-LSV_DEV void gemm_wide_body(const GemmArgs& a, const int M, u32x4_t* Bs, float* s_inv, int* s_seq, int* s_pos) {
+// The body for MTW activation tiles per wave.  The workgroup's 8 weight fragments of a
+// k-step go HBM -> registers -> LDS (double buffered) and every wave reads all 8; each wave
+// keeps its own MTW activation tiles (rows wave*16*MTW ..) in registers, straight from L2.
+// A k-step is 8 LDS reads and 8 x MTW MFMAs per wave, each read feeding MTW of them.  Tiles
+// past the device row count are computed on clamped rows and never stored.
+// Ws: two buffers of 8 fragments; s_inv / s_seq / s_pos: per-row epilogue inputs (LDS).
+template <int EPI, int MTW>
+LSV_DEV void gemm_wide_body(const GemmArgs& a, const int M, u32x4_t* Ws, float* s_inv, int* s_seq, int* s_pos) {
   using T = bf16_t;
-  constexpr int TPW = kWideTPW, KT = 32, EPL = 8, RW = kWideRingW, RB = kWideRingB;
-  static_assert(MT <= kWideMT, "activation tiles");
-  constexpr int PIECES = MT * kWave, PPT = (PIECES + 255) / 256;  // 16-byte pieces of one k-step's slab
+  constexpr int FR = kWideFR;
+  constexpr int RX = kWideRingX, RW = kWideRingW;
+  constexpr int PPT = FR * kWave / 256;  // 16-byte weight pieces per thread and k-step
+  static_assert(PPT * 256 == FR * kWave, "weight pieces divide over the threads");
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, l16 = lane & 15, g4 = lane >> 4;
   const int S = a.splits, tile = blockIdx.x / S, j = blockIdx.x % S;
   const int k0 = (int)((long long)j * a.Kt / S), k1 = (int)((long long)(j + 1) * a.Kt / S), nk = k1 - k0;
-  const int mt_n = min((M + 15) / 16, MT);                  // tiles holding device rows
-  const int tn0 = (tile * 4 + wave) * TPW;
-  bool tvalid[TPW];
-  int tr[TPW];
+  const int tn0 = tile * FR, mt0 = wave * MTW;
+  const int tiles_alloc = (a.M_max + 15) / 16;  // activation tiles in the buffer
+  bool tvalid[FR];
 #pragma unroll
-  for (int t = 0; t < TPW; ++t) {
-    tvalid[t] = tn0 + t < a.Nt;
-    tr[t] = tvalid[t] ? tn0 + t : 0;
-  }
-  const GLOBAL u32x4_t* wbase = (const GLOBAL u32x4_t*)a.W + lane;
-  const GLOBAL T* xg = (const GLOBAL T*)a.x;
+  for (int f = 0; f < FR; ++f) tvalid[f] = tn0 + f < a.Nt;
+  const GLOBAL u32x4_t* wg = (const GLOBAL u32x4_t*)a.W;
+  const GLOBAL u32x4_t* xg = (const GLOBAL u32x4_t*)a.x + lane;
+  int xt[MTW];  // activation tile of each of the wave's slots (clamped into the buffer)
+#pragma unroll
+  for (int mt = 0; mt < MTW; ++mt) xt[mt] = min(mt0 + mt, tiles_alloc - 1);
 
-  // Register rings: the wave's weight fragments of the next RW k-steps, and the slab pieces
-  // (piece p = (mt, ln): activation tile mt, lane ln of its fragment) of the next RB.
-  u32x4_t bst[RB][PPT], wa[RW][TPW];
+  // Register rings: weight pieces of the next RW k-steps (piece p = (fragment p / 64, lane
+  // p % 64)), and this wave's activation fragments of the next RX.
+  u32x4_t wst[RW][PPT], xr[RX][MTW];
   auto issue_w = [&](int sw, int k) {
     const int kk = max(min(k, nk - 1), 0);
 #pragma unroll
-    for (int t = 0; t < TPW; ++t) wa[sw][t] = wbase[frag_index(tr[t], k0 + kk, a.Nt, a.Kt) * 64];
+    for (int i = 0; i < PPT; ++i) {
+      const int p = tid + 256 * i, f = p / kWave, ln = p % kWave;
+      const int fr = tn0 + f < a.Nt ? tn0 + f : 0;
+      wst[sw][i] = wg[frag_index(fr, k0 + kk, a.Nt, a.Kt) * kWave + ln];
+    }
   };
-  auto issue_b = [&](int sb, int k) {
+  auto issue_x = [&](int sx, int k) {
     const int kk = max(min(k, nk - 1), 0);
 #pragma unroll
-    for (int i = 0; i < PPT; ++i) {
-      const int p = tid + 256 * i, mt = p / kWave, ln = p % kWave;
-      if (p < PIECES && mt < mt_n)
-        bst[sb][i] = *(const GLOBAL u32x4_t*)(xg + (((size_t)mt * a.Kt + k0 + kk) * kWave + ln) * EPL);
-    }
+    for (int mt = 0; mt < MTW; ++mt) xr[sx][mt] = xg[((size_t)xt[mt] * a.Kt + k0 + kk) * kWave];
   };
-  auto store = [&](int sb, int buf) {
+  auto store = [&](int sw, int buf) {
 #pragma unroll
-    for (int i = 0; i < PPT; ++i) {
-      const int p = tid + 256 * i;
-      if (p < PIECES && p / kWave < mt_n) Bs[buf * kWideMT * kWave + p] = bst[sb][i];
-    }
+    for (int i = 0; i < PPT; ++i) Ws[buf * FR * kWave + tid + 256 * i] = wst[sw][i];
   };
-  f32x4_t acc[TPW][MT];
+  f32x4_t acc[FR][MTW];
 #pragma unroll
-  for (int t = 0; t < TPW; ++t)
+  for (int f = 0; f < FR; ++f)
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt) acc[t][mt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  u32x4_t wcur[TPW];
+    for (int mt = 0; mt < MTW; ++mt) acc[f][mt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  u32x4_t xcur[MTW];
   auto compute = [&](int buf) {
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-      const u32x4_t b = Bs[(buf * kWideMT + mt) * kWave + lane];
+    for (int f = 0; f < FR; ++f) {
+      const u32x4_t w = Ws[(buf * FR + f) * kWave + lane];
 #pragma unroll
-      for (int t = 0; t < TPW; ++t) mfma_frag(wcur[t], b, acc[t][mt], T{});
+      for (int mt = 0; mt < MTW; ++mt) mfma_frag(w, xcur[mt], acc[f][mt], T{});
     }
   };
-  // k-step c: its slab sits in LDS buffer c & 1 (stored during step c - 1); the slab of
-  // step c + 1 moves from its register stage to the other buffer and that stage takes the
-  // slab of step c + 1 + RB; the weight stage of step c takes step c + RW.  One barrier
-  // per step.
-  // u = c mod UNR (a compile-time constant where step is called), so ring stages are static
-  constexpr int UNR = RW % RB == 0 ? RW : RW * RB;  // a multiple of both ring lengths
+  // k-step c: its weights sit in LDS buffer c & 1 (stored during step c - 1); the weights of
+  // step c + 1 move from their register stage to the other buffer and that stage takes step
+  // c + 1 + RW; the activation stage of step c takes step c + RX.  One barrier per step.
+  // u = c mod UNR (a compile-time constant where step is called), so ring stages are static.
+  constexpr int UNR = RX % RW == 0 ? RX : (RW % RX == 0 ? RW : RX * RW);
   auto step = [&](int c, int u) {
-    const int sw = u % RW, sb = (u + 1) % RB;
+    const int sx = u % RX, sw = (u + 1) % RW;
 #pragma unroll
-    for (int t = 0; t < TPW; ++t) wcur[t] = wa[sw][t];
-    if (c + 1 < nk) store(sb, (c + 1) & 1);
-    issue_b(sb, c + 1 + RB);
-    issue_w(sw, c + RW);
+    for (int mt = 0; mt < MTW; ++mt) xcur[mt] = xr[sx][mt];
+    if (c + 1 < nk) store(sw, (c + 1) & 1);
+    issue_w(sw, c + 1 + RW);
+    issue_x(sx, c + RX);
     compute(c & 1);
     __syncthreads();
   };
 #pragma unroll
-  for (int sw = 0; sw < RW; ++sw) issue_w(sw, sw);
+  for (int sx = 0; sx < RX; ++sx) issue_x(sx, sx);
 #pragma unroll
-  for (int sb = 0; sb < RB; ++sb) issue_b(sb, sb);
+  for (int sw = 0; sw < RW; ++sw) issue_w(sw, sw);
   store(0, 0);
-  issue_b(0, RB);
+  issue_w(0, RW);
   __syncthreads();
   int c = 0;
   for (; c + UNR <= nk; c += UNR) {
@@ -663,12 +658,12 @@ LSV_DEV void gemm_wide_body(const GemmArgs& a, const int M, u32x4_t* Bs, float* 
 
   if (S > 1) {  // partial sums of this k range: [tile][split][M_max][kWideCols]
 #pragma unroll
-    for (int t = 0; t < TPW; ++t)
+    for (int f = 0; f < FR; ++f)
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt) {
-        const int m = mt * 16 + l16, col = (wave * TPW + t) * 16 + 4 * g4;
-        if (mt < mt_n && m < M)
-          *(GLOBAL f32x4_t*)(a.part + (((size_t)tile * S + j) * a.M_max + m) * kWideCols + col) = acc[t][mt];
+      for (int mt = 0; mt < MTW; ++mt) {
+        const int m = (mt0 + mt) * 16 + l16, col = f * 16 + 4 * g4;
+        if (m < M)
+          *(GLOBAL f32x4_t*)(a.part + (((size_t)tile * S + j) * a.M_max + m) * kWideCols + col) = acc[f][mt];
       }
     return;
   }
@@ -682,34 +677,36 @@ LSV_DEV void gemm_wide_body(const GemmArgs& a, const int M, u32x4_t* Bs, float* 
   }
   __syncthreads();
   const RowInputs rin{s_inv, s_seq, s_pos};
-  const f32x4_t none[TPW][MT] = {};
-  gemm_epilogue<T, MT, TPW, EPI, false>(a, M, 0, tn0, tvalid, acc, none, &rin);
+  const f32x4_t none[FR][MTW] = {};
+  gemm_epilogue<T, MTW, FR, EPI, false>(a, M, mt0 * 16, tn0, tvalid, acc, none, &rin);
 }
 
 // One launch for any row count up to kWideRows: the body is chosen once per workgroup from
-// the device row count (5, 9, 13 or 17 activation tiles).
+// the device row count (1 to 5 activation tiles per wave).
 template <int EPI>
 __global__ void __launch_bounds__(256) gemm_wide_kernel(GemmArgs a) {
-  __shared__ u32x4_t Bs[2 * kWideMT * kWave];
+  __shared__ u32x4_t Ws[2 * kWideFR * kWave];
   __shared__ float s_inv[kWideRows];
   __shared__ int s_seq[kWideRows], s_pos[kWideRows];
   const int M = min(GL(a.row_offsets)[a.batch], a.M_max);  // never trust device rows beyond the host bound
-  const int mt_n = (M + 15) / 16;
-  if (mt_n <= 5)
-    gemm_wide_body<EPI, 5>(a, M, Bs, s_inv, s_seq, s_pos);
-  else if (mt_n <= 9)
-    gemm_wide_body<EPI, 9>(a, M, Bs, s_inv, s_seq, s_pos);
-  else if (mt_n <= 13)
-    gemm_wide_body<EPI, 13>(a, M, Bs, s_inv, s_seq, s_pos);
+  const int mtw = ((M + 15) / 16 + 3) / 4;                 // activation tiles per wave
+  if (mtw <= 1)
+    gemm_wide_body<EPI, 1>(a, M, Ws, s_inv, s_seq, s_pos);
+  else if (mtw == 2)
+    gemm_wide_body<EPI, 2>(a, M, Ws, s_inv, s_seq, s_pos);
+  else if (mtw == 3)
+    gemm_wide_body<EPI, 3>(a, M, Ws, s_inv, s_seq, s_pos);
+  else if (mtw == 4)
+    gemm_wide_body<EPI, 4>(a, M, Ws, s_inv, s_seq, s_pos);
   else
-    gemm_wide_body<EPI, kWideMT>(a, M, Bs, s_inv, s_seq, s_pos);
+    gemm_wide_body<EPI, 5>(a, M, Ws, s_inv, s_seq, s_pos);
 }
 
 // Split-K sums of the batched GEMM: one workgroup per (tile, 16 rows) adds the k ranges in
 // split order and runs the product's epilogue (wave w: fragment rows of the tile's wave w).
 template <int EPI>
 __global__ void __launch_bounds__(256) gemm_wide_reduce_kernel(GemmArgs a) {
-  constexpr int TPW = kWideTPW;
+  constexpr int TPW = kWideFR / 4;  // wave w sums fragment rows w*TPW ..
   const int tile = blockIdx.x, m0 = blockIdx.y * 16, S = a.splits;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, l16 = lane & 15, g4 = lane >> 4;
   const int M = min(GL(a.row_offsets)[a.batch], a.M_max);
@@ -750,7 +747,7 @@ __global__ void __launch_bounds__(256) qkv_rope_kernel(GemmArgs a, const float* 
 
 WidePlan plan_wide(int Nt, int Kt) {
   WidePlan p;
-  p.tiles = (Nt + 4 * kWideTPW - 1) / (4 * kWideTPW);
+  p.tiles = (Nt + kWideFR - 1) / kWideFR;
   // one resident workgroup per compute unit (the accumulators fill the AGPRs); at least
   // eight k-steps per workgroup
   p.splits = 256 / p.tiles;
