@@ -24,13 +24,16 @@
 namespace lsv {
 
 constexpr int kCh = kAttnChunk;  // keys per chunk
-constexpr int kAttnWgs = 256;     // split-kernel workgroups aimed for
-constexpr int kMaxChunksPerSplit = 16;  // a split walks its chunks in sequence
+// Split plan: about kAttnWgs split workgroups, and no split longer than kMaxChunksPerSplit
+// chunks (a split walks its chunks in sequence).  Fewer splits mean fewer partials to merge
+// -- one batch of merge loads for up to 16 -- against longer chunk walks; 128 measured best
+// for one sequence of 2K context (11 splits of 3 chunks).
+constexpr int kAttnWgs = 128;
+constexpr int kMaxChunksPerSplit = 16;
 
 AttnPlan plan_attention(int batch, int nkv, int max_ctx) {
   const int n_chunks = (max_ctx + kCh - 1) / kCh;
   const int units = batch * nkv;
-  // about one workgroup per compute unit, but no split longer than kMaxChunksPerSplit chunks
   int want = (kAttnWgs + units - 1) / units;
   const int by_length = (n_chunks + kMaxChunksPerSplit - 1) / kMaxChunksPerSplit;
   if (want < by_length) want = by_length;
