@@ -74,7 +74,9 @@ def test_tiny_f32_end_to_end():
             assert acc[0] == 16
 
 
-def _bf16_case(shape, seed, contexts, rows, tol=2e-2):
+def _bf16_case(shape, seed, contexts, rows, tol=2e-2, bound=None):
+    """Verify through the C-ABI against the oracle. bound: the host row bound of the call
+    (default: the workspace's, max(64, total rows))."""
     B = len(contexts)
     w = gen.model_weights(shape, seed)
     cap = runtime.kv_capacity(max(contexts) + max(rows) + 8)
@@ -89,7 +91,7 @@ def _bf16_case(shape, seed, contexts, rows, tol=2e-2):
             oc.v[l][b, :, :contexts[b]] = OF.stored_to_f64(v[0], "bf16")
     off = runtime.row_offsets_of(rows)
     toks = gen.randint(seed, 900, int(off[-1]), shape.vocab)
-    g_logits, st = gm.verify(contexts, toks, off)
+    g_logits, st = gm.verify(contexts, toks, off, max_rows=bound)
     assert np.all(st == 0)
     o_logits, _ = OF.verify_block(om, oc, contexts, toks, off)
     err = row_rel_err(g_logits, o_logits)
@@ -125,6 +127,19 @@ def test_bf16_hd128_ragged():
     _bf16_case(configs.SMALL_BF16, 12, [129, 300], [17, 9])
 
 
+def test_bf16_hd128_few_tiles_under_loose_bound():
+    """9 rows of a 4-query-head group under a 17-row bound: the attention split kernel takes
+    eight waves (chosen from the bound) but has three query tiles, so its two four-wave
+    groups take alternate chunks and combine their softmax states."""
+    _bf16_case(configs.SMALL_BF16, 15, [300], [9], bound=17)
+
+
+def test_bf16_hd128_two_passes_of_eight_waves():
+    """40 rows of a 4-query-head group: ten query tiles, two passes of the eight-wave
+    attention split kernel over the context."""
+    _bf16_case(configs.SMALL_BF16, 16, [200], [40], bound=64)
+
+
 def test_bf16_single_row_and_empty_sequence():
     _bf16_case(configs.TINY_BF16, 13, [64, 63], [1, 0])
 
@@ -136,9 +151,9 @@ def test_llama8b_width_two_layers():
 
 
 def test_workspace_reused_across_bounds():
-    """One zeroed workspace serves calls with different row and context bounds (the arrival
-    counters keep their place): prefill with the 64-row bound, then verify blocks with the
-    17-, 64- and 5-row bounds and a smaller max_ctx, each against the oracle."""
+    """One zeroed workspace serves calls with different row and context bounds: prefill with
+    the 64-row bound, then verify blocks with the 17-, 64- and 5-row bounds and a smaller
+    max_ctx, each against the oracle."""
     shape = configs.TINY_BF16
     w = gen.model_weights(shape, 14)
     cap = 256
