@@ -251,7 +251,8 @@ struct RowInputs {
 
 template <typename T, int MT, int TPW, int EPI, bool HPRE>
 LSV_DEV void gemm_epilogue(const GemmArgs& a, const int M, const int m0, const int tn0, const bool (&tvalid)[TPW],
-                           f32x4_t (&acc)[TPW][MT], const f32x4_t (&hpre)[TPW][MT], const RowInputs* rin = nullptr) {
+                           f32x4_t (&acc)[TPW][MT], const f32x4_t (&hpre)[TPW][MT], const RowInputs* rin = nullptr,
+                           const float* inv_pre = nullptr) {
   constexpr bool RMS = EPI != EPI_RESID;
   constexpr int KT = FragTraits<T>::KT;
   const int lane = threadIdx.x & 63, l16 = lane & 15, g4 = lane >> 4;
@@ -260,7 +261,7 @@ LSV_DEV void gemm_epilogue(const GemmArgs& a, const int M, const int m0, const i
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
       const int m = m0 + mt * 16 + l16;
-      inv[mt] = rin ? rin->inv[min(m, a.M_max - 1)] : inv_rms_of_row(a, m, g4);
+      inv[mt] = inv_pre ? inv_pre[mt] : (rin ? rin->inv[min(m, a.M_max - 1)] : inv_rms_of_row(a, m, g4));
     }
   }
   int qkv_b[MT], qkv_pos[MT];
@@ -353,11 +354,12 @@ LSV_DEV void gemm_epilogue(const GemmArgs& a, const int M, const int m0, const i
     }
 }
 
-template <typename T, int MT, int TPW, int KS, int U, int NS, int EPI, int MT_MAX>
+template <typename T, int MT, int TPW, int KS, int U, int NS, int EPI, int MT_MAX, int PSTAT>
 LSV_DEV void gemm_body(const GemmArgs& a, const int M, const int tile, const int m0,
                        f32x4_t (*red)[TPW][MT_MAX][kWave]) {
   constexpr int KT = FragTraits<T>::KT, EPL = FragTraits<T>::EPL;
   constexpr bool RMS = EPI != EPI_RESID;  // consumer of a normalised activation
+  constexpr bool PS = RMS && PSTAT;        // its 1/rms rides the weight stream
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, l16 = lane & 15, g4 = lane >> 4;
   // this workgroup: fragment rows tn0 .. tn0+TPW-1 over the whole K, activation rows
   // m0 .. min(M, m0 + 16 MT) - 1; wave = k-slice
@@ -400,12 +402,31 @@ LSV_DEV void gemm_body(const GemmArgs& a, const int M, const int tile, const int
   for (int t = 0; t < TPW; ++t)
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) acc[t][mt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  // PS: 1/rms of the normalised input rides the weight stream: pipeline stage j also loads
+  // float4 g4 + 4j of each row's per-16-column sums of squares (stats[m][0..P)), and the
+  // stage's compute adds it -- the order of inv_rms_of_row, so the value is the same --
+  // instead of a dependent round of loads after the stream.
+  const int P4 = a.P >> 2, nstat = (P4 + 3) / 4;  // float4s per row; per lane group
+  const GLOBAL f32x4_t* stp[MT];
+  float ss[MT];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt) {
+    stp[mt] = (const GLOBAL f32x4_t*)(a.stats + (size_t)min(m0 + mt * 16 + l16, a.M_max - 1) * a.P);
+    ss[mt] = 0.f;
+  }
+  int nstat_done = 0;  // stages whose stats have been added
   {
     // NS pipeline stages of U k-steps.  Every load hits an in-bounds fragment (index
     // clamped): a conditional load would become a select between addresses and a generic
     // access.  Steps past the range re-read the last one and are never used.
     u32x4_t wa[NS][U][TPW], xb[NS][U][MT];
+    f32x4_t sr[NS][MT];
     auto load_stage = [&](int st, int kb) {
+      if (PS) {
+        const int i = g4 + 4 * (kb / U);
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) sr[st][mt] = i < P4 ? stp[mt][i] : f32x4_t{0.f, 0.f, 0.f, 0.f};
+      }
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int kf = max(min(kb + u, nk - 1), 0);  // a slice may be empty when Kt < KS
@@ -416,6 +437,11 @@ LSV_DEV void gemm_body(const GemmArgs& a, const int M, const int tile, const int
       }
     };
     auto compute_stage = [&](int st, int kb, bool tail) {
+      if (PS && kb / U < nstat && (!tail || kb < nk)) {
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) ss[mt] += ((sr[st][mt][0] + sr[st][mt][1]) + sr[st][mt][2]) + sr[st][mt][3];
+        nstat_done = kb / U + 1;
+      }
 #pragma unroll
       for (int u = 0; u < U; ++u)
         if (!tail || kb + u < nk)
@@ -464,7 +490,22 @@ LSV_DEV void gemm_body(const GemmArgs& a, const int M, const int tile, const int
         for (int mt = 0; mt < MT; ++mt) acc[t][mt] += red[w - 1][t][mt][lane];
   }
 
-  gemm_epilogue<T, MT, TPW, EPI, true>(a, M, m0, tn0, tvalid, acc, hpre);
+  float inv[MT];
+  if (PS) {
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+      for (int j = nstat_done; j < nstat; ++j) {  // stages the k range did not reach
+        const int i = g4 + 4 * j;
+        const f32x4_t v = i < P4 ? stp[mt][i] : f32x4_t{0.f, 0.f, 0.f, 0.f};
+        ss[mt] += ((v[0] + v[1]) + v[2]) + v[3];
+      }
+      float t = ss[mt];
+      t += __shfl_xor(t, 16, kWave);
+      t += __shfl_xor(t, 32, kWave);
+      inv[mt] = 1.0f / sqrtf(t / (float)a.K + a.eps);
+    }
+  }
+  gemm_epilogue<T, MT, TPW, EPI, true>(a, M, m0, tn0, tvalid, acc, hpre, nullptr, PS ? inv : nullptr);
 }
 
 // Launch configuration of each product: fragment rows per wave (TPW), k-slices = waves
@@ -473,16 +514,18 @@ LSV_DEV void gemm_body(const GemmArgs& a, const int M, const int tile, const int
 // flight, beat many short ones (more concurrent streams read more scattered DRAM rows), so
 // every product runs one wave per workgroup over the whole K.
 template <int KIND> struct GemmCfg;
-template <> struct GemmCfg<GEMM_QKV> { static constexpr int TPW = 2, KS = 1, U = 4, NS = 3, EPI = EPI_QKV; };
-template <> struct GemmCfg<GEMM_O> { static constexpr int TPW = 1, KS = 1, U = 8, NS = 3, EPI = EPI_RESID; };
-template <> struct GemmCfg<GEMM_GATEUP> { static constexpr int TPW = 4, KS = 1, U = 4, NS = 3, EPI = EPI_SWIGLU; };
-template <> struct GemmCfg<GEMM_DOWN> { static constexpr int TPW = 1, KS = 1, U = 8, NS = 3, EPI = EPI_RESID; };
-template <> struct GemmCfg<GEMM_LMHEAD> { static constexpr int TPW = 4, KS = 1, U = 4, NS = 3, EPI = EPI_LOGITS; };
+// PSTAT: the 1/rms of a normalised input rides the weight stream (measured faster for the
+// wide gate/up and LM head; slower for QKV, which reads it in its epilogue).
+template <> struct GemmCfg<GEMM_QKV> { static constexpr int TPW = 2, KS = 1, U = 4, NS = 3, EPI = EPI_QKV, PSTAT = 0; };
+template <> struct GemmCfg<GEMM_O> { static constexpr int TPW = 1, KS = 1, U = 8, NS = 3, EPI = EPI_RESID, PSTAT = 0; };
+template <> struct GemmCfg<GEMM_GATEUP> { static constexpr int TPW = 4, KS = 1, U = 4, NS = 3, EPI = EPI_SWIGLU, PSTAT = 1; };
+template <> struct GemmCfg<GEMM_DOWN> { static constexpr int TPW = 1, KS = 1, U = 8, NS = 3, EPI = EPI_RESID, PSTAT = 0; };
+template <> struct GemmCfg<GEMM_LMHEAD> { static constexpr int TPW = 4, KS = 1, U = 4, NS = 3, EPI = EPI_LOGITS, PSTAT = 1; };
 
 // Wide activation tiles (prefill bounds) use a shallower pipeline to stay in registers.
 template <int KIND, int MT_MAX> struct GemmShape {
   using C = GemmCfg<KIND>;
-  static constexpr int TPW = C::TPW, KS = C::KS, EPI = C::EPI;
+  static constexpr int TPW = C::TPW, KS = C::KS, EPI = C::EPI, PSTAT = C::PSTAT;
   static constexpr int U = MT_MAX <= 2 ? C::U : 4, NS = MT_MAX <= 2 ? C::NS : 2;
 };
 
@@ -505,13 +548,13 @@ __global__ void __launch_bounds__(64 * GemmCfg<KIND>::KS) gemm_kernel(GemmArgs a
   const int M_end = m0 + Mc;
   const int mt = Mc <= 16 ? 1 : (Mc <= 32 ? 2 : (Mc <= 48 ? 3 : 4));
   if (mt <= 1 || MT_MAX == 1)
-    gemm_body<T, 1, S::TPW, S::KS, S::U, S::NS, S::EPI, MT_MAX>(a, M_end, tile, m0, red);
+    gemm_body<T, 1, S::TPW, S::KS, S::U, S::NS, S::EPI, MT_MAX, S::PSTAT>(a, M_end, tile, m0, red);
   else if (mt == 2 || MT_MAX == 2)
-    gemm_body<T, (MT_MAX >= 2 ? 2 : 1), S::TPW, S::KS, S::U, S::NS, S::EPI, MT_MAX>(a, M_end, tile, m0, red);
+    gemm_body<T, (MT_MAX >= 2 ? 2 : 1), S::TPW, S::KS, S::U, S::NS, S::EPI, MT_MAX, S::PSTAT>(a, M_end, tile, m0, red);
   else if (mt == 3 || MT_MAX == 3)
-    gemm_body<T, (MT_MAX >= 3 ? 3 : 1), S::TPW, S::KS, S::U, S::NS, S::EPI, MT_MAX>(a, M_end, tile, m0, red);
+    gemm_body<T, (MT_MAX >= 3 ? 3 : 1), S::TPW, S::KS, S::U, S::NS, S::EPI, MT_MAX, S::PSTAT>(a, M_end, tile, m0, red);
   else
-    gemm_body<T, MT_MAX, S::TPW, S::KS, S::U, S::NS, S::EPI, MT_MAX>(a, M_end, tile, m0, red);
+    gemm_body<T, MT_MAX, S::TPW, S::KS, S::U, S::NS, S::EPI, MT_MAX, S::PSTAT>(a, M_end, tile, m0, red);
 }
 
 // ------------------------------------------------------------------ planning and launch
