@@ -153,7 +153,8 @@ int lsv_workspace_clear(void* d_workspace, size_t workspace_bytes, void* stream)
  *
  *   cfg, d_packed      model and its packed weights
  *   d_kv, capacity     KV cache (layout above) with `capacity` positions per slab,
- *                      capacity % LSV_KV_ALIGN == 0
+ *                      capacity % LSV_KV_ALIGN == 0 and a slab under 2 GiB
+ *                      (capacity * head_dim * element size < 2^31)
  *   batch              number of sequences (1..LSV_MAX_BATCH)
  *   d_seq_len          [batch] int32, cached positions before this block
  *   d_tokens           [rows] int32 token ids

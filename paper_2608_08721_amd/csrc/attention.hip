@@ -27,7 +27,9 @@ constexpr int kCh = kAttnChunk;  // keys per chunk
 // Split plan: about kAttnWgs split workgroups, and no split longer than kMaxChunksPerSplit
 // chunks (a split walks its chunks in sequence).  Fewer splits mean fewer partials to merge
 // -- one batch of merge loads for up to 16 -- against longer chunk walks; 128 measured best
-// for one sequence of 2K context (11 splits of 3 chunks).
+// for one sequence of 2K context (11 splits of 3 chunks).  The length cap keeps the
+// workgroups of a batch with long contexts from running too long; 8 measured slower than 16
+// for eight sequences with 1K-8K contexts (more partials to write and merge).
 constexpr int kAttnWgs = 128;
 constexpr int kMaxChunksPerSplit = 16;
 
@@ -66,15 +68,24 @@ __global__ void __launch_bounds__(64 * NW) attn_split_bf16_kernel(AttnArgs a) {
   const int c0 = s * a.chunks_per_split, cap_chunks = a.capacity / kCh;
 
   // a step covers chunks c .. c+NG-1, group g loading chunk c+g into buffer g; the next
-  // step's chunks are in flight in registers while the current ones are used
+  // step's chunks are in flight in registers while the current ones are used. The loads go
+  // through buffer descriptors over this (sequence, kv head)'s slab: one 32-bit lane offset
+  // per operand, the chunk and piece offsets in scalar registers, and reads past the slab
+  // return zero.
+  const int slab_bytes = a.capacity * HD * (int)sizeof(bf16_t);
+  const __amdgpu_buffer_rsrc_t krs = __builtin_amdgcn_make_buffer_rsrc((void*)kb, 0, slab_bytes, 0x00020000);
+  const __amdgpu_buffer_rsrc_t vrs = __builtin_amdgcn_make_buffer_rsrc((void*)vb, 0, slab_bytes, 0x00020000);
+  const int koff = ((gtid / P8) * HD + (gtid % P8) * 8) * (int)sizeof(bf16_t);
+  const int voff = ((gtid >> 3) * a.capacity + (gtid & 7) * 8) * (int)sizeof(bf16_t);
   u32x4_t kr[NP], vr[NP];
   auto load_chunk = [&](int c) {
     const int k0 = c * kCh;
 #pragma unroll
-    for (int j = 0; j < NP; ++j) {
-      const int i = gtid + 256 * j;
-      kr[j] = *(const GLOBAL u32x4_t*)(kb + (size_t)(k0 + i / P8) * HD + (i % P8) * 8);
-      vr[j] = *(const GLOBAL u32x4_t*)(vb + (size_t)(i >> 3) * a.capacity + k0 + (i & 7) * 8);
+    for (int j = 0; j < NP; ++j) {  // piece gtid + 256 j: K row + j 256 / P8, V^T row + 32 j
+      kr[j] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(
+                                              krs, koff, (k0 + j * (256 / P8)) * HD * (int)sizeof(bf16_t), 0));
+      vr[j] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(
+                                              vrs, voff, (j * 32 * a.capacity + k0) * (int)sizeof(bf16_t), 0));
     }
   };
   auto store_chunk = [&]() {
@@ -101,13 +112,12 @@ __global__ void __launch_bounds__(64 * NW) attn_split_bf16_kernel(AttnArgs a) {
     }
     return;
   }
-  // With two groups and at most four query tiles, group g runs the tiles over chunks
-  // c0+g, c0+g+2, ... and the two running softmax states are combined at the end;
-  // otherwise every wave runs its own tile over all chunks in order.
-  const bool halves = NG == 2 && n_qt <= 4;
-  const int tiles_per_pass = halves ? 4 : NW;
-
-  for (int qbase = 0; qbase < n_qt; qbase += tiles_per_pass) {
+  // A pass over the split covers up to NW query tiles, one per wave, each wave running its
+  // tile over all chunks in order. With two groups, a pass left with at most four tiles
+  // (all of them, or the rest after full passes) has group g run them over chunks c0+g,
+  // c0+g+2, ..., and the two running softmax states are combined at the end.
+  for (int qbase = 0; qbase < n_qt;) {
+    const bool halves = NG == 2 && n_qt - qbase <= 4;
     const int qt = qbase + (halves ? (wave & 3) : wave);
     const bool active = qt < n_qt;  // wave-uniform
     u32x4_t qf[HD / 32];
@@ -271,6 +281,7 @@ __global__ void __launch_bounds__(64 * NW) attn_split_bf16_kernel(AttnArgs a) {
       if (g4 == 0) *(GLOBAL f32x2_t*)(a.ml_part + base * 2) = f32x2_t{mrun, lrun};
     }
     __syncthreads();  // the next pass refills the chunk buffers
+    qbase += halves ? 4 : NW;
   }
 }
 

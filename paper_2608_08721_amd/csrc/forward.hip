@@ -73,7 +73,7 @@ struct VerifyWs {
   float* o_part;   // attention split partials
   float* ml_part;
   float* part;     // wide blocks: k-split partials
-  float* qkv_y;    // wide blocks: [M_max][N_qkv] normalised QKV projection before RoPE
+  float* qkv_y;    // wide blocks with an unsplit QKV: [M_max][N_qkv] projection before RoPE
   size_t total;
 };
 
@@ -129,7 +129,8 @@ static VerifyWs carve_verify(const Shape& s, const ModelLayout& ml, const Verify
     w.o_part = w.ml_part = nullptr;
   }
   w.part = (float*)take(sizeof(float) * v.part_floats);
-  w.qkv_y = v.wide ? (float*)take(sizeof(float) * (size_t)max_rows * ml.qkv.N) : nullptr;
+  // the unsplit wide QKV projection goes through an fp32 copy before the rotary embedding
+  w.qkv_y = v.wide && v.w[GEMM_QKV].splits == 1 ? (float*)take(sizeof(float) * (size_t)max_rows * ml.qkv.N) : nullptr;
   w.total = off;
   return w;
 }

@@ -597,9 +597,9 @@ static int launch_typed(GemmKind kind, int MT, const GemmArgs& a, hipStream_t st
 // wave w keeps activation tiles w*MTW .. w*MTW+MTW-1 (MTW <= 5) in registers.  With more
 // than one k range per tile, each workgroup writes fp32 partials and
 // gemm_wide_reduce_kernel adds them in split order (deterministic) and runs the epilogue,
-// one workgroup per (tile, 16 rows).  The QKV projection runs the plain scaled epilogue
-// into an fp32 buffer, and qkv_rope_kernel applies the rotary embedding and the Q store /
-// cache append.
+// one workgroup per (tile, 16 rows); the QKV reduce applies the rotary embedding and the Q
+// store / cache append.  An unsplit QKV runs the plain scaled epilogue into an fp32 buffer
+// and qkv_rope_kernel does the rest.
 constexpr int kWideFR = 8;     // fragment rows of a workgroup
 constexpr int kWideRingW = 10;  // k-steps of weight pieces in flight (register ring)
 constexpr int kWideRingX = 2;   // k-steps of activation fragments in flight (from L2)
@@ -761,12 +761,26 @@ __global__ void __launch_bounds__(256) gemm_wide_reduce_kernel(GemmArgs a) {
 #pragma unroll
   for (int t = 0; t < TPW; ++t) {
     tvalid[t] = tn0 + t < a.Nt;
-    const int col = (wave * TPW + t) * 16 + 4 * g4;
-    f32x4_t sum = f32x4_t{0.f, 0.f, 0.f, 0.f};
-    if (m < M)
-      for (int j = 0; j < S; ++j)
-        sum += *(const GLOBAL f32x4_t*)(a.part + (((size_t)tile * S + j) * a.M_max + m) * kWideCols + col);
-    acc[t][0] = sum;
+    acc[t][0] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  }
+  if (m < M) {
+    // the partials of up to RB splits are in flight at once; they are added in split order
+    constexpr int RB = 8;
+    const GLOBAL f32x4_t* p = (const GLOBAL f32x4_t*)(a.part + ((size_t)tile * S * a.M_max + m) * kWideCols) +
+                              wave * TPW * 4 + g4;
+    const size_t split_step = (size_t)a.M_max * kWideCols / 4;
+    for (int j0 = 0; j0 < S; j0 += RB) {
+      f32x4_t v[RB][TPW];
+#pragma unroll
+      for (int i = 0; i < RB; ++i)
+#pragma unroll
+        for (int t = 0; t < TPW; ++t) v[i][t] = p[(size_t)min(j0 + i, S - 1) * split_step + 4 * t];
+#pragma unroll
+      for (int i = 0; i < RB; ++i)
+        if (j0 + i < S)
+#pragma unroll
+          for (int t = 0; t < TPW; ++t) acc[t][0] += v[i][t];
+    }
   }
   gemm_epilogue<bf16_t, 1, TPW, EPI, false>(a, M, m0, tn0, tvalid, acc, none);
 }
@@ -817,7 +831,15 @@ int launch_gemm_wide(GemmKind kind, const GemmArgs& a0, const WidePlan& p, hipSt
   a.splits = p.splits;
   switch (kind) {
     case GEMM_QKV: {
-      // scaled projection into the caller's fp32 buffer (out_f32, N columns), then RoPE
+      if (p.splits > 1) {
+        // the split-K reduce runs the rotary embedding and the Q store / cache append
+        hipLaunchKernelGGL(gemm_wide_kernel<EPI_LOGITS>, dim3((unsigned)(p.tiles * p.splits)), dim3(256), 0, st, a);
+        hipLaunchKernelGGL(gemm_wide_reduce_kernel<EPI_QKV>, dim3((unsigned)p.tiles, (unsigned)((a.M_max + 15) / 16)),
+                           dim3(256), 0, st, a);
+        break;
+      }
+      // one split: the scaled projection into the caller's fp32 buffer (out_f32, N columns),
+      // then RoPE (the fused epilogue would not fit the wide kernel's registers)
       if (!a.out_f32) return LSV_ERR_INVALID_ARG;
       a.ldo = a.N;
       launch_wide_epi<EPI_LOGITS>(a, p, a.M_max, st);

@@ -151,6 +151,9 @@ int lsv_verify_block(const lsv_model_config* cfg, const void* d_packed, void* d_
   if (capacity % LSV_KV_ALIGN)
     return fail(LSV_ERR_INVALID_ARG, "capacity %d is not a multiple of %d", capacity, (int)LSV_KV_ALIGN);
   const lsv::Shape s = lsv::shape_of(cfg);
+  if ((size_t)capacity * s.hd * s.es >= ((size_t)1 << 31))  // slab offsets are 32-bit in the kernels
+    return fail(LSV_ERR_INVALID_ARG, "capacity %d: a KV slab of %d x %d elements reaches 2 GiB", capacity, capacity,
+                s.hd);
   if (s.dtype == LSV_DTYPE_F32 && max_ctx > 16384)
     return fail(LSV_ERR_UNSUPPORTED, "fp32 models support max_ctx <= 16384");
   const size_t need = lsv::verify_workspace_bytes(s, batch, max_rows, max_ctx);

@@ -140,6 +140,13 @@ def test_bf16_hd128_two_passes_of_eight_waves():
     _bf16_case(configs.SMALL_BF16, 16, [200], [40], bound=64)
 
 
+def test_bf16_hd64_wide_block_unsplit_qkv():
+    """140 rows at head dim 64 (d 256): the batched GEMMs, whose QKV product is too narrow to
+    split K (projection, then the separate rotary-embedding kernel), and 18 query tiles of a
+    2-query-head group, three passes of the eight-wave attention split kernel."""
+    _bf16_case(configs.TINY_BF16, 18, [100], [140], bound=140)
+
+
 def test_bf16_single_row_and_empty_sequence():
     _bf16_case(configs.TINY_BF16, 13, [64, 63], [1, 0])
 
