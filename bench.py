@@ -50,6 +50,10 @@ def parse():
                         "gate/up profile summary")
     p.add_argument("--sweep-reps-counters", type=int, default=1,
                    help="--sweep-reps of the two counter runs (with --summarize)")
+    p.add_argument("--summarize-mfma", nargs=2, metavar=("TRACE_DIR", "PMC_DIR"),
+                   help="no GPU work: matrix-core summary of the batched workload's uniform-gamma-max sweep "
+                        "step from a kernel-trace run and a --pmc SQ_INSTS_MFMA SQ_VALU_MFMA_BUSY_CYCLES run "
+                        "of the same bench command")
     return p.parse_args()
 
 
@@ -236,6 +240,138 @@ def summarize(trace_dir, fetch_dir, write_dir, reps_c):
     return "\n".join(out) + "\n"
 
 
+MFMA_FLOPS_PER_INST = 16 * 16 * 32 * 2  # v_mfma_f32_16x16x32_bf16, the only MFMA of these kernels
+
+
+def summarize_mfma(trace_dir, pmc_dir):
+    """Matrix-core summary (markdown) of the batched workload at its largest uniform gamma:
+    per kernel kind, duration from a kernel-trace run and SQ_INSTS_MFMA / SQ_VALU_MFMA_BUSY_CYCLES
+    from a counter run of the same command.  Both runs issue the same calls in the same order;
+    a call starts at its embedding kernel, and the calls at the largest gamma are the ones whose
+    gate/up launches issue the most MFMAs (the row count picks the kernel body on the device)."""
+    import csv
+    import glob
+    from synth import configs, gen
+
+    def one(d, pat):
+        f = glob.glob(os.path.join(d, "**", pat), recursive=True)
+        assert len(f) == 1, (d, pat, f)
+        return f[0]
+
+    bt = json.loads(open(os.path.join(trace_dir, "bench.json")).read().strip().splitlines()[-1])
+    wl = configs.WORKLOADS[bt["config"]["workload"]]
+    m, G, B = wl.model, wl.G, wl.batch
+    ctx = [int(c) for c in gen.contexts(wl)]
+    rows = B * (G + 1)
+
+    def calls_of(rows_in):
+        calls, cur = [], None
+        for r in rows_in:
+            if r["Kernel_Name"].startswith("void lsv::embed_kernel") or "embed_kernel" in r["Kernel_Name"]:
+                cur = []
+                calls.append(cur)
+            if cur is not None:
+                cur.append(r)
+        return calls
+
+    trace = sorted(csv.DictReader(open(one(trace_dir, "*kernel_trace.csv"))), key=lambda r: int(r["Dispatch_Id"]))
+    tcalls = calls_of(trace)
+    pm = {}
+    for r in csv.DictReader(open(one(pmc_dir, "*counter_collection.csv"))):
+        d = pm.setdefault(int(r["Dispatch_Id"]), {"name": r["Kernel_Name"], "grid": int(r["Grid_Size"])})
+        d[r["Counter_Name"]] = d.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+    prow = [dict(Dispatch_Id=k, Kernel_Name=v["name"], **v) for k, v in sorted(pm.items())]
+    pcalls = calls_of(prow)
+    assert len(pcalls) == len(tcalls), (len(pcalls), len(tcalls))
+
+    def gateup_mfma(call):
+        v = [r["SQ_INSTS_MFMA"] for r in call if "gemm_wide_kernel<3>" in r["Kernel_Name"]]
+        return max(v) if v else 0
+    top = max(gateup_mfma(c) for c in pcalls)
+    hits = [i for i, c in enumerate(pcalls) if top > 0 and gateup_mfma(c) == top]
+    assert hits, "no batched gate/up launches in the counter run"
+    # prefill chunks of full blocks issue as many; the sweep's last gamma is the last run of
+    # consecutive calls that do
+    picked = [hits[-1]]
+    while picked[0] - 1 in hits:
+        picked.insert(0, picked[0] - 1)
+
+    d, F, V = m.d_model, m.d_ff, m.vocab
+    n_qkv = (m.n_q_heads + 2 * m.n_kv_heads) * m.head_dim
+    att_flops = sum(sum(4 * m.n_q_heads * m.head_dim * (C + v + 1) for v in range(G + 1)) for C in ctx)
+    useful = {"QKV": 2.0 * rows * n_qkv * d, "O": 2.0 * rows * d * m.n_q_heads * m.head_dim,
+              "gate/up": 2.0 * rows * 2 * F * d, "down": 2.0 * rows * d * F, "LM head": 2.0 * rows * V * d,
+              "attention split": float(att_flops)}
+
+    def kind(name, seen):
+        if "gemm_wide_kernel<3>" in name:
+            return "gate/up"
+        if "gemm_wide_kernel<2>" in name:
+            seen["resid"] += 1
+            return "O" if seen["resid"] % 2 == 1 else "down"
+        if "gemm_wide_kernel<0>" in name:
+            seen["logits"] += 1
+            return "QKV" if seen["logits"] <= m.n_layers else "LM head"
+        if "attn_split" in name:
+            return "attention split"
+        return None
+
+    stats = {}
+    for i in picked:
+        seen = {"resid": 0, "logits": 0}
+        for tr, pr in zip(tcalls[i], pcalls[i]):
+            assert _short(tr["Kernel_Name"]) == _short(pr["Kernel_Name"]), (tr["Kernel_Name"], pr["Kernel_Name"])
+            k = kind(tr["Kernel_Name"], seen)
+            if k is None:
+                continue
+            s = stats.setdefault(k, {"dur": [], "mfma": [], "busy": []})
+            s["dur"].append((int(tr["End_Timestamp"]) - int(tr["Start_Timestamp"])) / 1e3)
+            s["mfma"].append(pr.get("SQ_INSTS_MFMA", 0.0))
+            s["busy"].append(pr.get("SQ_VALU_MFMA_BUSY_CYCLES", 0.0))
+
+    out = []
+    w = out.append
+    cmd = ("python3 bench.py --workload {w} --steps 2 --warmup 1 --sweep-reps 1 --roofline-steps 1 "
+           "--no-cpu-baseline").format(w=wl.name)
+    w(f"# Batched GEMMs and attention on the matrix cores: {wl.name}, uniform gamma {G} ({rows} rows)")
+    w("")
+    w("Commands (repository root, after `cd /tmp && export TMPDIR=/tmp`; each run's stdout saved as bench.json in")
+    w("its output directory):")
+    w("")
+    w("```")
+    w(f"rocprofv3 --kernel-trace --output-format csv -d gpurun_out/mf/trace -o t -- {cmd}")
+    w(f"rocprofv3 --pmc SQ_INSTS_MFMA SQ_VALU_MFMA_BUSY_CYCLES --output-format csv -d gpurun_out/mf/pmc -o c -- {cmd}")
+    w("python3 bench.py --summarize-mfma gpurun_out/mf/trace gpurun_out/mf/pmc")
+    w("```")
+    w("")
+    w(f"Calls at gamma {G}: {len(picked)} (the sweep's graph body, run 1 + 3 + 1 times). Durations are kernel-trace")
+    w("times of the plain run. Issued rate: SQ_INSTS_MFMA x 16384 flops (v_mfma_f32_16x16x32_bf16) per second;")
+    w("useful rate: the product's own 2·M·N·K (attention: QKᵀ and PV over each row's causal context) per second;")
+    w("both as a share of the 2.5 PFLOP/s dense bf16 peak. The busy column is SQ_VALU_MFMA_BUSY_CYCLES over")
+    w("duration x 2.4 GHz x 1024 SIMDs.")
+    w("")
+    w("| kernel | launches per call | avg us | MFMA instructions per launch | issued % of peak | useful % of peak | MFMA busy |")
+    w("|---|---:|---:|---:|---:|---:|---:|")
+    order = ["gate/up", "attention split", "down", "O", "QKV", "LM head"]
+    for k in order:
+        if k not in stats:
+            continue
+        s = stats[k]
+        dur = statistics.mean(s["dur"])
+        inst = statistics.mean(s["mfma"])
+        busy = statistics.mean(s["busy"])
+        issued = inst * MFMA_FLOPS_PER_INST / (dur * 1e-6) / MFMA_PEAK_FLOPS
+        use = useful[k] / (dur * 1e-6) / MFMA_PEAK_FLOPS  # per launch (attention: one layer)
+        w(f"| {k} | {len(s['dur']) / len(picked):g} | {dur:.2f} | {inst:.0f} | {issued * 100:.1f}% | {use * 100:.1f}% | "
+          f"{busy / (dur * 1e-6 * 2.4e9 * 1024) * 100:.1f}% |")
+    w("")
+    sw = bt.get("uniform_gamma_max", {})
+    if sw:
+        w(f"Whole step at gamma {G} (HIP events, graph replays, no profiler): {sw['latency_us']:.0f} us, "
+          f"{sw['mfma_frac'] * 100:.1f}% of the MFMA peak, {sw['hbm_frac'] * 100:.1f}% of 8 TB/s.")
+    return "\n".join(out) + "\n"
+
+
 def step_bytes(m, contexts, rows):
     es = 2 if m.dtype == "bf16" else 4
     kv_row = 2 * m.n_kv_heads * m.head_dim * es
@@ -288,6 +424,9 @@ def main():
     args = parse()
     if args.summarize:
         sys.stdout.write(summarize(*args.summarize, args.sweep_reps_counters))
+        return
+    if args.summarize_mfma:
+        sys.stdout.write(summarize_mfma(*args.summarize_mfma))
         return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only: this build has no multi-GPU path (asked for --gpus {args.gpus}).",
