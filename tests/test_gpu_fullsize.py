@@ -1,0 +1,140 @@
+"""Verify at full size, in the launch configuration bench.py times: the Llama-3-8B shape with all
+32 layers, (a) batch 1 at context 2048 with a 17-row block under a 17-row bound, (b) batch 8 with
+contexts drawn from [1024, 8192] and 33 rows per sequence under a 264-row bound (the batched
+GEMM path).  The oracle cannot run 32 layers of this width in seconds, so the test checks what it
+can compute, and properties that hold at any size:
+
+* parity on sampled outputs: the K and V that the GPU appends at layers 0 and 1 (they depend on
+  the embedding, layer 0 and layer 1's projections) against the oracle run on those two layers;
+* causality: changing a sequence's last block token leaves every other row's logits bit-identical,
+  across sequences as well (each row's GEMM outputs, norms and attention see only its own row
+  and the keys at or before its position; masked keys add exact zeros);
+* determinism: the same call twice gives bit-identical logits (split-K sums run in split order,
+  with no atomics);
+* every logit is finite and every status is LSV_OK.
+
+The cache is filled with the seeded synthetic K/V (as in the other parity tests) rather than by a
+2K-8K token prefill, which the oracle could not replay."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import forward as OF
+from paper_2608_08721_amd import lsv, runtime
+from synth import configs, gen
+from tests.lsv_testing import i32, note
+
+pytestmark = pytest.mark.gpu
+
+SEED = configs.WORKLOADS["llama3-8b-b1-c2048"].seed
+
+
+class LazyLayers:
+    """Per-layer weights from the seeded generator, one layer held at a time."""
+
+    def __init__(self, m, seed):
+        self.m, self.seed, self.cur = m, seed, (None, None)
+
+    def __getitem__(self, layer):
+        if not 0 <= layer < self.m.n_layers:
+            raise IndexError(layer)
+        if self.cur[0] != layer:
+            self.cur = (layer, gen.layer_weights(self.m, self.seed, layer))
+        return self.cur[1]
+
+    def __len__(self):
+        return self.m.n_layers
+
+    def __iter__(self):
+        return (self[l] for l in range(self.m.n_layers))
+
+
+@pytest.fixture(scope="module")
+def model():
+    m = configs.LLAMA3_8B
+    cfg = runtime.model_config(m)
+    dm = runtime.DeviceModel(cfg)
+    dm.pack_globals(gen.embed_weights(m, SEED), gen.final_norm_weights(m), gen.lm_head_weights(m, SEED))
+    for l in range(m.n_layers):
+        dm.pack_layer(l, gen.layer_weights(m, SEED, l))
+    note(f"packed {m.name}: {m.n_layers} layers")
+    return m, cfg, dm
+
+
+def _run(m, cfg, dm, kv, ws, cap, bound, ctx, toks, off):
+    logits = torch.full((bound, m.vocab), float("nan"), dtype=torch.float32, device="cuda")
+    status = torch.full((len(ctx),), 99, dtype=torch.int32, device="cuda")
+    lsv.lsv_verify_block(cfg, dm.buf, kv.buf, cap, len(ctx), i32(ctx), i32(toks), i32(off), bound, cap, logits,
+                         status, ws.buf, ws.nbytes)
+    torch.cuda.synchronize()
+    M = int(off[-1])
+    return logits[:M].cpu().numpy(), status.cpu().numpy()
+
+
+def _check(model, ctx, rows, tol=2e-2):
+    m, cfg, dm = model
+    B = len(ctx)
+    off = runtime.row_offsets_of(rows)
+    bound = int(off[-1])
+    cap = runtime.kv_capacity(max(ctx) + max(rows) + 8)
+    kv = runtime.KVCache(cfg, B, cap)
+    ws = runtime.Workspace(lsv.lsv_verify_workspace_bytes(cfg, B, bound, cap))
+    for l in range(m.n_layers):
+        for b in range(B):
+            k, v = gen.synthetic_kv(m, SEED + 31 * b, l, 1, ctx[b])
+            kv.write(l, b, 0, runtime.to_device(k[0]), runtime.to_device(v[0]))
+    toks = gen.randint(SEED, 900, bound, m.vocab)
+    note(f"  contexts {ctx}, rows {rows}, row bound {bound}")
+
+    # determinism and finiteness
+    lg1, st = _run(m, cfg, dm, kv, ws, cap, bound, ctx, toks, off)
+    assert np.all(st == 0) and np.isfinite(lg1).all()
+    lg2, _ = _run(m, cfg, dm, kv, ws, cap, bound, ctx, toks, off)
+    assert np.array_equal(lg1, lg2)
+
+    # causality, per sequence: its last row changes, no other row does
+    for b in range(B):
+        t2 = toks.copy()
+        last = off[b + 1] - 1
+        t2[last] = (t2[last] + 1) % m.vocab
+        lg3, st3 = _run(m, cfg, dm, kv, ws, cap, bound, ctx, t2, off)
+        assert np.all(st3 == 0)
+        others = np.ones(bound, bool)
+        others[last] = False
+        assert np.array_equal(lg3[others], lg1[others]), b
+        assert not np.array_equal(lg3[last], lg1[last]), b
+    note(f"  bit-identical repeat; changing each sequence's last token moves only that row")
+
+    # the original block again, then the appended K/V of layers 0 and 1 against the oracle
+    _run(m, cfg, dm, kv, ws, cap, bound, ctx, toks, off)
+    two = m.with_layers(2)
+    # the oracle's logits are not compared here: a one-row head keeps its cost out of the check
+    w = {"embed": gen.embed_weights(m, SEED), "final_norm": gen.final_norm_weights(m),
+         "lm_head": np.zeros((1, m.d_model), np.uint16), "layers": LazyLayers(m, SEED)}
+    om = OF.Model(two, w)
+    oc = OF.KVCache(two, B, cap)
+    for l in range(2):
+        for b in range(B):
+            k, v = gen.synthetic_kv(m, SEED + 31 * b, l, 1, ctx[b])
+            oc.k[l][b, :, :ctx[b]] = OF.stored_to_f64(k[0], "bf16")
+            oc.v[l][b, :, :ctx[b]] = OF.stored_to_f64(v[0], "bf16")
+    OF.verify_block(om, oc, ctx, toks, off)
+    worst = 0.0
+    for l in range(2):
+        for b in range(B):
+            gk, gv = (t.float().cpu().numpy() for t in kv.read(l, b, ctx[b], rows[b]))
+            for got, want in ((gk, oc.k[l][b, :, ctx[b]:ctx[b] + rows[b]]), (gv, oc.v[l][b, :, ctx[b]:ctx[b] + rows[b]])):
+                err = np.abs(got - want).max() / max(np.abs(want).max(), 1e-6)
+                worst = max(worst, err)
+                assert err <= tol, (l, b, err)
+    note(f"  appended K/V of layers 0-1 vs the oracle: max rel err {worst:.2e}")
+
+
+def test_llama8b_batch1_context2048_17_rows(model):
+    wl = configs.WORKLOADS["llama3-8b-b1-c2048"]
+    _check(model, [int(c) for c in gen.contexts(wl)], [wl.G + 1])
+
+
+def test_llama8b_batch8_ragged_264_rows(model):
+    wl = configs.WORKLOADS["llama3-8b-b8-ragged"]
+    _check(model, [int(c) for c in gen.contexts(wl)], [wl.G + 1] * wl.batch)
