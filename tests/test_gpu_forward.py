@@ -134,6 +134,19 @@ def test_bf16_hd128_few_tiles_under_loose_bound():
     _bf16_case(configs.SMALL_BF16, 15, [300], [9], bound=17)
 
 
+def test_bf16_hd128_halves_with_one_or_two_tiles():
+    """Under a 17-rows-per-sequence bound the split kernel runs eight waves; sequences of 1
+    and 2 query tiles have the two four-wave groups take alternate chunks (a 30-token context
+    is a single chunk, so one group sees no chunk at all and hands over an empty state)."""
+    _bf16_case(configs.SMALL_BF16, 19, [300, 30, 129], [3, 7, 1], bound=51)
+
+
+def test_bf16_hd128_four_waves_few_tiles():
+    """Under an 8-rows-per-sequence bound the split kernel runs four waves, one query tile
+    each; 1 and 2 tiles leave waves idle, over a multi-chunk and a single-chunk context."""
+    _bf16_case(configs.SMALL_BF16, 20, [200, 30], [5, 2], bound=16)
+
+
 def test_bf16_hd128_two_passes_of_eight_waves():
     """40 rows of a 4-query-head group: ten query tiles, two passes of the eight-wave
     attention split kernel over the context."""
