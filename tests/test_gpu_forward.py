@@ -153,6 +153,13 @@ def test_bf16_hd128_two_passes_of_eight_waves():
     _bf16_case(configs.SMALL_BF16, 16, [200], [40], bound=64)
 
 
+def test_bf16_hd128_three_passes_beside_a_one_tile_sequence():
+    """Rows 70 + 2 under a 72-row bound: the first sequence's 18 query tiles take three passes
+    of the eight-wave split kernel (8, 8, then 2 in alternate chunks), the second sequence's
+    single tile one."""
+    _bf16_case(configs.SMALL_BF16, 21, [260, 40], [70, 2], bound=72)
+
+
 def test_bf16_hd64_wide_block_unsplit_qkv():
     """140 rows at head dim 64 (d 256): the batched GEMMs, whose QKV product is too narrow to
     split K (projection, then the separate rotary-embedding kernel), and 18 query tiles of a
