@@ -41,6 +41,9 @@ def parse():
     p.add_argument("--workload", default="llama3-8b-b1-c2048")
     p.add_argument("--sweep-reps", type=int, default=20)
     p.add_argument("--roofline-steps", type=int, default=5)
+    p.add_argument("--accept", choices=("greedy", "sample"), default=None,
+                   help="acceptance rule of the timed steps (default: greedy where the workload has it, else "
+                        "speculative rejection sampling at the workload's temperature)")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--calib-copy", action="store_true",
                    help="also run one plain 256 MiB copy kernel (counter calibration for --pmc runs)")
@@ -439,8 +442,10 @@ def main():
 
     wl = configs.WORKLOADS[args.workload]
     m = wl.model
-    if "greedy" not in wl.accept:
-        raise SystemExit("bench.py times the greedy-acceptance workloads")
+    mode_name = args.accept or ("greedy" if "greedy" in wl.accept else "sample")
+    if mode_name not in wl.accept:
+        raise SystemExit(f"workload {wl.name} has no {mode_name} acceptance")
+    sampling = mode_name == "sample"
     torch.cuda.set_device(0)
     dev = "cuda"
     i32 = lambda x: torch.tensor(np.asarray(x, dtype=np.int32), device=dev)
@@ -499,6 +504,17 @@ def main():
     log(f"model + prefill of {ctx} tokens ready ({time.time() - t0:.1f} s); roots {roots}")
 
     drafts = gen.draft_ids(seed, B, G, m.vocab)
+    if sampling:
+        # draft distributions q_v (a seeded softmax of N(0,1) logits per drafted position) and
+        # drafts drawn from them; accept rows index q at (row offset - b + v - 1) < B * G
+        q_np = gen.draft_probs(seed, B * G, m.vocab)
+        qrng = np.random.default_rng(seed)
+        drafts = np.array([[int(qrng.choice(m.vocab, p=q_np[b * G + v] / q_np[b * G + v].sum()))
+                            for v in range(G)] for b in range(B)], dtype=np.int64)
+        q_dev = torch.tensor(q_np, dtype=torch.float32, device=dev)
+        acc_mode, acc_q, acc_T = lsv.LSV_ACC_SAMPLE, q_dev, float(wl.temperature)
+    else:
+        acc_mode, acc_q, acc_T = lsv.LSV_ACC_GREEDY, None, 0.0
 
     def layout(gammas):
         """Verify rows [root_b, x_1..x_gamma_b] per sequence, concatenated."""
@@ -519,7 +535,7 @@ def main():
             seq_work.copy_(seq_base)
             lsv.lsv_verify_block(cfg, dm.buf, kv.buf, cap, B, seq_base, tok_g, ro, rows_step, cap, logits, status,
                                  ws.buf, ws.nbytes)
-            lsv.lsv_accept(lsv.LSV_ACC_GREEDY, B, m.vocab, logits, ro, rows_step, rows_seq, tok_g, None, 0.0, 0, 0,
+            lsv.lsv_accept(acc_mode, B, m.vocab, logits, ro, rows_step, rows_seq, tok_g, acc_q, acc_T, seed, 0,
                            acc, out, seq_work, status, aws.buf, aws.nbytes)
         body()
         graph = torch.cuda.CUDAGraph()
@@ -566,7 +582,7 @@ def main():
                               status)
         lsv.lsv_verify_block(cfg, dm.buf, kv.buf, cap, B, seq_base, tokens, row_off, rows_step, cap, logits, status,
                              ws.buf, ws.nbytes)
-        lsv.lsv_accept(lsv.LSV_ACC_GREEDY, B, m.vocab, logits, row_off, rows_step, rows_seq, tokens, None, 0.0, 0, 0,
+        lsv.lsv_accept(acc_mode, B, m.vocab, logits, row_off, rows_step, rows_seq, tokens, acc_q, acc_T, seed, 0,
                        acc, out, seq_work, status, aws.buf, aws.nbytes)
     step()
     torch.cuda.synchronize()
@@ -647,7 +663,8 @@ def main():
         "dtype": "bf16" if m.dtype == "bf16" else "f32",
         "data": "synthetic (seeded random-init weights, random prompt and draft ids)",
         "config": {"workload": wl.name, "model_shape": m.name, "batch": B, "context": one(ctx), "drafted": G,
-                   "gamma": one(g_star), "rows": rows, "selector": "marginal on measured cost", "accept": "greedy"},
+                   "gamma": one(g_star), "rows": rows, "selector": "marginal on measured cost",
+                   "accept": "greedy" if not sampling else f"sample T={wl.temperature}"},
         "roofline": roof,
         "step": {"latency_us": ms_step * 1e3, "wall_ms_per_step": t_wall / args.steps * 1e3,
                  "algorithmic_bytes": sb, "hbm_frac": sb / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBPS,

@@ -26,6 +26,8 @@
 // (1/rms, cache positions) are read in the epilogue.
 #include <math.h>
 
+#include <type_traits>
+
 #include "lsv_device.h"
 #include "lsv_attn.h"
 #include "lsv_gemm.h"
@@ -521,6 +523,13 @@ template <> struct GemmCfg<GEMM_O> { static constexpr int TPW = 1, KS = 1, U = 8
 template <> struct GemmCfg<GEMM_GATEUP> { static constexpr int TPW = 4, KS = 1, U = 4, NS = 3, EPI = EPI_SWIGLU, PSTAT = 1; };
 template <> struct GemmCfg<GEMM_DOWN> { static constexpr int TPW = 1, KS = 1, U = 8, NS = 3, EPI = EPI_RESID, PSTAT = 0; };
 template <> struct GemmCfg<GEMM_LMHEAD> { static constexpr int TPW = 4, KS = 1, U = 4, NS = 3, EPI = EPI_LOGITS, PSTAT = 1; };
+// gate/up of the wider models (3072 or more fragment rows: Qwen2.5-32B, Llama-3-70B shapes):
+// eight fragment rows per wave halve the workgroups and the activation loads per weight byte
+// (measured 5.45 -> 5.72 TB/s at d 5120, 5.62 -> 5.94 TB/s at d 8192; at d 4096 it lost);
+// blocks of up to 32 rows only
+constexpr int kGateUpWide = 5;  // internal kind id of that configuration
+constexpr int kGateUpWideRows = 3072;
+template <> struct GemmCfg<kGateUpWide> { static constexpr int TPW = 8, KS = 1, U = 2, NS = 3, EPI = EPI_SWIGLU, PSTAT = 1; };
 
 // Wide activation tiles (prefill bounds) use a shallower pipeline to stay in registers.
 template <int KIND, int MT_MAX> struct GemmShape {
@@ -583,7 +592,17 @@ static int launch_typed(GemmKind kind, int MT, const GemmArgs& a, hipStream_t st
   switch (kind) {
     case GEMM_QKV: return launch_mt<T, GEMM_QKV>(MT, a, st);
     case GEMM_O: return launch_mt<T, GEMM_O>(MT, a, st);
-    case GEMM_GATEUP: return launch_mt<T, GEMM_GATEUP>(MT, a, st);
+    case GEMM_GATEUP:
+      if constexpr (std::is_same<T, bf16_t>::value) {
+        if (a.Nt >= kGateUpWideRows && MT <= 2) {  // deeper row chunks would not fit its registers
+          if (MT == 1)
+            launch_one<T, kGateUpWide, 1>(a, st);
+          else
+            launch_one<T, kGateUpWide, 2>(a, st);
+          return LSV_OK;
+        }
+      }
+      return launch_mt<T, GEMM_GATEUP>(MT, a, st);
     case GEMM_DOWN: return launch_mt<T, GEMM_DOWN>(MT, a, st);
     case GEMM_LMHEAD: return launch_mt<T, GEMM_LMHEAD>(MT, a, st);
   }

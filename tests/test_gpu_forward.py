@@ -177,6 +177,14 @@ def test_llama8b_width_two_layers():
     _bf16_case(shape, 2, [2048], [17])
 
 
+def test_wide_model_gateup_skinny_blocks():
+    """Qwen2.5-32B and Llama-3-70B widths, one layer, blocks of 9 and 9 + 11 rows: their gate/up
+    products (3072 or more fragment rows) take the eight-fragment-rows-per-wave configuration,
+    with one and with two activation tiles."""
+    _bf16_case(configs.QWEN25_32B.with_layers(1), 22, [1000, 333], [9, 11])
+    _bf16_case(configs.LLAMA3_70B.with_layers(1), 23, [700], [9])
+
+
 def test_workspace_reused_across_bounds():
     """One zeroed workspace serves calls with different row and context bounds: prefill with
     the 64-row bound, then verify blocks with the 17-, 64- and 5-row bounds and a smaller
