@@ -531,7 +531,8 @@ constexpr int kGateUpWide = 5;  // internal kind id of that configuration
 constexpr int kGateUpWideRows = 3072;
 template <> struct GemmCfg<kGateUpWide> { static constexpr int TPW = 8, KS = 1, U = 2, NS = 3, EPI = EPI_SWIGLU, PSTAT = 1; };
 
-// Wide activation tiles (prefill bounds) use a shallower pipeline to stay in registers.
+// Bodies of three or four activation tiles (prefill bounds) use a shallower pipeline to stay in
+// registers.
 template <int KIND, int MT_MAX> struct GemmShape {
   using C = GemmCfg<KIND>;
   static constexpr int TPW = C::TPW, KS = C::KS, EPI = C::EPI, PSTAT = C::PSTAT;
@@ -556,10 +557,13 @@ __global__ void __launch_bounds__(64 * GemmCfg<KIND>::KS) gemm_kernel(GemmArgs a
   const int Mc = min(M - m0, 64);
   const int M_end = m0 + Mc;
   const int mt = Mc <= 16 ? 1 : (Mc <= 32 ? 2 : (Mc <= 48 ? 3 : 4));
+  // one or two tiles keep the product's full pipeline under any bound (lab: down at 9 rows under a
+  // 64-row bound, 41 -> 25 us); three or four take the shallower one
+  using C = GemmCfg<KIND>;
   if (mt <= 1 || MT_MAX == 1)
-    gemm_body<T, 1, S::TPW, S::KS, S::U, S::NS, S::EPI, MT_MAX, S::PSTAT>(a, M_end, tile, m0, red);
+    gemm_body<T, 1, S::TPW, S::KS, C::U, C::NS, S::EPI, MT_MAX, S::PSTAT>(a, M_end, tile, m0, red);
   else if (mt == 2 || MT_MAX == 2)
-    gemm_body<T, (MT_MAX >= 2 ? 2 : 1), S::TPW, S::KS, S::U, S::NS, S::EPI, MT_MAX, S::PSTAT>(a, M_end, tile, m0, red);
+    gemm_body<T, (MT_MAX >= 2 ? 2 : 1), S::TPW, S::KS, C::U, C::NS, S::EPI, MT_MAX, S::PSTAT>(a, M_end, tile, m0, red);
   else if (mt == 3 || MT_MAX == 3)
     gemm_body<T, (MT_MAX >= 3 ? 3 : 1), S::TPW, S::KS, S::U, S::NS, S::EPI, MT_MAX, S::PSTAT>(a, M_end, tile, m0, red);
   else
