@@ -634,9 +634,12 @@ constexpr int kWideCols = kWideFR * 16;  // output columns of a workgroup
 // keeps its own MTW activation tiles (rows wave*16*MTW ..) in registers, straight from L2.
 // A k-step is 8 LDS reads and 8 x MTW MFMAs per wave, each read feeding MTW of them.  Tiles
 // past the device row count are computed on clamped rows and never stored.
-// Ws: two buffers of 8 fragments; s_inv / s_seq / s_pos: per-row epilogue inputs (LDS).
+// Ws: two buffers of 8 fragments; s_inv: per-row 1/rms for the epilogue (LDS).  The QKV
+// projection never runs its fused epilogue here (split K: the reduce does; one split: the
+// scaled projection, then qkv_rope_kernel).
 template <int EPI, int MTW>
-LSV_DEV void gemm_wide_body(const GemmArgs& a, const int M, u32x4_t* Ws, float* s_inv, int* s_seq, int* s_pos) {
+LSV_DEV void gemm_wide_body(const GemmArgs& a, const int M, u32x4_t* Ws, float* s_inv) {
+  static_assert(EPI != EPI_QKV, "the batched QKV epilogue runs in the reduce or the RoPE kernel");
   using T = bf16_t;
   constexpr int FR = kWideFR;
   constexpr int RX = kWideRingX, RW = kWideRingW;
@@ -733,16 +736,10 @@ LSV_DEV void gemm_wide_body(const GemmArgs& a, const int M, u32x4_t* Ws, float* 
       }
     return;
   }
-  for (int r = tid; r < a.M_max; r += 256) {
-    if (EPI != EPI_RESID) s_inv[r] = inv_rms_serial(a, r);
-    if (EPI == EPI_QKV) {
-      const int b = seq_of_row(a.row_offsets, a.batch, r);
-      s_seq[r] = b;
-      s_pos[r] = GL(a.seq_len)[b] + (r - GL(a.row_offsets)[b]);
-    }
-  }
+  if (EPI != EPI_RESID)
+    for (int r = tid; r < a.M_max; r += 256) s_inv[r] = inv_rms_serial(a, r);
   __syncthreads();
-  const RowInputs rin{s_inv, s_seq, s_pos};
+  const RowInputs rin{s_inv, nullptr, nullptr};
   const f32x4_t none[FR][MTW] = {};
   gemm_epilogue<T, MTW, FR, EPI, false>(a, M, mt0 * 16, tn0, tvalid, acc, none, &rin);
 }
@@ -753,19 +750,18 @@ template <int EPI>
 __global__ void __launch_bounds__(256) gemm_wide_kernel(GemmArgs a) {
   __shared__ u32x4_t Ws[2 * kWideFR * kWave];
   __shared__ float s_inv[kWideRows];
-  __shared__ int s_seq[kWideRows], s_pos[kWideRows];
   const int M = min(GL(a.row_offsets)[a.batch], a.M_max);  // never trust device rows beyond the host bound
   const int mtw = ((M + 15) / 16 + 3) / 4;                 // activation tiles per wave
   if (mtw <= 1)
-    gemm_wide_body<EPI, 1>(a, M, Ws, s_inv, s_seq, s_pos);
+    gemm_wide_body<EPI, 1>(a, M, Ws, s_inv);
   else if (mtw == 2)
-    gemm_wide_body<EPI, 2>(a, M, Ws, s_inv, s_seq, s_pos);
+    gemm_wide_body<EPI, 2>(a, M, Ws, s_inv);
   else if (mtw == 3)
-    gemm_wide_body<EPI, 3>(a, M, Ws, s_inv, s_seq, s_pos);
+    gemm_wide_body<EPI, 3>(a, M, Ws, s_inv);
   else if (mtw == 4)
-    gemm_wide_body<EPI, 4>(a, M, Ws, s_inv, s_seq, s_pos);
+    gemm_wide_body<EPI, 4>(a, M, Ws, s_inv);
   else
-    gemm_wide_body<EPI, 5>(a, M, Ws, s_inv, s_seq, s_pos);
+    gemm_wide_body<EPI, 5>(a, M, Ws, s_inv);
 }
 
 // Split-K sums of the batched GEMM: one workgroup per (tile, 16 rows) adds the k ranges in
