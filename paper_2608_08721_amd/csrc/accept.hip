@@ -98,8 +98,21 @@ __global__ void __launch_bounds__(256) row_scan_kernel(const float* __restrict__
   const int x0 = c * kAcceptChunk, x1 = min(vocab, x0 + kAcceptChunk);
   float best = -INFINITY;
   int bidx = 0x7fffffff, bad = 0;
-  for (int x = x0 + threadIdx.x; x < x1; x += blockDim.x) {
-    float v = row[x];
+  // all of the thread's loads are issued before the first is used (one memory round trip);
+  // the elements are then taken in increasing x, as a strided loop would
+  constexpr int PER = kAcceptChunk / 256;
+  static_assert(PER * 256 == kAcceptChunk, "whole strides per chunk");
+  float vals[PER];
+#pragma unroll
+  for (int i = 0; i < PER; ++i) {
+    const int x = x0 + (int)threadIdx.x + 256 * i;
+    vals[i] = x < x1 ? row[x] : 0.f;
+  }
+#pragma unroll
+  for (int i = 0; i < PER; ++i) {
+    const int x = x0 + (int)threadIdx.x + 256 * i;
+    if (x >= x1) break;
+    float v = vals[i];
     if (!isfinite(v)) bad = 1;
     if (kSample) v = v / temperature;
     if (v > best || (v == best && x < bidx)) {
@@ -129,7 +142,11 @@ __global__ void __launch_bounds__(256) row_scan_kernel(const float* __restrict__
   }
   const float cmax = s_best[0];
   if (kSample) {
-    for (int x = x0 + threadIdx.x; x < x1; x += blockDim.x) sum += expf(row[x] / temperature - cmax);
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {  // the same elements, from registers, in the same order
+      if (x0 + (int)threadIdx.x + 256 * i >= x1) break;
+      sum += expf(vals[i] / temperature - cmax);
+    }
     s_sum[threadIdx.x] = sum;
     __syncthreads();
     for (int o = 128; o > 0; o >>= 1) {
