@@ -174,21 +174,32 @@ __global__ void __launch_bounds__(64) accept_greedy_kernel(const RowPartial* __r
   const bool in_bounds = r0 >= 0 && r1 >= r0 && r1 <= max_rows;
   const int rows = in_bounds ? r1 - r0 : 0, g = rows - 1;
   int am = 0, bad = 0;
+  const int next_tok = lane < g ? tokens[r0 + lane + 1] : 0;  // issued ahead of the partials' loads
   if (lane < rows) {
     float best = -INFINITY;
     int bi = 0x7fffffff;
-    for (int c = 0; c < nc; ++c) {  // chunks in ascending index order: strict '>' keeps the first maximum
-      RowPartial p = parts[(size_t)(r0 + lane) * nc + c];
-      bad |= p.bad;
-      if (p.a > best || bi == 0x7fffffff) {
-        best = p.a;
-        bi = p.idx;
+    // chunks in ascending index order (strict '>' keeps the first maximum), eight partials'
+    // loads in flight at a time
+    constexpr int NB = 8;
+    const RowPartial* rp = parts + (size_t)(r0 + lane) * nc;
+    for (int c0 = 0; c0 < nc; c0 += NB) {
+      RowPartial pb[NB];
+#pragma unroll
+      for (int i = 0; i < NB; ++i) pb[i] = rp[min(c0 + i, nc - 1)];
+#pragma unroll
+      for (int i = 0; i < NB; ++i) {
+        if (c0 + i >= nc) break;
+        bad |= pb[i].bad;
+        if (pb[i].a > best || bi == 0x7fffffff) {
+          best = pb[i].a;
+          bi = pb[i].idx;
+        }
       }
     }
     am = bi;
   }
   const bool any_bad = __any(bad);
-  const bool mismatch = lane < g && am != tokens[r0 + lane + 1];
+  const bool mismatch = lane < g && am != next_tok;
   const unsigned long long mm = __ballot(mismatch);
   const int a = mm ? __ffsll((long long)mm) - 1 : g;
   const int am_a = __shfl(am, a < 0 ? 0 : a, kWave);
