@@ -47,6 +47,15 @@ AttnPlan plan_attention(int batch, int nkv, int max_ctx) {
   return p;
 }
 
+// Splits of sequence b that hold keys: ceil(chunks / chunks_per_split), none for a sequence
+// without rows (or rows past the host bound).  At most n_splits, since L <= ctx_limit.
+LSV_DEV int active_splits(const AttnArgs& a, int r0, int rows, int C) {
+  if (r0 < 0 || rows <= 0 || r0 + rows > a.M_max) return 0;
+  const int L = min(C + rows, a.ctx_limit);
+  const int nch = L > 0 ? (L + kCh - 1) / kCh : 0;
+  return (nch + a.chunks_per_split - 1) / a.chunks_per_split;
+}
+
 template <int HD, int NW>
 __global__ void __launch_bounds__(64 * NW) attn_split_bf16_kernel(AttnArgs a) {
   constexpr int NG = NW / 4;               // wave groups: each loads one chunk per step
@@ -105,13 +114,7 @@ __global__ void __launch_bounds__(64 * NW) attn_split_bf16_kernel(AttnArgs a) {
   const int nch = L > 0 ? (L + kCh - 1) / kCh : 0;
   const int c1 = min(c0 + a.chunks_per_split, nch);
   const size_t prow = (size_t)s * a.M_max + r0;  // this split's partial row of the sequence's first row
-  if (c0 >= c1) {  // no key of this split exists for the sequence: mark its query vectors empty
-    for (int i = tid; i < nqv; i += 64 * NW) {
-      const size_t base = (prow + i / group) * a.nq + kvh * group + i % group;
-      *(GLOBAL f32x2_t*)(a.ml_part + base * 2) = f32x2_t{-INFINITY, 0.f};
-    }
-    return;
-  }
+  if (c0 >= c1) return;  // no key of this split exists for the sequence: the merge does not read it
   // A pass over the split covers up to NW query tiles, one per wave, each wave running its
   // tile over all chunks in order. With two groups, a pass left with at most four tiles
   // (all of them, or the rest after full passes) has group g run them over chunks c0+g,
@@ -287,38 +290,50 @@ __global__ void __launch_bounds__(64 * NW) attn_split_bf16_kernel(AttnArgs a) {
 
 // Merge the split partials of one (row, query head): out = sum_s w_s o_s / sum_s w_s l_s,
 // w_s = 2^(m_s - max_s m_s), splits in ascending order, 16 splits' loads in flight at a time.
+// Only the splits that hold keys of the row's sequence were written and are read.
 // A wave covers 256 / HD heads of one row, four head dimensions per lane.
 template <int HD>
 __global__ void __launch_bounds__(64) attn_merge_bf16_kernel(AttnArgs a) {
   constexpr int LPH = HD / 4, HPW = 64 / LPH, NB = 16;
   const int m = blockIdx.x, head = blockIdx.y * HPW + threadIdx.x / LPH, d = (threadIdx.x % LPH) * 4;
-  const int M = GL(a.row_offsets)[a.batch];
-  if (head >= a.nq) return;
+  // lane t: sequence t (batch <= 64); the row's sequence is the number of sequences ending at
+  // or before it
+  int mr0 = 0, mr1 = 0, mC = 0;
+  if ((int)threadIdx.x < a.batch) {
+    mr0 = GL(a.row_offsets)[threadIdx.x];
+    mr1 = GL(a.row_offsets)[threadIdx.x + 1];
+    mC = GL(a.seq_len)[threadIdx.x];
+  }
+  const int M = __shfl(mr1, a.batch - 1, kWave);
+  const int b = __popcll(__ballot((int)threadIdx.x < a.batch && mr1 <= m));
+  const int r0 = __shfl(mr0, b, kWave), r1 = __shfl(mr1, b, kWave), C = __shfl(mC, b, kWave);
+  if (m >= M || head >= a.nq) return;  // after the lane exchanges, which need every lane
+  const int ns = active_splits(a, r0, r1 - r0, C);
   const size_t stride = (size_t)a.M_max * a.nq, rh = (size_t)m * a.nq + head;
   const GLOBAL f32x2_t* ml = (const GLOBAL f32x2_t*)a.ml_part;
   const GLOBAL float* op = GL(a.o_part);
   float mx_all = -INFINITY, den = 0.f;
   f32x4_t num = {0.f, 0.f, 0.f, 0.f};
-  for (int s0 = 0; s0 < a.n_splits; s0 += NB) {
+  for (int s0 = 0; s0 < ns; s0 += NB) {
     f32x2_t mv[NB];
     f32x4_t ov[NB];
 #pragma unroll
     for (int i = 0; i < NB; ++i) {
-      const size_t s = (size_t)min(s0 + i, a.n_splits - 1);
+      const size_t s = (size_t)min(s0 + i, ns - 1);
       mv[i] = ml[s * stride + rh];
       ov[i] = *(const GLOBAL f32x4_t*)(op + (s * stride + rh) * HD + d);
     }
     float mx = mx_all;
 #pragma unroll
     for (int i = 0; i < NB; ++i)
-      if (s0 + i < a.n_splits) mx = fmaxf(mx, mv[i][0]);
+      if (s0 + i < ns) mx = fmaxf(mx, mv[i][0]);
     const float al = mx_all == -INFINITY ? 0.f : exp2f(mx_all - mx);
     den *= al;
     num *= al;
 #pragma unroll
     for (int i = 0; i < NB; ++i) {
-      // empty splits (max -inf) contribute nothing; their O was never written
-      if (s0 + i < a.n_splits && mv[i][0] != -INFINITY) {
+      // a split none of whose keys the row sees (max -inf) contributes nothing
+      if (s0 + i < ns && mv[i][0] != -INFINITY) {
         const float w = exp2f(mv[i][0] - mx);
         den += w * mv[i][1];
         num += w * ov[i];
@@ -326,7 +341,6 @@ __global__ void __launch_bounds__(64) attn_merge_bf16_kernel(AttnArgs a) {
     }
     mx_all = mx;
   }
-  if (m >= M) return;
   const f32x4_t r = num / den;
   const u32x2_t packed = {(uint32_t)f2bf(r[0]) | ((uint32_t)f2bf(r[1]) << 16),
                           (uint32_t)f2bf(r[2]) | ((uint32_t)f2bf(r[3]) << 16)};
