@@ -643,6 +643,31 @@ def main():
         y.copy_(x)
         torch.cuda.synchronize()
 
+    # baseline length policy (the G4-style rule of the comparison experiments): the next
+    # lengths from this step's outcome, and the rule's launch time (a graph of 100 launches)
+    g_in = torch.tensor(g_star, dtype=torch.int32, device=dev)
+    g_next = torch.zeros(B, dtype=torch.int32, device=dev)
+    ro_next = torch.zeros(B + 1, dtype=torch.int32, device=dev) if B <= lsv.LSV_MAX_BATCH else None
+
+    def g4():
+        lsv.lsv_next_length_g4(B, g_in, acc, status, 1, G, g_next, ro_next, None)
+    g4()
+    torch.cuda.synchronize()
+    g4_next = [int(x) for x in g_next.cpu()]
+    g4_graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g4_graph):
+        for _ in range(100):
+            g4()
+    g4_graph.replay()
+    torch.cuda.synchronize()
+    e2, e3 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e2.record()
+    g4_graph.replay()
+    e3.record()
+    torch.cuda.synchronize()
+    g4_us = e2.elapsed_time(e3) * 1e3 / 100
+    del g4_graph
+
     # expected emitted tokens per step under the drafter-confidence model (Assumption 3.7)
     exp_tokens = 0.0
     for b in range(B):
@@ -673,6 +698,8 @@ def main():
                  "realized_tokens_per_s": sum(a + 1 for a in a_len) / (ms_step * 1e-3)},
         "selection": {k: one(v) for k, v in chosen.items()},
         "sweep": {str(g): round(sweep[g] * 1e3, 2) for g in range(1, G + 1)},
+        "baseline_policies": {"static": "the sweep: one gamma for every sequence and round",
+                              "g4_next_gamma": one(g4_next), "g4_launch_us": round(g4_us, 2)},
     }
     if B > 1:
         # every sequence at the largest gamma: the batched regime the matrix cores serve

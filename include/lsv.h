@@ -255,6 +255,34 @@ int lsv_select_length(int32_t mode, int32_t batch, int32_t G, const float* d_con
                       int32_t* d_gamma, int32_t* d_aux, int32_t* d_row_offsets, int32_t* d_status,
                       void* stream);
 
+/* Baseline length policy of the comparison experiments (Sec. 4.1; Appendix B,
+ * baseline details: the dynamic-length rule adapted from Gemma 4's multi-token
+ * prediction, "G4-style").  From the round just verified, where sequence b drafted
+ * gamma_b tokens and accepted a_b of them (lsv_accept's d_accept_len):
+ *   raw_b = gamma_b + 2  if a_b == gamma_b (no draft rejected),
+ *           gamma_b - 1  otherwise;
+ *   gamma_next_b = min(max(raw_b, d_min), d_max).
+ * The rule states no bounds; the clamp to [d_min, d_max] is this library's reading.
+ * A sequence whose round failed (d_status[b] != LSV_OK) has no outcome: raw_b = gamma_b.
+ * A record outside 0 <= gamma_b < LSV_MAX_SEQ_ROWS, or (round OK) 0 <= a_b <= gamma_b,
+ * restarts at d_min and is flagged in d_err.
+ *
+ *   d_gamma        [batch] int32 in: this round's gamma_b
+ *   d_accept_len   [batch] int32 in: a_b
+ *   d_status       [batch] int32 in, nullable: lsv_accept's status per sequence
+ *   d_min, d_max   1 <= d_min <= d_max <= LSV_MAX_SEQ_ROWS - 1 (the next block must fit
+ *                  lsv_accept's one-wave limit)
+ *   d_gamma_next   [batch] out; may be the same buffer as d_gamma
+ *   d_row_offsets  [batch+1] out, nullable (needs batch <= LSV_MAX_BATCH): the next verify
+ *                  block's layout, row_offsets[b+1] = row_offsets[b] + gamma_next_b + 1
+ *   d_err          [batch] out, nullable: LSV_OK or LSV_ERR_INVALID_ARG (see above)
+ * Returns LSV_ERR_INVALID_ARG (nothing launched) for batch < 1, bounds outside the range
+ * above, NULL d_gamma / d_accept_len / d_gamma_next, or row offsets with batch > LSV_MAX_BATCH.
+ * One launch of one wave on the caller's stream. */
+int lsv_next_length_g4(int32_t batch, const int32_t* d_gamma, const int32_t* d_accept_len, const int32_t* d_status,
+                       int32_t d_min, int32_t d_max, int32_t* d_gamma_next, int32_t* d_row_offsets, int32_t* d_err,
+                       void* stream);
+
 /* ------------------------------------------------------------- measurement */
 /* Kernel classes of lsv_verify_block, one launch per layer each (LM head once). */
 enum {

@@ -214,6 +214,20 @@ int lsv_select_length(int32_t mode, int32_t batch, int32_t G, const float* d_con
   return hip_rc(rc, "select");
 }
 
+int lsv_next_length_g4(int32_t batch, const int32_t* d_gamma, const int32_t* d_accept_len, const int32_t* d_status,
+                       int32_t d_min, int32_t d_max, int32_t* d_gamma_next, int32_t* d_row_offsets, int32_t* d_err,
+                       void* stream) {
+  if (batch < 1) return fail(LSV_ERR_INVALID_ARG, "need batch >= 1");
+  if (d_min < 1 || d_min > d_max || d_max > LSV_MAX_SEQ_ROWS - 1)
+    return fail(LSV_ERR_INVALID_ARG, "need 1 <= d_min (%d) <= d_max (%d) <= %d", d_min, d_max, LSV_MAX_SEQ_ROWS - 1);
+  if (!d_gamma || !d_accept_len || !d_gamma_next) return fail(LSV_ERR_INVALID_ARG, "NULL pointer");
+  if (d_row_offsets && batch > LSV_MAX_BATCH)
+    return fail(LSV_ERR_INVALID_ARG, "row offsets need batch <= %d", LSV_MAX_BATCH);
+  int rc = lsv::launch_next_length_g4(batch, d_gamma, d_accept_len, d_status, d_min, d_max, d_gamma_next,
+                                      d_row_offsets, d_err, (hipStream_t)stream);
+  return hip_rc(rc, "next_length_g4");
+}
+
 int lsv_set_timing_events(int32_t kernel, void* const* events, int32_t n_slots, uint32_t record_flags) {
   if (kernel < LSV_KERNEL_QKV || kernel > LSV_KERNEL_ATTENTION) return fail(LSV_ERR_INVALID_ARG, "bad kernel class");
   if (n_slots < 0 || n_slots > LSV_MAX_TIMING_SLOTS || (n_slots > 0 && !events))

@@ -156,4 +156,48 @@ int launch_select(int mode, int batch, int G, const float* conf, const double* c
   return hipGetLastError() == hipSuccess ? LSV_OK : LSV_ERR_HIP;
 }
 
+// Baseline length policy of the comparison experiments (Sec. 4.1; Appendix B, baseline
+// details): the length rises by two after a round without a rejection and falls by one after a
+// round with one, kept in [d_min, d_max].  Lane b of the single wave takes sequence b + 64 k;
+// with row offsets requested (batch <= 64) the new lengths are scanned into them.  gamma_next
+// may alias gamma: each element is read before the same lane writes it.
+__global__ void __launch_bounds__(64) next_length_g4_kernel(int batch, const int32_t* gamma,
+                                                             const int32_t* __restrict__ accept_len,
+                                                             const int32_t* __restrict__ acc_status, int d_min,
+                                                             int d_max, int32_t* gamma_next,
+                                                             int32_t* __restrict__ row_offsets,
+                                                             int32_t* __restrict__ err) {
+  const int lane = threadIdx.x;
+  int mine = 0;  // this lane's new length when b = lane (the scan's input)
+  for (int b = lane; b < batch; b += kWave) {
+    const int g = gamma[b], a = accept_len[b];
+    const bool ok = acc_status == nullptr || acc_status[b] == LSV_OK;
+    const bool valid = g >= 0 && g < LSV_MAX_SEQ_ROWS && (!ok || (a >= 0 && a <= g));
+    const int raw = !valid ? d_min    // unusable round record: restart at the floor
+                    : !ok ? g         // the round failed: no outcome to react to
+                    : a == g ? g + 2  // every draft accepted
+                             : g - 1; // a draft rejected
+    const int next = min(max(raw, d_min), d_max);
+    gamma_next[b] = next;
+    if (err) err[b] = valid ? LSV_OK : LSV_ERR_INVALID_ARG;
+    if (b == lane) mine = next;
+  }
+  if (!row_offsets) return;
+  int v = lane < batch ? mine + 1 : 0;  // rows = root + gamma drafts
+  for (int o = 1; o < kWave; o <<= 1) {
+    const int t = __shfl_up(v, o, kWave);
+    if (lane >= o) v += t;
+  }
+  if (lane < batch) row_offsets[lane + 1] = v;
+  if (lane == 0) row_offsets[0] = 0;
+}
+
+int launch_next_length_g4(int batch, const int32_t* gamma, const int32_t* accept_len, const int32_t* status,
+                          int d_min, int d_max, int32_t* gamma_next, int32_t* row_offsets, int32_t* err,
+                          hipStream_t stream) {
+  hipLaunchKernelGGL(next_length_g4_kernel, dim3(1), dim3(kWave), 0, stream, batch, gamma, accept_len, status, d_min,
+                     d_max, gamma_next, row_offsets, err);
+  return hipGetLastError() == hipSuccess ? LSV_OK : LSV_ERR_HIP;
+}
+
 }  // namespace lsv

@@ -84,6 +84,15 @@ def test_host_validation(lib):
     expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_select_length, 2, 1, 4, 1, None, 1, 4, 2.0, 0, 0, 1, None, None, None, S)
     expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_select_length, 1, 1, 4, 1, 1, 1, 4, 2.0, 2, 4, 1, None, None, None, S)
     expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_select_length, 1, 65, 4, 1, 1, 1, 4, 2.0, 2, 0, 1, None, 1, None, S)
+    # baseline length policy: batch, bounds, required pointers, row offsets past LSV_MAX_BATCH
+    g4 = [1, 1, 1, None, 1, 16, 1, None, None, S]
+    expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_next_length_g4, *([0] + g4[1:]))
+    expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_next_length_g4, *(g4[:4] + [0] + g4[5:]))
+    expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_next_length_g4, *(g4[:4] + [17] + g4[5:]))
+    expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_next_length_g4, *(g4[:5] + [lsv.LSV_MAX_SEQ_ROWS] + g4[6:]))
+    expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_next_length_g4, *(g4[:2] + [None] + g4[3:]))
+    expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_next_length_g4, *(g4[:6] + [None] + g4[7:]))
+    expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_next_length_g4, *([65] + g4[1:7] + [1] + g4[8:]))
     # accept
     expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_accept, 3, 1, 10, 1, 1, 2, 2, 1, None, 0.0, 0, 0, 1, 1, None, None, 1,
            1 << 20, S)
