@@ -255,6 +255,33 @@ int lsv_select_length(int32_t mode, int32_t batch, int32_t G, const float* d_con
                       int32_t* d_gamma, int32_t* d_aux, int32_t* d_row_offsets, int32_t* d_status,
                       void* stream);
 
+/* ------------------------------------------------------------ round plumbing */
+/* Decoding runs in rounds (Sec. 3.1): each verifies the token emitted last (the root)
+ * followed by the round's drafts, and emits the accepted drafts plus one token, which is
+ * the next round's root.  These two calls carry tokens between the steps on the device,
+ * so that select -> pack -> verify -> accept -> next roots needs no host round trip.
+ *
+ * lsv_pack_block: the verify block's token array from the row layout that
+ *   lsv_select_length (or lsv_next_length_g4) wrote: for sequence b, row r0 = row_offsets[b]
+ *   gets d_roots[b] and rows r0 + k, k = 1..rows_b - 1, get d_drafts[b * G + k - 1].
+ *   d_row_offsets  [batch+1] in (device-written)
+ *   max_rows       host bound: no row at or past it is written; d_tokens holds max_rows
+ *   d_roots        [batch] in;  d_drafts [batch, G] in (may be NULL when G = 0)
+ *   d_tokens       [max_rows] out
+ *   d_status       [batch] out, nullable: LSV_OK, or LSV_ERR_INVALID_ARG when the
+ *                  sequence's rows are empty, past max_rows or more than G + 1 (then none
+ *                  of its rows is written)
+ *   Host errors: batch outside [1, LSV_MAX_BATCH], G outside [0, LSV_MAX_SEQ_ROWS - 1],
+ *   max_rows outside [1, LSV_MAX_ROWS], NULL pointers.
+ * lsv_next_roots: d_roots[b] = d_out_tokens[b * width + d_accept_len[b]] (lsv_accept's
+ *   outputs with max_rows_per_seq = width); a sequence whose status is not LSV_OK, or whose
+ *   accept_len is outside [0, width), keeps its root.  d_status nullable.
+ *   Host errors: batch < 1, width outside [1, LSV_MAX_SEQ_ROWS], NULL pointers. */
+int lsv_pack_block(int32_t batch, int32_t G, const int32_t* d_row_offsets, int32_t max_rows, const int32_t* d_roots,
+                   const int32_t* d_drafts, int32_t* d_tokens, int32_t* d_status, void* stream);
+int lsv_next_roots(int32_t batch, const int32_t* d_accept_len, const int32_t* d_out_tokens, int32_t width,
+                   const int32_t* d_status, int32_t* d_roots, void* stream);
+
 /* Baseline length policy of the comparison experiments (Sec. 4.1; Appendix B,
  * baseline details: the dynamic-length rule adapted from Gemma 4's multi-token
  * prediction, "G4-style").  From the round just verified, where sequence b drafted

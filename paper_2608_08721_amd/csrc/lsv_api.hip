@@ -228,6 +228,26 @@ int lsv_next_length_g4(int32_t batch, const int32_t* d_gamma, const int32_t* d_a
   return hip_rc(rc, "next_length_g4");
 }
 
+int lsv_pack_block(int32_t batch, int32_t G, const int32_t* d_row_offsets, int32_t max_rows, const int32_t* d_roots,
+                   const int32_t* d_drafts, int32_t* d_tokens, int32_t* d_status, void* stream) {
+  if (batch < 1 || batch > LSV_MAX_BATCH) return fail(LSV_ERR_INVALID_ARG, "need 1 <= batch <= %d", LSV_MAX_BATCH);
+  if (G < 0 || G > LSV_MAX_SEQ_ROWS - 1) return fail(LSV_ERR_INVALID_ARG, "need 0 <= G <= %d", LSV_MAX_SEQ_ROWS - 1);
+  if (max_rows < 1 || max_rows > LSV_MAX_ROWS) return fail(LSV_ERR_INVALID_ARG, "need 1 <= max_rows <= %d", LSV_MAX_ROWS);
+  if (!d_row_offsets || !d_roots || !d_tokens || (G > 0 && !d_drafts)) return fail(LSV_ERR_INVALID_ARG, "NULL pointer");
+  return hip_rc(lsv::launch_pack_block(batch, G, d_row_offsets, max_rows, d_roots, d_drafts, d_tokens, d_status,
+                                       (hipStream_t)stream),
+                "pack_block");
+}
+
+int lsv_next_roots(int32_t batch, const int32_t* d_accept_len, const int32_t* d_out_tokens, int32_t width,
+                   const int32_t* d_status, int32_t* d_roots, void* stream) {
+  if (batch < 1) return fail(LSV_ERR_INVALID_ARG, "need batch >= 1");
+  if (width < 1 || width > LSV_MAX_SEQ_ROWS) return fail(LSV_ERR_INVALID_ARG, "need 1 <= width <= %d", LSV_MAX_SEQ_ROWS);
+  if (!d_accept_len || !d_out_tokens || !d_roots) return fail(LSV_ERR_INVALID_ARG, "NULL pointer");
+  return hip_rc(lsv::launch_next_roots(batch, d_accept_len, d_out_tokens, width, d_status, d_roots, (hipStream_t)stream),
+                "next_roots");
+}
+
 int lsv_set_timing_events(int32_t kernel, void* const* events, int32_t n_slots, uint32_t record_flags) {
   if (kernel < LSV_KERNEL_QKV || kernel > LSV_KERNEL_ATTENTION) return fail(LSV_ERR_INVALID_ARG, "bad kernel class");
   if (n_slots < 0 || n_slots > LSV_MAX_TIMING_SLOTS || (n_slots > 0 && !events))

@@ -16,6 +16,12 @@ int launch_next_length_g4(int batch, const int32_t* gamma, const int32_t* accept
                           int d_min, int d_max, int32_t* gamma_next, int32_t* row_offsets, int32_t* err,
                           hipStream_t stream);
 
+// ---------------------------------------------------------------- rounds
+int launch_pack_block(int batch, int G, const int32_t* row_offsets, int max_rows, const int32_t* roots,
+                      const int32_t* drafts, int32_t* tokens, int32_t* status, hipStream_t stream);
+int launch_next_roots(int batch, const int32_t* accept_len, const int32_t* out_tokens, int width,
+                      const int32_t* status, int32_t* roots, hipStream_t stream);
+
 // measurement hook (lsv_set_timing_events): called around each launch of a kernel class
 void timing_before(int kernel, int index, hipStream_t st);
 void timing_after(int kernel, int index, hipStream_t st);

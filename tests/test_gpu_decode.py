@@ -1,0 +1,119 @@
+"""Multi-round decoding on the GPU (DecodeLoop: drafter -> length -> pack -> verify -> accept
+-> next roots, one captured graph per round):
+
+* the round plumbing kernels (lsv_pack_block, lsv_next_roots) against the oracle's plain
+  definitions, bit for bit, including rows that are empty, too long or past the bound;
+* the lossless property (Sec. 3.1): with greedy acceptance the emitted stream of every
+  length policy -- static 0 (plain decoding), static 4, the marginal rule, Algorithm 1 and the
+  G4-style rule -- equals the oracle's greedy continuation, on the fp32 tiny model (bar 1e-5)
+  where every step's top-2 logit gap is far above that bar.  The drafter is the planted,
+  calibrated stand-in of synth/drafter.py, fed the oracle's continuation."""
+import copy
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import forward as OF
+from oracle import rounds as OR
+from paper_2608_08721_amd import decode, lsv, runtime
+from synth import configs, drafter, gen
+from tests.lsv_testing import i32, note
+
+pytestmark = pytest.mark.gpu
+
+
+def test_pack_block_and_next_roots_parity():
+    rng = np.random.default_rng(3)
+    for trial in range(20):
+        B = int(rng.integers(1, lsv.LSV_MAX_BATCH + 1))
+        G = int(rng.integers(0, 20))
+        rows = rng.integers(1, G + 2, size=B)
+        bad = rng.random(B) < 0.15
+        rows[bad] = np.where(rng.random(bad.sum()) < 0.5, 0, G + 2)  # empty or one too many
+        off = np.concatenate([[0], np.cumsum(rows)]).astype(np.int32)
+        # the bound: the rows' end, a little short of it (the last rows are refused), or LSV_MAX_ROWS
+        max_rows = int(min(max(1, off[-1] - (rng.integers(0, 3) if trial % 4 == 0 else 0)), lsv.LSV_MAX_ROWS))
+        roots = rng.integers(0, 1000, size=B).astype(np.int32)
+        drafts = rng.integers(0, 1000, size=(B, max(G, 1))).astype(np.int32)
+        tok = torch.full((max_rows,), -5, dtype=torch.int32, device="cuda")
+        st = torch.full((B,), 99, dtype=torch.int32, device="cuda")
+        lsv.lsv_pack_block(B, G, i32(off), max_rows, i32(roots), i32(drafts), tok, st)
+        want_tok = [-5] * max_rows
+        want_st = OR.pack_block(off, roots, drafts, G, max_rows, want_tok)
+        assert tok.cpu().tolist() == want_tok and st.cpu().tolist() == want_st
+        # next roots from an accept-shaped record
+        width = G + 1
+        acc = rng.integers(-1, width + 1, size=B).astype(np.int32)
+        out = rng.integers(0, 1000, size=(B, width)).astype(np.int32)
+        ast = np.where(rng.random(B) < 0.2, lsv.LSV_ERR_NONFINITE, 0).astype(np.int32)
+        r = i32(roots)
+        lsv.lsv_next_roots(B, i32(acc), i32(out), width, i32(ast), r)
+        assert r.cpu().tolist() == OR.next_roots(acc, out, width, ast, roots)
+    torch.cuda.synchronize()
+
+
+SEED = 51
+N = 40  # greedy tokens per sequence that the test checks
+
+
+def _setup(m, w, contexts, G):
+    cfg = runtime.model_config(m)
+    dm = runtime.DeviceModel.from_weights(cfg, w)
+    # room for every round the test may run (up to 2N rounds of G + 1 rows past the contexts)
+    cap = runtime.kv_capacity(max(contexts) + 2 * N * (G + 1) + G + 2)
+    kv = runtime.KVCache(cfg, len(contexts), cap)
+    om = OF.Model(m, w)
+    conts, roots = [], []
+    for b, C in enumerate(contexts):
+        oc = OF.KVCache(m, 1, cap)
+        for l in range(m.n_layers):
+            k, v = gen.synthetic_kv(m, SEED + 31 * b, l, 1, C)
+            kv.write(l, b, 0, runtime.to_device(k[0]), runtime.to_device(v[0]))
+            oc.k[l][0, :, :C] = OF.stored_to_f64(k[0], "f32")
+            oc.v[l][0, :, :C] = OF.stored_to_f64(v[0], "f32")
+        root = int(gen.randint(SEED, 7 + b, 1, m.vocab)[0])
+        cont = OF.greedy_continuation(om, copy.deepcopy(oc), C, root, N)
+        # every step is decided by a clear margin (the fp32 path is within 1e-5 of the oracle)
+        lg, _ = OF.verify_block(om, copy.deepcopy(oc), [C], [root] + cont[:-1], [0, N])
+        top2 = np.sort(lg, axis=1)[:, -2:]
+        assert np.all(top2[:, 1] - top2[:, 0] > 1e-3 * np.abs(lg).max()), "pick a seed with settled steps"
+        assert list(np.argmax(lg, axis=1)) == cont
+        conts.append(cont)
+        roots.append(root)
+    return cfg, dm, kv, cap, conts, roots
+
+
+@pytest.mark.parametrize("policy,gamma0", [("static", 0), ("static", 4), ("marginal", None), ("alg1", None),
+                                           ("g4", 3)])
+def test_loop_is_lossless_fp32(policy, gamma0):
+    m, G = configs.TINY_F32, 12
+    contexts = [40, 75]
+    B = len(contexts)
+    w = gen.model_weights(m, SEED)
+    cfg, dm, kv, cap, conts, roots = _setup(m, w, contexts, G)
+    L = cap
+    stream = np.zeros((B, L), np.int64)
+    for b, C in enumerate(contexts):
+        stream[b, C] = roots[b]
+        stream[b, C + 1:C + 1 + N] = conts[b]
+    q = drafter.confidences(SEED, B, L)
+    dr = drafter.PlantedDrafter(stream, q, SEED, m.vocab, G)
+    cost = np.array([0.0] + [1.0 + 0.05 * d for d in range(1, G + 1)])
+    loop = decode.DecodeLoop(cfg, dm, kv, cap, B, G, policy, dr, cost=cost, block_n=4, gamma0=gamma0)
+    loop.reset(contexts, roots)
+    loop.round()  # one eager round, then the captured one replays from where it left off
+    got = [list(e) for e in loop.emitted()]
+    loop.capture()
+    rounds = 1
+    while min(len(g) for g in got) < N and rounds < 2 * N:
+        loop.replay()
+        for b, e in enumerate(loop.emitted()):
+            got[b] += e
+        rounds += 1
+    torch.cuda.synchronize()
+    assert bool((loop.status == 0).all())
+    for b in range(B):
+        assert got[b][:N] == conts[b], (b, got[b][:N], conts[b])
+        assert int(loop.seq_len[b]) == contexts[b] + len(got[b])
+    note(f"  {policy} (gamma0 {gamma0}): {N} tokens per sequence in {rounds} rounds, identical to greedy decoding")
