@@ -13,6 +13,9 @@ Beta(8, 2) * 0.92^i.
 
 Prints one JSON line (rank 0).  `value` = verified tokens per second
 (batch * (gamma + 1) / step time); the per-gamma latency sweep is in `sweep`.
+With --rounds R the line also carries `decode_loop`: R rounds of multi-round decoding per
+length policy (static lengths, the marginal rule, Algorithm 1, the G4-style rule) fed by a
+planted calibrated drafter, as tokens per second against plain greedy decoding.
 """
 import argparse
 import ctypes
@@ -45,6 +48,8 @@ def parse():
                    help="acceptance rule of the timed steps (default: greedy where the workload has it, else "
                         "speculative rejection sampling at the workload's temperature)")
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--rounds", type=int, default=0,
+                   help="also run multi-round decoding for this many rounds per length policy (planted drafter)")
     p.add_argument("--calib-copy", action="store_true",
                    help="also run one plain 256 MiB copy kernel (counter calibration for --pmc runs)")
     p.add_argument("--summarize", nargs=3, metavar=("TRACE_DIR", "FETCH_DIR", "WRITE_DIR"),
@@ -423,6 +428,90 @@ def cpu_baseline(m, seed, C, rows, tokens, gamma):
             "seconds_per_step": t_step}
 
 
+def decode_loop_measure(m, cfg, dm, B, G, ctx, prompts, pre, rows_buf, roots, cost, seed, n_rounds, dev):
+    """Multi-round decoding (select or a baseline policy -> pack -> verify -> accept -> next
+    roots, one graph per round) on its own cache with room for the rounds, fed by the planted
+    calibrated drafter: realized tokens per second for each length policy, against plain greedy
+    decoding (gamma = 0) on the same GPU.  The drafter plants the target's own greedy stream,
+    taken from the plain run."""
+    import torch
+
+    from paper_2608_08721_amd import decode, lsv, runtime
+    from synth import drafter
+    i32 = lambda x: torch.tensor(np.asarray(x, dtype=np.int32), device=dev)
+    n_tok = n_rounds * (G + 1) + G + 2  # the longest stream any policy can consume
+    cap2 = runtime.kv_capacity(max(ctx) + n_tok + G + 2)
+    kv2 = runtime.KVCache(cfg, B, cap2, dev)
+    ws2 = runtime.Workspace(lsv.lsv_verify_workspace_bytes(cfg, B, rows_buf, cap2), dev)
+    lg2 = torch.zeros((rows_buf, m.vocab), dtype=torch.float32, device=dev)
+    st2 = torch.zeros(B, dtype=torch.int32, device=dev)
+    filled = [0] * B
+    while filled != ctx:
+        take = [min(pre, ctx[b] - filled[b]) for b in range(B)]
+        off = runtime.row_offsets_of(take)
+        toks = np.concatenate([prompts[b][filled[b]:filled[b] + take[b]] for b in range(B)])
+        lsv.lsv_verify_block(cfg, dm.buf, kv2.buf, cap2, B, i32(filled), i32(toks), i32(off), rows_buf, cap2, lg2,
+                             st2, ws2.buf, ws2.nbytes)
+        filled = [filled[b] + take[b] for b in range(B)]
+    del ws2, lg2
+    ev = lambda: torch.cuda.Event(enable_timing=True)
+
+    def timed(loop):
+        loop.reset(ctx, roots)
+        torch.cuda.synchronize()
+        e0, e1 = ev(), ev()
+        e0.record()
+        for _ in range(n_rounds):
+            loop.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        toks = int((loop.seq_len.cpu() - torch.tensor(ctx, dtype=torch.int32)).sum())
+        return e0.elapsed_time(e1), toks
+
+    def streams(loop, n):
+        loop.reset(ctx, roots)
+        got = [[] for _ in range(B)]
+        while min(len(g) for g in got) < n:
+            loop.replay()
+            for b, e in enumerate(loop.emitted()):
+                got[b] += e
+        return got
+
+    plain = decode.DecodeLoop(cfg, dm, kv2, cap2, B, G, "static", None, gamma0=0)
+    plain.reset(ctx, roots)
+    plain.round()
+    plain.capture()
+    greedy = streams(plain, n_tok)
+    ms_plain, tok_plain = timed(plain)
+    del plain
+    stream = np.zeros((B, cap2), np.int64)
+    for b in range(B):
+        stream[b, ctx[b]] = roots[b]
+        stream[b, ctx[b] + 1:ctx[b] + 1 + n_tok] = greedy[b][:n_tok]
+    q = drafter.confidences(seed, B, cap2)
+    dr = drafter.PlantedDrafter(stream, q, seed, m.vocab, G, device=dev)
+    base_tps = tok_plain / (ms_plain * 1e-3)
+    out = {"rounds": n_rounds, "drafter": "planted greedy stream, confidences Beta(6, 1.5), calibrated",
+           "plain_decoding": {"tokens_per_s": base_tps, "ms_per_token": ms_plain / max(tok_plain, 1)},
+           "policies": {}}
+    policies = [("static", g) for g in (2, 4, 8, G)] + [("marginal", None), ("alg1", None), ("g4", 8)]
+    for pol, g0 in policies:
+        loop = decode.DecodeLoop(cfg, dm, kv2, cap2, B, G, pol, dr, cost=cost, block_n=8, gamma0=g0)
+        loop.reset(ctx, roots)
+        loop.round()
+        loop.capture()
+        ms, toks = timed(loop)
+        got = streams(loop, n_rounds)  # the emitted stream of n_rounds tokens or more per sequence
+        n_cmp = min(min(len(g) for g in got), n_tok)
+        same = all(got[b][:n_cmp] == greedy[b][:n_cmp] for b in range(B))
+        name = pol if g0 is None or pol == "g4" else f"{pol}{g0}"
+        out["policies"][name] = {"tokens_per_round": toks / (n_rounds * B), "ms_per_round": ms / n_rounds,
+                                 "tokens_per_s": toks / (ms * 1e-3), "speedup_vs_plain": toks / (ms * 1e-3) / base_tps,
+                                 "stream_equals_plain": same}
+        del loop
+    return out
+
+
 def main():
     args = parse()
     if args.summarize:
@@ -710,6 +799,10 @@ def main():
         result["uniform_gamma_max"] = {"gamma": G, "rows": rows_g, "latency_us": sweep[G] * 1e3,
                                        "mfma_frac": sf_g / t_g / MFMA_PEAK_FLOPS,
                                        "hbm_frac": sb_g / t_g / 1e9 / HBM_PEAK_GBPS}
+    if args.rounds > 0:
+        log(f"decode loop: {args.rounds} rounds per length policy")
+        result["decode_loop"] = decode_loop_measure(m, cfg, dm, B, G, ctx, prompts, pre, rows_buf, roots, cost, seed,
+                                                    args.rounds, dev)
     if not args.no_cpu_baseline and B == 1:
         log("cpu baseline: timing the oracle on a bounded sample")
         result["cpu_baseline"] = cpu_baseline(m, seed, ctx[0], rows, [roots[0]] + list(drafts[0]), g_star[0])

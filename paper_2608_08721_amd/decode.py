@@ -65,7 +65,7 @@ class DecodeLoop:
 
     def round(self):
         B, G = self.B, self.G
-        if G > 0:
+        if G > 0 and self.drafter is not None:  # no drafter: the drafts buffer keeps its contents
             self.drafter(self.seq_len, self.drafts, self.conf)
         if self.policy in ("marginal", "exhaustive", "alg1"):
             mode = {"marginal": lsv.LSV_SEL_MARGINAL, "exhaustive": lsv.LSV_SEL_EXHAUSTIVE,
