@@ -468,11 +468,21 @@ def decode_loop_measure(m, cfg, dm, B, G, ctx, prompts, pre, rows_buf, roots, co
         toks = int((loop.seq_len.cpu() - torch.tensor(ctx, dtype=torch.int32)).sum())
         return e0.elapsed_time(e1), toks
 
-    def streams(loop, n):
+    cost_d = torch.tensor(cost, dtype=torch.float64, device=dev)
+    g_ex = torch.zeros(B, dtype=torch.int32, device=dev)
+
+    def streams(loop, n, mad=None):
+        """Replay round by round until every sequence emitted n tokens; with mad (a list), also
+        append |gamma - gamma_exhaustive| per sequence and round, the exhaustive length taken on
+        the round's own confidences and the measured cost table."""
         loop.reset(ctx, roots)
         got = [[] for _ in range(B)]
         while min(len(g) for g in got) < n:
             loop.replay()
+            if mad is not None:
+                lsv.lsv_select_length(lsv.LSV_SEL_EXHAUSTIVE, B, G, loop.conf, cost_d, 1, G, 0.0, 1, 0, g_ex, None,
+                                      None, None)
+                mad += [abs(a - e) for a, e in zip(loop.gamma.cpu().tolist(), g_ex.cpu().tolist())]
             for b, e in enumerate(loop.emitted()):
                 got[b] += e
         return got
@@ -494,20 +504,23 @@ def decode_loop_measure(m, cfg, dm, B, G, ctx, prompts, pre, rows_buf, roots, co
     out = {"rounds": n_rounds, "drafter": "planted greedy stream, confidences Beta(6, 1.5), calibrated",
            "plain_decoding": {"tokens_per_s": base_tps, "ms_per_token": ms_plain / max(tok_plain, 1)},
            "policies": {}}
-    policies = [("static", g) for g in (2, 4, 8, G)] + [("marginal", None), ("alg1", None), ("g4", 8)]
-    for pol, g0 in policies:
-        loop = decode.DecodeLoop(cfg, dm, kv2, cap2, B, G, pol, dr, cost=cost, block_n=8, gamma0=g0)
+    policies = [("static", g, None) for g in (2, 4, 8, G)] + [("marginal", None, None), ("g4", 8, None)]
+    policies += [("alg1", None, a) for a in (1.8, 2.0, 2.2, 2.6)]  # the trade-off sweep
+    for pol, g0, alpha in policies:
+        loop = decode.DecodeLoop(cfg, dm, kv2, cap2, B, G, pol, dr, cost=cost, block_n=8, gamma0=g0,
+                                 alpha=alpha or 2.2)
         loop.reset(ctx, roots)
         loop.round()
         loop.capture()
         ms, toks = timed(loop)
-        got = streams(loop, n_rounds)  # the emitted stream of n_rounds tokens or more per sequence
+        mad = []
+        got = streams(loop, n_rounds, mad)  # the emitted stream of n_rounds tokens or more per sequence
         n_cmp = min(min(len(g) for g in got), n_tok)
         same = all(got[b][:n_cmp] == greedy[b][:n_cmp] for b in range(B))
-        name = pol if g0 is None or pol == "g4" else f"{pol}{g0}"
+        name = {"static": f"static{g0}", "alg1": f"alg1_alpha{alpha}"}.get(pol, pol)
         out["policies"][name] = {"tokens_per_round": toks / (n_rounds * B), "ms_per_round": ms / n_rounds,
                                  "tokens_per_s": toks / (ms * 1e-3), "speedup_vs_plain": toks / (ms * 1e-3) / base_tps,
-                                 "stream_equals_plain": same}
+                                 "mad_vs_exhaustive": statistics.mean(mad), "stream_equals_plain": same}
         del loop
     return out
 
