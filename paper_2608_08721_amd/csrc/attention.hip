@@ -116,12 +116,11 @@ __global__ void __launch_bounds__(64 * NW) attn_split_bf16_kernel(AttnArgs a) {
   const size_t prow = (size_t)s * a.M_max + r0;  // this split's partial row of the sequence's first row
   if (c0 >= c1) return;  // no key of this split exists for the sequence: the merge does not read it
   // A pass over the split covers up to NW query tiles, one per wave, each wave running its
-  // tile over all chunks in order. With two groups, a pass left with at most four tiles
-  // (all of them, or the rest after full passes) has group g run them over chunks c0+g,
-  // c0+g+2, ..., and the two running softmax states are combined at the end.
-  for (int qbase = 0; qbase < n_qt;) {
-    const bool halves = NG == 2 && n_qt - qbase <= 4;
-    const int qt = qbase + (halves ? (wave & 3) : wave);
+  // tile over all chunks in order.  Every tile takes the same chunk order and the same
+  // arithmetic whatever the block's tile count, so a row's result does not depend on how
+  // many rows share its block (decoding then emits the same tokens for every length).
+  for (int qbase = 0; qbase < n_qt; qbase += NW) {
+    const int qt = qbase + wave;
     const bool active = qt < n_qt;  // wave-uniform
     u32x4_t qf[HD / 32];
     f32x4_t o[HD / 16];
@@ -144,9 +143,10 @@ __global__ void __launch_bounds__(64 * NW) attn_split_bf16_kernel(AttnArgs a) {
     if (qbase > 0 && c0 + grp < c1) load_chunk(c0 + grp);  // a later pass over the same split
 
     // scores and running-softmax update of this wave's tile for the chunk in buffer g.
-    // A chunk below the cached length C is visible to every row of the block: no mask,
-    // and its scores are finite (the hardware exp2 then needs no guard); only chunks that
-    // reach the block's own keys apply the causal and length mask.
+    // A chunk below the cached length C is visible to every row of the block: no mask, and
+    // its scores are finite (exp2 needs no guard); only chunks that reach the block's own
+    // keys apply the causal and length mask.  Both take the same hardware exp2, so a key
+    // contributes the same bits whether or not its chunk was masked.
     auto consume = [&](int g, int c, auto masked) {
       constexpr bool MASK = decltype(masked)::value;
       const int k0 = c * kCh;
@@ -180,12 +180,12 @@ __global__ void __launch_bounds__(64 * NW) attn_split_bf16_kernel(AttnArgs a) {
       const float mnew = fmaxf(mrun, mx);
       float alpha, sum = 0.f;
       if (MASK) {
-        alpha = mrun == -INFINITY ? 0.f : exp2f(mrun - mnew);
+        alpha = mrun == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(mrun - mnew);
 #pragma unroll
         for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
-            const float p = mnew == -INFINITY ? 0.f : exp2f(sc[kt][r] - mnew);
+            const float p = mnew == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(sc[kt][r] - mnew);
             sc[kt][r] = p;
             sum += p;
           }
@@ -230,53 +230,15 @@ __global__ void __launch_bounds__(64 * NW) attn_split_bf16_kernel(AttnArgs a) {
       if (!active) continue;  // wave-uniform: a wave without a query tile in this pass
       using Masked = std::true_type;
       using Full = std::false_type;
-      if (halves) {
-        const int cc = c + grp;
-        if (cc < c1) {
-          if ((cc + 1) * kCh <= C) consume(grp, cc, Full{});
-          else consume(grp, cc, Masked{});
-        }
-      } else {
 #pragma unroll
-        for (int g = 0; g < NG; ++g)
-          if (c + g < c1) {
-            if ((c + g + 1) * kCh <= C) consume(g, c + g, Full{});
-            else consume(g, c + g, Masked{});
-          }
-      }
+      for (int g = 0; g < NG; ++g)
+        if (c + g < c1) {
+          if ((c + g + 1) * kCh <= C) consume(g, c + g, Full{});
+          else consume(g, c + g, Masked{});
+        }
     }
 
-    if (halves) {
-      // group 1 hands its state to group 0 through the (now free) chunk buffers; group 0
-      // combines them: its own chunks first, in a fixed order
-      constexpr int OW = HD / 16 * 4 + 2;  // floats per lane: o, then m and l
-      float* xch = reinterpret_cast<float*>(&Ks[0][0]);
-      static_assert(NG == 1 || 4 * 64 * OW * sizeof(float) <= sizeof(Ks), "the exchange fits the K buffers");
-      __syncthreads();
-      float* mine = xch + ((size_t)(wave & 3) * 64 + lane) * OW;
-      if (grp == 1 && active) {
-#pragma unroll
-        for (int dt = 0; dt < HD / 16; ++dt)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) mine[dt * 4 + r] = o[dt][r];
-        mine[OW - 2] = mrun;
-        mine[OW - 1] = lrun;
-      }
-      __syncthreads();
-      if (grp == 0 && active) {
-        const float m1 = mine[OW - 2], l1 = mine[OW - 1];
-        const float mnew = fmaxf(mrun, m1);
-        const float a0 = mrun == -INFINITY ? 0.f : exp2f(mrun - mnew);
-        const float a1 = m1 == -INFINITY ? 0.f : exp2f(m1 - mnew);
-        lrun = lrun * a0 + l1 * a1;
-#pragma unroll
-        for (int dt = 0; dt < HD / 16; ++dt)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) o[dt][r] = o[dt][r] * a0 + mine[dt * 4 + r] * a1;
-        mrun = mnew;
-      }
-    }
-    if (active && qval && (!halves || grp == 0)) {
+    if (active && qval) {
       const size_t base = (prow + qv / group) * a.nq + kvh * group + qv % group;
       GLOBAL float* op = GL(a.o_part) + base * HD;
 #pragma unroll
@@ -284,7 +246,6 @@ __global__ void __launch_bounds__(64 * NW) attn_split_bf16_kernel(AttnArgs a) {
       if (g4 == 0) *(GLOBAL f32x2_t*)(a.ml_part + base * 2) = f32x2_t{mrun, lrun};
     }
     __syncthreads();  // the next pass refills the chunk buffers
-    qbase += halves ? 4 : NW;
   }
 }
 

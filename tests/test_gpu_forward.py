@@ -129,15 +129,15 @@ def test_bf16_hd128_ragged():
 
 def test_bf16_hd128_few_tiles_under_loose_bound():
     """9 rows of a 4-query-head group under a 17-row bound: the attention split kernel takes
-    eight waves (chosen from the bound) but has three query tiles, so its two four-wave
-    groups take alternate chunks and combine their softmax states."""
+    eight waves (chosen from the bound) but has three query tiles, so five waves idle while
+    both four-wave groups keep loading chunks."""
     _bf16_case(configs.SMALL_BF16, 15, [300], [9], bound=17)
 
 
-def test_bf16_hd128_halves_with_one_or_two_tiles():
+def test_bf16_hd128_eight_waves_with_one_or_two_tiles():
     """Under a 17-rows-per-sequence bound the split kernel runs eight waves; sequences of 1
-    and 2 query tiles have the two four-wave groups take alternate chunks (a 30-token context
-    is a single chunk, so one group sees no chunk at all and hands over an empty state)."""
+    and 2 query tiles leave most waves idle (a 30-token context is a single chunk, so the
+    second group's buffer stays unused)."""
     _bf16_case(configs.SMALL_BF16, 19, [300, 30, 129], [3, 7, 1], bound=51)
 
 
@@ -155,7 +155,7 @@ def test_bf16_hd128_two_passes_of_eight_waves():
 
 def test_bf16_hd128_three_passes_beside_a_one_tile_sequence():
     """Rows 70 + 2 under a 72-row bound: the first sequence's 18 query tiles take three passes
-    of the eight-wave split kernel (8, 8, then 2 in alternate chunks), the second sequence's
+    of the eight-wave split kernel (8, 8, then 2 tiles), the second sequence's
     single tile one."""
     _bf16_case(configs.SMALL_BF16, 21, [260, 40], [70, 2], bound=72)
 

@@ -1,0 +1,39 @@
+"""A row's verify result does not depend on the block it is verified in.
+
+The same 17 rows are verified as one block, then again at their own positions as blocks of
+1 (under a one-row bound, which takes the smaller kernel variants), of 5 and of 11 rows; the
+logits of every row must be bit-identical.  Every GEMM output accumulates its k-steps in the
+same order whatever the row count, and every attention tile walks the context's chunks in the
+same order with the same exp2 whether or not its chunk is masked.  This is what makes
+multi-round greedy decoding emit exactly the plain greedy stream for every speculative
+length (see test_gpu_decode.py)."""
+import numpy as np
+import pytest
+
+from paper_2608_08721_amd import runtime
+from synth import configs, gen
+from tests.lsv_testing import GpuModel, note
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.mark.parametrize("shape", [configs.SMALL_BF16, configs.TINY_BF16])
+def test_row_logits_do_not_depend_on_block_size(shape):
+    seed, C, R = 61, 150, 17
+    w = gen.model_weights(shape, seed)
+    cap = runtime.kv_capacity(C + R + 8)
+    gm = GpuModel(shape, w, 1, cap, max_rows=R)
+    for l in range(shape.n_layers):
+        k, v = gen.synthetic_kv(shape, seed, l, 1, C)
+        gm.kv.write(l, 0, 0, runtime.to_device(k[0]), runtime.to_device(v[0]))
+    toks = gen.randint(seed, 900, R, shape.vocab)
+    whole, st = gm.verify([C], toks, [0, R])
+    assert st[0] == 0 and np.isfinite(whole).all()
+    for sizes, bound in (([1] * R, 1), ([5, 5, 5, 2], R), ([11, 6], R)):
+        pos = 0
+        for n in sizes:
+            lg, st = gm.verify([C + pos], toks[pos:pos + n], [0, n], max_rows=bound)
+            assert st[0] == 0
+            assert np.array_equal(lg, whole[pos:pos + n]), (shape.name, sizes, pos)
+            pos += n
+    note(f"  {shape.name}: 17 rows bit-identical as one block and as blocks of 1, 5 and 11 rows")
