@@ -674,6 +674,44 @@ def main():
     tokens = layout(g_star)
     log(f"chosen gamma: {chosen}")
 
+    # ---- joint batched selection on a cost table over total drafts R (linear between the
+    # uniform-gamma points R = B * gamma of the sweep), with its launch time
+    cost_j = np.empty(B * G + 1)
+    for R in range(B * G + 1):
+        lo = max(1, min(R // B, G))
+        hi = min(lo + 1, G)
+        fr = 0.0 if lo == hi else max(0.0, (R - B * lo) / B)
+        cost_j[R] = sweep[lo] * (1.0 - fr) + sweep[hi] * fr
+    cost_jt = torch.tensor(cost_j, device=dev)
+    g_joint = torch.zeros(B, dtype=torch.int32, device=dev)
+    tot_joint = torch.zeros(1, dtype=torch.int32, device=dev)
+
+    def joint():
+        lsv.lsv_select_joint(B, G, conf, cost_jt, G, 0, g_joint, tot_joint, None, None)
+    joint()
+    torch.cuda.synchronize()
+    chosen["joint"] = [int(x) for x in g_joint.cpu()]
+    jg = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(jg):
+        for _ in range(20):
+            joint()
+    jg.replay()
+    torch.cuda.synchronize()
+    ej0, ej1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ej0.record()
+    jg.replay()
+    ej1.record()
+    torch.cuda.synchronize()
+    joint_us = ej0.elapsed_time(ej1) * 1e3 / 20
+    del jg
+
+    def predicted(gs):  # expected emitted tokens (drafts + one) per ms of verify, confidence model
+        e = sum(1.0 + float(np.cumprod(conf_np[b].astype(np.float64))[:gs[b]].sum()) for b in range(B))
+        return e / cost_j[sum(gs)]
+    joint_info = {"gamma": chosen["joint"], "total_drafts": int(tot_joint.cpu()[0]), "launch_us": round(joint_us, 2),
+                  "predicted_tokens_per_ms": predicted(chosen["joint"]),
+                  "predicted_tokens_per_ms_marginal": predicted(g_star)}
+
     # ---- the timed step: select -> verify -> accept, one graph, dominant kernel bracketed by events
     n_slots = m.n_layers
     hev = HipEvents(2 * n_slots)
@@ -800,6 +838,7 @@ def main():
                  "realized_tokens_per_s": sum(a + 1 for a in a_len) / (ms_step * 1e-3)},
         "selection": {k: one(v) for k, v in chosen.items()},
         "sweep": {str(g): round(sweep[g] * 1e3, 2) for g in range(1, G + 1)},
+        "joint_selection": joint_info,
         "baseline_policies": {"static": "the sweep: one gamma for every sequence and round",
                               "g4_next_gamma": one(g4_next), "g4_launch_us": round(g4_us, 2)},
     }

@@ -255,6 +255,32 @@ int lsv_select_length(int32_t mode, int32_t batch, int32_t G, const float* d_con
                       int32_t* d_gamma, int32_t* d_aux, int32_t* d_row_offsets, int32_t* d_status,
                       void* stream);
 
+/* Joint batched selection: gamma_b in [1, d_max] for every sequence at once, maximising
+ *   F(gamma) = sum_b N_b(gamma_b) / cost[R],  R = sum_b gamma_b,
+ * the objective of Eq. 2 (expected accepted tokens per unit of verify time) over a batch
+ * whose verify cost is shared.  The paper gives only the per-sequence rule; this batch
+ * form is the library's extension.  N_b as for lsv_select_length (binary64, same order).
+ * For each R the best allocation gives every sequence one draft and then the R - batch
+ * largest increments P_{b,j}, j >= 2 (N_b has non-increasing increments), ties to the
+ * smaller b, then the smaller j; F(R) sums N_b(gamma_b) over b in order; the smallest R
+ * with the largest F wins.
+ *
+ *   d_conf        [batch, G] fp32 confidences in [0, 1]
+ *   d_cost        [batch * d_max + 1] fp64: cost[R] = verify cost of a batch with R drafts in
+ *                 total (root rows included in the cost); entries R < batch are not read;
+ *                 entries R in [batch, batch * d_max] must be finite and > 0
+ *   flags         LSV_SEL_BONUS as for lsv_select_length
+ *   d_gamma       [batch] out;  d_total [1] out (nullable): R
+ *   d_row_offsets [batch+1] out (nullable): row_offsets[b+1] = row_offsets[b] + gamma_b + 1
+ *   d_status      [batch] out (nullable): LSV_OK, or LSV_ERR_INVALID_ARG for every sequence
+ *                 when a confidence or a needed cost is invalid (then gamma = 0, R = 0 and
+ *                 the row offsets give each sequence its root row only)
+ * Host errors: batch outside [1, LSV_MAX_BATCH], G outside [1, LSV_MAX_G], d_max outside
+ * [1, G], unknown flags, NULL d_conf / d_cost / d_gamma.  One workgroup on the caller's stream. */
+int lsv_select_joint(int32_t batch, int32_t G, const float* d_conf, const double* d_cost, int32_t d_max,
+                     uint32_t flags, int32_t* d_gamma, int32_t* d_total, int32_t* d_row_offsets, int32_t* d_status,
+                     void* stream);
+
 /* ------------------------------------------------------------ round plumbing */
 /* Decoding runs in rounds (Sec. 3.1): each verifies the token emitted last (the root)
  * followed by the round's drafts, and emits the accepted drafts plus one token, which is

@@ -149,3 +149,45 @@ def select_batch(mode, conf, cost, d_init, d_max, alpha, n, flags=0):
         g.append(x)
         a.append(y)
     return g, a
+
+
+def select_joint(conf, cost, d_max, bonus=False):
+    """Joint batched selection: gamma_b in [1, d_max] maximising
+        F(gamma) = sum_b N_b(gamma_b) / cost[sum_b gamma_b]
+    (Eq. 2's expected-tokens-per-verify-time objective over a batch whose verify cost is
+    shared; the paper states only the per-sequence rule, so this extension and its readings
+    are the library's).  cost[R] is the verify cost of a batch with R drafts in total
+    (R in [B, B * d_max]; lower entries unused).
+
+    For a fixed total R the best allocation gives every sequence its first draft and then
+    the R - B largest increments P_{b,j} (2 <= j <= d_max): each N_b has non-increasing
+    increments (P_{b,j+1} = P_{b,j} q_{b,j+1} <= P_{b,j}), so an exchange argument makes the
+    greedy choice optimal.  Ties between increments go to the smaller b, then the smaller j
+    (which keeps every sequence's choice a prefix).  F is then evaluated for every R with
+    N_b from ``expected_accepted`` summed over b in order, and the smallest maximising R
+    wins.  Returns (gamma[B], R)."""
+    B = len(conf)
+    P = [prefix_products([float(v) for v in row]) for row in conf]
+    N = [expected_accepted([float(v) for v in row], bonus) for row in conf]
+    inc = sorted(((-P[b][j - 1], b, j) for b in range(B) for j in range(2, d_max + 1)))
+    gamma = [1] * B
+    best_f, best_R, best_g = None, None, None
+    for R in range(B, B * d_max + 1):
+        if R > B:
+            _, b, j = inc[R - B - 1]
+            gamma[b] = j
+        s = 0.0
+        for b in range(B):
+            s = s + N[b][gamma[b] - 1]
+        f = s / float(cost[R])
+        if best_f is None or f > best_f:
+            best_f, best_R, best_g = f, R, list(gamma)
+    return best_g, best_R
+
+
+def joint_objective(conf, cost, gamma, bonus=False):
+    """F(gamma) for a given allocation (used by the brute-force pins)."""
+    s = 0.0
+    for row, g in zip(conf, gamma):
+        s = s + expected_accepted([float(v) for v in row], bonus)[g - 1]
+    return s / float(cost[sum(gamma)])

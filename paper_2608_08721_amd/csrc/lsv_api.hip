@@ -214,6 +214,18 @@ int lsv_select_length(int32_t mode, int32_t batch, int32_t G, const float* d_con
   return hip_rc(rc, "select");
 }
 
+int lsv_select_joint(int32_t batch, int32_t G, const float* d_conf, const double* d_cost, int32_t d_max, uint32_t flags,
+                     int32_t* d_gamma, int32_t* d_total, int32_t* d_row_offsets, int32_t* d_status, void* stream) {
+  if (batch < 1 || batch > LSV_MAX_BATCH) return fail(LSV_ERR_INVALID_ARG, "need 1 <= batch <= %d", LSV_MAX_BATCH);
+  if (G < 1 || G > LSV_MAX_G) return fail(LSV_ERR_INVALID_ARG, "need 1 <= G <= %d", LSV_MAX_G);
+  if (d_max < 1 || d_max > G) return fail(LSV_ERR_INVALID_ARG, "need 1 <= d_max (%d) <= G (%d)", d_max, G);
+  if (flags & ~(uint32_t)LSV_SEL_BONUS) return fail(LSV_ERR_INVALID_ARG, "unknown flags");
+  if (!d_conf || !d_cost || !d_gamma) return fail(LSV_ERR_INVALID_ARG, "NULL pointer");
+  return hip_rc(lsv::launch_select_joint(batch, G, d_conf, d_cost, d_max, flags, d_gamma, d_total, d_row_offsets,
+                                         d_status, (hipStream_t)stream),
+                "select_joint");
+}
+
 int lsv_next_length_g4(int32_t batch, const int32_t* d_gamma, const int32_t* d_accept_len, const int32_t* d_status,
                        int32_t d_min, int32_t d_max, int32_t* d_gamma_next, int32_t* d_row_offsets, int32_t* d_err,
                        void* stream) {

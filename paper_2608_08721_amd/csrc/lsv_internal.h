@@ -12,6 +12,8 @@ namespace lsv {
 int launch_select(int mode, int batch, int G, const float* conf, const double* cost, int d_init, int d_max,
                   double alpha, int block_n, unsigned flags, int32_t* gamma, int32_t* aux, int32_t* row_offsets,
                   int32_t* status, hipStream_t stream);
+int launch_select_joint(int batch, int G, const float* conf, const double* cost, int d_max, unsigned flags,
+                        int32_t* gamma, int32_t* total, int32_t* row_offsets, int32_t* status, hipStream_t stream);
 int launch_next_length_g4(int batch, const int32_t* gamma, const int32_t* accept_len, const int32_t* status,
                           int d_min, int d_max, int32_t* gamma_next, int32_t* row_offsets, int32_t* err,
                           hipStream_t stream);

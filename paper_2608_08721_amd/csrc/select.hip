@@ -156,6 +156,158 @@ int launch_select(int mode, int batch, int G, const float* conf, const double* c
   return hipGetLastError() == hipSuccess ? LSV_OK : LSV_ERR_HIP;
 }
 
+// Joint batched selection: gamma_b in [1, d_max] maximising sum_b N_b(gamma_b) / cost[R],
+// R = sum_b gamma_b (Eq. 2's objective over a batch that shares one verify cost).  For each
+// R the best allocation is every sequence's first draft plus the R - B largest increments
+// P_{b,j} (j >= 2; N_b has non-increasing increments), ties to the smaller b, then j.  One
+// workgroup: the increments' ranks in that order come from binary searches in each
+// sequence's (non-increasing) list, the allocation for every R from binary searches in the
+// ranks, and the objective for every R in the same binary64 order as a sequential
+// evaluation (N_b left to right, summed over b in order).
+constexpr int kJointThreads = 1024;
+
+__global__ void __launch_bounds__(kJointThreads) select_joint_kernel(int batch, int G, const float* __restrict__ conf,
+                                                                      const double* __restrict__ cost, int d_max,
+                                                                      unsigned flags, int32_t* __restrict__ gamma,
+                                                                      int32_t* __restrict__ total,
+                                                                      int32_t* __restrict__ row_offsets,
+                                                                      int32_t* __restrict__ status) {
+  __shared__ double sP[LSV_MAX_BATCH][LSV_MAX_G];  // P_{b,j} at [b][j-1]
+  __shared__ double sN[LSV_MAX_BATCH][LSV_MAX_G];  // N_b(j) at [b][j-1]
+  __shared__ int sRank[LSV_MAX_BATCH][LSV_MAX_G];  // rank of increment (b, j >= 2) at [b][j-1]
+  __shared__ double sBestF[kJointThreads / 64];
+  __shared__ int sBestR[kJointThreads / 64], sBad;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const bool bonus = flags & LSV_SEL_BONUS;
+  if (tid == 0) sBad = 0;
+  __syncthreads();
+  // 1. prefix products and expected accepted counts, one wave per sequence
+  for (int b = wave; b < batch; b += kJointThreads / 64) {
+    const float q = lane < G ? conf[(size_t)b * G + lane] : 0.0f;
+    if (__any(lane < G && !(q >= 0.0f && q <= 1.0f))) sBad = 1;  // NaN fails both tests
+    double p = 1.0, n = bonus ? 1.0 : 0.0;
+    for (int j = 1; j <= d_max; ++j) {
+      p = p * (double)bcastf(q, j - 1);
+      n = n + p;
+      if (lane == j - 1) {
+        sP[b][lane] = p;
+        sN[b][lane] = n;
+      }
+    }
+  }
+  const int Rmin = batch, Rmax = batch * d_max;
+  for (int R = Rmin + tid; R <= Rmax; R += kJointThreads)
+    if (!(cost[R] > 0.0 && cost[R] <= 1.7976931348623157e308)) sBad = 1;
+  __syncthreads();
+  if (sBad) {
+    for (int b = tid; b < batch; b += kJointThreads) {
+      gamma[b] = 0;
+      if (status) status[b] = LSV_ERR_INVALID_ARG;
+    }
+    if (tid == 0 && total) *total = 0;
+    if (row_offsets)
+      for (int i = tid; i <= batch; i += kJointThreads) row_offsets[i] = i;  // root rows only
+    return;
+  }
+  // 2. rank of every increment (b, j), 2 <= j <= d_max, in (value desc, b asc, j asc) order
+  const int per = d_max - 1;  // increments per sequence
+  for (int e = tid; e < batch * per; e += kJointThreads) {
+    const int b = e / per, j = 2 + e % per;
+    const double v = sP[b][j - 1];
+    int rank = j - 2;  // the sequence's own earlier increments
+    for (int o = 0; o < batch; ++o) {
+      if (o == b) continue;
+      // count of j' in [2, d_max] with P > v (o > b) or P >= v (o < b): a prefix of o's list
+      int lo = 2, hi = d_max + 1;
+      while (lo < hi) {
+        const int mid = (lo + hi) >> 1;
+        const double w = sP[o][mid - 1];
+        if (o < b ? w >= v : w > v) lo = mid + 1;
+        else hi = mid;
+      }
+      rank += lo - 2;
+    }
+    sRank[b][j - 1] = rank;
+  }
+  __syncthreads();
+  // 3. objective for every total R; the best (largest f, then smallest R) per thread, then per wave
+  double bestF = -1.0;
+  int bestR = 0x7fffffff;
+  for (int R = Rmin + tid; R <= Rmax; R += kJointThreads) {
+    const int take = R - Rmin;  // increments beyond the first drafts
+    double s = 0.0;
+    for (int b = 0; b < batch; ++b) {
+      int lo = 2, hi = d_max + 1;  // gamma_b = 1 + #{j >= 2 : rank < take} (ranks rise with j)
+      while (lo < hi) {
+        const int mid = (lo + hi) >> 1;
+        if (sRank[b][mid - 1] < take) lo = mid + 1;
+        else hi = mid;
+      }
+      s = s + sN[b][lo - 2];  // N_b(gamma_b), gamma_b = lo - 1
+    }
+    const double f = s / cost[R];
+    if (f > bestF) {  // R rises within a thread: ties keep the smaller R
+      bestF = f;
+      bestR = R;
+    }
+  }
+  for (int o = 32; o > 0; o >>= 1) {
+    const double f2 = __shfl_xor(bestF, o, kWave);
+    const int r2 = __shfl_xor(bestR, o, kWave);
+    if (f2 > bestF || (f2 == bestF && r2 < bestR)) {
+      bestF = f2;
+      bestR = r2;
+    }
+  }
+  if (lane == 0) {
+    sBestF[wave] = bestF;
+    sBestR[wave] = bestR;
+  }
+  __syncthreads();
+  if (wave != 0) return;
+  bestF = lane < kJointThreads / 64 ? sBestF[lane] : -1.0;
+  bestR = lane < kJointThreads / 64 ? sBestR[lane] : 0x7fffffff;
+  for (int o = 32; o > 0; o >>= 1) {
+    const double f2 = __shfl_xor(bestF, o, kWave);
+    const int r2 = __shfl_xor(bestR, o, kWave);
+    if (f2 > bestF || (f2 == bestF && r2 < bestR)) {
+      bestF = f2;
+      bestR = r2;
+    }
+  }
+  // 4. the allocation at the best R, its status and the verify row offsets (batch <= 64)
+  int g = 0;
+  if (lane < batch) {
+    const int take = bestR - Rmin;
+    int lo = 2, hi = d_max + 1;
+    while (lo < hi) {
+      const int mid = (lo + hi) >> 1;
+      if (sRank[lane][mid - 1] < take) lo = mid + 1;
+      else hi = mid;
+    }
+    g = lo - 1;
+    gamma[lane] = g;
+    if (status) status[lane] = LSV_OK;
+  }
+  if (lane == 0 && total) *total = bestR;
+  if (row_offsets) {
+    int v = lane < batch ? g + 1 : 0;
+    for (int o = 1; o < kWave; o <<= 1) {
+      const int t = __shfl_up(v, o, kWave);
+      if (lane >= o) v += t;
+    }
+    if (lane < batch) row_offsets[lane + 1] = v;
+    if (lane == 0) row_offsets[0] = 0;
+  }
+}
+
+int launch_select_joint(int batch, int G, const float* conf, const double* cost, int d_max, unsigned flags,
+                        int32_t* gamma, int32_t* total, int32_t* row_offsets, int32_t* status, hipStream_t stream) {
+  hipLaunchKernelGGL(select_joint_kernel, dim3(1), dim3(kJointThreads), 0, stream, batch, G, conf, cost, d_max, flags,
+                     gamma, total, row_offsets, status);
+  return hipGetLastError() == hipSuccess ? LSV_OK : LSV_ERR_HIP;
+}
+
 // Baseline length policy of the comparison experiments (Sec. 4.1; Appendix B, baseline
 // details): the length rises by two after a round without a rejection and falls by one after a
 // round with one, kept in [d_min, d_max].  Lane b of the single wave takes sequence b + 64 k;

@@ -22,7 +22,7 @@ LSV_SEL_BONUS = 1
 EXPORTED = (
     "lsv_status_string", "lsv_last_error", "lsv_abi_version", "lsv_packed_model_bytes", "lsv_pack_globals",
     "lsv_pack_layer", "lsv_kv_cache_bytes", "lsv_verify_workspace_bytes", "lsv_workspace_clear",
-    "lsv_verify_block", "lsv_accept_workspace_bytes", "lsv_accept", "lsv_select_length", "lsv_next_length_g4", "lsv_pack_block", "lsv_next_roots",
+    "lsv_verify_block", "lsv_accept_workspace_bytes", "lsv_accept", "lsv_select_length", "lsv_select_joint", "lsv_next_length_g4", "lsv_pack_block", "lsv_next_roots",
     "lsv_set_timing_events",
 )
 LSV_KERNEL_QKV, LSV_KERNEL_O, LSV_KERNEL_GATEUP, LSV_KERNEL_DOWN, LSV_KERNEL_LMHEAD, LSV_KERNEL_ATTENTION = range(6)
@@ -76,6 +76,7 @@ def load(path=LIB_PATH):
         "lsv_accept_workspace_bytes": (SZ, [I32, I32, I32]),
         "lsv_accept": (ctypes.c_int, [I32, I32, I32, P, P, I32, I32, P, P, F32, U64, U64, P, P, P, P, P, SZ, P]),
         "lsv_select_length": (ctypes.c_int, [I32, I32, I32, P, P, I32, I32, F64, I32, U32, P, P, P, P, P]),
+        "lsv_select_joint": (ctypes.c_int, [I32, I32, P, P, I32, U32, P, P, P, P, P]),
         "lsv_next_length_g4": (ctypes.c_int, [I32, P, P, P, I32, I32, P, P, P, P]),
         "lsv_pack_block": (ctypes.c_int, [I32, I32, P, I32, P, P, P, P, P]),
         "lsv_next_roots": (ctypes.c_int, [I32, P, P, I32, P, P, P]),
@@ -171,6 +172,11 @@ def lsv_select_length(mode, batch, G, conf, cost, d_init, d_max, alpha, block_n,
                       status, stream=None):
     _check(load().lsv_select_length(mode, batch, G, _ptr(conf), _ptr(cost), d_init, d_max, alpha, block_n, flags,
                                     _ptr(gamma), _ptr(aux), _ptr(row_offsets), _ptr(status), _stream(stream)))
+
+
+def lsv_select_joint(batch, G, conf, cost, d_max, flags, gamma, total, row_offsets, status, stream=None):
+    _check(load().lsv_select_joint(batch, G, _ptr(conf), _ptr(cost), d_max, flags, _ptr(gamma), _ptr(total),
+                                   _ptr(row_offsets), _ptr(status), _stream(stream)))
 
 
 def lsv_next_length_g4(batch, gamma, accept_len, status, d_min, d_max, gamma_next, row_offsets, err, stream=None):

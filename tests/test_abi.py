@@ -84,6 +84,12 @@ def test_host_validation(lib):
     expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_select_length, 2, 1, 4, 1, None, 1, 4, 2.0, 0, 0, 1, None, None, None, S)
     expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_select_length, 1, 1, 4, 1, 1, 1, 4, 2.0, 2, 4, 1, None, None, None, S)
     expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_select_length, 1, 65, 4, 1, 1, 1, 4, 2.0, 2, 0, 1, None, 1, None, S)
+    # joint selection: batch, G, d_max, flags, required pointers
+    expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_select_joint, 65, 4, 1, 1, 4, 0, 1, None, None, None, S)
+    expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_select_joint, 2, 65, 1, 1, 4, 0, 1, None, None, None, S)
+    expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_select_joint, 2, 4, 1, 1, 5, 0, 1, None, None, None, S)
+    expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_select_joint, 2, 4, 1, 1, 4, 2, 1, None, None, None, S)
+    expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_select_joint, 2, 4, 1, None, 4, 0, 1, None, None, None, S)
     # baseline length policy: batch, bounds, required pointers, row offsets past LSV_MAX_BATCH
     g4 = [1, 1, 1, None, 1, 16, 1, None, None, S]
     expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_next_length_g4, *([0] + g4[1:]))

@@ -105,3 +105,53 @@ def test_selector_paper_hyperparameters():
         g, aux, st = gpu_select(S.SEL_ALG1, conf, None, 1, d_max, alpha, n, 0)
         want = S.select_batch(S.SEL_ALG1, conf, None, 1, d_max, alpha, n)
         assert list(g) == want[0] and list(aux) == want[1]
+
+
+def gpu_joint(conf, cost, d_max, flags):
+    B, G = conf.shape
+    c = torch.tensor(conf, dtype=torch.float32, device="cuda")
+    co = torch.tensor(cost, dtype=torch.float64, device="cuda")
+    g = torch.full((B,), -7, dtype=torch.int32, device="cuda")
+    tot = torch.full((1,), -7, dtype=torch.int32, device="cuda")
+    ro = torch.full((B + 1,), -7, dtype=torch.int32, device="cuda")
+    st = torch.full((B,), 99, dtype=torch.int32, device="cuda")
+    lsv.lsv_select_joint(B, G, c, co, d_max, flags, g, tot, ro, st)
+    torch.cuda.synchronize()
+    return g.cpu().numpy(), int(tot.cpu()[0]), ro.cpu().numpy(), st.cpu().numpy()
+
+
+@pytest.mark.parametrize("B,G", [(1, 16), (3, 5), (8, 16), (17, 33), (64, 64)])
+def test_joint_selector_parity(B, G):
+    """Joint batched selection vs the oracle, bit for bit: gamma, the total and the row layout."""
+    rng = np.random.default_rng(B * 100 + G)
+    for trial in range(4):
+        conf = random_conf(rng, B, G)
+        d_max = G if trial % 2 == 0 else int(rng.integers(1, G + 1))
+        R = np.arange(B * d_max + 1)
+        base, slope = rng.uniform(0.5, 2.0), rng.uniform(0.0, 0.05)
+        cost = base + slope * R + np.where(R > B * d_max * rng.uniform(0.3, 0.9), rng.uniform(0, 1), 0.0)
+        if trial == 3:
+            cost = base + slope * np.sqrt(R)  # concave: many drafts in total
+        flags = S.FLAG_BONUS if trial % 2 else 0
+        g, tot, ro, st = gpu_joint(conf, cost, d_max, flags)
+        want_g, want_R = S.select_joint(conf, cost, d_max, bool(flags))
+        assert g.tolist() == want_g and tot == want_R and np.all(st == 0)
+        assert ro.tolist() == [0] + list(np.cumsum(np.array(want_g) + 1))
+    note(f"  joint B={B} G={G}: 4 cases bit-exact (last total {tot})")
+
+
+def test_joint_selector_rejects_bad_input():
+    conf = np.full((3, 4), 0.5, np.float32)
+    conf[1, 2] = np.nan
+    cost = np.ones(3 * 4 + 1)
+    g, tot, ro, st = gpu_joint(conf, cost, 4, 0)
+    assert g.tolist() == [0, 0, 0] and tot == 0 and np.all(st == lsv.LSV_ERR_INVALID_ARG)
+    assert ro.tolist() == [0, 1, 2, 3]
+    conf[1, 2] = 0.5
+    cost[7] = 0.0  # a needed entry (R in [3, 12])
+    g, tot, ro, st = gpu_joint(conf, cost, 4, 0)
+    assert np.all(st == lsv.LSV_ERR_INVALID_ARG)
+    cost[7] = 1.0
+    cost[1] = np.nan  # below the smallest total: never read
+    g, tot, ro, st = gpu_joint(conf, cost, 4, 0)
+    assert np.all(st == 0) and tot == 12
