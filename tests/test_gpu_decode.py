@@ -117,3 +117,47 @@ def test_loop_is_lossless_fp32(policy, gamma0):
         assert got[b][:N] == conts[b], (b, got[b][:N], conts[b])
         assert int(loop.seq_len[b]) == contexts[b] + len(got[b])
     note(f"  {policy} (gamma0 {gamma0}): {N} tokens per sequence in {rounds} rounds, identical to greedy decoding")
+
+
+def test_bf16_loop_streams_agree_for_every_length():
+    """bf16, hd 128 (the eight-wave attention under a 17-row bound): plain decoding (static 0)
+    gives the greedy stream; static 16 (17-row blocks), the marginal rule and the G4-style
+    rule, fed drafts planted from that stream, must emit it token for token -- a row's
+    logits do not depend on the block it is verified in."""
+    m, G, seed, n = configs.SMALL_BF16, 16, 71, 48
+    contexts = [130, 200]
+    B = len(contexts)
+    w = gen.model_weights(m, seed)
+    cfg = runtime.model_config(m)
+    dm = runtime.DeviceModel.from_weights(cfg, w)
+    cap = runtime.kv_capacity(max(contexts) + 2 * n * (G + 1) + G + 2)
+    kv = runtime.KVCache(cfg, B, cap)
+    for b, C in enumerate(contexts):
+        for l in range(m.n_layers):
+            k, v = gen.synthetic_kv(m, seed + 31 * b, l, 1, C)
+            kv.write(l, b, 0, runtime.to_device(k[0]), runtime.to_device(v[0]))
+    roots = [int(x) for x in gen.randint(seed, 7, B, m.vocab)]
+
+    def run(policy, gamma0, dr, cost=None):
+        loop = decode.DecodeLoop(cfg, dm, kv, cap, B, G, policy, dr, cost=cost, gamma0=gamma0)
+        loop.reset(contexts, roots)
+        loop.round()
+        got = [list(e) for e in loop.emitted()]
+        loop.capture()
+        while min(len(g) for g in got) < n:
+            loop.replay()
+            for b, e in enumerate(loop.emitted()):
+                got[b] += e
+        assert bool((loop.status == 0).all())
+        return [g[:n] for g in got]
+
+    plain = run("static", 0, None)
+    stream = np.zeros((B, cap), np.int64)
+    for b, C in enumerate(contexts):
+        stream[b, C] = roots[b]
+        stream[b, C + 1:C + 1 + n] = plain[b]
+    dr = drafter.PlantedDrafter(stream, drafter.confidences(seed, B, cap), seed, m.vocab, G)
+    cost = np.array([0.0] + [1.0 + 0.02 * d for d in range(1, G + 1)])
+    for policy, g0 in (("static", 16), ("marginal", None), ("g4", 8)):
+        assert run(policy, g0, dr, cost) == plain, policy
+    note(f"  small bf16: {n} tokens per sequence identical for static 0 / 16, marginal and G4-style")
