@@ -9,6 +9,10 @@
  *      giving the target distribution at every drafted position (Sec. 3.1);
  *   3. lsv_accept         -- compare draft and target, keep the accepted prefix
  *      and emit one corrected or bonus token (Sec. 3.1).
+ * Around them: lsv_select_joint (one length allocation for a whole batch),
+ * lsv_next_length_g4 (the G4-style baseline rule of the comparison experiments),
+ * and lsv_pack_block / lsv_next_roots, which carry tokens from one round to the
+ * next on the device.
  *
  * Conventions for every entry point
  *   - All buffers are caller-owned.  "d_" arguments are device pointers, all
