@@ -471,7 +471,7 @@ def decode_loop_measure(m, cfg, dm, B, G, ctx, prompts, pre, rows_buf, roots, co
     cost_d = torch.tensor(cost, dtype=torch.float64, device=dev)
     g_ex = torch.zeros(B, dtype=torch.int32, device=dev)
 
-    def streams(loop, n, mad=None):
+    def streams(loop, n, mad=None, blocks=None):
         """Replay round by round until every sequence emitted n tokens; with mad (a list), also
         append |gamma - gamma_exhaustive| per sequence and round, the exhaustive length taken on
         the round's own confidences and the measured cost table."""
@@ -483,6 +483,8 @@ def decode_loop_measure(m, cfg, dm, B, G, ctx, prompts, pre, rows_buf, roots, co
                 lsv.lsv_select_length(lsv.LSV_SEL_EXHAUSTIVE, B, G, loop.conf, cost_d, 1, G, 0.0, 1, 0, g_ex, None,
                                       None, None)
                 mad += [abs(a - e) for a, e in zip(loop.gamma.cpu().tolist(), g_ex.cpu().tolist())]
+            if blocks is not None:
+                blocks += loop.aux.cpu().tolist()
             for b, e in enumerate(loop.emitted()):
                 got[b] += e
         return got
@@ -513,14 +515,16 @@ def decode_loop_measure(m, cfg, dm, B, G, ctx, prompts, pre, rows_buf, roots, co
         loop.round()
         loop.capture()
         ms, toks = timed(loop)
-        mad = []
-        got = streams(loop, n_rounds, mad)  # the emitted stream of n_rounds tokens or more per sequence
+        mad, blocks = [], ([] if pol == "alg1" else None)
+        got = streams(loop, n_rounds, mad, blocks)  # the emitted stream of n_rounds tokens or more per sequence
         n_cmp = min(min(len(g) for g in got), n_tok)
         same = all(got[b][:n_cmp] == greedy[b][:n_cmp] for b in range(B))
         name = {"static": f"static{g0}", "alg1": f"alg1_alpha{alpha}"}.get(pol, pol)
         out["policies"][name] = {"tokens_per_round": toks / (n_rounds * B), "ms_per_round": ms / n_rounds,
                                  "tokens_per_s": toks / (ms * 1e-3), "speedup_vs_plain": toks / (ms * 1e-3) / base_tps,
                                  "mad_vs_exhaustive": statistics.mean(mad), "stream_equals_plain": same}
+        if blocks:  # drafter blocks of n = 8 that Algorithm 1 asked for per sequence and round
+            out["policies"][name]["blocks_per_round"] = statistics.mean(blocks)
         del loop
     return out
 
