@@ -13,7 +13,8 @@ Beta(8, 2) * 0.92^i.
 
 Prints one JSON line (rank 0).  `value` = verified tokens per second
 (batch * (gamma + 1) / step time); the per-gamma latency sweep is in `sweep`.
-With --rounds R the line also carries `decode_loop`: R rounds of multi-round decoding per
+With --rounds R (default 0: off, so profiles of the step see only its kernels) the line also
+carries `decode_loop`: R rounds of multi-round decoding per
 length policy (static lengths, the marginal rule, Algorithm 1, the G4-style rule) fed by a
 planted calibrated drafter, as tokens per second against plain greedy decoding.
 """
@@ -857,8 +858,12 @@ def main():
                                        "hbm_frac": sb_g / t_g / 1e9 / HBM_PEAK_GBPS}
     if args.rounds > 0:
         log(f"decode loop: {args.rounds} rounds per length policy")
-        result["decode_loop"] = decode_loop_measure(m, cfg, dm, B, G, ctx, prompts, pre, rows_buf, roots, cost, seed,
-                                                    args.rounds, dev)
+        try:
+            result["decode_loop"] = decode_loop_measure(m, cfg, dm, B, G, ctx, prompts, pre, rows_buf, roots, cost,
+                                                        seed, args.rounds, dev)
+        except Exception as e:  # reported in the line; the verify-step measurement above stands
+            log(f"decode loop failed: {e!r}")
+            result["decode_loop"] = {"error": repr(e)}
     if not args.no_cpu_baseline and B == 1:
         log("cpu baseline: timing the oracle on a bounded sample")
         result["cpu_baseline"] = cpu_baseline(m, seed, ctx[0], rows, [roots[0]] + list(drafts[0]), g_star[0])
