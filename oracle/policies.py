@@ -7,6 +7,10 @@ prediction adapted to the diffusion drafter ("G4-style"): after a round in which
 every drafted token was accepted the next round drafts two more, after a round
 with at least one rejection one fewer.
 
+The paper prints no trajectory of the rule, so it is parity unpinned by a printed example;
+the tests pin it by the closed forms of the stated rule's trajectories and by its link to the
+acceptance oracle's count of accepted drafts.
+
 Readings where the paper is silent (each listed in the design notes):
 * "every drafted token accepted" means a == gamma, where a counts the accepted
   drafts (the bonus token is not a draft); a round of gamma = 0 has no rejection;
