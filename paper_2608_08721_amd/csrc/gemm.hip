@@ -222,10 +222,17 @@ LSV_DEV void qkv_store4(const GemmArgs& a, int m, int n0, const f32x4_t v, int b
             (size_t)pos * a.hd;
     }
     GLOBAL T* gd = GL(dst);
-    gd[i0] = from_f32<T>(out[0]);
-    gd[i0 + a.hd / 2] = from_f32<T>(out[1]);
-    gd[i0 + 1] = from_f32<T>(out[2]);
-    gd[i0 + 1 + a.hd / 2] = from_f32<T>(out[3]);
+    if constexpr (sizeof(T) == 2) {
+      // dims (i0, i0+1) and (i0+hd/2, i0+1+hd/2) are adjacent pairs (i0 and hd/2 are even):
+      // two 4-byte stores instead of four 2-byte ones
+      *(GLOBAL uint32_t*)(gd + i0) = (uint32_t)f2bf(out[0]) | ((uint32_t)f2bf(out[2]) << 16);
+      *(GLOBAL uint32_t*)(gd + i0 + a.hd / 2) = (uint32_t)f2bf(out[1]) | ((uint32_t)f2bf(out[3]) << 16);
+    } else {
+      gd[i0] = from_f32<T>(out[0]);
+      gd[i0 + a.hd / 2] = from_f32<T>(out[1]);
+      gd[i0 + 1] = from_f32<T>(out[2]);
+      gd[i0 + 1 + a.hd / 2] = from_f32<T>(out[3]);
+    }
   } else {
     if (pos < 0 || pos >= a.capacity) return;
     // V rows are stored transposed: [head_dim][capacity], column v_column(pos)
