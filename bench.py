@@ -429,7 +429,7 @@ def cpu_baseline(m, seed, C, rows, tokens, gamma):
             "seconds_per_step": t_step}
 
 
-def decode_loop_measure(m, cfg, dm, B, G, ctx, prompts, pre, rows_buf, roots, cost, seed, n_rounds, dev):
+def decode_loop_measure(m, cfg, dm, B, G, ctx, prompts, pre, rows_buf, roots, cost, cost_total, seed, n_rounds, dev):
     """Multi-round decoding (select or a baseline policy -> pack -> verify -> accept -> next
     roots, one graph per round) on its own cache with room for the rounds, fed by the planted
     calibrated drafter: realized tokens per second for each length policy, against plain greedy
@@ -508,10 +508,12 @@ def decode_loop_measure(m, cfg, dm, B, G, ctx, prompts, pre, rows_buf, roots, co
            "plain_decoding": {"tokens_per_s": base_tps, "ms_per_token": ms_plain / max(tok_plain, 1)},
            "policies": {}}
     policies = [("static", g, None) for g in (2, 4, 8, G)] + [("marginal", None, None), ("g4", 8, None)]
+    if B > 1:
+        policies.append(("joint", None, None))
     policies += [("alg1", None, a) for a in (1.8, 2.0, 2.2, 2.6)]  # the trade-off sweep
     for pol, g0, alpha in policies:
-        loop = decode.DecodeLoop(cfg, dm, kv2, cap2, B, G, pol, dr, cost=cost, block_n=8, gamma0=g0,
-                                 alpha=alpha or 2.2)
+        loop = decode.DecodeLoop(cfg, dm, kv2, cap2, B, G, pol, dr, cost=cost_total if pol == "joint" else cost,
+                                 block_n=8, gamma0=g0, alpha=alpha or 2.2)
         loop.reset(ctx, roots)
         loop.round()
         loop.capture()
@@ -860,7 +862,7 @@ def main():
         log(f"decode loop: {args.rounds} rounds per length policy")
         try:
             result["decode_loop"] = decode_loop_measure(m, cfg, dm, B, G, ctx, prompts, pre, rows_buf, roots, cost,
-                                                        seed, args.rounds, dev)
+                                                        cost_j, seed, args.rounds, dev)
         except Exception as e:  # reported in the line; the verify-step measurement above stands
             log(f"decode loop failed: {e!r}")
             result["decode_loop"] = {"error": repr(e)}

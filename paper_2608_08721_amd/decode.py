@@ -2,18 +2,20 @@
 selection, and the baseline policies of Sec. 4.1 / Appendix B).
 
 A round is, on one stream and without a host round trip:
-  drafter -> length (lsv_select_length | lsv_next_length_g4 | a static length)
+  drafter -> length (lsv_select_length | lsv_select_joint | lsv_next_length_g4 | a static length)
           -> lsv_pack_block -> lsv_verify_block -> lsv_accept (greedy, commits seq_len)
           -> lsv_next_roots.
 The drafter is the caller's: a callable (seq_len, drafts, conf) that fills the round's
-drafts [B, G] and confidences [B, G] on the device.  ``capture()`` records one round in a
+drafts [B, G] and confidences [B, G] on the device.  ``cost`` is indexed by gamma (cost[0]
+unused) for the per-sequence rules, and by the batch's total drafts (B * G + 1 entries) for
+the joint rule.  ``capture()`` records one round in a
 graph; ``replay()`` runs it.  This module only marshals buffers: every step runs in the
 library's kernels."""
 import torch
 
 from . import lsv, runtime
 
-POLICIES = ("marginal", "exhaustive", "alg1", "g4", "static")
+POLICIES = ("marginal", "exhaustive", "alg1", "joint", "g4", "static")
 
 
 class DecodeLoop:
@@ -21,8 +23,8 @@ class DecodeLoop:
                  d_min=1, gamma0=None, max_ctx=None, device="cuda"):
         if policy not in POLICIES:
             raise ValueError(f"policy must be one of {POLICIES}")
-        if policy in ("marginal", "exhaustive") and cost is None:
-            raise ValueError("the marginal and exhaustive rules need a cost table")
+        if policy in ("marginal", "exhaustive", "joint") and cost is None:
+            raise ValueError("the marginal, exhaustive and joint rules need a cost table")
         B = batch
         self.cfg, self.dm, self.kv, self.cap, self.B, self.G = cfg, dm, kv, capacity, B, G
         self.policy, self.drafter, self.alpha, self.block_n, self.d_min = policy, drafter, alpha, block_n, d_min
@@ -72,6 +74,8 @@ class DecodeLoop:
                     "alg1": lsv.LSV_SEL_ALG1}[self.policy]
             lsv.lsv_select_length(mode, B, G, self.conf, self.cost, 1, G, self.alpha, self.block_n, 0, self.gamma,
                                   self.aux, self.row_off, self.status)
+        elif self.policy == "joint":
+            lsv.lsv_select_joint(B, G, self.conf, self.cost, G, 0, self.gamma, None, self.row_off, self.status)
         elif self.policy == "g4":
             lsv.lsv_next_length_g4(B, self.gamma, self.acc, self.status, self.d_min, G, self.gamma, self.row_off,
                                    None)
