@@ -121,8 +121,8 @@ def test_loop_is_lossless_fp32(policy, gamma0):
 
 def test_bf16_loop_streams_agree_for_every_length():
     """bf16, hd 128 (the eight-wave attention under a 17-row bound): plain decoding (static 0)
-    gives the greedy stream; static 16 (17-row blocks), the marginal rule and the G4-style
-    rule, fed drafts planted from that stream, must emit it token for token -- a row's
+    gives the greedy stream; static 16 (17-row blocks), the marginal rule, the G4-style rule
+    and the joint rule, fed drafts planted from that stream, must emit it token for token -- a row's
     logits do not depend on the block it is verified in."""
     m, G, seed, n = configs.SMALL_BF16, 16, 71, 48
     contexts = [130, 200]
@@ -158,6 +158,7 @@ def test_bf16_loop_streams_agree_for_every_length():
         stream[b, C + 1:C + 1 + n] = plain[b]
     dr = drafter.PlantedDrafter(stream, drafter.confidences(seed, B, cap), seed, m.vocab, G)
     cost = np.array([0.0] + [1.0 + 0.02 * d for d in range(1, G + 1)])
-    for policy, g0 in (("static", 16), ("marginal", None), ("g4", 8)):
-        assert run(policy, g0, dr, cost) == plain, policy
-    note(f"  small bf16: {n} tokens per sequence identical for static 0 / 16, marginal and G4-style")
+    cost_total = np.array([1.0 + 0.01 * r for r in range(B * G + 1)])  # by the batch's total drafts
+    for policy, g0 in (("static", 16), ("marginal", None), ("g4", 8), ("joint", None)):
+        assert run(policy, g0, dr, cost_total if policy == "joint" else cost) == plain, policy
+    note(f"  small bf16: {n} tokens per sequence identical for static 0 / 16, marginal, G4-style and joint")
