@@ -8,24 +8,24 @@ this module writes out directly in fp64:
 
   h = E[tok]
   per layer:
-    q, k, v = N(h, g_attn) Wq^T, ... Wk^T, ... Wv^T      N(x, g) = x / sqrt(mean(x^2) + eps) * g
+    a = R(N(h, g_attn))                    N(x, g) = x / sqrt(mean(x^2) + eps) * g
+    q, k, v = a Wq^T, a Wk^T, a Wv^T
     q, k = rope(q, pos), rope(k, pos)      rotate-half pairs (i, i + hd/2),
                                            angle = pos * base^(-2i/hd)
     q, k, v = R(q), R(k), R(v);  cache[pos] <- k, v
     o = R(softmax(q K^T / sqrt(hd)) V)     keys 0..pos of the same sequence;
                                            query head h reads kv head h // (n_q / n_kv)
     h = h + o Wo^T
-    u = R(silu(N(h, g_ffn) Wg^T) * (N(h, g_ffn) Wu^T));  h = h + u Wd^T
-  logits = N(h, g_final) Wlm^T
+    a = R(N(h, g_ffn));  u = R(silu(a Wg^T) * (a Wu^T));  h = h + u Wd^T
+  logits = R(N(h, g_final)) Wlm^T
 
 R() is the identity for fp32 models.  For bf16 models it rounds to bf16
-(fp64 -> fp32 -> bf16, nearest-even both times) where the GPU stores bf16
-operands, and a normalised projection N(h, g) W^T is formed as the identical
-product  inv_rms(h) * (R(h) R(W * g)^T):  the norm's per-row scale commutes with
-the projection, the residual h is stored once in bf16, and the gain is folded
-into the weights in storage precision.  inv_rms uses the unrounded h.  The
-residual stream h and the logits stay wide.  Weights arrive in their storage
-type (bf16 values are exact in fp64).
+(fp64 -> fp32 -> bf16, nearest-even both times) at the points where a bf16 model
+stores a matrix operand: the normalised activations, q, k, v, the attention output
+and the SwiGLU output.  Everything else -- the residual stream h, every product and
+the logits -- stays in fp64.  Weights arrive in their storage type (bf16 values are
+exact in fp64).  This is the plain definition of the model; how a kernel schedules
+the norm (for example folding the gain into the weights) is not mirrored here.
 
 Row layout: ``tokens`` holds, per sequence b, rows row_offsets[b]..row_offsets[b+1]-1
 at positions seq_len[b] + (row - row_offsets[b]); the block's K/V overwrite those
@@ -97,29 +97,21 @@ class Model:
     def R(self, x):
         return round_bf16(x) if self.dtype == "bf16" else x
 
-    def linear(self, x, key, layer=None, gain=None):
-        """x @ (W o gain)^T, the folded weights rounded by R().  Large matrices are
-        converted in slices of output rows; every output element is still one full
-        dot product."""
+    def linear(self, x, key, layer=None):
+        """x @ W^T.  Large matrices are converted to fp64 in slices of output rows; every
+        output element is still one full dot product."""
         src = self.w["layers"][layer][key] if layer is not None else self.w[key]
-        n_out = src.shape[0]
-
-        def weights(rows):
-            w = stored_to_f64(rows, self.dtype)
-            return w if gain is None else self.R(w * gain[None, :])
         if src.size <= (1 << 24):
-            w = self.f64(key, layer) if gain is None else self.R(self.f64(key, layer) * gain[None, :])
-            return x @ w.T
-        out = np.empty((x.shape[0], n_out))
+            return x @ self.f64(key, layer).T
+        out = np.empty((x.shape[0], src.shape[0]))
         step = max(1, (1 << 23) // src.shape[1])
-        for s in range(0, n_out, step):
-            out[:, s:s + step] = x @ weights(src[s:s + step]).T
+        for s in range(0, src.shape[0], step):
+            out[:, s:s + step] = x @ stored_to_f64(src[s:s + step], self.dtype).T
         return out
 
-    def normed_linear(self, h, gain, key, layer=None):
-        """N(h, gain) W^T = inv_rms(h) * (R(h) @ R(W o gain)^T)  (see the module docstring)."""
-        inv = 1.0 / np.sqrt(np.mean(h * h, axis=-1, keepdims=True) + self.m.rms_eps)
-        return inv * self.linear(self.R(h), key, layer, gain=gain)
+    def normed(self, h, gain):
+        """R(N(h, gain)): the normalised activation a projection consumes."""
+        return self.R(rmsnorm(h, gain, self.m.rms_eps))
 
 
 class KVCache:
@@ -160,10 +152,10 @@ def verify_block(model, cache, seq_len, tokens, row_offsets, collect_hidden=Fals
             h[r] = stored_to_f64(emb[tokens[r]], model.dtype)
     hidden = []
     for l in range(model.n_layers):
-        g_attn = model.f64("attn_norm", l)
-        q = model.normed_linear(h, g_attn, "wq", l).reshape(M, nq, hd)
-        k = model.normed_linear(h, g_attn, "wk", l).reshape(M, nkv, hd)
-        v = model.normed_linear(h, g_attn, "wv", l).reshape(M, nkv, hd)
+        a = model.normed(h, model.f64("attn_norm", l))
+        q = model.linear(a, "wq", l).reshape(M, nq, hd)
+        k = model.linear(a, "wk", l).reshape(M, nkv, hd)
+        v = model.linear(a, "wv", l).reshape(M, nkv, hd)
         q = model.R(rope(q, pos, m.rope_base))
         k = model.R(rope(k, pos, m.rope_base))
         v = model.R(v)
@@ -189,12 +181,12 @@ def verify_block(model, cache, seq_len, tokens, row_offsets, collect_hidden=Fals
                 o[r, hq] = p @ Vv
         o = model.R(o)
         h = h + model.linear(o.reshape(M, nq * hd), "wo", l)
-        g_ffn = model.f64("ffn_norm", l)
-        u = model.R(silu(model.normed_linear(h, g_ffn, "wg", l)) * model.normed_linear(h, g_ffn, "wu", l))
+        a = model.normed(h, model.f64("ffn_norm", l))
+        u = model.R(silu(model.linear(a, "wg", l)) * model.linear(a, "wu", l))
         h = h + model.linear(u, "wd", l)
         if collect_hidden:
             hidden.append(h.copy())
-    logits = model.normed_linear(h, stored_to_f64(model.w["final_norm"], model.dtype), "lm_head")
+    logits = model.linear(model.normed(h, stored_to_f64(model.w["final_norm"], model.dtype)), "lm_head")
     if collect_hidden:
         return logits, status, hidden
     return logits, status

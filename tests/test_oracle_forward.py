@@ -130,15 +130,3 @@ def test_status_capacity_and_bad_token(synth_built):
     _, st = F.verify_block(om, cache, [6, 0], [1, 2, 3, 4, shape.vocab], [0, 3, 5])
     assert list(st) == [F.LSV_ERR_CAPACITY, F.LSV_ERR_INVALID_ARG]
     assert np.all(cache.k[0] == 0)
-
-
-def test_norm_scale_commutes_with_projection(synth_built):
-    """N(h, g) W^T == inv_rms(h) * (h (W o g)^T) without storage rounding (fp32 model)."""
-    shape = configs.TINY_F32
-    w = nonunit_norms(gen.model_weights(shape, 8), shape, 8)
-    om = F.Model(shape, w)
-    h = np.random.default_rng(0).normal(size=(5, shape.d_model))
-    g = F.stored_to_f64(w["layers"][0]["attn_norm"], "f32")
-    want = F.rmsnorm(h, g, shape.rms_eps) @ F.stored_to_f64(w["layers"][0]["wq"], "f32").T
-    got = om.normed_linear(h, g, "wq", 0)
-    assert np.abs(got - want).max() <= 1e-12 * np.abs(want).max()
