@@ -207,11 +207,15 @@ int lsv_verify_block(const lsv_model_config* cfg, const void* d_packed, void* d_
  *   d_out_tokens       [batch, max_rows_per_seq] out: emitted tokens, then -1
  *   d_seq_len          [batch] in/out, nullable: if given, d_seq_len[b] += a_b + 1
  *                      (root and accepted drafts stay cached) for sequences with status OK
- *   d_status           [batch] out (nullable): LSV_OK; LSV_ERR_NONFINITE (a non-finite
- *                      logit in the sequence's rows, or a non-finite draft probability read);
- *                      LSV_ERR_INVALID_ARG if the sequence has no rows or more than
- *                      max_rows_per_seq (sampling: then every sequence of the batch), or
- *                      the rows run past max_rows
+ *   d_status           [batch] in/out (nullable).  In: a sequence whose d_status[b] is not
+ *                      LSV_OK (e.g. lsv_verify_block's LSV_ERR_CAPACITY for this block) is
+ *                      skipped: accept_len 0, out_tokens all -1, no commit, status kept.
+ *                      Pass the verify call's status array, or one set to LSV_OK.
+ *                      Out: LSV_OK; LSV_ERR_NONFINITE (a non-finite logit in the sequence's
+ *                      rows, or a non-finite draft probability read); LSV_ERR_INVALID_ARG if
+ *                      the sequence has no rows or more than max_rows_per_seq (sampling: then
+ *                      every sequence of the batch that arrived OK), or the rows run past
+ *                      max_rows
  *   d_workspace        lsv_accept_workspace_bytes(batch, max_rows, vocab) bytes */
 enum { LSV_ACC_GREEDY = 0, LSV_ACC_SAMPLE = 1 };
 enum { LSV_MAX_SEQ_ROWS = 64 };
@@ -234,11 +238,13 @@ int lsv_accept(int32_t mode, int32_t batch, int32_t vocab, const float* d_logits
  *   adjustments (Def. 3.1): d += 1 while f(d+1) > f(d), else d -= 1 while
  *   f(d-1) >= f(d).  By Thm. 3.5/3.6 this reaches the EXHAUSTIVE answer when the
  *   cost table is convex.  aux = number of steps.
- * LSV_SEL_ALG1: Algorithm 1 with block size n = block_n and trade-off alpha:
- *   d = min(n, d_max), B = 0; while d < d_max: eps* = min_{i<=d} floor(alpha * S_i + i),
- *   S_i = sum_{j=i}^{d} prod_{k=i}^{j} q_k; if eps* <= d { d = eps*; stop }
- *   eps* = min(eps*, d_max); B -= eps* - d; d = eps*; if B < 0 request
- *   ceil(-B/n) more blocks and add them to B.  cost is not read.  aux = blocks used.
+ * LSV_SEL_ALG1: Algorithm 1 with block size n = block_n and trade-off alpha.  With
+ *   eps*(d) = min_{i<=d} floor(alpha * S_i + i), S_i = sum_{j=i}^{d} prod_{k=i}^{j} q_k
+ *   (the position-wise bounds of Thm. 3.3 over the current length d), the length starts
+ *   at min(n, d_max), climbs to min(eps*(d), d_max) while eps*(d) > d, and settles on
+ *   eps*(d) at the first d where eps*(d) <= d (the single rollback); d_max also stops it.
+ *   cost is not read.  aux = drafter blocks of n used: ceil(d_peak / n), d_peak the
+ *   highest length reached (Algorithm 1's budget of drafted but unused tokens).
  *
  *   d_conf   [batch, G] fp32 confidences in [0, 1]
  *   d_cost   [G+1] fp64 verification cost of each length, cost[0] unused; cost[d] > 0

@@ -22,9 +22,9 @@ Readings where the paper is silent (each listed in the design notes):
 * MARGINAL moves one position at a time: extend while f(d+1) > f(d) strictly
   (Def. 3.1 requires a strict gain), else contract while f(d-1) >= f(d);
 * ALG1 follows Algorithm 1: eps_i = floor(alpha * S_i + i) with S_i summed up to
-  the *current* d, eps* = min_i eps_i; stop with d = eps* at the first eps* <= d
-  (the single rollback); otherwise eps* is clamped to d_max, the budget B pays for
-  the extension and ceil(-B/n) new blocks are requested when B < 0.
+  the *current* d, eps* = min_i eps_i; the length climbs to min(eps*, d_max) while
+  eps* > d and settles on eps* at the first d where eps* <= d (the single rollback);
+  the blocks counted are those the drafter needs to cover the highest length reached.
 """
 import math
 
@@ -104,28 +104,34 @@ def eps_star(q, d, alpha):
 
 
 def select_alg1(q, d_max, alpha, n, trace=None):
-    """Algorithm 1 (LibraSpec).  q holds the confidences of all G drafted tokens;
-    d_max <= G.  Returns (d, blocks) where blocks counts drafter blocks of size n
-    (the initial one included).  ``trace`` (a list) receives (d, eps*, B) per
-    iteration."""
+    """Algorithm 1 (LibraSpec), restated.  q holds the confidences of all G drafted tokens;
+    d_max <= G.
+
+    eps*(d) = min_i eps_i over the positions of the current length d is the longest length
+    that every position-wise bound (Thm. 3.3) admits.  The length starts at the drafter's
+    block size n and climbs along d -> min(eps*(d), d_max) while that raises it; at the first
+    d where it does not, the length settles on eps*(d) itself -- the same length or a single
+    step back, after which the rule stops.  Reaching d_max also stops it.
+
+    The budget of Algorithm 1 counts drafted tokens not yet used: new blocks of n are drafted
+    only when an extension runs past what is drafted, so the drafter has produced
+    ceil(d_peak / n) blocks (at least one) when the highest length reached is d_peak, and the
+    budget at length d is (-d) mod n.
+
+    Returns (d, blocks).  ``trace`` (a list) receives (d, eps*(d), budget) for every
+    evaluation of eps*."""
     d = min(n, d_max)
-    B = 0
-    blocks = 1
-    while d < d_max:
+    settled = None
+    while settled is None and d < d_max:
         e = eps_star(q, d, alpha)
         if trace is not None:
-            trace.append((d, e, B))
-        if e <= d:
-            d = e
-            break
-        e = min(e, d_max)
-        B = B - (e - d)
-        d = e
-        if B < 0:
-            k = -(B // n)          # ceil(-B / n) for B < 0
-            blocks += k
-            B = B + k * n
-    return d, blocks
+            trace.append((d, e, (-d) % n))
+        if e > d:
+            d = min(e, d_max)      # climb
+        else:
+            settled = e            # stay, or one step back
+    blocks = max(1, -(-d // n))    # d is the highest length reached here
+    return (d if settled is None else settled), blocks
 
 
 def select(mode, q, cost, d_init, d_max, alpha, n, flags=0):

@@ -68,25 +68,18 @@ LSV_DEV int select_wave(int mode, int G, const float* __restrict__ conf, const d
   int d = 0, a = 0;
   if (ok) {
     if (mode == LSV_SEL_ALG1) {
+      // Algorithm 1: from the block size the length climbs along d -> min(eps*(d), d_max)
+      // while that raises it, and settles on eps*(d) (itself, or one step back) at the first d
+      // where it does not.  Blocks: enough drafter blocks of n to cover the highest length.
       d = block_n < d_max ? block_n : d_max;
-      long long B = 0;
-      int blocks = 1;
-      while (d < d_max) {
-        int e = eps_star_wave(q, d, alpha, lane);
-        if (e <= d) {  // single rollback, then stop
-          d = e;
-          break;
-        }
-        if (e > d_max) e = d_max;
-        B -= (long long)(e - d);
-        d = e;
-        if (B < 0) {
-          long long k = (-B + block_n - 1) / block_n;
-          blocks += (int)k;
-          B += k * block_n;
-        }
+      int settled = 0;  // eps* >= 1 always, so 0 means "still climbing"
+      while (settled == 0 && d < d_max) {
+        const int e = eps_star_wave(q, d, alpha, lane);
+        if (e > d) d = e < d_max ? e : d_max;
+        else settled = e;
       }
-      a = blocks;
+      a = (d + block_n - 1) / block_n;  // d >= 1 here, so at least one block
+      if (settled) d = settled;
     } else {
       const double f = objective_lane(q, cost, d_max, (flags & LSV_SEL_BONUS) != 0, lane);
       if (mode == LSV_SEL_EXHAUSTIVE) {
