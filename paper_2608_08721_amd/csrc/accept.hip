@@ -170,6 +170,13 @@ __global__ void __launch_bounds__(64) accept_greedy_kernel(const RowPartial* __r
                                                            const int32_t* tokens, int width, int32_t* accept_len,
                                                            int32_t* out_tokens, int32_t* seq_len, int32_t* status) {
   const int b = blockIdx.x, lane = threadIdx.x;
+  // a sequence that arrives with an error (e.g. the verify step's capacity check) is skipped:
+  // no tokens, accept_len 0, no commit, its status kept
+  if (status && status[b] != LSV_OK) {
+    if (lane < width) out_tokens[(size_t)b * width + lane] = -1;
+    if (lane == 0) accept_len[b] = 0;
+    return;
+  }
   const int r0 = row_offsets[b], r1 = row_offsets[b + 1];
   const bool in_bounds = r0 >= 0 && r1 >= r0 && r1 <= max_rows;
   const int rows = in_bounds ? r1 - r0 : 0, g = rows - 1;
@@ -231,8 +238,19 @@ __global__ void __launch_bounds__(64) accept_sample_decide_kernel(const RowParti
                                                                   const float* __restrict__ q, float temperature,
                                                                   const int32_t* row_offsets, int batch, int max_rows,
                                                                   int width, const int32_t* tokens, uint64_t seed,
-                                                                  uint64_t round, SeqDecision* dec) {
+                                                                  uint64_t round, const int32_t* status,
+                                                                  SeqDecision* dec) {
   const int b = blockIdx.x, lane = threadIdx.x;
+  // a sequence that arrives with an error keeps it: the race kernel then emits nothing for it
+  const int in_status = status ? status[b] : LSV_OK;
+  if (in_status != LSV_OK) {
+    if (lane == 0) {
+      SeqDecision d = {};
+      d.status = in_status;
+      dec[b] = d;
+    }
+    return;
+  }
   // draft rows are indexed row_offsets[b] - b + v - 1, which needs every sequence to own 1..width rows
   bool shape_bad = false;
   for (int bb = lane; bb < batch; bb += kWave) {
@@ -431,7 +449,7 @@ int launch_accept(int mode, int batch, int vocab, const float* logits, const int
                        temperature, w.rows);
     hipLaunchKernelGGL(accept_sample_decide_kernel, dim3(batch), dim3(64), 0, stream, w.rows, nc, logits, vocab,
                        draft_probs, temperature, row_offsets, batch, max_rows, max_rows_per_seq, tokens, seed, round,
-                       w.seq);
+                       status, w.seq);
     hipLaunchKernelGGL(accept_sample_race_kernel, dim3(nc, batch), dim3(256), 0, stream, logits, vocab, draft_probs,
                        temperature, row_offsets, tokens, seed, round, w.seq, w.race, w.counters, max_rows_per_seq,
                        accept_len, out_tokens, seq_len, status);

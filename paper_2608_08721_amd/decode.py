@@ -8,7 +8,9 @@ A round is, on one stream and without a host round trip:
 The drafter is the caller's: a callable (seq_len, drafts, conf) that fills the round's
 drafts [B, G] and confidences [B, G] on the device.  ``cost`` is indexed by gamma (cost[0]
 unused) for the per-sequence rules, and by the batch's total drafts (B * G + 1 entries) for
-the joint rule.  ``capture()`` records one round in a
+the joint rule.  The status array is shared by verify and accept: the acceptance skips a
+sequence whose verify step failed (for instance a block past ``max_ctx``), so nothing is
+committed for it and its root is kept.  ``capture()`` records one round in a
 graph; ``replay()`` runs it.  This module only marshals buffers: every step runs in the
 library's kernels."""
 import torch
@@ -25,6 +27,10 @@ class DecodeLoop:
             raise ValueError(f"policy must be one of {POLICIES}")
         if policy in ("marginal", "exhaustive", "joint") and cost is None:
             raise ValueError("the marginal, exhaustive and joint rules need a cost table")
+        if cost is not None and policy in ("marginal", "exhaustive", "joint"):
+            need = batch * G + 1 if policy == "joint" else G + 1
+            if len(cost) < need:
+                raise ValueError(f"the {policy} rule reads {need} cost entries (cost[0..{need - 1}]); got {len(cost)}")
         B = batch
         self.cfg, self.dm, self.kv, self.cap, self.B, self.G = cfg, dm, kv, capacity, B, G
         self.policy, self.drafter, self.alpha, self.block_n, self.d_min = policy, drafter, alpha, block_n, d_min

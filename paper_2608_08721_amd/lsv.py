@@ -107,6 +107,17 @@ def _stream(s):
     return s.cuda_stream
 
 
+def _need(t, name, n, dtype):
+    """Marshalling check of a tensor argument the kernels read n elements of: a device tensor
+    of the expected dtype and length (raw integer addresses are passed through unchecked)."""
+    if t is None or isinstance(t, int):
+        return
+    import torch
+    if t.device.type != "cuda" or t.dtype != dtype or t.numel() < n or not t.is_contiguous():
+        raise LsvError(LSV_ERR_INVALID_ARG, f"{name}: need a contiguous cuda {dtype} tensor of >= {n} elements, got "
+                                            f"{t.dtype} {tuple(t.shape)} on {t.device}")
+
+
 def _check(rc):
     if rc != LSV_OK:
         raise LsvError(rc, load().lsv_last_error().decode())
@@ -170,11 +181,18 @@ def lsv_accept(mode, batch, vocab, logits, row_offsets, max_rows, max_rows_per_s
 
 def lsv_select_length(mode, batch, G, conf, cost, d_init, d_max, alpha, block_n, flags, gamma, aux, row_offsets,
                       status, stream=None):
+    import torch
+    _need(conf, "conf", batch * G, torch.float32)
+    if mode != LSV_SEL_ALG1:
+        _need(cost, "cost", d_max + 1, torch.float64)
     _check(load().lsv_select_length(mode, batch, G, _ptr(conf), _ptr(cost), d_init, d_max, alpha, block_n, flags,
                                     _ptr(gamma), _ptr(aux), _ptr(row_offsets), _ptr(status), _stream(stream)))
 
 
 def lsv_select_joint(batch, G, conf, cost, d_max, flags, gamma, total, row_offsets, status, stream=None):
+    import torch
+    _need(conf, "conf", batch * G, torch.float32)
+    _need(cost, "cost", batch * d_max + 1, torch.float64)
     _check(load().lsv_select_joint(batch, G, _ptr(conf), _ptr(cost), d_max, flags, _ptr(gamma), _ptr(total),
                                    _ptr(row_offsets), _ptr(status), _stream(stream)))
 

@@ -17,7 +17,8 @@ _lib = None
 # Stream numbering (purpose -> stream id).
 S_EMBED, S_LM_HEAD = 1, 2
 S_PREFIX, S_DRAFT, S_CONF, S_CONTEXT, S_DRAFT_LOGITS, S_KV, S_PLANT, S_LOGITS = 10, 11, 12, 13, 14, 15, 17, 18
-LAYER_KINDS = {"wq": 1, "wk": 2, "wv": 3, "wo": 4, "wg": 5, "wu": 6, "wd": 7}
+LAYER_KINDS = {"wq": 1, "wk": 2, "wv": 3, "wo": 4, "wg": 5, "wu": 6, "wd": 7, "attn_norm": 8, "ffn_norm": 9}
+S_FINAL_NORM = 20
 
 
 def layer_stream(layer: int, kind: str) -> int:
@@ -108,16 +109,23 @@ def tensor_shapes(m):
     }
 
 
-def layer_weights(m, seed, layer):
+def _gain(m, seed, stream, gains):
+    """RMSNorm gain vector in the storage dtype: ones, or (gains="random") 0.5 + U(0, 1) per
+    column, so that tests see gains that differ from column to column."""
+    g = np.ones(m.d_model, np.float32) if gains == "ones" else (0.5 + uniform(seed, stream, m.d_model)).astype(np.float32)
+    return g if m.dtype == "f32" else f32_to_bf16(g)
+
+
+def layer_weights(m, seed, layer, gains="ones"):
     """Row-major [out_features, in_features] matrices (torch.nn.Linear layout) of one layer,
-    in the storage dtype (np.float32, or np.uint16 bf16 bits).  Norm gains are ones."""
+    in the storage dtype (np.float32, or np.uint16 bf16 bits), and its two norm gains."""
+    assert gains in ("ones", "random")
     out = {}
     for kind, shp in tensor_shapes(m).items():
         n = shp[0] * shp[1]
         out[kind] = normal(seed, layer_stream(layer, kind), n, m.init_std, m.dtype).reshape(shp)
-    one = np.ones(m.d_model, np.float32)
-    out["attn_norm"] = one if m.dtype == "f32" else f32_to_bf16(one)
-    out["ffn_norm"] = out["attn_norm"].copy()
+    out["attn_norm"] = _gain(m, seed, layer_stream(layer, "attn_norm"), gains)
+    out["ffn_norm"] = _gain(m, seed, layer_stream(layer, "ffn_norm"), gains)
     return out
 
 
@@ -129,17 +137,18 @@ def lm_head_weights(m, seed):
     return normal(seed, S_LM_HEAD, m.vocab * m.d_model, m.init_std, m.dtype).reshape(m.vocab, m.d_model)
 
 
-def final_norm_weights(m):
-    one = np.ones(m.d_model, np.float32)
-    return one if m.dtype == "f32" else f32_to_bf16(one)
+def final_norm_weights(m, seed=0, gains="ones"):
+    return _gain(m, seed, S_FINAL_NORM, gains)
 
 
-def model_weights(m, seed):
+def model_weights(m, seed, gains="ones"):
+    """Every tensor of a model.  gains: "ones" (the workloads) or "random" (tests of the
+    norm gains: 0.5 + U(0, 1) per column, seeded)."""
     return {
         "embed": embed_weights(m, seed),
-        "final_norm": final_norm_weights(m),
+        "final_norm": final_norm_weights(m, seed, gains),
         "lm_head": lm_head_weights(m, seed),
-        "layers": [layer_weights(m, seed, l) for l in range(m.n_layers)],
+        "layers": [layer_weights(m, seed, l, gains) for l in range(m.n_layers)],
     }
 
 

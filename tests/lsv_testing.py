@@ -69,3 +69,28 @@ def row_rel_err(got, want):
 def top2_margin(row):
     s = np.sort(row)
     return s[-1] - s[-2]
+
+
+def greedy_decisions(got, want, min_decided, label=""):
+    """Greedy decisions of GPU logits `got` against oracle logits `want`, row by row.
+
+    e_r = max_j |got_rj - want_rj| is row r's measured error.  Where the oracle's top-1 /
+    top-2 margin exceeds 2 e_r the row has a single argmax that any logits within e_r of
+    the oracle's share ("decided"): GPU and oracle must pick the same token.  Elsewhere
+    both picks are near-maximal: the GPU's pick must lie within 2 e_r of the oracle's
+    maximum.  At least `min_decided` of the rows must be decided.  Returns the decided
+    share."""
+    e = np.abs(got - want).max(axis=1)
+    am_g, am_o = got.argmax(axis=1), want.argmax(axis=1)
+    margin = np.array([top2_margin(r) for r in want])
+    decided = margin > 2 * e
+    bad = [r for r in np.flatnonzero(decided) if am_g[r] != am_o[r]]
+    assert not bad, f"argmax differs on decided rows {bad}"
+    rows = np.arange(len(want))
+    near = want.max(axis=1) - want[rows, am_g] <= 2 * e
+    assert near.all(), f"GPU picks far from the oracle's maximum on rows {np.flatnonzero(~near)}"
+    frac = float(decided.mean()) if len(decided) else 1.0
+    note(f"    {label}argmax equal on {int(decided.sum())}/{len(decided)} decided rows ({frac:.0%}); "
+         f"{int((am_g == am_o).sum())}/{len(am_o)} rows equal in all")
+    assert frac >= min_decided, (frac, min_decided)
+    return frac

@@ -16,7 +16,7 @@ from tests.lsv_testing import i32, note
 pytestmark = pytest.mark.gpu
 
 
-def gpu_accept(mode, logits, off, tokens, width, q=None, temperature=0.0, seed=0, rnd=0, seq_len=None):
+def gpu_accept(mode, logits, off, tokens, width, q=None, temperature=0.0, seed=0, rnd=0, seq_len=None, status_in=None):
     B = len(off) - 1
     M, V = logits.shape
     ws = runtime.Workspace(lsv.lsv_accept_workspace_bytes(B, M, V))
@@ -24,7 +24,7 @@ def gpu_accept(mode, logits, off, tokens, width, q=None, temperature=0.0, seed=0
     qq = torch.tensor(q, dtype=torch.float32, device="cuda") if q is not None else None
     acc = torch.full((B,), -9, dtype=torch.int32, device="cuda")
     out = torch.full((B, width), -9, dtype=torch.int32, device="cuda")
-    st = torch.full((B,), 99, dtype=torch.int32, device="cuda")
+    st = i32(status_in if status_in is not None else [0] * B)  # in/out: the incoming status
     sl = i32(seq_len) if seq_len is not None else None
     lsv.lsv_accept(mode, B, V, lg, i32(off), M, width, i32(tokens), qq, temperature, seed, rnd, acc, out, sl, st,
                    ws.buf, ws.nbytes)
@@ -149,3 +149,29 @@ def test_sampling_nonfinite_and_one_hot():
     logits[1, 5] = np.nan
     acc, out, st, _ = gpu_accept(lsv.LSV_ACC_SAMPLE, logits, [0, 4], tokens, 4, q, 1.0, 9, 9)
     assert st[0] == lsv.LSV_ERR_NONFINITE and acc[0] == 0 and list(out[0]) == [-1] * 4
+
+
+@pytest.mark.parametrize("mode", [lsv.LSV_ACC_GREEDY, lsv.LSV_ACC_SAMPLE])
+def test_incoming_error_status_skips_the_sequence(mode):
+    """A sequence that arrives with an error (as lsv_verify_block reports a block past the cache
+    capacity) emits nothing, accepts nothing, is not committed and keeps its status; the others
+    are decided as usual."""
+    rng = np.random.default_rng(77)
+    B, V, width = 3, 300, 6
+    rows = [4, 6, 2]
+    off = runtime.row_offsets_of(rows)
+    M = int(off[-1])
+    logits = rng.normal(size=(M, V)).astype(np.float32)
+    tokens = rng.integers(0, V, size=M).astype(np.int32)
+    q = None
+    if mode == lsv.LSV_ACC_SAMPLE:
+        q = rng.dirichlet(np.ones(V), size=M - B).astype(np.float32)
+    seq_len = [10, 20, 30]
+    args = dict(q=q, temperature=0.0 if q is None else 1.0, seed=5, rnd=3, seq_len=seq_len)
+    acc0, out0, st0, sl0 = gpu_accept(mode, logits, off, tokens, width, **args)
+    assert list(st0) == [0, 0, 0]
+    acc, out, st, sl = gpu_accept(mode, logits, off, tokens, width, status_in=[0, lsv.LSV_ERR_CAPACITY, 0], **args)
+    assert list(st) == [0, lsv.LSV_ERR_CAPACITY, 0]
+    assert acc[1] == 0 and np.all(out[1] == -1) and sl[1] == seq_len[1]
+    for b in (0, 2):
+        assert acc[b] == acc0[b] and np.array_equal(out[b], out0[b]) and sl[b] == sl0[b]

@@ -70,3 +70,12 @@ def test_llama70b_width_greedy_and_sampling():
     note("llama3-70b width, 1 layer, 4 x 33 rows, context 8192")
     gm, g_logits, o_logits, toks, off = _bf16_case(shape, 5, [8192] * 4, [33] * 4)
     _sampling_matches(g_logits, off, toks, 0.7, 505)
+
+
+def test_short_blocks_under_a_batched_bound():
+    """Blocks of at most 64 rows under a bound above 64 (the selected lengths of a batch whose
+    worst case is large): the 64-row GEMM kernel serves them and the batched kernels, launched
+    too, return at once; Llama-3-70B width with 28 rows under a 132-row bound, the small model
+    with 20 rows under 272."""
+    _bf16_case(configs.LLAMA3_70B.with_layers(1), 24, [8192, 8100, 5000, 7000], [8, 8, 6, 6], bound=132)
+    _bf16_case(configs.SMALL_BF16, 25, [300, 40, 129], [9, 5, 6], bound=272)

@@ -162,3 +162,41 @@ def test_bf16_loop_streams_agree_for_every_length():
     for policy, g0 in (("static", 16), ("marginal", None), ("g4", 8), ("joint", None)):
         assert run(policy, g0, dr, cost_total if policy == "joint" else cost) == plain, policy
     note(f"  small bf16: {n} tokens per sequence identical for static 0 / 16, marginal, G4-style and joint")
+
+
+def test_loop_stops_a_sequence_at_max_ctx():
+    """A block that would run past max_ctx is refused by the verify step (LSV_ERR_CAPACITY); the
+    acceptance then skips that sequence -- no tokens, no commit, the status kept -- and the next
+    roots keep its pending token, so the sequence stays where it was while the other one decodes
+    on.  Everything emitted before is the oracle's greedy continuation."""
+    m, G, gamma, max_ctx = configs.TINY_F32, 12, 4, 80
+    contexts = [40, 75]
+    B = len(contexts)
+    w = gen.model_weights(m, SEED)
+    cfg, dm, kv, cap, conts, roots = _setup(m, w, contexts, G)
+    stream = np.zeros((B, cap), np.int64)
+    for b, C in enumerate(contexts):
+        stream[b, C] = roots[b]
+        stream[b, C + 1:C + 1 + N] = conts[b]
+    dr = drafter.PlantedDrafter(stream, drafter.confidences(SEED, B, cap), SEED, m.vocab, G)
+    loop = decode.DecodeLoop(cfg, dm, kv, cap, B, G, "static", dr, gamma0=gamma, max_ctx=max_ctx)
+    loop.reset(contexts, roots)
+    got, frozen = [[] for _ in range(B)], [None] * B
+    for r in range(40):
+        loop.round()
+        st, sl, em = loop.status.cpu().tolist(), loop.seq_len.cpu().tolist(), loop.emitted()
+        for b in range(B):
+            if st[b] == lsv.LSV_OK:
+                assert frozen[b] is None, (r, b)
+                got[b] += em[b]
+                assert sl[b] == contexts[b] + len(got[b])
+            else:
+                assert st[b] == lsv.LSV_ERR_CAPACITY and em[b] == [-1], (r, b, st[b], em[b])
+                frozen[b] = sl[b] if frozen[b] is None else frozen[b]
+                assert sl[b] == frozen[b]
+        if all(f is not None for f in frozen):
+            break
+    for b in range(B):
+        assert frozen[b] is not None and max_ctx - (gamma + 1) < frozen[b] <= max_ctx, (b, frozen[b])
+        assert got[b] == conts[b][:len(got[b])], b
+    note(f"  sequences stopped at {frozen} of max_ctx {max_ctx} after emitting {[len(g) for g in got]} tokens")

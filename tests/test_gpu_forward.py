@@ -5,9 +5,12 @@
   greedy accept results bit-exact (argmax margins dwarf that error);
 * bf16 decoders (grouped-query attention, head_dim 64 and 128, ragged contexts over
   several 64-key chunks): logits within 2e-2; greedy decisions equal wherever the
-  oracle's top-2 margin exceeds twice the measured logit error;
+  oracle's top-2 margin exceeds twice the row's measured logit error, and at least half
+  of the rows decided (tests.lsv_testing.greedy_decisions);
 * Llama-3-8B width (d 4096, 32/8 x 128 heads, F 14336, V 128256) with 2 of its 32
-  layers, context 2048 from the seeded KV generator, 17 rows: the same bf16 bar."""
+  layers, context 2048 from the seeded KV generator, 17 rows: the same bf16 bar.
+Unless a test says otherwise the RMSNorm gains are random per column (0.5 + U(0, 1)), so
+the attention, FFN and final norms' gains all reach the logits."""
 import copy
 
 import numpy as np
@@ -18,7 +21,7 @@ from oracle import accept as OA
 from oracle import forward as OF
 from paper_2608_08721_amd import lsv, runtime
 from synth import configs, gen
-from tests.lsv_testing import GpuModel, i32, note, row_rel_err, top2_margin
+from tests.lsv_testing import GpuModel, greedy_decisions, i32, note, row_rel_err, top2_margin
 
 pytestmark = pytest.mark.gpu
 
@@ -36,13 +39,14 @@ def greedy_gpu(logits_t, off, tokens, width):
     return acc.cpu().numpy(), out.cpu().numpy(), st.cpu().numpy()
 
 
-def test_tiny_f32_end_to_end():
+@pytest.mark.parametrize("gains", ["ones", "random"])
+def test_tiny_f32_end_to_end(gains):
     wl = configs.WORKLOADS["tiny-f32-b1-c128"]
     m = wl.model
-    w = gen.model_weights(m, wl.seed)
+    w = gen.model_weights(m, wl.seed, gains)
     C = int(gen.contexts(wl)[0])
     prompt = gen.prefix_ids(wl.seed, 1, [C], m.vocab)[0]
-    note(f"tiny f32: prefill {C} tokens")
+    note(f"tiny f32, {gains} gains: prefill {C} tokens")
     om = OF.Model(m, w)
     ocache = OF.KVCache(m, 1, 256)
     o_last, o_len = OF.prefill(om, ocache, [prompt])
@@ -74,11 +78,11 @@ def test_tiny_f32_end_to_end():
             assert acc[0] == 16
 
 
-def _bf16_case(shape, seed, contexts, rows, tol=2e-2, bound=None):
+def _bf16_case(shape, seed, contexts, rows, tol=2e-2, bound=None, gains="random", min_decided=0.5):
     """Verify through the C-ABI against the oracle. bound: the host row bound of the call
     (default: the workspace's, max(64, total rows))."""
     B = len(contexts)
-    w = gen.model_weights(shape, seed)
+    w = gen.model_weights(shape, seed, gains)
     cap = runtime.kv_capacity(max(contexts) + max(rows) + 8)
     gm = GpuModel(shape, w, B, cap, max_rows=max(64, int(sum(rows))))
     om = OF.Model(shape, w)
@@ -110,12 +114,8 @@ def _bf16_case(shape, seed, contexts, rows, tol=2e-2, bound=None):
                 new_g = got[:, contexts[b]:]
                 new_o = want[b, :, contexts[b]:contexts[b] + rows[b]]
                 assert np.abs(new_g - new_o).max() <= tol * max(np.abs(new_o).max(), 1e-6) * 4
-    # greedy decisions agree wherever the oracle's margin clears the error
-    abs_err = np.abs(g_logits - o_logits).max()
-    am_g, am_o = g_logits.argmax(axis=1), o_logits.argmax(axis=1)
-    decided = [r for r in range(len(o_logits)) if top2_margin(o_logits[r]) > 2 * abs_err]
-    assert all(am_g[r] == am_o[r] for r in decided)
-    note(f"    argmax equal on {len(decided)}/{len(o_logits)} decided rows")
+    # greedy decisions agree wherever the oracle's margin clears the row's error
+    greedy_decisions(g_logits, o_logits, min_decided)
     return gm, g_logits, o_logits, toks, off
 
 
@@ -177,6 +177,11 @@ def test_llama8b_width_two_layers():
     _bf16_case(shape, 2, [2048], [17])
 
 
+def test_bf16_unit_gains():
+    """Gains of one (the workloads' setting): the folded gain is the weight itself."""
+    _bf16_case(configs.SMALL_BF16, 12, [129, 300], [17, 9], gains="ones")
+
+
 def test_wide_model_gateup_skinny_blocks():
     """Qwen2.5-32B and Llama-3-70B widths, one layer, blocks of 9 and 9 + 11 rows: their gate/up
     products (3072 or more fragment rows) take the eight-fragment-rows-per-wave configuration,
@@ -190,7 +195,7 @@ def test_workspace_reused_across_bounds():
     the 64-row bound, then verify blocks with the 17-, 64- and 5-row bounds and a smaller
     max_ctx, each against the oracle."""
     shape = configs.TINY_BF16
-    w = gen.model_weights(shape, 14)
+    w = gen.model_weights(shape, 14, "random")
     cap = 256
     gm = GpuModel(shape, w, 1, cap)
     om = OF.Model(shape, w)
