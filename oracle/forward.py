@@ -125,8 +125,37 @@ class KVCache:
         self.capacity = capacity
 
 
-def verify_block(model, cache, seq_len, tokens, row_offsets, collect_hidden=False):
-    """One forward pass over the block; returns (logits fp64 [M, V], status [B])."""
+def tree_depths(parents):
+    """Depth of every node of one tree (node 0 the root, parent[0] = -1, parent[r] < r);
+    None when the parents do not form such a tree."""
+    par = [int(p) for p in parents]
+    if not par or par[0] != -1:
+        return None
+    depth = [0]
+    for r in range(1, len(par)):
+        if not 0 <= par[r] < r:
+            return None
+        depth.append(depth[par[r]] + 1)
+    return depth
+
+
+def ancestors(parents, r):
+    """Node r and its ancestors, in increasing order (the root first)."""
+    out = [r]
+    while parents[out[-1]] >= 0:
+        out.append(int(parents[out[-1]]))
+    return out[::-1]
+
+
+def verify_block(model, cache, seq_len, tokens, row_offsets, parents=None, collect_hidden=False):
+    """One forward pass over the block; returns (logits fp64 [M, V], status [B]).
+
+    parents (optional, [M]): the block of each sequence is a tree of drafts -- parents[r] is the
+    parent of row r as a row index within its sequence's block (-1 for the sequence's first row,
+    the root; a parent precedes its children).  Row r then sits at position seq_len + depth(r),
+    is stored at cache slot seq_len + (r - row_offsets[b]), and attends to the cached context and
+    to the slots of its ancestors and itself.  Without parents the block is a chain: row r's
+    parent is r - 1, which is the plain causal block."""
     m = model.m
     off = [int(x) for x in row_offsets]
     B = len(off) - 1
@@ -136,11 +165,23 @@ def verify_block(model, cache, seq_len, tokens, row_offsets, collect_hidden=Fals
     group = nq // nkv
     status = np.zeros(B, np.int32)
     seq_of_row = np.zeros(M, np.int64)
-    pos = np.zeros(M, np.int64)
+    pos = np.zeros(M, np.int64)     # rotary position
+    slot = np.zeros(M, np.int64)    # cache slot
+    keys = [None] * M               # block slots a row attends to, besides the cached context
     for b in range(B):
+        n = off[b + 1] - off[b]
+        C = int(seq_len[b])
+        par = list(range(-1, n - 1)) if parents is None else [int(p) for p in parents[off[b]:off[b + 1]]]
+        depth = tree_depths(par) if n else []
         seq_of_row[off[b]:off[b + 1]] = b
-        pos[off[b]:off[b + 1]] = int(seq_len[b]) + np.arange(off[b + 1] - off[b])
-        if int(seq_len[b]) + off[b + 1] - off[b] > cache.capacity:
+        slot[off[b]:off[b + 1]] = C + np.arange(n)
+        if depth is None:
+            status[b] = LSV_ERR_INVALID_ARG
+            continue
+        pos[off[b]:off[b + 1]] = C + np.asarray(depth, dtype=np.int64)
+        for i in range(n):
+            keys[off[b] + i] = [C + j for j in ancestors(par, i)]
+        if C + n > cache.capacity:
             status[b] = LSV_ERR_CAPACITY
         if np.any((tokens[off[b]:off[b + 1]] < 0) | (tokens[off[b]:off[b + 1]] >= m.vocab)):
             status[b] = LSV_ERR_INVALID_ARG
@@ -162,18 +203,22 @@ def verify_block(model, cache, seq_len, tokens, row_offsets, collect_hidden=Fals
         for r in range(M):
             b = seq_of_row[r]
             if status[b] == LSV_OK:
-                cache.k[l][b, :, pos[r], :] = k[r]
-                cache.v[l][b, :, pos[r], :] = v[r]
+                cache.k[l][b, :, slot[r], :] = k[r]
+                cache.v[l][b, :, slot[r], :] = v[r]
         o = np.zeros((M, nq, hd))
         for r in range(M):
             b = seq_of_row[r]
             if status[b] != LSV_OK:
                 continue
-            n_keys = pos[r] + 1
+            C = int(seq_len[b])
+            if keys[r] == list(range(C, C + len(keys[r]))):  # a chain prefix: the causal keys
+                ks = slice(0, C + len(keys[r]))
+            else:
+                ks = np.concatenate([np.arange(C), np.asarray(keys[r], dtype=np.int64)])
             for hq in range(nq):
                 kv = hq // group
-                K = cache.k[l][b, kv, :n_keys, :]
-                Vv = cache.v[l][b, kv, :n_keys, :]
+                K = cache.k[l][b, kv, ks, :]
+                Vv = cache.v[l][b, kv, ks, :]
                 s = (K @ q[r, hq]) / np.sqrt(hd)
                 s = s - s.max()
                 p = np.exp(s)
