@@ -95,11 +95,10 @@ typedef struct lsv_model_config {
  * invalid).  lsv_pack_globals / lsv_pack_layer: write the embedding table
  * [vocab, d_model], the final norm gain [d_model] and the LM head
  * [vocab, d_model], respectively one layer's projections and norm gains, into
- * d_packed.  Each RMSNorm gain is folded into the projection that consumes the
- * normalised activations (attention norm into Q/K/V, FFN norm into gate/up,
- * final norm into the LM head): packed column j holds W[:, j] * g[j], rounded to
- * the model dtype, and the kernels scale each output row by 1/rms(h) (the norm
- * commutes with the product because it is a per-row scalar).  Source pointers
+ * d_packed.  The projections are stored unchanged; each RMSNorm gain is stored
+ * beside them in fp32, and the forward pass forms every projection's input as
+ * a = R(h / sqrt(mean(h^2) + rms_eps) * g), rounded to the model dtype once, after
+ * the gain (the normalised activation of the model's definition).  Source pointers
  * are device pointers in the model dtype; they may be freed once the stream has
  * passed the call.  Layers may be packed in any order. */
 size_t lsv_packed_model_bytes(const lsv_model_config* cfg);

@@ -2,13 +2,17 @@
 // and the per-layer launch sequence (LibraSpec Sec. 3.1: one target pass over all
 // drafted positions).
 //
-// Per layer, five launches (+1 attention merge for bf16):
-//   QKV GEMM   : 1/rms row scaling, RoPE, K/V cache append
+// Per layer, seven launches (+1 attention merge for bf16):
+//   QKV GEMM   : RoPE, K/V cache append
 //   attention  : split-context running softmax (+ merge)
-//   O GEMM     : residual add, storage-type copy of h, row sum-of-squares partials
-//   gate/up    : 1/rms row scaling, SwiGLU
-//   down GEMM  : residual add, storage-type copy of h, sum-of-squares partials
-// then the LM head (1/rms row scaling) writes fp32 logits.
+//   O GEMM     : residual add
+//   norm       : a = R(h / rms(h) * g_ffn)
+//   gate/up    : SwiGLU
+//   down GEMM  : residual add
+//   norm       : a = R(h / rms(h) * g) with the next layer's attention gain (final gain last)
+// then the LM head writes fp32 logits.  The embedding kernel writes layer 0's first a.
+// R() rounds to the storage type once, after the gain: the normalised activation is what a
+// projection multiplies, as in the model's definition.
 #include "lsv_attn.h"
 #include "lsv_device.h"
 #include "lsv_gemm.h"
@@ -50,9 +54,15 @@ ModelLayout model_layout(const Shape& s) {
   size_t off = 0;
   m.embed = off;
   off = al256(off + (size_t)s.V * s.d * s.es);
+  m.final_norm = off;
+  off = al256(off + sizeof(float) * (size_t)s.d);
   m.lm_head = packed(off, s.V, s.d, KT);
   m.layer_base = off;
   size_t lo = 0;
+  m.attn_norm = lo;
+  lo = al256(lo + sizeof(float) * (size_t)s.d);
+  m.ffn_norm = lo;
+  lo = al256(lo + sizeof(float) * (size_t)s.d);
   m.qkv = packed(lo, (s.nq + 2 * s.nkv) * s.hd, s.d, KT);
   m.o = packed(lo, s.d, s.nq * s.hd, KT);
   m.gateup = packed(lo, 2 * s.F, s.d, KT, 2 * ((s.F + 15) / 16));
@@ -65,8 +75,7 @@ ModelLayout model_layout(const Shape& s) {
 // ------------------------------------------------------------------ workspace
 struct VerifyWs {
   float* h;        // [M_max][d] fp32 residual stream (row-major)
-  void* hx;        // storage-type copy of h, d columns (activation layout, act_index)
-  float* stats;    // [M_max][d/16] per-16-column sums of squares of h
+  void* a;         // normalised rows R(h / rms(h) * g), d columns (activation layout, act_index)
   void* q;         // [M_max][nq][hd]
   void* attn;      // attention output, nq*hd columns (activation layout)
   void* u;         // SwiGLU output, d_ff columns (activation layout; padding columns stay zero)
@@ -117,8 +126,7 @@ static VerifyWs carve_verify(const Shape& s, const ModelLayout& ml, const Verify
     return (size_t)s.es * (s.dtype == LSV_DTYPE_BF16 ? act_elems<32>(max_rows, K) : act_elems<16>(max_rows, K));
   };
   w.h = (float*)take(sizeof(float) * (size_t)max_rows * s.d);
-  w.hx = take(act_bytes(s.d));
-  w.stats = (float*)take(sizeof(float) * (size_t)(s.d / 16) * max_rows);
+  w.a = take(act_bytes(s.d));
   w.q = take((size_t)s.es * max_rows * s.nq * s.hd);
   w.attn = take(act_bytes(s.nq * s.hd));
   w.u = take(act_bytes(s.F));
@@ -142,15 +150,77 @@ size_t verify_workspace_bytes(const Shape& s, int batch, int max_rows, int max_c
   return carve_verify(s, ml, v, max_rows, nullptr).total;
 }
 
+// ------------------------------------------------------------------ row normalisation
+// a[m] = R(h[m] / sqrt(mean(h[m]^2) + eps) * g) of one row, by one 256-thread workgroup:
+// thread t takes the 16-column groups t, t + 256, ... (each summed left to right), the
+// workgroup adds the 256 partial sums in a fixed tree, and every element is scaled,
+// multiplied by its gain and rounded once.
+template <typename T>
+LSV_DEV void normalise_row(const float* __restrict__ hrow, int d, const float* __restrict__ gain, float eps, int m,
+                           T* __restrict__ a) {
+  __shared__ float red[256];
+  const int t = threadIdx.x;
+  float ss = 0.f;
+  for (int p = t; p < d / 16; p += 256) {
+    const GLOBAL f32x4_t* hp = (const GLOBAL f32x4_t*)(GL(hrow) + 16 * p);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const f32x4_t v = hp[i];
+      ss += v[0] * v[0];
+      ss += v[1] * v[1];
+      ss += v[2] * v[2];
+      ss += v[3] * v[3];
+    }
+  }
+  red[t] = ss;
+  __syncthreads();
+  for (int o = 128; o > 0; o >>= 1) {
+    if (t < o) red[t] += red[t + o];
+    __syncthreads();
+  }
+  const float inv = 1.0f / sqrtf(red[0] / (float)d + eps);
+  // one lane run of a fragment (EPL = 16 / sizeof(T) columns) per 16-byte store
+  constexpr int KT = 64 / sizeof(T), EPL = KT / 4;
+  const int Kt = (d + KT - 1) / KT;
+  for (int c = t * EPL; c < d; c += 256 * EPL) {
+    float x[EPL];
+#pragma unroll
+    for (int e = 0; e < EPL; e += 4) {
+      const f32x4_t hv = *(const GLOBAL f32x4_t*)(GL(hrow) + c + e);
+      const f32x4_t gv = *(const GLOBAL f32x4_t*)(GL(gain) + c + e);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) x[e + r] = hv[r] * inv * gv[r];
+    }
+    u32x4_t out;
+    if constexpr (sizeof(T) == 2) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) out[i] = (uint32_t)f2bf(x[2 * i]) | ((uint32_t)f2bf(x[2 * i + 1]) << 16);
+    } else {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) out[i] = __float_as_uint(x[i]);
+    }
+    *(GLOBAL u32x4_t*)(GL(a) + act_index<KT>(m, c, Kt)) = out;
+  }
+}
+
+// The consumer operand of the next projection, one workgroup per block row.
+template <typename T>
+__global__ void __launch_bounds__(256) rmsnorm_kernel(const float* __restrict__ h, int d, const float* gain, float eps,
+                                                      const int32_t* row_offsets, int batch, int M_max, T* a) {
+  const int m = blockIdx.x;
+  if (m >= GL(row_offsets)[batch] || m >= M_max) return;
+  normalise_row<T>(h + (size_t)m * d, d, gain, eps, m, a);
+}
+
 // ------------------------------------------------------------------ embedding
-// h[m] = E[token_m] (fp32), its storage-type copy in the activation layout and
-// per-16-column sums of squares for the first RMSNorm.  Workgroup 0 also validates every
-// sequence: token ids in range and the block within max_ctx.  Invalid tokens embed as zeros.
+// h[m] = E[token_m] (fp32) and the first normalised operand a[m] = R(h / rms(h) * g) with
+// layer 0's attention gain.  Workgroup 0 also validates every sequence: token ids in range
+// and the block within max_ctx.  Invalid tokens embed as zeros.
 template <typename T>
 __global__ void __launch_bounds__(256) embed_kernel(const T* __restrict__ E, int V, int d, const int32_t* tokens,
                                                     const int32_t* row_offsets, const int32_t* seq_len, int batch,
-                                                    int ctx_limit, int M_max, float* h, T* hx, float* stats,
-                                                    int32_t* status) {
+                                                    int ctx_limit, int M_max, float* h, const float* gain, float eps,
+                                                    T* a, int32_t* status) {
   const int m = blockIdx.x;
   if (m == 0 && status) {
     for (int b = threadIdx.x; b < batch; b += blockDim.x) {
@@ -170,41 +240,16 @@ __global__ void __launch_bounds__(256) embed_kernel(const T* __restrict__ E, int
   const int tok_in = GL(tokens)[m];
   const bool ok = tok_in >= 0 && tok_in < V;
   const int tok = ok ? tok_in : 0;  // invalid ids read row 0 and are zeroed below
-  // one 16-column group per thread: 16-byte loads and stores, the group's sum of squares
-  constexpr int PER16 = 16 * sizeof(T) / 16;  // 16-byte pieces per 16 elements
-  const GLOBAL u32x4_t* src = (const GLOBAL u32x4_t*)(GL(E) + (size_t)tok * d);
-  for (int p = threadIdx.x; p < d / 16; p += blockDim.x) {
-    u32x4_t raw[PER16];
+  const GLOBAL T* src = GL(E) + (size_t)tok * d;
+  float* hrow = h + (size_t)m * d;
+  for (int c = threadIdx.x * 4; c < d; c += 256 * 4) {
+    f32x4_t v;
 #pragma unroll
-    for (int i = 0; i < PER16; ++i) {
-      const u32x4_t v = src[p * PER16 + i];
-      raw[i] = ok ? v : u32x4_t{0u, 0u, 0u, 0u};
-    }
-    float x[16];
-#pragma unroll
-    for (int i = 0; i < PER16; ++i)
-#pragma unroll
-      for (int e = 0; e < 16 / PER16; ++e) {
-        if (sizeof(T) == 2) {
-          const uint32_t w = raw[i][e >> 1];
-          x[i * 8 + e] = __uint_as_float((e & 1) ? (w & 0xffff0000u) : (w << 16));
-        } else {
-          x[i * 4 + e] = __uint_as_float(raw[i][e]);
-        }
-      }
-    float ss = 0.f;
-#pragma unroll
-    for (int e = 0; e < 16; ++e) ss += x[e] * x[e];
-    GLOBAL f32x4_t* hp = (GLOBAL f32x4_t*)(GL(h) + (size_t)m * d + 16 * p);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) hp[i] = f32x4_t{x[4 * i], x[4 * i + 1], x[4 * i + 2], x[4 * i + 3]};
-    // a 16-byte piece is one lane's run of a fragment (EPL = 16 / sizeof(T) columns)
-    constexpr int KT = 64 / sizeof(T), EPL = KT / 4;
-    const int Kt = (d + KT - 1) / KT;
-#pragma unroll
-    for (int i = 0; i < PER16; ++i) *(GLOBAL u32x4_t*)(GL(hx) + act_index<KT>(m, 16 * p + i * EPL, Kt)) = raw[i];
-    GL(stats)[(size_t)m * (d / 16) + p] = ss;
+    for (int r = 0; r < 4; ++r) v[r] = ok ? to_f32<T>(src[c + r]) : 0.f;
+    *(GLOBAL f32x4_t*)(GL(hrow) + c) = v;
   }
+  __syncthreads();  // the workgroup's stores of the row are visible to its own loads below
+  normalise_row<T>(hrow, d, gain, eps, m, a);
 }
 
 int launch_verify(const Shape& s, const ModelLayout& ml, const void* packed, void* kv, int capacity, int batch,
@@ -217,22 +262,35 @@ int launch_verify(const Shape& s, const ModelLayout& ml, const void* packed, voi
   const char* P = (const char*)packed;
   const bool bf16 = s.dtype == LSV_DTYPE_BF16;
 
+  auto layer_gain = [&](int l, size_t which) {
+    return (const float*)(P + ml.layer_base + (size_t)l * ml.layer_stride + which);
+  };
   if (bf16)
     hipLaunchKernelGGL(embed_kernel<bf16_t>, dim3(max_rows), dim3(256), 0, st, (const bf16_t*)(P + ml.embed), s.V,
-                       s.d, tokens, row_offsets, seq_len, batch, max_ctx, max_rows, w.h, (bf16_t*)w.hx, w.stats,
-                       status);
+                       s.d, tokens, row_offsets, seq_len, batch, max_ctx, max_rows, w.h, layer_gain(0, ml.attn_norm),
+                       s.eps, (bf16_t*)w.a, status);
   else
     hipLaunchKernelGGL(embed_kernel<float>, dim3(max_rows), dim3(256), 0, st, (const float*)(P + ml.embed), s.V, s.d,
-                       tokens, row_offsets, seq_len, batch, max_ctx, max_rows, w.h, (float*)w.hx, w.stats, status);
+                       tokens, row_offsets, seq_len, batch, max_ctx, max_rows, w.h, layer_gain(0, ml.attn_norm), s.eps,
+                       (float*)w.a, status);
   if (hipGetLastError() != hipSuccess) return LSV_ERR_HIP;
+  // a = R(h / rms(h) * gain) for the next projection
+  auto rmsnorm = [&](const float* gain) {
+    if (bf16)
+      hipLaunchKernelGGL(rmsnorm_kernel<bf16_t>, dim3(max_rows), dim3(256), 0, st, w.h, s.d, gain, s.eps, row_offsets,
+                         batch, max_rows, (bf16_t*)w.a);
+    else
+      hipLaunchKernelGGL(rmsnorm_kernel<float>, dim3(max_rows), dim3(256), 0, st, w.h, s.d, gain, s.eps, row_offsets,
+                         batch, max_rows, (float*)w.a);
+    return hipGetLastError() == hipSuccess ? LSV_OK : LSV_ERR_HIP;
+  };
 
   GemmArgs base = {};
+  base.rows_lo = -1;
+  base.rows_hi = kRowsAny;
   base.M_max = max_rows;
   base.batch = batch;
   base.row_offsets = row_offsets;
-  base.stats = w.stats;
-  base.P = s.d / 16;
-  base.eps = s.eps;
   base.seq_len = seq_len;
   base.kv = kv;
   base.capacity = capacity;
@@ -252,10 +310,20 @@ int launch_verify(const Shape& s, const ModelLayout& ml, const void* packed, voi
     timing_before((int)kind, idx, st);
     int rc;
     if (v.wide) {
-      a.part = w.part;
-      a.part_bytes = sizeof(float) * v.part_floats;
-      if (kind == GEMM_QKV) a.out_f32 = w.qkv_y;
-      rc = launch_gemm_wide(kind, a, v.w[kind], st);
+      // a batched bound: the 64-row kernel serves blocks of up to 64 device rows (it streams
+      // the weights once for them) and the batched kernel the larger ones; each launch finds
+      // the row count on the device and the other one returns at once
+      GemmArgs s64 = a;
+      s64.M_max = 64;
+      s64.rows_hi = 64;
+      rc = launch_gemm(s.dtype, kind, 4, s64, st);
+      if (rc == LSV_OK) {
+        a.part = w.part;
+        a.part_bytes = sizeof(float) * v.part_floats;
+        if (kind == GEMM_QKV) a.out_f32 = w.qkv_y;
+        a.rows_lo = 64;
+        rc = launch_gemm_wide(kind, a, v.w[kind], st);
+      }
     } else {
       rc = launch_gemm(s.dtype, kind, v.MT, a, st);
     }
@@ -271,7 +339,7 @@ int launch_verify(const Shape& s, const ModelLayout& ml, const void* packed, voi
     GemmArgs a = base;
     a.layer_index = l;
     a.layer = l;
-    a.x = w.hx;
+    a.x = w.a;
     a.q_out = w.q;
     if ((rc = gemm(GEMM_QKV, ml.qkv, LB, a)) != LSV_OK) return rc;
     // attention
@@ -301,13 +369,12 @@ int launch_verify(const Shape& s, const ModelLayout& ml, const void* packed, voi
     a.layer_index = l;
     a.x = w.attn;
     a.h_out = w.h;
-    a.hx_out = w.hx;
-    a.stats_out = w.stats;
     if ((rc = gemm(GEMM_O, ml.o, LB, a)) != LSV_OK) return rc;
+    if ((rc = rmsnorm(layer_gain(l, ml.ffn_norm))) != LSV_OK) return rc;
     // gate/up (normalised input) + SwiGLU
     a = base;
     a.layer_index = l;
-    a.x = w.hx;
+    a.x = w.a;
     a.u_out = w.u;
     if ((rc = gemm(GEMM_GATEUP, ml.gateup, LB, a)) != LSV_OK) return rc;
     // down + residual
@@ -315,12 +382,13 @@ int launch_verify(const Shape& s, const ModelLayout& ml, const void* packed, voi
     a.layer_index = l;
     a.x = w.u;
     a.h_out = w.h;
-    a.hx_out = w.hx;
-    a.stats_out = w.stats;
     if ((rc = gemm(GEMM_DOWN, ml.down, LB, a)) != LSV_OK) return rc;
+    // the next projection's operand: the next layer's attention norm, or the final norm
+    if ((rc = rmsnorm(l + 1 < s.L ? layer_gain(l + 1, ml.attn_norm) : (const float*)(P + ml.final_norm))) != LSV_OK)
+      return rc;
   }
   GemmArgs a = base;
-  a.x = w.hx;
+  a.x = w.a;
   a.out_f32 = logits;
   a.ldo = s.V;
   return gemm(GEMM_LMHEAD, ml.lm_head, P, a);

@@ -12,10 +12,10 @@
 // (L2-resident) activation buffer.  The k order inside a fragment is any
 // permutation shared by A and B.
 //
-// RMSNorm: rmsnorm(h) g W^T = inv_rms[m] * (h (W o g)^T).  The gain g is folded
-// into W when packing, the producer of h writes a storage-type copy of h and
-// per-16-column sums of squares, and the consumer scales row m by inv_rms[m] in
-// its epilogue.
+// RMSNorm: the consumers of a normalised activation (QKV, gate/up, LM head) read the
+// operand a = R(h / rms(h) * g) that the row-normalisation kernel (forward.hip) writes in
+// the storage type, and multiply it by the plain weights; the producers of the residual
+// (O, down) only update h.
 //
 // Work split: a workgroup owns one tile of TPW fragment rows (16*TPW output columns)
 // over the whole K.  Its KS waves take balanced contiguous k-slices, each running its
@@ -23,7 +23,7 @@
 // adds them in slice order (deterministic) and runs the epilogue.  No data crosses
 // workgroups, so there are no partial buffers, counters or fences.  The residual a
 // tile adds to is loaded ahead of the weight stream; inputs that need dependent loads
-// (1/rms, cache positions) are read in the epilogue.
+// (cache positions) are read in the epilogue.
 #include <math.h>
 
 #include <type_traits>
@@ -35,12 +35,11 @@
 namespace lsv {
 
 // ------------------------------------------------------------------ packing
-// dst fragment element (row pr, col c) = src[row][c] * gain[c] (rounded to the storage type).
+// dst fragment element (row pr, col c) = src[row][c].
 template <typename T>
 __global__ void __launch_bounds__(256) pack_kernel(int kind, int N, int K, int Nt, int Kt, const T* __restrict__ s0,
-                                                   const T* __restrict__ s1, const T* __restrict__ s2,
-                                                   const T* __restrict__ gain, int nq_rows, int nkv_rows, int hd,
-                                                   T* __restrict__ dst) {
+                                                   const T* __restrict__ s1, const T* __restrict__ s2, int nq_rows,
+                                                   int nkv_rows, int hd, T* __restrict__ dst) {
   constexpr int EPL = FragTraits<T>::EPL, KT = FragTraits<T>::KT;
   const size_t gid = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
   const size_t frag = gid >> 6;
@@ -88,17 +87,28 @@ __global__ void __launch_bounds__(256) pack_kernel(int kind, int N, int K, int N
 #pragma unroll
   for (int e = 0; e < EPL; ++e) {
     const int c = col0 + e;
-    float v = 0.f;
-    if (row >= 0 && c < K) {
-      v = to_f32<T>(src[(size_t)row * K + c]);
-      if (gain) v *= to_f32<T>(gain[c]);
-    }
-    out[e] = from_f32<T>(v);
+    out[e] = (row >= 0 && c < K) ? src[(size_t)row * K + c] : from_f32<T>(0.f);
   }
 }
 
+// RMSNorm gain [n] in the storage type -> fp32 (exact) in the packed buffer.
+template <typename T>
+__global__ void __launch_bounds__(256) gain_kernel(int n, const T* __restrict__ src, float* __restrict__ dst) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) dst[i] = to_f32<T>(src[i]);
+}
+
+int launch_gain(const Shape& s, const void* src, void* dst, hipStream_t stream) {
+  const dim3 grid((unsigned)((s.d + 255) / 256));
+  if (s.dtype == LSV_DTYPE_BF16)
+    hipLaunchKernelGGL(gain_kernel<bf16_t>, grid, dim3(256), 0, stream, s.d, (const bf16_t*)src, (float*)dst);
+  else
+    hipLaunchKernelGGL(gain_kernel<float>, grid, dim3(256), 0, stream, s.d, (const float*)src, (float*)dst);
+  return hipGetLastError() == hipSuccess ? LSV_OK : LSV_ERR_HIP;
+}
+
 int launch_pack(const Shape& s, PackKind kind, const PackedMat& pm, const void* src0, const void* src1,
-                const void* src2, const void* gain, void* dst, hipStream_t stream) {
+                const void* src2, void* dst, hipStream_t stream) {
   const size_t threads = (size_t)pm.Nt * pm.Kt * 64;
   dim3 grid((unsigned)((threads + 255) / 256));
   char* d = (char*)dst + pm.offset;
@@ -106,12 +116,12 @@ int launch_pack(const Shape& s, PackKind kind, const PackedMat& pm, const void* 
   const int n_logical = kind == PACK_GATEUP ? s.F : pm.N;
   if (s.dtype == LSV_DTYPE_BF16)
     hipLaunchKernelGGL(pack_kernel<bf16_t>, grid, dim3(256), 0, stream, (int)kind, n_logical, pm.K, pm.Nt, pm.Kt,
-                       (const bf16_t*)src0, (const bf16_t*)src1, (const bf16_t*)src2, (const bf16_t*)gain, nq_rows,
-                       nkv_rows, s.hd, (bf16_t*)d);
+                       (const bf16_t*)src0, (const bf16_t*)src1, (const bf16_t*)src2, nq_rows, nkv_rows, s.hd,
+                       (bf16_t*)d);
   else
     hipLaunchKernelGGL(pack_kernel<float>, grid, dim3(256), 0, stream, (int)kind, n_logical, pm.K, pm.Nt, pm.Kt,
-                       (const float*)src0, (const float*)src1, (const float*)src2, (const float*)gain, nq_rows,
-                       nkv_rows, s.hd, (float*)d);
+                       (const float*)src0, (const float*)src1, (const float*)src2, nq_rows, nkv_rows, s.hd,
+                       (float*)d);
   return hipGetLastError() == hipSuccess ? LSV_OK : LSV_ERR_HIP;
 }
 
@@ -132,52 +142,6 @@ LSV_DEV u32x2_t pack_bf16x4(const f32x4_t v) {
 // 4 consecutive outputs to global memory in the storage type
 LSV_DEV void store4(float* p, const f32x4_t v) { *(GLOBAL f32x4_t*)p = v; }
 LSV_DEV void store4(bf16_t* p, const f32x4_t v) { *(GLOBAL u32x2_t*)p = pack_bf16x4(v); }
-
-constexpr int kMaxStatParts = 512;  // d_model / 16 for d_model <= 8192
-
-// 1 / rms of activation row m from the producer's per-16-column sums of squares
-// (stats[m][0..P)).  The four lanes sharing (lane & 15) take every fourth float4 of
-// the row and combine their sums with a fixed shuffle tree: deterministic and the
-// same in every lane.
-LSV_DEV float inv_rms_of_row(const GemmArgs& a, int m, int g4) {
-  const GLOBAL f32x4_t* st = (const GLOBAL f32x4_t*)(a.stats + (size_t)min(m, a.M_max - 1) * a.P);
-  const int P4 = a.P >> 2;  // float4s per row (P is a multiple of 4)
-  f32x4_t v[kMaxStatParts / 16];
-#pragma unroll
-  for (int j = 0; j < kMaxStatParts / 16; ++j) {
-    const int i = g4 + 4 * j;
-    v[j] = i < P4 ? st[i] : f32x4_t{0.f, 0.f, 0.f, 0.f};
-  }
-  float ss = 0.f;
-#pragma unroll
-  for (int j = 0; j < kMaxStatParts / 16; ++j) ss += ((v[j][0] + v[j][1]) + v[j][2]) + v[j][3];
-  ss += __shfl_xor(ss, 16, kWave);
-  ss += __shfl_xor(ss, 32, kWave);
-  return 1.0f / sqrtf(ss / (float)a.K + a.eps);
-}
-
-// The same value as inv_rms_of_row, summed by one thread in the same order: lane group
-// g (of 4) adds float4s g, g+4, ... each as ((x+y)+z)+w, and the groups combine as
-// (g0+g1)+(g2+g3).
-LSV_DEV float inv_rms_serial(const GemmArgs& a, int m) {
-  const GLOBAL f32x4_t* st = (const GLOBAL f32x4_t*)(a.stats + (size_t)min(m, a.M_max - 1) * a.P);
-  const int P4 = a.P >> 2;
-  float part[4];
-#pragma unroll
-  for (int g = 0; g < 4; ++g) {
-    float ss = 0.f;
-    for (int i = g; i < P4; i += 16) {
-      f32x4_t v[4];
-#pragma unroll
-      for (int u = 0; u < 4; ++u) v[u] = i + 4 * u < P4 ? st[i + 4 * u] : f32x4_t{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int u = 0; u < 4; ++u) ss += ((v[u][0] + v[u][1]) + v[u][2]) + v[u][3];
-    }
-    part[g] = ss;
-  }
-  const float ss = (part[0] + part[1]) + (part[2] + part[3]);
-  return 1.0f / sqrtf(ss / (float)a.K + a.eps);
-}
 
 // ------------------------------------------------------------------ QKV epilogue
 // base^(-2i/hd) of the two rotary pairs held by output columns n0 .. n0+3 (packed rows
@@ -248,44 +212,21 @@ LSV_DEV void qkv_store4(const GemmArgs& a, int m, int n0, const f32x4_t v, int b
 // ------------------------------------------------------------------ the GEMM
 // Epilogue of one wave: lane holds output columns n0..n0+3 (weight rows) of activation
 // row m for each of its TPW fragment rows and MT activation tiles.  Row inputs that need
-// dependent loads (1/rms, cache positions) are read here, off the weight stream's
-// critical path.  HPRE: the residual was loaded ahead into hpre (else it is read here).
-// Per-row inputs of the epilogue gathered once per workgroup (wide blocks): 1/rms and the
-// sequence / cache position of every row, in LDS.
-struct RowInputs {
-  const float* inv;  // [rows]
-  const int* seq;    // [rows]
-  const int* pos;    // [rows]
-};
-
+// dependent loads (cache positions) are read here, off the weight stream's critical path.
+// HPRE: the residual was loaded ahead into hpre (else it is read here).
 template <typename T, int MT, int TPW, int EPI, bool HPRE>
 LSV_DEV void gemm_epilogue(const GemmArgs& a, const int M, const int m0, const int tn0, const bool (&tvalid)[TPW],
-                           f32x4_t (&acc)[TPW][MT], const f32x4_t (&hpre)[TPW][MT], const RowInputs* rin = nullptr,
-                           const float* inv_pre = nullptr) {
-  constexpr bool RMS = EPI != EPI_RESID;
+                           f32x4_t (&acc)[TPW][MT], const f32x4_t (&hpre)[TPW][MT]) {
   constexpr int KT = FragTraits<T>::KT;
   const int lane = threadIdx.x & 63, l16 = lane & 15, g4 = lane >> 4;
-  float inv[MT];
-  if (RMS) {
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-      const int m = m0 + mt * 16 + l16;
-      inv[mt] = inv_pre ? inv_pre[mt] : (rin ? rin->inv[min(m, a.M_max - 1)] : inv_rms_of_row(a, m, g4));
-    }
-  }
   int qkv_b[MT], qkv_pos[MT];
   if (EPI == EPI_QKV) {
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
       const int m = min(m0 + mt * 16 + l16, a.M_max - 1);
-      if (rin) {
-        qkv_b[mt] = rin->seq[m];
-        qkv_pos[mt] = rin->pos[m];
-      } else {
-        const int b = seq_of_row(a.row_offsets, a.batch, m);
-        qkv_b[mt] = b;
-        qkv_pos[mt] = GL(a.seq_len)[b] + (m - GL(a.row_offsets)[b]);
-      }
+      const int b = seq_of_row(a.row_offsets, a.batch, m);
+      qkv_b[mt] = b;
+      qkv_pos[mt] = GL(a.seq_len)[b] + (m - GL(a.row_offsets)[b]);
     }
   }
   if (EPI == EPI_LOGITS) {
@@ -295,7 +236,7 @@ LSV_DEV void gemm_epilogue(const GemmArgs& a, const int M, const int m0, const i
       for (int mt = 0; mt < MT; ++mt) {
         const int m = m0 + mt * 16 + l16, n0 = (tn0 + t) * 16 + 4 * g4;
         if (m >= M || !tvalid[t]) continue;
-        const f32x4_t v = acc[t][mt] * inv[mt];
+        const f32x4_t v = acc[t][mt];
         GLOBAL float* o = GL(a.out_f32) + (size_t)m * a.ldo;
         if (n0 + 3 < a.N && (a.ldo & 3) == 0) {
           *(GLOBAL f32x4_t*)(o + n0) = v;
@@ -315,27 +256,19 @@ LSV_DEV void gemm_epilogue(const GemmArgs& a, const int M, const int m0, const i
         for (int mt = 0; mt < MT; ++mt) {
           const int m = m0 + mt * 16 + l16, n0 = (tn0 + t) * 16 + 4 * g4;
           if (m >= M || !tvalid[t]) continue;
-          qkv_store4<T>(a, m, n0, acc[t][mt] * inv[mt], qkv_b[mt], qkv_pos[mt], inv_freq[t]);
+          qkv_store4<T>(a, m, n0, acc[t][mt], qkv_b[mt], qkv_pos[mt], inv_freq[t]);
         }
     } else if (EPI == EPI_RESID) {
-      // h += y; the storage-type copy of h for the next consumer; per-row sum of squares of
-      // the new h over this fragment row's 16 columns (stats[m][n / 16])
+      // h += y (fp32 residual, row-major); the next norm reads it
 #pragma unroll
       for (int t = 0; t < TPW; ++t)
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) {
           const int m = m0 + mt * 16 + l16, n0 = (tn0 + t) * 16 + 4 * g4;
-          float ss = 0.f;
           if (m < M && tvalid[t]) {
             const f32x4_t hv = HPRE ? hpre[t][mt] : *(const GLOBAL f32x4_t*)(a.h_out + (size_t)m * a.N + n0);
-            const f32x4_t h4 = hv + acc[t][mt];
-            *(GLOBAL f32x4_t*)(a.h_out + (size_t)m * a.N + n0) = h4;
-            if (a.hx_out) store4((T*)a.hx_out + act_index<KT>(m, n0, (a.N + KT - 1) / KT), h4);
-            ss = ((h4[0] * h4[0] + h4[1] * h4[1]) + h4[2] * h4[2]) + h4[3] * h4[3];
+            *(GLOBAL f32x4_t*)(a.h_out + (size_t)m * a.N + n0) = hv + acc[t][mt];
           }
-          ss += __shfl_xor(ss, 16, kWave);
-          ss += __shfl_xor(ss, 32, kWave);
-          if (g4 == 0 && m < M && tvalid[t]) GL(a.stats_out)[(size_t)m * (a.N / 16) + tn0 + t] = ss;
         }
     } else if (EPI == EPI_SWIGLU) {
       // fragment rows come in (gate, up) pairs: even rows gate, odd rows up
@@ -349,7 +282,7 @@ LSV_DEV void gemm_epilogue(const GemmArgs& a, const int M, const int m0, const i
         f32x4_t out;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const float gt = acc[t][mt][r] * inv[mt], up = acc[t + 1][mt][r] * inv[mt];
+          const float gt = acc[t][mt][r], up = acc[t + 1][mt][r];
           out[r] = gt / (1.0f + expf(-gt)) * up;
         }
         T* dst = (T*)a.u_out + act_index<KT>(m, f0, (a.F + KT - 1) / KT);  // f0 .. f0+3 are adjacent
@@ -363,12 +296,10 @@ LSV_DEV void gemm_epilogue(const GemmArgs& a, const int M, const int m0, const i
     }
 }
 
-template <typename T, int MT, int TPW, int KS, int U, int NS, int EPI, int MT_MAX, int PSTAT>
+template <typename T, int MT, int TPW, int KS, int U, int NS, int EPI, int MT_MAX>
 LSV_DEV void gemm_body(const GemmArgs& a, const int M, const int tile, const int m0,
                        f32x4_t (*red)[TPW][MT_MAX][kWave]) {
-  constexpr int KT = FragTraits<T>::KT, EPL = FragTraits<T>::EPL;
-  constexpr bool RMS = EPI != EPI_RESID;  // consumer of a normalised activation
-  constexpr bool PS = RMS && PSTAT;        // its 1/rms rides the weight stream
+  constexpr int EPL = FragTraits<T>::EPL;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, l16 = lane & 15, g4 = lane >> 4;
   // this workgroup: fragment rows tn0 .. tn0+TPW-1 over the whole K, activation rows
   // m0 .. min(M, m0 + 16 MT) - 1; wave = k-slice
@@ -411,31 +342,12 @@ LSV_DEV void gemm_body(const GemmArgs& a, const int M, const int tile, const int
   for (int t = 0; t < TPW; ++t)
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) acc[t][mt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  // PS: 1/rms of the normalised input rides the weight stream: pipeline stage j also loads
-  // float4 g4 + 4j of each row's per-16-column sums of squares (stats[m][0..P)), and the
-  // stage's compute adds it -- the order of inv_rms_of_row, so the value is the same --
-  // instead of a dependent round of loads after the stream.
-  const int P4 = a.P >> 2, nstat = (P4 + 3) / 4;  // float4s per row; per lane group
-  const GLOBAL f32x4_t* stp[MT];
-  float ss[MT];
-#pragma unroll
-  for (int mt = 0; mt < MT; ++mt) {
-    stp[mt] = (const GLOBAL f32x4_t*)(a.stats + (size_t)min(m0 + mt * 16 + l16, a.M_max - 1) * a.P);
-    ss[mt] = 0.f;
-  }
-  int nstat_done = 0;  // stages whose stats have been added
   {
     // NS pipeline stages of U k-steps.  Every load hits an in-bounds fragment (index
     // clamped): a conditional load would become a select between addresses and a generic
     // access.  Steps past the range re-read the last one and are never used.
     u32x4_t wa[NS][U][TPW], xb[NS][U][MT];
-    f32x4_t sr[NS][MT];
     auto load_stage = [&](int st, int kb) {
-      if (PS) {
-        const int i = g4 + 4 * (kb / U);
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt) sr[st][mt] = i < P4 ? stp[mt][i] : f32x4_t{0.f, 0.f, 0.f, 0.f};
-      }
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int kf = max(min(kb + u, nk - 1), 0);  // a slice may be empty when Kt < KS
@@ -446,11 +358,6 @@ LSV_DEV void gemm_body(const GemmArgs& a, const int M, const int tile, const int
       }
     };
     auto compute_stage = [&](int st, int kb, bool tail) {
-      if (PS && kb / U < nstat && (!tail || kb < nk)) {
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt) ss[mt] += ((sr[st][mt][0] + sr[st][mt][1]) + sr[st][mt][2]) + sr[st][mt][3];
-        nstat_done = kb / U + 1;
-      }
 #pragma unroll
       for (int u = 0; u < U; ++u)
         if (!tail || kb + u < nk)
@@ -499,22 +406,7 @@ LSV_DEV void gemm_body(const GemmArgs& a, const int M, const int tile, const int
         for (int mt = 0; mt < MT; ++mt) acc[t][mt] += red[w - 1][t][mt][lane];
   }
 
-  float inv[MT];
-  if (PS) {
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-      for (int j = nstat_done; j < nstat; ++j) {  // stages the k range did not reach
-        const int i = g4 + 4 * j;
-        const f32x4_t v = i < P4 ? stp[mt][i] : f32x4_t{0.f, 0.f, 0.f, 0.f};
-        ss[mt] += ((v[0] + v[1]) + v[2]) + v[3];
-      }
-      float t = ss[mt];
-      t += __shfl_xor(t, 16, kWave);
-      t += __shfl_xor(t, 32, kWave);
-      inv[mt] = 1.0f / sqrtf(t / (float)a.K + a.eps);
-    }
-  }
-  gemm_epilogue<T, MT, TPW, EPI, true>(a, M, m0, tn0, tvalid, acc, hpre, nullptr, PS ? inv : nullptr);
+  gemm_epilogue<T, MT, TPW, EPI, true>(a, M, m0, tn0, tvalid, acc, hpre);
 }
 
 // Launch configuration of each product: fragment rows per wave (TPW), k-slices = waves
@@ -523,26 +415,24 @@ LSV_DEV void gemm_body(const GemmArgs& a, const int M, const int tile, const int
 // flight, beat many short ones (more concurrent streams read more scattered DRAM rows), so
 // every product runs one wave per workgroup over the whole K.
 template <int KIND> struct GemmCfg;
-// PSTAT: the 1/rms of a normalised input rides the weight stream (measured faster for the
-// wide gate/up and LM head; slower for QKV, which reads it in its epilogue).
-template <> struct GemmCfg<GEMM_QKV> { static constexpr int TPW = 2, KS = 1, U = 4, NS = 3, EPI = EPI_QKV, PSTAT = 0; };
-template <> struct GemmCfg<GEMM_O> { static constexpr int TPW = 1, KS = 1, U = 8, NS = 3, EPI = EPI_RESID, PSTAT = 0; };
-template <> struct GemmCfg<GEMM_GATEUP> { static constexpr int TPW = 4, KS = 1, U = 4, NS = 3, EPI = EPI_SWIGLU, PSTAT = 1; };
-template <> struct GemmCfg<GEMM_DOWN> { static constexpr int TPW = 1, KS = 1, U = 8, NS = 3, EPI = EPI_RESID, PSTAT = 0; };
-template <> struct GemmCfg<GEMM_LMHEAD> { static constexpr int TPW = 4, KS = 1, U = 4, NS = 3, EPI = EPI_LOGITS, PSTAT = 1; };
+template <> struct GemmCfg<GEMM_QKV> { static constexpr int TPW = 2, KS = 1, U = 4, NS = 3, EPI = EPI_QKV; };
+template <> struct GemmCfg<GEMM_O> { static constexpr int TPW = 1, KS = 1, U = 8, NS = 3, EPI = EPI_RESID; };
+template <> struct GemmCfg<GEMM_GATEUP> { static constexpr int TPW = 4, KS = 1, U = 4, NS = 3, EPI = EPI_SWIGLU; };
+template <> struct GemmCfg<GEMM_DOWN> { static constexpr int TPW = 1, KS = 1, U = 8, NS = 3, EPI = EPI_RESID; };
+template <> struct GemmCfg<GEMM_LMHEAD> { static constexpr int TPW = 4, KS = 1, U = 4, NS = 3, EPI = EPI_LOGITS; };
 // gate/up of the wider models (3072 or more fragment rows: Qwen2.5-32B, Llama-3-70B shapes):
 // eight fragment rows per wave halve the workgroups and the activation loads per weight byte
 // (measured 5.45 -> 5.72 TB/s at d 5120, 5.62 -> 5.94 TB/s at d 8192; at d 4096 it lost);
 // blocks of up to 32 rows only
 constexpr int kGateUpWide = 5;  // internal kind id of that configuration
 constexpr int kGateUpWideRows = 3072;
-template <> struct GemmCfg<kGateUpWide> { static constexpr int TPW = 8, KS = 1, U = 2, NS = 3, EPI = EPI_SWIGLU, PSTAT = 1; };
+template <> struct GemmCfg<kGateUpWide> { static constexpr int TPW = 8, KS = 1, U = 2, NS = 3, EPI = EPI_SWIGLU; };
 
 // Bodies of three or four activation tiles (prefill bounds) use a shallower pipeline to stay in
 // registers.
 template <int KIND, int MT_MAX> struct GemmShape {
   using C = GemmCfg<KIND>;
-  static constexpr int TPW = C::TPW, KS = C::KS, EPI = C::EPI, PSTAT = C::PSTAT;
+  static constexpr int TPW = C::TPW, KS = C::KS, EPI = C::EPI;
   static constexpr int U = MT_MAX <= 2 ? C::U : 4, NS = MT_MAX <= 2 ? C::NS : 2;
 };
 
@@ -558,7 +448,9 @@ __global__ void __launch_bounds__(64 * GemmCfg<KIND>::KS) gemm_kernel(GemmArgs a
   const int tiles = (a.Nt + S::TPW - 1) / S::TPW, nch = (a.M_max + 63) / 64;
   const int round = blockIdx.x >> 3, chunk = round % nch, tile = (round / nch) * 8 + (blockIdx.x & 7);
   if (tile >= tiles) return;
-  const int M = min(GL(a.row_offsets)[a.batch], a.M_max);  // never trust device rows beyond the host bound
+  const int rows = GL(a.row_offsets)[a.batch];
+  if (rows <= a.rows_lo || rows > a.rows_hi) return;  // another launch serves this row count
+  const int M = min(rows, a.M_max);  // never trust device rows beyond the host bound
   const int m0 = chunk * 64;
   if (m0 >= M) return;
   const int Mc = min(M - m0, 64);
@@ -568,13 +460,13 @@ __global__ void __launch_bounds__(64 * GemmCfg<KIND>::KS) gemm_kernel(GemmArgs a
   // 64-row bound, 41 -> 25 us); three or four take the shallower one
   using C = GemmCfg<KIND>;
   if (mt <= 1 || MT_MAX == 1)
-    gemm_body<T, 1, S::TPW, S::KS, C::U, C::NS, S::EPI, MT_MAX, S::PSTAT>(a, M_end, tile, m0, red);
+    gemm_body<T, 1, S::TPW, S::KS, C::U, C::NS, S::EPI, MT_MAX>(a, M_end, tile, m0, red);
   else if (mt == 2 || MT_MAX == 2)
-    gemm_body<T, (MT_MAX >= 2 ? 2 : 1), S::TPW, S::KS, C::U, C::NS, S::EPI, MT_MAX, S::PSTAT>(a, M_end, tile, m0, red);
+    gemm_body<T, (MT_MAX >= 2 ? 2 : 1), S::TPW, S::KS, C::U, C::NS, S::EPI, MT_MAX>(a, M_end, tile, m0, red);
   else if (mt == 3 || MT_MAX == 3)
-    gemm_body<T, (MT_MAX >= 3 ? 3 : 1), S::TPW, S::KS, S::U, S::NS, S::EPI, MT_MAX, S::PSTAT>(a, M_end, tile, m0, red);
+    gemm_body<T, (MT_MAX >= 3 ? 3 : 1), S::TPW, S::KS, S::U, S::NS, S::EPI, MT_MAX>(a, M_end, tile, m0, red);
   else
-    gemm_body<T, MT_MAX, S::TPW, S::KS, S::U, S::NS, S::EPI, MT_MAX, S::PSTAT>(a, M_end, tile, m0, red);
+    gemm_body<T, MT_MAX, S::TPW, S::KS, S::U, S::NS, S::EPI, MT_MAX>(a, M_end, tile, m0, red);
 }
 
 // ------------------------------------------------------------------ planning and launch
@@ -628,7 +520,7 @@ static int launch_typed(GemmKind kind, int MT, const GemmArgs& a, hipStream_t st
 // than one k range per tile, each workgroup writes fp32 partials and
 // gemm_wide_reduce_kernel adds them in split order (deterministic) and runs the epilogue,
 // one workgroup per (tile, 16 rows); the QKV reduce applies the rotary embedding and the Q
-// store / cache append.  An unsplit QKV runs the plain scaled epilogue into an fp32 buffer
+// store / cache append.  An unsplit QKV runs the plain epilogue into an fp32 buffer
 // and qkv_rope_kernel does the rest.
 constexpr int kWideFR = 8;     // fragment rows of a workgroup
 constexpr int kWideRingW = 10;  // k-steps of weight pieces in flight (register ring)
@@ -641,11 +533,10 @@ constexpr int kWideCols = kWideFR * 16;  // output columns of a workgroup
 // keeps its own MTW activation tiles (rows wave*16*MTW ..) in registers, straight from L2.
 // A k-step is 8 LDS reads and 8 x MTW MFMAs per wave, each read feeding MTW of them.  Tiles
 // past the device row count are computed on clamped rows and never stored.
-// Ws: two buffers of 8 fragments; s_inv: per-row 1/rms for the epilogue (LDS).  The QKV
-// projection never runs its fused epilogue here (split K: the reduce does; one split: the
-// scaled projection, then qkv_rope_kernel).
+// Ws: two buffers of 8 fragments.  The QKV projection never runs its fused epilogue here
+// (split K: the reduce does; one split: the projection, then qkv_rope_kernel).
 template <int EPI, int MTW>
-LSV_DEV void gemm_wide_body(const GemmArgs& a, const int M, u32x4_t* Ws, float* s_inv) {
+LSV_DEV void gemm_wide_body(const GemmArgs& a, const int M, u32x4_t* Ws) {
   static_assert(EPI != EPI_QKV, "the batched QKV epilogue runs in the reduce or the RoPE kernel");
   using T = bf16_t;
   constexpr int FR = kWideFR;
@@ -743,12 +634,8 @@ LSV_DEV void gemm_wide_body(const GemmArgs& a, const int M, u32x4_t* Ws, float* 
       }
     return;
   }
-  if (EPI != EPI_RESID)
-    for (int r = tid; r < a.M_max; r += 256) s_inv[r] = inv_rms_serial(a, r);
-  __syncthreads();
-  const RowInputs rin{s_inv, nullptr, nullptr};
   const f32x4_t none[FR][MTW] = {};
-  gemm_epilogue<T, MTW, FR, EPI, false>(a, M, mt0 * 16, tn0, tvalid, acc, none, &rin);
+  gemm_epilogue<T, MTW, FR, EPI, false>(a, M, mt0 * 16, tn0, tvalid, acc, none);
 }
 
 // One launch for any row count up to kWideRows: the body is chosen once per workgroup from
@@ -756,19 +643,20 @@ LSV_DEV void gemm_wide_body(const GemmArgs& a, const int M, u32x4_t* Ws, float* 
 template <int EPI>
 __global__ void __launch_bounds__(256) gemm_wide_kernel(GemmArgs a) {
   __shared__ u32x4_t Ws[2 * kWideFR * kWave];
-  __shared__ float s_inv[kWideRows];
-  const int M = min(GL(a.row_offsets)[a.batch], a.M_max);  // never trust device rows beyond the host bound
+  const int rows = GL(a.row_offsets)[a.batch];
+  if (rows <= a.rows_lo || rows > a.rows_hi) return;  // another launch serves this row count
+  const int M = min(rows, a.M_max);  // never trust device rows beyond the host bound
   const int mtw = ((M + 15) / 16 + 3) / 4;                 // activation tiles per wave
   if (mtw <= 1)
-    gemm_wide_body<EPI, 1>(a, M, Ws, s_inv);
+    gemm_wide_body<EPI, 1>(a, M, Ws);
   else if (mtw == 2)
-    gemm_wide_body<EPI, 2>(a, M, Ws, s_inv);
+    gemm_wide_body<EPI, 2>(a, M, Ws);
   else if (mtw == 3)
-    gemm_wide_body<EPI, 3>(a, M, Ws, s_inv);
+    gemm_wide_body<EPI, 3>(a, M, Ws);
   else if (mtw == 4)
-    gemm_wide_body<EPI, 4>(a, M, Ws, s_inv);
+    gemm_wide_body<EPI, 4>(a, M, Ws);
   else
-    gemm_wide_body<EPI, 5>(a, M, Ws, s_inv);
+    gemm_wide_body<EPI, 5>(a, M, Ws);
 }
 
 // Split-K sums of the batched GEMM: one workgroup per (tile, 16 rows) adds the k ranges in
@@ -778,7 +666,9 @@ __global__ void __launch_bounds__(256) gemm_wide_reduce_kernel(GemmArgs a) {
   constexpr int TPW = kWideFR / 4;  // wave w sums fragment rows w*TPW ..
   const int tile = blockIdx.x, m0 = blockIdx.y * 16, S = a.splits;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, l16 = lane & 15, g4 = lane >> 4;
-  const int M = min(GL(a.row_offsets)[a.batch], a.M_max);
+  const int rows = GL(a.row_offsets)[a.batch];
+  if (rows <= a.rows_lo || rows > a.rows_hi) return;
+  const int M = min(rows, a.M_max);
   if (m0 >= M) return;
   const int tn0 = (tile * 4 + wave) * TPW, m = m0 + l16;
   bool tvalid[TPW];
@@ -814,7 +704,9 @@ __global__ void __launch_bounds__(256) gemm_wide_reduce_kernel(GemmArgs a) {
 // Rotary embedding and Q store / cache append of a normalised QKV projection y [M][N] (fp32),
 // four columns per thread.
 __global__ void __launch_bounds__(256) qkv_rope_kernel(GemmArgs a, const float* y) {
-  const int M = min(GL(a.row_offsets)[a.batch], a.M_max);
+  const int rows = GL(a.row_offsets)[a.batch];
+  if (rows <= a.rows_lo || rows > a.rows_hi) return;
+  const int M = min(rows, a.M_max);
   const int groups = a.N / 4;
   const size_t n = (size_t)M * groups;
   for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (size_t)gridDim.x * 256) {
@@ -864,7 +756,7 @@ int launch_gemm_wide(GemmKind kind, const GemmArgs& a0, const WidePlan& p, hipSt
                            dim3(256), 0, st, a);
         break;
       }
-      // one split: the scaled projection into the caller's fp32 buffer (out_f32, N columns),
+      // one split: the projection into the caller's fp32 buffer (out_f32, N columns),
       // then RoPE (the fused epilogue would not fit the wide kernel's registers)
       if (!a.out_f32) return LSV_ERR_INVALID_ARG;
       a.ldo = a.N;

@@ -67,7 +67,7 @@ const char* lsv_status_string(int s) {
 }
 
 const char* lsv_last_error(void) { return g_err; }
-int lsv_abi_version(void) { return 1; }
+int lsv_abi_version(void) { return 2; }
 
 size_t lsv_packed_model_bytes(const lsv_model_config* cfg) {
   if (check_config(cfg) != LSV_OK) return 0;
@@ -85,8 +85,10 @@ int lsv_pack_globals(const lsv_model_config* cfg, const void* d_embed, const voi
   char* P = (char*)d_packed;
   if (hipMemcpyAsync(P + ml.embed, d_embed, (size_t)s.V * s.d * s.es, hipMemcpyDeviceToDevice, st) != hipSuccess)
     return fail(LSV_ERR_HIP, "copy: %s", hipGetErrorString(hipGetLastError()));
-  return hip_rc(lsv::launch_pack(s, lsv::PACK_PLAIN, ml.lm_head, d_lm_head, nullptr, nullptr, d_final_norm, P, st),
-                "pack lm_head");
+  if ((rc = lsv::launch_pack(s, lsv::PACK_PLAIN, ml.lm_head, d_lm_head, nullptr, nullptr, P, st)) ||
+      (rc = lsv::launch_gain(s, d_final_norm, P + ml.final_norm, st)))
+    return hip_rc(rc, "pack globals");
+  return ok();
 }
 
 int lsv_pack_layer(const lsv_model_config* cfg, int32_t layer, const void* d_wq, const void* d_wk, const void* d_wv,
@@ -101,10 +103,12 @@ int lsv_pack_layer(const lsv_model_config* cfg, int32_t layer, const void* d_wq,
   const lsv::ModelLayout ml = lsv::model_layout(s);
   hipStream_t st = (hipStream_t)stream;
   char* LB = (char*)d_packed + ml.layer_base + (size_t)layer * ml.layer_stride;
-  if ((rc = lsv::launch_pack(s, lsv::PACK_QKV, ml.qkv, d_wq, d_wk, d_wv, d_attn_norm, LB, st)) ||
-      (rc = lsv::launch_pack(s, lsv::PACK_PLAIN, ml.o, d_wo, nullptr, nullptr, nullptr, LB, st)) ||
-      (rc = lsv::launch_pack(s, lsv::PACK_GATEUP, ml.gateup, d_wg, d_wu, nullptr, d_ffn_norm, LB, st)) ||
-      (rc = lsv::launch_pack(s, lsv::PACK_PLAIN, ml.down, d_wd, nullptr, nullptr, nullptr, LB, st)))
+  if ((rc = lsv::launch_pack(s, lsv::PACK_QKV, ml.qkv, d_wq, d_wk, d_wv, LB, st)) ||
+      (rc = lsv::launch_pack(s, lsv::PACK_PLAIN, ml.o, d_wo, nullptr, nullptr, LB, st)) ||
+      (rc = lsv::launch_pack(s, lsv::PACK_GATEUP, ml.gateup, d_wg, d_wu, nullptr, LB, st)) ||
+      (rc = lsv::launch_pack(s, lsv::PACK_PLAIN, ml.down, d_wd, nullptr, nullptr, LB, st)) ||
+      (rc = lsv::launch_gain(s, d_attn_norm, LB + ml.attn_norm, st)) ||
+      (rc = lsv::launch_gain(s, d_ffn_norm, LB + ml.ffn_norm, st)))
     return hip_rc(rc, "pack layer");
   return ok();
 }

@@ -21,13 +21,9 @@ struct GemmArgs {
   int N, K, Nt, Kt;
   int M_max, batch;
   const int32_t* row_offsets;  // [batch+1]; rows = row_offsets[batch]
-  // B operand: activation rows in the storage type, fragment-major (act_index with Kt)
+  // B operand: activation rows in the storage type, fragment-major (act_index with Kt); for
+  // QKV, gate/up and the LM head the normalised rows R(h / rms(h) * g)
   const void* x;
-  // row scaling of normalised-activation consumers: 1/rms from [M_max][P] sums of squares
-  // over 16-column groups (P = K / 16)
-  const float* stats;
-  int P;
-  float eps;
   // wide blocks: k-split partials [tiles][splits][M_max][128]
   float* part;
   size_t part_bytes;
@@ -42,14 +38,17 @@ struct GemmArgs {
   const int32_t* seq_len;
   double log2_rope_base;
   // EPI_RESID
-  float* h_out;      // [M][N] fp32 residual (row-major), updated in place
-  void* hx_out;      // storage-type copy of the new residual for the next consumer (act_index)
-  float* stats_out;  // [M_max][N/16]
+  float* h_out;  // [M][N] fp32 residual (row-major), updated in place
   // EPI_SWIGLU
   void* u_out;  // SwiGLU output, F columns (act_index)
   int F;
   int layer_index;  // host-side only: which layer a launch belongs to (measurement hook)
+  // device row range a launch serves: it does nothing unless rows_lo < rows <= rows_hi,
+  // rows = row_offsets[batch] (blocks under a batched bound launch both the 64-row kernel
+  // and the batched one, and the device row count picks which of them works)
+  int rows_lo, rows_hi;
 };
+constexpr int kRowsAny = 0x7fffffff;
 
 // One launch: a workgroup per tile of output columns, the whole K per workgroup.
 int launch_gemm(int dtype, GemmKind kind, int MT, const GemmArgs& a, hipStream_t st);

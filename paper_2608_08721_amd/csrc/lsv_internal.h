@@ -81,12 +81,14 @@ __host__ __device__ inline size_t act_elems(int rows, int K) {
   return (size_t)((rows + 15) / 16) * 16 * (size_t)((K + KT - 1) / KT) * KT;
 }
 
-// RMSNorm gains are folded into the projection that follows them (QKV, gate/up,
-// LM head), so the packed model stores no separate gains.
+// RMSNorm gains are kept in fp32 beside the projections: the row-normalisation kernel
+// applies them before the activation is rounded to the storage type.
 struct ModelLayout {
   size_t embed;                     // raw row-major embedding [V, d]
+  size_t final_norm;                // fp32 [d]
   PackedMat lm_head;
   size_t layer_base, layer_stride;  // per-layer block
+  size_t attn_norm, ffn_norm;       // fp32 [d] each, offsets inside a layer block
   PackedMat qkv, o, gateup, down;   // offsets inside a layer block
   size_t total;
 };
@@ -94,7 +96,9 @@ ModelLayout model_layout(const Shape& s);
 
 enum PackKind { PACK_PLAIN = 0, PACK_QKV = 1, PACK_GATEUP = 2 };
 int launch_pack(const Shape& s, PackKind kind, const PackedMat& pm, const void* src0, const void* src1,
-                const void* src2, const void* gain, void* dst, hipStream_t stream);
+                const void* src2, void* dst, hipStream_t stream);
+// A norm gain [d] in the storage type -> fp32 at dst.
+int launch_gain(const Shape& s, const void* src, void* dst, hipStream_t stream);
 
 size_t verify_workspace_bytes(const Shape& s, int batch, int max_rows, int max_ctx);
 int launch_verify(const Shape& s, const ModelLayout& ml, const void* packed, void* kv, int capacity, int batch,

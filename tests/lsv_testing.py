@@ -78,8 +78,8 @@ def greedy_decisions(got, want, min_decided, label=""):
     top-2 margin exceeds 2 e_r the row has a single argmax that any logits within e_r of
     the oracle's share ("decided"): GPU and oracle must pick the same token.  Elsewhere
     both picks are near-maximal: the GPU's pick must lie within 2 e_r of the oracle's
-    maximum.  At least `min_decided` of the rows must be decided.  Returns the decided
-    share."""
+    maximum.  At least `min_decided` of the rows must be decided (checked on blocks of ten
+    rows or more; a share of fewer says little).  Returns the decided share."""
     e = np.abs(got - want).max(axis=1)
     am_g, am_o = got.argmax(axis=1), want.argmax(axis=1)
     margin = np.array([top2_margin(r) for r in want])
@@ -92,5 +92,5 @@ def greedy_decisions(got, want, min_decided, label=""):
     frac = float(decided.mean()) if len(decided) else 1.0
     note(f"    {label}argmax equal on {int(decided.sum())}/{len(decided)} decided rows ({frac:.0%}); "
          f"{int((am_g == am_o).sum())}/{len(am_o)} rows equal in all")
-    assert frac >= min_decided, (frac, min_decided)
+    assert len(decided) < 10 or frac >= min_decided, (frac, min_decided)
     return frac

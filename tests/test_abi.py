@@ -36,7 +36,7 @@ def test_exports_every_declared_symbol(lib):
 def test_status_strings(lib):
     assert lsv.lsv_status_string(0) == "ok"
     assert "capacity" in lsv.lsv_status_string(lsv.LSV_ERR_CAPACITY)
-    assert lsv.lsv_abi_version() == 1
+    assert lsv.lsv_abi_version() == 2
 
 
 def test_timing_hook_validation(lib):
@@ -127,3 +127,4 @@ def test_host_validation(lib):
     # pack
     expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_pack_layer, cfg, 2, *([1] * 10), S)
     expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_workspace_clear, 1, 17, S)
+

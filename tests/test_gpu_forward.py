@@ -84,7 +84,7 @@ def _bf16_case(shape, seed, contexts, rows, tol=2e-2, bound=None, gains="random"
     B = len(contexts)
     w = gen.model_weights(shape, seed, gains)
     cap = runtime.kv_capacity(max(contexts) + max(rows) + 8)
-    gm = GpuModel(shape, w, B, cap, max_rows=max(64, int(sum(rows))))
+    gm = GpuModel(shape, w, B, cap, max_rows=max(64, int(sum(rows)), bound or 0))
     om = OF.Model(shape, w)
     oc = OF.KVCache(shape, B, cap)
     for l in range(shape.n_layers):
