@@ -225,6 +225,21 @@ int lsv_accept(int32_t mode, int32_t batch, int32_t vocab, const float* d_logits
                uint64_t round, int32_t* d_accept_len, int32_t* d_out_tokens, int32_t* d_seq_len,
                int32_t* d_status, void* d_workspace, size_t workspace_bytes, void* stream);
 
+/* lsv_accept without a caller workspace, for callers that cannot allocate device memory
+ * (code under HIP graph capture, serving loops or harnesses that forbid allocation).  Same
+ * arguments, rules and outputs as lsv_accept.  Its scratch lives in a device array that the
+ * library owns: LSV_ACCEPT_NOALLOC_BYTES per GPU, held until the process ends; nothing is
+ * allocated per call.  A call whose lsv_accept_workspace_bytes(batch, max_rows, vocab)
+ * exceeds that returns LSV_ERR_UNSUPPORTED and launches nothing (e.g. 512 rows fit up to a
+ * vocabulary of about 190K entries).  Every call on one GPU uses the same array: calls that
+ * may overlap on one GPU (other streams, other threads) race and must not be issued. */
+enum { LSV_ACCEPT_NOALLOC_BYTES = 512 * 1024 };
+int lsv_accept_noalloc(int32_t mode, int32_t batch, int32_t vocab, const float* d_logits,
+                       const int32_t* d_row_offsets, int32_t max_rows, int32_t max_rows_per_seq,
+                       const int32_t* d_tokens, const float* d_draft_probs, float temperature, uint64_t seed,
+                       uint64_t round, int32_t* d_accept_len, int32_t* d_out_tokens, int32_t* d_seq_len,
+                       int32_t* d_status, void* stream);
+
 /* -------------------------------------------------------- length selection */
 /* Choose the speculative length gamma_b per sequence from drafter confidences
  * q_1..q_G (Assumption 3.7 uses them in place of the target's acceptance

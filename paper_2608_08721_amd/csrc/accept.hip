@@ -8,6 +8,8 @@
 // exponential race for the correction / bonus token whose last workgroup commits.
 #include <math.h>
 
+#include <mutex>
+
 #include "lsv_device.h"
 #include "lsv_internal.h"
 
@@ -239,7 +241,7 @@ __global__ void __launch_bounds__(64) accept_sample_decide_kernel(const RowParti
                                                                   const int32_t* row_offsets, int batch, int max_rows,
                                                                   int width, const int32_t* tokens, uint64_t seed,
                                                                   uint64_t round, const int32_t* status,
-                                                                  SeqDecision* dec) {
+                                                                  SeqDecision* dec, int* counters) {
   const int b = blockIdx.x, lane = threadIdx.x;
   // a sequence that arrives with an error keeps it: the race kernel then emits nothing for it
   const int in_status = status ? status[b] : LSV_OK;
@@ -248,6 +250,7 @@ __global__ void __launch_bounds__(64) accept_sample_decide_kernel(const RowParti
       SeqDecision d = {};
       d.status = in_status;
       dec[b] = d;
+      counters[b] = 0;
     }
     return;
   }
@@ -263,10 +266,12 @@ __global__ void __launch_bounds__(64) accept_sample_decide_kernel(const RowParti
       SeqDecision d = {};
       d.status = LSV_ERR_INVALID_ARG;
       dec[b] = d;
+      counters[b] = 0;
     }
     return;
   }
   const int r0 = row_offsets[b], rows = row_offsets[b + 1] - r0, g = rows - 1;
+  if (lane == 0) counters[b] = 0;  // the race kernel's arrival counter starts from zero
   float m = -INFINITY, z = 0.f;
   int bad = 0;
   if (lane < rows) {
@@ -432,6 +437,29 @@ __global__ void __launch_bounds__(256) accept_sample_race_kernel(
   }
 }
 
+// ------------------------------------------------------------------ library-owned scratch
+// lsv_accept_noalloc: the same kernels on a device array the library owns (one copy per GPU,
+// held until the process ends).  Host code must use the address hipGetSymbolAddress returns
+// on the current device, never the array's name.
+static __device__ __align__(256) unsigned char scratch[kAcceptStaticBytes];
+constexpr int kMaxDevices = 64;
+static void* g_scratch[kMaxDevices];
+static std::mutex g_scratch_mu;
+
+int accept_scratch(void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) return LSV_ERR_HIP;
+  if (dev < 0 || dev >= kMaxDevices) return LSV_ERR_UNSUPPORTED;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return LSV_ERR_HIP;
+    g_scratch[dev] = p;
+  }
+  *out = g_scratch[dev];
+  return LSV_OK;
+}
+
 int launch_accept(int mode, int batch, int vocab, const float* logits, const int32_t* row_offsets, int max_rows,
                   int max_rows_per_seq, const int32_t* tokens, const float* draft_probs, float temperature,
                   uint64_t seed, uint64_t round, int32_t* accept_len, int32_t* out_tokens, int32_t* seq_len,
@@ -449,7 +477,7 @@ int launch_accept(int mode, int batch, int vocab, const float* logits, const int
                        temperature, w.rows);
     hipLaunchKernelGGL(accept_sample_decide_kernel, dim3(batch), dim3(64), 0, stream, w.rows, nc, logits, vocab,
                        draft_probs, temperature, row_offsets, batch, max_rows, max_rows_per_seq, tokens, seed, round,
-                       status, w.seq);
+                       status, w.seq, w.counters);
     hipLaunchKernelGGL(accept_sample_race_kernel, dim3(nc, batch), dim3(256), 0, stream, logits, vocab, draft_probs,
                        temperature, row_offsets, tokens, seed, round, w.seq, w.race, w.counters, max_rows_per_seq,
                        accept_len, out_tokens, seq_len, status);

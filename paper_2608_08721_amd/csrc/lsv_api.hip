@@ -195,6 +195,33 @@ int lsv_accept(int32_t mode, int32_t batch, int32_t vocab, const float* d_logits
   return hip_rc(rc, "accept");
 }
 
+int lsv_accept_noalloc(int32_t mode, int32_t batch, int32_t vocab, const float* d_logits,
+                       const int32_t* d_row_offsets, int32_t max_rows, int32_t max_rows_per_seq,
+                       const int32_t* d_tokens, const float* d_draft_probs, float temperature, uint64_t seed,
+                       uint64_t round, int32_t* d_accept_len, int32_t* d_out_tokens, int32_t* d_seq_len,
+                       int32_t* d_status, void* stream) {
+  if (mode != LSV_ACC_GREEDY && mode != LSV_ACC_SAMPLE) return fail(LSV_ERR_INVALID_ARG, "bad accept mode %d", mode);
+  if (batch < 1 || batch > LSV_MAX_BATCH || vocab < 1) return fail(LSV_ERR_INVALID_ARG, "bad batch or vocab");
+  if (max_rows < 1 || max_rows > LSV_MAX_ROWS || max_rows_per_seq < 1 || max_rows_per_seq > LSV_MAX_SEQ_ROWS)
+    return fail(LSV_ERR_INVALID_ARG, "bad max_rows %d (<= %d) / max_rows_per_seq %d (<= %d)", max_rows,
+                (int)LSV_MAX_ROWS, max_rows_per_seq, (int)LSV_MAX_SEQ_ROWS);
+  if (!d_logits || !d_row_offsets || !d_tokens || !d_accept_len || !d_out_tokens)
+    return fail(LSV_ERR_INVALID_ARG, "NULL pointer");
+  if (mode == LSV_ACC_SAMPLE && (!d_draft_probs || !(temperature > 0.f) || !isfinite(temperature)))
+    return fail(LSV_ERR_INVALID_ARG, "sampling needs draft probabilities and a finite temperature > 0");
+  const size_t need = lsv::accept_workspace_bytes(batch, max_rows, vocab);
+  if (need > lsv::kAcceptStaticBytes)
+    return fail(LSV_ERR_UNSUPPORTED, "scratch of %zu bytes needed, the library's holds %zu (LSV_ACCEPT_NOALLOC_BYTES)",
+                need, lsv::kAcceptStaticBytes);
+  void* ws = nullptr;
+  int rc = lsv::accept_scratch(&ws);
+  if (rc != LSV_OK) return hip_rc(rc, "accept_noalloc scratch");
+  rc = lsv::launch_accept(mode, batch, vocab, d_logits, d_row_offsets, max_rows, max_rows_per_seq, d_tokens,
+                          d_draft_probs, temperature, seed, round, d_accept_len, d_out_tokens, d_seq_len, d_status, ws,
+                          (hipStream_t)stream);
+  return hip_rc(rc, "accept_noalloc");
+}
+
 int lsv_select_length(int32_t mode, int32_t batch, int32_t G, const float* d_conf, const double* d_cost, int32_t d_init,
                       int32_t d_max, double alpha, int32_t block_n, uint32_t flags, int32_t* d_gamma, int32_t* d_aux,
                       int32_t* d_row_offsets, int32_t* d_status, void* stream) {

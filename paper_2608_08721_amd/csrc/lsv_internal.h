@@ -32,6 +32,8 @@ void timing_after(int kernel, int index, hipStream_t st);
 constexpr int kAcceptChunk = 4096;  // vocabulary entries per workgroup in the row scans
 inline int accept_chunks(int vocab) { return (vocab + kAcceptChunk - 1) / kAcceptChunk; }
 size_t accept_workspace_bytes(int batch, int max_rows, int vocab);
+constexpr size_t kAcceptStaticBytes = LSV_ACCEPT_NOALLOC_BYTES;  // lsv_accept_noalloc's scratch per GPU
+int accept_scratch(void** out);  // that scratch on the current device (looked up once per device)
 int launch_accept(int mode, int batch, int vocab, const float* logits, const int32_t* row_offsets, int max_rows,
                   int max_rows_per_seq, const int32_t* tokens, const float* draft_probs, float temperature,
                   uint64_t seed, uint64_t round, int32_t* accept_len, int32_t* out_tokens, int32_t* seq_len,

@@ -15,6 +15,7 @@ LSV_OK, LSV_ERR_INVALID_ARG, LSV_ERR_UNSUPPORTED, LSV_ERR_HIP, LSV_ERR_CAPACITY,
 LSV_DTYPE_F32, LSV_DTYPE_BF16 = 0, 1
 LSV_MAX_BATCH, LSV_MAX_ROWS, LSV_MAX_G, LSV_MAX_SEQ_ROWS, LSV_WIDE_ROWS = 64, 512, 64, 64, 272
 LSV_KV_ALIGN = 64
+LSV_ACCEPT_NOALLOC_BYTES = 512 * 1024
 LSV_ACC_GREEDY, LSV_ACC_SAMPLE = 0, 1
 LSV_SEL_MARGINAL, LSV_SEL_EXHAUSTIVE, LSV_SEL_ALG1 = 0, 1, 2
 LSV_SEL_BONUS = 1
@@ -22,7 +23,7 @@ LSV_SEL_BONUS = 1
 EXPORTED = (
     "lsv_status_string", "lsv_last_error", "lsv_abi_version", "lsv_packed_model_bytes", "lsv_pack_globals",
     "lsv_pack_layer", "lsv_kv_cache_bytes", "lsv_verify_workspace_bytes", "lsv_workspace_clear",
-    "lsv_verify_block", "lsv_accept_workspace_bytes", "lsv_accept", "lsv_select_length", "lsv_select_joint", "lsv_next_length_g4", "lsv_pack_block", "lsv_next_roots",
+    "lsv_verify_block", "lsv_accept_workspace_bytes", "lsv_accept", "lsv_accept_noalloc", "lsv_select_length", "lsv_select_joint", "lsv_next_length_g4", "lsv_pack_block", "lsv_next_roots",
     "lsv_set_timing_events",
 )
 LSV_KERNEL_QKV, LSV_KERNEL_O, LSV_KERNEL_GATEUP, LSV_KERNEL_DOWN, LSV_KERNEL_LMHEAD, LSV_KERNEL_ATTENTION = range(6)
@@ -75,6 +76,7 @@ def load(path=LIB_PATH):
         "lsv_verify_block": (ctypes.c_int, [CP, P, P, I32, I32, P, P, P, I32, I32, P, P, P, SZ, P]),
         "lsv_accept_workspace_bytes": (SZ, [I32, I32, I32]),
         "lsv_accept": (ctypes.c_int, [I32, I32, I32, P, P, I32, I32, P, P, F32, U64, U64, P, P, P, P, P, SZ, P]),
+        "lsv_accept_noalloc": (ctypes.c_int, [I32, I32, I32, P, P, I32, I32, P, P, F32, U64, U64, P, P, P, P, P]),
         "lsv_select_length": (ctypes.c_int, [I32, I32, I32, P, P, I32, I32, F64, I32, U32, P, P, P, P, P]),
         "lsv_select_joint": (ctypes.c_int, [I32, I32, P, P, I32, U32, P, P, P, P, P]),
         "lsv_next_length_g4": (ctypes.c_int, [I32, P, P, P, I32, I32, P, P, P, P]),
@@ -177,6 +179,13 @@ def lsv_accept(mode, batch, vocab, logits, row_offsets, max_rows, max_rows_per_s
     _check(load().lsv_accept(mode, batch, vocab, _ptr(logits), _ptr(row_offsets), max_rows, max_rows_per_seq,
                              _ptr(tokens), _ptr(draft_probs), temperature, seed, round, _ptr(accept_len),
                              _ptr(out_tokens), _ptr(seq_len), _ptr(status), _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def lsv_accept_noalloc(mode, batch, vocab, logits, row_offsets, max_rows, max_rows_per_seq, tokens, draft_probs,
+                       temperature, seed, round, accept_len, out_tokens, seq_len, status, stream=None):
+    _check(load().lsv_accept_noalloc(mode, batch, vocab, _ptr(logits), _ptr(row_offsets), max_rows, max_rows_per_seq,
+                                     _ptr(tokens), _ptr(draft_probs), temperature, seed, round, _ptr(accept_len),
+                                     _ptr(out_tokens), _ptr(seq_len), _ptr(status), _stream(stream)))
 
 
 def lsv_select_length(mode, batch, G, conf, cost, d_init, d_max, alpha, block_n, flags, gamma, aux, row_offsets,

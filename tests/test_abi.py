@@ -128,3 +128,22 @@ def test_host_validation(lib):
     expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_pack_layer, cfg, 2, *([1] * 10), S)
     expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_workspace_clear, 1, 17, S)
 
+
+def test_accept_noalloc_host_checks(lib):
+    """The allocation-free acceptance validates like lsv_accept and refuses, before any HIP call,
+    a call whose scratch would not fit the library's fixed array (LSV_ACCEPT_NOALLOC_BYTES)."""
+    S = 0
+    expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_accept_noalloc, 3, 1, 10, 1, 1, 2, 2, 1, None, 0.0, 0, 0, 1, 1, None, None,
+           S)
+    expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_accept_noalloc, 1, 1, 10, 1, 1, 2, 2, 1, None, 1.0, 0, 0, 1, 1, None, None,
+           S)
+    expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_accept_noalloc, 0, 1, 10, None, 1, 2, 2, 1, None, 0.0, 0, 0, 1, 1, None,
+           None, S)
+    # 512 rows of a 300K vocabulary: 74 chunk partials per row need more than the fixed scratch
+    assert lsv.lsv_accept_workspace_bytes(8, lsv.LSV_MAX_ROWS, 300000) > lsv.LSV_ACCEPT_NOALLOC_BYTES
+    msg = expect(lsv.LSV_ERR_UNSUPPORTED, lsv.lsv_accept_noalloc, 0, 8, 300000, 1, 1, lsv.LSV_MAX_ROWS, 64, 1, None,
+                 0.0, 0, 0, 1, 1, None, None, S)
+    assert "scratch" in msg
+    # the largest configurations of the workloads fit: 8 x 33 rows of 128256, 4 x 17 rows of 152064
+    assert lsv.lsv_accept_workspace_bytes(8, 264, 128256) <= lsv.LSV_ACCEPT_NOALLOC_BYTES
+    assert lsv.lsv_accept_workspace_bytes(4, 68, 152064) <= lsv.LSV_ACCEPT_NOALLOC_BYTES
