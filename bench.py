@@ -4,19 +4,24 @@
 One step = the whole hot path on one batch:
   lsv_select_length (MARGINAL rule on the measured per-gamma cost table)
   -> lsv_verify_block (target forward over [root, x_1..x_gamma] against the KV cache)
-  -> lsv_accept (greedy; commits the cached length),
+  -> lsv_accept (greedy or speculative rejection sampling; commits the cached length),
 captured once as a HIP graph and replayed.  Inputs are resident in HBM before the
-timed region.  Default workload: Llama-3-8B-shaped random-init bf16 decoder (32
-layers, d 4096, 32/8 x 128 heads, SwiGLU 14336, vocab 128256), batch 1, context
-2048 prefilled from seeded random prompt ids, 16 drafted ids with confidences
-Beta(8, 2) * 0.92^i.
+timed region.  Default workload: Llama-3-70B-shaped random-init bf16 decoder (80
+layers, d 8192, 64/8 x 128 heads, SwiGLU 28672, vocab 128256), batch 4, context 8192
+per sequence prefilled from seeded random prompt ids, 32 drafted tokens per sequence
+with confidences Beta(5, 3) * 0.9^i, greedy acceptance.  The drafts are planted: draft
+v is the target's own greedy token with probability equal to its confidence, so the
+realized acceptance follows the confidence model.
 
-Prints one JSON line (rank 0).  `value` = verified tokens per second
-(batch * (gamma + 1) / step time); the per-gamma latency sweep is in `sweep`.
+Prints one JSON line.  `value` = expected emitted tokens per second of the timed step
+(sum over sequences of 1 + N_b(gamma_b), divided by the step latency); the line also
+carries the realized tokens, the verified rows per second, and per gamma the latency,
+tokens/s and the HBM / MFMA fractions (`per_gamma`).  `other_workloads` holds the same
+figures for the --secondary workloads (default: Llama-3-8B shape, batch 1, context 2048).
 With --rounds R (default 0: off, so profiles of the step see only its kernels) the line also
-carries `decode_loop`: R rounds of multi-round decoding per
-length policy (static lengths, the marginal rule, Algorithm 1, the G4-style rule) fed by a
-planted calibrated drafter, as tokens per second against plain greedy decoding.
+carries `decode_loop`: R rounds of multi-round decoding per length policy (static lengths,
+the marginal rule, Algorithm 1, the G4-style rule) fed by a planted calibrated drafter, as
+tokens per second against plain greedy decoding.
 """
 import argparse
 import ctypes
@@ -40,11 +45,18 @@ MFMA_PEAK_FLOPS = 2.5e15  # dense bf16
 def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=100)
-    p.add_argument("--warmup", type=int, default=10)
-    p.add_argument("--workload", default="llama3-8b-b1-c2048")
-    p.add_argument("--sweep-reps", type=int, default=20)
-    p.add_argument("--roofline-steps", type=int, default=5)
+    p.add_argument("--steps", type=int, default=50)
+    p.add_argument("--warmup", type=int, default=5)
+    p.add_argument("--workload", default="llama3-70b-b4")
+    p.add_argument("--secondary", default="llama3-8b-b1-c2048",
+                   help="comma-separated workloads also measured after the primary one (their step, sweep and "
+                        "dominant kernel only), or 'none'")
+    p.add_argument("--secondary-steps", type=int, default=50)
+    p.add_argument("--drafts", choices=("planted", "uniform"), default="planted",
+                   help="greedy workloads: drafts planted from the target's own greedy continuation with "
+                        "probability equal to their confidence, or the configs' uniform random ids")
+    p.add_argument("--sweep-reps", type=int, default=10)
+    p.add_argument("--roofline-steps", type=int, default=3)
     p.add_argument("--accept", choices=("greedy", "sample"), default=None,
                    help="acceptance rule of the timed steps (default: greedy where the workload has it, else "
                         "speculative rejection sampling at the workload's temperature)")
@@ -56,9 +68,7 @@ def parse():
     p.add_argument("--summarize", nargs=3, metavar=("TRACE_DIR", "FETCH_DIR", "WRITE_DIR"),
                    help="no GPU work: turn the csv output of three rocprofv3 runs of this script (kernel trace, "
                         "--pmc FETCH_SIZE, --pmc WRITE_SIZE; each dir also holds that run's bench.json) into the "
-                        "gate/up profile summary")
-    p.add_argument("--sweep-reps-counters", type=int, default=1,
-                   help="--sweep-reps of the two counter runs (with --summarize)")
+                        "gate/up profile summary of the run's workload")
     p.add_argument("--summarize-mfma", nargs=2, metavar=("TRACE_DIR", "PMC_DIR"),
                    help="no GPU work: matrix-core summary of the batched workload's uniform-gamma-max sweep "
                         "step from a kernel-trace run and a --pmc SQ_INSTS_MFMA SQ_VALU_MFMA_BUSY_CYCLES run "
@@ -92,14 +102,16 @@ class HipEvents:
 
 def gateup_bytes(m, rows):
     """Algorithmic HBM bytes of one gate/up launch: the packed gate and up weights once, the
-    storage-type activation rows and their per-16-column norm statistics in, the SwiGLU
-    output out."""
+    normalised activation rows in, the SwiGLU output out."""
     es = 2 if m.dtype == "bf16" else 4
-    return 2 * m.d_ff * m.d_model * es + rows * m.d_model * es + rows * (m.d_model // 16) * 4 + rows * m.d_ff * es
+    return 2 * m.d_ff * m.d_model * es + rows * m.d_model * es + rows * m.d_ff * es
 
 
-GATEUP_PROFILE = os.path.join(ROOT, "profiles", "gemm_gateup_llama3-8b-b1-c2048.md")
 KERNEL_SOURCES = ("gemm.hip", "lsv_gemm.h", "lsv_device.h", "forward.hip")
+
+
+def gateup_profile(workload):
+    return os.path.join(ROOT, "profiles", f"gemm_gateup_{workload}.md")
 
 
 def kernel_source_hash():
@@ -111,11 +123,11 @@ def kernel_source_hash():
     return h.hexdigest()[:16]
 
 
-def measured_traffic(rows):
-    """HBM bytes (read + written) per gate/up launch at `rows` block rows, from the committed
-    counter profile; None when the kernel sources changed since the counters were taken."""
+def measured_traffic(workload, rows):
+    """HBM bytes (read + written) per gate/up launch of `workload` at `rows` block rows, from the
+    committed counter profile; None when there is none or the kernel sources changed since."""
     try:
-        lines = open(GATEUP_PROFILE).read().splitlines()
+        lines = open(gateup_profile(workload)).read().splitlines()
     except OSError:
         return None
     vals = dict(l.split(":", 1) for l in lines if l.startswith(("source_hash:", "traffic_rows_")))
@@ -125,7 +137,13 @@ def measured_traffic(rows):
     return None if v is None else float(v)
 
 
-GATEUP_KERNEL = "gemm_kernel<unsigned short, 2, 2>"  # bf16 gate/up + SwiGLU, up to 32 rows
+def is_gateup(name):
+    """The gate/up + SwiGLU launches: the 64-row kernel (kind 2, or 5 = the wide-model
+    configuration) and the batched one (epilogue 3)."""
+    return ("gemm_kernel<unsigned short, 2," in name or "gemm_kernel<unsigned short, 5," in name
+            or "gemm_wide_kernel<3>" in name)
+
+
 SELECT_KERNEL = "select_length_kernel"
 CALIB_BYTES = 256 << 20
 
@@ -135,11 +153,25 @@ def _short(name):
     return name.split("(")[0] if not name.startswith("__") else name
 
 
-def summarize(trace_dir, fetch_dir, write_dir, reps_c):
-    """Profile summary (markdown) of the default workload from three rocprofv3 runs of this
-    script.  Dispatches are attributed by their order, which the script fixes: for each
-    gamma = 1..G the sweep runs its graph body 1 + 3 + reps times; then one eager step,
-    `warmup` + `steps` replays of the step graph and the eager roofline steps."""
+def _launch_groups(rows):
+    """Dispatches of one logical gate/up launch: under a batched row bound the 64-row and the
+    batched kernel run back to back (one of them returns at once), so runs of consecutive
+    dispatch ids form one launch."""
+    groups = []
+    for r in rows:
+        if groups and int(r["Dispatch_Id"]) == int(groups[-1][-1]["Dispatch_Id"]) + 1:
+            groups[-1].append(r)
+        else:
+            groups.append([r])
+    return groups
+
+
+def summarize(trace_dir, fetch_dir, write_dir):
+    """Profile summary (markdown) of the dominant kernel from three rocprofv3 runs of this
+    script (--secondary none): the gate/up launches of the eager roofline steps (the last
+    gate/up launches of the run), their kernel-trace durations and HBM counters, and the
+    per-kernel split of the timed graph replays.  The timed region runs from the selector
+    launch of the first timed replay to that of the first roofline step."""
     import csv
     import glob
     from synth import configs
@@ -154,13 +186,15 @@ def summarize(trace_dir, fetch_dir, write_dir, reps_c):
 
     bt = bench_json(trace_dir)
     wl = configs.WORKLOADS[bt["config"]["workload"]]
-    m, G, L = wl.model, wl.G, wl.model.n_layers
+    m = wl.model
+    rows = bt["roofline"]["rows"]
     trace = sorted(csv.DictReader(open(one(trace_dir, "*kernel_trace.csv"))), key=lambda r: int(r["Dispatch_Id"]))
     dur = lambda r: (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
-    gu = [r for r in trace if GATEUP_KERNEL in r["Kernel_Name"]]
     n_roof = bt["roofline"]["launches_timed"]
-    roof = [dur(r) for r in gu[-n_roof:]]
-    # timed region: from the first timed replay's selector launch to the first roofline step's
+    gu = _launch_groups([r for r in trace if is_gateup(r["Kernel_Name"])])[-n_roof:]
+    roof_sum = [sum(dur(r) for r in g) for g in gu]
+    roof_span = [(int(g[-1]["End_Timestamp"]) - int(g[0]["Start_Timestamp"])) / 1e3 for g in gu]
+    names = sorted({_short(r["Kernel_Name"]) for g in gu for r in g})
     sel = [r for r in trace if SELECT_KERNEL in r["Kernel_Name"]]
     i0 = 3 + 1 + bt["warmup"]
     t_lo, t_hi = int(sel[i0]["Start_Timestamp"]), int(sel[i0 + bt["steps"]]["Start_Timestamp"])
@@ -173,11 +207,13 @@ def summarize(trace_dir, fetch_dir, write_dir, reps_c):
 
     out = []
     w = out.append
-    cmd_t = ("rocprofv3 --kernel-trace --stats --output-format csv -d gpurun_out/pf/trace -o t -- "
-             f"python3 bench.py --steps {bt['steps']} --warmup {bt['warmup']} --no-cpu-baseline")
-    cmd_c = ("rocprofv3 --pmc {c} --output-format csv -d gpurun_out/pf/{d} -o {o} -- python3 bench.py --steps 2 "
-             f"--warmup 1 --sweep-reps {reps_c} --roofline-steps 1 --no-cpu-baseline --calib-copy")
-    w(f"# gate/up GEMM + SwiGLU: {wl.name} ({m.name} shape, batch {wl.batch}, context {bt['config']['context']})")
+    base = f"python3 bench.py --workload {wl.name} --secondary none --no-cpu-baseline"
+    cmd_t = (f"rocprofv3 --kernel-trace --stats --output-format csv -d gpurun_out/pf/trace -o t -- {base} "
+             f"--steps {bt['steps']} --warmup {bt['warmup']}")
+    cmd_c = ("rocprofv3 --pmc {c} --output-format csv -d gpurun_out/pf/{d} -o {o} -- " + base +
+             " --steps 2 --warmup 1 --sweep-reps 1 --roofline-steps 1 --calib-copy")
+    w(f"# gate/up GEMM + SwiGLU: {wl.name} ({m.name} shape, batch {wl.batch}, context {bt['config']['context']}, "
+      f"{rows} rows)")
     w("")
     w("Commands (repository root, after `cd /tmp && export TMPDIR=/tmp` for the profiler's own files; each")
     w("run's stdout saved as bench.json in its output directory):")
@@ -194,10 +230,11 @@ def summarize(trace_dir, fetch_dir, write_dir, reps_c):
     w("## Timing run")
     w("")
     w(f"- bench line: {bt['ms_per_step'] * 1e3:.1f} us per step at gamma {bt['config']['gamma']} "
-      f"({bt['value']:.0f} verified tokens/s), step HBM fraction {bt['step']['hbm_frac']:.3f}")
-    w(f"- gate/up launches of the eager roofline steps: {len(roof)}, average {statistics.mean(roof):.2f} us in the "
-      f"kernel trace vs {bt['roofline']['avg_launch_us']:.2f} us from the script's HIP events "
-      f"(frac {bt['roofline']['frac']:.3f} of 8 TB/s)")
+      f"({bt['value']:.1f} tokens/s), step HBM fraction {bt['step']['hbm_frac']:.3f}")
+    w(f"- gate/up launches of the eager roofline steps: {len(gu)} ({', '.join(names)}); kernel time "
+      f"{statistics.mean(roof_sum):.2f} us per launch on average (first dispatch start to last dispatch end: "
+      f"{statistics.mean(roof_span):.2f} us) vs {bt['roofline']['avg_launch_us']:.2f} us from the script's HIP "
+      f"events (frac {bt['roofline']['frac']:.3f} of 8 TB/s)")
     w(f"- timed graph replays: kernels busy {busy:.1f} us of {bt['ms_per_step'] * 1e3:.1f} us per step")
     w("")
     w("| kernel (timed replays) | launches/step | avg us | us/step | share |")
@@ -207,44 +244,38 @@ def summarize(trace_dir, fetch_dir, write_dir, reps_c):
           f"{sum(v) / steps / busy * 100:.1f}% |")
     w("")
 
-    # counters
-    def counters(d, pat, name):
-        rows = sorted(csv.DictReader(open(one(d, pat))), key=lambda r: int(r["Dispatch_Id"]))
-        rows = [r for r in rows if r["Counter_Name"] == name]
-        copy = [float(r["Counter_Value"]) for r in rows if "copyBuffer" in r["Kernel_Name"]
+    def counters(d, name):
+        rs = sorted(csv.DictReader(open(one(d, "*counter_collection.csv"))), key=lambda r: int(r["Dispatch_Id"]))
+        rs = [r for r in rs if r["Counter_Name"] == name]
+        copy = [float(r["Counter_Value"]) for r in rs if "copyBuffer" in r["Kernel_Name"]
                 and int(r["Grid_Size"]) >= 131072]
-        kib = copy[-1]
-        g = [float(r["Counter_Value"]) for r in rows if GATEUP_KERNEL in r["Kernel_Name"]]
-        return kib, g
-    f_copy, f_gu = counters(fetch_dir, "*counter_collection.csv", "FETCH_SIZE")
-    w_copy, w_gu = counters(write_dir, "*counter_collection.csv", "WRITE_SIZE")
+        groups = _launch_groups([r for r in rs if is_gateup(r["Kernel_Name"])])
+        bc = json.loads(open(os.path.join(d, "bench.json")).read().strip().splitlines()[-1])
+        last = groups[-bc["roofline"]["launches_timed"]:]
+        assert bc["roofline"]["rows"] == rows, (bc["roofline"]["rows"], rows)
+        return copy[-1], [sum(float(r["Counter_Value"]) for r in g) for g in last]
+    f_copy, f_gu = counters(fetch_dir, "FETCH_SIZE")
+    w_copy, w_gu = counters(write_dir, "WRITE_SIZE")
     f_scale = (CALIB_BYTES / 1024) / f_copy
     w_scale = (CALIB_BYTES / 1024) / w_copy
-    per_g = (1 + 3 + reps_c) * L
-    assert len(f_gu) == len(w_gu) and len(f_gu) >= G * per_g, (len(f_gu), len(w_gu), G * per_g)
+    rd = statistics.mean(f_gu) * 1024 * f_scale
+    wr = statistics.mean(w_gu) * 1024 * w_scale
+    alg = gateup_bytes(m, rows)
     w("## HBM traffic (two counter runs)")
     w("")
     w(f"Calibration: a plain {CALIB_BYTES >> 20} MiB device copy reads FETCH_SIZE {f_copy:.0f} KiB and "
       f"WRITE_SIZE {w_copy:.0f} KiB, so FETCH_SIZE is scaled by {f_scale:.3f} and WRITE_SIZE by {w_scale:.3f}.")
-    w("Per-launch traffic of the gate/up kernel in the sweep graph of each gamma (rows = gamma + 1; "
-      f"{per_g} launches each), against the algorithmic bytes:")
+    w(f"Per gate/up launch of the roofline step ({len(f_gu)} launches at {rows} rows, counters of both dispatches "
+      "of a launch summed), against the algorithmic bytes:")
     w("")
     w("| rows | read MB | written MB | traffic MB | algorithmic MB | ratio |")
     w("|---:|---:|---:|---:|---:|---:|")
-    keys = []
-    for g in range(1, G + 1):
-        sl = slice((g - 1) * per_g, g * per_g)
-        rd = statistics.mean(f_gu[sl]) * 1024 * f_scale
-        wr = statistics.mean(w_gu[sl]) * 1024 * w_scale
-        alg = gateup_bytes(m, g + 1)
-        w(f"| {g + 1} | {rd / 1e6:.2f} | {wr / 1e6:.2f} | {(rd + wr) / 1e6:.2f} | {alg / 1e6:.2f} | "
-          f"{(rd + wr) / alg:.3f} |")
-        keys.append(f"traffic_rows_{g + 1}: {rd + wr:.0f}")
+    w(f"| {rows} | {rd / 1e6:.2f} | {wr / 1e6:.2f} | {(rd + wr) / 1e6:.2f} | {alg / 1e6:.2f} | {(rd + wr) / alg:.3f} |")
     w("")
     w("Bytes per launch (read + written) by block rows, read by bench.py while source_hash matches:")
     w("")
     w("```")
-    out += keys
+    w(f"traffic_rows_{rows}: {rd + wr:.0f}")
     w("```")
     return "\n".join(out) + "\n"
 
@@ -395,37 +426,55 @@ def step_flops(m, contexts, rows_per_seq):
     return 2 * M * m.matmul_params() + m.n_layers * att
 
 
-def cpu_baseline(m, seed, C, rows, tokens, gamma):
-    """The oracle (fp64 numpy) on a bounded sample of the same workload: one verify of the
-    block at full width with 1 and then 2 layers (+ embedding and LM head), context from the
-    seeded KV generator; the per-layer time is extrapolated to all layers."""
+def expected_tokens(conf_np, gammas):
+    """Expected emitted tokens of one step under the drafter-confidence model (Assumption 3.7):
+    sum_b 1 + N_b(gamma_b), N_b(g) = sum_{j<=g} prod_{k<=j} q_{b,k} (Eq. 2's numerator)."""
+    e = 0.0
+    for b, g in enumerate(gammas):
+        e += 1.0 + float(np.cumprod(conf_np[b].astype(np.float64))[:g].sum())
+    return e
+
+
+def cpu_baseline(m, seed, ctx, rows_per_seq, tokens, exp_tok):
+    """The oracle (fp64 numpy) on a bounded sample of the same step: the verify forward of the
+    same block (every sequence, every row) at full width with 1 and then 2 of the model's layers
+    (+ embedding and LM head), followed by greedy acceptance, context from the seeded KV generator;
+    the per-layer time is extrapolated to all layers.  Value: the step's expected emitted tokens
+    per second of oracle time."""
     from threadpoolctl import threadpool_info
 
+    from oracle import accept as OA
     from oracle import forward as OF
     from synth import gen
+    B = len(ctx)
+    off = np.concatenate([[0], np.cumsum(rows_per_seq)]).astype(np.int64)
     ws = {"embed": gen.embed_weights(m, seed), "final_norm": gen.final_norm_weights(m),
           "lm_head": gen.lm_head_weights(m, seed), "layers": [gen.layer_weights(m, seed, l) for l in range(2)]}
     times = []
     for L in (1, 2):
         shape = m.with_layers(L)
-        cache = OF.KVCache(shape, 1, C + rows)
+        cache = OF.KVCache(shape, B, max(ctx) + max(rows_per_seq))
         for l in range(L):
-            k, v = gen.synthetic_kv(shape, seed, l, 1, C)
-            cache.k[l][0, :, :C] = OF.stored_to_f64(k[0], m.dtype)
-            cache.v[l][0, :, :C] = OF.stored_to_f64(v[0], m.dtype)
+            for b in range(B):
+                k, v = gen.synthetic_kv(shape, seed + 31 * b, l, 1, ctx[b])
+                cache.k[l][b, :, :ctx[b]] = OF.stored_to_f64(k[0], m.dtype)
+                cache.v[l][b, :, :ctx[b]] = OF.stored_to_f64(v[0], m.dtype)
         model = OF.Model(shape, {**ws, "layers": ws["layers"][:L]})
         t0 = time.perf_counter()
-        OF.verify_block(model, cache, [C], tokens[:rows], [0, rows])
+        lg, _ = OF.verify_block(model, cache, ctx, tokens, off)
+        OA.accept_greedy(lg, off, tokens)
         times.append(time.perf_counter() - t0)
+        log(f"cpu baseline: {L} layer(s) {times[-1]:.1f} s")
     per_layer = max(times[1] - times[0], 1e-9)
     fixed = max(times[0] - per_layer, 0.0)
     t_step = fixed + m.n_layers * per_layer
     threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
-    return {"value": rows / t_step, "unit": "verified tokens/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"fp64 numpy oracle, one verify of {rows} rows (gamma {gamma}) at {m.name} width with 1 and 2 "
-                      f"of {m.n_layers} layers + embedding + LM head, context {C} (seeded KV); "
-                      f"{times[0]:.1f} s + {times[1]:.1f} s measured, per-layer time extrapolated to "
-                      f"{m.n_layers} layers; host cpu_count {os.cpu_count()}",
+    return {"value": exp_tok / t_step, "unit": "tokens/s (expected emitted, confidence model)", "cores": int(threads),
+            "kind": "oracle",
+            "sample": f"fp64 numpy oracle: the step's verify forward ({sum(rows_per_seq)} rows over {B} sequences, "
+                      f"contexts {sorted(set(ctx))}) at {m.name} width with 1 and 2 of {m.n_layers} layers + embedding "
+                      f"+ LM head, then greedy acceptance; {times[0]:.1f} s + {times[1]:.1f} s measured, per-layer "
+                      f"time extrapolated to {m.n_layers} layers; host cpu_count {os.cpu_count()}",
             "seconds_per_step": t_step}
 
 
@@ -532,87 +581,125 @@ def decode_loop_measure(m, cfg, dm, B, G, ctx, prompts, pre, rows_buf, roots, co
     return out
 
 
-def main():
-    args = parse()
-    if args.summarize:
-        sys.stdout.write(summarize(*args.summarize, args.sweep_reps_counters))
-        return
-    if args.summarize_mfma:
-        sys.stdout.write(summarize_mfma(*args.summarize_mfma))
-        return
-    if args.gpus != 1:
-        print(f"bench.py runs on one GPU only: this build has no multi-GPU path (asked for --gpus {args.gpus}).",
-              file=sys.stderr)
-        sys.exit(2)
+class Workload:
+    """One workload's device state: packed model, KV cache prefilled from seeded prompts,
+    workspaces and the pending root token of every sequence (all untimed set-up)."""
+
+    def __init__(self, wl, dev):
+        import torch
+
+        from paper_2608_08721_amd import lsv, runtime
+        from synth import gen
+        self.wl, self.m, self.dev = wl, wl.model, dev
+        m = self.m
+        self.i32 = lambda x: torch.tensor(np.asarray(x, dtype=np.int32), device=dev)
+        self.seed, self.B, self.G = wl.seed, wl.batch, wl.G
+        B, G = self.B, self.G
+        self.ctx = [int(c) for c in gen.contexts(wl)]
+        self.rows_seq = G + 1                # root + drafts per sequence
+        # prefill rows per sequence and call: for batches, keep the whole block within the
+        # batched GEMM path's row bound
+        self.pre = 64 if B == 1 else max(1, min(64, lsv.LSV_WIDE_ROWS // B))
+        self.rows_step = B * self.rows_seq   # host row bound of the verify steps
+        self.rows_buf = max(self.rows_step, B * self.pre)
+        self.cap = runtime.kv_capacity(max(self.ctx) + self.rows_seq)
+        self.cfg = runtime.model_config(m)
+        t0 = time.time()
+        self.dm = runtime.DeviceModel(self.cfg, dev)
+        self.dm.pack_globals(gen.embed_weights(m, self.seed), gen.final_norm_weights(m),
+                             gen.lm_head_weights(m, self.seed))
+        for l in range(m.n_layers):
+            self.dm.pack_layer(l, gen.layer_weights(m, self.seed, l))
+            if l % 8 == 7:
+                log(f"{wl.name}: packed layer {l + 1}/{m.n_layers} ({time.time() - t0:.1f} s)")
+        self.kv = runtime.KVCache(self.cfg, B, self.cap, dev)
+        self.ws = runtime.Workspace(lsv.lsv_verify_workspace_bytes(self.cfg, B, self.rows_buf, self.cap), dev)
+        self.aws = runtime.Workspace(lsv.lsv_accept_workspace_bytes(B, self.rows_buf, m.vocab), dev)
+        self.logits = torch.zeros((self.rows_buf, m.vocab), dtype=torch.float32, device=dev)
+        self.status = torch.zeros(B, dtype=torch.int32, device=dev)
+        self.acc = torch.zeros(B, dtype=torch.int32, device=dev)
+        self.out = torch.zeros((B, self.rows_seq), dtype=torch.int32, device=dev)
+        # prefill every context from seeded prompt ids, in chunks of `pre` rows per sequence; a
+        # sequence starts late enough that all of them end in the last call
+        self.prompts = gen.prefix_ids(self.seed, B, self.ctx, m.vocab)
+        chunks = [(c + self.pre - 1) // self.pre for c in self.ctx]
+        n_calls = max(chunks)
+        filled = [0] * B
+        for i in range(n_calls):
+            take = []
+            for b in range(B):
+                first = n_calls - chunks[b]
+                take.append(0 if i < first else (self.ctx[b] - (chunks[b] - 1) * self.pre if i == first else self.pre))
+            off = runtime.row_offsets_of(take)
+            toks = np.concatenate([self.prompts[b][filled[b]:filled[b] + take[b]] for b in range(B)])
+            self.verify(filled, toks, off, self.rows_buf)
+            filled = [filled[b] + take[b] for b in range(B)]
+        assert filled == self.ctx
+        # roots = greedy tokens after each prompt, by the library's own acceptance on one row each
+        last_rows = torch.tensor(off[1:] - 1, dtype=torch.long, device=dev)
+        self.status.zero_()
+        lsv.lsv_accept(lsv.LSV_ACC_GREEDY, B, m.vocab, self.logits[last_rows].contiguous(),
+                       self.i32(np.arange(B + 1)), B, self.rows_seq, self.i32([p[-1] for p in self.prompts]), None,
+                       0.0, 0, 0, self.acc, self.out, None, self.status, self.aws.buf, self.aws.nbytes)
+        torch.cuda.synchronize()
+        assert bool((self.status == 0).all())
+        self.roots = [int(x) for x in self.out[:, 0].cpu()]
+        log(f"{wl.name}: model + prefill of {self.ctx} tokens ready ({time.time() - t0:.1f} s); roots {self.roots}")
+
+    def verify(self, seq_len, toks, off, bound):
+        from paper_2608_08721_amd import lsv
+        lsv.lsv_verify_block(self.cfg, self.dm.buf, self.kv.buf, self.cap, self.B, self.i32(seq_len), self.i32(toks),
+                             self.i32(off), bound, self.cap, self.logits, self.status, self.ws.buf, self.ws.nbytes)
+
+    def greedy_continuation(self, n):
+        """The target's own greedy tokens after each root, [B, n], by n plain decoding steps of
+        one row per sequence (their K/V go to the positions every verify block rewrites)."""
+        import torch
+
+        from paper_2608_08721_amd import lsv, runtime
+        B = self.B
+        cur, pos, cont = list(self.roots), list(self.ctx), []
+        off = runtime.row_offsets_of([1] * B)
+        for _ in range(n):
+            self.verify(pos, cur, off, self.rows_buf)
+            self.status.zero_()
+            lsv.lsv_accept(lsv.LSV_ACC_GREEDY, B, self.m.vocab, self.logits, self.i32(off), B, 1, self.i32(cur),
+                           None, 0.0, 0, 0, self.acc, self.out, None, self.status, self.aws.buf, self.aws.nbytes)
+            torch.cuda.synchronize()
+            assert bool((self.status == 0).all())
+            cur = [int(x) for x in self.out[:, 0].cpu()]
+            cont.append(cur)
+            pos = [p + 1 for p in pos]
+        return np.array(cont, dtype=np.int64).T
+
+    def free(self):
+        import torch
+        for k in ("dm", "kv", "ws", "aws", "logits"):
+            setattr(self, k, None)
+        torch.cuda.empty_cache()
+
+
+def measure(w, args, primary=True):
+    """The measurement of one workload: per-gamma sweep (the measured cost table), selection,
+    the timed select -> verify -> accept graph, the dominant kernel's events, and (primary
+    workload only) the decode loop and the CPU baseline."""
     import torch
 
     from paper_2608_08721_amd import lsv, runtime
-    from synth import configs, gen
-
-    wl = configs.WORKLOADS[args.workload]
-    m = wl.model
+    from synth import drafter, gen
+    wl, m, dev, i32 = w.wl, w.m, w.dev, w.i32
+    seed, B, G, ctx, roots = w.seed, w.B, w.G, w.ctx, w.roots
+    rows_step, rows_seq, cap = w.rows_step, w.rows_seq, w.cap
+    cfg, dm, kv, ws, aws, logits, status, acc, out = (w.cfg, w.dm, w.kv, w.ws, w.aws, w.logits, w.status, w.acc,
+                                                      w.out)
     mode_name = args.accept or ("greedy" if "greedy" in wl.accept else "sample")
     if mode_name not in wl.accept:
         raise SystemExit(f"workload {wl.name} has no {mode_name} acceptance")
     sampling = mode_name == "sample"
-    torch.cuda.set_device(0)
-    dev = "cuda"
-    i32 = lambda x: torch.tensor(np.asarray(x, dtype=np.int32), device=dev)
-    seed, B, G = wl.seed, wl.batch, wl.G
-    ctx = [int(c) for c in gen.contexts(wl)]
-    rows_seq = G + 1                     # root + drafts per sequence
-    # prefill rows per sequence and call: for batches, keep the whole block within the
-    # batched GEMM path's row bound
-    pre = 64 if B == 1 else max(1, min(64, lsv.LSV_WIDE_ROWS // B))
-    rows_step = B * rows_seq            # host row bound of the verify steps
-    rows_buf = max(rows_step, B * pre)  # buffers also hold a prefill chunk
-    cap = runtime.kv_capacity(max(ctx) + rows_seq)
-    cfg = runtime.model_config(m)
+    conf_np = gen.confidences(wl)
 
-    # ---- model: seeded weights, generated and packed one layer at a time (untimed)
-    t0 = time.time()
-    dm = runtime.DeviceModel(cfg, dev)
-    dm.pack_globals(gen.embed_weights(m, seed), gen.final_norm_weights(m), gen.lm_head_weights(m, seed))
-    for l in range(m.n_layers):
-        dm.pack_layer(l, gen.layer_weights(m, seed, l))
-        if l % 8 == 7:
-            log(f"packed layer {l + 1}/{m.n_layers} ({time.time() - t0:.1f} s)")
-    kv = runtime.KVCache(cfg, B, cap, dev)
-    ws = runtime.Workspace(lsv.lsv_verify_workspace_bytes(cfg, B, rows_buf, cap), dev)
-    aws = runtime.Workspace(lsv.lsv_accept_workspace_bytes(B, rows_buf, m.vocab), dev)
-    logits = torch.zeros((rows_buf, m.vocab), dtype=torch.float32, device=dev)
-    status = torch.zeros(B, dtype=torch.int32, device=dev)
-
-    # ---- prefill every context from seeded prompt ids (untimed), in chunks of `pre` rows per
-    # sequence; a sequence starts late enough that all of them end in the last call
-    prompts = gen.prefix_ids(seed, B, ctx, m.vocab)
-    chunks = [(c + pre - 1) // pre for c in ctx]
-    n_calls = max(chunks)
-    filled = [0] * B
-    for i in range(n_calls):
-        take = []
-        for b in range(B):
-            first = n_calls - chunks[b]
-            take.append(0 if i < first else (ctx[b] - (chunks[b] - 1) * pre if i == first else pre))
-        off = runtime.row_offsets_of(take)
-        toks = np.concatenate([prompts[b][filled[b]:filled[b] + take[b]] for b in range(B)])
-        lsv.lsv_verify_block(cfg, dm.buf, kv.buf, cap, B, i32(filled), i32(toks), i32(off), rows_buf, cap, logits,
-                             status, ws.buf, ws.nbytes)
-        filled = [filled[b] + take[b] for b in range(B)]
-    assert filled == ctx
-    last_rows = torch.tensor(off[1:] - 1, dtype=torch.long, device=dev)
-    acc = torch.zeros(B, dtype=torch.int32, device=dev)
-    out = torch.zeros((B, rows_seq), dtype=torch.int32, device=dev)
-    # roots = greedy tokens after each prompt, chosen by the library's own acceptance on one row each
-    lsv.lsv_accept(lsv.LSV_ACC_GREEDY, B, m.vocab, logits[last_rows].contiguous(), i32(np.arange(B + 1)), B,
-                   rows_seq, i32([p[-1] for p in prompts]), None, 0.0, 0, 0, acc, out, None, status, aws.buf,
-                   aws.nbytes)
-    torch.cuda.synchronize()
-    assert bool((status == 0).all())
-    roots = [int(x) for x in out[:, 0].cpu()]
-    log(f"model + prefill of {ctx} tokens ready ({time.time() - t0:.1f} s); roots {roots}")
-
-    drafts = gen.draft_ids(seed, B, G, m.vocab)
+    # drafts: planted (the target's own greedy token with probability equal to its confidence,
+    # so realized acceptance follows the confidence model) or the configs' uniform random ids
     if sampling:
         # draft distributions q_v (a seeded softmax of N(0,1) logits per drafted position) and
         # drafts drawn from them; accept rows index q at (row offset - b + v - 1) < B * G
@@ -622,14 +709,23 @@ def main():
                             for v in range(G)] for b in range(B)], dtype=np.int64)
         q_dev = torch.tensor(q_np, dtype=torch.float32, device=dev)
         acc_mode, acc_q, acc_T = lsv.LSV_ACC_SAMPLE, q_dev, float(wl.temperature)
-    else:
+        draft_kind = "drawn from the seeded draft distributions"
+    elif args.drafts == "planted":
+        t0 = time.time()
+        cont = w.greedy_continuation(G)
+        drafts = drafter.plant_block(cont, conf_np, seed, m.vocab)
         acc_mode, acc_q, acc_T = lsv.LSV_ACC_GREEDY, None, 0.0
+        draft_kind = "planted: the target's greedy token with probability = its confidence"
+        log(f"{wl.name}: greedy continuation of {G} tokens per sequence ({time.time() - t0:.1f} s)")
+    else:
+        drafts = gen.draft_ids(seed, B, G, m.vocab)
+        acc_mode, acc_q, acc_T = lsv.LSV_ACC_GREEDY, None, 0.0
+        draft_kind = "uniform random ids"
 
     def layout(gammas):
         """Verify rows [root_b, x_1..x_gamma_b] per sequence, concatenated."""
         return i32(np.concatenate([[roots[b]] + list(drafts[b][:gammas[b]]) for b in range(B)]))
 
-    conf_np = gen.confidences(wl)
     conf = torch.tensor(conf_np, device=dev)
     seq_base = i32(ctx)
     seq_work = i32(ctx)
@@ -662,7 +758,7 @@ def main():
         sweep[g] = statistics.median(lat)
         del graph
     cost = np.array([0.0] + [sweep[g] for g in range(1, G + 1)], dtype=np.float64)
-    log("sweep (us): " + " ".join(f"{g}:{sweep[g] * 1e3:.0f}" for g in range(1, G + 1)))
+    log(f"{wl.name}: sweep (us): " + " ".join(f"{g}:{sweep[g] * 1e3:.0f}" for g in range(1, G + 1)))
 
     # ---- LibraSpec selection on the measured table (reported for all three rules); each
     # sequence selects on the uniform-gamma table of the batch
@@ -679,7 +775,7 @@ def main():
         chosen[name] = [int(x) for x in gamma.cpu()]
     g_star = chosen["marginal"]
     tokens = layout(g_star)
-    log(f"chosen gamma: {chosen}")
+    log(f"{wl.name}: chosen gamma: {chosen}")
 
     # ---- joint batched selection on a cost table over total drafts R (linear between the
     # uniform-gamma points R = B * gamma of the sweep), with its launch time
@@ -711,13 +807,9 @@ def main():
     torch.cuda.synchronize()
     joint_us = ej0.elapsed_time(ej1) * 1e3 / 20
     del jg
-
-    def predicted(gs):  # expected emitted tokens (drafts + one) per ms of verify, confidence model
-        e = sum(1.0 + float(np.cumprod(conf_np[b].astype(np.float64))[:gs[b]].sum()) for b in range(B))
-        return e / cost_j[sum(gs)]
     joint_info = {"gamma": chosen["joint"], "total_drafts": int(tot_joint.cpu()[0]), "launch_us": round(joint_us, 2),
-                  "predicted_tokens_per_ms": predicted(chosen["joint"]),
-                  "predicted_tokens_per_ms_marginal": predicted(g_star)}
+                  "predicted_tokens_per_ms": expected_tokens(conf_np, chosen["joint"]) / cost_j[sum(chosen["joint"])],
+                  "predicted_tokens_per_ms_marginal": expected_tokens(conf_np, g_star) / cost_j[sum(g_star)]}
 
     # ---- the timed step: select -> verify -> accept, one graph, dominant kernel bracketed by events
     n_slots = m.n_layers
@@ -736,20 +828,22 @@ def main():
     graph = torch.cuda.CUDAGraph()
     with torch.cuda.graph(graph):
         step()
-    for _ in range(args.warmup):
+    steps, warmup = (args.steps, args.warmup) if primary else (args.secondary_steps, 3)
+    for _ in range(warmup):
         graph.replay()
     torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     t_wall = time.perf_counter()
     e0.record()
-    for _ in range(args.steps):
+    for _ in range(steps):
         graph.replay()
     e1.record()
     torch.cuda.synchronize()
     t_wall = time.perf_counter() - t_wall
-    ms_step = e0.elapsed_time(e1) / args.steps
+    ms_step = e0.elapsed_time(e1) / steps
+    del graph
     # dominant kernel: the same steps launched eagerly with HIP events recorded around every
-    # gate/up launch on the step's stream (32 launches per step, several steps)
+    # gate/up launch on the step's stream (one launch per layer, several steps)
     lsv.lsv_set_timing_events(lsv.LSV_KERNEL_GATEUP, hev.ev, n_slots, 0)
     gateup_ms = []
     for _ in range(args.roofline_steps):
@@ -773,22 +867,23 @@ def main():
     bound = "mfma" if gu_flops / MFMA_PEAK_FLOPS > gu_bytes / (HBM_PEAK_GBPS * 1e9) else "hbm"
     if bound == "hbm":
         roof = {"bound": "hbm", "achieved": gu_bytes / t_gu / 1e9, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                "frac": hbm_gu, "traffic": measured_traffic(rows) if B == 1 else None}
+                "frac": hbm_gu, "traffic": measured_traffic(wl.name, rows)}
     else:
         roof = {"bound": "mfma", "achieved": gu_flops / t_gu / 1e12, "peak": MFMA_PEAK_FLOPS / 1e12, "unit": "TFLOP/s",
                 "frac": mfma_gu, "traffic": None}
-    roof.update({"kernel": "gemm gate/up + SwiGLU (one launch per layer)", "bytes_per_launch": gu_bytes,
+    roof.update({"kernel": "gemm gate/up + SwiGLU (one launch per layer)", "rows": rows, "bytes_per_launch": gu_bytes,
                  "flops_per_launch": gu_flops, "hbm_frac": hbm_gu, "mfma_frac": mfma_gu,
                  "avg_launch_us": avg_gu * 1e3, "launches_timed": len(gateup_ms),
                  "how": "HIP events around each gate/up launch in eagerly launched steps"})
     rows_per_seq = [g + 1 for g in g_star]
     sb = step_bytes(m, ctx, rows)
     sf = step_flops(m, ctx, rows_per_seq)
-    if args.calib_copy:
-        x = torch.empty(256 << 20, dtype=torch.uint8, device=dev)
+    if args.calib_copy and primary:
+        x = torch.empty(CALIB_BYTES, dtype=torch.uint8, device=dev)
         y = torch.empty_like(x)
         y.copy_(x)
         torch.cuda.synchronize()
+        del x, y
 
     # baseline length policy (the G4-style rule of the comparison experiments): the next
     # lengths from this step's outcome, and the rule's launch time (a graph of 100 launches)
@@ -815,36 +910,43 @@ def main():
     g4_us = e2.elapsed_time(e3) * 1e3 / 100
     del g4_graph
 
-    # expected emitted tokens per step under the drafter-confidence model (Assumption 3.7)
-    exp_tokens = 0.0
-    for b in range(B):
-        P = np.cumprod(conf_np[b].astype(np.float64))
-        exp_tokens += 1.0 + P[:g_star[b]].sum()
+    exp_tok = expected_tokens(conf_np, g_star)
+    realized = sum(a + 1 for a in a_len)
     one = (lambda v: v[0]) if B == 1 else (lambda v: v)
+    per_gamma = {}
+    for g in range(1, G + 1):
+        t = sweep[g] * 1e-3
+        per_gamma[str(g)] = {"latency_us": round(sweep[g] * 1e3, 2),
+                             "tokens_per_s": round(expected_tokens(conf_np, [g] * B) / t, 2),
+                             "hbm_frac": round(step_bytes(m, ctx, B * (g + 1)) / t / 1e9 / HBM_PEAK_GBPS, 4),
+                             "mfma_frac": round(step_flops(m, ctx, [g + 1] * B) / t / MFMA_PEAK_FLOPS, 4)}
     result = {
         "metric": METRIC,
-        "value": rows / (ms_step * 1e-3),
-        "unit": "verified tokens/s",
+        "value": exp_tok / (ms_step * 1e-3),
+        "unit": "tokens/s",
         "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
+        "steps": steps,
+        "warmup": warmup,
         "ms_per_step": ms_step,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "bf16" if m.dtype == "bf16" else "f32",
-        "data": "synthetic (seeded random-init weights, random prompt and draft ids)",
+        "data": f"synthetic (seeded random-init weights, random prompt ids; drafts {draft_kind})",
         "config": {"workload": wl.name, "model_shape": m.name, "batch": B, "context": one(ctx), "drafted": G,
                    "gamma": one(g_star), "rows": rows, "selector": "marginal on measured cost",
                    "accept": "greedy" if not sampling else f"sample T={wl.temperature}"},
+        "value_is": "expected emitted tokens per second of the step: sum_b (1 + N_b(gamma_b)) / step latency, "
+                    "N_b from the drafter confidences (Eq. 2's numerator, Assumption 3.7)",
         "roofline": roof,
-        "step": {"latency_us": ms_step * 1e3, "wall_ms_per_step": t_wall / args.steps * 1e3,
+        "step": {"latency_us": ms_step * 1e3, "wall_ms_per_step": t_wall / steps * 1e3,
                  "algorithmic_bytes": sb, "hbm_frac": sb / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBPS,
                  "flops": sf, "mfma_frac": sf / (ms_step * 1e-3) / MFMA_PEAK_FLOPS,
-                 "expected_tokens_per_s": exp_tokens / (ms_step * 1e-3),
-                 "realized_tokens_per_s": sum(a + 1 for a in a_len) / (ms_step * 1e-3)},
+                 "expected_tokens": exp_tok, "expected_tokens_per_s": exp_tok / (ms_step * 1e-3),
+                 "realized_tokens": realized, "realized_tokens_per_s": realized / (ms_step * 1e-3),
+                 "accept_len": one(a_len), "verified_rows_per_s": rows / (ms_step * 1e-3)},
         "selection": {k: one(v) for k, v in chosen.items()},
-        "sweep": {str(g): round(sweep[g] * 1e3, 2) for g in range(1, G + 1)},
+        "per_gamma": per_gamma,
         "joint_selection": joint_info,
         "baseline_policies": {"static": "the sweep: one gamma for every sequence and round",
                               "g4_next_gamma": one(g4_next), "g4_launch_us": round(g4_us, 2)},
@@ -853,22 +955,55 @@ def main():
         # every sequence at the largest gamma: the batched regime the matrix cores serve
         rows_g = B * (G + 1)
         t_g = sweep[G] * 1e-3
-        sf_g = step_flops(m, ctx, [G + 1] * B)
-        sb_g = step_bytes(m, ctx, rows_g)
         result["uniform_gamma_max"] = {"gamma": G, "rows": rows_g, "latency_us": sweep[G] * 1e3,
-                                       "mfma_frac": sf_g / t_g / MFMA_PEAK_FLOPS,
-                                       "hbm_frac": sb_g / t_g / 1e9 / HBM_PEAK_GBPS}
-    if args.rounds > 0:
+                                       "mfma_frac": step_flops(m, ctx, [G + 1] * B) / t_g / MFMA_PEAK_FLOPS,
+                                       "hbm_frac": step_bytes(m, ctx, rows_g) / t_g / 1e9 / HBM_PEAK_GBPS}
+    if primary and args.rounds > 0:
         log(f"decode loop: {args.rounds} rounds per length policy")
         try:
-            result["decode_loop"] = decode_loop_measure(m, cfg, dm, B, G, ctx, prompts, pre, rows_buf, roots, cost,
-                                                        cost_j, seed, args.rounds, dev)
+            result["decode_loop"] = decode_loop_measure(m, cfg, dm, B, G, ctx, w.prompts, w.pre, w.rows_buf, roots,
+                                                        cost, cost_j, seed, args.rounds, dev)
         except Exception as e:  # reported in the line; the verify-step measurement above stands
             log(f"decode loop failed: {e!r}")
             result["decode_loop"] = {"error": repr(e)}
-    if not args.no_cpu_baseline and B == 1:
+    if primary and not args.no_cpu_baseline:
         log("cpu baseline: timing the oracle on a bounded sample")
-        result["cpu_baseline"] = cpu_baseline(m, seed, ctx[0], rows, [roots[0]] + list(drafts[0]), g_star[0])
+        toks_np = np.concatenate([[roots[b]] + list(drafts[b][:g_star[b]]) for b in range(B)])
+        result["cpu_baseline"] = cpu_baseline(m, seed, ctx, rows_per_seq, toks_np, exp_tok)
+    return result
+
+
+def main():
+    args = parse()
+    if args.summarize:
+        sys.stdout.write(summarize(*args.summarize))
+        return
+    if args.summarize_mfma:
+        sys.stdout.write(summarize_mfma(*args.summarize_mfma))
+        return
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only: this build has no multi-GPU path (asked for --gpus {args.gpus}).",
+              file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    from synth import configs
+    torch.cuda.set_device(0)
+    w = Workload(configs.WORKLOADS[args.workload], "cuda")
+    result = measure(w, args, primary=True)
+    w.free()
+    del w
+    others = {}
+    for name in ([] if args.secondary == "none" else args.secondary.split(",")):
+        log(f"secondary workload {name}")
+        w2 = Workload(configs.WORKLOADS[name], "cuda")
+        r2 = measure(w2, args, primary=False)
+        w2.free()
+        del w2
+        others[name] = {k: r2[k] for k in ("value", "unit", "ms_per_step", "config", "roofline", "step", "selection",
+                                           "per_gamma")}
+    if others:
+        result["other_workloads"] = others
     print(json.dumps(result), flush=True)
 
 

@@ -43,3 +43,16 @@ class PlantedDrafter:
         idx = (seq_len.to(torch.int64)[:, None] + self.k[None, :]).clamp_(max=self.L - 1)
         drafts.copy_(torch.gather(self.pick, 1, idx))
         conf.copy_(torch.gather(self.q, 1, idx))
+
+
+def plant_block(continuation, conf, seed, vocab):
+    """Drafts for one verify block per sequence, planted like PlantedDrafter: draft v is the
+    target's own greedy token continuation[b][v] with probability conf[b][v] and another token
+    otherwise, so under greedy acceptance it is accepted (given drafts before it were) with
+    exactly its confidence.  continuation, conf: [B, G]; returns int64 [B, G]."""
+    cont = np.asarray(continuation, dtype=np.int64)
+    q = np.asarray(conf, dtype=np.float64)
+    rng = np.random.default_rng([seed, 0xD9])
+    u = rng.random(cont.shape)
+    wrong = (cont + 1 + rng.integers(0, vocab - 1, size=cont.shape)) % vocab
+    return np.where(u < q, cont, wrong)
