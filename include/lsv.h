@@ -9,7 +9,8 @@
  *      giving the target distribution at every drafted position (Sec. 3.1);
  *   3. lsv_accept         -- compare draft and target, keep the accepted prefix
  *      and emit one corrected or bonus token (Sec. 3.1).
- * Around them: lsv_select_joint (one length allocation for a whole batch),
+ * Around them: lsv_verify_tree / lsv_accept_tree / lsv_commit_tree (blocks whose drafts
+ * form a tree), lsv_select_joint (one length allocation for a whole batch),
  * lsv_next_length_g4 (the G4-style baseline rule of the comparison experiments),
  * and lsv_pack_block / lsv_next_roots, which carry tokens from one round to the
  * next on the device.
@@ -179,6 +180,23 @@ int lsv_verify_block(const lsv_model_config* cfg, const void* d_packed, void* d_
                      const int32_t* d_row_offsets, int32_t max_rows, int32_t max_ctx, float* d_logits,
                      int32_t* d_status, void* d_workspace, size_t workspace_bytes, void* stream);
 
+/* Tree blocks (Sec. 4.3, Table 2: tree drafts such as DDTree, verified in one target pass;
+ * Appendix B gives node budgets of 64 to 512).  The same call as lsv_verify_block, except
+ * that each sequence's rows form a tree:
+ *   d_parents     [rows] int32: the parent of row r as a row index within its sequence's
+ *                 block (0-based); the first row of every sequence is the root (the pending
+ *                 token) with parent -1, and every other row's parent precedes it.  A
+ *                 sequence has at most LSV_MAX_ROWS rows.
+ * Row r of sequence b (local index i) is stored at cache slot d_seq_len[b] + i, takes the
+ * rotary position d_seq_len[b] + depth(i), and attends to the cached positions below
+ * d_seq_len[b] and to the slots of its ancestors and itself.  Its logits are those of a
+ * plain block over its root-to-node path.  A sequence whose parents do not form such a
+ * tree gets LSV_ERR_INVALID_ARG in d_status.  Workspace: lsv_verify_workspace_bytes. */
+int lsv_verify_tree(const lsv_model_config* cfg, const void* d_packed, void* d_kv, int32_t capacity, int32_t batch,
+                    const int32_t* d_seq_len, const int32_t* d_tokens, const int32_t* d_row_offsets,
+                    const int32_t* d_parents, int32_t max_rows, int32_t max_ctx, float* d_logits, int32_t* d_status,
+                    void* d_workspace, size_t workspace_bytes, void* stream);
+
 /* -------------------------------------------------------------- acceptance */
 /* Compare drafts with the target's scores (Sec. 3.1).  Per sequence b with
  * g_b = rows_b - 1 drafts, row v of the block scores draft x_{v+1}.
@@ -239,6 +257,36 @@ int lsv_accept_noalloc(int32_t mode, int32_t batch, int32_t vocab, const float* 
                        const int32_t* d_tokens, const float* d_draft_probs, float temperature, uint64_t seed,
                        uint64_t round, int32_t* d_accept_len, int32_t* d_out_tokens, int32_t* d_seq_len,
                        int32_t* d_status, void* stream);
+
+/* Greedy acceptance of tree blocks (after lsv_verify_tree): a node is accepted with its
+ * parent when its token is the argmax of the parent's row (first index of the maximum); the
+ * accepted path runs from the root to the deepest node whose ancestors below the root are all
+ * accepted (the smallest node index among equally deep ones), i.e. the longest root-to-node
+ * path that greedy acceptance of a chain would keep.  With a = its depth:
+ *   d_accept_len  [batch] out: a
+ *   d_out_tokens  [batch, width] out: the tokens of the path's nodes at depths 1..a, then the
+ *                 argmax of the last node's row, then -1
+ *   d_path        [batch, width] out: the node (row index within the block) at depth
+ *                 0..a, then -1
+ *   d_seq_len     [batch] in/out, nullable: += a + 1 for sequences with status OK
+ *   d_status      [batch] in/out, nullable: as for lsv_accept (an incoming error skips the
+ *                 sequence); out: LSV_OK, LSV_ERR_NONFINITE, or LSV_ERR_INVALID_ARG (invalid
+ *                 parents, rows outside [1, LSV_MAX_ROWS] or past max_rows, a path of more
+ *                 than width - 1 drafts)
+ *   width         1..LSV_MAX_SEQ_ROWS;  d_workspace: lsv_accept_workspace_bytes(batch, max_rows, vocab)
+ * lsv_commit_tree then moves each accepted path's K and V to consecutive positions: with
+ * C = d_seq_len[b] - a - 1 (call it after lsv_accept_tree committed d_seq_len), the node at
+ * depth k moves from slot C + d_path[b, k] to position C + k, k = 1..a, in every layer and kv
+ * head, so that the cache holds what a plain block over the path would have written (the
+ * rotary position of that node was already C + k).  Sequences whose status is not LSV_OK are
+ * left alone.  One launch. */
+int lsv_accept_tree(int32_t batch, int32_t vocab, const float* d_logits, const int32_t* d_row_offsets,
+                    const int32_t* d_parents, const int32_t* d_tokens, int32_t max_rows, int32_t width,
+                    int32_t* d_accept_len, int32_t* d_out_tokens, int32_t* d_path, int32_t* d_seq_len,
+                    int32_t* d_status, void* d_workspace, size_t workspace_bytes, void* stream);
+int lsv_commit_tree(const lsv_model_config* cfg, void* d_kv, int32_t capacity, int32_t batch, const int32_t* d_seq_len,
+                    const int32_t* d_accept_len, const int32_t* d_path, int32_t width, const int32_t* d_status,
+                    void* stream);
 
 /* -------------------------------------------------------- length selection */
 /* Choose the speculative length gamma_b per sequence from drafter confidences

@@ -234,6 +234,139 @@ __global__ void __launch_bounds__(64) accept_greedy_kernel(const RowPartial* __r
   }
 }
 
+// ------------------------------------------------------------------ greedy, tree blocks
+// One workgroup per sequence whose block is a tree (kTreeNodes nodes at most): every node's
+// argmax from the row partials; a node is reachable when its token is its parent's argmax and
+// its parent is reachable (the root always is); the accepted path ends at the deepest reachable
+// node (the smallest index among equally deep ones).  Depth and reachability settle level by
+// level: each round resolves the nodes whose parent was resolved before it.
+__global__ void __launch_bounds__(256) accept_tree_kernel(const RowPartial* __restrict__ parts, int nc,
+                                                          const int32_t* row_offsets, int max_rows,
+                                                          const int32_t* parents, const int32_t* tokens, int width,
+                                                          int32_t* accept_len, int32_t* out_tokens, int32_t* path,
+                                                          int32_t* seq_len, int32_t* status) {
+  __shared__ int s_par[kTreeNodes], s_tok[kTreeNodes], s_top[kTreeNodes], s_dep[kTreeNodes];
+  __shared__ int s_reach[kTreeNodes];
+  __shared__ int s_key[256];
+  const int b = blockIdx.x, t = threadIdx.x;
+  auto finish = [&](int st) {  // nothing accepted: -1 tokens and path, status st
+    for (int j = t; j < width; j += 256) {
+      out_tokens[(size_t)b * width + j] = -1;
+      path[(size_t)b * width + j] = -1;
+    }
+    if (t == 0) {
+      accept_len[b] = 0;
+      if (status) status[b] = st;
+    }
+  };
+  if (status && status[b] != LSV_OK) {  // a failed verify step: skipped, status kept
+    finish(status[b]);
+    return;
+  }
+  const int r0 = row_offsets[b], r1 = row_offsets[b + 1], n = r1 - r0;
+  if (r0 < 0 || n < 1 || n > kTreeNodes || r1 > max_rows) {
+    finish(LSV_ERR_INVALID_ARG);
+    return;
+  }
+  int bad_tree = 0, bad_val = 0;
+  for (int i = t; i < n; i += 256) {
+    const int p = parents[r0 + i];
+    s_par[i] = p;
+    s_tok[i] = tokens[r0 + i];
+    bad_tree |= i == 0 ? p != -1 : (p < 0 || p >= i);
+    // argmax of row i: chunk partials in ascending order, strict '>' keeps the first maximum
+    float best = -INFINITY;
+    int bi = 0x7fffffff;
+    const RowPartial* rp = parts + (size_t)(r0 + i) * nc;
+    for (int c = 0; c < nc; ++c) {
+      const RowPartial q = rp[c];
+      bad_val |= q.bad;
+      if (q.a > best || bi == 0x7fffffff) {
+        best = q.a;
+        bi = q.idx;
+      }
+    }
+    s_top[i] = bi;
+    s_dep[i] = i == 0 ? 0 : -1;
+    s_reach[i] = i == 0;
+  }
+  const int any_tree = __syncthreads_or(bad_tree), any_val = __syncthreads_or(bad_val);
+  if (any_tree || any_val) {
+    finish(any_tree ? LSV_ERR_INVALID_ARG : LSV_ERR_NONFINITE);
+    return;
+  }
+  // levels: a round reads the parents' state, then writes the nodes it resolves
+  for (int round = 0; round < n; ++round) {
+    int upd = 0;
+    int nd[kTreeNodes / 256], nr[kTreeNodes / 256];
+#pragma unroll
+    for (int k = 0; k < kTreeNodes / 256; ++k) {
+      const int i = t + 256 * k;
+      nd[k] = -1;
+      nr[k] = 0;
+      if (i < n && i > 0 && s_dep[i] < 0) {
+        const int p = s_par[i];
+        if (s_dep[p] >= 0) {
+          nd[k] = s_dep[p] + 1;
+          nr[k] = s_reach[p] && s_tok[i] == s_top[p];
+        }
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < kTreeNodes / 256; ++k)
+      if (nd[k] >= 0) {
+        s_dep[t + 256 * k] = nd[k];
+        s_reach[t + 256 * k] = nr[k];
+        upd = 1;
+      }
+    if (!__syncthreads_or(upd)) break;
+  }
+  // deepest reachable node, smallest index on ties: key = depth * 1024 + (1023 - index)
+  int key = -1;
+  for (int i = t; i < n; i += 256)
+    if (s_reach[i]) key = max(key, s_dep[i] * 1024 + (1023 - i));
+  s_key[t] = key;
+  __syncthreads();
+  for (int o = 128; o > 0; o >>= 1) {
+    if (t < o) s_key[t] = max(s_key[t], s_key[t + o]);
+    __syncthreads();
+  }
+  const int last = 1023 - (s_key[0] & 1023), a = s_key[0] >> 10;
+  if (a + 1 > width) {
+    finish(LSV_ERR_INVALID_ARG);
+    return;
+  }
+  if (t == 0) {  // walk up from the last node: path[k] = the node at depth k
+    int u = last, child = -1;
+    for (int k = a; k >= 0; --k) {
+      path[(size_t)b * width + k] = u;
+      out_tokens[(size_t)b * width + k] = k == a ? s_top[last] : s_tok[child];
+      child = u;
+      u = s_par[u];
+    }
+    accept_len[b] = a;
+    if (seq_len) seq_len[b] += a + 1;
+    if (status) status[b] = LSV_OK;
+  }
+  for (int j = a + 1 + t; j < width; j += 256) {
+    out_tokens[(size_t)b * width + j] = -1;
+    path[(size_t)b * width + j] = -1;
+  }
+}
+
+int launch_accept_tree(int batch, int vocab, const float* logits, const int32_t* row_offsets, const int32_t* parents,
+                       const int32_t* tokens, int max_rows, int width, int32_t* accept_len, int32_t* out_tokens,
+                       int32_t* path, int32_t* seq_len, int32_t* status, void* ws, hipStream_t stream) {
+  const int nc = accept_chunks(vocab);
+  AcceptWs w = carve(ws, batch, max_rows, vocab);
+  hipLaunchKernelGGL(row_scan_kernel<false>, dim3(nc, max_rows), dim3(256), 0, stream, logits, row_offsets, batch,
+                     vocab, 1.0f, w.rows);
+  hipLaunchKernelGGL(accept_tree_kernel, dim3(batch), dim3(256), 0, stream, w.rows, nc, row_offsets, max_rows, parents,
+                     tokens, width, accept_len, out_tokens, path, seq_len, status);
+  return hipGetLastError() == hipSuccess ? LSV_OK : LSV_ERR_HIP;
+}
+
 // ------------------------------------------------------------------ sampling
 __global__ void __launch_bounds__(64) accept_sample_decide_kernel(const RowPartial* __restrict__ parts, int nc,
                                                                   const float* __restrict__ logits, int vocab,

@@ -170,7 +170,15 @@ __global__ void __launch_bounds__(64 * NW) attn_split_bf16_kernel(AttnArgs a) {
           float v = sc[kt][r] * a.scale_log2;
           if (MASK) {
             const int kp = k0 + 16 * kt + 4 * g4 + r;
-            v = qval && kp < L && kp <= qpos ? v : -INFINITY;
+            bool vis;
+            if (a.anc) {  // tree block: cached keys, then the slots of the row's ancestors and itself
+              const int j = kp - C;
+              vis = kp < C || (kp < L && j < kTreeNodes &&
+                               ((GL(a.anc)[(size_t)(r0 + rr) * kAncWords + (j >> 5)] >> (j & 31)) & 1u));
+            } else {
+              vis = kp < L && kp <= qpos;
+            }
+            v = qval && vis ? v : -INFINITY;
           }
           sc[kt][r] = v;
           mx = fmaxf(mx, v);
@@ -316,8 +324,14 @@ __global__ void __launch_bounds__(64) attn_f32_kernel(AttnArgs a, int hd) {
   if (m >= a.row_offsets[a.batch]) return;
   const int b = seq_of_row(a.row_offsets, a.batch, m);
   const int r0 = a.row_offsets[b], rows = a.row_offsets[b + 1] - r0;
-  const int pos = a.seq_len[b] + (m - r0);
-  const int L = min(min(pos + 1, a.seq_len[b] + rows), a.ctx_limit);
+  const int C = a.seq_len[b], pos = C + (m - r0);
+  // causal: keys 0..pos; tree block: keys below C + rows, block keys masked to the row's ancestors
+  const int L = a.anc ? min(C + rows, a.ctx_limit) : min(min(pos + 1, C + rows), a.ctx_limit);
+  auto visible = [&](int j) {
+    if (!a.anc || j < C) return true;
+    const int i = j - C;
+    return i < kTreeNodes && ((a.anc[(size_t)m * kAncWords + (i >> 5)] >> (i & 31)) & 1u) != 0;
+  };
   const int kvh = head / (a.nq / a.nkv);
   const size_t slab = ((size_t)b * a.nkv + kvh) * (size_t)a.capacity * hd;
   const float* K = (const float*)a.k + slab;
@@ -326,9 +340,12 @@ __global__ void __launch_bounds__(64) attn_f32_kernel(AttnArgs a, int hd) {
   const float scale = rsqrtf((float)hd);
   float mx = -INFINITY;
   for (int j = t; j < L; j += 64) {
-    float s = 0.f;
-    for (int i = 0; i < hd; ++i) s += q[i] * K[(size_t)j * hd + i];
-    s *= scale;
+    float s = -INFINITY;
+    if (visible(j)) {
+      s = 0.f;
+      for (int i = 0; i < hd; ++i) s += q[i] * K[(size_t)j * hd + i];
+      s *= scale;
+    }
     sc[j] = s;
     mx = fmaxf(mx, s);
   }

@@ -83,6 +83,9 @@ struct VerifyWs {
   float* ml_part;
   float* part;     // wide blocks: k-split partials
   float* qkv_y;    // wide blocks with an unsplit QKV: [M_max][N_qkv] projection before RoPE
+  int32_t* depth;  // tree blocks: [M_max] depth of each row in its sequence's tree
+  uint32_t* anc;   // tree blocks: [M_max][kAncWords] ancestor-or-self masks over block rows
+  int32_t* bad;    // tree blocks: [M_max] 1 where a row's parent chain is not a valid tree
   size_t total;
 };
 
@@ -139,6 +142,9 @@ static VerifyWs carve_verify(const Shape& s, const ModelLayout& ml, const Verify
   w.part = (float*)take(sizeof(float) * v.part_floats);
   // the unsplit wide QKV projection goes through an fp32 copy before the rotary embedding
   w.qkv_y = v.wide && v.w[GEMM_QKV].splits == 1 ? (float*)take(sizeof(float) * (size_t)max_rows * ml.qkv.N) : nullptr;
+  w.depth = (int32_t*)take(sizeof(int32_t) * (size_t)max_rows);
+  w.anc = (uint32_t*)take(sizeof(uint32_t) * (size_t)max_rows * kAncWords);
+  w.bad = (int32_t*)take(sizeof(int32_t) * (size_t)max_rows);
   w.total = off;
   return w;
 }
@@ -212,6 +218,54 @@ __global__ void __launch_bounds__(256) rmsnorm_kernel(const float* __restrict__ 
   normalise_row<T>(h + (size_t)m * d, d, gain, eps, m, a);
 }
 
+// ------------------------------------------------------------------ tree blocks
+// Per block row m (one thread each): its depth in its sequence's tree and the bit mask of
+// its ancestors and itself over the sequence's block rows, by walking its parent chain.
+// A row whose chain leaves the tree shape (the first row's parent is not -1, or a parent
+// does not precede its child) is flagged in bad[m]; its depth is 0 and its mask itself.
+__global__ void __launch_bounds__(256) tree_prep_kernel(const int32_t* __restrict__ parents,
+                                                        const int32_t* __restrict__ row_offsets, int batch, int M_max,
+                                                        int32_t* __restrict__ depth, uint32_t* __restrict__ anc,
+                                                        int32_t* __restrict__ bad) {
+  const int m = blockIdx.x * blockDim.x + threadIdx.x;
+  const int M = min(GL(row_offsets)[batch], M_max);
+  if (m >= M) return;
+  const int b = seq_of_row(row_offsets, batch, m);
+  const int r0 = GL(row_offsets)[b], i = m - r0;
+  uint32_t bits[kAncWords];
+#pragma unroll
+  for (int w = 0; w < kAncWords; ++w) bits[w] = 0u;
+  if (r0 < 0 || i < 0 || i >= kTreeNodes) {  // row offsets the embedding kernel will refuse
+    GL(depth)[m] = 0;
+    GL(bad)[m] = 1;
+#pragma unroll
+    for (int w = 0; w < kAncWords; ++w) GL(anc)[(size_t)m * kAncWords + w] = 0u;
+    return;
+  }
+  bool ok = GL(parents)[r0] == -1;
+  int d = 0;
+  for (int cur = i; ok && cur != 0;) {  // each step moves to a smaller index: at most i steps
+    const int p = GL(parents)[r0 + cur];
+    if (p < 0 || p >= cur) {
+      ok = false;
+      break;
+    }
+    bits[p >> 5] |= 1u << (p & 31);
+    cur = p;
+    ++d;
+  }
+  if (!ok) {
+#pragma unroll
+    for (int w = 0; w < kAncWords; ++w) bits[w] = 0u;
+    d = 0;
+  }
+  bits[i >> 5] |= 1u << (i & 31);
+  GL(depth)[m] = d;
+  GL(bad)[m] = ok ? 0 : 1;
+#pragma unroll
+  for (int w = 0; w < kAncWords; ++w) GL(anc)[(size_t)m * kAncWords + w] = bits[w];
+}
+
 // ------------------------------------------------------------------ embedding
 // h[m] = E[token_m] (fp32) and the first normalised operand a[m] = R(h / rms(h) * g) with
 // layer 0's attention gain.  Workgroup 0 also validates every sequence: token ids in range
@@ -220,7 +274,7 @@ template <typename T>
 __global__ void __launch_bounds__(256) embed_kernel(const T* __restrict__ E, int V, int d, const int32_t* tokens,
                                                     const int32_t* row_offsets, const int32_t* seq_len, int batch,
                                                     int ctx_limit, int M_max, float* h, const float* gain, float eps,
-                                                    T* a, int32_t* status) {
+                                                    T* a, const int32_t* tree_bad, int32_t* status) {
   const int m = blockIdx.x;
   if (m == 0 && status) {
     for (int b = threadIdx.x; b < batch; b += blockDim.x) {
@@ -232,7 +286,7 @@ __global__ void __launch_bounds__(256) embed_kernel(const T* __restrict__ E, int
         continue;
       }
       for (int r = r0; r < r1; ++r)
-        if (tokens[r] < 0 || tokens[r] >= V) st = LSV_ERR_INVALID_ARG;
+        if (tokens[r] < 0 || tokens[r] >= V || (tree_bad && tree_bad[r])) st = LSV_ERR_INVALID_ARG;
       status[b] = st;
     }
   }
@@ -253,8 +307,9 @@ __global__ void __launch_bounds__(256) embed_kernel(const T* __restrict__ E, int
 }
 
 int launch_verify(const Shape& s, const ModelLayout& ml, const void* packed, void* kv, int capacity, int batch,
-                  const int32_t* seq_len, const int32_t* tokens, const int32_t* row_offsets, int max_rows,
-                  int max_ctx, float* logits, int32_t* status, void* ws, size_t ws_bytes, hipStream_t st) {
+                  const int32_t* seq_len, const int32_t* tokens, const int32_t* row_offsets, const int32_t* parents,
+                  int max_rows, int max_ctx, float* logits, int32_t* status, void* ws, size_t ws_bytes,
+                  hipStream_t st) {
   const VerifyPlan v = plan_verify(s, ml, batch, max_rows, max_ctx);
   const VerifyWs w = carve_verify(s, ml, v, max_rows, ws);
   if (w.total > ws_bytes) return LSV_ERR_INVALID_ARG;
@@ -265,14 +320,18 @@ int launch_verify(const Shape& s, const ModelLayout& ml, const void* packed, voi
   auto layer_gain = [&](int l, size_t which) {
     return (const float*)(P + ml.layer_base + (size_t)l * ml.layer_stride + which);
   };
+  if (parents)
+    hipLaunchKernelGGL(tree_prep_kernel, dim3((max_rows + 255) / 256), dim3(256), 0, st, parents, row_offsets, batch,
+                       max_rows, w.depth, w.anc, w.bad);
+  const int32_t* tree_bad = parents ? w.bad : nullptr;
   if (bf16)
     hipLaunchKernelGGL(embed_kernel<bf16_t>, dim3(max_rows), dim3(256), 0, st, (const bf16_t*)(P + ml.embed), s.V,
                        s.d, tokens, row_offsets, seq_len, batch, max_ctx, max_rows, w.h, layer_gain(0, ml.attn_norm),
-                       s.eps, (bf16_t*)w.a, status);
+                       s.eps, (bf16_t*)w.a, tree_bad, status);
   else
     hipLaunchKernelGGL(embed_kernel<float>, dim3(max_rows), dim3(256), 0, st, (const float*)(P + ml.embed), s.V, s.d,
                        tokens, row_offsets, seq_len, batch, max_ctx, max_rows, w.h, layer_gain(0, ml.attn_norm), s.eps,
-                       (float*)w.a, status);
+                       (float*)w.a, tree_bad, status);
   if (hipGetLastError() != hipSuccess) return LSV_ERR_HIP;
   // a = R(h / rms(h) * gain) for the next projection
   auto rmsnorm = [&](const float* gain) {
@@ -292,6 +351,7 @@ int launch_verify(const Shape& s, const ModelLayout& ml, const void* packed, voi
   base.batch = batch;
   base.row_offsets = row_offsets;
   base.seq_len = seq_len;
+  base.depth = parents ? w.depth : nullptr;
   base.kv = kv;
   base.capacity = capacity;
   base.nq = s.nq;
@@ -361,6 +421,7 @@ int launch_verify(const Shape& s, const ModelLayout& ml, const void* packed, voi
     at.scale_log2 = (float)(1.4426950408889634 / sqrt((double)s.hd));
     at.n_splits = v.attn.n_splits;
     at.chunks_per_split = v.attn.chunks_per_split;
+    at.anc = parents ? w.anc : nullptr;
     timing_before(LSV_KERNEL_ATTENTION, l, st);
     if ((rc = launch_attention(s.dtype, s.hd, at, max_rows, st)) != LSV_OK) return rc;
     timing_after(LSV_KERNEL_ATTENTION, l, st);

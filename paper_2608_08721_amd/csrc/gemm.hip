@@ -158,7 +158,9 @@ LSV_DEV void qkv_inv_freq(const GemmArgs& a, int n0, double (&f)[2]) {
 // sequence b at cache position pos: rotary embedding of q and k, then the Q store or the
 // cache append (V transposed).
 template <typename T>
-LSV_DEV void qkv_store4(const GemmArgs& a, int m, int n0, const f32x4_t v, int b, int pos, const double (&inv_freq)[2]) {
+// pos: the cache slot; rpos: the rotary position (the slot, or for a tree node seq_len + its depth).
+LSV_DEV void qkv_store4(const GemmArgs& a, int m, int n0, const f32x4_t v, int b, int pos, int rpos,
+                        const double (&inv_freq)[2]) {
   const int qrows = a.nq * a.hd, krows = a.nkv * a.hd;
   if (n0 >= qrows + 2 * krows) return;
   if (n0 < qrows + krows) {
@@ -169,7 +171,7 @@ LSV_DEV void qkv_store4(const GemmArgs& a, int m, int n0, const f32x4_t v, int b
 #pragma unroll
     for (int pr = 0; pr < 2; ++pr) {
       // angle = pos * base^(-2i/hd) in fp64, reduced to [-pi, pi] in fp64, then fp32 sin/cos
-      const double ang = (double)pos * inv_freq[pr];
+      const double ang = (double)rpos * inv_freq[pr];
       const double red2pi = ang - 6.283185307179586 * rint(ang * 0.15915494309189535);
       float sn, cs;
       sincosf((float)red2pi, &sn, &cs);
@@ -219,7 +221,7 @@ LSV_DEV void gemm_epilogue(const GemmArgs& a, const int M, const int m0, const i
                            f32x4_t (&acc)[TPW][MT], const f32x4_t (&hpre)[TPW][MT]) {
   constexpr int KT = FragTraits<T>::KT;
   const int lane = threadIdx.x & 63, l16 = lane & 15, g4 = lane >> 4;
-  int qkv_b[MT], qkv_pos[MT];
+  int qkv_b[MT], qkv_pos[MT], qkv_rpos[MT];
   if (EPI == EPI_QKV) {
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
@@ -227,6 +229,7 @@ LSV_DEV void gemm_epilogue(const GemmArgs& a, const int M, const int m0, const i
       const int b = seq_of_row(a.row_offsets, a.batch, m);
       qkv_b[mt] = b;
       qkv_pos[mt] = GL(a.seq_len)[b] + (m - GL(a.row_offsets)[b]);
+      qkv_rpos[mt] = a.depth ? GL(a.seq_len)[b] + GL(a.depth)[m] : qkv_pos[mt];
     }
   }
   if (EPI == EPI_LOGITS) {
@@ -256,7 +259,7 @@ LSV_DEV void gemm_epilogue(const GemmArgs& a, const int M, const int m0, const i
         for (int mt = 0; mt < MT; ++mt) {
           const int m = m0 + mt * 16 + l16, n0 = (tn0 + t) * 16 + 4 * g4;
           if (m >= M || !tvalid[t]) continue;
-          qkv_store4<T>(a, m, n0, acc[t][mt], qkv_b[mt], qkv_pos[mt], inv_freq[t]);
+          qkv_store4<T>(a, m, n0, acc[t][mt], qkv_b[mt], qkv_pos[mt], qkv_rpos[mt], inv_freq[t]);
         }
     } else if (EPI == EPI_RESID) {
       // h += y (fp32 residual, row-major); the next norm reads it
@@ -714,9 +717,10 @@ __global__ void __launch_bounds__(256) qkv_rope_kernel(GemmArgs a, const float* 
     const f32x4_t v = *(const GLOBAL f32x4_t*)(y + (size_t)m * a.N + n0);
     const int b = seq_of_row(a.row_offsets, a.batch, m);
     const int pos = GL(a.seq_len)[b] + (m - GL(a.row_offsets)[b]);
+    const int rpos = a.depth ? GL(a.seq_len)[b] + GL(a.depth)[m] : pos;
     double f[2];
     qkv_inv_freq(a, n0, f);
-    qkv_store4<bf16_t>(a, m, n0, v, b, pos, f);
+    qkv_store4<bf16_t>(a, m, n0, v, b, pos, rpos, f);
   }
 }
 

@@ -139,10 +139,11 @@ int lsv_workspace_clear(void* d_workspace, size_t bytes, void* stream) {
   return hip_rc(hipGetLastError() == hipSuccess ? LSV_OK : LSV_ERR_HIP, "workspace clear");
 }
 
-int lsv_verify_block(const lsv_model_config* cfg, const void* d_packed, void* d_kv, int32_t capacity, int32_t batch,
-                     const int32_t* d_seq_len, const int32_t* d_tokens, const int32_t* d_row_offsets, int32_t max_rows,
-                     int32_t max_ctx, float* d_logits, int32_t* d_status, void* d_workspace, size_t workspace_bytes,
-                     void* stream) {
+namespace {
+int verify(const lsv_model_config* cfg, const void* d_packed, void* d_kv, int32_t capacity, int32_t batch,
+           const int32_t* d_seq_len, const int32_t* d_tokens, const int32_t* d_row_offsets, const int32_t* d_parents,
+           int32_t max_rows, int32_t max_ctx, float* d_logits, int32_t* d_status, void* d_workspace,
+           size_t workspace_bytes, void* stream) {
   int rc = check_config(cfg);
   if (rc) return rc;
   if (!d_packed || !d_kv || !d_seq_len || !d_tokens || !d_row_offsets || !d_logits || !d_workspace)
@@ -164,9 +165,62 @@ int lsv_verify_block(const lsv_model_config* cfg, const void* d_packed, void* d_
   if (workspace_bytes < need)
     return fail(LSV_ERR_INVALID_ARG, "workspace %zu bytes < %zu required", workspace_bytes, need);
   const lsv::ModelLayout ml = lsv::model_layout(s);
-  rc = lsv::launch_verify(s, ml, d_packed, d_kv, capacity, batch, d_seq_len, d_tokens, d_row_offsets, max_rows, max_ctx,
-                          d_logits, d_status, d_workspace, workspace_bytes, (hipStream_t)stream);
+  rc = lsv::launch_verify(s, ml, d_packed, d_kv, capacity, batch, d_seq_len, d_tokens, d_row_offsets, d_parents,
+                          max_rows, max_ctx, d_logits, d_status, d_workspace, workspace_bytes, (hipStream_t)stream);
   return hip_rc(rc, "verify");
+}
+}  // namespace
+
+int lsv_verify_block(const lsv_model_config* cfg, const void* d_packed, void* d_kv, int32_t capacity, int32_t batch,
+                     const int32_t* d_seq_len, const int32_t* d_tokens, const int32_t* d_row_offsets, int32_t max_rows,
+                     int32_t max_ctx, float* d_logits, int32_t* d_status, void* d_workspace, size_t workspace_bytes,
+                     void* stream) {
+  return verify(cfg, d_packed, d_kv, capacity, batch, d_seq_len, d_tokens, d_row_offsets, nullptr, max_rows, max_ctx,
+                d_logits, d_status, d_workspace, workspace_bytes, stream);
+}
+
+int lsv_verify_tree(const lsv_model_config* cfg, const void* d_packed, void* d_kv, int32_t capacity, int32_t batch,
+                    const int32_t* d_seq_len, const int32_t* d_tokens, const int32_t* d_row_offsets,
+                    const int32_t* d_parents, int32_t max_rows, int32_t max_ctx, float* d_logits, int32_t* d_status,
+                    void* d_workspace, size_t workspace_bytes, void* stream) {
+  if (!d_parents) return fail(LSV_ERR_INVALID_ARG, "NULL parents");
+  return verify(cfg, d_packed, d_kv, capacity, batch, d_seq_len, d_tokens, d_row_offsets, d_parents, max_rows, max_ctx,
+                d_logits, d_status, d_workspace, workspace_bytes, stream);
+}
+
+int lsv_accept_tree(int32_t batch, int32_t vocab, const float* d_logits, const int32_t* d_row_offsets,
+                    const int32_t* d_parents, const int32_t* d_tokens, int32_t max_rows, int32_t width,
+                    int32_t* d_accept_len, int32_t* d_out_tokens, int32_t* d_path, int32_t* d_seq_len,
+                    int32_t* d_status, void* d_workspace, size_t workspace_bytes, void* stream) {
+  if (batch < 1 || batch > LSV_MAX_BATCH || vocab < 1) return fail(LSV_ERR_INVALID_ARG, "bad batch or vocab");
+  if (max_rows < 1 || max_rows > LSV_MAX_ROWS || width < 1 || width > LSV_MAX_SEQ_ROWS)
+    return fail(LSV_ERR_INVALID_ARG, "bad max_rows %d (<= %d) / width %d (<= %d)", max_rows, (int)LSV_MAX_ROWS, width,
+                (int)LSV_MAX_SEQ_ROWS);
+  if (!d_logits || !d_row_offsets || !d_parents || !d_tokens || !d_accept_len || !d_out_tokens || !d_path ||
+      !d_workspace)
+    return fail(LSV_ERR_INVALID_ARG, "NULL pointer");
+  if (workspace_bytes < lsv::accept_workspace_bytes(batch, max_rows, vocab))
+    return fail(LSV_ERR_INVALID_ARG, "accept workspace too small");
+  return hip_rc(lsv::launch_accept_tree(batch, vocab, d_logits, d_row_offsets, d_parents, d_tokens, max_rows, width,
+                                        d_accept_len, d_out_tokens, d_path, d_seq_len, d_status, d_workspace,
+                                        (hipStream_t)stream),
+                "accept_tree");
+}
+
+int lsv_commit_tree(const lsv_model_config* cfg, void* d_kv, int32_t capacity, int32_t batch, const int32_t* d_seq_len,
+                    const int32_t* d_accept_len, const int32_t* d_path, int32_t width, const int32_t* d_status,
+                    void* stream) {
+  int rc = check_config(cfg);
+  if (rc) return rc;
+  if (!d_kv || !d_seq_len || !d_accept_len || !d_path) return fail(LSV_ERR_INVALID_ARG, "NULL pointer");
+  if (batch < 1 || batch > LSV_MAX_BATCH) return fail(LSV_ERR_INVALID_ARG, "batch %d not in [1, %d]", batch, LSV_MAX_BATCH);
+  if (capacity < 1 || capacity % LSV_KV_ALIGN)
+    return fail(LSV_ERR_INVALID_ARG, "capacity %d is not a positive multiple of %d", capacity, (int)LSV_KV_ALIGN);
+  if (width < 1 || width > LSV_MAX_SEQ_ROWS) return fail(LSV_ERR_INVALID_ARG, "width %d not in [1, %d]", width,
+                                                         (int)LSV_MAX_SEQ_ROWS);
+  return hip_rc(lsv::launch_commit_tree(lsv::shape_of(cfg), d_kv, capacity, batch, d_seq_len, d_accept_len, d_path,
+                                        width, d_status, (hipStream_t)stream),
+                "commit_tree");
 }
 
 size_t lsv_accept_workspace_bytes(int32_t batch, int32_t max_rows, int32_t vocab) {

@@ -23,6 +23,10 @@ struct AttnArgs {
   void* out;       // nq*hd columns per row in the activation layout (act_index), storage type
   float scale_log2;
   int n_splits, chunks_per_split;
+  // tree blocks: [M_max][kAncWords] ancestor-or-self masks; a block key (position >= the
+  // cached length C) at slot C + j is visible to row m iff bit j of its mask is set.  NULL:
+  // the causal block.
+  const uint32_t* anc;
 };
 
 // Split of the context into n_splits ranges of chunks_per_split chunks (bf16 path).

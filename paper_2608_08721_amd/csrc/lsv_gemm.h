@@ -36,6 +36,7 @@ struct GemmArgs {
   void* kv;     // KV cache base
   int capacity, layer, nq, nkv, hd;
   const int32_t* seq_len;
+  const int32_t* depth;  // tree blocks: row m's rotary position is seq_len + depth[m] (else its slot)
   double log2_rope_base;
   // EPI_RESID
   float* h_out;  // [M][N] fp32 residual (row-major), updated in place

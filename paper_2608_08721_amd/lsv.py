@@ -23,7 +23,7 @@ LSV_SEL_BONUS = 1
 EXPORTED = (
     "lsv_status_string", "lsv_last_error", "lsv_abi_version", "lsv_packed_model_bytes", "lsv_pack_globals",
     "lsv_pack_layer", "lsv_kv_cache_bytes", "lsv_verify_workspace_bytes", "lsv_workspace_clear",
-    "lsv_verify_block", "lsv_accept_workspace_bytes", "lsv_accept", "lsv_accept_noalloc", "lsv_select_length", "lsv_select_joint", "lsv_next_length_g4", "lsv_pack_block", "lsv_next_roots",
+    "lsv_verify_block", "lsv_verify_tree", "lsv_accept_tree", "lsv_commit_tree", "lsv_accept_workspace_bytes", "lsv_accept", "lsv_accept_noalloc", "lsv_select_length", "lsv_select_joint", "lsv_next_length_g4", "lsv_pack_block", "lsv_next_roots",
     "lsv_set_timing_events",
 )
 LSV_KERNEL_QKV, LSV_KERNEL_O, LSV_KERNEL_GATEUP, LSV_KERNEL_DOWN, LSV_KERNEL_LMHEAD, LSV_KERNEL_ATTENTION = range(6)
@@ -74,6 +74,9 @@ def load(path=LIB_PATH):
         "lsv_verify_workspace_bytes": (SZ, [CP, I32, I32, I32]),
         "lsv_workspace_clear": (ctypes.c_int, [P, SZ, P]),
         "lsv_verify_block": (ctypes.c_int, [CP, P, P, I32, I32, P, P, P, I32, I32, P, P, P, SZ, P]),
+        "lsv_verify_tree": (ctypes.c_int, [CP, P, P, I32, I32, P, P, P, P, I32, I32, P, P, P, SZ, P]),
+        "lsv_accept_tree": (ctypes.c_int, [I32, I32, P, P, P, P, I32, I32, P, P, P, P, P, P, SZ, P]),
+        "lsv_commit_tree": (ctypes.c_int, [CP, P, I32, I32, P, P, P, I32, P, P]),
         "lsv_accept_workspace_bytes": (SZ, [I32, I32, I32]),
         "lsv_accept": (ctypes.c_int, [I32, I32, I32, P, P, I32, I32, P, P, F32, U64, U64, P, P, P, P, P, SZ, P]),
         "lsv_accept_noalloc": (ctypes.c_int, [I32, I32, I32, P, P, I32, I32, P, P, F32, U64, U64, P, P, P, P, P]),
@@ -168,6 +171,25 @@ def lsv_verify_block(cfg, packed, kv, capacity, batch, seq_len, tokens, row_offs
     _check(load().lsv_verify_block(ctypes.byref(cfg), _ptr(packed), _ptr(kv), capacity, batch, _ptr(seq_len),
                                    _ptr(tokens), _ptr(row_offsets), max_rows, max_ctx, _ptr(logits), _ptr(status),
                                    _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def lsv_verify_tree(cfg, packed, kv, capacity, batch, seq_len, tokens, row_offsets, parents, max_rows, max_ctx, logits,
+                    status, ws, ws_bytes, stream=None):
+    _check(load().lsv_verify_tree(ctypes.byref(cfg), _ptr(packed), _ptr(kv), capacity, batch, _ptr(seq_len),
+                                  _ptr(tokens), _ptr(row_offsets), _ptr(parents), max_rows, max_ctx, _ptr(logits),
+                                  _ptr(status), _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def lsv_accept_tree(batch, vocab, logits, row_offsets, parents, tokens, max_rows, width, accept_len, out_tokens, path,
+                    seq_len, status, ws, ws_bytes, stream=None):
+    _check(load().lsv_accept_tree(batch, vocab, _ptr(logits), _ptr(row_offsets), _ptr(parents), _ptr(tokens), max_rows,
+                                  width, _ptr(accept_len), _ptr(out_tokens), _ptr(path), _ptr(seq_len), _ptr(status),
+                                  _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def lsv_commit_tree(cfg, kv, capacity, batch, seq_len, accept_len, path, width, status, stream=None):
+    _check(load().lsv_commit_tree(ctypes.byref(cfg), _ptr(kv), capacity, batch, _ptr(seq_len), _ptr(accept_len),
+                                  _ptr(path), width, _ptr(status), _stream(stream)))
 
 
 def lsv_accept_workspace_bytes(batch, max_rows, vocab):

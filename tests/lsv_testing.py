@@ -39,6 +39,15 @@ class GpuModel:
         torch.cuda.synchronize()
         return self.logits[:M].double().cpu().numpy(), self.status.cpu().numpy()
 
+    def verify_tree(self, seq_len, tokens, row_offsets, parents, max_rows=None):
+        """One lsv_verify_tree call (each sequence's rows form a tree given by parents)."""
+        M = int(row_offsets[-1])
+        lsv.lsv_verify_tree(self.cfg, self.dm.buf, self.kv.buf, self.capacity, self.batch, i32(seq_len), i32(tokens),
+                            i32(row_offsets), i32(parents), max_rows or self.max_rows, self.capacity, self.logits,
+                            self.status, self.ws.buf, self.ws.nbytes)
+        torch.cuda.synchronize()
+        return self.logits[:M].double().cpu().numpy(), self.status.cpu().numpy()
+
     def prefill(self, prompts):
         """Chunked prefill of every sequence through lsv_verify_block; returns last-row logits."""
         B = len(prompts)
