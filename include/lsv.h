@@ -129,9 +129,25 @@ int lsv_pack_layer(const lsv_model_config* cfg, int32_t layer,
  * Sequence b owns `capacity` positions per slab; d_seq_len[b] of them are valid.
  * capacity must be a positive multiple of LSV_KV_ALIGN (lsv_kv_cache_bytes returns 0
  * and lsv_verify_block LSV_ERR_INVALID_ARG otherwise). */
-enum { LSV_KV_ALIGN = 64 };
+enum { LSV_KV_ALIGN = 64, LSV_KV_PAGE = 64 };
 #define LSV_V_COLUMN(pos) (((pos) & ~31) | (((pos) & 12) << 1) | (((pos) & 16) >> 2) | ((pos) & 3))
 size_t lsv_kv_cache_bytes(const lsv_model_config* cfg, int32_t batch, int32_t capacity);
+
+/* Paged KV cache, for serving many sequences of changing lengths from one pool (the
+ * joint batched selection, lsv_select_joint, hands a batch lengths that vary per round and
+ * sequence).  One device buffer in the model dtype: per layer a K pool then a V pool, each
+ * of n_pages pages of LSV_KV_PAGE positions for every kv head:
+ *   pool(l, kv) = (l * 2 + kv) * n_pages * n_kv_heads * LSV_KV_PAGE * head_dim
+ *   K(l, page, h, j, i) at pool(l, 0) + ((page * n_kv_heads + h) * LSV_KV_PAGE + j) * head_dim + i
+ *   V(l, page, h, j, i) at pool(l, 1) + ((page * n_kv_heads + h) * head_dim + i) * LSV_KV_PAGE
+ *                                     + LSV_V_COLUMN(j)
+ * i.e. a page is laid out like a 64-position slab.  Position pos of sequence b lives in page
+ * d_page_table[b * max_pages + pos / 64] at j = pos % 64; a table entry outside
+ * [0, n_pages) reads as zeros and is never written.  The caller owns the pool and the table
+ * (any page order; pages need not be contiguous).  A layer's K pool must stay under 2 GiB
+ * ((n_pages + 1) * n_kv_heads * 64 * head_dim * element size < 2^31).
+ * lsv_kv_pool_bytes: size of the buffer (0 if cfg is invalid). */
+size_t lsv_kv_pool_bytes(const lsv_model_config* cfg, int32_t n_pages);
 
 /* ------------------------------------------------------------ verify step */
 /* Workspace for lsv_verify_block with the given bounds.  The workspace must be
@@ -196,6 +212,17 @@ int lsv_verify_tree(const lsv_model_config* cfg, const void* d_packed, void* d_k
                     const int32_t* d_seq_len, const int32_t* d_tokens, const int32_t* d_row_offsets,
                     const int32_t* d_parents, int32_t max_rows, int32_t max_ctx, float* d_logits, int32_t* d_status,
                     void* d_workspace, size_t workspace_bytes, void* stream);
+
+/* lsv_verify_block (d_parents NULL) or lsv_verify_tree (d_parents given) over a paged KV cache
+ * (layout above): the same arguments, rules and results, with d_kv_pool / n_pages /
+ * d_page_table / max_pages in place of d_kv / capacity.  Positions per sequence are bounded by
+ * max_pages * LSV_KV_PAGE (max_ctx must not exceed it); a block position whose page entry is
+ * outside the pool is not written (its keys read as zero). */
+int lsv_verify_paged(const lsv_model_config* cfg, const void* d_packed, void* d_kv_pool, int32_t n_pages,
+                     const int32_t* d_page_table, int32_t max_pages, int32_t batch, const int32_t* d_seq_len,
+                     const int32_t* d_tokens, const int32_t* d_row_offsets, const int32_t* d_parents, int32_t max_rows,
+                     int32_t max_ctx, float* d_logits, int32_t* d_status, void* d_workspace, size_t workspace_bytes,
+                     void* stream);
 
 /* -------------------------------------------------------------- acceptance */
 /* Compare drafts with the target's scores (Sec. 3.1).  Per sequence b with
@@ -287,6 +314,10 @@ int lsv_accept_tree(int32_t batch, int32_t vocab, const float* d_logits, const i
 int lsv_commit_tree(const lsv_model_config* cfg, void* d_kv, int32_t capacity, int32_t batch, const int32_t* d_seq_len,
                     const int32_t* d_accept_len, const int32_t* d_path, int32_t width, const int32_t* d_status,
                     void* stream);
+/* The same commit on a paged KV cache (layout above). */
+int lsv_commit_tree_paged(const lsv_model_config* cfg, void* d_kv_pool, int32_t n_pages, const int32_t* d_page_table,
+                          int32_t max_pages, int32_t batch, const int32_t* d_seq_len, const int32_t* d_accept_len,
+                          const int32_t* d_path, int32_t width, const int32_t* d_status, void* stream);
 
 /* -------------------------------------------------------- length selection */
 /* Choose the speculative length gamma_b per sequence from drafter confidences

@@ -69,32 +69,57 @@ __global__ void __launch_bounds__(64 * NW) attn_split_bf16_kernel(AttnArgs a) {
   const int s = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, g4 = lane >> 4, l16 = lane & 15;
   const int grp = wave >> 2, gtid = tid & 255;
-  const size_t slab = ((size_t)b * a.nkv + kvh) * (size_t)a.capacity * HD;
-  const GLOBAL bf16_t* kb = GL((const bf16_t*)a.k) + slab;
-  const GLOBAL bf16_t* vb = GL((const bf16_t*)a.v) + slab;
-  // The grid covers the chunks of ctx_limit <= capacity and capacity is a multiple of the
-  // chunk, so every chunk below capacity / kCh lies inside the slab.
-  const int c0 = s * a.chunks_per_split, cap_chunks = a.capacity / kCh;
+  // Slab mode: the grid covers the chunks of ctx_limit <= capacity and capacity is a multiple
+  // of the chunk, so every chunk below capacity / kCh lies inside the slab.  Paged mode: a
+  // chunk is a page; chunks below max_pages have a page-table entry.
+  const bool paged = a.kv.pages != nullptr;
+  const int c0 = s * a.chunks_per_split, cap_chunks = paged ? a.kv.max_pages : a.capacity / kCh;
 
   // a step covers chunks c .. c+NG-1, group g loading chunk c+g into buffer g; the next
   // step's chunks are in flight in registers while the current ones are used. The loads go
-  // through buffer descriptors over this (sequence, kv head)'s slab: one 32-bit lane offset
-  // per operand, the chunk and piece offsets in scalar registers, and reads past the slab
-  // return zero.
-  const int slab_bytes = a.capacity * HD * (int)sizeof(bf16_t);
-  const __amdgpu_buffer_rsrc_t krs = __builtin_amdgcn_make_buffer_rsrc((void*)kb, 0, slab_bytes, 0x00020000);
-  const __amdgpu_buffer_rsrc_t vrs = __builtin_amdgcn_make_buffer_rsrc((void*)vb, 0, slab_bytes, 0x00020000);
+  // through buffer descriptors -- over this (sequence, kv head)'s slab, or over the layer's
+  // page pool -- with one 32-bit lane offset per operand and the chunk and piece offsets in
+  // scalar registers; reads past the descriptor return zero (a page number outside the pool
+  // points there).
+  const GLOBAL bf16_t* kb = GL((const bf16_t*)a.k);
+  const GLOBAL bf16_t* vb = GL((const bf16_t*)a.v);
+  int span_bytes, vstride;
+  if (paged) {
+    span_bytes = a.kv.n_pages * a.nkv * kCh * HD * (int)sizeof(bf16_t);  // < 2^31, checked on the host
+    vstride = kCh;
+  } else {
+    const size_t slab = ((size_t)b * a.nkv + kvh) * (size_t)a.capacity * HD;
+    kb += slab;
+    vb += slab;
+    span_bytes = a.capacity * HD * (int)sizeof(bf16_t);
+    vstride = a.capacity;
+  }
+  const __amdgpu_buffer_rsrc_t krs = __builtin_amdgcn_make_buffer_rsrc((void*)kb, 0, span_bytes, 0x00020000);
+  const __amdgpu_buffer_rsrc_t vrs = __builtin_amdgcn_make_buffer_rsrc((void*)vb, 0, span_bytes, 0x00020000);
   const int koff = ((gtid / P8) * HD + (gtid % P8) * 8) * (int)sizeof(bf16_t);
-  const int voff = ((gtid >> 3) * a.capacity + (gtid & 7) * 8) * (int)sizeof(bf16_t);
+  const int voff = ((gtid >> 3) * vstride + (gtid & 7) * 8) * (int)sizeof(bf16_t);
+  // element offset of chunk c's first K row (its V^T columns start at the same offset /
+  // HD * ... : a slab chunk's V^T block starts at column c * kCh, a page's at its base)
+  auto chunk_base = [&](int c, int& kbase, int& vbase) {
+    if (!paged) {
+      kbase = c * kCh * HD;
+      vbase = c * kCh;
+      return;
+    }
+    int page = GL(a.kv.pages)[(size_t)b * a.kv.max_pages + c];
+    if (page < 0 || page >= a.kv.n_pages) page = a.kv.n_pages;  // past the pool: reads zero
+    kbase = vbase = (page * a.nkv + kvh) * kCh * HD;
+  };
   u32x4_t kr[NP], vr[NP];
   auto load_chunk = [&](int c) {
-    const int k0 = c * kCh;
+    int kbase, vbase;
+    chunk_base(c, kbase, vbase);
 #pragma unroll
     for (int j = 0; j < NP; ++j) {  // piece gtid + 256 j: K row + j 256 / P8, V^T row + 32 j
       kr[j] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(
-                                              krs, koff, (k0 + j * (256 / P8)) * HD * (int)sizeof(bf16_t), 0));
+                                              krs, koff, (kbase + j * (256 / P8) * HD) * (int)sizeof(bf16_t), 0));
       vr[j] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(
-                                              vrs, voff, (j * 32 * a.capacity + k0) * (int)sizeof(bf16_t), 0));
+                                              vrs, voff, (vbase + j * 32 * vstride) * (int)sizeof(bf16_t), 0));
     }
   };
   auto store_chunk = [&]() {
@@ -333,17 +358,18 @@ __global__ void __launch_bounds__(64) attn_f32_kernel(AttnArgs a, int hd) {
     return i < kTreeNodes && ((a.anc[(size_t)m * kAncWords + (i >> 5)] >> (i & 31)) & 1u) != 0;
   };
   const int kvh = head / (a.nq / a.nkv);
-  const size_t slab = ((size_t)b * a.nkv + kvh) * (size_t)a.capacity * hd;
-  const float* K = (const float*)a.k + slab;
-  const float* Vt = (const float*)a.v + slab;
+  const float* K = (const float*)a.k;
+  const float* Vt = (const float*)a.v;
   const float* q = (const float*)a.q + ((size_t)m * a.nq + head) * hd;
   const float scale = rsqrtf((float)hd);
   float mx = -INFINITY;
   for (int j = t; j < L; j += 64) {
     float s = -INFINITY;
-    if (visible(j)) {
+    size_t ko, vo;
+    int vs;
+    if (visible(j) && kv_locate(a.kv, a.nkv, hd, b, kvh, j, ko, vo, vs)) {
       s = 0.f;
-      for (int i = 0; i < hd; ++i) s += q[i] * K[(size_t)j * hd + i];
+      for (int i = 0; i < hd; ++i) s += q[i] * K[ko + i];
       s *= scale;
     }
     sc[j] = s;
@@ -359,9 +385,12 @@ __global__ void __launch_bounds__(64) attn_f32_kernel(AttnArgs a, int hd) {
   sum = wave_sum(sum);
   __syncthreads();
   for (int i = t; i < hd; i += 64) {
-    const float* vrow = Vt + (size_t)i * a.capacity;
     float o = 0.f;
-    for (int j = 0; j < L; ++j) o += sc[j] * vrow[v_column(j)];
+    for (int j = 0; j < L; ++j) {
+      size_t ko, vo;
+      int vs;
+      if (sc[j] != 0.f && kv_locate(a.kv, a.nkv, hd, b, kvh, j, ko, vo, vs)) o += sc[j] * Vt[vo + (size_t)i * vs];
+    }
     ((float*)a.out)[act_index<16>(m, head * hd + i, a.nq * hd / 16)] = o / sum;
   }
 }

@@ -306,7 +306,7 @@ __global__ void __launch_bounds__(256) embed_kernel(const T* __restrict__ E, int
   normalise_row<T>(hrow, d, gain, eps, m, a);
 }
 
-int launch_verify(const Shape& s, const ModelLayout& ml, const void* packed, void* kv, int capacity, int batch,
+int launch_verify(const Shape& s, const ModelLayout& ml, const void* packed, void* kv, const KvLayout& kvl, int batch,
                   const int32_t* seq_len, const int32_t* tokens, const int32_t* row_offsets, const int32_t* parents,
                   int max_rows, int max_ctx, float* logits, int32_t* status, void* ws, size_t ws_bytes,
                   hipStream_t st) {
@@ -353,7 +353,8 @@ int launch_verify(const Shape& s, const ModelLayout& ml, const void* packed, voi
   base.seq_len = seq_len;
   base.depth = parents ? w.depth : nullptr;
   base.kv = kv;
-  base.capacity = capacity;
+  base.kvl = kvl;
+  base.capacity = kvl.capacity;
   base.nq = s.nq;
   base.nkv = s.nkv;
   base.hd = s.hd;
@@ -391,7 +392,7 @@ int launch_verify(const Shape& s, const ModelLayout& ml, const void* packed, voi
     return rc;
   };
 
-  const size_t kv_layer_elems = (size_t)2 * batch * s.nkv * (size_t)capacity * s.hd;
+  const size_t kv_block = kv_layer_block(kvl, batch, s.nkv, s.hd);  // elements of one layer's K (or V) block
   int rc;
   for (int l = 0; l < s.L; ++l) {
     const char* LB = P + ml.layer_base + (size_t)l * ml.layer_stride;
@@ -405,9 +406,10 @@ int launch_verify(const Shape& s, const ModelLayout& ml, const void* packed, voi
     // attention
     AttnArgs at;
     at.q = w.q;
-    at.k = (const char*)kv + (size_t)l * kv_layer_elems * s.es;
-    at.v = (const char*)at.k + kv_layer_elems / 2 * s.es;
-    at.capacity = capacity;
+    at.k = (const char*)kv + 2 * (size_t)l * kv_block * s.es;
+    at.v = (const char*)at.k + kv_block * s.es;
+    at.kv = kvl;
+    at.capacity = kvl.capacity;
     at.ctx_limit = max_ctx;
     at.batch = batch;
     at.nq = s.nq;

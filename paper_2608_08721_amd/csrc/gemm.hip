@@ -183,9 +183,11 @@ LSV_DEV void qkv_store4(const GemmArgs& a, int m, int n0, const f32x4_t v, int b
     if (isq) {
       dst = (T*)a.q_out + ((size_t)m * a.nq + head) * a.hd;
     } else {
-      if (pos < 0 || pos >= a.capacity) return;
-      dst = (T*)a.kv + ((((size_t)a.layer * 2 + 0) * a.batch + b) * a.nkv + head) * (size_t)a.capacity * a.hd +
-            (size_t)pos * a.hd;
+      size_t ko, vo;
+      int vs;
+      if (pos < 0 || (!a.kvl.pages && pos >= a.capacity) || !kv_locate(a.kvl, a.nkv, a.hd, b, head, pos, ko, vo, vs))
+        return;
+      dst = (T*)a.kv + 2 * (size_t)a.layer * kv_layer_block(a.kvl, a.batch, a.nkv, a.hd) + ko;
     }
     GLOBAL T* gd = GL(dst);
     if constexpr (sizeof(T) == 2) {
@@ -200,14 +202,18 @@ LSV_DEV void qkv_store4(const GemmArgs& a, int m, int n0, const f32x4_t v, int b
       gd[i0 + 1 + a.hd / 2] = from_f32<T>(out[3]);
     }
   } else {
-    if (pos < 0 || pos >= a.capacity) return;
-    // V rows are stored transposed: [head_dim][capacity], column v_column(pos)
+    // V rows are stored transposed: [head_dim][capacity] per slab ([head_dim][64] per page),
+    // column v_column(pos)
     const int local = n0 - qrows - krows;
     const int head = local / a.hd, d0 = local % a.hd;
-    GLOBAL T* dst = GL((T*)a.kv) + ((((size_t)a.layer * 2 + 1) * a.batch + b) * a.nkv + head) * (size_t)a.capacity * a.hd +
-                    (size_t)d0 * a.capacity + v_column(pos);
+    size_t ko, vo;
+    int vs;
+    if (pos < 0 || (!a.kvl.pages && pos >= a.capacity) || !kv_locate(a.kvl, a.nkv, a.hd, b, head, pos, ko, vo, vs))
+      return;
+    const size_t blk = kv_layer_block(a.kvl, a.batch, a.nkv, a.hd);
+    GLOBAL T* dst = GL((T*)a.kv) + (2 * (size_t)a.layer + 1) * blk + vo + (size_t)d0 * vs;
 #pragma unroll
-    for (int r = 0; r < 4; ++r) dst[(size_t)r * a.capacity] = from_f32<T>(v[r]);
+    for (int r = 0; r < 4; ++r) dst[(size_t)r * vs] = from_f32<T>(v[r]);
   }
 }
 

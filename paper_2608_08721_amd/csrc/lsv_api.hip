@@ -140,7 +140,26 @@ int lsv_workspace_clear(void* d_workspace, size_t bytes, void* stream) {
 }
 
 namespace {
-int verify(const lsv_model_config* cfg, const void* d_packed, void* d_kv, int32_t capacity, int32_t batch,
+// Host checks of a cache description: a slab cache (pages NULL: capacity positions per slab) or a
+// page pool (n_pages pages of LSV_KV_PAGE positions, a page table of max_pages entries per sequence).
+int check_kv(const lsv::Shape& s, const lsv::KvLayout& kvl) {
+  if (!kvl.pages) {
+    if (kvl.capacity < 1 || kvl.capacity % LSV_KV_ALIGN)
+      return fail(LSV_ERR_INVALID_ARG, "capacity %d is not a positive multiple of %d", kvl.capacity, (int)LSV_KV_ALIGN);
+    if ((size_t)kvl.capacity * s.hd * s.es >= ((size_t)1 << 31))  // slab offsets are 32-bit in the kernels
+      return fail(LSV_ERR_INVALID_ARG, "capacity %d: a KV slab of %d x %d elements reaches 2 GiB", kvl.capacity,
+                  kvl.capacity, s.hd);
+    return LSV_OK;
+  }
+  if (kvl.n_pages < 1 || kvl.max_pages < 1 || kvl.max_pages > (1 << 20))
+    return fail(LSV_ERR_INVALID_ARG, "need n_pages >= 1 and 1 <= max_pages <= 2^20");
+  // the attention reads a layer's pool through 32-bit offsets, one page past the end included
+  if (((size_t)kvl.n_pages + 1) * s.nkv * LSV_KV_PAGE * s.hd * s.es >= ((size_t)1 << 31))
+    return fail(LSV_ERR_INVALID_ARG, "a layer's K pool of %d pages reaches 2 GiB", kvl.n_pages);
+  return LSV_OK;
+}
+
+int verify(const lsv_model_config* cfg, const void* d_packed, void* d_kv, const lsv::KvLayout& kvl, int32_t batch,
            const int32_t* d_seq_len, const int32_t* d_tokens, const int32_t* d_row_offsets, const int32_t* d_parents,
            int32_t max_rows, int32_t max_ctx, float* d_logits, int32_t* d_status, void* d_workspace,
            size_t workspace_bytes, void* stream) {
@@ -151,23 +170,25 @@ int verify(const lsv_model_config* cfg, const void* d_packed, void* d_kv, int32_
   if (batch < 1 || batch > LSV_MAX_BATCH) return fail(LSV_ERR_INVALID_ARG, "batch %d not in [1, %d]", batch, LSV_MAX_BATCH);
   if (max_rows < 1 || max_rows > LSV_MAX_ROWS)
     return fail(LSV_ERR_INVALID_ARG, "max_rows %d not in [1, %d]", max_rows, LSV_MAX_ROWS);
+  const int capacity = kvl.pages ? kvl.max_pages * LSV_KV_PAGE : kvl.capacity;  // positions per sequence
   if (capacity < 1 || max_ctx < 1 || max_ctx > capacity)
     return fail(LSV_ERR_INVALID_ARG, "need 1 <= max_ctx (%d) <= capacity (%d)", max_ctx, capacity);
-  if (capacity % LSV_KV_ALIGN)
-    return fail(LSV_ERR_INVALID_ARG, "capacity %d is not a multiple of %d", capacity, (int)LSV_KV_ALIGN);
   const lsv::Shape s = lsv::shape_of(cfg);
-  if ((size_t)capacity * s.hd * s.es >= ((size_t)1 << 31))  // slab offsets are 32-bit in the kernels
-    return fail(LSV_ERR_INVALID_ARG, "capacity %d: a KV slab of %d x %d elements reaches 2 GiB", capacity, capacity,
-                s.hd);
+  if ((rc = check_kv(s, kvl)) != LSV_OK) return rc;
   if (s.dtype == LSV_DTYPE_F32 && max_ctx > 16384)
     return fail(LSV_ERR_UNSUPPORTED, "fp32 models support max_ctx <= 16384");
   const size_t need = lsv::verify_workspace_bytes(s, batch, max_rows, max_ctx);
   if (workspace_bytes < need)
     return fail(LSV_ERR_INVALID_ARG, "workspace %zu bytes < %zu required", workspace_bytes, need);
   const lsv::ModelLayout ml = lsv::model_layout(s);
-  rc = lsv::launch_verify(s, ml, d_packed, d_kv, capacity, batch, d_seq_len, d_tokens, d_row_offsets, d_parents,
+  rc = lsv::launch_verify(s, ml, d_packed, d_kv, kvl, batch, d_seq_len, d_tokens, d_row_offsets, d_parents,
                           max_rows, max_ctx, d_logits, d_status, d_workspace, workspace_bytes, (hipStream_t)stream);
   return hip_rc(rc, "verify");
+}
+
+lsv::KvLayout slab_kv(int capacity) { return lsv::KvLayout{capacity, nullptr, 0, 0}; }
+lsv::KvLayout paged_kv(const int32_t* pages, int max_pages, int n_pages) {
+  return lsv::KvLayout{max_pages * LSV_KV_PAGE, pages, max_pages, n_pages};
 }
 }  // namespace
 
@@ -175,8 +196,24 @@ int lsv_verify_block(const lsv_model_config* cfg, const void* d_packed, void* d_
                      const int32_t* d_seq_len, const int32_t* d_tokens, const int32_t* d_row_offsets, int32_t max_rows,
                      int32_t max_ctx, float* d_logits, int32_t* d_status, void* d_workspace, size_t workspace_bytes,
                      void* stream) {
-  return verify(cfg, d_packed, d_kv, capacity, batch, d_seq_len, d_tokens, d_row_offsets, nullptr, max_rows, max_ctx,
-                d_logits, d_status, d_workspace, workspace_bytes, stream);
+  return verify(cfg, d_packed, d_kv, slab_kv(capacity), batch, d_seq_len, d_tokens, d_row_offsets, nullptr, max_rows,
+                max_ctx, d_logits, d_status, d_workspace, workspace_bytes, stream);
+}
+
+size_t lsv_kv_pool_bytes(const lsv_model_config* cfg, int32_t n_pages) {
+  if (check_config(cfg) != LSV_OK || n_pages < 1) return 0;
+  const lsv::Shape s = lsv::shape_of(cfg);
+  return (size_t)s.L * 2 * (size_t)n_pages * s.nkv * LSV_KV_PAGE * s.hd * s.es;
+}
+
+int lsv_verify_paged(const lsv_model_config* cfg, const void* d_packed, void* d_kv_pool, int32_t n_pages,
+                     const int32_t* d_page_table, int32_t max_pages, int32_t batch, const int32_t* d_seq_len,
+                     const int32_t* d_tokens, const int32_t* d_row_offsets, const int32_t* d_parents, int32_t max_rows,
+                     int32_t max_ctx, float* d_logits, int32_t* d_status, void* d_workspace, size_t workspace_bytes,
+                     void* stream) {
+  if (!d_page_table) return fail(LSV_ERR_INVALID_ARG, "NULL page table");
+  return verify(cfg, d_packed, d_kv_pool, paged_kv(d_page_table, max_pages, n_pages), batch, d_seq_len, d_tokens,
+                d_row_offsets, d_parents, max_rows, max_ctx, d_logits, d_status, d_workspace, workspace_bytes, stream);
 }
 
 int lsv_verify_tree(const lsv_model_config* cfg, const void* d_packed, void* d_kv, int32_t capacity, int32_t batch,
@@ -184,8 +221,8 @@ int lsv_verify_tree(const lsv_model_config* cfg, const void* d_packed, void* d_k
                     const int32_t* d_parents, int32_t max_rows, int32_t max_ctx, float* d_logits, int32_t* d_status,
                     void* d_workspace, size_t workspace_bytes, void* stream) {
   if (!d_parents) return fail(LSV_ERR_INVALID_ARG, "NULL parents");
-  return verify(cfg, d_packed, d_kv, capacity, batch, d_seq_len, d_tokens, d_row_offsets, d_parents, max_rows, max_ctx,
-                d_logits, d_status, d_workspace, workspace_bytes, stream);
+  return verify(cfg, d_packed, d_kv, slab_kv(capacity), batch, d_seq_len, d_tokens, d_row_offsets, d_parents, max_rows,
+                max_ctx, d_logits, d_status, d_workspace, workspace_bytes, stream);
 }
 
 int lsv_accept_tree(int32_t batch, int32_t vocab, const float* d_logits, const int32_t* d_row_offsets,
@@ -207,20 +244,36 @@ int lsv_accept_tree(int32_t batch, int32_t vocab, const float* d_logits, const i
                 "accept_tree");
 }
 
-int lsv_commit_tree(const lsv_model_config* cfg, void* d_kv, int32_t capacity, int32_t batch, const int32_t* d_seq_len,
-                    const int32_t* d_accept_len, const int32_t* d_path, int32_t width, const int32_t* d_status,
-                    void* stream) {
+namespace {
+int commit_tree(const lsv_model_config* cfg, void* d_kv, const lsv::KvLayout& kvl, int32_t batch,
+                const int32_t* d_seq_len, const int32_t* d_accept_len, const int32_t* d_path, int32_t width,
+                const int32_t* d_status, void* stream) {
   int rc = check_config(cfg);
   if (rc) return rc;
   if (!d_kv || !d_seq_len || !d_accept_len || !d_path) return fail(LSV_ERR_INVALID_ARG, "NULL pointer");
   if (batch < 1 || batch > LSV_MAX_BATCH) return fail(LSV_ERR_INVALID_ARG, "batch %d not in [1, %d]", batch, LSV_MAX_BATCH);
-  if (capacity < 1 || capacity % LSV_KV_ALIGN)
-    return fail(LSV_ERR_INVALID_ARG, "capacity %d is not a positive multiple of %d", capacity, (int)LSV_KV_ALIGN);
-  if (width < 1 || width > LSV_MAX_SEQ_ROWS) return fail(LSV_ERR_INVALID_ARG, "width %d not in [1, %d]", width,
-                                                         (int)LSV_MAX_SEQ_ROWS);
-  return hip_rc(lsv::launch_commit_tree(lsv::shape_of(cfg), d_kv, capacity, batch, d_seq_len, d_accept_len, d_path,
-                                        width, d_status, (hipStream_t)stream),
+  if (width < 1 || width > LSV_MAX_SEQ_ROWS)
+    return fail(LSV_ERR_INVALID_ARG, "width %d not in [1, %d]", width, (int)LSV_MAX_SEQ_ROWS);
+  const lsv::Shape s = lsv::shape_of(cfg);
+  if ((rc = check_kv(s, kvl)) != LSV_OK) return rc;
+  return hip_rc(lsv::launch_commit_tree(s, d_kv, kvl, batch, d_seq_len, d_accept_len, d_path, width, d_status,
+                                        (hipStream_t)stream),
                 "commit_tree");
+}
+}  // namespace
+
+int lsv_commit_tree(const lsv_model_config* cfg, void* d_kv, int32_t capacity, int32_t batch, const int32_t* d_seq_len,
+                    const int32_t* d_accept_len, const int32_t* d_path, int32_t width, const int32_t* d_status,
+                    void* stream) {
+  return commit_tree(cfg, d_kv, slab_kv(capacity), batch, d_seq_len, d_accept_len, d_path, width, d_status, stream);
+}
+
+int lsv_commit_tree_paged(const lsv_model_config* cfg, void* d_kv_pool, int32_t n_pages, const int32_t* d_page_table,
+                          int32_t max_pages, int32_t batch, const int32_t* d_seq_len, const int32_t* d_accept_len,
+                          const int32_t* d_path, int32_t width, const int32_t* d_status, void* stream) {
+  if (!d_page_table) return fail(LSV_ERR_INVALID_ARG, "NULL page table");
+  return commit_tree(cfg, d_kv_pool, paged_kv(d_page_table, max_pages, n_pages), batch, d_seq_len, d_accept_len, d_path,
+                     width, d_status, stream);
 }
 
 size_t lsv_accept_workspace_bytes(int32_t batch, int32_t max_rows, int32_t vocab) {

@@ -1,5 +1,6 @@
 // Internal interface of the attention kernels (attention.hip).
 #pragma once
+#include "lsv_device.h"
 #include "lsv_internal.h"
 
 namespace lsv {
@@ -11,10 +12,40 @@ constexpr int kAttnChunk = 64;  // keys per LDS chunk in the bf16 split-context 
 // 4g..4g+3 and 16+4g..16+4g+3 of the block) are adjacent.
 __host__ __device__ inline int v_column(int p) { return LSV_V_COLUMN(p); }
 
+// Element offsets of K(b, h, pos, 0) and V(b, h, pos, 0) within the layer's K block / V block
+// (slab mode: [batch][nkv] slabs; paged: the layer's pool) and the distance between V's head
+// dimensions; false when the position has no valid page.
+LSV_DEV bool kv_locate(const KvLayout& L, int nkv, int hd, int b, int h, int pos, size_t& k_off, size_t& v_off,
+                       int& v_stride) {
+  if (!L.pages) {
+    const size_t slab = ((size_t)b * nkv + h) * (size_t)L.capacity * hd;
+    k_off = slab + (size_t)pos * hd;
+    v_off = slab + v_column(pos);
+    v_stride = L.capacity;
+    return true;
+  }
+  const int blk = pos / kAttnChunk;
+  if (pos < 0 || blk >= L.max_pages) return false;
+  const int page = L.pages[(size_t)b * L.max_pages + blk];
+  if (page < 0 || page >= L.n_pages) return false;
+  const size_t base = ((size_t)page * nkv + h) * kAttnChunk * hd;
+  k_off = base + (size_t)(pos % kAttnChunk) * hd;
+  v_off = base + v_column(pos % kAttnChunk);
+  v_stride = kAttnChunk;
+  return true;
+}
+
+// Elements of one layer's K block (the V block follows it).
+__host__ __device__ inline size_t kv_layer_block(const KvLayout& L, int batch, int nkv, int hd) {
+  return L.pages ? (size_t)L.n_pages * nkv * kAttnChunk * hd : (size_t)batch * nkv * (size_t)L.capacity * hd;
+}
+
 struct AttnArgs {
   const void* q;  // [M][nq][hd] storage type
-  const void* k;  // this layer's K block: [batch][nkv][capacity][hd]
+  const void* k;  // this layer's K block: [batch][nkv][capacity][hd] (paged: [n_pages][nkv][64][hd])
   const void* v;  // this layer's V block: [batch][nkv][hd][capacity], columns by v_column()
+                  // (paged: [n_pages][nkv][hd][64])
+  KvLayout kv;
   int capacity, ctx_limit, batch, nq, nkv, M_max;
   const int32_t* row_offsets;
   const int32_t* seq_len;

@@ -1,5 +1,6 @@
 // Internal interface of the skinny-M GEMM (gemm.hip).
 #pragma once
+#include "lsv_attn.h"
 #include "lsv_device.h"
 #include "lsv_internal.h"
 
@@ -34,6 +35,7 @@ struct GemmArgs {
   // EPI_QKV
   void* q_out;  // [M][nq][hd]
   void* kv;     // KV cache base
+  KvLayout kvl;  // slab or paged layout of the cache
   int capacity, layer, nq, nkv, hd;
   const int32_t* seq_len;
   const int32_t* depth;  // tree blocks: row m's rotary position is seq_len + depth[m] (else its slot)

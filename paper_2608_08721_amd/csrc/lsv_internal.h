@@ -102,6 +102,16 @@ int launch_pack(const Shape& s, PackKind kind, const PackedMat& pm, const void* 
 // A norm gain [d] in the storage type -> fp32 at dst.
 int launch_gain(const Shape& s, const void* src, void* dst, hipStream_t stream);
 
+// Where a layer's cache entries live.  Slab mode (pages == NULL): one slab of `capacity`
+// positions per (sequence, kv head).  Paged mode: a pool of n_pages pages of LSV_KV_PAGE
+// positions per layer; sequence b's positions p .. p + 63 (p a multiple of 64) are in page
+// pages[b * max_pages + p / 64], laid out inside the page as in a 64-position slab.
+struct KvLayout {
+  int capacity;
+  const int32_t* pages;
+  int max_pages, n_pages;
+};
+
 // Tree blocks: up to LSV_MAX_ROWS nodes per sequence; a node's ancestor set is a bit mask
 // over its sequence's block rows.
 constexpr int kTreeNodes = LSV_MAX_ROWS;
@@ -110,7 +120,7 @@ constexpr int kAncWords = kTreeNodes / 32;
 size_t verify_workspace_bytes(const Shape& s, int batch, int max_rows, int max_ctx);
 // parents: NULL for a chain block (row r's parent is r - 1), else the tree of each sequence's
 // block (parent row index within the block, -1 for the root).
-int launch_verify(const Shape& s, const ModelLayout& ml, const void* packed, void* kv, int capacity, int batch,
+int launch_verify(const Shape& s, const ModelLayout& ml, const void* packed, void* kv, const KvLayout& kvl, int batch,
                   const int32_t* seq_len, const int32_t* tokens, const int32_t* row_offsets, const int32_t* parents,
                   int max_rows, int max_ctx, float* logits, int32_t* status, void* ws, size_t ws_bytes,
                   hipStream_t stream);
@@ -118,7 +128,7 @@ int launch_verify(const Shape& s, const ModelLayout& ml, const void* packed, voi
 int launch_accept_tree(int batch, int vocab, const float* logits, const int32_t* row_offsets, const int32_t* parents,
                        const int32_t* tokens, int max_rows, int width, int32_t* accept_len, int32_t* out_tokens,
                        int32_t* path, int32_t* seq_len, int32_t* status, void* ws, hipStream_t stream);
-int launch_commit_tree(const Shape& s, void* kv, int capacity, int batch, const int32_t* seq_len,
+int launch_commit_tree(const Shape& s, void* kv, const KvLayout& kvl, int batch, const int32_t* seq_len,
                        const int32_t* accept_len, const int32_t* path, int width, const int32_t* status,
                        hipStream_t stream);
 

@@ -14,7 +14,7 @@
 namespace lsv {
 
 template <typename T>
-__global__ void __launch_bounds__(128) commit_tree_kernel(T* kv, int capacity, int batch, int nkv, int hd,
+__global__ void __launch_bounds__(128) commit_tree_kernel(T* kv, KvLayout kvl, int batch, int nkv, int hd,
                                                           const int32_t* __restrict__ seq_len,
                                                           const int32_t* __restrict__ accept_len,
                                                           const int32_t* __restrict__ path, int width,
@@ -25,28 +25,31 @@ __global__ void __launch_bounds__(128) commit_tree_kernel(T* kv, int capacity, i
   const int a = accept_len[b];
   const int C = seq_len[b] - a - 1;  // the committed length minus the root and the a accepted drafts
   if (a < 1 || a >= width || C < 0) return;
-  const size_t slab = (size_t)capacity * hd;
-  T* K = kv + (((size_t)l * 2 + 0) * batch + b) * nkv * slab + (size_t)h * slab;
-  T* V = kv + (((size_t)l * 2 + 1) * batch + b) * nkv * slab + (size_t)h * slab + (size_t)i * capacity;
+  const size_t blk = kv_layer_block(kvl, batch, nkv, hd);
+  T* K = kv + 2 * (size_t)l * blk;
+  T* V = K + blk;
   for (int k = 1; k <= a; ++k) {
     const int src = C + path[(size_t)b * width + k], dst = C + k;
-    if (src < dst || src >= capacity || dst >= capacity) continue;  // not a path the acceptance wrote
-    if (src == dst) continue;
-    K[(size_t)dst * hd + i] = K[(size_t)src * hd + i];
-    V[v_column(dst)] = V[v_column(src)];
+    if (src <= dst) continue;  // src == dst needs no copy; src < dst is not a path the acceptance wrote
+    size_t ks, vs_, kd, vd;
+    int ss, sd;
+    if (!kvl.pages && src >= kvl.capacity) continue;
+    if (!kv_locate(kvl, nkv, hd, b, h, src, ks, vs_, ss) || !kv_locate(kvl, nkv, hd, b, h, dst, kd, vd, sd)) continue;
+    K[kd + i] = K[ks + i];
+    V[vd + (size_t)i * sd] = V[vs_ + (size_t)i * ss];
   }
 }
 
-int launch_commit_tree(const Shape& s, void* kv, int capacity, int batch, const int32_t* seq_len,
+int launch_commit_tree(const Shape& s, void* kv, const KvLayout& kvl, int batch, const int32_t* seq_len,
                        const int32_t* accept_len, const int32_t* path, int width, const int32_t* status,
                        hipStream_t stream) {
   const dim3 grid((unsigned)s.nkv, (unsigned)batch, (unsigned)s.L);
   if (s.dtype == LSV_DTYPE_BF16)
-    hipLaunchKernelGGL(commit_tree_kernel<bf16_t>, grid, dim3(128), 0, stream, (bf16_t*)kv, capacity, batch, s.nkv,
-                       s.hd, seq_len, accept_len, path, width, status);
+    hipLaunchKernelGGL(commit_tree_kernel<bf16_t>, grid, dim3(128), 0, stream, (bf16_t*)kv, kvl, batch, s.nkv, s.hd,
+                       seq_len, accept_len, path, width, status);
   else
-    hipLaunchKernelGGL(commit_tree_kernel<float>, grid, dim3(128), 0, stream, (float*)kv, capacity, batch, s.nkv,
-                       s.hd, seq_len, accept_len, path, width, status);
+    hipLaunchKernelGGL(commit_tree_kernel<float>, grid, dim3(128), 0, stream, (float*)kv, kvl, batch, s.nkv, s.hd,
+                       seq_len, accept_len, path, width, status);
   return hipGetLastError() == hipSuccess ? LSV_OK : LSV_ERR_HIP;
 }
 

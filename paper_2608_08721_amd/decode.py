@@ -5,7 +5,8 @@ A round is, on one stream and without a host round trip:
   drafter -> length (lsv_select_length | lsv_select_joint | lsv_next_length_g4 | a static length)
           -> lsv_pack_block -> lsv_verify_block -> lsv_accept (greedy, commits seq_len)
           -> lsv_next_roots.
-The drafter is the caller's: a callable (seq_len, drafts, conf) that fills the round's
+``kv`` is a slab cache (runtime.KVCache, ``capacity`` positions per sequence) or a paged one
+(runtime.PagedKVCache, ``capacity`` = its pages per sequence x 64).  The drafter is the caller's: a callable (seq_len, drafts, conf) that fills the round's
 drafts [B, G] and confidences [B, G] on the device.  ``cost`` is indexed by gamma (cost[0]
 unused) for the per-sequence rules, and by the batch's total drafts (B * G + 1 entries) for
 the joint rule.  The status array is shared by verify and accept: the acceptance skips a
@@ -86,9 +87,14 @@ class DecodeLoop:
             lsv.lsv_next_length_g4(B, self.gamma, self.acc, self.status, self.d_min, G, self.gamma, self.row_off,
                                    None)
         lsv.lsv_pack_block(B, G, self.row_off, self.max_rows, self.roots, self.drafts, self.tokens, None)
-        lsv.lsv_verify_block(self.cfg, self.dm.buf, self.kv.buf, self.cap, B, self.seq_len, self.tokens,
-                             self.row_off, self.max_rows, self.max_ctx, self.logits, self.status, self.ws.buf,
-                             self.ws.nbytes)
+        if isinstance(self.kv, runtime.PagedKVCache):
+            lsv.lsv_verify_paged(self.cfg, self.dm.buf, self.kv.buf, self.kv.n_pages, self.kv.table, self.kv.max_pages,
+                                 B, self.seq_len, self.tokens, self.row_off, None, self.max_rows, self.max_ctx,
+                                 self.logits, self.status, self.ws.buf, self.ws.nbytes)
+        else:
+            lsv.lsv_verify_block(self.cfg, self.dm.buf, self.kv.buf, self.cap, B, self.seq_len, self.tokens,
+                                 self.row_off, self.max_rows, self.max_ctx, self.logits, self.status, self.ws.buf,
+                                 self.ws.nbytes)
         lsv.lsv_accept(lsv.LSV_ACC_GREEDY, B, self.cfg.vocab, self.logits, self.row_off, self.max_rows, self.width,
                        self.tokens, None, 0.0, 0, 0, self.acc, self.out, self.seq_len, self.status, self.aws.buf,
                        self.aws.nbytes)

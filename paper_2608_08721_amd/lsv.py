@@ -14,7 +14,7 @@ LIB_PATH = os.path.join(_HERE, "liblsv.so")
 LSV_OK, LSV_ERR_INVALID_ARG, LSV_ERR_UNSUPPORTED, LSV_ERR_HIP, LSV_ERR_CAPACITY, LSV_ERR_NONFINITE = 0, -1, -2, -3, -4, -5
 LSV_DTYPE_F32, LSV_DTYPE_BF16 = 0, 1
 LSV_MAX_BATCH, LSV_MAX_ROWS, LSV_MAX_G, LSV_MAX_SEQ_ROWS, LSV_WIDE_ROWS = 64, 512, 64, 64, 272
-LSV_KV_ALIGN = 64
+LSV_KV_ALIGN = LSV_KV_PAGE = 64
 LSV_ACCEPT_NOALLOC_BYTES = 512 * 1024
 LSV_ACC_GREEDY, LSV_ACC_SAMPLE = 0, 1
 LSV_SEL_MARGINAL, LSV_SEL_EXHAUSTIVE, LSV_SEL_ALG1 = 0, 1, 2
@@ -23,7 +23,8 @@ LSV_SEL_BONUS = 1
 EXPORTED = (
     "lsv_status_string", "lsv_last_error", "lsv_abi_version", "lsv_packed_model_bytes", "lsv_pack_globals",
     "lsv_pack_layer", "lsv_kv_cache_bytes", "lsv_verify_workspace_bytes", "lsv_workspace_clear",
-    "lsv_verify_block", "lsv_verify_tree", "lsv_accept_tree", "lsv_commit_tree", "lsv_accept_workspace_bytes", "lsv_accept", "lsv_accept_noalloc", "lsv_select_length", "lsv_select_joint", "lsv_next_length_g4", "lsv_pack_block", "lsv_next_roots",
+    "lsv_verify_block", "lsv_verify_tree", "lsv_accept_tree", "lsv_commit_tree", "lsv_kv_pool_bytes",
+    "lsv_verify_paged", "lsv_commit_tree_paged", "lsv_accept_workspace_bytes", "lsv_accept", "lsv_accept_noalloc", "lsv_select_length", "lsv_select_joint", "lsv_next_length_g4", "lsv_pack_block", "lsv_next_roots",
     "lsv_set_timing_events",
 )
 LSV_KERNEL_QKV, LSV_KERNEL_O, LSV_KERNEL_GATEUP, LSV_KERNEL_DOWN, LSV_KERNEL_LMHEAD, LSV_KERNEL_ATTENTION = range(6)
@@ -77,6 +78,9 @@ def load(path=LIB_PATH):
         "lsv_verify_tree": (ctypes.c_int, [CP, P, P, I32, I32, P, P, P, P, I32, I32, P, P, P, SZ, P]),
         "lsv_accept_tree": (ctypes.c_int, [I32, I32, P, P, P, P, I32, I32, P, P, P, P, P, P, SZ, P]),
         "lsv_commit_tree": (ctypes.c_int, [CP, P, I32, I32, P, P, P, I32, P, P]),
+        "lsv_kv_pool_bytes": (SZ, [CP, I32]),
+        "lsv_verify_paged": (ctypes.c_int, [CP, P, P, I32, P, I32, I32, P, P, P, P, I32, I32, P, P, P, SZ, P]),
+        "lsv_commit_tree_paged": (ctypes.c_int, [CP, P, I32, P, I32, I32, P, P, P, I32, P, P]),
         "lsv_accept_workspace_bytes": (SZ, [I32, I32, I32]),
         "lsv_accept": (ctypes.c_int, [I32, I32, I32, P, P, I32, I32, P, P, F32, U64, U64, P, P, P, P, P, SZ, P]),
         "lsv_accept_noalloc": (ctypes.c_int, [I32, I32, I32, P, P, I32, I32, P, P, F32, U64, U64, P, P, P, P, P]),
@@ -190,6 +194,24 @@ def lsv_accept_tree(batch, vocab, logits, row_offsets, parents, tokens, max_rows
 def lsv_commit_tree(cfg, kv, capacity, batch, seq_len, accept_len, path, width, status, stream=None):
     _check(load().lsv_commit_tree(ctypes.byref(cfg), _ptr(kv), capacity, batch, _ptr(seq_len), _ptr(accept_len),
                                   _ptr(path), width, _ptr(status), _stream(stream)))
+
+
+def lsv_kv_pool_bytes(cfg, n_pages):
+    return load().lsv_kv_pool_bytes(ctypes.byref(cfg), n_pages)
+
+
+def lsv_verify_paged(cfg, packed, kv_pool, n_pages, page_table, max_pages, batch, seq_len, tokens, row_offsets, parents,
+                     max_rows, max_ctx, logits, status, ws, ws_bytes, stream=None):
+    _check(load().lsv_verify_paged(ctypes.byref(cfg), _ptr(packed), _ptr(kv_pool), n_pages, _ptr(page_table), max_pages,
+                                   batch, _ptr(seq_len), _ptr(tokens), _ptr(row_offsets), _ptr(parents), max_rows,
+                                   max_ctx, _ptr(logits), _ptr(status), _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def lsv_commit_tree_paged(cfg, kv_pool, n_pages, page_table, max_pages, batch, seq_len, accept_len, path, width, status,
+                          stream=None):
+    _check(load().lsv_commit_tree_paged(ctypes.byref(cfg), _ptr(kv_pool), n_pages, _ptr(page_table), max_pages, batch,
+                                        _ptr(seq_len), _ptr(accept_len), _ptr(path), width, _ptr(status),
+                                        _stream(stream)))
 
 
 def lsv_accept_workspace_bytes(batch, max_rows, vocab):

@@ -112,6 +112,60 @@ class KVCache:
         return k, v
 
 
+class PagedKVCache:
+    """A paged KV cache (lsv.h, lsv_kv_pool_bytes): n_pages pages of LSV_KV_PAGE positions per
+    layer and K|V, and a page table [batch][max_pages] (int32, device) mapping each sequence's
+    64-position blocks to pages."""
+
+    def __init__(self, cfg, n_pages, page_table, device="cuda"):
+        self.cfg, self.n_pages = cfg, n_pages
+        nbytes = lsv.lsv_kv_pool_bytes(cfg, n_pages)
+        if nbytes == 0:
+            raise lsv.LsvError(lsv.LSV_ERR_INVALID_ARG, "invalid KV pool shape")
+        self.buf = torch.zeros(nbytes, dtype=torch.uint8, device=device)
+        self.table_np = np.ascontiguousarray(page_table, dtype=np.int32)
+        self.batch, self.max_pages = self.table_np.shape
+        self.table = torch.tensor(self.table_np, device=device)
+
+    def _pages(self):
+        c, P = self.cfg, lsv.LSV_KV_PAGE
+        return self.buf.view(storage_dtype(c)).view(c.n_layers, 2, self.n_pages, c.n_kv_heads, P * c.head_dim)
+
+    def _views(self, layer):
+        c, P = self.cfg, lsv.LSV_KV_PAGE
+        kp = self._pages()[layer, 0].view(self.n_pages, c.n_kv_heads, P, c.head_dim)
+        vp = self._pages()[layer, 1].view(self.n_pages, c.n_kv_heads, c.head_dim, P)
+        return kp, vp
+
+    def _runs(self, b, start, n):
+        """(page, first slot in the page, offset in the run, length) of each run of positions
+        start..start+n-1 inside one page."""
+        P, pos, out = lsv.LSV_KV_PAGE, start, []
+        while pos < start + n:
+            ln = min(P - pos % P, start + n - pos)
+            out.append((int(self.table_np[b, pos // P]), pos % P, pos - start, ln))
+            pos += ln
+        return out
+
+    def write(self, layer, b, start, k, v):
+        """Store K and V of positions start.. (device tensors [kv_head][n][head_dim])."""
+        kp, vp = self._views(layer)
+        for pg, j0, t0, ln in self._runs(b, start, k.shape[1]):
+            kp[pg, :, j0:j0 + ln] = k[:, t0:t0 + ln]
+            cols = v_column(torch.arange(j0, j0 + ln, device=self.buf.device))
+            vp[pg][:, :, cols] = v[:, t0:t0 + ln].transpose(1, 2)
+
+    def read(self, layer, b, start, n):
+        """(K, V) of positions start..start+n-1 as [kv_head][n][head_dim] tensors."""
+        kp, vp = self._views(layer)
+        ks, vs = [], []
+        for pg, j0, t0, ln in self._runs(b, start, n):
+            ks.append(kp[pg, :, j0:j0 + ln])
+            cols = v_column(torch.arange(j0, j0 + ln, device=self.buf.device))
+            vs.append(vp[pg][:, :, cols].transpose(1, 2))
+        return torch.cat(ks, dim=1), torch.cat(vs, dim=1)
+
+
 class Workspace:
     """Zero-initialised device scratch (the library keeps its counters at zero)."""
 
