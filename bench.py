@@ -65,6 +65,9 @@ def parse():
                    help="also run multi-round decoding for this many rounds per length policy (planted drafter)")
     p.add_argument("--calib-copy", action="store_true",
                    help="also run one plain 256 MiB copy kernel (counter calibration for --pmc runs)")
+    p.add_argument("--counters-only", type=int, default=0, metavar="GAMMA",
+                   help="counter runs of the profile: no prefill, sweep or CPU baseline; the eager roofline steps "
+                        "at uniform GAMMA for every sequence, then the calibration copy")
     p.add_argument("--summarize", nargs=3, metavar=("TRACE_DIR", "FETCH_DIR", "WRITE_DIR"),
                    help="no GPU work: turn the csv output of three rocprofv3 runs of this script (kernel trace, "
                         "--pmc FETCH_SIZE, --pmc WRITE_SIZE; each dir also holds that run's bench.json) into the "
@@ -210,8 +213,10 @@ def summarize(trace_dir, fetch_dir, write_dir):
     base = f"python3 bench.py --workload {wl.name} --secondary none --no-cpu-baseline"
     cmd_t = (f"rocprofv3 --kernel-trace --stats --output-format csv -d gpurun_out/pf/trace -o t -- {base} "
              f"--steps {bt['steps']} --warmup {bt['warmup']}")
-    cmd_c = ("rocprofv3 --pmc {c} --output-format csv -d gpurun_out/pf/{d} -o {o} -- " + base +
-             " --steps 2 --warmup 1 --sweep-reps 1 --roofline-steps 1 --calib-copy")
+    g_sel = bt["config"]["gamma"]
+    g_sel = g_sel[0] if isinstance(g_sel, list) else g_sel
+    cmd_c = ("rocprofv3 --pmc {c} --output-format csv -d gpurun_out/pf/{d} -o {o} -- " +
+             f"python3 bench.py --workload {wl.name} --counters-only {g_sel} --roofline-steps 2")
     w(f"# gate/up GEMM + SwiGLU: {wl.name} ({m.name} shape, batch {wl.batch}, context {bt['config']['context']}, "
       f"{rows} rows)")
     w("")
@@ -679,6 +684,43 @@ class Workload:
         torch.cuda.empty_cache()
 
 
+def counters_only(wl, args, dev):
+    """Counter passes: the gate/up launches of eager verify steps at uniform gamma (no prefill: the
+    cache holds zeros, which changes no projection's traffic), then a plain copy for calibration.
+    Prints the roofline fields summarize() reads."""
+    import torch
+
+    from paper_2608_08721_amd import lsv, runtime
+    from synth import gen
+    m, B, G, g = wl.model, wl.batch, wl.G, args.counters_only
+    cfg = runtime.model_config(m)
+    ctx = [int(c) for c in gen.contexts(wl)]
+    cap = runtime.kv_capacity(max(ctx) + G + 1)
+    rows_step = B * (G + 1)
+    dm = runtime.DeviceModel(cfg, dev)
+    dm.pack_globals(gen.embed_weights(m, wl.seed), gen.final_norm_weights(m), gen.lm_head_weights(m, wl.seed))
+    for l in range(m.n_layers):
+        dm.pack_layer(l, gen.layer_weights(m, wl.seed, l))
+    kv = runtime.KVCache(cfg, B, cap, dev)
+    ws = runtime.Workspace(lsv.lsv_verify_workspace_bytes(cfg, B, rows_step, cap), dev)
+    logits = torch.zeros((rows_step, m.vocab), dtype=torch.float32, device=dev)
+    status = torch.zeros(B, dtype=torch.int32, device=dev)
+    i32 = lambda x: torch.tensor(np.asarray(x, dtype=np.int32), device=dev)
+    off = i32(runtime.row_offsets_of([g + 1] * B))
+    toks = i32(gen.randint(wl.seed, 900, B * (g + 1), m.vocab))
+    seq = i32(ctx)
+    steps = args.roofline_steps
+    for _ in range(steps):
+        lsv.lsv_verify_block(cfg, dm.buf, kv.buf, cap, B, seq, toks, off, rows_step, cap, logits, status, ws.buf,
+                             ws.nbytes)
+    torch.cuda.synchronize()
+    x = torch.empty(CALIB_BYTES, dtype=torch.uint8, device=dev)
+    torch.empty_like(x).copy_(x)
+    torch.cuda.synchronize()
+    print(json.dumps({"config": {"workload": wl.name}, "roofline": {"rows": B * (g + 1),
+                                                                  "launches_timed": steps * m.n_layers}}), flush=True)
+
+
 def measure(w, args, primary=True):
     """The measurement of one workload: per-gamma sweep (the measured cost table), selection,
     the timed select -> verify -> accept graph, the dominant kernel's events, and (primary
@@ -989,6 +1031,9 @@ def main():
 
     from synth import configs
     torch.cuda.set_device(0)
+    if args.counters_only:
+        counters_only(configs.WORKLOADS[args.workload], args, "cuda")
+        return
     w = Workload(configs.WORKLOADS[args.workload], "cuda")
     result = measure(w, args, primary=True)
     w.free()
