@@ -142,9 +142,9 @@ def measured_traffic(workload, rows):
 
 def is_gateup(name):
     """The gate/up + SwiGLU launches: the 64-row kernel (kind 2, or 5 = the wide-model
-    configuration) and the batched one (epilogue 3)."""
+    configuration) and the fused 64-row / batched kernel of batched bounds (kind 2)."""
     return ("gemm_kernel<unsigned short, 2," in name or "gemm_kernel<unsigned short, 5," in name
-            or "gemm_wide_kernel<3>" in name)
+            or "gemm_fused_kernel<2," in name)
 
 
 SELECT_KERNEL = "select_length_kernel"
@@ -330,7 +330,7 @@ def summarize_mfma(trace_dir, pmc_dir):
     assert len(pcalls) == len(tcalls), (len(pcalls), len(tcalls))
 
     def gateup_mfma(call):
-        v = [r["SQ_INSTS_MFMA"] for r in call if "gemm_wide_kernel<3>" in r["Kernel_Name"]]
+        v = [r["SQ_INSTS_MFMA"] for r in call if "gemm_fused_kernel<2," in r["Kernel_Name"]]
         return max(v) if v else 0
     top = max(gateup_mfma(c) for c in pcalls)
     hits = [i for i, c in enumerate(pcalls) if top > 0 and gateup_mfma(c) == top]
@@ -349,14 +349,11 @@ def summarize_mfma(trace_dir, pmc_dir):
               "attention split": float(att_flops)}
 
     def kind(name, seen):
-        if "gemm_wide_kernel<3>" in name:
-            return "gate/up"
-        if "gemm_wide_kernel<2>" in name:
-            seen["resid"] += 1
-            return "O" if seen["resid"] % 2 == 1 else "down"
-        if "gemm_wide_kernel<0>" in name:
-            seen["logits"] += 1
-            return "QKV" if seen["logits"] <= m.n_layers else "LM head"
+        for k, label in (("gemm_fused_kernel<2,", "gate/up"), ("gemm_fused_kernel<1,", "O"),
+                         ("gemm_fused_kernel<3,", "down"), ("gemm_fused_kernel<0,", "QKV"),
+                         ("gemm_fused_kernel<4,", "LM head")):
+            if k in name:
+                return label
         if "attn_split" in name:
             return "attention split"
         return None

@@ -157,53 +157,58 @@ size_t verify_workspace_bytes(const Shape& s, int batch, int max_rows, int max_c
 }
 
 // ------------------------------------------------------------------ row normalisation
-// a[m] = R(h[m] / sqrt(mean(h[m]^2) + eps) * g) of one row, by one 256-thread workgroup:
-// thread t takes the 16-column groups t, t + 256, ... (each summed left to right), the
-// workgroup adds the 256 partial sums in a fixed tree, and every element is scaled,
+// a[m] = R(h[m] / sqrt(mean(h[m]^2) + eps) * g) of one row, by one 256-thread workgroup.
+// Thread t holds the lane runs of EPL columns t, t + 256, ... of the row (EPL = 8 bf16 or
+// 4 fp32 columns: one 16-byte store of the operand each) in registers from a single read;
+// its sum of squares runs over them in order, the wave adds its lanes in a fixed shuffle
+// tree and wave 0 adds the four waves' sums in order.  Every element is then scaled,
 // multiplied by its gain and rounded once.
 template <typename T>
 LSV_DEV void normalise_row(const float* __restrict__ hrow, int d, const float* __restrict__ gain, float eps, int m,
                            T* __restrict__ a) {
-  __shared__ float red[256];
-  const int t = threadIdx.x;
-  float ss = 0.f;
-  for (int p = t; p < d / 16; p += 256) {
-    const GLOBAL f32x4_t* hp = (const GLOBAL f32x4_t*)(GL(hrow) + 16 * p);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const f32x4_t v = hp[i];
-      ss += v[0] * v[0];
-      ss += v[1] * v[1];
-      ss += v[2] * v[2];
-      ss += v[3] * v[3];
-    }
-  }
-  red[t] = ss;
-  __syncthreads();
-  for (int o = 128; o > 0; o >>= 1) {
-    if (t < o) red[t] += red[t + o];
-    __syncthreads();
-  }
-  const float inv = 1.0f / sqrtf(red[0] / (float)d + eps);
-  // one lane run of a fragment (EPL = 16 / sizeof(T) columns) per 16-byte store
   constexpr int KT = 64 / sizeof(T), EPL = KT / 4;
-  const int Kt = (d + KT - 1) / KT;
-  for (int c = t * EPL; c < d; c += 256 * EPL) {
-    float x[EPL];
+  constexpr int RUNS = 8192 / (256 * EPL);  // d_model <= 8192
+  __shared__ float wsum[4];
+  const int t = threadIdx.x;
+  float x[RUNS][EPL];
+  float ss = 0.f;
+#pragma unroll
+  for (int r = 0; r < RUNS; ++r) {
+    const int c = (t + 256 * r) * EPL;
 #pragma unroll
     for (int e = 0; e < EPL; e += 4) {
-      const f32x4_t hv = *(const GLOBAL f32x4_t*)(GL(hrow) + c + e);
+      f32x4_t v = {0.f, 0.f, 0.f, 0.f};
+      if (c < d) v = *(const GLOBAL f32x4_t*)(GL(hrow) + c + e);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        x[r][e + q] = v[q];
+        ss += v[q] * v[q];
+      }
+    }
+  }
+  for (int o = 32; o > 0; o >>= 1) ss += __shfl_xor(ss, o, kWave);
+  if ((t & 63) == 0) wsum[t >> 6] = ss;
+  __syncthreads();
+  const float inv = 1.0f / sqrtf(((wsum[0] + wsum[1]) + (wsum[2] + wsum[3])) / (float)d + eps);
+  const int Kt = (d + KT - 1) / KT;
+#pragma unroll
+  for (int r = 0; r < RUNS; ++r) {
+    const int c = (t + 256 * r) * EPL;
+    if (c >= d) break;
+    float y[EPL];
+#pragma unroll
+    for (int e = 0; e < EPL; e += 4) {
       const f32x4_t gv = *(const GLOBAL f32x4_t*)(GL(gain) + c + e);
 #pragma unroll
-      for (int r = 0; r < 4; ++r) x[e + r] = hv[r] * inv * gv[r];
+      for (int q = 0; q < 4; ++q) y[e + q] = x[r][e + q] * inv * gv[q];
     }
     u32x4_t out;
     if constexpr (sizeof(T) == 2) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) out[i] = (uint32_t)f2bf(x[2 * i]) | ((uint32_t)f2bf(x[2 * i + 1]) << 16);
+      for (int i = 0; i < 4; ++i) out[i] = (uint32_t)f2bf(y[2 * i]) | ((uint32_t)f2bf(y[2 * i + 1]) << 16);
     } else {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) out[i] = __float_as_uint(x[i]);
+      for (int i = 0; i < 4; ++i) out[i] = __float_as_uint(y[i]);
     }
     *(GLOBAL u32x4_t*)(GL(a) + act_index<KT>(m, c, Kt)) = out;
   }
@@ -371,20 +376,12 @@ int launch_verify(const Shape& s, const ModelLayout& ml, const void* packed, voi
     timing_before((int)kind, idx, st);
     int rc;
     if (v.wide) {
-      // a batched bound: the 64-row kernel serves blocks of up to 64 device rows (it streams
-      // the weights once for them) and the batched kernel the larger ones; each launch finds
-      // the row count on the device and the other one returns at once
-      GemmArgs s64 = a;
-      s64.M_max = 64;
-      s64.rows_hi = 64;
-      rc = launch_gemm(s.dtype, kind, 4, s64, st);
-      if (rc == LSV_OK) {
-        a.part = w.part;
-        a.part_bytes = sizeof(float) * v.part_floats;
-        if (kind == GEMM_QKV) a.out_f32 = w.qkv_y;
-        a.rows_lo = 64;
-        rc = launch_gemm_wide(kind, a, v.w[kind], st);
-      }
+      // a batched bound: one launch whose workgroups run the 64-row body (the weights streamed
+      // once) for blocks of up to 64 device rows and the batched body for larger ones
+      a.part = w.part;
+      a.part_bytes = sizeof(float) * v.part_floats;
+      if (kind == GEMM_QKV) a.out_f32 = w.qkv_y;
+      rc = launch_gemm_fused(kind, a, v.w[kind], st);
     } else {
       rc = launch_gemm(s.dtype, kind, v.MT, a, st);
     }

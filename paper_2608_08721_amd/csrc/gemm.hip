@@ -307,9 +307,9 @@ LSV_DEV void gemm_epilogue(const GemmArgs& a, const int M, const int m0, const i
 
 template <typename T, int MT, int TPW, int KS, int U, int NS, int EPI, int MT_MAX>
 LSV_DEV void gemm_body(const GemmArgs& a, const int M, const int tile, const int m0,
-                       f32x4_t (*red)[TPW][MT_MAX][kWave]) {
+                       f32x4_t (*red)[TPW][MT_MAX][kWave], const int kslice) {
   constexpr int EPL = FragTraits<T>::EPL;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, l16 = lane & 15, g4 = lane >> 4;
+  const int wave = kslice, lane = threadIdx.x & 63, l16 = lane & 15, g4 = lane >> 4;
   // this workgroup: fragment rows tn0 .. tn0+TPW-1 over the whole K, activation rows
   // m0 .. min(M, m0 + 16 MT) - 1; wave = k-slice
   const int tn0 = tile * TPW;
@@ -468,14 +468,15 @@ __global__ void __launch_bounds__(64 * GemmCfg<KIND>::KS) gemm_kernel(GemmArgs a
   // one or two tiles keep the product's full pipeline under any bound (lab: down at 9 rows under a
   // 64-row bound, 41 -> 25 us); three or four take the shallower one
   using C = GemmCfg<KIND>;
+  const int ks = threadIdx.x >> 6;
   if (mt <= 1 || MT_MAX == 1)
-    gemm_body<T, 1, S::TPW, S::KS, C::U, C::NS, S::EPI, MT_MAX>(a, M_end, tile, m0, red);
+    gemm_body<T, 1, S::TPW, S::KS, C::U, C::NS, S::EPI, MT_MAX>(a, M_end, tile, m0, red, ks);
   else if (mt == 2 || MT_MAX == 2)
-    gemm_body<T, (MT_MAX >= 2 ? 2 : 1), S::TPW, S::KS, C::U, C::NS, S::EPI, MT_MAX>(a, M_end, tile, m0, red);
+    gemm_body<T, (MT_MAX >= 2 ? 2 : 1), S::TPW, S::KS, C::U, C::NS, S::EPI, MT_MAX>(a, M_end, tile, m0, red, ks);
   else if (mt == 3 || MT_MAX == 3)
-    gemm_body<T, (MT_MAX >= 3 ? 3 : 1), S::TPW, S::KS, S::U, S::NS, S::EPI, MT_MAX>(a, M_end, tile, m0, red);
+    gemm_body<T, (MT_MAX >= 3 ? 3 : 1), S::TPW, S::KS, S::U, S::NS, S::EPI, MT_MAX>(a, M_end, tile, m0, red, ks);
   else
-    gemm_body<T, MT_MAX, S::TPW, S::KS, S::U, S::NS, S::EPI, MT_MAX>(a, M_end, tile, m0, red);
+    gemm_body<T, MT_MAX, S::TPW, S::KS, S::U, S::NS, S::EPI, MT_MAX>(a, M_end, tile, m0, red, ks);
 }
 
 // ------------------------------------------------------------------ planning and launch
@@ -647,25 +648,58 @@ LSV_DEV void gemm_wide_body(const GemmArgs& a, const int M, u32x4_t* Ws) {
   gemm_epilogue<T, MTW, FR, EPI, false>(a, M, mt0 * 16, tn0, tvalid, acc, none);
 }
 
-// One launch for any row count up to kWideRows: the body is chosen once per workgroup from
-// the device row count (1 to 5 activation tiles per wave).
-template <int EPI>
-__global__ void __launch_bounds__(256) gemm_wide_kernel(GemmArgs a) {
+// One launch for blocks under a batched row bound (64 < bound <= kWideRows).  Up to 64 device
+// rows, each of a workgroup's four waves runs the 64-row body on a column tile of its own --
+// tile (wave x grid + workgroup), so that the busy waves spread over the compute units -- and
+// streams its weights once, as gemm_kernel does (gate/up of the wider models with up to 32 rows
+// takes its eight-fragment-row configuration); more rows run the batched body on the
+// workgroup's (tile, k-split).  One launch instead of one of each kind, one of which would
+// find no work.
+template <int KIND, int WIDE_EPI>
+__global__ void __launch_bounds__(256) gemm_fused_kernel(GemmArgs a) {
   __shared__ u32x4_t Ws[2 * kWideFR * kWave];
-  const int rows = GL(a.row_offsets)[a.batch];
-  if (rows <= a.rows_lo || rows > a.rows_hi) return;  // another launch serves this row count
-  const int M = min(rows, a.M_max);  // never trust device rows beyond the host bound
-  const int mtw = ((M + 15) / 16 + 3) / 4;                 // activation tiles per wave
+  const int M = min(GL(a.row_offsets)[a.batch], a.M_max);  // never trust device rows beyond the host bound
+  if (M <= 64) {
+    if (M <= 0) return;
+    const int vt = (int)(threadIdx.x >> 6) * (int)gridDim.x + (int)blockIdx.x;  // this wave's column tile
+    const int mt = M <= 16 ? 1 : (M <= 32 ? 2 : (M <= 48 ? 3 : 4));
+    if constexpr (KIND == GEMM_GATEUP) {
+      if (a.Nt >= kGateUpWideRows && mt <= 2) {
+        using W = GemmCfg<kGateUpWide>;
+        if (vt >= (a.Nt + W::TPW - 1) / W::TPW) return;
+        if (mt == 1)
+          gemm_body<bf16_t, 1, W::TPW, 1, W::U, W::NS, W::EPI, 2>(a, M, vt, 0, nullptr, 0);
+        else
+          gemm_body<bf16_t, 2, W::TPW, 1, W::U, W::NS, W::EPI, 2>(a, M, vt, 0, nullptr, 0);
+        return;
+      }
+    }
+    using C = GemmCfg<KIND>;
+    using S = GemmShape<KIND, 4>;
+    static_assert(C::KS == 1, "one wave per column tile");
+    if (vt >= (a.Nt + S::TPW - 1) / S::TPW) return;
+    if (mt == 1)
+      gemm_body<bf16_t, 1, S::TPW, 1, C::U, C::NS, S::EPI, 4>(a, M, vt, 0, nullptr, 0);
+    else if (mt == 2)
+      gemm_body<bf16_t, 2, S::TPW, 1, C::U, C::NS, S::EPI, 4>(a, M, vt, 0, nullptr, 0);
+    else if (mt == 3)
+      gemm_body<bf16_t, 3, S::TPW, 1, S::U, S::NS, S::EPI, 4>(a, M, vt, 0, nullptr, 0);
+    else
+      gemm_body<bf16_t, 4, S::TPW, 1, S::U, S::NS, S::EPI, 4>(a, M, vt, 0, nullptr, 0);
+    return;
+  }
+  if ((int)blockIdx.x >= (a.Nt + kWideFR - 1) / kWideFR * a.splits) return;
+  const int mtw = ((M + 15) / 16 + 3) / 4;  // activation tiles per wave
   if (mtw <= 1)
-    gemm_wide_body<EPI, 1>(a, M, Ws);
+    gemm_wide_body<WIDE_EPI, 1>(a, M, Ws);
   else if (mtw == 2)
-    gemm_wide_body<EPI, 2>(a, M, Ws);
+    gemm_wide_body<WIDE_EPI, 2>(a, M, Ws);
   else if (mtw == 3)
-    gemm_wide_body<EPI, 3>(a, M, Ws);
+    gemm_wide_body<WIDE_EPI, 3>(a, M, Ws);
   else if (mtw == 4)
-    gemm_wide_body<EPI, 4>(a, M, Ws);
+    gemm_wide_body<WIDE_EPI, 4>(a, M, Ws);
   else
-    gemm_wide_body<EPI, 5>(a, M, Ws);
+    gemm_wide_body<WIDE_EPI, 5>(a, M, Ws);
 }
 
 // Split-K sums of the batched GEMM: one workgroup per (tile, 16 rows) adds the k ranges in
@@ -746,39 +780,52 @@ size_t wide_part_floats(const WidePlan& p, int M_max) {
   return p.splits > 1 ? (size_t)p.tiles * p.splits * M_max * kWideCols : 0;
 }
 
-template <int EPI>
-static void launch_wide_epi(const GemmArgs& a, const WidePlan& p, int max_rows, hipStream_t st) {
-  hipLaunchKernelGGL(gemm_wide_kernel<EPI>, dim3((unsigned)(p.tiles * p.splits)), dim3(256), 0, st, a);
-  if (p.splits > 1)
-    hipLaunchKernelGGL(gemm_wide_reduce_kernel<EPI>, dim3((unsigned)p.tiles, (unsigned)((max_rows + 15) / 16)), dim3(256),
-                       0, st, a);
+// The fused launch of a product (and, for the batched body, its split-K reduce or the separate
+// rotary-embedding pass; those return at once for blocks of up to 64 rows).
+template <int KIND, int WIDE_EPI>
+static void launch_fused_one(const GemmArgs& a, const WidePlan& p, hipStream_t st) {
+  using S = GemmShape<KIND, 4>;
+  const int skinny_wgs = ((a.Nt + S::TPW - 1) / S::TPW + 3) / 4;
+  const int grid = p.tiles * p.splits > skinny_wgs ? p.tiles * p.splits : skinny_wgs;
+  hipLaunchKernelGGL((gemm_fused_kernel<KIND, WIDE_EPI>), dim3((unsigned)grid), dim3(256), 0, st, a);
 }
 
-int launch_gemm_wide(GemmKind kind, const GemmArgs& a0, const WidePlan& p, hipStream_t st) {
+int launch_gemm_fused(GemmKind kind, const GemmArgs& a0, const WidePlan& p, hipStream_t st) {
   GemmArgs a = a0;
   a.splits = p.splits;
+  GemmArgs big = a;  // the passes after the batched body: only for more than 64 rows
+  big.rows_lo = 64;
+  const dim3 rgrid((unsigned)p.tiles, (unsigned)((a.M_max + 15) / 16));
   switch (kind) {
-    case GEMM_QKV: {
+    case GEMM_QKV:
       if (p.splits > 1) {
-        // the split-K reduce runs the rotary embedding and the Q store / cache append
-        hipLaunchKernelGGL(gemm_wide_kernel<EPI_LOGITS>, dim3((unsigned)(p.tiles * p.splits)), dim3(256), 0, st, a);
-        hipLaunchKernelGGL(gemm_wide_reduce_kernel<EPI_QKV>, dim3((unsigned)p.tiles, (unsigned)((a.M_max + 15) / 16)),
-                           dim3(256), 0, st, a);
-        break;
+        launch_fused_one<GEMM_QKV, EPI_LOGITS>(a, p, st);
+        hipLaunchKernelGGL(gemm_wide_reduce_kernel<EPI_QKV>, rgrid, dim3(256), 0, st, big);
+      } else {
+        if (!a.out_f32) return LSV_ERR_INVALID_ARG;
+        a.ldo = a.N;  // the batched body writes the projection to out_f32; the 64-row body does not read it
+        big.ldo = a.N;
+        launch_fused_one<GEMM_QKV, EPI_LOGITS>(a, p, st);
+        const size_t n = (size_t)a.M_max * (a.N / 4);
+        hipLaunchKernelGGL(qkv_rope_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, big, big.out_f32);
       }
-      // one split: the projection into the caller's fp32 buffer (out_f32, N columns),
-      // then RoPE (the fused epilogue would not fit the wide kernel's registers)
-      if (!a.out_f32) return LSV_ERR_INVALID_ARG;
-      a.ldo = a.N;
-      launch_wide_epi<EPI_LOGITS>(a, p, a.M_max, st);
-      const size_t n = (size_t)a.M_max * (a.N / 4);
-      hipLaunchKernelGGL(qkv_rope_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, a, a.out_f32);
       break;
-    }
-    case GEMM_O: launch_wide_epi<EPI_RESID>(a, p, a.M_max, st); break;
-    case GEMM_GATEUP: launch_wide_epi<EPI_SWIGLU>(a, p, a.M_max, st); break;
-    case GEMM_DOWN: launch_wide_epi<EPI_RESID>(a, p, a.M_max, st); break;
-    case GEMM_LMHEAD: launch_wide_epi<EPI_LOGITS>(a, p, a.M_max, st); break;
+    case GEMM_O:
+      launch_fused_one<GEMM_O, EPI_RESID>(a, p, st);
+      if (p.splits > 1) hipLaunchKernelGGL(gemm_wide_reduce_kernel<EPI_RESID>, rgrid, dim3(256), 0, st, big);
+      break;
+    case GEMM_GATEUP:
+      launch_fused_one<GEMM_GATEUP, EPI_SWIGLU>(a, p, st);
+      if (p.splits > 1) hipLaunchKernelGGL(gemm_wide_reduce_kernel<EPI_SWIGLU>, rgrid, dim3(256), 0, st, big);
+      break;
+    case GEMM_DOWN:
+      launch_fused_one<GEMM_DOWN, EPI_RESID>(a, p, st);
+      if (p.splits > 1) hipLaunchKernelGGL(gemm_wide_reduce_kernel<EPI_RESID>, rgrid, dim3(256), 0, st, big);
+      break;
+    case GEMM_LMHEAD:
+      launch_fused_one<GEMM_LMHEAD, EPI_LOGITS>(a, p, st);
+      if (p.splits > 1) hipLaunchKernelGGL(gemm_wide_reduce_kernel<EPI_LOGITS>, rgrid, dim3(256), 0, st, big);
+      break;
   }
   return hipGetLastError() == hipSuccess ? LSV_OK : LSV_ERR_HIP;
 }

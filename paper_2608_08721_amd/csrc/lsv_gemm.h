@@ -63,6 +63,8 @@ struct WidePlan {
 };
 WidePlan plan_wide(int Nt, int Kt);
 size_t wide_part_floats(const WidePlan& p, int M_max);
-int launch_gemm_wide(GemmKind kind, const GemmArgs& a, const WidePlan& p, hipStream_t st);
+// Blocks under a batched bound: one launch whose workgroups take the 64-row body or the batched
+// one from the device row count (plus the batched body's reduce, which returns for <= 64 rows).
+int launch_gemm_fused(GemmKind kind, const GemmArgs& a, const WidePlan& p, hipStream_t st);
 
 }  // namespace lsv
