@@ -28,10 +28,13 @@ constexpr int kCh = kAttnChunk;  // keys per chunk
 // chunks (a split walks its chunks in sequence).  Fewer splits mean fewer partials to merge
 // -- one batch of merge loads for up to 16 -- against longer chunk walks; 128 measured best
 // for one sequence of 2K context (11 splits of 3 chunks).  The length cap keeps the
-// workgroups of a batch with long contexts from running too long; 8 measured slower than 16
-// for eight sequences with 1K-8K contexts (more partials to write and merge).
+// workgroups of a batch with long contexts from running too long -- but never beyond one
+// workgroup per compute unit: a grid larger than the chip runs its last workgroups in a
+// second round, which costs more than longer splits (Llama-3-70B, four sequences of 8K
+// context: 9 splits, 288 workgroups, 49 us; 8 splits, 256 workgroups, 34 us).
 constexpr int kAttnWgs = 128;
 constexpr int kMaxChunksPerSplit = 16;
+constexpr int kComputeUnits = 256;  // gfx950 (MI350X, MI355X)
 
 AttnPlan plan_attention(int batch, int nkv, int max_ctx) {
   const int n_chunks = (max_ctx + kCh - 1) / kCh;
@@ -39,6 +42,8 @@ AttnPlan plan_attention(int batch, int nkv, int max_ctx) {
   int want = (kAttnWgs + units - 1) / units;
   const int by_length = (n_chunks + kMaxChunksPerSplit - 1) / kMaxChunksPerSplit;
   if (want < by_length) want = by_length;
+  const int fit = kComputeUnits / units;  // splits per (sequence, kv head) in one round
+  if (want > fit) want = fit;
   if (want > n_chunks) want = n_chunks;
   if (want < 1) want = 1;
   AttnPlan p;
@@ -67,7 +72,10 @@ __global__ void __launch_bounds__(64 * NW) attn_split_bf16_kernel(AttnArgs a) {
   __shared__ __align__(16) bf16_t Vt[NG][HD * VPITCH];
 
   const int s = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, g4 = lane >> 4, l16 = lane & 15;
+  // the wave index in a scalar register: the group, its chunk offsets and the page-table reads
+  // are then wave-uniform, and the buffer loads take their chunk offsets in scalar registers
+  const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
+  const int g4 = lane >> 4, l16 = lane & 15;
   const int grp = wave >> 2, gtid = tid & 255;
   // Slab mode: the grid covers the chunks of ctx_limit <= capacity and capacity is a multiple
   // of the chunk, so every chunk below capacity / kCh lies inside the slab.  Paged mode: a
