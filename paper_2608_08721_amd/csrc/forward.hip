@@ -214,13 +214,54 @@ LSV_DEV void normalise_row(const float* __restrict__ hrow, int d, const float* _
   }
 }
 
-// The consumer operand of the next projection, one workgroup per block row.
+// The consumer operand of the next projection, one workgroup per block row.  part: the k-split
+// partial sums [tile][split][M_max][kWideCols] that the batched body of the residual product
+// before it left for a block of more than 64 rows (NULL when that product runs unsplit): they
+// are added in split order and the sum joins the residual stream, h += sum, before the row is
+// normalised.
 template <typename T>
-__global__ void __launch_bounds__(256) rmsnorm_kernel(const float* __restrict__ h, int d, const float* gain, float eps,
-                                                      const int32_t* row_offsets, int batch, int M_max, T* a) {
+__global__ void __launch_bounds__(256) rmsnorm_kernel(float* __restrict__ h, int d, const float* gain, float eps,
+                                                      const int32_t* row_offsets, int batch, int M_max, T* a,
+                                                      const float* __restrict__ part, int splits) {
   const int m = blockIdx.x;
-  if (m >= GL(row_offsets)[batch] || m >= M_max) return;
-  normalise_row<T>(h + (size_t)m * d, d, gain, eps, m, a);
+  const int M = min(GL(row_offsets)[batch], M_max);
+  if (m >= M) return;
+  float* hrow = h + (size_t)m * d;
+  if (part && M > 64) {
+    // thread t: columns 4 (t + 256 r) .. +3, r < RUNS (d <= 8192); the partials of JB splits
+    // for all of its columns are in flight at once
+    constexpr int RUNS = 8192 / 1024, JB = 4;
+    const size_t jstride = (size_t)M_max * kWideCols;
+    f32x4_t acc[RUNS];
+#pragma unroll
+    for (int r = 0; r < RUNS; ++r) acc[r] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    for (int j0 = 0; j0 < splits; j0 += JB) {
+      f32x4_t v[JB][RUNS];
+#pragma unroll
+      for (int r = 0; r < RUNS; ++r) {
+        const int c = (threadIdx.x + 256 * r) * 4;
+        const GLOBAL float* p =
+            GL(part) + ((size_t)(min(c, d - 4) / kWideCols) * splits * M_max + m) * kWideCols + min(c, d - 4) % kWideCols;
+#pragma unroll
+        for (int i = 0; i < JB; ++i) v[i][r] = *(const GLOBAL f32x4_t*)(p + (size_t)min(j0 + i, splits - 1) * jstride);
+      }
+#pragma unroll
+      for (int i = 0; i < JB; ++i)
+        if (j0 + i < splits)
+#pragma unroll
+          for (int r = 0; r < RUNS; ++r) acc[r] += v[i][r];
+    }
+#pragma unroll
+    for (int r = 0; r < RUNS; ++r) {
+      const int c = (threadIdx.x + 256 * r) * 4;
+      if (c < d) {
+        const f32x4_t hv = *(const GLOBAL f32x4_t*)(GL(hrow) + c);
+        *(GLOBAL f32x4_t*)(GL(hrow) + c) = hv + acc[r];
+      }
+    }
+    __syncthreads();  // the workgroup's stores of the row are visible to its own loads below
+  }
+  normalise_row<T>(hrow, d, gain, eps, m, a);
 }
 
 // ------------------------------------------------------------------ tree blocks
@@ -339,13 +380,17 @@ int launch_verify(const Shape& s, const ModelLayout& ml, const void* packed, voi
                        (float*)w.a, tree_bad, status);
   if (hipGetLastError() != hipSuccess) return LSV_ERR_HIP;
   // a = R(h / rms(h) * gain) for the next projection
-  auto rmsnorm = [&](const float* gain) {
+  // a = R(h / rms(h) * gain) for the next projection, after the k-split partials of the
+  // residual product before it (batched bounds) join h
+  auto rmsnorm = [&](const float* gain, GemmKind after) {
+    const int splits = v.wide ? v.w[after].splits : 1;
+    const float* part = splits > 1 ? w.part : nullptr;
     if (bf16)
       hipLaunchKernelGGL(rmsnorm_kernel<bf16_t>, dim3(max_rows), dim3(256), 0, st, w.h, s.d, gain, s.eps, row_offsets,
-                         batch, max_rows, (bf16_t*)w.a);
+                         batch, max_rows, (bf16_t*)w.a, part, splits);
     else
       hipLaunchKernelGGL(rmsnorm_kernel<float>, dim3(max_rows), dim3(256), 0, st, w.h, s.d, gain, s.eps, row_offsets,
-                         batch, max_rows, (float*)w.a);
+                         batch, max_rows, (float*)w.a, part, splits);
     return hipGetLastError() == hipSuccess ? LSV_OK : LSV_ERR_HIP;
   };
 
@@ -430,7 +475,7 @@ int launch_verify(const Shape& s, const ModelLayout& ml, const void* packed, voi
     a.x = w.attn;
     a.h_out = w.h;
     if ((rc = gemm(GEMM_O, ml.o, LB, a)) != LSV_OK) return rc;
-    if ((rc = rmsnorm(layer_gain(l, ml.ffn_norm))) != LSV_OK) return rc;
+    if ((rc = rmsnorm(layer_gain(l, ml.ffn_norm), GEMM_O)) != LSV_OK) return rc;
     // gate/up (normalised input) + SwiGLU
     a = base;
     a.layer_index = l;
@@ -444,7 +489,8 @@ int launch_verify(const Shape& s, const ModelLayout& ml, const void* packed, voi
     a.h_out = w.h;
     if ((rc = gemm(GEMM_DOWN, ml.down, LB, a)) != LSV_OK) return rc;
     // the next projection's operand: the next layer's attention norm, or the final norm
-    if ((rc = rmsnorm(l + 1 < s.L ? layer_gain(l + 1, ml.attn_norm) : (const float*)(P + ml.final_norm))) != LSV_OK)
+    if ((rc = rmsnorm(l + 1 < s.L ? layer_gain(l + 1, ml.attn_norm) : (const float*)(P + ml.final_norm), GEMM_DOWN)) !=
+        LSV_OK)
       return rc;
   }
   GemmArgs a = base;

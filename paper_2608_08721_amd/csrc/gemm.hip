@@ -531,12 +531,10 @@ static int launch_typed(GemmKind kind, int MT, const GemmArgs& a, hipStream_t st
 // gemm_wide_reduce_kernel adds them in split order (deterministic) and runs the epilogue,
 // one workgroup per (tile, 16 rows); the QKV reduce applies the rotary embedding and the Q
 // store / cache append.  An unsplit QKV runs the plain epilogue into an fp32 buffer
-// and qkv_rope_kernel does the rest.
-constexpr int kWideFR = 8;     // fragment rows of a workgroup
+// and qkv_rope_kernel does the rest.  The residual products (O, down) launch no reduce: the
+// row normalisation that follows each of them adds their partials to the residual stream.
 constexpr int kWideRingW = 10;  // k-steps of weight pieces in flight (register ring)
 constexpr int kWideRingX = 2;   // k-steps of activation fragments in flight (from L2)
-
-constexpr int kWideCols = kWideFR * 16;  // output columns of a workgroup
 
 // The body for MTW activation tiles per wave.  The workgroup's 8 weight fragments of a
 // k-step go HBM -> registers -> LDS (double buffered) and every wave reads all 8; each wave
@@ -810,17 +808,15 @@ int launch_gemm_fused(GemmKind kind, const GemmArgs& a0, const WidePlan& p, hipS
         hipLaunchKernelGGL(qkv_rope_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, big, big.out_f32);
       }
       break;
-    case GEMM_O:
+    case GEMM_O:  // k-split partials are added by the next row normalisation
       launch_fused_one<GEMM_O, EPI_RESID>(a, p, st);
-      if (p.splits > 1) hipLaunchKernelGGL(gemm_wide_reduce_kernel<EPI_RESID>, rgrid, dim3(256), 0, st, big);
       break;
     case GEMM_GATEUP:
       launch_fused_one<GEMM_GATEUP, EPI_SWIGLU>(a, p, st);
       if (p.splits > 1) hipLaunchKernelGGL(gemm_wide_reduce_kernel<EPI_SWIGLU>, rgrid, dim3(256), 0, st, big);
       break;
-    case GEMM_DOWN:
+    case GEMM_DOWN:  // k-split partials are added by the next row normalisation
       launch_fused_one<GEMM_DOWN, EPI_RESID>(a, p, st);
-      if (p.splits > 1) hipLaunchKernelGGL(gemm_wide_reduce_kernel<EPI_RESID>, rgrid, dim3(256), 0, st, big);
       break;
     case GEMM_LMHEAD:
       launch_fused_one<GEMM_LMHEAD, EPI_LOGITS>(a, p, st);

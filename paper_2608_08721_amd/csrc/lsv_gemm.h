@@ -58,6 +58,8 @@ int launch_gemm(int dtype, GemmKind kind, int MT, const GemmArgs& a, hipStream_t
 
 // Batched blocks (bf16, 64 < rows <= kWideRows): every row in one workgroup, activations via LDS.
 constexpr int kWideRows = LSV_WIDE_ROWS;
+constexpr int kWideFR = 8;               // fragment rows of a batched workgroup's column tile
+constexpr int kWideCols = kWideFR * 16;  // its output columns: k-split partials are [tile][split][M_max][kWideCols]
 struct WidePlan {
   int tiles, splits;
 };
@@ -65,6 +67,8 @@ WidePlan plan_wide(int Nt, int Kt);
 size_t wide_part_floats(const WidePlan& p, int M_max);
 // Blocks under a batched bound: one launch whose workgroups take the 64-row body or the batched
 // one from the device row count (plus the batched body's reduce, which returns for <= 64 rows).
+// The residual products (GEMM_O, GEMM_DOWN) with more than one k-split leave their partials in
+// a.part for more than 64 rows: the caller's next row normalisation adds them to h.
 int launch_gemm_fused(GemmKind kind, const GemmArgs& a, const WidePlan& p, hipStream_t st);
 
 }  // namespace lsv
