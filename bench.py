@@ -61,8 +61,9 @@ def parse():
                    help="acceptance rule of the timed steps (default: greedy where the workload has it, else "
                         "speculative rejection sampling at the workload's temperature)")
     p.add_argument("--no-cpu-baseline", action="store_true")
-    p.add_argument("--rounds", type=int, default=0,
-                   help="also run multi-round decoding for this many rounds per length policy (planted drafter)")
+    p.add_argument("--rounds", type=int, default=12,
+                   help="multi-round decoding of the primary workload: rounds per length policy (planted drafter; "
+                        "0 skips it)")
     p.add_argument("--calib-copy", action="store_true",
                    help="also run one plain 256 MiB copy kernel (counter calibration for --pmc runs)")
     p.add_argument("--counters-only", type=int, default=0, metavar="GAMMA",
@@ -480,6 +481,60 @@ def cpu_baseline(m, seed, ctx, rows_per_seq, tokens, exp_tok):
             "seconds_per_step": t_step}
 
 
+def length_rules(wl, cost, dev, n_rows=4096):
+    """The length rules on the measured cost table over many draws of the workload's
+    confidence model -- the synthetic analogue of the trade-off sensitivity of Table 4 and of
+    the deviation from the oracle length of Sec. 4.7.  Per rule: mean length, mean
+    |gamma - gamma_exhaustive|, and the mean of f(gamma) / f(gamma_exhaustive) with
+    f = (1 + sum_{j<=gamma} prod_{k<=j} q_k) / cost[gamma] (Eq. 2's objective with the always
+    emitted token); Algorithm 1 also the drafter blocks of n its budget requests.  All
+    selections run in the library's selector on the GPU."""
+    import torch
+
+    from paper_2608_08721_amd import lsv
+    from synth import gen
+    G = wl.G
+    conf_np = gen.confidences(wl, seed=wl.seed + 7, batch=n_rows)
+    conf = torch.tensor(conf_np, device=dev)
+    cost_t = torch.tensor(cost, dtype=torch.float64, device=dev)
+    gamma = torch.zeros(n_rows, dtype=torch.int32, device=dev)
+    aux = torch.zeros(n_rows, dtype=torch.int32, device=dev)
+    p = np.cumprod(conf_np.astype(np.float64), axis=1)
+    n_tok = 1.0 + np.cumsum(p, axis=1)                      # N(gamma), gamma = 1..G
+    f = n_tok / np.asarray(cost[1:G + 1], dtype=np.float64)[None, :]
+    rows = np.arange(n_rows)
+
+    def run(mode, alpha=2.2, n=8, d_init=1):
+        lsv.lsv_select_length(mode, n_rows, G, conf, cost_t, d_init, G, alpha, n, 0, gamma, aux, None, None)
+        torch.cuda.synchronize()
+        return gamma.cpu().numpy().astype(np.int64), aux.cpu().numpy().astype(np.int64)
+
+    g_ex, _ = run(lsv.LSV_SEL_EXHAUSTIVE)
+    f_ex = f[rows, g_ex - 1]
+
+    def summary(g, extra=None):
+        r = {"mean_gamma": round(float(g.mean()), 3), "mad_vs_exhaustive": round(float(np.abs(g - g_ex).mean()), 3),
+             "objective_vs_exhaustive": round(float((f[rows, g - 1] / f_ex).mean()), 4)}
+        if extra:
+            r.update(extra)
+        return r
+    out = {"rows": n_rows, "confidence_model": list(wl.conf), "cost": "the measured per-gamma step latency",
+           "exhaustive": summary(g_ex)}
+    out["marginal_from_1"] = summary(run(lsv.LSV_SEL_MARGINAL, d_init=1)[0])
+    out["marginal_from_G"] = summary(run(lsv.LSV_SEL_MARGINAL, d_init=G)[0])
+    for n in (8, 16):
+        if n > G:
+            continue
+        for a in (1.8, 2.0, 2.2, 2.6):
+            g, blk = run(lsv.LSV_SEL_ALG1, alpha=a, n=n)
+            out[f"alg1_n{n}_alpha{a}"] = summary(g, {"mean_blocks": round(float(blk.mean()), 3),
+                                                     "blocks_all_up_front": -(-G // n)})
+    mean_f = f.mean(axis=0)
+    g_st = int(np.argmax(mean_f)) + 1                       # the best single static length on these draws
+    out[f"static_best_{g_st}"] = summary(np.full(n_rows, g_st))
+    return out
+
+
 def decode_loop_measure(m, cfg, dm, B, G, ctx, prompts, pre, rows_buf, roots, cost, cost_total, seed, n_rounds, dev):
     """Multi-round decoding (select or a baseline policy -> pack -> verify -> accept -> next
     roots, one graph per round) on its own cache with room for the rounds, fed by the planted
@@ -535,8 +590,8 @@ def decode_loop_measure(m, cfg, dm, B, G, ctx, prompts, pre, rows_buf, roots, co
                 lsv.lsv_select_length(lsv.LSV_SEL_EXHAUSTIVE, B, G, loop.conf, cost_d, 1, G, 0.0, 1, 0, g_ex, None,
                                       None, None)
                 mad += [abs(a - e) for a, e in zip(loop.gamma.cpu().tolist(), g_ex.cpu().tolist())]
-            if blocks is not None:
-                blocks += loop.aux.cpu().tolist()
+            if blocks is not None:  # blocks the drafter produced this round (on demand for alg1)
+                blocks += loop.blocks.cpu().tolist()
             for b, e in enumerate(loop.emitted()):
                 got[b] += e
         return got
@@ -556,6 +611,10 @@ def decode_loop_measure(m, cfg, dm, B, G, ctx, prompts, pre, rows_buf, roots, co
     dr = drafter.PlantedDrafter(stream, q, seed, m.vocab, G, device=dev)
     base_tps = tok_plain / (ms_plain * 1e-3)
     out = {"rounds": n_rounds, "drafter": "planted greedy stream, confidences Beta(6, 1.5), calibrated",
+           "stream_note": "blocks of more than 64 rows take the batched GEMM path, whose split-K sum rounds "
+                          "differently in bf16 from the 64-row path that plain decoding takes: such a policy's "
+                          "greedy stream can part from plain decoding at a near-tie (the blocks of at most 64 rows "
+                          "give bit-identical rows whatever their size)",
            "plain_decoding": {"tokens_per_s": base_tps, "ms_per_token": ms_plain / max(tok_plain, 1)},
            "policies": {}}
     policies = [("static", g, None) for g in (2, 4, 8, G)] + [("marginal", None, None), ("g4", 8, None)]
@@ -577,8 +636,9 @@ def decode_loop_measure(m, cfg, dm, B, G, ctx, prompts, pre, rows_buf, roots, co
         out["policies"][name] = {"tokens_per_round": toks / (n_rounds * B), "ms_per_round": ms / n_rounds,
                                  "tokens_per_s": toks / (ms * 1e-3), "speedup_vs_plain": toks / (ms * 1e-3) / base_tps,
                                  "mad_vs_exhaustive": statistics.mean(mad), "stream_equals_plain": same}
-        if blocks:  # drafter blocks of n = 8 that Algorithm 1 asked for per sequence and round
+        if blocks:  # drafter blocks of n = 8 that Algorithm 1's budget requested per sequence and round
             out["policies"][name]["blocks_per_round"] = statistics.mean(blocks)
+            out["policies"][name]["blocks_all_up_front"] = -(-G // 8)
         del loop
     return out
 
@@ -997,6 +1057,8 @@ def measure(w, args, primary=True):
         result["uniform_gamma_max"] = {"gamma": G, "rows": rows_g, "latency_us": sweep[G] * 1e3,
                                        "mfma_frac": step_flops(m, ctx, [G + 1] * B) / t_g / MFMA_PEAK_FLOPS,
                                        "hbm_frac": step_bytes(m, ctx, rows_g) / t_g / 1e9 / HBM_PEAK_GBPS}
+    if primary:
+        result["length_rules"] = length_rules(wl, cost, dev)
     if primary and args.rounds > 0:
         log(f"decode loop: {args.rounds} rounds per length policy")
         try:

@@ -338,20 +338,29 @@ int lsv_commit_tree_paged(const lsv_model_config* cfg, void* d_kv_pool, int32_t 
  *   eps*(d) at the first d where eps*(d) <= d (the single rollback); d_max also stops it.
  *   cost is not read.  aux = drafter blocks of n used: ceil(d_peak / n), d_peak the
  *   highest length reached (Algorithm 1's budget of drafted but unused tokens).
+ *   With LSV_SEL_DRAFTED (blocks on demand) d_aux is in/out: in, the blocks of n drafted
+ *   so far for the sequence (>= 1); only the first min(aux * n, G) confidences are read.
+ *   When the length reaches past them (the budget goes negative) the rule stops with
+ *   gamma = 0 and aux = ceil(d / n), the blocks it needs before it is run again; run
+ *   again with those blocks it takes the same steps, so after at most ceil(d_max / n)
+ *   calls it ends where the rule over all G confidences ends, with the same aux.
  *
  *   d_conf   [batch, G] fp32 confidences in [0, 1]
  *   d_cost   [G+1] fp64 verification cost of each length, cost[0] unused; cost[d] > 0
  *            for d <= d_max (MARGINAL / EXHAUSTIVE; may be NULL for ALG1)
- *   flags    LSV_SEL_BONUS: count the always-emitted token in N(d)
- *   d_gamma  [batch] out; d_aux [batch] out (nullable)
+ *   flags    LSV_SEL_BONUS: count the always-emitted token in N(d);
+ *            LSV_SEL_DRAFTED: ALG1 with blocks on demand (above; needs d_aux)
+ *   d_gamma  [batch] out (0: more blocks needed, LSV_SEL_DRAFTED only);
+ *            d_aux [batch] out (nullable; in/out with LSV_SEL_DRAFTED)
  *   d_row_offsets [batch+1] out (nullable; needs batch <= LSV_MAX_BATCH): the row layout of
  *            the verify block that follows, row_offsets[0] = 0 and
  *            row_offsets[b+1] = row_offsets[b] + gamma_b + 1 (root plus gamma_b drafts), so
  *            select -> verify -> accept can run without a host round trip
  *   d_status [batch] out (nullable): LSV_OK, or LSV_ERR_INVALID_ARG when a confidence is
- *            outside [0, 1] or a needed cost is not finite and positive (then gamma = 0). */
+ *            outside [0, 1], a needed cost is not finite and positive, or (LSV_SEL_DRAFTED)
+ *            the blocks drafted are fewer than one (then gamma = 0). */
 enum { LSV_SEL_MARGINAL = 0, LSV_SEL_EXHAUSTIVE = 1, LSV_SEL_ALG1 = 2 };
-enum { LSV_SEL_BONUS = 1 };
+enum { LSV_SEL_BONUS = 1, LSV_SEL_DRAFTED = 2 };
 enum { LSV_MAX_G = 64 };
 int lsv_select_length(int32_t mode, int32_t batch, int32_t G, const float* d_conf, const double* d_cost,
                       int32_t d_init, int32_t d_max, double alpha, int32_t block_n, uint32_t flags,

@@ -103,7 +103,7 @@ def eps_star(q, d, alpha):
     return best
 
 
-def select_alg1(q, d_max, alpha, n, trace=None):
+def select_alg1(q, d_max, alpha, n, trace=None, drafted=None):
     """Algorithm 1 (LibraSpec), restated.  q holds the confidences of all G drafted tokens;
     d_max <= G.
 
@@ -119,10 +119,17 @@ def select_alg1(q, d_max, alpha, n, trace=None):
     budget at length d is (-d) mod n.
 
     Returns (d, blocks).  ``trace`` (a list) receives (d, eps*(d), budget) for every
-    evaluation of eps*."""
+    evaluation of eps*.
+
+    drafted (blocks on demand): only the first drafted * n confidences exist (q may be
+    shorter).  When the length reaches past them -- the budget of drafted but unused tokens
+    goes negative -- the rule cannot go on: it returns (0, blocks), blocks = ceil(d / n) being
+    what the drafter must have produced before the rule is run again.  Run again with more
+    blocks it takes the same steps, so it ends where the rule over all G confidences ends."""
+    avail = len(q) if drafted is None else min(drafted * n, len(q))
     d = min(n, d_max)
     settled = None
-    while settled is None and d < d_max:
+    while settled is None and d < d_max and d <= avail:
         e = eps_star(q, d, alpha)
         if trace is not None:
             trace.append((d, e, (-d) % n))
@@ -131,6 +138,8 @@ def select_alg1(q, d_max, alpha, n, trace=None):
         else:
             settled = e            # stay, or one step back
     blocks = max(1, -(-d // n))    # d is the highest length reached here
+    if settled is None and d > avail:
+        return 0, blocks           # more blocks first
     return (d if settled is None else settled), blocks
 
 

@@ -337,7 +337,9 @@ int lsv_select_length(int32_t mode, int32_t batch, int32_t G, const float* d_con
   if (batch < 1 || G < 1 || G > LSV_MAX_G) return fail(LSV_ERR_INVALID_ARG, "need batch >= 1 and 1 <= G <= %d", LSV_MAX_G);
   if (d_max < 1 || d_max > G) return fail(LSV_ERR_INVALID_ARG, "need 1 <= d_max (%d) <= G (%d)", d_max, G);
   if (!d_conf || !d_gamma) return fail(LSV_ERR_INVALID_ARG, "NULL pointer");
-  if (flags & ~(uint32_t)LSV_SEL_BONUS) return fail(LSV_ERR_INVALID_ARG, "unknown flags");
+  if (flags & ~(uint32_t)(LSV_SEL_BONUS | LSV_SEL_DRAFTED)) return fail(LSV_ERR_INVALID_ARG, "unknown flags");
+  if ((flags & LSV_SEL_DRAFTED) && (mode != LSV_SEL_ALG1 || !d_aux))
+    return fail(LSV_ERR_INVALID_ARG, "LSV_SEL_DRAFTED needs LSV_SEL_ALG1 and d_aux (blocks drafted)");
   if (d_row_offsets && batch > LSV_MAX_BATCH)
     return fail(LSV_ERR_INVALID_ARG, "row offsets need batch <= %d", LSV_MAX_BATCH);
   if (mode == LSV_SEL_ALG1) {

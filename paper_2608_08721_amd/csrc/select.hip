@@ -58,8 +58,14 @@ LSV_DEV int select_wave(int mode, int G, const float* __restrict__ conf, const d
                         int d_max, double alpha, int block_n, unsigned flags, int b, int32_t* __restrict__ aux,
                         int32_t* __restrict__ status) {
   const int lane = threadIdx.x & 63;
-  const float q = lane < G ? conf[(size_t)b * G + lane] : 0.0f;
-  bool bad = lane < G && !(q >= 0.0f && q <= 1.0f);  // true for NaN
+  // blocks on demand (ALG1): only the first aux[b] * n confidences have been drafted, and
+  // only those are read
+  const bool on_demand = mode == LSV_SEL_ALG1 && (flags & LSV_SEL_DRAFTED);
+  const int drafted = on_demand ? aux[b] : 0;
+  const long long dn = (long long)drafted * block_n;
+  const int avail = !on_demand ? G : (drafted < 1 ? 0 : (dn < G ? (int)dn : G));
+  const float q = lane < avail ? conf[(size_t)b * G + lane] : 0.0f;
+  bool bad = (lane < avail && !(q >= 0.0f && q <= 1.0f)) || (on_demand && drafted < 1);  // true for NaN
   if (mode != LSV_SEL_ALG1 && lane < d_max) {
     const double c = cost[lane + 1];
     bad = bad || !(c > 0.0 && c <= 1.7976931348623157e308);
@@ -71,15 +77,18 @@ LSV_DEV int select_wave(int mode, int G, const float* __restrict__ conf, const d
       // Algorithm 1: from the block size the length climbs along d -> min(eps*(d), d_max)
       // while that raises it, and settles on eps*(d) (itself, or one step back) at the first d
       // where it does not.  Blocks: enough drafter blocks of n to cover the highest length.
+      // A length past the drafted confidences (the budget went negative) stops the rule with
+      // gamma 0 and the blocks it needs.
       d = block_n < d_max ? block_n : d_max;
       int settled = 0;  // eps* >= 1 always, so 0 means "still climbing"
-      while (settled == 0 && d < d_max) {
+      while (settled == 0 && d < d_max && d <= avail) {
         const int e = eps_star_wave(q, d, alpha, lane);
         if (e > d) d = e < d_max ? e : d_max;
         else settled = e;
       }
       a = (d + block_n - 1) / block_n;  // d >= 1 here, so at least one block
       if (settled) d = settled;
+      else if (d > avail) d = 0;  // more blocks first
     } else {
       const double f = objective_lane(q, cost, d_max, (flags & LSV_SEL_BONUS) != 0, lane);
       if (mode == LSV_SEL_EXHAUSTIVE) {

@@ -13,7 +13,20 @@ the joint rule.  The status array is shared by verify and accept: the acceptance
 sequence whose verify step failed (for instance a block past ``max_ctx``), so nothing is
 committed for it and its root is kept.  ``capture()`` records one round in a
 graph; ``replay()`` runs it.  This module only marshals buffers: every step runs in the
-library's kernels."""
+library's kernels.
+
+Blocks on demand (Algorithm 1's budget): with the 'alg1' policy and a drafter that has
+``fill_blocks(seq_len, have, want, drafts, conf, n)`` (fill the blocks of n = ``block_n``
+drafts [have_b, want_b) of each sequence), a round drafts the first block only, runs the rule with
+LSV_SEL_DRAFTED, drafts the blocks it asks for, and runs it again -- at most
+ceil(G / block_n) times, all on the device -- so the drafter produces exactly the blocks the
+rule's budget requests (``blocks`` after the round).  Other policies draft all G tokens.
+
+Sampling (Sec. 3.1's sampling setting): ``accept="sample"`` with a temperature and a seed
+uses lsv_accept's speculative rejection sampling; the drafter is then called as
+``drafter(seq_len, drafts, conf, probs)`` and also writes its proposal distributions
+probs [B, G, vocab] (draft k of sequence b drawn from probs[b, k]).  The Philox round index
+is the round count, a host argument, so sampling rounds run eagerly (no capture)."""
 import torch
 
 from . import lsv, runtime
@@ -23,9 +36,13 @@ POLICIES = ("marginal", "exhaustive", "alg1", "joint", "g4", "static")
 
 class DecodeLoop:
     def __init__(self, cfg, dm, kv, capacity, batch, G, policy, drafter, cost=None, alpha=2.2, block_n=8,
-                 d_min=1, gamma0=None, max_ctx=None, device="cuda"):
+                 d_min=1, gamma0=None, max_ctx=None, device="cuda", accept="greedy", temperature=1.0, seed=0):
         if policy not in POLICIES:
             raise ValueError(f"policy must be one of {POLICIES}")
+        if accept not in ("greedy", "sample"):
+            raise ValueError("accept must be 'greedy' or 'sample'")
+        if accept == "sample" and not temperature > 0.0:
+            raise ValueError("sampling needs a temperature > 0")
         if policy in ("marginal", "exhaustive", "joint") and cost is None:
             raise ValueError("the marginal, exhaustive and joint rules need a cost table")
         if cost is not None and policy in ("marginal", "exhaustive", "joint"):
@@ -52,6 +69,19 @@ class DecodeLoop:
         self.out = torch.zeros((B, self.width), **i32)
         self.logits = torch.zeros((self.max_rows, cfg.vocab), dtype=torch.float32, device=device)
         self.cost = torch.tensor(cost, dtype=torch.float64, device=device) if cost is not None else None
+        # blocks on demand: blocks drafted this round per sequence
+        self.on_demand = policy == "alg1" and G > 0 and hasattr(drafter, "fill_blocks")
+        self.blocks = torch.zeros(B, **i32)
+        self.no_blocks = torch.zeros(B, **i32)
+        self.accept, self.temperature, self.seed, self.rounds = accept, float(temperature), int(seed), 0
+        if accept == "sample":
+            # proposal distributions in the drafter's layout, and in lsv_accept's (row
+            # row_offsets[b] - b + v - 1 holds q_v of sequence b; one spare row takes the
+            # positions past each sequence's gamma)
+            self.probs = torch.zeros((B, max(G, 1), cfg.vocab), dtype=torch.float32, device=device)
+            self.draft_probs = torch.zeros((B * max(G, 1) + 1, cfg.vocab), dtype=torch.float32, device=device)
+            self.kk = torch.arange(max(G, 1), dtype=torch.int64, device=device)
+            self.bb = torch.arange(B, dtype=torch.int64, device=device)
         self.ws = runtime.Workspace(lsv.lsv_verify_workspace_bytes(cfg, B, self.max_rows, capacity))
         self.aws = runtime.Workspace(lsv.lsv_accept_workspace_bytes(B, self.max_rows, cfg.vocab))
         g0 = G if gamma0 is None else gamma0
@@ -72,11 +102,35 @@ class DecodeLoop:
             self.acc.fill_(acc)
             self.status.zero_()
 
+    def _draft_on_demand(self):
+        """Algorithm 1 with blocks on demand: the first block, then what the rule asks for."""
+        B, G, n = self.B, self.G, self.block_n
+        self.blocks.fill_(1)
+        self.drafter.fill_blocks(self.seq_len, self.no_blocks, self.blocks, self.drafts, self.conf, n)
+        for _ in range(-(-G // n)):
+            self.aux.copy_(self.blocks)
+            lsv.lsv_select_length(lsv.LSV_SEL_ALG1, B, G, self.conf, None, 1, G, self.alpha, n, lsv.LSV_SEL_DRAFTED,
+                                  self.gamma, self.aux, self.row_off, self.status)
+            self.drafter.fill_blocks(self.seq_len, self.blocks, self.aux, self.drafts, self.conf, n)
+            torch.maximum(self.blocks, self.aux, out=self.blocks)
+        # the rule over the drafted blocks ends here (it never asks for more than it reaches)
+        self.aux.copy_(self.blocks)
+        lsv.lsv_select_length(lsv.LSV_SEL_ALG1, B, G, self.conf, None, 1, G, self.alpha, n, lsv.LSV_SEL_DRAFTED,
+                              self.gamma, self.aux, self.row_off, self.status)
+
     def round(self):
         B, G = self.B, self.G
-        if G > 0 and self.drafter is not None:  # no drafter: the drafts buffer keeps its contents
-            self.drafter(self.seq_len, self.drafts, self.conf)
-        if self.policy in ("marginal", "exhaustive", "alg1"):
+        if self.on_demand:
+            self._draft_on_demand()
+        elif G > 0 and self.drafter is not None:  # no drafter: the drafts buffer keeps its contents
+            if self.accept == "sample":
+                self.drafter(self.seq_len, self.drafts, self.conf, self.probs)
+            else:
+                self.drafter(self.seq_len, self.drafts, self.conf)
+            self.blocks.fill_(-(-G // self.block_n))
+        if self.on_demand:
+            pass  # the length came with the drafting
+        elif self.policy in ("marginal", "exhaustive", "alg1"):
             mode = {"marginal": lsv.LSV_SEL_MARGINAL, "exhaustive": lsv.LSV_SEL_EXHAUSTIVE,
                     "alg1": lsv.LSV_SEL_ALG1}[self.policy]
             lsv.lsv_select_length(mode, B, G, self.conf, self.cost, 1, G, self.alpha, self.block_n, 0, self.gamma,
@@ -95,13 +149,26 @@ class DecodeLoop:
             lsv.lsv_verify_block(self.cfg, self.dm.buf, self.kv.buf, self.cap, B, self.seq_len, self.tokens,
                                  self.row_off, self.max_rows, self.max_ctx, self.logits, self.status, self.ws.buf,
                                  self.ws.nbytes)
-        lsv.lsv_accept(lsv.LSV_ACC_GREEDY, B, self.cfg.vocab, self.logits, self.row_off, self.max_rows, self.width,
-                       self.tokens, None, 0.0, 0, 0, self.acc, self.out, self.seq_len, self.status, self.aws.buf,
-                       self.aws.nbytes)
+        if self.accept == "sample":
+            # q_v of sequence b to row row_offsets[b] - b + v - 1 (v <= gamma_b), the rest to the spare row
+            start = self.row_off[:-1].to(torch.int64) - self.bb
+            dst = start[:, None] + self.kk[None, :]
+            dst = torch.where(self.kk[None, :] < self.gamma.to(torch.int64)[:, None], dst, B * max(G, 1))
+            self.draft_probs.index_copy_(0, dst.reshape(-1), self.probs.reshape(-1, self.cfg.vocab))
+            lsv.lsv_accept(lsv.LSV_ACC_SAMPLE, B, self.cfg.vocab, self.logits, self.row_off, self.max_rows,
+                           self.width, self.tokens, self.draft_probs, self.temperature, self.seed, self.rounds,
+                           self.acc, self.out, self.seq_len, self.status, self.aws.buf, self.aws.nbytes)
+        else:
+            lsv.lsv_accept(lsv.LSV_ACC_GREEDY, B, self.cfg.vocab, self.logits, self.row_off, self.max_rows,
+                           self.width, self.tokens, None, 0.0, 0, 0, self.acc, self.out, self.seq_len, self.status,
+                           self.aws.buf, self.aws.nbytes)
         lsv.lsv_next_roots(B, self.acc, self.out, self.width, self.status, self.roots)
+        self.rounds += 1
 
     def capture(self):
         """Record one round in a graph (run one round eagerly first to warm the launches)."""
+        if self.accept == "sample":
+            raise RuntimeError("sampling rounds take the round index from the host: run them eagerly")
         self.graph = torch.cuda.CUDAGraph()
         with torch.cuda.graph(self.graph):
             self.round()

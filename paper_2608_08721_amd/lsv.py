@@ -19,6 +19,7 @@ LSV_ACCEPT_NOALLOC_BYTES = 512 * 1024
 LSV_ACC_GREEDY, LSV_ACC_SAMPLE = 0, 1
 LSV_SEL_MARGINAL, LSV_SEL_EXHAUSTIVE, LSV_SEL_ALG1 = 0, 1, 2
 LSV_SEL_BONUS = 1
+LSV_SEL_DRAFTED = 2
 
 EXPORTED = (
     "lsv_status_string", "lsv_last_error", "lsv_abi_version", "lsv_packed_model_bytes", "lsv_pack_globals",

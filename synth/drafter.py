@@ -24,7 +24,7 @@ def confidences(seed, B, L, kind="beta"):
 
 
 class PlantedDrafter:
-    def __init__(self, stream, q, seed, vocab, G, device="cuda"):
+    def __init__(self, stream, q, seed, vocab, G, device="cuda", n=8):
         stream = np.asarray(stream, dtype=np.int64)
         q = np.asarray(q, dtype=np.float32)
         B, L = stream.shape
@@ -32,7 +32,8 @@ class PlantedDrafter:
         u = rng.random((B, L))
         wrong = (stream + 1 + rng.integers(0, vocab - 1, size=(B, L))) % vocab  # never the stream token
         pick = np.where(u < q, stream, wrong)
-        self.G, self.L = G, L
+        self.G, self.L, self.n = G, L, n
+        self.drafted = torch.zeros(B, dtype=torch.int64, device=device)  # drafts produced, per sequence
         self.pick = torch.tensor(pick, dtype=torch.int32, device=device)
         self.q = torch.tensor(q, dtype=torch.float32, device=device)
         self.k = torch.arange(1, G + 1, dtype=torch.int64, device=device)
@@ -43,6 +44,17 @@ class PlantedDrafter:
         idx = (seq_len.to(torch.int64)[:, None] + self.k[None, :]).clamp_(max=self.L - 1)
         drafts.copy_(torch.gather(self.pick, 1, idx))
         conf.copy_(torch.gather(self.q, 1, idx))
+
+    def fill_blocks(self, seq_len, have, want, drafts, conf, n=None):
+        """Blocks on demand: drafts and confidences k in [have_b * n, want_b * n) of each
+        sequence (the other entries keep what they hold).  Device ops only."""
+        n = n or self.n
+        idx = (seq_len.to(torch.int64)[:, None] + self.k[None, :]).clamp_(max=self.L - 1)
+        blk = (self.k - 1) // n
+        mask = (blk[None, :] >= have.to(torch.int64)[:, None]) & (blk[None, :] < want.to(torch.int64)[:, None])
+        drafts.copy_(torch.where(mask, torch.gather(self.pick, 1, idx).to(drafts.dtype), drafts))
+        conf.copy_(torch.where(mask, torch.gather(self.q, 1, idx), conf))
+        self.drafted += mask.sum(dim=1, dtype=torch.int64)
 
 
 def plant_block(continuation, conf, seed, vocab):
@@ -56,3 +68,25 @@ def plant_block(continuation, conf, seed, vocab):
     u = rng.random(cont.shape)
     wrong = (cont + 1 + rng.integers(0, vocab - 1, size=cont.shape)) % vocab
     return np.where(u < q, cont, wrong)
+
+
+class SampledDrafter:
+    """A proposal distribution per draft for the sampling setting: q = softmax(scale * z),
+    z standard normal, drawn on the device from a generator seeded per call, and the draft
+    drawn from q; its confidence is q(draft).  Any proposal keeps speculative rejection
+    sampling lossless (the emitted tokens follow the target's distribution); this one is
+    only there to be one."""
+
+    def __init__(self, seed, vocab, scale=3.0, device="cuda"):
+        self.seed, self.vocab, self.scale, self.calls = seed, vocab, scale, 0
+        self.gen = torch.Generator(device=device)
+
+    def __call__(self, seq_len, drafts, conf, probs):
+        self.gen.manual_seed(self.seed * 1000003 + self.calls)
+        self.calls += 1
+        B, G, V = probs.shape
+        z = torch.randn((B, G, V), generator=self.gen, device=probs.device) * self.scale
+        probs.copy_(torch.softmax(z, dim=-1))
+        x = torch.multinomial(probs.reshape(-1, V), 1, generator=self.gen).reshape(B, G)
+        drafts.copy_(x.to(drafts.dtype))
+        conf.copy_(torch.gather(probs, 2, x[:, :, None])[:, :, 0])

@@ -200,3 +200,107 @@ def test_loop_stops_a_sequence_at_max_ctx():
         assert frozen[b] is not None and max_ctx - (gamma + 1) < frozen[b] <= max_ctx, (b, frozen[b])
         assert got[b] == conts[b][:len(got[b])], b
     note(f"  sequences stopped at {frozen} of max_ctx {max_ctx} after emitting {[len(g) for g in got]} tokens")
+
+
+def test_alg1_drafts_blocks_on_demand():
+    """Algorithm 1's budget drives the drafter (blocks of n only when the budget goes
+    negative): each round drafts exactly the blocks the oracle's rule uses over that round's
+    confidences, verifies the oracle's length, and the stream stays the greedy one."""
+    from oracle import selector as S
+    m, G, n = configs.TINY_F32, 16, 4
+    contexts = [40, 75]
+    B = len(contexts)
+    w = gen.model_weights(m, SEED)
+    cfg, dm, kv, cap, conts, roots = _setup(m, w, contexts, G)
+    L = cap
+    stream = np.zeros((B, L), np.int64)
+    for b, C in enumerate(contexts):
+        stream[b, C] = roots[b]
+        stream[b, C + 1:C + 1 + N] = conts[b]
+    q = drafter.confidences(SEED + 1, B, L)
+    dr = drafter.PlantedDrafter(stream, q, SEED, m.vocab, G, n=n)
+    loop = decode.DecodeLoop(cfg, dm, kv, cap, B, G, "alg1", dr, block_n=n, alpha=2.2)
+    assert loop.on_demand
+    loop.reset(contexts, roots)
+    got = [[] for _ in range(B)]
+    rounds = blocks_total = 0
+    while min(len(g) for g in got) < N and rounds < 2 * N:
+        sl = loop.seq_len.cpu().numpy()
+        want = [S.select_alg1([float(q[b, min(sl[b] + k, L - 1)]) for k in range(1, G + 1)], G, 2.2, n)
+                for b in range(B)]
+        before = dr.drafted.clone()
+        loop.round()
+        for b, e in enumerate(loop.emitted()):
+            got[b] += e
+        gam, blk = loop.gamma.cpu().tolist(), loop.blocks.cpu().tolist()
+        assert [(gam[b], blk[b]) for b in range(B)] == want, (rounds, want, gam, blk)
+        assert (dr.drafted - before).cpu().tolist() == [min(bl * n, G) for bl in blk]
+        blocks_total += sum(blk)
+        rounds += 1
+    assert bool((loop.status == 0).all())
+    for b in range(B):
+        assert got[b][:N] == conts[b]
+    note(f"  alg1 with blocks on demand: {rounds} rounds, {blocks_total} blocks of {n} drafted "
+         f"(all up front: {rounds * B * (-(-G // n))}), stream identical to greedy decoding")
+
+
+def test_sampling_round_emits_the_target_distribution():
+    """Sec. 3.1's sampling setting, a whole round on the device: with proposals from an
+    unrelated distribution, the first emitted token of a round follows the target's
+    softmax(logits / T) at the root (chi-square over 64 sequences x 160 rounds); a run of
+    rounds keeps every status OK and commits every emitted token."""
+    from scipy import stats
+    m, G, T = configs.TINY_F32, 4, 0.7
+    B, C = 64, 50
+    w = gen.model_weights(m, SEED)
+    cfg = runtime.model_config(m)
+    dm = runtime.DeviceModel.from_weights(cfg, w)
+    cap = runtime.kv_capacity(C + 40 * (G + 1) + 8)
+    kv = runtime.KVCache(cfg, B, cap)
+    om = OF.Model(m, w)
+    oc = OF.KVCache(m, 1, cap)
+    for l in range(m.n_layers):
+        k, v = gen.synthetic_kv(m, SEED, l, 1, C)
+        kd, vd = runtime.to_device(k[0]), runtime.to_device(v[0])
+        for b in range(B):
+            kv.write(l, b, 0, kd, vd)
+        oc.k[l][0, :, :C] = OF.stored_to_f64(k[0], "f32")
+        oc.v[l][0, :, :C] = OF.stored_to_f64(v[0], "f32")
+    root = int(gen.randint(SEED, 5, 1, m.vocab)[0])
+    lg, _ = OF.verify_block(om, oc, [C], [root], [0, 1])
+    z = lg[0] / T
+    p0 = np.exp(z - z.max())
+    p0 /= p0.sum()
+    dr = drafter.SampledDrafter(SEED, m.vocab)
+    loop = decode.DecodeLoop(cfg, dm, kv, cap, B, G, "static", dr, gamma0=G, accept="sample", temperature=T)
+    with pytest.raises(RuntimeError):
+        loop.capture()
+    counts = np.zeros(m.vocab)
+    trials = 160
+    for t in range(trials):
+        loop.reset([C] * B, [root] * B)
+        loop.seed = 1000 + t
+        loop.round()
+        first = loop.out[:, 0].cpu().numpy()
+        assert bool((loop.status == 0).all())
+        np.add.at(counts, first, 1)
+    n_s = B * trials
+    exp_ = p0 * n_s
+    big = exp_ >= 5
+    obs = np.concatenate([counts[big], [counts[~big].sum()]])
+    ex = np.concatenate([exp_[big], [exp_[~big].sum()]])
+    keep = ex > 0
+    chi = stats.chisquare(obs[keep], ex[keep])
+    note(f"  sampling round at T {T}: first emitted token over {n_s} draws, {int(big.sum())} bins + rest, "
+         f"chi-square p {chi.pvalue:.3f}")
+    assert chi.pvalue > 1e-3
+    # a run of rounds: statuses OK, every emitted token committed
+    loop.reset([C] * B, [root] * B)
+    total = np.zeros(B, np.int64)
+    for r in range(20):
+        loop.seed = 77
+        loop.round()
+        acc = loop.acc.cpu().numpy()
+        assert bool((loop.status == 0).all()) and np.all((acc >= 0) & (acc <= G))
+        total += acc + 1
+    assert np.array_equal(loop.seq_len.cpu().numpy(), C + total)

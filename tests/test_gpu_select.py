@@ -155,3 +155,57 @@ def test_joint_selector_rejects_bad_input():
     cost[1] = np.nan  # below the smallest total: never read
     g, tot, ro, st = gpu_joint(conf, cost, 4, 0)
     assert np.all(st == 0) and tot == 12
+
+
+def test_alg1_blocks_on_demand_parity():
+    """LSV_SEL_DRAFTED: d_aux brings the blocks drafted so far; gamma (0 = more blocks
+    needed) and the blocks out match the oracle bit for bit, and iterating the requests on
+    the device ends on the all-confidences answer."""
+    rng = np.random.default_rng(77)
+    for trial in range(40):
+        B = int(rng.integers(1, 97))
+        G = int(rng.integers(1, 65))
+        conf = random_conf(rng, B, G)
+        d_max = int(rng.integers(1, G + 1))
+        n = int(rng.integers(1, min(G, 16) + 1))
+        alpha = float(rng.choice([1.8, 2.0, 2.2, 0.5, 4.0]))
+        drafted = rng.integers(1, -(-G // n) + 2, size=B).astype(np.int32)
+        poisoned = conf.copy()   # confidences not drafted yet: never read
+        for b in range(B):
+            poisoned[b, min(int(drafted[b]) * n, G):] = np.nan
+        c = torch.tensor(poisoned, device="cuda")
+        g = torch.full((B,), -7, dtype=torch.int32, device="cuda")
+        aux = torch.tensor(drafted, device="cuda")
+        st = torch.full((B,), 99, dtype=torch.int32, device="cuda")
+        lsv.lsv_select_length(S.SEL_ALG1, B, G, c, None, 1, d_max, alpha, n, lsv.LSV_SEL_DRAFTED, g, aux, None, st)
+        torch.cuda.synchronize()
+        assert (st.cpu().numpy() == 0).all()
+        for b in range(B):
+            want = S.select_alg1([float(v) for v in conf[b]], d_max, alpha, n, drafted=int(drafted[b]))
+            assert (int(g[b]), int(aux[b])) == want, (trial, b)
+        # the request loop on the device: first block only, then what each call asks for
+        have = torch.ones(B, dtype=torch.int32, device="cuda")
+        c = torch.tensor(conf, device="cuda")
+        aux.fill_(1)
+        have.fill_(1)
+        for _ in range(-(-d_max // n)):
+            lsv.lsv_select_length(S.SEL_ALG1, B, G, c, None, 1, d_max, alpha, n, lsv.LSV_SEL_DRAFTED, g, aux, None, st)
+            torch.maximum(have, aux, out=have)
+            aux.copy_(have)
+        g_eager, a_eager, _ = gpu_select(S.SEL_ALG1, conf, None, 1, d_max, alpha, n, 0)
+        lsv.lsv_select_length(S.SEL_ALG1, B, G, c, None, 1, d_max, alpha, n, lsv.LSV_SEL_DRAFTED, g, aux, None, st)
+        torch.cuda.synchronize()
+        assert np.array_equal(g.cpu().numpy(), g_eager) and np.array_equal(aux.cpu().numpy(), a_eager)
+    note("  ALG1 with blocks on demand: 40 batches bit-exact, request loops end on the full-G answer")
+
+
+def test_alg1_blocks_on_demand_rejects_bad_input():
+    c = torch.full((2, 8), 0.9, device="cuda")
+    g = torch.zeros(2, dtype=torch.int32, device="cuda")
+    st = torch.zeros(2, dtype=torch.int32, device="cuda")
+    with pytest.raises(lsv.LsvError):   # needs d_aux
+        lsv.lsv_select_length(S.SEL_ALG1, 2, 8, c, None, 1, 8, 2.0, 4, lsv.LSV_SEL_DRAFTED, g, None, None, st)
+    aux = torch.tensor([0, 2], dtype=torch.int32, device="cuda")
+    lsv.lsv_select_length(S.SEL_ALG1, 2, 8, c, None, 1, 8, 2.0, 4, lsv.LSV_SEL_DRAFTED, g, aux, None, st)
+    torch.cuda.synchronize()
+    assert st.cpu().tolist() == [lsv.LSV_ERR_INVALID_ARG, 0] and int(g[0]) == 0

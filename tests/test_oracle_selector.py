@@ -218,3 +218,50 @@ def test_select_dispatch_and_batch():
     assert g[1] == 1 and a == [0, 0]
     g2, _ = S.select_batch(S.SEL_MARGINAL, q, cost, 4, 4, 2.0, 2)
     assert g2 == g
+
+
+def test_alg1_blocks_on_demand_ends_where_the_full_rule_ends():
+    """Algorithm 1 drafts a new block only when the budget of drafted but unused tokens goes
+    negative.  Run with the first block only, then again with the blocks each call asks for,
+    the rule never reads a confidence that was not drafted (q is cut to the drafted blocks)
+    and ends with the length and block count of the rule over all G confidences, after at
+    most ceil(d_max / n) calls."""
+    rng = np.random.default_rng(16)
+    for _ in range(600):
+        G = int(rng.integers(1, 41))
+        q = rand_q(rng, G)
+        d_max = int(rng.integers(1, G + 1))
+        n = int(rng.integers(1, G + 1))
+        alpha = float(rng.choice([1.8, 2.0, 2.2, 0.5, 5.0]))
+        want = S.select_alg1(q, d_max, alpha, n)
+        k, calls = 1, 0
+        while True:
+            calls += 1
+            g, blocks = S.select_alg1(q[:k * n], d_max, alpha, n, drafted=k)
+            if g:
+                break
+            assert blocks > k          # a request is always for more than is drafted
+            k = blocks
+        assert (g, blocks) == want
+        assert calls <= -(-d_max // n)
+
+
+def test_alg1_blocks_on_demand_golden_traces():
+    """With one block drafted, the rule stops at the first length of the golden trace that
+    runs past the block and asks for ceil(d / n) blocks; if the trace never leaves the first
+    block the answer is the golden one."""
+    for c in json.load(open(GOLDEN))["cases"]:
+        exp = c["expect"]
+        if "alg1_trace" not in exp:
+            continue
+        n, d_max = c["n"], c["d_max"]
+        lengths = [t[0] for t in exp["alg1_trace"]]
+        last = exp["alg1_trace"][-1]
+        if last[1] > last[0]:          # ended by reaching d_max: that length is reached too
+            lengths.append(min(last[1], d_max))
+        past = [d for d in lengths if d > n]
+        g, blocks = S.select_alg1(c["q"][:n], d_max, c["alpha"], n, drafted=1)
+        if past:
+            assert (g, blocks) == (0, -(-past[0] // n)), c["name"]
+        else:
+            assert [g, blocks] == exp["alg1"], c["name"]
