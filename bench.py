@@ -73,6 +73,10 @@ def parse():
                    help="no GPU work: turn the csv output of three rocprofv3 runs of this script (kernel trace, "
                         "--pmc FETCH_SIZE, --pmc WRITE_SIZE; each dir also holds that run's bench.json) into the "
                         "gate/up profile summary of the run's workload")
+    p.add_argument("--summarize-counters", nargs="+", metavar="DIR",
+                   help="no GPU work: per-kernel counter summary (markdown) of --counters-only runs: the first "
+                        "DIR holds a kernel-trace run of the same workload (durations), the others one --pmc "
+                        "run each (bench.json + counter csv)")
     p.add_argument("--summarize-mfma", nargs=2, metavar=("TRACE_DIR", "PMC_DIR"),
                    help="no GPU work: matrix-core summary of the batched workload's uniform-gamma-max sweep "
                         "step from a kernel-trace run and a --pmc SQ_INSTS_MFMA SQ_VALU_MFMA_BUSY_CYCLES run "
@@ -211,12 +215,13 @@ def summarize(trace_dir, fetch_dir, write_dir):
 
     out = []
     w = out.append
-    base = f"python3 bench.py --workload {wl.name} --secondary none --no-cpu-baseline"
-    cmd_t = (f"rocprofv3 --kernel-trace --stats --output-format csv -d gpurun_out/pf/trace -o t -- {base} "
+    base = f"python3 bench.py --workload {wl.name} --secondary none --no-cpu-baseline --rounds 0"
+    dirs = [os.path.normpath(d) for d in (trace_dir, fetch_dir, write_dir)]
+    cmd_t = (f"rocprofv3 --kernel-trace --stats --output-format csv -d {dirs[0]} -o t -- {base} "
              f"--steps {bt['steps']} --warmup {bt['warmup']}")
     g_sel = bt["config"]["gamma"]
     g_sel = g_sel[0] if isinstance(g_sel, list) else g_sel
-    cmd_c = ("rocprofv3 --pmc {c} --output-format csv -d gpurun_out/pf/{d} -o {o} -- " +
+    cmd_c = ("rocprofv3 --pmc {c} --output-format csv -d {d} -o {o} -- " +
              f"python3 bench.py --workload {wl.name} --counters-only {g_sel} --roofline-steps 2")
     w(f"# gate/up GEMM + SwiGLU: {wl.name} ({m.name} shape, batch {wl.batch}, context {bt['config']['context']}, "
       f"{rows} rows)")
@@ -226,9 +231,9 @@ def summarize(trace_dir, fetch_dir, write_dir):
     w("")
     w("```")
     w(cmd_t)
-    w(cmd_c.format(c="FETCH_SIZE", d="fetch", o="f"))
-    w(cmd_c.format(c="WRITE_SIZE", d="write", o="w"))
-    w("python3 bench.py --summarize gpurun_out/pf/trace gpurun_out/pf/fetch gpurun_out/pf/write")
+    w(cmd_c.format(c="FETCH_SIZE", d=dirs[1], o="f"))
+    w(cmd_c.format(c="WRITE_SIZE", d=dirs[2], o="w"))
+    w(f"python3 bench.py --summarize {' '.join(dirs)}")
     w("```")
     w("")
     w(f"source_hash: {kernel_source_hash()}")
@@ -287,6 +292,98 @@ def summarize(trace_dir, fetch_dir, write_dir):
 
 
 MFMA_FLOPS_PER_INST = 16 * 16 * 32 * 2  # v_mfma_f32_16x16x32_bf16, the only MFMA of these kernels
+
+
+def summarize_counters(trace_dir, pmc_dirs):
+    """Per-kernel counter means of --counters-only runs (one --pmc run per directory), next to
+    the kernel durations of a kernel-trace run, as markdown.  FETCH_SIZE and WRITE_SIZE are in
+    KiB per dispatch as rocprofv3 reports them; the calibration copy at the end of each run
+    gives the factor that turns them into bytes (a plain copy of CALIB_BYTES reads and writes
+    that many bytes)."""
+    import csv
+    import glob
+    import re
+
+    def short(name):
+        return re.sub(r"\(.*$", "", re.sub(r"^void ", "", name)).replace("lsv::", "").replace("unsigned short", "bf16")
+
+    f = glob.glob(os.path.join(trace_dir, "**", "*kernel_trace.csv"), recursive=True)
+    dur = {}
+    for r in (csv.DictReader(open(f[0])) if f else []):
+        dur.setdefault(short(r["Kernel_Name"]), []).append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
+    per = {}  # kernel -> counter -> [per-dispatch values]
+    scale = {}
+    runs = []
+    for d in pmc_dirs:
+        f = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)
+        assert len(f) == 1, (d, f)
+        disp = {}
+        for r in csv.DictReader(open(f[0])):
+            e = disp.setdefault(int(r["Dispatch_Id"]), {"name": short(r["Kernel_Name"]), "grid": int(r["Grid_Size"])})
+            e[r["Counter_Name"]] = e.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+        cmds = json.loads(open(os.path.join(d, "bench.json")).read().strip().splitlines()[-1])
+        names = sorted({k for e in disp.values() for k in e if k not in ("name", "grid")})
+        runs.append((d, names, cmds["config"]["workload"]))
+        for i in sorted(disp):
+            e = disp[i]
+            if "copyBuffer" in e["name"]:
+                if e["grid"] >= 131072:  # the calibration copy (the last one): bytes per counter unit
+                    for c in ("FETCH_SIZE", "WRITE_SIZE"):
+                        if e.get(c, 0.0) > 0:
+                            scale[c] = CALIB_BYTES / e[c]
+                continue
+            for c in names:
+                if c in e:
+                    per.setdefault(e["name"], {}).setdefault(c, []).append(e[c])
+    wl = runs[0][2] if runs else "?"
+    out = [f"# Per-kernel counters: {wl}\n",
+           "Counter runs (`--counters-only`: eager verify steps at one uniform gamma, the cache holding zeros, which "
+           "changes no kernel's traffic or instruction mix), one `--pmc` set per run; values are means per "
+           "dispatch. Kernels are listed by their total time in the kernel-trace run; the timed step's per-kernel "
+           "durations are in the gate/up summary of the same workload.\n"]
+    for d, names, _ in runs:
+        out.append(f"- `{os.path.basename(os.path.normpath(d))}`: {' '.join(names)}")
+    out.append("")
+    for c in ("FETCH_SIZE", "WRITE_SIZE"):
+        if c in scale:
+            out.append(f"- {c} scale from the calibration copy: {scale[c]:.3f} bytes per counter unit")
+    out.append("")
+    # the verify step's kernels only (not the packing, the workspace fills or the calibration copy)
+    per = {k: v for k, v in per.items() if re.match(r"(gemm_|attn_|rmsnorm_|embed_|tree_|commit_)", k)}
+    cols = sorted({c for k in per.values() for c in k})
+    hdr = "| kernel | dispatches | " + " | ".join(cols) + " |"
+    out.append(hdr)
+    out.append("|---|---:|" + "---:|" * len(cols))
+    order = sorted(per, key=lambda k: -sum(dur.get(k, [0.0])))
+    for k in order:
+        n = max(len(v) for v in per[k].values())
+        row = [f"`{k[:60]}`", str(n)]
+        for c in cols:
+            v = per[k].get(c)
+            if not v:
+                row.append("-")
+                continue
+            mean = sum(v) / len(v)
+            if c in scale:
+                row.append(f"{mean * scale[c] / 1e6:.2f} MB")
+            else:
+                row.append(f"{mean:.4g}")
+        out.append("| " + " | ".join(row) + " |")
+    out.append("")
+    # derived ratios where the counters are there
+    for k in order:
+        c = {n: sum(v) / len(v) for n, v in per[k].items()}
+        notes = []
+        if c.get("SQ_INSTS_LDS"):
+            if "SQ_LDS_BANK_CONFLICT" in c:
+                notes.append(f"LDS bank-conflict cycles per LDS instruction {c['SQ_LDS_BANK_CONFLICT'] / c['SQ_INSTS_LDS']:.3f}")
+        if c.get("SQ_WAVE_CYCLES") and "SQ_WAIT_INST_ANY" in c:
+            notes.append(f"waiting on a memory/LDS counter {c['SQ_WAIT_INST_ANY'] / c['SQ_WAVE_CYCLES']:.2f} of wave cycles")
+        if c.get("SQ_BUSY_CYCLES") and "SQ_WAVE_CYCLES" in c:
+            notes.append(f"mean resident waves per SQ-busy cycle {c['SQ_WAVE_CYCLES'] / c['SQ_BUSY_CYCLES']:.1f}")
+        if notes:
+            out.append(f"- `{k[:60]}`: " + "; ".join(notes))
+    return "\n".join(out) + "\n"
 
 
 def summarize_mfma(trace_dir, pmc_dir):
@@ -1078,6 +1175,9 @@ def main():
     args = parse()
     if args.summarize:
         sys.stdout.write(summarize(*args.summarize))
+        return
+    if args.summarize_counters:
+        sys.stdout.write(summarize_counters(args.summarize_counters[0], args.summarize_counters[1:]))
         return
     if args.summarize_mfma:
         sys.stdout.write(summarize_mfma(*args.summarize_mfma))
