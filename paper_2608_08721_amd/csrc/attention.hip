@@ -66,7 +66,9 @@ __global__ void __launch_bounds__(64 * NW) attn_split_bf16_kernel(AttnArgs a) {
   constexpr int NG = NW / 4;               // wave groups: each loads one chunk per step
   constexpr int P8 = HD / 8;               // 16-byte pieces per K row
   constexpr int NP = kCh * HD / 8 / 256;   // pieces of K (and of V^T) per thread of a group and chunk
-  constexpr int KPITCH = HD + 8, VPITCH = kCh + 8;  // padded LDS rows: conflict-free fragment reads
+  // LDS rows padded by 32 bytes: on gfx950 a 16-byte pad still left 2.5 bank-conflict cycles per
+  // LDS instruction (SQ_LDS_BANK_CONFLICT); 32 bytes leaves none
+  constexpr int KPITCH = HD + 16, VPITCH = kCh + 16;
   static_assert(NG >= 1 && NG * 4 == NW && NP >= 1 && NP * 256 * 8 == kCh * HD, "four-wave groups");
   __shared__ __align__(16) bf16_t Ks[NG][kCh * KPITCH];  // one chunk buffer per group
   __shared__ __align__(16) bf16_t Vt[NG][HD * VPITCH];
