@@ -448,6 +448,18 @@ template <int KIND, int MT_MAX> struct GemmShape {
   static constexpr int U = MT_MAX <= 2 ? C::U : 4, NS = MT_MAX <= 2 ? C::NS : 2;
 };
 
+// Two or more activation tiles: a product that streams one or two fragment rows per wave takes
+// twice as many when that still leaves a stream per compute unit.  Each activation tile adds one
+// load per k-step to every wave, and per-wave issue, not DRAM, bounds these streams, so this halves
+// the activation loads per weight byte (lab, Llama-3-70B, 20 / 52 rows: down 102 -> 79 / 146 ->
+// 116 us, O 31 -> 26 / 44 -> 36 us); with fewer streams than compute units it loses (Llama-3-8B
+// at 17 rows: +0.5 ms per step), and four rows per wave lost everywhere.
+constexpr int kComputeUnits = 256;
+template <int KIND> struct MultiTile {
+  static constexpr int TPW = GemmCfg<KIND>::TPW <= 2 ? 2 * GemmCfg<KIND>::TPW : GemmCfg<KIND>::TPW;
+  LSV_DEV static bool use(int mt, int Nt) { return mt >= 2 && TPW != GemmCfg<KIND>::TPW && (Nt + TPW - 1) / TPW >= kComputeUnits; }
+};
+
 // Rows come in chunks of 64 (4 activation tiles); a chunk's workgroups read the same
 // weights, so the grid puts the chunks of one column tile on the same XCD (workgroup
 // ids congruent mod 8 share one) where the repeated reads hit its L2.  The host bound
@@ -472,6 +484,19 @@ __global__ void __launch_bounds__(64 * GemmCfg<KIND>::KS) gemm_kernel(GemmArgs a
   // 64-row bound, 41 -> 25 us); three or four take the shallower one
   using C = GemmCfg<KIND>;
   const int ks = threadIdx.x >> 6;
+  if constexpr (std::is_same<T, bf16_t>::value && S::KS == 1 && MT_MAX >= 2) {
+    using X = MultiTile<KIND>;
+    if (X::use(mt, a.Nt)) {
+      if (tile >= (a.Nt + X::TPW - 1) / X::TPW) return;
+      if (mt == 2 || MT_MAX == 2)
+        gemm_body<T, 2, X::TPW, 1, C::U, C::NS, S::EPI, MT_MAX>(a, M_end, tile, m0, nullptr, 0);
+      else if (mt == 3 || MT_MAX == 3)
+        gemm_body<T, (MT_MAX >= 3 ? 3 : 2), X::TPW, 1, S::U, S::NS, S::EPI, MT_MAX>(a, M_end, tile, m0, nullptr, 0);
+      else
+        gemm_body<T, MT_MAX, X::TPW, 1, S::U, S::NS, S::EPI, MT_MAX>(a, M_end, tile, m0, nullptr, 0);
+      return;
+    }
+  }
   if (mt <= 1 || MT_MAX == 1)
     gemm_body<T, 1, S::TPW, S::KS, C::U, C::NS, S::EPI, MT_MAX>(a, M_end, tile, m0, red, ks);
   else if (mt == 2 || MT_MAX == 2)
@@ -678,6 +703,17 @@ __global__ void __launch_bounds__(256) gemm_fused_kernel(GemmArgs a) {
     using C = GemmCfg<KIND>;
     using S = GemmShape<KIND, 4>;
     static_assert(C::KS == 1, "one wave per column tile");
+    using X = MultiTile<KIND>;
+    if (X::use(mt, a.Nt)) {  // two or more activation tiles on a wide product
+      if (vt >= (a.Nt + X::TPW - 1) / X::TPW) return;
+      if (mt == 2)
+        gemm_body<bf16_t, 2, X::TPW, 1, C::U, C::NS, S::EPI, 4>(a, M, vt, 0, nullptr, 0);
+      else if (mt == 3)
+        gemm_body<bf16_t, 3, X::TPW, 1, S::U, S::NS, S::EPI, 4>(a, M, vt, 0, nullptr, 0);
+      else
+        gemm_body<bf16_t, 4, X::TPW, 1, S::U, S::NS, S::EPI, 4>(a, M, vt, 0, nullptr, 0);
+      return;
+    }
     if (vt >= (a.Nt + S::TPW - 1) / S::TPW) return;
     if (mt == 1)
       gemm_body<bf16_t, 1, S::TPW, 1, C::U, C::NS, S::EPI, 4>(a, M, vt, 0, nullptr, 0);
