@@ -336,7 +336,20 @@ def summarize_counters(trace_dir, pmc_dirs):
                 if c in e:
                     per.setdefault(e["name"], {}).setdefault(c, []).append(e[c])
     wl = runs[0][2] if runs else "?"
+    from synth import configs
+    B = configs.WORKLOADS[wl].batch if wl in configs.WORKLOADS else 1
+    cmds = [f"rocprofv3 --kernel-trace --stats --output-format csv -d {os.path.normpath(trace_dir)} -o t -- python3 "
+            f"bench.py --workload {wl} --secondary none --no-cpu-baseline --rounds 0 --steps 50 --warmup 5"]
+    for d, names, _ in runs:
+        bj = json.loads(open(os.path.join(d, "bench.json")).read().strip().splitlines()[-1])
+        g = bj["roofline"]["rows"] // B - 1
+        dn = os.path.normpath(d)
+        cmds.append(f"rocprofv3 --pmc {' '.join(names)} --output-format csv -d {dn} -o {os.path.basename(dn)[0]} -- "
+                    f"python3 bench.py --workload {wl} --counters-only {g} --roofline-steps 2")
+    cmds.append("python3 bench.py --summarize-counters " + " ".join(os.path.normpath(x) for x in [trace_dir] + list(pmc_dirs)))
     out = [f"# Per-kernel counters: {wl}\n",
+           "Commands (repository root, after `cd /tmp && export TMPDIR=/tmp` for the profiler's own files; each run's "
+           "stdout saved as bench.json in its output directory):\n", "```", *cmds, "```\n",
            "Counter runs (`--counters-only`: eager verify steps at one uniform gamma, the cache holding zeros, which "
            "changes no kernel's traffic or instruction mix), one `--pmc` set per run; values are means per "
            "dispatch. Kernels are listed by their total time in the kernel-trace run; the timed step's per-kernel "
@@ -376,11 +389,11 @@ def summarize_counters(trace_dir, pmc_dirs):
         notes = []
         if c.get("SQ_INSTS_LDS"):
             if "SQ_LDS_BANK_CONFLICT" in c:
-                notes.append(f"LDS bank-conflict cycles per LDS instruction {c['SQ_LDS_BANK_CONFLICT'] / c['SQ_INSTS_LDS']:.3f}")
+                notes.append(f"SQ_LDS_BANK_CONFLICT / SQ_INSTS_LDS {c['SQ_LDS_BANK_CONFLICT'] / c['SQ_INSTS_LDS']:.3f}")
         if c.get("SQ_WAVE_CYCLES") and "SQ_WAIT_INST_ANY" in c:
-            notes.append(f"waiting on a memory/LDS counter {c['SQ_WAIT_INST_ANY'] / c['SQ_WAVE_CYCLES']:.2f} of wave cycles")
+            notes.append(f"SQ_WAIT_INST_ANY / SQ_WAVE_CYCLES {c['SQ_WAIT_INST_ANY'] / c['SQ_WAVE_CYCLES']:.2f}")
         if c.get("SQ_BUSY_CYCLES") and "SQ_WAVE_CYCLES" in c:
-            notes.append(f"mean resident waves per SQ-busy cycle {c['SQ_WAVE_CYCLES'] / c['SQ_BUSY_CYCLES']:.1f}")
+            notes.append(f"SQ_WAVE_CYCLES / SQ_BUSY_CYCLES {c['SQ_WAVE_CYCLES'] / c['SQ_BUSY_CYCLES']:.1f}")
         if notes:
             out.append(f"- `{k[:60]}`: " + "; ".join(notes))
     return "\n".join(out) + "\n"
@@ -471,17 +484,18 @@ def summarize_mfma(trace_dir, pmc_dir):
 
     out = []
     w = out.append
-    cmd = ("python3 bench.py --workload {w} --steps 2 --warmup 1 --sweep-reps 1 --roofline-steps 1 "
-           "--no-cpu-baseline").format(w=wl.name)
+    cmd = ("python3 bench.py --workload {w} --secondary none --rounds 0 --steps 2 --warmup 1 --sweep-reps 1 "
+           "--roofline-steps 1 --no-cpu-baseline").format(w=wl.name)
+    td, pd = os.path.normpath(trace_dir), os.path.normpath(pmc_dir)
     w(f"# Batched GEMMs and attention on the matrix cores: {wl.name}, uniform gamma {G} ({rows} rows)")
     w("")
     w("Commands (repository root, after `cd /tmp && export TMPDIR=/tmp`; each run's stdout saved as bench.json in")
     w("its output directory):")
     w("")
     w("```")
-    w(f"rocprofv3 --kernel-trace --output-format csv -d gpurun_out/mf/trace -o t -- {cmd}")
-    w(f"rocprofv3 --pmc SQ_INSTS_MFMA SQ_VALU_MFMA_BUSY_CYCLES --output-format csv -d gpurun_out/mf/pmc -o c -- {cmd}")
-    w("python3 bench.py --summarize-mfma gpurun_out/mf/trace gpurun_out/mf/pmc")
+    w(f"rocprofv3 --kernel-trace --output-format csv -d {td} -o t -- {cmd}")
+    w(f"rocprofv3 --pmc SQ_INSTS_MFMA SQ_VALU_MFMA_BUSY_CYCLES --output-format csv -d {pd} -o c -- {cmd}")
+    w(f"python3 bench.py --summarize-mfma {td} {pd}")
     w("```")
     w("")
     w(f"Calls at gamma {G}: {len(picked)} (the sweep's graph body, run 1 + 3 + 1 times). Durations are kernel-trace")
