@@ -118,17 +118,20 @@ int lsv_pack_layer(const lsv_model_config* cfg, int32_t layer,
 
 /* ---------------------------------------------------------------- KV cache */
 /* One device buffer in the model dtype.  For layer l the K block precedes the V
- * block; each holds batch x n_kv_heads slabs of capacity x head_dim elements:
- *   slab(l, kv, b, h) = (((l * 2 + kv) * batch + b) * n_kv_heads + h) * capacity * head_dim
- * with kv = 0 for K and 1 for V.
- *   K (after the rotary embedding) is row-major [capacity][head_dim]:
- *     K(l, b, h, pos, i) at slab(l, 0, b, h) + pos * head_dim + i
- *   V is transposed, [head_dim][capacity], with positions permuted inside each
- *   aligned block of 32 so that the keys one matrix-core lane consumes are adjacent:
- *     V(l, b, h, pos, i) at slab(l, 1, b, h) + i * capacity + LSV_V_COLUMN(pos)
- * Sequence b owns `capacity` positions per slab; d_seq_len[b] of them are valid.
- * capacity must be a positive multiple of LSV_KV_ALIGN (lsv_kv_cache_bytes returns 0
- * and lsv_verify_block LSV_ERR_INVALID_ARG otherwise). */
+ * block; each holds batch x capacity / 64 blocks of 64 positions, and a block holds
+ * the n_kv_heads heads side by side (the same layout as a page of the paged cache
+ * below, the blocks of sequence b being its pages in order):
+ *   blk(l, kv, b, p, h) = ((((l * 2 + kv) * batch + b) * (capacity / 64) + p) * n_kv_heads + h)
+ *                         * 64 * head_dim
+ * with kv = 0 for K and 1 for V, p = pos / 64 and j = pos % 64.
+ *   K (after the rotary embedding) is row-major [64][head_dim] per block and head:
+ *     K(l, b, h, pos, i) at blk(l, 0, b, p, h) + j * head_dim + i
+ *   V is transposed, [head_dim][64] per block and head, with positions permuted inside
+ *   each aligned run of 32 so that the keys one matrix-core lane consumes are adjacent:
+ *     V(l, b, h, pos, i) at blk(l, 1, b, p, h) + i * 64 + LSV_V_COLUMN(j)
+ * Sequence b owns `capacity` positions; d_seq_len[b] of them are valid.  capacity must
+ * be a positive multiple of LSV_KV_ALIGN (lsv_kv_cache_bytes returns 0 and
+ * lsv_verify_block LSV_ERR_INVALID_ARG otherwise). */
 enum { LSV_KV_ALIGN = 64, LSV_KV_PAGE = 64 };
 #define LSV_V_COLUMN(pos) (((pos) & ~31) | (((pos) & 12) << 1) | (((pos) & 16) >> 2) | ((pos) & 3))
 size_t lsv_kv_cache_bytes(const lsv_model_config* cfg, int32_t batch, int32_t capacity);
@@ -141,7 +144,7 @@ size_t lsv_kv_cache_bytes(const lsv_model_config* cfg, int32_t batch, int32_t ca
  *   K(l, page, h, j, i) at pool(l, 0) + ((page * n_kv_heads + h) * LSV_KV_PAGE + j) * head_dim + i
  *   V(l, page, h, j, i) at pool(l, 1) + ((page * n_kv_heads + h) * head_dim + i) * LSV_KV_PAGE
  *                                     + LSV_V_COLUMN(j)
- * i.e. a page is laid out like a 64-position slab.  Position pos of sequence b lives in page
+ * i.e. a page is laid out like a block of the slab cache above.  Position pos of sequence b lives in page
  * d_page_table[b * max_pages + pos / 64] at j = pos % 64; a table entry outside
  * [0, n_pages) reads as zeros and is never written.  The caller owns the pool and the table
  * (any page order; pages need not be contiguous).  A layer's K pool must stay under 2 GiB
@@ -172,9 +175,10 @@ int lsv_workspace_clear(void* d_workspace, size_t workspace_bytes, void* stream)
  * is a prefill; long prompts may be fed in chunks.
  *
  *   cfg, d_packed      model and its packed weights
- *   d_kv, capacity     KV cache (layout above) with `capacity` positions per slab,
- *                      capacity % LSV_KV_ALIGN == 0 and a slab under 2 GiB
- *                      (capacity * head_dim * element size < 2^31)
+ *   d_kv, capacity     KV cache (layout above) with `capacity` positions per sequence,
+ *                      capacity % LSV_KV_ALIGN == 0 and a sequence's share of a layer's
+ *                      K block under 2 GiB (n_kv_heads * capacity * head_dim * element
+ *                      size < 2^31)
  *   batch              number of sequences (1..LSV_MAX_BATCH)
  *   d_seq_len          [batch] int32, cached positions before this block
  *   d_tokens           [rows] int32 token ids

@@ -3,9 +3,9 @@
 // bf16 path (matrix cores), two kernels:
 //  * split kernel: one workgroup of four or eight waves per (context split, kv head,
 //    sequence).  A split is a run of 64-key chunks.  Each chunk's K rows and transposed V
-//    rows go HBM -> registers -> LDS with 16-byte accesses; the first chunk's loads are
-//    issued before any device metadata is read, and each next chunk's loads are in flight
-//    while the current one is consumed.  A wave owns one tile of 16 query vectors (block
+//    rows (a contiguous [64][hd] and [hd][64] block per chunk, next to the other kv heads'
+//    blocks) go HBM -> registers -> LDS with 16-byte accesses; the first chunk's loads are issued before any device metadata is read, and
+//    each next chunk's loads are in flight while the current one is consumed.  A wave owns one tile of 16 query vectors (block
 //    rows x query heads of this kv head) per pass over the split -- eight waves cover up to
 //    32 rows of a 4-query-head group in one pass -- and keeps a running softmax:
 //    S^T = K Q^T and O^T = V^T P^T on v_mfma_f32_16x16x32_bf16.  The probabilities stay in
@@ -79,41 +79,42 @@ __global__ void __launch_bounds__(64 * NW) attn_split_bf16_kernel(AttnArgs a) {
   const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
   const int g4 = lane >> 4, l16 = lane & 15;
   const int grp = wave >> 2, gtid = tid & 255;
-  // Slab mode: the grid covers the chunks of ctx_limit <= capacity and capacity is a multiple
-  // of the chunk, so every chunk below capacity / kCh lies inside the slab.  Paged mode: a
-  // chunk is a page; chunks below max_pages have a page-table entry.
+  // A chunk is one 64-position block of the cache.  Slab mode: the grid covers the chunks of
+  // ctx_limit <= capacity and capacity is a multiple of the chunk, so every chunk below
+  // capacity / kCh is one of the sequence's blocks.  Paged mode: a chunk is a page; chunks
+  // below max_pages have a page-table entry.
   const bool paged = a.kv.pages != nullptr;
   const int c0 = s * a.chunks_per_split, cap_chunks = paged ? a.kv.max_pages : a.capacity / kCh;
 
   // a step covers chunks c .. c+NG-1, group g loading chunk c+g into buffer g; the next
   // step's chunks are in flight in registers while the current ones are used. The loads go
-  // through buffer descriptors -- over this (sequence, kv head)'s slab, or over the layer's
-  // page pool -- with one 32-bit lane offset per operand and the chunk and piece offsets in
-  // scalar registers; reads past the descriptor return zero (a page number outside the pool
-  // points there).
+  // through buffer descriptors -- over this sequence's blocks, or over the layer's page pool
+  // -- with one 32-bit lane offset per operand and the chunk and piece offsets in scalar
+  // registers; reads past the descriptor return zero (a page number outside the pool points
+  // there).
   const GLOBAL bf16_t* kb = GL((const bf16_t*)a.k);
   const GLOBAL bf16_t* vb = GL((const bf16_t*)a.v);
-  int span_bytes, vstride;
+  // V^T comes in blocks of one chunk, [hd][64], in both modes: the rows of a chunk's V^T are kCh
+  // elements apart
+  constexpr int vstride = kCh;
+  int span_bytes;
   if (paged) {
     span_bytes = a.kv.n_pages * a.nkv * kCh * HD * (int)sizeof(bf16_t);  // < 2^31, checked on the host
-    vstride = kCh;
   } else {
-    const size_t slab = ((size_t)b * a.nkv + kvh) * (size_t)a.capacity * HD;
-    kb += slab;
-    vb += slab;
-    span_bytes = a.capacity * HD * (int)sizeof(bf16_t);
-    vstride = a.capacity;
+    const size_t seq = (size_t)b * a.nkv * a.capacity * HD;  // this sequence's blocks
+    kb += seq;
+    vb += seq;
+    span_bytes = a.nkv * a.capacity * HD * (int)sizeof(bf16_t);  // < 2^31, checked on the host
   }
   const __amdgpu_buffer_rsrc_t krs = __builtin_amdgcn_make_buffer_rsrc((void*)kb, 0, span_bytes, 0x00020000);
   const __amdgpu_buffer_rsrc_t vrs = __builtin_amdgcn_make_buffer_rsrc((void*)vb, 0, span_bytes, 0x00020000);
   const int koff = ((gtid / P8) * HD + (gtid % P8) * 8) * (int)sizeof(bf16_t);
   const int voff = ((gtid >> 3) * vstride + (gtid & 7) * 8) * (int)sizeof(bf16_t);
-  // element offset of chunk c's first K row (its V^T columns start at the same offset /
-  // HD * ... : a slab chunk's V^T block starts at column c * kCh, a page's at its base)
+  // element offset of chunk c's K rows and of its V^T block (the same offset: a block starts a
+  // [64][hd] K block and a [hd][64] V^T block for each kv head)
   auto chunk_base = [&](int c, int& kbase, int& vbase) {
     if (!paged) {
-      kbase = c * kCh * HD;
-      vbase = c * kCh;
+      kbase = vbase = (c * a.nkv + kvh) * kCh * HD;
       return;
     }
     int page = GL(a.kv.pages)[(size_t)b * a.kv.max_pages + c];

@@ -202,8 +202,8 @@ LSV_DEV void qkv_store4(const GemmArgs& a, int m, int n0, const f32x4_t v, int b
       gd[i0 + 1 + a.hd / 2] = from_f32<T>(out[3]);
     }
   } else {
-    // V rows are stored transposed: [head_dim][capacity] per slab ([head_dim][64] per page),
-    // column v_column(pos)
+    // V rows are stored transposed: [head_dim][64] per 64-position block and kv head, column
+    // v_column(pos % 64)
     const int local = n0 - qrows - krows;
     const int head = local / a.hd, d0 = local % a.hd;
     size_t ko, vo;

@@ -67,7 +67,7 @@ const char* lsv_status_string(int s) {
 }
 
 const char* lsv_last_error(void) { return g_err; }
-int lsv_abi_version(void) { return 2; }
+int lsv_abi_version(void) { return 3; }
 
 size_t lsv_packed_model_bytes(const lsv_model_config* cfg) {
   if (check_config(cfg) != LSV_OK) return 0;
@@ -140,15 +140,16 @@ int lsv_workspace_clear(void* d_workspace, size_t bytes, void* stream) {
 }
 
 namespace {
-// Host checks of a cache description: a slab cache (pages NULL: capacity positions per slab) or a
+// Host checks of a cache description: a slab cache (pages NULL: capacity positions per sequence) or a
 // page pool (n_pages pages of LSV_KV_PAGE positions, a page table of max_pages entries per sequence).
 int check_kv(const lsv::Shape& s, const lsv::KvLayout& kvl) {
   if (!kvl.pages) {
     if (kvl.capacity < 1 || kvl.capacity % LSV_KV_ALIGN)
       return fail(LSV_ERR_INVALID_ARG, "capacity %d is not a positive multiple of %d", kvl.capacity, (int)LSV_KV_ALIGN);
-    if ((size_t)kvl.capacity * s.hd * s.es >= ((size_t)1 << 31))  // slab offsets are 32-bit in the kernels
-      return fail(LSV_ERR_INVALID_ARG, "capacity %d: a KV slab of %d x %d elements reaches 2 GiB", kvl.capacity,
-                  kvl.capacity, s.hd);
+    // offsets inside a sequence's blocks are 32-bit in the kernels
+    if ((size_t)s.nkv * kvl.capacity * s.hd * s.es >= ((size_t)1 << 31))
+      return fail(LSV_ERR_INVALID_ARG, "capacity %d: a sequence's KV block of %d x %d x %d elements reaches 2 GiB",
+                  kvl.capacity, s.nkv, kvl.capacity, s.hd);
     return LSV_OK;
   }
   if (kvl.n_pages < 1 || kvl.max_pages < 1 || kvl.max_pages > (1 << 20))

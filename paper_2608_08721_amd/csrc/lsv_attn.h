@@ -13,15 +13,18 @@ constexpr int kAttnChunk = 64;  // keys per LDS chunk in the bf16 split-context 
 __host__ __device__ inline int v_column(int p) { return LSV_V_COLUMN(p); }
 
 // Element offsets of K(b, h, pos, 0) and V(b, h, pos, 0) within the layer's K block / V block
-// (slab mode: [batch][nkv] slabs; paged: the layer's pool) and the distance between V's head
-// dimensions; false when the position has no valid page.
+// and the distance between V's head dimensions; false when the position has no valid page.
+// Both modes store 64-position blocks with the kv heads of a block side by side ([nkv][64][hd]
+// for K, [nkv][hd][64] for V^T): slab mode gives sequence b the blocks b * capacity / 64 ..
+// in order (as if its page table were the identity), paged mode takes them from the page table.
+// The attention's workgroups for the kv heads of one block then read neighbouring memory.
 LSV_DEV bool kv_locate(const KvLayout& L, int nkv, int hd, int b, int h, int pos, size_t& k_off, size_t& v_off,
                        int& v_stride) {
   if (!L.pages) {
-    const size_t slab = ((size_t)b * nkv + h) * (size_t)L.capacity * hd;
-    k_off = slab + (size_t)pos * hd;
-    v_off = slab + v_column(pos);
-    v_stride = L.capacity;
+    const size_t blk = (((size_t)b * (L.capacity / kAttnChunk) + pos / kAttnChunk) * nkv + h) * kAttnChunk * hd;
+    k_off = blk + (size_t)(pos % kAttnChunk) * hd;
+    v_off = blk + v_column(pos % kAttnChunk);
+    v_stride = kAttnChunk;
     return true;
   }
   const int blk = pos / kAttnChunk;
@@ -42,9 +45,9 @@ __host__ __device__ inline size_t kv_layer_block(const KvLayout& L, int batch, i
 
 struct AttnArgs {
   const void* q;  // [M][nq][hd] storage type
-  const void* k;  // this layer's K block: [batch][nkv][capacity][hd] (paged: [n_pages][nkv][64][hd])
-  const void* v;  // this layer's V block: [batch][nkv][hd][capacity], columns by v_column()
-                  // (paged: [n_pages][nkv][hd][64])
+  const void* k;  // this layer's K block: [batch][capacity / 64][nkv][64][hd] (paged: [n_pages][nkv][64][hd])
+  const void* v;  // this layer's V block: [batch][capacity / 64][nkv][hd][64], columns by
+                  // v_column() (paged: [n_pages][nkv][hd][64])
   KvLayout kv;
   int capacity, ctx_limit, batch, nq, nkv, M_max;
   const int32_t* row_offsets;

@@ -102,10 +102,10 @@ int launch_pack(const Shape& s, PackKind kind, const PackedMat& pm, const void* 
 // A norm gain [d] in the storage type -> fp32 at dst.
 int launch_gain(const Shape& s, const void* src, void* dst, hipStream_t stream);
 
-// Where a layer's cache entries live.  Slab mode (pages == NULL): one slab of `capacity`
-// positions per (sequence, kv head).  Paged mode: a pool of n_pages pages of LSV_KV_PAGE
-// positions per layer; sequence b's positions p .. p + 63 (p a multiple of 64) are in page
-// pages[b * max_pages + p / 64], laid out inside the page as in a 64-position slab.
+// Where a layer's cache entries live.  Slab mode (pages == NULL): `capacity` positions per
+// sequence, in capacity / 64 consecutive blocks laid out like pages.  Paged mode: a pool of
+// n_pages pages of LSV_KV_PAGE positions per layer; sequence b's positions p .. p + 63 (p a
+// multiple of 64) are in page pages[b * max_pages + p / 64].
 struct KvLayout {
   int capacity;
   const int32_t* pages;

@@ -72,7 +72,8 @@ def v_column(pos):
 
 
 class KVCache:
-    """The library's KV cache: K row-major per slab, V transposed with permuted columns."""
+    """The library's KV cache (lsv.h): per layer and K|V, each sequence's 64-position blocks in
+    order, the kv heads of a block side by side; K row-major, V transposed with permuted columns."""
 
     def __init__(self, cfg, batch, capacity, device="cuda"):
         self.cfg, self.batch, self.capacity = cfg, batch, capacity
@@ -83,32 +84,37 @@ class KVCache:
         self.buf = torch.zeros(nbytes, dtype=torch.uint8, device=device)
 
     def _blocks(self):
-        c = self.cfg
-        return self.buf.view(storage_dtype(c)).view(c.n_layers, 2, self.batch, c.n_kv_heads,
-                                                    self.capacity * c.head_dim)
+        c, P = self.cfg, lsv.LSV_KV_ALIGN
+        return self.buf.view(storage_dtype(c)).view(c.n_layers, 2, self.batch, self.capacity // P, c.n_kv_heads,
+                                                    P * c.head_dim)
 
     def k_view(self):
-        """[layer][batch][kv_head][pos][head_dim] view of the K blocks."""
-        c = self.cfg
-        return self._blocks()[:, 0].view(c.n_layers, self.batch, c.n_kv_heads, self.capacity, c.head_dim)
+        """[layer][batch][block][kv_head][j][head_dim] view of the K blocks (position 64 block + j)."""
+        c, P = self.cfg, lsv.LSV_KV_ALIGN
+        return self._blocks()[:, 0].view(c.n_layers, self.batch, self.capacity // P, c.n_kv_heads, P, c.head_dim)
 
     def vt_view(self):
-        """[layer][batch][kv_head][head_dim][column] view of the transposed V blocks."""
-        c = self.cfg
-        return self._blocks()[:, 1].view(c.n_layers, self.batch, c.n_kv_heads, c.head_dim, self.capacity)
+        """[layer][batch][block][kv_head][head_dim][column] view of the transposed V blocks."""
+        c, P = self.cfg, lsv.LSV_KV_ALIGN
+        return self._blocks()[:, 1].view(c.n_layers, self.batch, self.capacity // P, c.n_kv_heads, c.head_dim, P)
+
+    def _index(self, start, n):
+        pos = torch.arange(start, start + n, device=self.buf.device)
+        j = pos % lsv.LSV_KV_ALIGN
+        return pos // lsv.LSV_KV_ALIGN, j, v_column(j)
 
     def write(self, layer, b, start, k, v):
         """Store K and V of positions start.. (device tensors [kv_head][n][head_dim])."""
-        n = k.shape[1]
-        self.k_view()[layer, b, :, start:start + n] = k
-        cols = v_column(torch.arange(start, start + n, device=self.buf.device))
-        self.vt_view()[layer, b][:, :, cols] = v.transpose(1, 2)
+        blk, j, col = self._index(start, k.shape[1])
+        # the indexed views put the position first: [n][kv_head][head_dim]
+        self.k_view()[layer, b][blk, :, j] = k.transpose(0, 1)
+        self.vt_view()[layer, b][blk, :, :, col] = v.transpose(0, 1)
 
     def read(self, layer, b, start, n):
         """(K, V) of positions start..start+n-1 as [kv_head][n][head_dim] tensors."""
-        k = self.k_view()[layer, b, :, start:start + n]
-        cols = v_column(torch.arange(start, start + n, device=self.buf.device))
-        v = self.vt_view()[layer, b][:, :, cols].transpose(1, 2)
+        blk, j, col = self._index(start, n)
+        k = self.k_view()[layer, b][blk, :, j].transpose(0, 1)
+        v = self.vt_view()[layer, b][blk, :, :, col].transpose(0, 1)
         return k, v
 
 

@@ -36,7 +36,7 @@ def test_exports_every_declared_symbol(lib):
 def test_status_strings(lib):
     assert lsv.lsv_status_string(0) == "ok"
     assert "capacity" in lsv.lsv_status_string(lsv.LSV_ERR_CAPACITY)
-    assert lsv.lsv_abi_version() == 2
+    assert lsv.lsv_abi_version() == 3
 
 
 def test_timing_hook_validation(lib):
@@ -118,7 +118,7 @@ def test_host_validation(lib):
     assert "multiple" in msg
     expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_verify_block, *(args[:8] + [lsv.LSV_MAX_ROWS + 1] + args[9:]))
     msg = expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_verify_block, *(args[:3] + [1 << 23] + args[4:]))
-    assert "2 GiB" in msg  # 2^23 positions x 64 dims x 4 bytes: the slab offsets would not fit 32 bits
+    assert "2 GiB" in msg  # 2^23 positions x kv heads x 64 dims x 4 bytes: block offsets would not fit 32 bits
     expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_verify_block, *(args[:4] + [0] + args[5:]))
     expect(lsv.LSV_ERR_INVALID_ARG, lsv.lsv_verify_block, *(args[:13] + [16] + args[14:]))
     expect(lsv.LSV_ERR_UNSUPPORTED, lsv.lsv_verify_block, *([tiny_cfg(head_dim=96)] + args[1:]))
