@@ -597,9 +597,10 @@ def length_rules(wl, cost, dev, n_rows=4096):
     confidence model -- the synthetic analogue of the trade-off sensitivity of Table 4 and of
     the deviation from the oracle length of Sec. 4.7.  Per rule: mean length, mean
     |gamma - gamma_exhaustive|, and the mean of f(gamma) / f(gamma_exhaustive) with
-    f = (1 + sum_{j<=gamma} prod_{k<=j} q_k) / cost[gamma] (Eq. 2's objective with the always
-    emitted token); Algorithm 1 also the drafter blocks of n its budget requests.  All
-    selections run in the library's selector on the GPU."""
+    f = (sum_{j<=gamma} prod_{k<=j} q_k) / cost[gamma], Eq. 2's objective as the selectors run it
+    (no LSV_SEL_BONUS), so EXHAUSTIVE's own ratio is 1 and no rule's exceeds it; Algorithm 1 also
+    the drafter blocks of n its budget requests.  All selections run in the library's selector on
+    the GPU."""
     import torch
 
     from paper_2608_08721_amd import lsv
@@ -611,7 +612,7 @@ def length_rules(wl, cost, dev, n_rows=4096):
     gamma = torch.zeros(n_rows, dtype=torch.int32, device=dev)
     aux = torch.zeros(n_rows, dtype=torch.int32, device=dev)
     p = np.cumprod(conf_np.astype(np.float64), axis=1)
-    n_tok = 1.0 + np.cumsum(p, axis=1)                      # N(gamma), gamma = 1..G
+    n_tok = np.cumsum(p, axis=1)                            # N(gamma), gamma = 1..G
     f = n_tok / np.asarray(cost[1:G + 1], dtype=np.float64)[None, :]
     rows = np.arange(n_rows)
 
