@@ -460,6 +460,20 @@ template <int KIND> struct MultiTile {
   LSV_DEV static bool use(int mt, int Nt) { return mt >= 2 && TPW != GemmCfg<KIND>::TPW && (Nt + TPW - 1) / TPW >= kComputeUnits; }
 };
 
+// One activation tile on the residual products (O, down): a one-row stream spends half of its
+// load instructions on the block's activation fragments, so two fragment rows per wave -- while a
+// stream per compute unit remains -- move more weight bytes per instruction (lab, Llama-3-70B at
+// 16 rows: down 80.1 -> 68.3 us, O 24.3 -> 22.4 us; the QKV projection lost, 33 -> 37 us, and
+// the same for two tiles lost).  Two k-steps per stage and six stages keep 24 KB in flight per
+// stream, as one row at U 8 did; 32 KB lost.  A wave's products and sums are those of one row per
+// wave, so the outputs are bit-identical either way.
+template <int KIND> struct PairRows {
+  static constexpr int TPW = 2, U = 2, NS = 6;
+  LSV_DEV static bool use(int mt, int Nt) {
+    return (KIND == GEMM_O || KIND == GEMM_DOWN) && mt == 1 && (Nt + TPW - 1) / TPW >= kComputeUnits;
+  }
+};
+
 // Rows come in chunks of 64 (4 activation tiles); a chunk's workgroups read the same
 // weights, so the grid puts the chunks of one column tile on the same XCD (workgroup
 // ids congruent mod 8 share one) where the repeated reads hit its L2.  The host bound
@@ -484,6 +498,14 @@ __global__ void __launch_bounds__(64 * GemmCfg<KIND>::KS) gemm_kernel(GemmArgs a
   // 64-row bound, 41 -> 25 us); three or four take the shallower one
   using C = GemmCfg<KIND>;
   const int ks = threadIdx.x >> 6;
+  if constexpr (std::is_same<T, bf16_t>::value && S::KS == 1 && (KIND == GEMM_O || KIND == GEMM_DOWN)) {
+    using P = PairRows<KIND>;
+    if (P::use(mt, a.Nt)) {
+      if (tile >= (a.Nt + P::TPW - 1) / P::TPW) return;
+      gemm_body<T, 1, P::TPW, 1, P::U, P::NS, S::EPI, MT_MAX>(a, M_end, tile, m0, nullptr, 0);
+      return;
+    }
+  }
   if constexpr (std::is_same<T, bf16_t>::value && S::KS == 1 && MT_MAX >= 2) {
     using X = MultiTile<KIND>;
     if (X::use(mt, a.Nt)) {
@@ -703,6 +725,14 @@ __global__ void __launch_bounds__(256) gemm_fused_kernel(GemmArgs a) {
     using C = GemmCfg<KIND>;
     using S = GemmShape<KIND, 4>;
     static_assert(C::KS == 1, "one wave per column tile");
+    if constexpr (KIND == GEMM_O || KIND == GEMM_DOWN) {
+      using P = PairRows<KIND>;
+      if (P::use(mt, a.Nt)) {  // one activation tile on a wide residual product
+        if (vt >= (a.Nt + P::TPW - 1) / P::TPW) return;
+        gemm_body<bf16_t, 1, P::TPW, 1, P::U, P::NS, S::EPI, 4>(a, M, vt, 0, nullptr, 0);
+        return;
+      }
+    }
     using X = MultiTile<KIND>;
     if (X::use(mt, a.Nt)) {  // two or more activation tiles on a wide product
       if (vt >= (a.Nt + X::TPW - 1) / X::TPW) return;

@@ -194,9 +194,11 @@ def test_wide_model_two_fragment_rows_per_wave():
     """Blocks of two to four activation tiles at Llama-3-70B width, one layer: QKV, O and down
     then stream two fragment rows per wave (640 and 512 fragment rows still leave a stream per
     compute unit) -- 22 rows under a 64-row bound (the 64-row kernel) and 50 rows under a
-    batched bound (the fused kernel's 64-row body)."""
+    batched bound (the fused kernel's 64-row body).  With one activation tile O and down still
+    take two rows per wave (12 rows under a batched bound)."""
     _bf16_case(configs.LLAMA3_70B.with_layers(1), 24, [500, 300], [13, 9])
     _bf16_case(configs.LLAMA3_70B.with_layers(1), 25, [400], [50], bound=132)
+    _bf16_case(configs.LLAMA3_70B.with_layers(1), 26, [300, 200], [5, 7], bound=132)
 
 
 def test_workspace_reused_across_bounds():

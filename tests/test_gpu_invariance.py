@@ -37,3 +37,28 @@ def test_row_logits_do_not_depend_on_block_size(shape):
             assert np.array_equal(lg, whole[pos:pos + n]), (shape.name, sizes, pos)
             pos += n
     note(f"  {shape.name}: 17 rows bit-identical as one block and as blocks of 1, 5 and 11 rows")
+
+
+def test_row_logits_do_not_depend_on_block_size_wide_model():
+    """Llama-3-70B width, one layer: its O and down products stream two fragment rows per wave
+    for one activation tile and its QKV, O and down for two or more (each wave's sums are those
+    of one row per wave), so the same 20 rows as one block, as blocks of 9 and 11 under a batched
+    bound and as blocks of 5 under a 16-row bound must give bit-identical logits."""
+    shape = configs.LLAMA3_70B.with_layers(1)
+    seed, C, R = 62, 150, 20
+    w = gen.model_weights(shape, seed)
+    cap = runtime.kv_capacity(C + R + 8)
+    gm = GpuModel(shape, w, 1, cap, max_rows=132)
+    k, v = gen.synthetic_kv(shape, seed, 0, 1, C)
+    gm.kv.write(0, 0, 0, runtime.to_device(k[0]), runtime.to_device(v[0]))
+    toks = gen.randint(seed, 900, R, shape.vocab)
+    whole, st = gm.verify([C], toks, [0, R], max_rows=132)
+    assert st[0] == 0 and np.isfinite(whole).all()
+    for sizes, bound in (([9, 11], 132), ([5, 5, 5, 5], 16)):
+        pos = 0
+        for n in sizes:
+            lg, st = gm.verify([C + pos], toks[pos:pos + n], [0, n], max_rows=bound)
+            assert st[0] == 0
+            assert np.array_equal(lg, whole[pos:pos + n]), (sizes, bound, pos)
+            pos += n
+    note(f"  {shape.name}: 20 rows bit-identical as one block and as blocks of 9 + 11 and 5")
