@@ -103,6 +103,8 @@ static VerifyPlan plan_verify(const Shape& s, const ModelLayout& ml, int batch, 
   v.MT = max_rows > 64 ? 4 : (max_rows + 15) / 16;  // activation tiles per 64-row chunk
   v.wide = s.dtype == LSV_DTYPE_BF16 && max_rows > 64 && max_rows <= kWideRows;
   v.part_floats = 0;
+  if (s.dtype == LSV_DTYPE_BF16 && residual_split_pairs(GEMM_O, ml.o.Nt))  // O and down: Nt = d / 16
+    v.part_floats = split_pair_floats(ml.o.Nt, max_rows);
   if (v.wide) {
     const PackedMat* mats[5] = {&ml.qkv, &ml.o, &ml.gateup, &ml.down, &ml.lm_head};
     for (int k = 0; k < 5; ++k) {
@@ -158,34 +160,76 @@ size_t verify_workspace_bytes(const Shape& s, int batch, int max_rows, int max_c
 
 // ------------------------------------------------------------------ row normalisation
 // a[m] = R(h[m] / sqrt(mean(h[m]^2) + eps) * g) of one row, by one 256-thread workgroup.
-// Thread t holds the lane runs of EPL columns t, t + 256, ... of the row (EPL = 8 bf16 or
-// 4 fp32 columns: one 16-byte store of the operand each) in registers from a single read;
+// Thread t holds the lane runs of EPL columns t, t + 256, ... of the row (EPL = 8 bf16 or 4 fp32
+// columns: one 16-byte store of the operand each) in registers from a single read;
 // its sum of squares runs over them in order, the wave adds its lanes in a fixed shuffle
 // tree and wave 0 adds the four waves' sums in order.  Every element is then scaled,
 // multiplied by its gain and rounded once.
+// part (NULL: none): the k-split partial sums [tile][split][M_max][kWideCols] that the residual
+// product before it left; the `splits` pieces of each of the thread's columns are loaded with
+// its h (all in flight at once), added in split order, ((0 + p_0) + p_1) + ..., and the sum
+// joins the residual stream, h += sum, which is stored before the row is normalised from the
+// same registers.
 template <typename T>
-LSV_DEV void normalise_row(const float* __restrict__ hrow, int d, const float* __restrict__ gain, float eps, int m,
-                           T* __restrict__ a) {
+LSV_DEV void normalise_row(float* __restrict__ hrow, int d, const float* __restrict__ gain, float eps, int m,
+                           T* __restrict__ a, const float* __restrict__ part, int splits, int M_max) {
   constexpr int KT = 64 / sizeof(T), EPL = KT / 4;
   constexpr int RUNS = 8192 / (256 * EPL);  // d_model <= 8192
+  constexpr int JB = 4;                     // splits whose pieces are in flight together
   __shared__ float wsum[4];
   const int t = threadIdx.x;
-  float x[RUNS][EPL];
-  float ss = 0.f;
+  f32x4_t x[RUNS][EPL / 4];
 #pragma unroll
   for (int r = 0; r < RUNS; ++r) {
     const int c = (t + 256 * r) * EPL;
 #pragma unroll
-    for (int e = 0; e < EPL; e += 4) {
-      f32x4_t v = {0.f, 0.f, 0.f, 0.f};
-      if (c < d) v = *(const GLOBAL f32x4_t*)(GL(hrow) + c + e);
+    for (int e = 0; e < EPL / 4; ++e)
+      x[r][e] = c < d ? *(const GLOBAL f32x4_t*)(GL(hrow) + c + 4 * e) : f32x4_t{0.f, 0.f, 0.f, 0.f};
+  }
+  if (part && splits > 1) {
+    const size_t jstride = (size_t)M_max * kWideCols;
+    f32x4_t acc[RUNS][EPL / 4];
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        x[r][e + q] = v[q];
-        ss += v[q] * v[q];
-      }
+    for (int r = 0; r < RUNS; ++r)
+#pragma unroll
+      for (int e = 0; e < EPL / 4; ++e) acc[r][e] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    for (int j0 = 0; j0 < splits; j0 += JB) {
+      f32x4_t v[JB][RUNS][EPL / 4];
+#pragma unroll
+      for (int r = 0; r < RUNS; ++r)
+#pragma unroll
+        for (int e = 0; e < EPL / 4; ++e) {
+          const int c = min((t + 256 * r) * EPL + 4 * e, d - 4);  // columns past d read the last piece
+          const GLOBAL float* p = GL(part) + ((size_t)(c / kWideCols) * splits * M_max + m) * kWideCols + c % kWideCols;
+#pragma unroll
+          for (int i = 0; i < JB; ++i) v[i][r][e] = *(const GLOBAL f32x4_t*)(p + (size_t)min(j0 + i, splits - 1) * jstride);
+        }
+#pragma unroll
+      for (int i = 0; i < JB; ++i)
+        if (j0 + i < splits)
+#pragma unroll
+          for (int r = 0; r < RUNS; ++r)
+#pragma unroll
+            for (int e = 0; e < EPL / 4; ++e) acc[r][e] += v[i][r][e];
+    }
+#pragma unroll
+    for (int r = 0; r < RUNS; ++r) {
+      const int c = (t + 256 * r) * EPL;
+#pragma unroll
+      for (int e = 0; e < EPL / 4; ++e)
+        if (c < d) {
+          x[r][e] = x[r][e] + acc[r][e];
+          *(GLOBAL f32x4_t*)(GL(hrow) + c + 4 * e) = x[r][e];
+        }
     }
   }
+  float ss = 0.f;
+#pragma unroll
+  for (int r = 0; r < RUNS; ++r)
+#pragma unroll
+    for (int e = 0; e < EPL / 4; ++e)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) ss += x[r][e][q] * x[r][e][q];
   for (int o = 32; o > 0; o >>= 1) ss += __shfl_xor(ss, o, kWave);
   if ((t & 63) == 0) wsum[t >> 6] = ss;
   __syncthreads();
@@ -200,7 +244,7 @@ LSV_DEV void normalise_row(const float* __restrict__ hrow, int d, const float* _
     for (int e = 0; e < EPL; e += 4) {
       const f32x4_t gv = *(const GLOBAL f32x4_t*)(GL(gain) + c + e);
 #pragma unroll
-      for (int q = 0; q < 4; ++q) y[e + q] = x[r][e + q] * inv * gv[q];
+      for (int q = 0; q < 4; ++q) y[e + q] = x[r][e / 4][q] * inv * gv[q];
     }
     u32x4_t out;
     if constexpr (sizeof(T) == 2) {
@@ -215,53 +259,18 @@ LSV_DEV void normalise_row(const float* __restrict__ hrow, int d, const float* _
 }
 
 // The consumer operand of the next projection, one workgroup per block row.  part: the k-split
-// partial sums [tile][split][M_max][kWideCols] that the batched body of the residual product
-// before it left for a block of more than 64 rows (NULL when that product runs unsplit): they
-// are added in split order and the sum joins the residual stream, h += sum, before the row is
-// normalised.
+// partial sums [tile][split][M_max][kWideCols] that the residual product before it left -- the
+// batched body for a block of more than 64 rows (splits_hi of them), the split pairs of the
+// narrower models otherwise (splits_lo = 2); a count of 1 means none.  normalise_row adds them to
+// the residual stream before it normalises the row.
 template <typename T>
 __global__ void __launch_bounds__(256) rmsnorm_kernel(float* __restrict__ h, int d, const float* gain, float eps,
                                                       const int32_t* row_offsets, int batch, int M_max, T* a,
-                                                      const float* __restrict__ part, int splits) {
+                                                      const float* __restrict__ part, int splits_lo, int splits_hi) {
   const int m = blockIdx.x;
   const int M = min(GL(row_offsets)[batch], M_max);
   if (m >= M) return;
-  float* hrow = h + (size_t)m * d;
-  if (part && M > 64) {
-    // thread t: columns 4 (t + 256 r) .. +3, r < RUNS (d <= 8192); the partials of JB splits
-    // for all of its columns are in flight at once
-    constexpr int RUNS = 8192 / 1024, JB = 4;
-    const size_t jstride = (size_t)M_max * kWideCols;
-    f32x4_t acc[RUNS];
-#pragma unroll
-    for (int r = 0; r < RUNS; ++r) acc[r] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-    for (int j0 = 0; j0 < splits; j0 += JB) {
-      f32x4_t v[JB][RUNS];
-#pragma unroll
-      for (int r = 0; r < RUNS; ++r) {
-        const int c = (threadIdx.x + 256 * r) * 4;
-        const GLOBAL float* p =
-            GL(part) + ((size_t)(min(c, d - 4) / kWideCols) * splits * M_max + m) * kWideCols + min(c, d - 4) % kWideCols;
-#pragma unroll
-        for (int i = 0; i < JB; ++i) v[i][r] = *(const GLOBAL f32x4_t*)(p + (size_t)min(j0 + i, splits - 1) * jstride);
-      }
-#pragma unroll
-      for (int i = 0; i < JB; ++i)
-        if (j0 + i < splits)
-#pragma unroll
-          for (int r = 0; r < RUNS; ++r) acc[r] += v[i][r];
-    }
-#pragma unroll
-    for (int r = 0; r < RUNS; ++r) {
-      const int c = (threadIdx.x + 256 * r) * 4;
-      if (c < d) {
-        const f32x4_t hv = *(const GLOBAL f32x4_t*)(GL(hrow) + c);
-        *(GLOBAL f32x4_t*)(GL(hrow) + c) = hv + acc[r];
-      }
-    }
-    __syncthreads();  // the workgroup's stores of the row are visible to its own loads below
-  }
-  normalise_row<T>(hrow, d, gain, eps, m, a);
+  normalise_row<T>(h + (size_t)m * d, d, gain, eps, m, a, part, M > 64 ? splits_hi : splits_lo, M_max);
 }
 
 // ------------------------------------------------------------------ tree blocks
@@ -349,7 +358,7 @@ __global__ void __launch_bounds__(256) embed_kernel(const T* __restrict__ E, int
     *(GLOBAL f32x4_t*)(GL(hrow) + c) = v;
   }
   __syncthreads();  // the workgroup's stores of the row are visible to its own loads below
-  normalise_row<T>(hrow, d, gain, eps, m, a);
+  normalise_row<T>(hrow, d, gain, eps, m, a, nullptr, 1, M_max);
 }
 
 int launch_verify(const Shape& s, const ModelLayout& ml, const void* packed, void* kv, const KvLayout& kvl, int batch,
@@ -383,14 +392,15 @@ int launch_verify(const Shape& s, const ModelLayout& ml, const void* packed, voi
   // a = R(h / rms(h) * gain) for the next projection, after the k-split partials of the
   // residual product before it (batched bounds) join h
   auto rmsnorm = [&](const float* gain, GemmKind after) {
-    const int splits = v.wide ? v.w[after].splits : 1;
-    const float* part = splits > 1 ? w.part : nullptr;
+    const int lo = bf16 && residual_split_pairs(after, ml.o.Nt) ? 2 : 1;  // O and down share Nt = d / 16
+    const int hi = v.wide ? v.w[after].splits : lo;
+    const float* part = lo > 1 || hi > 1 ? w.part : nullptr;
     if (bf16)
       hipLaunchKernelGGL(rmsnorm_kernel<bf16_t>, dim3(max_rows), dim3(256), 0, st, w.h, s.d, gain, s.eps, row_offsets,
-                         batch, max_rows, (bf16_t*)w.a, part, splits);
+                         batch, max_rows, (bf16_t*)w.a, part, lo, hi);
     else
       hipLaunchKernelGGL(rmsnorm_kernel<float>, dim3(max_rows), dim3(256), 0, st, w.h, s.d, gain, s.eps, row_offsets,
-                         batch, max_rows, (float*)w.a, part, splits);
+                         batch, max_rows, (float*)w.a, part, lo, hi);
     return hipGetLastError() == hipSuccess ? LSV_OK : LSV_ERR_HIP;
   };
 
@@ -420,11 +430,11 @@ int launch_verify(const Shape& s, const ModelLayout& ml, const void* packed, voi
     const int idx = kind == GEMM_LMHEAD ? 0 : a.layer_index;
     timing_before((int)kind, idx, st);
     int rc;
+    a.part = w.part;  // the residual products' split pairs (narrower bf16 models) or batched split-K
+    a.part_bytes = sizeof(float) * v.part_floats;
     if (v.wide) {
       // a batched bound: one launch whose workgroups run the 64-row body (the weights streamed
       // once) for blocks of up to 64 device rows and the batched body for larger ones
-      a.part = w.part;
-      a.part_bytes = sizeof(float) * v.part_floats;
       if (kind == GEMM_QKV) a.out_f32 = w.qkv_y;
       rc = launch_gemm_fused(kind, a, v.w[kind], st);
     } else {

@@ -397,6 +397,23 @@ LSV_DEV void gemm_body(const GemmArgs& a, const int M, const int tile, const int
     for (int st = 0; st < NS; ++st) compute_stage(st, nfull + st * U, true);
   }
 
+  // ---- a k range of a split pair (EPI_PART, residual_split_pairs): this range's sums, k slice
+  // `kslice` of 2, to the partials [tile][2][M_max][128] (tile = 8 fragment rows); rows past M
+  // are not written
+  if constexpr (EPI == EPI_PART) {
+    static_assert(KS == 2 && MT_MAX >= MT, "two k ranges per fragment-row pair");
+#pragma unroll
+    for (int t = 0; t < TPW; ++t)
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) {
+        const int m = m0 + mt * 16 + l16, fr = tn0 + t;
+        if (m < M && tvalid[t])
+          *(GLOBAL f32x4_t*)(a.part + (((size_t)(fr >> 3) * 2 + kslice) * a.M_max + m) * kWideCols + (fr & 7) * 16 +
+                             4 * g4) = acc[t][mt];
+      }
+    return;
+  }
+
   // ---- k-slices: waves 1.. hand their sums to wave 0 through LDS; summed in slice order
   if (KS > 1) {
     if (wave > 0) {
@@ -474,6 +491,18 @@ template <int KIND> struct PairRows {
   }
 };
 
+// The narrower residual products (residual_split_pairs): stream `s` of the launch takes fragment
+// rows 2 (s / 2), +1 over k half s % 2 -- one stream per fragment row as before, with the
+// activation loads of two rows per weight load -- and writes its half's sums (EPI_PART).  The
+// pipeline is PairRows' for one or two activation tiles and shallower for three or four.
+template <int MT, int MT_MAX>
+LSV_DEV void split_pair_body(const GemmArgs& a, const int M, const int stream, const int m0) {
+  if constexpr (MT <= 2)
+    gemm_body<bf16_t, MT, 2, 2, 2, 6, EPI_PART, MT_MAX>(a, M, stream >> 1, m0, nullptr, stream & 1);
+  else
+    gemm_body<bf16_t, MT, 2, 2, 2, 3, EPI_PART, MT_MAX>(a, M, stream >> 1, m0, nullptr, stream & 1);
+}
+
 // Rows come in chunks of 64 (4 activation tiles); a chunk's workgroups read the same
 // weights, so the grid puts the chunks of one column tile on the same XCD (workgroup
 // ids congruent mod 8 share one) where the repeated reads hit its L2.  The host bound
@@ -499,6 +528,17 @@ __global__ void __launch_bounds__(64 * GemmCfg<KIND>::KS) gemm_kernel(GemmArgs a
   using C = GemmCfg<KIND>;
   const int ks = threadIdx.x >> 6;
   if constexpr (std::is_same<T, bf16_t>::value && S::KS == 1 && (KIND == GEMM_O || KIND == GEMM_DOWN)) {
+    if (residual_split_pairs(KIND, a.Nt)) {  // one stream per fragment row: tile < tiles = Nt
+      if (mt <= 1 || MT_MAX == 1)
+        split_pair_body<1, MT_MAX>(a, M_end, tile, m0);
+      else if (mt == 2 || MT_MAX == 2)
+        split_pair_body<(MT_MAX >= 2 ? 2 : 1), MT_MAX>(a, M_end, tile, m0);
+      else if (mt == 3 || MT_MAX == 3)
+        split_pair_body<(MT_MAX >= 3 ? 3 : 1), MT_MAX>(a, M_end, tile, m0);
+      else
+        split_pair_body<MT_MAX, MT_MAX>(a, M_end, tile, m0);
+      return;
+    }
     using P = PairRows<KIND>;
     if (P::use(mt, a.Nt)) {
       if (tile >= (a.Nt + P::TPW - 1) / P::TPW) return;
@@ -726,6 +766,18 @@ __global__ void __launch_bounds__(256) gemm_fused_kernel(GemmArgs a) {
     using S = GemmShape<KIND, 4>;
     static_assert(C::KS == 1, "one wave per column tile");
     if constexpr (KIND == GEMM_O || KIND == GEMM_DOWN) {
+      if (residual_split_pairs(KIND, a.Nt)) {  // one stream per fragment row
+        if (vt >= a.Nt) return;
+        if (mt == 1)
+          split_pair_body<1, 4>(a, M, vt, 0);
+        else if (mt == 2)
+          split_pair_body<2, 4>(a, M, vt, 0);
+        else if (mt == 3)
+          split_pair_body<3, 4>(a, M, vt, 0);
+        else
+          split_pair_body<4, 4>(a, M, vt, 0);
+        return;
+      }
       using P = PairRows<KIND>;
       if (P::use(mt, a.Nt)) {  // one activation tile on a wide residual product
         if (vt >= (a.Nt + P::TPW - 1) / P::TPW) return;

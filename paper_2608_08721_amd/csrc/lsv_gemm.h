@@ -14,7 +14,7 @@ template <> struct FragTraits<float> {
   static constexpr int KT = 16, EPL = 4;
 };
 
-enum { EPI_LOGITS = 0, EPI_QKV = 1, EPI_RESID = 2, EPI_SWIGLU = 3 };
+enum { EPI_LOGITS = 0, EPI_QKV = 1, EPI_RESID = 2, EPI_SWIGLU = 3, EPI_PART = 4 };
 enum GemmKind { GEMM_QKV = 0, GEMM_O = 1, GEMM_GATEUP = 2, GEMM_DOWN = 3, GEMM_LMHEAD = 4 };
 
 struct GemmArgs {
@@ -55,6 +55,20 @@ constexpr int kRowsAny = 0x7fffffff;
 
 // One launch: a workgroup per tile of output columns, the whole K per workgroup.
 int launch_gemm(int dtype, GemmKind kind, int MT, const GemmArgs& a, hipStream_t st);
+
+// Residual products (O, down) of bf16 models narrower than Llama-3-70B (fewer than 512 fragment
+// rows of output, so two rows per stream would leave compute units idle): blocks of up to 64 rows
+// (and every block of the 64-row kernel) stream two fragment rows over half of K each, one stream
+// per fragment row, and leave the two halves' fp32 sums in a.part -- [tile][2][M_max][128], tile
+// = 8 fragment rows, the layout of the batched partials -- for the row normalisation that follows,
+// which adds them to h in half order.
+constexpr int kGemmComputeUnits = 256;  // gfx950 (MI350X, MI355X)
+__host__ __device__ inline bool residual_split_pairs(int kind, int Nt) {
+  return (kind == GEMM_O || kind == GEMM_DOWN) && (Nt + 1) / 2 < kGemmComputeUnits;
+}
+__host__ __device__ inline size_t split_pair_floats(int Nt, int M_max) {
+  return (size_t)((Nt + 7) / 8) * 2 * M_max * 128;
+}
 
 // Batched blocks (bf16, 64 < rows <= kWideRows): every row in one workgroup, activations via LDS.
 constexpr int kWideRows = LSV_WIDE_ROWS;
