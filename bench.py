@@ -984,9 +984,7 @@ def measure(w, args, primary=True):
         lsv.lsv_select_length(mode, B, G, conf, cost_t, 1, G, 2.2, n_alg1, 0, gamma, aux, row_off, status)
         torch.cuda.synchronize()
         chosen[name] = [int(x) for x in gamma.cpu()]
-    g_star = chosen["marginal"]
-    tokens = layout(g_star)
-    log(f"{wl.name}: chosen gamma: {chosen}")
+    g_marginal = chosen["marginal"]
 
     # ---- joint batched selection on a cost table over total drafts R (linear between the
     # uniform-gamma points R = B * gamma of the sweep), with its launch time
@@ -1020,7 +1018,15 @@ def measure(w, args, primary=True):
     del jg
     joint_info = {"gamma": chosen["joint"], "total_drafts": int(tot_joint.cpu()[0]), "launch_us": round(joint_us, 2),
                   "predicted_tokens_per_ms": expected_tokens(conf_np, chosen["joint"]) / cost_j[sum(chosen["joint"])],
-                  "predicted_tokens_per_ms_marginal": expected_tokens(conf_np, g_star) / cost_j[sum(g_star)]}
+                  "predicted_tokens_per_ms_marginal": expected_tokens(conf_np, g_marginal) / cost_j[sum(g_marginal)]}
+    # the timed step's rule: a single sequence takes MARGINAL on the per-gamma table; a batch takes the
+    # joint rule, Eq. 2 over the batch's total drafts, because one step verifies all of the batch's rows
+    # and its cost follows their total (the per-sequence rule prices each sequence as if the whole batch
+    # had its length, and can pick a length that lengthens everyone's step)
+    rule = "joint" if B > 1 else "marginal"
+    g_star = chosen[rule]
+    tokens = layout(g_star)
+    log(f"{wl.name}: chosen gamma: {chosen}; timed step: {rule}")
 
     # ---- the timed step: select -> verify -> accept, one graph, dominant kernel bracketed by events
     n_slots = m.n_layers
@@ -1028,8 +1034,11 @@ def measure(w, args, primary=True):
 
     def step():
         seq_work.copy_(seq_base)
-        lsv.lsv_select_length(lsv.LSV_SEL_MARGINAL, B, G, conf, cost_t, 1, G, 2.2, n_alg1, 0, gamma, aux, row_off,
-                              status)
+        if B > 1:
+            lsv.lsv_select_joint(B, G, conf, cost_jt, G, 0, gamma, tot_joint, row_off, status)
+        else:
+            lsv.lsv_select_length(lsv.LSV_SEL_MARGINAL, B, G, conf, cost_t, 1, G, 2.2, n_alg1, 0, gamma, aux,
+                                  row_off, status)
         lsv.lsv_verify_block(cfg, dm.buf, kv.buf, cap, B, seq_base, tokens, row_off, rows_step, cap, logits, status,
                              ws.buf, ws.nbytes)
         lsv.lsv_accept(acc_mode, B, m.vocab, logits, row_off, rows_step, rows_seq, tokens, acc_q, acc_T, seed, 0,
@@ -1145,7 +1154,8 @@ def measure(w, args, primary=True):
         "dtype": "bf16" if m.dtype == "bf16" else "f32",
         "data": f"synthetic (seeded random-init weights, random prompt ids; drafts {draft_kind})",
         "config": {"workload": wl.name, "model_shape": m.name, "batch": B, "context": one(ctx), "drafted": G,
-                   "gamma": one(g_star), "rows": rows, "selector": "marginal on measured cost",
+                   "gamma": one(g_star), "rows": rows,
+                   "selector": ("joint (Eq. 2 over the batch's total drafts)" if B > 1 else "marginal") + " on measured cost",
                    "accept": "greedy" if not sampling else f"sample T={wl.temperature}"},
         "value_is": "expected emitted tokens per second of the step: sum_b (1 + N_b(gamma_b)) / step latency, "
                     "N_b from the drafter confidences (Eq. 2's numerator, Assumption 3.7)",
