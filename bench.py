@@ -338,8 +338,10 @@ def summarize_counters(trace_dir, pmc_dirs):
     wl = runs[0][2] if runs else "?"
     from synth import configs
     B = configs.WORKLOADS[wl].batch if wl in configs.WORKLOADS else 1
+    bt = json.loads(open(os.path.join(trace_dir, "bench.json")).read().strip().splitlines()[-1])
     cmds = [f"rocprofv3 --kernel-trace --stats --output-format csv -d {os.path.normpath(trace_dir)} -o t -- python3 "
-            f"bench.py --workload {wl} --secondary none --no-cpu-baseline --rounds 0 --steps 50 --warmup 5"]
+            f"bench.py --workload {wl} --secondary none --no-cpu-baseline --rounds 0 --steps {bt['steps']} "
+            f"--warmup {bt['warmup']}"]
     for d, names, _ in runs:
         bj = json.loads(open(os.path.join(d, "bench.json")).read().strip().splitlines()[-1])
         g = bj["roofline"]["rows"] // B - 1
