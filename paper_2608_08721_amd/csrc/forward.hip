@@ -178,14 +178,25 @@ LSV_DEV void normalise_row(float* __restrict__ hrow, int d, const float* __restr
   constexpr int JB = 4;                     // splits whose pieces are in flight together
   __shared__ float wsum[4];
   const int t = threadIdx.x;
-  f32x4_t x[RUNS][EPL / 4];
+  // the row and the gains of the thread's columns are loaded together (the gains do not depend on
+  // the row, and loading them after the reduction would add a memory round trip); columns past d
+  // load the last piece (in bounds, no branch) and count as zeros
+  f32x4_t x[RUNS][EPL / 4], gv[RUNS][EPL / 4];
 #pragma unroll
   for (int r = 0; r < RUNS; ++r) {
     const int c = (t + 256 * r) * EPL;
 #pragma unroll
-    for (int e = 0; e < EPL / 4; ++e)
-      x[r][e] = c < d ? *(const GLOBAL f32x4_t*)(GL(hrow) + c + 4 * e) : f32x4_t{0.f, 0.f, 0.f, 0.f};
+    for (int e = 0; e < EPL / 4; ++e) {
+      const int cc = min(c + 4 * e, d - 4);
+      x[r][e] = *(const GLOBAL f32x4_t*)(GL(hrow) + cc);
+      gv[r][e] = *(const GLOBAL f32x4_t*)(GL(gain) + cc);
+    }
   }
+#pragma unroll
+  for (int r = 0; r < RUNS; ++r)
+#pragma unroll
+    for (int e = 0; e < EPL / 4; ++e)
+      if ((t + 256 * r) * EPL >= d) x[r][e] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   if (part && splits > 1) {
     const size_t jstride = (size_t)M_max * kWideCols;
     f32x4_t acc[RUNS][EPL / 4];
@@ -241,11 +252,9 @@ LSV_DEV void normalise_row(float* __restrict__ hrow, int d, const float* __restr
     if (c >= d) break;
     float y[EPL];
 #pragma unroll
-    for (int e = 0; e < EPL; e += 4) {
-      const f32x4_t gv = *(const GLOBAL f32x4_t*)(GL(gain) + c + e);
+    for (int e = 0; e < EPL; e += 4)
 #pragma unroll
-      for (int q = 0; q < 4; ++q) y[e + q] = x[r][e / 4][q] * inv * gv[q];
-    }
+      for (int q = 0; q < 4; ++q) y[e + q] = x[r][e / 4][q] * inv * gv[r][e / 4][q];
     u32x4_t out;
     if constexpr (sizeof(T) == 2) {
 #pragma unroll
