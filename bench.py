@@ -203,8 +203,15 @@ def summarize(trace_dir, fetch_dir, write_dir):
     roof_sum = [sum(dur(r) for r in g) for g in gu]
     roof_span = [(int(g[-1]["End_Timestamp"]) - int(g[0]["Start_Timestamp"])) / 1e3 for g in gu]
     names = sorted({_short(r["Kernel_Name"]) for g in gu for r in g})
-    sel = [r for r in trace if SELECT_KERNEL in r["Kernel_Name"]]
-    i0 = 3 + 1 + bt["warmup"]
+    # one selector launch per step: a batch's timed step selects with the joint rule, whose kernel
+    # first ran 1 + 2 x 20 times (the selection and its timing graph); a single sequence's with
+    # MARGINAL, after the three rules' own selections; then the step before capture and the warmups
+    if bt["config"]["batch"] > 1:
+        sel = [r for r in trace if "select_joint_kernel" in r["Kernel_Name"]]
+        i0 = 1 + 2 * 20 + 1 + bt["warmup"]
+    else:
+        sel = [r for r in trace if SELECT_KERNEL in r["Kernel_Name"]]
+        i0 = 3 + 1 + bt["warmup"]
     t_lo, t_hi = int(sel[i0]["Start_Timestamp"]), int(sel[i0 + bt["steps"]]["Start_Timestamp"])
     per = {}
     for r in trace:
