@@ -66,9 +66,9 @@ def parse():
                         "0 skips it)")
     p.add_argument("--calib-copy", action="store_true",
                    help="also run one plain 256 MiB copy kernel (counter calibration for --pmc runs)")
-    p.add_argument("--counters-only", type=int, default=0, metavar="GAMMA",
+    p.add_argument("--counters-only", default="", metavar="GAMMA[,GAMMA...]",
                    help="counter runs of the profile: no prefill, sweep or CPU baseline; the eager roofline steps "
-                        "at uniform GAMMA for every sequence, then the calibration copy")
+                        "at each uniform GAMMA in turn (every sequence), then the calibration copy")
     p.add_argument("--summarize", nargs=3, metavar=("TRACE_DIR", "FETCH_DIR", "WRITE_DIR"),
                    help="no GPU work: turn the csv output of three rocprofv3 runs of this script (kernel trace, "
                         "--pmc FETCH_SIZE, --pmc WRITE_SIZE; each dir also holds that run's bench.json) into the "
@@ -226,10 +226,11 @@ def summarize(trace_dir, fetch_dir, write_dir):
     dirs = [os.path.normpath(d) for d in (trace_dir, fetch_dir, write_dir)]
     cmd_t = (f"rocprofv3 --kernel-trace --stats --output-format csv -d {dirs[0]} -o t -- {base} "
              f"--steps {bt['steps']} --warmup {bt['warmup']}")
-    g_sel = bt["config"]["gamma"]
-    g_sel = g_sel[0] if isinstance(g_sel, list) else g_sel
+    bf, bw = bench_json(fetch_dir), bench_json(write_dir)
+    assert bf["config"]["counters_gammas"] == bw["config"]["counters_gammas"], "the two counter runs differ"
     cmd_c = ("rocprofv3 --pmc {c} --output-format csv -d {d} -o {o} -- " +
-             f"python3 bench.py --workload {wl.name} --counters-only {g_sel} --roofline-steps 2")
+             f"python3 bench.py --workload {wl.name} --counters-only {bf['config']['counters_gammas']} "
+             "--roofline-steps 2")
     w(f"# gate/up GEMM + SwiGLU: {wl.name} ({m.name} shape, batch {wl.batch}, context {bt['config']['context']}, "
       f"{rows} rows)")
     w("")
@@ -263,37 +264,47 @@ def summarize(trace_dir, fetch_dir, write_dir):
     w("")
 
     def counters(d, name):
+        """Calibration copy and, per row count of the run (in launch order), the counter summed
+        over the dispatches of each gate/up launch."""
         rs = sorted(csv.DictReader(open(one(d, "*counter_collection.csv"))), key=lambda r: int(r["Dispatch_Id"]))
         rs = [r for r in rs if r["Counter_Name"] == name]
         copy = [float(r["Counter_Value"]) for r in rs if "copyBuffer" in r["Kernel_Name"]
                 and int(r["Grid_Size"]) >= 131072]
         groups = _launch_groups([r for r in rs if is_gateup(r["Kernel_Name"])])
-        bc = json.loads(open(os.path.join(d, "bench.json")).read().strip().splitlines()[-1])
-        last = groups[-bc["roofline"]["launches_timed"]:]
-        assert bc["roofline"]["rows"] == rows, (bc["roofline"]["rows"], rows)
-        return copy[-1], [sum(float(r["Counter_Value"]) for r in g) for g in last]
+        rf = bench_json(d)["roofline"]
+        last = groups[-rf["launches_timed"]:]
+        n = rf["launches_per_rows"]
+        return copy[-1], {r: [sum(float(x["Counter_Value"]) for x in g) for g in last[i * n:(i + 1) * n]]
+                          for i, r in enumerate(rf["rows_list"])}
     f_copy, f_gu = counters(fetch_dir, "FETCH_SIZE")
     w_copy, w_gu = counters(write_dir, "WRITE_SIZE")
+    assert rows in f_gu, f"the counter runs cover rows {sorted(f_gu)}, not the timed step's {rows}"
     f_scale = (CALIB_BYTES / 1024) / f_copy
     w_scale = (CALIB_BYTES / 1024) / w_copy
-    rd = statistics.mean(f_gu) * 1024 * f_scale
-    wr = statistics.mean(w_gu) * 1024 * w_scale
-    alg = gateup_bytes(m, rows)
     w("## HBM traffic (two counter runs)")
     w("")
     w(f"Calibration: a plain {CALIB_BYTES >> 20} MiB device copy reads FETCH_SIZE {f_copy:.0f} KiB and "
       f"WRITE_SIZE {w_copy:.0f} KiB, so FETCH_SIZE is scaled by {f_scale:.3f} and WRITE_SIZE by {w_scale:.3f}.")
-    w(f"Per gate/up launch of the roofline step ({len(f_gu)} launches at {rows} rows, counters of both dispatches "
-      "of a launch summed), against the algorithmic bytes:")
+    w(f"Per gate/up launch ({len(f_gu[rows])} launches at each row count, uniform gamma per sequence, counters of "
+      f"both dispatches of a launch summed), against the algorithmic bytes; the timed step ran {rows} rows:")
     w("")
     w("| rows | read MB | written MB | traffic MB | algorithmic MB | ratio |")
     w("|---:|---:|---:|---:|---:|---:|")
-    w(f"| {rows} | {rd / 1e6:.2f} | {wr / 1e6:.2f} | {(rd + wr) / 1e6:.2f} | {alg / 1e6:.2f} | {(rd + wr) / alg:.3f} |")
+    traffic = {}
+    for r in sorted(f_gu):
+        rd = statistics.mean(f_gu[r]) * 1024 * f_scale
+        wr = statistics.mean(w_gu[r]) * 1024 * w_scale
+        alg = gateup_bytes(m, r)
+        traffic[r] = rd + wr
+        mark = "**" if r == rows else ""
+        w(f"| {mark}{r}{mark} | {rd / 1e6:.2f} | {wr / 1e6:.2f} | {(rd + wr) / 1e6:.2f} | {alg / 1e6:.2f} | "
+          f"{(rd + wr) / alg:.3f} |")
     w("")
     w("Bytes per launch (read + written) by block rows, read by bench.py while source_hash matches:")
     w("")
     w("```")
-    w(f"traffic_rows_{rows}: {rd + wr:.0f}")
+    for r in sorted(traffic):
+        w(f"traffic_rows_{r}: {traffic[r]:.0f}")
     w("```")
     return "\n".join(out) + "\n"
 
@@ -351,7 +362,7 @@ def summarize_counters(trace_dir, pmc_dirs):
             f"--warmup {bt['warmup']}"]
     for d, names, _ in runs:
         bj = json.loads(open(os.path.join(d, "bench.json")).read().strip().splitlines()[-1])
-        g = bj["roofline"]["rows"] // B - 1
+        g = bj["config"].get("counters_gammas", bj["roofline"]["rows"] // B - 1)
         dn = os.path.normpath(d)
         cmds.append(f"rocprofv3 --pmc {' '.join(names)} --output-format csv -d {dn} -o {os.path.basename(dn)[0]} -- "
                     f"python3 bench.py --workload {wl} --counters-only {g} --roofline-steps 2")
@@ -870,7 +881,10 @@ def counters_only(wl, args, dev):
 
     from paper_2608_08721_amd import lsv, runtime
     from synth import gen
-    m, B, G, g = wl.model, wl.batch, wl.G, args.counters_only
+    m, B, G = wl.model, wl.batch, wl.G
+    gammas = [int(x) for x in args.counters_only.split(",")]
+    if not all(1 <= g <= G for g in gammas):
+        raise SystemExit(f"--counters-only: every gamma must lie in [1, {G}]")
     cfg = runtime.model_config(m)
     ctx = [int(c) for c in gen.contexts(wl)]
     cap = runtime.kv_capacity(max(ctx) + G + 1)
@@ -884,19 +898,22 @@ def counters_only(wl, args, dev):
     logits = torch.zeros((rows_step, m.vocab), dtype=torch.float32, device=dev)
     status = torch.zeros(B, dtype=torch.int32, device=dev)
     i32 = lambda x: torch.tensor(np.asarray(x, dtype=np.int32), device=dev)
-    off = i32(runtime.row_offsets_of([g + 1] * B))
-    toks = i32(gen.randint(wl.seed, 900, B * (g + 1), m.vocab))
     seq = i32(ctx)
     steps = args.roofline_steps
-    for _ in range(steps):
-        lsv.lsv_verify_block(cfg, dm.buf, kv.buf, cap, B, seq, toks, off, rows_step, cap, logits, status, ws.buf,
-                             ws.nbytes)
+    for g in gammas:
+        off = i32(runtime.row_offsets_of([g + 1] * B))
+        toks = i32(gen.randint(wl.seed, 900, B * (g + 1), m.vocab))
+        for _ in range(steps):
+            lsv.lsv_verify_block(cfg, dm.buf, kv.buf, cap, B, seq, toks, off, rows_step, cap, logits, status, ws.buf,
+                                 ws.nbytes)
     torch.cuda.synchronize()
     x = torch.empty(CALIB_BYTES, dtype=torch.uint8, device=dev)
     torch.empty_like(x).copy_(x)
     torch.cuda.synchronize()
-    print(json.dumps({"config": {"workload": wl.name}, "roofline": {"rows": B * (g + 1),
-                                                                  "launches_timed": steps * m.n_layers}}), flush=True)
+    rows = [B * (g + 1) for g in gammas]
+    print(json.dumps({"config": {"workload": wl.name, "counters_gammas": args.counters_only},
+                      "roofline": {"rows": rows[0], "rows_list": rows, "launches_per_rows": steps * m.n_layers,
+                                   "launches_timed": steps * m.n_layers * len(rows)}}), flush=True)
 
 
 def measure(w, args, primary=True):
