@@ -128,9 +128,9 @@ __global__ void __launch_bounds__(64 * NW) attn_split_bf16_kernel(AttnArgs a) {
 #pragma unroll
     for (int j = 0; j < NP; ++j) {  // piece gtid + 256 j: K row + j 256 / P8, V^T row + 32 j
       kr[j] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(
-                                              krs, koff, (kbase + j * (256 / P8) * HD) * (int)sizeof(bf16_t), 0));
+                                              krs, koff, (kbase + j * (256 / P8) * HD) * (int)sizeof(bf16_t), kBufferStream));
       vr[j] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(
-                                              vrs, voff, (vbase + j * 32 * vstride) * (int)sizeof(bf16_t), 0));
+                                              vrs, voff, (vbase + j * 32 * vstride) * (int)sizeof(bf16_t), kBufferStream));
     }
   };
   auto store_chunk = [&]() {

@@ -361,7 +361,7 @@ LSV_DEV void gemm_body(const GemmArgs& a, const int M, const int tile, const int
       for (int u = 0; u < U; ++u) {
         const int kf = max(min(kb + u, nk - 1), 0);  // a slice may be empty when Kt < KS
 #pragma unroll
-        for (int t = 0; t < TPW; ++t) wa[st][u][t] = wbase[frag_index(tr[t], k0 + kf, a.Nt, a.Kt) * 64];
+        for (int t = 0; t < TPW; ++t) wa[st][u][t] = load_stream(&wbase[frag_index(tr[t], k0 + kf, a.Nt, a.Kt) * 64]);
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) xb[st][u][mt] = *(const GLOBAL u32x4_t*)(xp[mt] + (size_t)kf * kWave * EPL);
       }
@@ -664,7 +664,7 @@ LSV_DEV void gemm_wide_body(const GemmArgs& a, const int M, u32x4_t* Ws) {
     for (int i = 0; i < PPT; ++i) {
       const int p = tid + 256 * i, f = p / kWave, ln = p % kWave;
       const int fr = tn0 + f < a.Nt ? tn0 + f : 0;
-      wst[sw][i] = wg[frag_index(fr, k0 + kk, a.Nt, a.Kt) * kWave + ln];
+      wst[sw][i] = load_stream(&wg[frag_index(fr, k0 + kk, a.Nt, a.Kt) * kWave + ln]);
     }
   };
   auto issue_x = [&](int sx, int k) {

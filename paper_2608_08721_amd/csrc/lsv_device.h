@@ -25,6 +25,13 @@ namespace lsv {
 
 constexpr int kWave = 64;
 
+// Streams read once per verify step -- packed weights, the KV cache -- are loaded non-temporal
+// (the nt cache policy; for buffer loads, bit 1 of the aux operand): without it these lines are
+// cached on their way in, evicting what is re-read (activation fragments) for nothing.  Measured
+// on Llama-3-70B at 16 rows: gate/up 150.4 -> 137.5 us per launch, QKV 33.7 -> 31.8.
+constexpr int kBufferStream = 2;
+template <typename T> LSV_DEV T load_stream(const GLOBAL T* p) { return __builtin_nontemporal_load(p); }
+
 LSV_DEV float bf2f(bf16_t b) { return __uint_as_float(((uint32_t)b) << 16); }
 
 // fp32 -> bf16, round to nearest even; NaN stays a quiet NaN.
