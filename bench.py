@@ -332,6 +332,7 @@ def summarize_counters(trace_dir, pmc_dirs):
     per = {}  # kernel -> counter -> [per-dispatch values]
     scale = {}
     runs = []
+    bt = json.loads(open(os.path.join(trace_dir, "bench.json")).read().strip().splitlines()[-1])
     for d in pmc_dirs:
         f = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)
         assert len(f) == 1, (d, f)
@@ -342,8 +343,20 @@ def summarize_counters(trace_dir, pmc_dirs):
         cmds = json.loads(open(os.path.join(d, "bench.json")).read().strip().splitlines()[-1])
         names = sorted({k for e in disp.values() for k in e if k not in ("name", "grid")})
         runs.append((d, names, cmds["config"]["workload"]))
+        # a run over several gammas: only the verify calls (each starts at its embedding kernel)
+        # at the trace run's row count
+        rows_list = cmds["roofline"].get("rows_list", [cmds["roofline"]["rows"]])
+        n_calls = sum("embed_kernel" in e["name"] for e in disp.values())
+        per_rows = n_calls // len(rows_list)
+        gi = rows_list.index(bt["roofline"]["rows"]) if len(rows_list) > 1 else 0
+        call = -1
         for i in sorted(disp):
             e = disp[i]
+            if "embed_kernel" in e["name"]:
+                call += 1
+            if len(rows_list) > 1 and call >= 0 and not gi * per_rows <= call < (gi + 1) * per_rows \
+                    and "copyBuffer" not in e["name"]:
+                continue
             if "copyBuffer" in e["name"]:
                 if e["grid"] >= 131072:  # the calibration copy (the last one): bytes per counter unit
                     for c in ("FETCH_SIZE", "WRITE_SIZE"):
@@ -356,7 +369,6 @@ def summarize_counters(trace_dir, pmc_dirs):
     wl = runs[0][2] if runs else "?"
     from synth import configs
     B = configs.WORKLOADS[wl].batch if wl in configs.WORKLOADS else 1
-    bt = json.loads(open(os.path.join(trace_dir, "bench.json")).read().strip().splitlines()[-1])
     cmds = [f"rocprofv3 --kernel-trace --stats --output-format csv -d {os.path.normpath(trace_dir)} -o t -- python3 "
             f"bench.py --workload {wl} --secondary none --no-cpu-baseline --rounds 0 --steps {bt['steps']} "
             f"--warmup {bt['warmup']}"]
@@ -370,10 +382,11 @@ def summarize_counters(trace_dir, pmc_dirs):
     out = [f"# Per-kernel counters: {wl}\n",
            "Commands (repository root, after `cd /tmp && export TMPDIR=/tmp` for the profiler's own files; each run's "
            "stdout saved as bench.json in its output directory):\n", "```", *cmds, "```\n",
-           "Counter runs (`--counters-only`: eager verify steps at one uniform gamma, the cache holding zeros, which "
+           "Counter runs (`--counters-only`: eager verify steps at uniform gammas, the cache holding zeros, which "
            "changes no kernel's traffic or instruction mix), one `--pmc` set per run; values are means per "
-           "dispatch. Kernels are listed by their total time in the kernel-trace run; the timed step's per-kernel "
-           "durations are in the gate/up summary of the same workload.\n"]
+           f"dispatch over the calls at the kernel-trace run's {bt['roofline']['rows']} rows. Kernels are listed by "
+           "their total time in the kernel-trace run; the timed step's per-kernel durations are in the gate/up "
+           "summary of the same workload.\n"]
     for d, names, _ in runs:
         out.append(f"- `{os.path.basename(os.path.normpath(d))}`: {' '.join(names)}")
     out.append("")

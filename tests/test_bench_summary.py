@@ -115,3 +115,30 @@ def test_summary_refuses_counter_runs_without_the_timed_rows(tmp_path):
     counter_run(w, "WRITE_SIZE", [4, 5], 2, {4: 1.0, 5: 1.0}, 1.0)
     with pytest.raises(AssertionError, match="rows"):
         bench.summarize(t, f, w)
+
+
+def test_counter_summary_keeps_the_timed_rows_of_a_multi_gamma_run(tmp_path):
+    """A per-kernel counter summary of a run over gammas 8, 9, 10 averages only the verify calls
+    (each opened by its embedding kernel) at the kernel-trace run's 10 rows."""
+    t, f = str(tmp_path / "t"), str(tmp_path / "f")
+    trace_run(t, warmup=1, steps=2, n_roof=2, rows=10)
+    embed = "void lsv::embed_kernel<unsigned short>(lsv::EmbedArgs)"
+    rows_csv, i = [], 0
+    for g in (8, 9, 10):
+        for _ in range(2):  # two calls per gamma
+            for name, v in ((embed, 1.0), (GATEUP, 1000.0 * g), (NORM, 10.0 * g)):
+                rows_csv.append([i, name, 1024, "FETCH_SIZE", v])
+                i += 2
+    rows_csv.append([i, COPY, 1 << 20, "FETCH_SIZE", bench.CALIB_BYTES >> 10])  # scale 1 KiB per unit
+    write_csv(os.path.join(f, "c_counter_collection.csv"),
+              ["Dispatch_Id", "Kernel_Name", "Grid_Size", "Counter_Name", "Counter_Value"], rows_csv)
+    write_json(f, {"config": {"workload": WL, "counters_gammas": "8,9,10"},
+                   "roofline": {"rows": 9, "rows_list": [9, 10, 11], "launches_per_rows": 2,
+                                "launches_timed": 6}})
+    # the trace ran 10 rows = gamma 9, the second of the run's three row counts
+    md = bench.summarize_counters(t, [f])
+    gu = next(l for l in md.splitlines() if l.startswith("| `gemm_kernel"))
+    nm = next(l for l in md.splitlines() if l.startswith("| `rmsnorm_kernel"))
+    assert gu.split("|")[2].strip() == "2" and gu.split("|")[3].strip() == f"{9000 * 1024 / 1e6:.2f} MB"
+    assert nm.split("|")[3].strip() == f"{90 * 1024 / 1e6:.2f} MB"
+    assert "--counters-only 8,9,10 --roofline-steps 2" in md
