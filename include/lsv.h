@@ -69,7 +69,9 @@ enum { LSV_DTYPE_F32 = 0, LSV_DTYPE_BF16 = 1 };
  * dtype is the storage and matrix-operand type of weights, KV cache and
  * activations between kernels; residual stream, softmax and logits are fp32.
  * Supported: head_dim in {64, 128}; n_q_heads % n_kv_heads == 0;
- * d_model % 64 == 0; rope applies to q and k. */
+ * d_model % 64 == 0, d_model <= 8192; every packed projection, the LM head
+ * included, below 4 GiB (vocab < 262,144 at d_model 8192 in bf16: the kernels
+ * address each with 32-bit byte offsets); rope applies to q and k. */
 typedef struct lsv_model_config {
   int32_t n_layers;
   int32_t d_model;

@@ -322,7 +322,8 @@ LSV_DEV void gemm_body(const GemmArgs& a, const int M, const int tile, const int
     tvalid[t] = tn0 + t < a.Nt;
     tr[t] = tvalid[t] ? tn0 + t : 0;
   }
-  const GLOBAL u32x4_t* wbase = (const GLOBAL u32x4_t*)a.W + lane;
+  // the packed weights: fragment f is the KiB at byte f * 1024, this lane's 16 bytes at + lane * 16
+  const __amdgpu_buffer_rsrc_t wrs = stream_rsrc(a.W, (size_t)a.Nt * a.Kt * 1024);
 
   // ---- the residual this tile adds to (EPI_RESID, wave 0 runs the epilogue): its loads are
   // issued ahead of the weight stream and retire with it
@@ -361,7 +362,7 @@ LSV_DEV void gemm_body(const GemmArgs& a, const int M, const int tile, const int
       for (int u = 0; u < U; ++u) {
         const int kf = max(min(kb + u, nk - 1), 0);  // a slice may be empty when Kt < KS
 #pragma unroll
-        for (int t = 0; t < TPW; ++t) wa[st][u][t] = load_stream(&wbase[frag_index(tr[t], k0 + kf, a.Nt, a.Kt) * 64]);
+        for (int t = 0; t < TPW; ++t) wa[st][u][t] = load_stream(wrs, (uint32_t)((frag_index(tr[t], k0 + kf, a.Nt, a.Kt) * 64 + lane) * 16));
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) xb[st][u][mt] = *(const GLOBAL u32x4_t*)(xp[mt] + (size_t)kf * kWave * EPL);
       }

@@ -47,6 +47,11 @@ int check_config(const lsv_model_config* c) {
   if (c->dtype != LSV_DTYPE_F32 && c->dtype != LSV_DTYPE_BF16) return fail(LSV_ERR_INVALID_ARG, "bad dtype");
   if (!(c->rms_eps > 0.f) || !(c->rope_base > 0.0) || !isfinite(c->rope_base) || c->reserved0 != 0.f)
     return fail(LSV_ERR_INVALID_ARG, "bad rms_eps / rope_base / reserved0");
+  // the weight streams address a packed matrix with 32-bit byte offsets
+  const lsv::ModelLayout ml = lsv::model_layout(lsv::shape_of(c));
+  for (const lsv::PackedMat* p : {&ml.lm_head, &ml.qkv, &ml.o, &ml.gateup, &ml.down})
+    if ((size_t)p->Nt * p->Kt * 1024 >= ((size_t)1 << 32))
+      return fail(LSV_ERR_UNSUPPORTED, "a packed projection of %zu bytes reaches 4 GiB", (size_t)p->Nt * p->Kt * 1024);
   return LSV_OK;
 }
 

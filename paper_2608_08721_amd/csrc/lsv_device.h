@@ -28,8 +28,22 @@ constexpr int kWave = 64;
 // Streams read once per verify step -- packed weights, the KV cache -- are loaded non-temporal
 // (the nt cache policy; for buffer loads, bit 1 of the aux operand): without it these lines are
 // cached on their way in, evicting what is re-read (activation fragments) for nothing.  Measured
-// on Llama-3-70B at 16 rows: gate/up 150.4 -> 137.5 us per launch, QKV 33.7 -> 31.8.
+// on Llama-3-70B at 16 rows: gate/up 150.4 -> 137.2 us per launch, QKV 33.8 -> 31.5.  The scope
+// bits (sc0, sc1) on top of nt changed nothing.
 constexpr int kBufferStream = 2;
+
+// A raw buffer resource over `bytes` bytes at p (below 4 GiB: the library refuses larger
+// packed matrices); loads past the end return zero.
+LSV_DEV __amdgpu_buffer_rsrc_t stream_rsrc(const void* p, size_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), 0, (int)(uint32_t)bytes, 0x00020000);
+}
+// 16 bytes at byte offset `off` of a read-once stream.  A buffer load takes its base from scalar
+// registers and one 32-bit lane offset, where a global load needs a 64-bit address per lane
+// (Llama-3-70B, lab: down at 36 rows 108.9 -> 100.2 us, O 34.0 -> 31.7, against global nt loads).
+LSV_DEV u32x4_t load_stream(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, kBufferStream));
+}
+// The same through a global address (the batched GEMM body, where buffer loads lost 0.3%).
 template <typename T> LSV_DEV T load_stream(const GLOBAL T* p) { return __builtin_nontemporal_load(p); }
 
 LSV_DEV float bf2f(bf16_t b) { return __uint_as_float(((uint32_t)b) << 16); }

@@ -63,6 +63,11 @@ def test_size_queries_are_host_only(lib):
     assert lsv.lsv_packed_model_bytes(tiny_cfg(head_dim=96)) == 0
     assert lsv.lsv_packed_model_bytes(tiny_cfg(n_kv_heads=3)) == 0
     assert lsv.lsv_accept_workspace_bytes(1, 17, 128256) > 0
+    # every packed matrix stays below 4 GiB: at d_model 8192 in bf16 an LM head fragment row is 256 KiB
+    wide = dict(d_model=8192, n_q_heads=64, n_kv_heads=8, head_dim=128, d_ff=28672, dtype=lsv.LSV_DTYPE_BF16)
+    assert lsv.lsv_packed_model_bytes(tiny_cfg(vocab=16383 * 16, **wide)) > 0
+    assert lsv.lsv_packed_model_bytes(tiny_cfg(vocab=16384 * 16, **wide)) == 0
+    assert "4 GiB" in lsv.lsv_last_error()
 
 
 def expect(code, fn, *args):
