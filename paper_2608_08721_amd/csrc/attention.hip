@@ -36,6 +36,15 @@ constexpr int kAttnWgs = 128;
 constexpr int kMaxChunksPerSplit = 16;
 constexpr int kComputeUnits = 256;  // gfx950 (MI350X, MI355X)
 
+//
+// Long contexts over many (sequence, kv head) pairs -- when one round's splits would walk more
+// than twice the length cap -- take a whole number of rounds' worth of splits instead, on a
+// packed grid: the splits that hold keys come first, so in a batch of ragged contexts the
+// empty splits of the short sequences no longer hold compute units while a long sequence walks
+// its splits (Llama-3-8B, batch 8, contexts of 1.7K-8.2K: 4 splits of 33 chunks become 12 of
+// 11).  With every context at the bound, three rounds of a third of the length cost what one
+// round costs.  Split boundaries still follow from the host bound alone, so a row's result does
+// not depend on its block, its batch or the other sequences' lengths.
 AttnPlan plan_attention(int batch, int nkv, int max_ctx) {
   const int n_chunks = (max_ctx + kCh - 1) / kCh;
   const int units = batch * nkv;
@@ -43,10 +52,14 @@ AttnPlan plan_attention(int batch, int nkv, int max_ctx) {
   const int by_length = (n_chunks + kMaxChunksPerSplit - 1) / kMaxChunksPerSplit;
   if (want < by_length) want = by_length;
   const int fit = kComputeUnits / units;  // splits per (sequence, kv head) in one round
-  if (want > fit) want = fit;
+  AttnPlan p;
+  p.packed = fit >= 1 && by_length > 2 * fit;
+  if (p.packed)
+    want = (by_length + fit - 1) / fit * fit;
+  else if (want > fit)
+    want = fit;
   if (want > n_chunks) want = n_chunks;
   if (want < 1) want = 1;
-  AttnPlan p;
   p.chunks_per_split = (n_chunks + want - 1) / want;
   p.n_splits = (n_chunks + p.chunks_per_split - 1) / p.chunks_per_split;
   return p;
@@ -61,6 +74,45 @@ LSV_DEV int active_splits(const AttnArgs& a, int r0, int rows, int C) {
   return (nch + a.chunks_per_split - 1) / a.chunks_per_split;
 }
 
+// Packed grid: workgroup i takes the i-th split that holds keys -- every sequence's full splits
+// first (ordered by sequence, split, kv head), then every sequence's last split (by sequence, kv
+// head) -- so the longest splits start first.  One lane per sequence (batch <= 64); every wave
+// computes the same answer, moved to scalar registers.  False: no split is left for i.
+LSV_DEV bool packed_unit(const AttnArgs& a, int i, int& s, int& kvh, int& b) {
+  const int lane = threadIdx.x & 63;
+  int act = 0;
+  if (lane < a.batch) {
+    const int r0 = GL(a.row_offsets)[lane], r1 = GL(a.row_offsets)[lane + 1];
+    act = active_splits(a, r0, r1 - r0, GL(a.seq_len)[lane]);
+  }
+  const int full = act > 0 ? (act - 1) * a.nkv : 0, last = act > 0 ? a.nkv : 0;
+  int pf = full, pl = last;  // inclusive prefix sums over the lanes
+  for (int o = 1; o < kWave; o <<= 1) {
+    const int tf = __shfl_up(pf, o, kWave), tl = __shfl_up(pl, o, kWave);
+    if (lane >= o) {
+      pf += tf;
+      pl += tl;
+    }
+  }
+  const int F = __builtin_amdgcn_readfirstlane(__shfl(pf, kWave - 1, kWave));
+  const int P = __builtin_amdgcn_readfirstlane(__shfl(pl, kWave - 1, kWave));
+  const bool in_full = i < F;
+  const int j = in_full ? i : i - F;
+  if (!in_full && j >= P) return false;
+  const unsigned long long over = __ballot(in_full ? pf > j : pl > j);  // lanes past unit j
+  const int bb = __builtin_amdgcn_readfirstlane(__ffsll((long long)over) - 1);
+  const int local = j - __builtin_amdgcn_readfirstlane(__shfl(in_full ? pf - full : pl - last, bb, kWave));
+  b = bb;
+  if (in_full) {
+    s = local / a.nkv;
+    kvh = local % a.nkv;
+  } else {
+    s = __builtin_amdgcn_readfirstlane(__shfl(act, bb, kWave)) - 1;
+    kvh = local;
+  }
+  return true;
+}
+
 template <int HD, int NW>
 __global__ void __launch_bounds__(64 * NW) attn_split_bf16_kernel(AttnArgs a) {
   constexpr int NG = NW / 4;               // wave groups: each loads one chunk per step
@@ -73,7 +125,8 @@ __global__ void __launch_bounds__(64 * NW) attn_split_bf16_kernel(AttnArgs a) {
   __shared__ __align__(16) bf16_t Ks[NG][kCh * KPITCH];  // one chunk buffer per group
   __shared__ __align__(16) bf16_t Vt[NG][HD * VPITCH];
 
-  const int s = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
+  int s = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
+  if (a.packed && !packed_unit(a, blockIdx.x, s, kvh, b)) return;
   // the wave index in a scalar register: the group, its chunk offsets and the page-table reads
   // are then wave-uniform, and the buffer loads take their chunk offsets in scalar registers
   const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
@@ -408,7 +461,7 @@ __global__ void __launch_bounds__(64) attn_f32_kernel(AttnArgs a, int hd) {
 
 int launch_attention(int dtype, int hd, const AttnArgs& a, int max_rows, hipStream_t st) {
   if (dtype == LSV_DTYPE_BF16) {
-    const dim3 grid(a.n_splits, a.nkv, a.batch);
+    const dim3 grid = a.packed ? dim3(a.n_splits * a.nkv * a.batch) : dim3(a.n_splits, a.nkv, a.batch);
     const int hpw = 256 / hd;
     const dim3 mgrid(max_rows, (a.nq + hpw - 1) / hpw);
     // query tiles per sequence (rows of a single sequence, else the mean over the batch): up

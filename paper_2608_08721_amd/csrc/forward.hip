@@ -484,6 +484,7 @@ int launch_verify(const Shape& s, const ModelLayout& ml, const void* packed, voi
     at.scale_log2 = (float)(1.4426950408889634 / sqrt((double)s.hd));
     at.n_splits = v.attn.n_splits;
     at.chunks_per_split = v.attn.chunks_per_split;
+    at.packed = v.attn.packed;
     at.anc = parents ? w.anc : nullptr;
     timing_before(LSV_KERNEL_ATTENTION, l, st);
     if ((rc = launch_attention(s.dtype, s.hd, at, max_rows, st)) != LSV_OK) return rc;

@@ -57,15 +57,19 @@ struct AttnArgs {
   void* out;       // nq*hd columns per row in the activation layout (act_index), storage type
   float scale_log2;
   int n_splits, chunks_per_split;
+  // packed grid (a 1-D grid of n_splits * nkv * batch workgroups): workgroup i takes the i-th
+  // (sequence, kv head, split) that holds keys instead of blockIdx = (split, kv head, sequence)
+  int packed;
   // tree blocks: [M_max][kAncWords] ancestor-or-self masks; a block key (position >= the
   // cached length C) at slot C + j is visible to row m iff bit j of its mask is set.  NULL:
   // the causal block.
   const uint32_t* anc;
 };
 
-// Split of the context into n_splits ranges of chunks_per_split chunks (bf16 path).
+// Split of the context into n_splits ranges of chunks_per_split chunks (bf16 path); packed:
+// the split kernel runs on a packed grid (AttnArgs::packed).
 struct AttnPlan {
-  int n_splits, chunks_per_split;
+  int n_splits, chunks_per_split, packed;
 };
 AttnPlan plan_attention(int batch, int nkv, int max_ctx);
 

@@ -12,6 +12,7 @@
 Unless a test says otherwise the RMSNorm gains are random per column (0.5 + U(0, 1)), so
 the attention, FFN and final norms' gains all reach the logits."""
 import copy
+import dataclasses
 
 import numpy as np
 import pytest
@@ -117,6 +118,18 @@ def _bf16_case(shape, seed, contexts, rows, tol=2e-2, bound=None, gains="random"
     # greedy decisions agree wherever the oracle's margin clears the row's error
     greedy_decisions(g_logits, o_logits, min_decided)
     return gm, g_logits, o_logits, toks, off
+
+
+# eight kv heads: with eight sequences, 64 (sequence, kv head) pairs share the split kernel's grid
+SMALL_KV8 = dataclasses.replace(configs.SMALL_BF16, n_kv_heads=8, n_layers=1, name="small-bf16-kv8")
+
+
+def test_bf16_packed_attention_grid_ragged_long_contexts():
+    """Eight sequences of 1 to 8,190 cached positions over eight kv heads: one round of splits
+    (four per pair) would walk 33 chunks each of the 129-chunk bound, so the split kernel runs
+    on the packed grid -- 12 splits of 11 chunks, the splits that hold keys first.  Logits,
+    appended K/V and greedy decisions against the oracle."""
+    _bf16_case(SMALL_KV8, 17, [8190, 1200, 4000, 300, 7000, 1, 2500, 6100], [3, 5, 1, 17, 2, 4, 9, 1])
 
 
 def test_bf16_gqa_hd64_ragged():

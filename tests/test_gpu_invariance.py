@@ -7,6 +7,8 @@ same order whatever the row count, and every attention tile walks the context's 
 same order with the same exp2 whether or not its chunk is masked.  This is what makes
 multi-round greedy decoding emit exactly the plain greedy stream for every speculative
 length (see test_gpu_decode.py)."""
+import dataclasses
+
 import numpy as np
 import pytest
 
@@ -62,3 +64,42 @@ def test_row_logits_do_not_depend_on_block_size_wide_model():
             assert np.array_equal(lg, whole[pos:pos + n]), (sizes, bound, pos)
             pos += n
     note(f"  {shape.name}: 20 rows bit-identical as one block and as blocks of 9 + 11 and 5")
+
+
+def test_packed_attention_grid_rows_do_not_depend_on_the_batch():
+    """The packed split grid (eight ragged sequences of up to 8,190 positions over eight kv
+    heads) takes a workgroup per split that holds keys, so which workgroup computes a split
+    depends on the other sequences' lengths and rows; the split boundaries do not.  Sequence 3's
+    17 rows verified in one batch, and again as blocks of 9 and 8 in batches whose other
+    sequences carry other rows, must give bit-identical logits."""
+    shape = dataclasses.replace(configs.SMALL_BF16, n_kv_heads=8, n_layers=1, name="small-bf16-kv8")
+    seed = 63
+    contexts = [8190, 1200, 4000, 300, 7000, 1, 2500, 6100]
+    B = len(contexts)
+    w = gen.model_weights(shape, seed)
+    cap = runtime.kv_capacity(max(contexts) + 17 + 8)
+    gm = GpuModel(shape, w, B, cap, max_rows=64)
+    for b in range(B):
+        k, v = gen.synthetic_kv(shape, seed + b, 0, 1, contexts[b])
+        gm.kv.write(0, b, 0, runtime.to_device(k[0]), runtime.to_device(v[0]))
+    rows = [3, 5, 1, 17, 2, 4, 9, 1]
+    off = runtime.row_offsets_of(rows)
+    toks = gen.randint(seed, 900, int(off[-1]), shape.vocab)
+    whole, st = gm.verify(contexts, toks, off, max_rows=64)
+    assert np.all(st == 0) and np.isfinite(whole).all()
+    mine = toks[off[3]:off[4]]
+    want = whole[off[3]:off[4]]
+    pos = 0
+    for n, others in ((9, 1), (8, 2)):
+        r = [others] * B
+        r[3] = n
+        o = runtime.row_offsets_of(r)
+        t = gen.randint(seed + n, 901, int(o[-1]), shape.vocab)
+        t[o[3]:o[4]] = mine[pos:pos + n]
+        ctx = list(contexts)
+        ctx[3] += pos
+        lg, st = gm.verify(ctx, t, o, max_rows=64)
+        assert np.all(st == 0)
+        assert np.array_equal(lg[o[3]:o[4]], want[pos:pos + n]), (n, pos)
+        pos += n
+    note("  packed grid: 17 rows of one sequence bit-identical across batches with other rows")
