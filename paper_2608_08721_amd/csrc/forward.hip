@@ -166,10 +166,10 @@ size_t verify_workspace_bytes(const Shape& s, int batch, int max_rows, int max_c
 // tree and wave 0 adds the four waves' sums in order.  Every element is then scaled,
 // multiplied by its gain and rounded once.
 // part (NULL: none): the k-split partial sums [tile][split][M_max][kWideCols] that the residual
-// product before it left; the `splits` pieces of each of the thread's columns are loaded with
-// its h (all in flight at once), added in split order, ((0 + p_0) + p_1) + ..., and the sum
-// joins the residual stream, h += sum, which is stored before the row is normalised from the
-// same registers.
+// product before it left; the `splits` pieces of each of the thread's columns (up to four in
+// flight at once, issued once h has arrived) are added in split order, ((0 + p_0) + p_1) + ...,
+// and the sum joins the residual stream, h += sum, which is stored before the row is normalised
+// from the same registers.
 template <typename T>
 LSV_DEV void normalise_row(float* __restrict__ hrow, int d, const float* __restrict__ gain, float eps, int m,
                            T* __restrict__ a, const float* __restrict__ part, int splits, int M_max) {

@@ -440,8 +440,8 @@ LSV_DEV void gemm_body(const GemmArgs& a, const int M, const int tile, const int
 // per workgroup (KS), k-steps per pipeline stage (U) and stages in flight (NS).  Chosen by
 // measurement on the Llama-3-8B shapes: few long weight streams, each with many bytes in
 // flight, beat many short ones (more concurrent streams read more scattered DRAM rows), so
-// every product runs one wave per workgroup over the whole K.  A stream sustains about
-// 11-14 GB/s however deep its pipeline, so a product with few fragment rows needs one per
+// every product runs one wave per workgroup over the whole K.  A stream sustained about
+// 11-14 GB/s however deep its pipeline (default-policy loads), so a product with few fragment rows needs one per
 // wave: the QKV projection of Llama-3-70B (640 fragment rows) takes 38 us at two per wave
 // and 34 us at one (a lane's four outputs hold whole rotary pairs either way).
 template <int KIND> struct GemmCfg;
