@@ -70,6 +70,21 @@ def test_size_queries_are_host_only(lib):
     assert "4 GiB" in lsv.lsv_last_error()
 
 
+def test_attention_split_plan_in_the_workspace_size(lib):
+    """The attention partials take n_splits x max_rows x n_q x (head_dim + 2) floats of the
+    workspace, so its size shows the host's split plan.  Eight sequences over eight kv heads:
+    a 128-chunk bound fits one round of four splits of 32 chunks, a 129-chunk bound would walk 33
+    per split, more than twice the 16-chunk cap, and takes the packed grid's three rounds of
+    splits (12 of 11 chunks).  Four sequences (one round of eight splits either way) keep the
+    same plan, and so the same workspace."""
+    cfg = tiny_cfg(n_layers=1, d_model=1024, n_q_heads=8, n_kv_heads=8, head_dim=128, d_ff=2816, vocab=4096,
+                   dtype=lsv.LSV_DTYPE_BF16)
+    per_split = 64 * 8 * (128 + 2) * 4  # max_rows 64, 8 query heads
+    ws = lambda batch, ctx: lsv.lsv_verify_workspace_bytes(cfg, batch, 64, ctx)
+    assert ws(8, 129 * 64) - ws(8, 128 * 64) == (12 - 4) * per_split
+    assert ws(4, 129 * 64) == ws(4, 128 * 64)
+
+
 def expect(code, fn, *args):
     with pytest.raises(lsv.LsvError) as e:
         fn(*args)
